@@ -1,0 +1,202 @@
+"""CPU oracle of the batched energy-aware placement and migration search.
+
+TEST INFRASTRUCTURE ONLY: the test suite, the package smoke check and the
+benchmark's CPU-baseline leg are the only callers.  The product path never
+imports this package.  It wraps ``festina_oracle.c`` (plain C, float64) with
+ctypes; nothing here is shared with the HIP library.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "festina_oracle.c")
+LIB_PATH = os.environ.get("FESTINA_ORACLE_LIB") or os.path.join(_HERE, "libfestina_oracle.so")
+BUILD_CMD = ["gcc", "-O2", "-ffp-contract=off", "-fPIC", "-shared", "-Wall", "-Wextra",
+             "-o", LIB_PATH, _SRC, "-lm"]
+
+_lib = None
+
+
+def build() -> str:
+    """Compile the oracle library in place (gcc, -O2, no FP contraction, no fast-math)."""
+    subprocess.run(BUILD_CMD, check=True)
+    return LIB_PATH
+
+
+class _Lut(C.Structure):
+    _fields_ = [("n_models", C.c_int32), ("n_rows", C.c_int32), ("n_sm", C.c_int32),
+                ("n_freq", C.c_int32), ("sm_level", C.c_void_p), ("freq_level", C.c_void_p),
+                ("pf", C.c_void_p), ("dc", C.c_void_p), ("p0_w", C.c_double)]
+
+
+class _Gpus(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("n_waves", C.c_int32), ("batch", C.c_void_p),
+                ("k_dyn_w", C.c_void_p), ("resident", C.c_void_p), ("cap_pf", C.c_void_p),
+                ("cap_dc", C.c_void_p)]
+
+
+class _Requests(C.Structure):
+    _fields_ = [("n_requests", C.c_int32), ("model", C.c_void_p), ("wave", C.c_void_p),
+                ("prompt_tokens", C.c_void_p), ("pred_out_tokens", C.c_void_p),
+                ("slo_ttft_ms", C.c_void_p), ("slo_tbt_ms", C.c_void_p)]
+
+
+class _Fleet(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("max_inst", C.c_int32), ("n_inst", C.c_void_p),
+                ("inst_model", C.c_void_p), ("inst_prompt_tokens", C.c_void_p),
+                ("inst_batch", C.c_void_p), ("inst_sm", C.c_void_p),
+                ("inst_slo_ttft_ms", C.c_void_p), ("inst_slo_tbt_ms", C.c_void_p),
+                ("hbm_mib", C.c_void_p), ("sm_permille", C.c_void_p), ("util", C.c_void_p),
+                ("k_dyn_w", C.c_void_p), ("hbm_cap_mib", C.c_int32), ("sm_cap_permille", C.c_int32)]
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if "FESTINA_ORACLE_LIB" not in os.environ and (
+                not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(_SRC)):
+            build()
+        L = C.CDLL(LIB_PATH)
+        P = C.POINTER
+        L.festina_oracle_score_placements.argtypes = [P(_Lut), P(_Gpus), P(_Requests), C.c_int32,
+                                                      C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.festina_oracle_score_placements.restype = C.c_int
+        L.festina_oracle_candidate.argtypes = [P(_Lut), P(_Gpus), P(_Requests), C.c_int32,
+                                               C.c_int64, P(C.c_double)]
+        L.festina_oracle_candidate.restype = C.c_int
+        L.festina_oracle_score_migrations.argtypes = [P(_Lut), P(_Fleet), C.c_int32, C.c_void_p,
+                                                      C.c_void_p, C.c_void_p, C.c_void_p]
+        L.festina_oracle_score_migrations.restype = C.c_int
+        L.festina_oracle_pair.argtypes = [P(_Lut), P(_Fleet), C.c_int32, C.c_int32,
+                                          P(C.c_int32), P(C.c_double)]
+        L.festina_oracle_pair.restype = C.c_int
+        L.festina_oracle_prompt_row.argtypes = [C.c_int32]
+        L.festina_oracle_prompt_row.restype = C.c_int
+        L.festina_oracle_padded_out.argtypes = [C.c_int32]
+        L.festina_oracle_padded_out.restype = C.c_int64
+        _lib = L
+    return _lib
+
+
+# ------------------------------------------------------------------ marshalling
+def _arr(a, dtype):
+    if a is None:
+        return None
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+class _Pinned:
+    """Holds the contiguous arrays alive while the structs point at them."""
+
+    def __init__(self):
+        self.keep = []
+
+    def __call__(self, a, dtype):
+        a = _arr(a, dtype)
+        if a is not None:
+            self.keep.append(a)
+        return _p(a)
+
+
+def _lut(d, pin):
+    return _Lut(int(d["n_models"]), int(d["n_rows"]), int(d["n_sm"]), int(d["n_freq"]),
+                pin(d["sm_level"], np.float32), pin(d["freq_level"], np.float32),
+                pin(d["pf"], np.float32), pin(d["dc"], np.float32), float(d["p0_w"]))
+
+
+def _gpus(d, pin):
+    return _Gpus(int(d["n_gpus"]), int(d["n_waves"]), pin(d["batch"], np.int32),
+                 pin(d["k_dyn_w"], np.float32), pin(d["resident"], np.uint32),
+                 pin(d.get("cap_pf"), np.int8), pin(d.get("cap_dc"), np.int8))
+
+
+def _requests(d, pin):
+    return _Requests(int(d["n_requests"]), pin(d["model"], np.int32), pin(d.get("wave"), np.int32),
+                     pin(d["prompt_tokens"], np.int32), pin(d["pred_out_tokens"], np.int32),
+                     pin(d["slo_ttft_ms"], np.float32), pin(d["slo_tbt_ms"], np.float32))
+
+
+def _fleet(d, pin):
+    return _Fleet(int(d["n_gpus"]), int(d["max_inst"]), pin(d["n_inst"], np.int32),
+                  pin(d["inst_model"], np.int32), pin(d["inst_prompt_tokens"], np.int32),
+                  pin(d["inst_batch"], np.int32), pin(d["inst_sm"], np.int32),
+                  pin(d["inst_slo_ttft_ms"], np.float32), pin(d["inst_slo_tbt_ms"], np.float32),
+                  pin(d["hbm_mib"], np.int32), pin(d["sm_permille"], np.int32),
+                  pin(d["util"], np.float32), pin(d["k_dyn_w"], np.float32),
+                  int(d["hbm_cap_mib"]), int(d["sm_cap_permille"]))
+
+
+# ------------------------------------------------------------------ public API
+def score_placements(inp: dict, sel=None):
+    """Oracle placements for all requests (or the request ids in ``sel``).
+
+    Returns (choice int32, feasible uint8, energy_mj float64), indexed like ``sel``.
+    """
+    pin = _Pinned()
+    lut, gpus, req = _lut(inp["lut"], pin), _gpus(inp["gpus"], pin), _requests(inp["requests"], pin)
+    n = int(inp["requests"]["n_requests"]) if sel is None else len(sel)
+    sel_a = None if sel is None else _arr(sel, np.int32)
+    choice = np.empty(n, np.int32)
+    feas = np.empty(n, np.uint8)
+    energy = np.empty(n, np.float64)
+    rc = lib().festina_oracle_score_placements(C.byref(lut), C.byref(gpus), C.byref(req), n,
+                                               _p(sel_a), _p(choice), _p(feas), _p(energy))
+    if rc != 0:
+        raise ValueError("oracle rejected the placement arguments")
+    return choice, feas, energy
+
+
+def candidate_energy(inp: dict, r: int, idx: int):
+    """(eligible, energy_mj) of candidate ``idx`` for request ``r``."""
+    pin = _Pinned()
+    lut, gpus, req = _lut(inp["lut"], pin), _gpus(inp["gpus"], pin), _requests(inp["requests"], pin)
+    e = C.c_double(0.0)
+    ok = lib().festina_oracle_candidate(C.byref(lut), C.byref(gpus), C.byref(req), int(r), int(idx),
+                                        C.byref(e))
+    return bool(ok), float(e.value)
+
+
+def score_migrations(inp: dict, sel=None):
+    """Oracle per-source best destinations (or for the source ids in ``sel``).
+
+    Returns (best_dst int32, saving_w float64, freq_level int32).
+    """
+    pin = _Pinned()
+    lut, fleet = _lut(inp["lut"], pin), _fleet(inp["fleet"], pin)
+    n = int(inp["fleet"]["n_gpus"]) if sel is None else len(sel)
+    sel_a = None if sel is None else _arr(sel, np.int32)
+    best = np.empty(n, np.int32)
+    sav = np.empty(n, np.float64)
+    lev = np.empty(n, np.int32)
+    rc = lib().festina_oracle_score_migrations(C.byref(lut), C.byref(fleet), n, _p(sel_a),
+                                               _p(best), _p(sav), _p(lev))
+    if rc != 0:
+        raise ValueError("oracle rejected the migration arguments")
+    return best, sav, lev
+
+
+def pair_saving(inp: dict, s: int, d: int):
+    """(eligible, k_star, saving_w) of moving source ``s`` onto destination ``d``."""
+    pin = _Pinned()
+    lut, fleet = _lut(inp["lut"], pin), _fleet(inp["fleet"], pin)
+    k = C.c_int32(-1)
+    sv = C.c_double(0.0)
+    ok = lib().festina_oracle_pair(C.byref(lut), C.byref(fleet), int(s), int(d), C.byref(k), C.byref(sv))
+    return bool(ok), int(k.value), float(sv.value)
+
+
+def prompt_row(tokens: int) -> int:
+    return int(lib().festina_oracle_prompt_row(int(tokens)))
+
+
+def padded_out(predicted: int) -> int:
+    return int(lib().festina_oracle_padded_out(int(predicted)))

@@ -1,0 +1,283 @@
+/*
+ * festina_oracle.c -- plain, slow, obviously-correct CPU oracle of the batched
+ * energy-aware placement and migration search.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the package smoke check and the
+ * benchmark's CPU-baseline leg may load or call this library.  The product path
+ * (the HIP library) never links it, includes it, or falls back to it, and the two
+ * share no code: this file re-declares everything it needs.
+ *
+ * Arithmetic is float64 throughout (inputs are float32 and are promoted).  Every
+ * SLO test compares a float32 table entry with a float32 SLO, so promoting does not
+ * change its outcome.  Loops run in the order of the plain definitions:
+ *
+ *   placement (Sec. 3.3, Phase One and Phase Two; energy = power x time, Eq. energy):
+ *     for every request r, every GPU g hosting r's model, every SM level j and
+ *     frequency level k: the candidate is feasible when its prefill latency (TTFT)
+ *     is strictly below the TTFT SLO and its decode-step latency (TBT) is strictly
+ *     below the TBT SLO (Phase One: "complete before its SLO deadline");
+ *     its energy is
+ *        E = Pp * TTFT + Lout * Pd * TBT,   P = P0 + k_g * s * f^3 * u_g
+ *     (Phase Two's E^k = Power x Latency, split into the prefill phase and Lout decode
+ *     steps, each at its own SM level); the chosen candidate is the least-energy
+ *     feasible one (Phase Two argmin), exact ties going to the lowest linear index
+ *     idx = (g*NS + j)*NF + k.  No feasible candidate -> flagged, not placed
+ *     (Phase Three: the caller scales out).
+ *
+ *   migration (Sec. 3.5.2 capacity check; Sec. 1 "saved idle power"; one device-wide
+ *   operating point shared by co-located models, Sec. 2.2 / 3.5.1):
+ *     for every ordered pair s != d: the merged GPU must fit the HBM and SM budgets
+ *     (inclusive) and some frequency level must let every instance of s and of d meet
+ *     both SLOs at its own SM level; it then runs at the lowest such level k*;
+ *     saving = P0 - k_d * (f[k*]^3 * (u_s + u_d) - f[kd0]^3 * u_d), where kd0 is d's own
+ *     lowest feasible level.  Per source: the largest saving, lowest d on exact ties.
+ *
+ * Request pre-processing (Sec. 3.2.1 input-length axis 256..8192; Sec. 3.2.2 / 3.3 the
+ * 5% output-length safety pad):
+ *   Lout = ceil(1.05 * predicted_out)            (integer: (105*L + 99) / 100)
+ *   prompt row = min(ceil(prompt_tokens / 256), 32) - 1; no prompt (0 tokens) -> the
+ *   decode batch row is used for the TTFT lookup as well.
+ * GPU state (Sec. 3.3 Phase One, post-admission): b = min(B + 1, 32), u = b / 32.
+ *
+ * Invalid per-element data (model id out of range, negative batch / tokens, wave out
+ * of range, SM cap outside [0, NS-1], instance fields out of range) never causes an
+ * out-of-bounds read: the request / GPU / pair simply becomes infeasible.
+ * A candidate is eligible only when its energy rounded to float32 is below +inf
+ * (so NaN and overflowing energies are never chosen); a pair only when its saving
+ * rounded to float32 is above -inf.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fPIC -shared (no fast-math).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#define OR_ROWS 32
+#define OR_ROW_TOKENS 256
+
+/* ---------------------------------------------------------------- oracle's own records */
+typedef struct {
+  int32_t n_models, n_rows, n_sm, n_freq;
+  const float *sm_level, *freq_level, *pf, *dc;
+  double p0_w;
+} or_lut;
+
+typedef struct {
+  int32_t n_gpus, n_waves;
+  const int32_t *batch;       /* [W][G] */
+  const float *k_dyn_w;       /* [G] */
+  const uint32_t *resident;   /* [G][(M+31)/32] */
+  const int8_t *cap_pf, *cap_dc; /* [G] or NULL */
+} or_gpus;
+
+typedef struct {
+  int32_t n_requests;
+  const int32_t *model, *wave, *prompt_tokens, *pred_out_tokens;
+  const float *slo_ttft_ms, *slo_tbt_ms;
+} or_requests;
+
+typedef struct {
+  int32_t n_gpus, max_inst;
+  const int32_t *n_inst, *inst_model, *inst_prompt_tokens, *inst_batch, *inst_sm;
+  const float *inst_slo_ttft_ms, *inst_slo_tbt_ms;
+  const int32_t *hbm_mib, *sm_permille;
+  const float *util, *k_dyn_w;
+  int32_t hbm_cap_mib, sm_cap_permille;
+} or_fleet;
+
+/* ---------------------------------------------------------------- pre-processing */
+/* -2 invalid, -1 no prompt, else row 0..31 */
+static int or_prompt_row(int32_t tokens) {
+  if (tokens < 0) return -2;
+  if (tokens == 0) return -1;
+  int64_t r = ((int64_t)tokens + OR_ROW_TOKENS - 1) / OR_ROW_TOKENS;
+  if (r > OR_ROWS) r = OR_ROWS;
+  return (int)(r - 1);
+}
+
+static int64_t or_padded_out(int32_t predicted) {
+  return ((int64_t)predicted * 105 + 99) / 100;
+}
+
+int festina_oracle_prompt_row(int32_t tokens) { return or_prompt_row(tokens); }
+int64_t festina_oracle_padded_out(int32_t predicted) { return or_padded_out(predicted); }
+
+static double or_cube(double x) { return x * x * x; }
+
+static size_t or_cell(const or_lut *L, int m, int row, int j, int k) {
+  return (((size_t)m * OR_ROWS + (size_t)row) * (size_t)L->n_sm + (size_t)j) * (size_t)L->n_freq + (size_t)k;
+}
+
+static int or_lut_ok(const or_lut *L) {
+  if (!L || L->n_models < 1 || L->n_rows != OR_ROWS || L->n_sm < 1 || L->n_freq < 1) return 0;
+  if (!L->sm_level || !L->freq_level || !L->pf || !L->dc) return 0;
+  return 1;
+}
+
+/* ---------------------------------------------------------------- placement */
+/* Energy of candidate idx for request r.  Returns 1 and sets *energy when the candidate
+ * exists, hosts the request's model, is SLO-feasible and has an eligible energy. */
+static int or_candidate(const or_lut *L, const or_gpus *G, const or_requests *Q,
+                        int32_t r, int64_t idx, double *energy) {
+  const int NS = L->n_sm, NF = L->n_freq, M = L->n_models;
+  if (r < 0 || r >= Q->n_requests) return 0;
+  if (idx < 0 || idx >= (int64_t)G->n_gpus * NS * NF) return 0;
+  const int g = (int)(idx / ((int64_t)NS * NF));
+  const int j = (int)((idx / NF) % NS);
+  const int k = (int)(idx % NF);
+  const int m = Q->model[r];
+  const int w = Q->wave ? Q->wave[r] : 0;
+  if (m < 0 || m >= M || w < 0 || w >= G->n_waves) return 0;
+  if (Q->pred_out_tokens[r] < 0) return 0;
+  const int prow = or_prompt_row(Q->prompt_tokens[r]);
+  if (prow == -2) return 0;
+  const int words = (M + 31) / 32;
+  if (!((G->resident[(size_t)g * words + (size_t)(m / 32)] >> (m % 32)) & 1u)) return 0;
+  const int32_t B = G->batch[(size_t)w * G->n_gpus + g];
+  if (B < 0) return 0;
+  const int b = (B + 1 > OR_ROWS) ? OR_ROWS : B + 1;
+  const int cp = G->cap_pf ? G->cap_pf[g] : NS - 1;
+  const int cd = G->cap_dc ? G->cap_dc[g] : NS - 1;
+  if (cp < 0 || cp >= NS || cd < 0 || cd >= NS) return 0;
+  const int jp = j < cp ? j : cp;
+  const int jd = j < cd ? j : cd;
+  const int row_p = prow >= 0 ? prow : b - 1;
+  const float ttft = L->pf[or_cell(L, m, row_p, jp, k)];
+  const float tbt = L->dc[or_cell(L, m, b - 1, jd, k)];
+  if (!(ttft < Q->slo_ttft_ms[r] && tbt < Q->slo_tbt_ms[r])) return 0;
+  const double u = (double)b / 32.0;
+  const double f3 = or_cube((double)L->freq_level[k]);
+  const double kg = (double)G->k_dyn_w[g];
+  const double Pp = L->p0_w + kg * (double)L->sm_level[jp] * f3 * u;
+  const double Pd = L->p0_w + kg * (double)L->sm_level[jd] * f3 * u;
+  const double Lout = (double)or_padded_out(Q->pred_out_tokens[r]);
+  const double E = Pp * (double)ttft + Lout * Pd * (double)tbt;
+  if (!((float)E < INFINITY)) return 0;
+  *energy = E;
+  return 1;
+}
+
+int festina_oracle_candidate(const or_lut *L, const or_gpus *G, const or_requests *Q,
+                             int32_t r, int64_t idx, double *energy) {
+  if (!or_lut_ok(L) || !G || !Q || !energy) return 0;
+  return or_candidate(L, G, Q, r, idx, energy);
+}
+
+/* Score requests sel[0..n_sel) (all requests when sel == NULL; then n_sel is ignored).
+ * Output i belongs to request sel[i].  Returns 0, or 1 on invalid arguments. */
+int festina_oracle_score_placements(const or_lut *L, const or_gpus *G, const or_requests *Q,
+                                    int32_t n_sel, const int32_t *sel,
+                                    int32_t *choice, uint8_t *feasible, double *energy_mj) {
+  if (!or_lut_ok(L) || !G || !Q || !choice || !feasible || !energy_mj) return 1;
+  if (G->n_gpus < 0 || G->n_waves < 1 || Q->n_requests < 0) return 1;
+  const int64_t cells = (int64_t)L->n_sm * L->n_freq;
+  const int words = (L->n_models + 31) / 32;
+  const int32_t n = sel ? n_sel : Q->n_requests;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t r = sel ? sel[i] : i;
+    const int m = (r >= 0 && r < Q->n_requests) ? Q->model[r] : -1;
+    int64_t best_idx = -1;
+    double best_e = INFINITY;
+    for (int32_t g = 0; g < G->n_gpus && m >= 0 && m < L->n_models; ++g) {
+      /* GPUs not hosting the model have no candidates: skip them whole */
+      if (!((G->resident[(size_t)g * words + (size_t)(m / 32)] >> (m % 32)) & 1u)) continue;
+      for (int64_t c = 0; c < cells; ++c) {
+        const int64_t idx = (int64_t)g * cells + c; /* ascending (g, j, k) */
+        double e;
+        if (!or_candidate(L, G, Q, r, idx, &e)) continue;
+        if (best_idx < 0 || e < best_e) {
+          best_idx = idx;
+          best_e = e;
+        }
+      }
+    }
+    choice[i] = (int32_t)best_idx;
+    feasible[i] = best_idx >= 0 ? 1 : 0;
+    energy_mj[i] = best_idx >= 0 ? best_e : INFINITY;
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------- migration */
+/* Does instance i of GPU g meet both SLOs at frequency level k (at its own SM level)? */
+static int or_instance_ok(const or_lut *L, const or_fleet *F, int g, int i, int k) {
+  const size_t at = (size_t)g * F->max_inst + (size_t)i;
+  const int m = F->inst_model[at];
+  const int j = F->inst_sm[at];
+  const int32_t B = F->inst_batch[at];
+  const int prow = or_prompt_row(F->inst_prompt_tokens[at]);
+  if (m < 0 || m >= L->n_models || j < 0 || j >= L->n_sm || B < 0 || prow == -2) return 0;
+  const int b = (B + 1 > OR_ROWS) ? OR_ROWS : B + 1;
+  const int row_p = prow >= 0 ? prow : b - 1;
+  const float ttft = L->pf[or_cell(L, m, row_p, j, k)];
+  const float tbt = L->dc[or_cell(L, m, b - 1, j, k)];
+  return ttft < F->inst_slo_ttft_ms[at] && tbt < F->inst_slo_tbt_ms[at];
+}
+
+/* Do all instances of GPU g meet their SLOs at level k? */
+static int or_gpu_ok(const or_lut *L, const or_fleet *F, int g, int k) {
+  const int n = F->n_inst[g];
+  if (n < 1 || n > F->max_inst) return 0;
+  for (int i = 0; i < n; ++i)
+    if (!or_instance_ok(L, F, g, i, k)) return 0;
+  return 1;
+}
+
+static int or_pair(const or_lut *L, const or_fleet *F, int s, int d, int *kstar_out, double *saving) {
+  if (s < 0 || d < 0 || s >= F->n_gpus || d >= F->n_gpus || s == d) return 0;
+  if ((int64_t)F->hbm_mib[s] + F->hbm_mib[d] > (int64_t)F->hbm_cap_mib) return 0;
+  if ((int64_t)F->sm_permille[s] + F->sm_permille[d] > (int64_t)F->sm_cap_permille) return 0;
+  int kstar = -1;
+  for (int k = 0; k < L->n_freq && kstar < 0; ++k)
+    if (or_gpu_ok(L, F, s, k) && or_gpu_ok(L, F, d, k)) kstar = k;
+  if (kstar < 0) return 0;
+  int kd0 = -1;
+  for (int k = 0; k < L->n_freq && kd0 < 0; ++k)
+    if (or_gpu_ok(L, F, d, k)) kd0 = k;
+  const double us = (double)F->util[s], ud = (double)F->util[d];
+  const double kd = (double)F->k_dyn_w[d];
+  const double added = or_cube((double)L->freq_level[kstar]) * (us + ud) - or_cube((double)L->freq_level[kd0]) * ud;
+  const double sv = L->p0_w - kd * added;
+  if (!((float)sv > -INFINITY)) return 0;
+  *kstar_out = kstar;
+  *saving = sv;
+  return 1;
+}
+
+int festina_oracle_pair(const or_lut *L, const or_fleet *F, int32_t s, int32_t d,
+                        int32_t *kstar, double *saving) {
+  if (!or_lut_ok(L) || !F || !kstar || !saving) return 0;
+  int k;
+  double sv;
+  if (!or_pair(L, F, s, d, &k, &sv)) return 0;
+  *kstar = k;
+  *saving = sv;
+  return 1;
+}
+
+/* Score sources sel[0..n_sel) (all when sel == NULL).  Output i belongs to source sel[i]. */
+int festina_oracle_score_migrations(const or_lut *L, const or_fleet *F, int32_t n_sel, const int32_t *sel,
+                                    int32_t *best_dst, double *saving_w, int32_t *freq_level) {
+  if (!or_lut_ok(L) || !F || !best_dst || !saving_w || !freq_level) return 1;
+  if (F->n_gpus < 0 || F->max_inst < 1) return 1;
+  const int32_t n = sel ? n_sel : F->n_gpus;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = sel ? sel[i] : i;
+    int32_t bd = -1, bk = -1;
+    double bs = -INFINITY;
+    for (int32_t d = 0; d < F->n_gpus; ++d) {
+      int k;
+      double sv;
+      if (!or_pair(L, F, s, d, &k, &sv)) continue;
+      if (bd < 0 || sv > bs) {
+        bd = d;
+        bs = sv;
+        bk = k;
+      }
+    }
+    best_dst[i] = bd;
+    saving_w[i] = bd >= 0 ? bs : -INFINITY;
+    freq_level[i] = bk;
+  }
+  return 0;
+}

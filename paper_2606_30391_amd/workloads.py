@@ -1,0 +1,348 @@
+"""Seeded synthetic inputs for the batched placement and migration search.
+
+This module only *draws inputs*: request features, GPU state snapshots, fleet
+records and the offline profile tables (latency look-up tables).  It holds none
+of the search itself: no output-length padding, no prompt bucketing, no power
+or energy, no SLO test, no argmin.  Both the HIP path and the CPU oracle consume
+what it returns, and neither shares any other code.
+
+The paper's workloads (ShareGPT arrivals, Azure-derived prompt lengths) are not
+available here; the laws below stand in for them.  Profile tables follow the
+paper's look-up-table axes (Sec. 3.2.1: frequency, SM share, input length) with
+a closed-form latency model per model:
+
+* decode step (TBT):  a_m + c_m * b / (s * f)           rows = batch 1..32
+* prefill (TTFT):     a_m + cp_m * 256 (p+1) / (s * f)   rows = 256-token prompt buckets
+  (the tiny configuration has no prompts and uses the decode table for both)
+
+Tables are evaluated in float64 and rounded once to float32; configurations 3-5
+add independent multiplicative noise U(0.95, 1.05) per entry, so nothing may
+assume monotone tables.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+P0_W = 120.0              # static power, W
+N_ROWS = 32               # table rows (batch 1..32, or prompt buckets of 256 tokens)
+ROW_TOKENS = 256          # prompt tokens per prefill-table row (32 * 256 = 8192)
+HBM_CAP_MIB = 288 * 1024  # one MI355X-class GPU: 288 GiB
+SM_CAP_PERMILLE = 1000
+MAX_INST = 4
+
+CONFIG_SEED_BASE = 30391000
+
+TTFT_SLO_SET = (100.0, 200.0, 400.0)
+TBT_SLO_SET = (25.0, 50.0, 100.0)
+
+
+def config_seed(n: int, extra: int = 0) -> int:
+    """Seed of configuration n (1..5); extra parity seeds add 100, 200, 300."""
+    return CONFIG_SEED_BASE + n + extra
+
+
+# --------------------------------------------------------------------------- levels
+def sm_levels(ns: int) -> np.ndarray:
+    """SM-partition levels s_j = (j+1)/NS (tiny: {.25,.5,.75,1}; others: eighths)."""
+    return ((np.arange(ns, dtype=np.float64) + 1.0) / ns).astype(np.float32)
+
+
+def freq_levels(nf: int) -> np.ndarray:
+    """Normalised frequency levels evenly spaced over [0.5, 1.0]."""
+    if nf == 1:
+        return np.ones(1, dtype=np.float32)
+    return (0.5 + 0.5 * np.arange(nf, dtype=np.float64) / (nf - 1)).astype(np.float32)
+
+
+# --------------------------------------------------------------------------- tables
+def _latency_params(rng, m, prefill):
+    a = rng.uniform(5.0, 20.0, m)
+    c = rng.uniform(0.5, 3.0, m)
+    cp = rng.uniform(0.02, 0.1, m) if prefill else None
+    return a, c, cp
+
+
+def _tables(rng, m, s, f, a, c, cp, noise):
+    """Return (pf, dc) float32 [M][32][NS][NF] from the closed-form latency model."""
+    sf = s.astype(np.float64)[:, None] * f.astype(np.float64)[None, :]        # [NS][NF]
+    rows = np.arange(1, N_ROWS + 1, dtype=np.float64)                          # 1..32
+    dc = a[:, None, None, None] + c[:, None, None, None] * rows[None, :, None, None] / sf[None, None]
+    if cp is None:
+        pf = dc.copy()
+    else:
+        tok = ROW_TOKENS * rows
+        pf = a[:, None, None, None] + cp[:, None, None, None] * tok[None, :, None, None] / sf[None, None]
+    if noise:
+        dc = dc * rng.uniform(0.95, 1.05, dc.shape)
+        pf = pf * rng.uniform(0.95, 1.05, pf.shape)
+    return np.ascontiguousarray(pf, dtype=np.float32), np.ascontiguousarray(dc, dtype=np.float32)
+
+
+def _lut(pf, dc, s, f, p0=P0_W):
+    m, nr, ns, nf = pf.shape
+    return {"n_models": m, "n_rows": nr, "n_sm": ns, "n_freq": nf,
+            "sm_level": s, "freq_level": f, "pf": pf, "dc": dc, "p0_w": float(p0)}
+
+
+def _resident_bits(models_per_gpu, m):
+    """Pack per-GPU model lists into [G][ceil(M/32)] uint32 bitmasks."""
+    g = len(models_per_gpu)
+    words = (m + 31) // 32
+    bits = np.zeros((g, words), dtype=np.uint32)
+    for gi, ms in enumerate(models_per_gpu):
+        for mm in ms:
+            bits[gi, mm // 32] |= np.uint32(1) << np.uint32(mm % 32)
+    return bits
+
+
+def _lognormal_tokens(rng, mu, n, lo, hi):
+    return np.clip(np.rint(rng.lognormal(mu, 1.0, n)), lo, hi).astype(np.int32)
+
+
+def _distinct_models(rng, g, m, counts):
+    return [np.sort(rng.choice(m, int(k), replace=False)) for k in counts[:g]]
+
+
+# --------------------------------------------------------------------------- placement
+def make_placement(config: int, seed: int | None = None, n_requests: int | None = None,
+                   n_gpus: int | None = None) -> dict:
+    """Placement inputs of configuration 1-4 (optionally with fewer requests/GPUs).
+
+    Returned dict: {"lut": ..., "gpus": ..., "requests": ..., "meta": ...} of
+    numpy arrays laid out as the C ABI expects (structure of arrays).
+    """
+    if seed is None:
+        seed = config_seed(config)
+    rng = np.random.default_rng(seed)
+    if config == 1:
+        M, G, R, NS, NF, W = 2, 8, 64, 4, 8, 1
+    elif config == 2:
+        M, G, R, NS, NF, W = 8, 64, 4096, 8, 16, 1
+    elif config == 3:
+        M, G, R, NS, NF, W = 32, 512, 65536, 8, 16, 1
+    elif config == 4:
+        M, G, R, NS, NF, W = 32, 1024, 262144, 8, 16, 64
+    else:
+        raise ValueError(f"placement configuration {config} does not exist")
+    if n_requests is not None:
+        R = int(n_requests)
+    if n_gpus is not None:
+        G = int(n_gpus)
+    s, f = sm_levels(NS), freq_levels(NF)
+
+    # --- profile tables
+    a, c, cp = _latency_params(rng, M, prefill=(config != 1))
+    pf, dc = _tables(rng, M, s, f, a, c, cp, noise=(config >= 3))
+    lut = _lut(pf, dc, s, f)
+
+    # --- GPU state
+    cap_pf = cap_dc = None
+    if config == 1:
+        batch = rng.integers(0, 17, size=(W, G), dtype=np.int32)
+        kdyn = rng.uniform(300.0, 500.0, G).astype(np.float32)
+        models_per_gpu = [np.arange(M)] * G
+        slo_m_ttft = np.full(M, 200.0)
+        slo_m_tbt = np.full(M, 50.0)
+    else:
+        slo_m_ttft = rng.choice(TTFT_SLO_SET, M)
+        slo_m_tbt = rng.choice(TBT_SLO_SET, M)
+        if config == 2:
+            batch = rng.integers(0, 17, size=(W, G), dtype=np.int32)
+            kdyn = rng.uniform(300.0, 500.0, G).astype(np.float32)
+            models_per_gpu = _distinct_models(rng, G, M, np.full(G, 2))
+        else:
+            nres = rng.integers(1, 5, size=G)
+            models_per_gpu = _distinct_models(rng, G, M, nres)
+            kdyn = rng.uniform(300.0, 500.0, G).astype(np.float32)
+            if config == 4:
+                sig = np.array([0.25, 0.5, 0.75])
+                cap_pf = (np.rint(rng.choice(sig, G) * NS) - 1).astype(np.int8)
+                cap_dc = (np.rint(rng.choice(sig, G) * NS) - 1).astype(np.int8)
+            batch = np.minimum(rng.poisson(4.0, size=(W, G)), 31).astype(np.int32)
+    resident = _resident_bits(models_per_gpu, M)
+    gpus = {"n_gpus": G, "n_waves": W, "batch": np.ascontiguousarray(batch),
+            "k_dyn_w": kdyn, "resident": resident, "cap_pf": cap_pf, "cap_dc": cap_dc}
+
+    # --- requests
+    model = rng.integers(0, M, size=R, dtype=np.int32)
+    if config == 1:
+        prompt = np.zeros(R, dtype=np.int32)          # no prompt phase: decode-row lookup
+        pred_out = np.zeros(R, dtype=np.int32)
+    else:
+        if config == 4:
+            long_mask = rng.random(R) < 0.3
+            short = _lognormal_tokens(rng, 5.0, R, 16, 8192)
+            longp = _lognormal_tokens(rng, 8.0, R, 16, 8192)
+            prompt = np.where(long_mask, longp, short).astype(np.int32)
+        else:
+            prompt = _lognormal_tokens(rng, 6.0, R, 16, 8192)
+        pred_out = _lognormal_tokens(rng, 5.0, R, 1, 8192)
+    slo_ttft = slo_m_ttft[model].astype(np.float32)
+    slo_tbt = slo_m_tbt[model].astype(np.float32)
+    if config == 3:
+        planted = rng.random(R) < 0.1
+        slo_ttft[planted] = 1.0
+        slo_tbt[planted] = 1.0
+    else:
+        planted = np.zeros(R, dtype=bool)
+    wave = ((np.arange(R, dtype=np.int64) * W) // max(R, 1)).astype(np.int32)
+    requests = {"n_requests": R, "model": model, "wave": wave, "prompt_tokens": prompt,
+                "pred_out_tokens": pred_out, "slo_ttft_ms": slo_ttft, "slo_tbt_ms": slo_tbt}
+    meta = {"config": config, "seed": seed, "a": a, "c": c, "cp": cp, "planted": planted,
+            "models_per_gpu": models_per_gpu}
+    return {"lut": lut, "gpus": gpus, "requests": requests, "meta": meta}
+
+
+# --------------------------------------------------------------------------- migration
+def _preferred_sm_level(a, c, cp, slo_ttft, slo_tbt, prompt_tokens, batch, s, f):
+    """Instance SM level: the smallest level whose noise-free latencies at the top
+    frequency meet both SLOs (else the top level).  This models the local
+    scheduler's per-model preferred configuration (App. E, first step) as an
+    input; the scoring below never sees the noise-free model."""
+    ns = len(s)
+    ptok = ROW_TOKENS * np.minimum(np.maximum((prompt_tokens + ROW_TOKENS - 1) // ROW_TOKENS, 1), N_ROWS)
+    b = np.minimum(batch + 1, N_ROWS)
+    fmax = float(f[-1])
+    out = np.full(prompt_tokens.shape, ns - 1, dtype=np.int32)
+    done = np.zeros(prompt_tokens.shape, dtype=bool)
+    for j in range(ns):
+        sj = float(s[j])
+        ok = (a + cp * ptok / (sj * fmax) < slo_ttft) & (a + c * b / (sj * fmax) < slo_tbt)
+        pick = ok & ~done
+        out[pick] = j
+        done |= ok
+    return out
+
+
+def make_fleet(seed: int | None = None, n_gpus: int = 2048) -> dict:
+    """Consolidation fleet of configuration 5 (optionally fewer GPUs)."""
+    if seed is None:
+        seed = config_seed(5)
+    rng = np.random.default_rng(seed)
+    M, NS, NF, G, K = 32, 8, 16, int(n_gpus), MAX_INST
+    s, f = sm_levels(NS), freq_levels(NF)
+    a, c, cp = _latency_params(rng, M, prefill=True)
+    pf, dc = _tables(rng, M, s, f, a, c, cp, noise=True)
+    lut = _lut(pf, dc, s, f)
+    slo_m_ttft = rng.choice(TTFT_SLO_SET, M)
+    slo_m_tbt = rng.choice(TBT_SLO_SET, M)
+
+    n_want = rng.integers(1, K + 1, size=G)
+    inst_model = np.zeros((G, K), dtype=np.int32)
+    n_inst = np.zeros(G, dtype=np.int32)
+    hbm = np.zeros(G, dtype=np.int32)
+    foot = np.rint(rng.uniform(8.0, 80.0, size=(G, K)) * 1024.0).astype(np.int64)
+    for g in range(G):
+        ms = rng.choice(M, int(n_want[g]), replace=False)
+        tot = 0
+        for i, mm in enumerate(ms):
+            if tot + foot[g, i] > HBM_CAP_MIB:
+                break
+            tot += int(foot[g, i])
+            inst_model[g, n_inst[g]] = mm
+            n_inst[g] += 1
+        hbm[g] = tot
+    inst_prompt = _lognormal_tokens(rng, 6.0, G * K, 16, 8192).reshape(G, K)
+    inst_batch = np.minimum(rng.poisson(4.0, size=(G, K)), 31).astype(np.int32)
+    slo_ttft = slo_m_ttft[inst_model].astype(np.float32)
+    slo_tbt = slo_m_tbt[inst_model].astype(np.float32)
+    inst_sm = _preferred_sm_level(a[inst_model], c[inst_model], cp[inst_model],
+                                  slo_ttft.astype(np.float64), slo_tbt.astype(np.float64),
+                                  inst_prompt.astype(np.int64), inst_batch.astype(np.int64), s, f)
+    # unused slots hold zeros: they are never read
+    unused = np.arange(K)[None, :] >= n_inst[:, None]
+    for arr in (inst_model, inst_prompt, inst_batch, inst_sm):
+        arr[unused] = 0
+    slo_ttft[unused] = 0.0
+    slo_tbt[unused] = 0.0
+    sm_pm = np.rint(1000.0 * rng.uniform(0.0, 0.6, G)).astype(np.int32)
+    util = (sm_pm.astype(np.float64) / 1000.0).astype(np.float32)
+    kdyn = rng.uniform(300.0, 500.0, G).astype(np.float32)
+    fleet = {"n_gpus": G, "max_inst": K, "n_inst": n_inst, "inst_model": inst_model,
+             "inst_prompt_tokens": inst_prompt.astype(np.int32), "inst_batch": inst_batch,
+             "inst_sm": inst_sm, "inst_slo_ttft_ms": slo_ttft, "inst_slo_tbt_ms": slo_tbt,
+             "hbm_mib": hbm, "sm_permille": sm_pm, "util": util, "k_dyn_w": kdyn,
+             "hbm_cap_mib": HBM_CAP_MIB, "sm_cap_permille": SM_CAP_PERMILLE}
+    meta = {"config": 5, "seed": seed, "a": a, "c": c, "cp": cp}
+    return {"lut": lut, "fleet": fleet, "meta": meta}
+
+
+# --------------------------------------------------------------------------- tiny random cases
+def make_tiny_placement(rng: np.random.Generator, R=None, G=None, M=None, NS=None, NF=None,
+                        W=None, caps=None, ties=False, nan_cells=False) -> dict:
+    """Small random placement instance for brute-force comparison and parity edge cases."""
+    R = int(rng.integers(1, 9)) if R is None else R
+    G = int(rng.integers(1, 6)) if G is None else G
+    M = int(rng.integers(1, 4)) if M is None else M
+    NS = int(rng.integers(1, 5)) if NS is None else NS
+    NF = int(rng.integers(1, 7)) if NF is None else NF
+    W = int(rng.integers(1, 3)) if W is None else W
+    caps = bool(rng.integers(0, 2)) if caps is None else caps
+    s, f = sm_levels(NS), freq_levels(NF)
+    if ties:
+        pf = np.full((M, N_ROWS, NS, NF), np.float32(rng.uniform(5, 30)), dtype=np.float32)
+        dc = np.full((M, N_ROWS, NS, NF), np.float32(rng.uniform(5, 30)), dtype=np.float32)
+    else:
+        pf = rng.uniform(5.0, 60.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+        dc = rng.uniform(2.0, 40.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    if nan_cells:
+        mask = rng.random(pf.shape) < 0.1
+        pf[mask] = np.nan
+        dc[rng.random(dc.shape) < 0.05] = np.inf
+    lut = _lut(pf, dc, s, f, p0=float(rng.uniform(0.0, 150.0)))
+    batch = rng.integers(0, 32, size=(W, G), dtype=np.int32)
+    if ties:
+        kdyn = np.full(G, np.float32(rng.uniform(300, 500)), dtype=np.float32)
+        batch[:] = batch[:, :1]
+    else:
+        kdyn = rng.uniform(0.0, 500.0, G).astype(np.float32)
+    models_per_gpu = [np.flatnonzero(rng.random(M) < 0.7) for _ in range(G)]
+    resident = _resident_bits(models_per_gpu, M)
+    cap_pf = rng.integers(0, NS, G).astype(np.int8) if caps else None
+    cap_dc = rng.integers(0, NS, G).astype(np.int8) if caps else None
+    gpus = {"n_gpus": G, "n_waves": W, "batch": batch, "k_dyn_w": kdyn,
+            "resident": resident, "cap_pf": cap_pf, "cap_dc": cap_dc}
+    prompt = np.where(rng.random(R) < 0.3, 0, rng.integers(1, 9000, R)).astype(np.int32)
+    requests = {"n_requests": R, "model": rng.integers(0, M, R).astype(np.int32),
+                "wave": rng.integers(0, W, R).astype(np.int32), "prompt_tokens": prompt,
+                "pred_out_tokens": rng.integers(0, 300, R).astype(np.int32),
+                "slo_ttft_ms": rng.uniform(10.0, 70.0, R).astype(np.float32),
+                "slo_tbt_ms": rng.uniform(5.0, 45.0, R).astype(np.float32)}
+    return {"lut": lut, "gpus": gpus, "requests": requests,
+            "meta": {"models_per_gpu": models_per_gpu}}
+
+
+def make_tiny_fleet(rng: np.random.Generator, G=None, M=None, NS=None, NF=None,
+                    loose=False, huge_budget=False) -> dict:
+    """Small random consolidation fleet for brute-force comparison."""
+    G = int(rng.integers(2, 7)) if G is None else G
+    M = int(rng.integers(1, 4)) if M is None else M
+    NS = int(rng.integers(1, 5)) if NS is None else NS
+    NF = int(rng.integers(1, 9)) if NF is None else NF
+    K = MAX_INST
+    s, f = sm_levels(NS), freq_levels(NF)
+    pf = rng.uniform(5.0, 60.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    dc = rng.uniform(2.0, 40.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    lut = _lut(pf, dc, s, f, p0=float(rng.uniform(50.0, 150.0)))
+    n_inst = rng.integers(1, K + 1, G).astype(np.int32)
+    inst_model = rng.integers(0, M, (G, K)).astype(np.int32)
+    inst_prompt = np.where(rng.random((G, K)) < 0.2, 0, rng.integers(1, 9000, (G, K))).astype(np.int32)
+    inst_batch = rng.integers(0, 32, (G, K)).astype(np.int32)
+    inst_sm = rng.integers(0, NS, (G, K)).astype(np.int32)
+    if loose:
+        slo_ttft = np.full((G, K), 1e9, dtype=np.float32)
+        slo_tbt = np.full((G, K), 1e9, dtype=np.float32)
+    else:
+        slo_ttft = rng.uniform(20.0, 80.0, (G, K)).astype(np.float32)
+        slo_tbt = rng.uniform(10.0, 50.0, (G, K)).astype(np.float32)
+    hbm = rng.integers(1000, 200000, G).astype(np.int32)
+    sm_pm = rng.integers(0, 700, G).astype(np.int32)
+    util = (sm_pm.astype(np.float64) / 1000.0).astype(np.float32)
+    kdyn = rng.uniform(300.0, 500.0, G).astype(np.float32)
+    fleet = {"n_gpus": G, "max_inst": K, "n_inst": n_inst, "inst_model": inst_model,
+             "inst_prompt_tokens": inst_prompt, "inst_batch": inst_batch, "inst_sm": inst_sm,
+             "inst_slo_ttft_ms": slo_ttft, "inst_slo_tbt_ms": slo_tbt, "hbm_mib": hbm,
+             "sm_permille": sm_pm, "util": util, "k_dyn_w": kdyn,
+             "hbm_cap_mib": (1 << 30) if huge_budget else HBM_CAP_MIB,
+             "sm_cap_permille": (1 << 30) if huge_budget else SM_CAP_PERMILLE}
+    return {"lut": lut, "fleet": fleet, "meta": {}}

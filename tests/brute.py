@@ -1,0 +1,153 @@
+"""Brute-force enumeration for tiny instances (test helper, not collected).
+
+Written independently of the C oracle: request pre-processing uses exact
+rationals, every candidate is listed, its energy is the sum over the two phases
+of power x time (Eq. energy), and the answer is the minimum of the list under
+the (energy, index) order -- no running minimum, no shared code.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+from fractions import Fraction
+
+import numpy as np
+
+
+def padded_out(pred: int) -> int:
+    """ceil(1.05 * L) with exact rationals (5% safety pad, Sec. 3.2.2)."""
+    return math.ceil(Fraction(105, 100) * pred)
+
+
+def prompt_row(tokens: int):
+    """None for invalid, -1 for no prompt, else the 256-token bucket row (rounded up)."""
+    if tokens < 0:
+        return None
+    if tokens == 0:
+        return -1
+    return min(math.ceil(Fraction(tokens, 256)), 32) - 1
+
+
+def power(p0, k, s, f, u):
+    """Closed-form power model P0 + k * s * f^3 * u (W)."""
+    return p0 + k * s * f ** 3 * u
+
+
+def placement_candidates(inp, r):
+    """All (energy, idx) of SLO-feasible candidates of request r, in float64."""
+    lut, gp, rq = inp["lut"], inp["gpus"], inp["requests"]
+    M, NS, NF = lut["n_models"], lut["n_sm"], lut["n_freq"]
+    G, W = gp["n_gpus"], gp["n_waves"]
+    m = int(rq["model"][r])
+    w = int(rq["wave"][r]) if rq.get("wave") is not None else 0
+    prow = prompt_row(int(rq["prompt_tokens"][r]))
+    pred = int(rq["pred_out_tokens"][r])
+    if not (0 <= m < M and 0 <= w < W) or prow is None or pred < 0:
+        return []
+    lout = padded_out(pred)
+    out = []
+    for g, j, k in itertools.product(range(G), range(NS), range(NF)):
+        if not (int(gp["resident"][g, m // 32]) >> (m % 32)) & 1:
+            continue
+        B = int(gp["batch"][w, g])
+        if B < 0:
+            continue
+        b = min(B + 1, 32)
+        cap_p = NS - 1 if gp.get("cap_pf") is None else int(gp["cap_pf"][g])
+        cap_d = NS - 1 if gp.get("cap_dc") is None else int(gp["cap_dc"][g])
+        if not (0 <= cap_p < NS and 0 <= cap_d < NS):
+            continue
+        jp, jd = min(j, cap_p), min(j, cap_d)
+        ttft = lut["pf"][m, b - 1 if prow < 0 else prow, jp, k]
+        tbt = lut["dc"][m, b - 1, jd, k]
+        if not (ttft < rq["slo_ttft_ms"][r] and tbt < rq["slo_tbt_ms"][r]):
+            continue
+        f = float(lut["freq_level"][k])
+        u = b / 32
+        kg = float(gp["k_dyn_w"][g])
+        phases = [(float(lut["sm_level"][jp]), float(ttft)),
+                  (float(lut["sm_level"][jd]), lout * float(tbt))]
+        e = sum(power(lut["p0_w"], kg, s, f, u) * t for s, t in phases)
+        if not np.float32(e) < np.inf:
+            continue
+        out.append((e, (g * NS + j) * NF + k))
+    return out
+
+
+def brute_placements(inp):
+    R = inp["requests"]["n_requests"]
+    choice = np.full(R, -1, np.int32)
+    energy = np.full(R, np.inf)
+    for r in range(R):
+        c = placement_candidates(inp, r)
+        if c:
+            e, idx = min(c)
+            choice[r], energy[r] = idx, e
+    return choice, (choice >= 0).astype(np.uint8), energy
+
+
+# ------------------------------------------------------------------ migration
+def feasible_levels(inp, g):
+    """Set of frequency levels at which every instance of GPU g meets both SLOs."""
+    lut, fl = inp["lut"], inp["fleet"]
+    NS, NF, M = lut["n_sm"], lut["n_freq"], lut["n_models"]
+    n = int(fl["n_inst"][g])
+    if not 1 <= n <= fl["max_inst"]:
+        return set()
+    levels = set(range(NF))
+    for i in range(n):
+        m = int(fl["inst_model"][g, i])
+        j = int(fl["inst_sm"][g, i])
+        B = int(fl["inst_batch"][g, i])
+        prow = prompt_row(int(fl["inst_prompt_tokens"][g, i]))
+        if not (0 <= m < M and 0 <= j < NS and B >= 0) or prow is None:
+            return set()
+        b = min(B + 1, 32)
+        ok = {k for k in range(NF)
+              if lut["pf"][m, b - 1 if prow < 0 else prow, j, k] < fl["inst_slo_ttft_ms"][g, i]
+              and lut["dc"][m, b - 1, j, k] < fl["inst_slo_tbt_ms"][g, i]}
+        levels &= ok
+    return levels
+
+
+def migration_pairs(inp, s):
+    """All (saving, d, k_star) of feasible destinations of source s."""
+    lut, fl = inp["lut"], inp["fleet"]
+    G = fl["n_gpus"]
+    fs = feasible_levels(inp, s)
+    out = []
+    for d in range(G):
+        if d == s:
+            continue
+        if int(fl["hbm_mib"][s]) + int(fl["hbm_mib"][d]) > fl["hbm_cap_mib"]:
+            continue
+        if int(fl["sm_permille"][s]) + int(fl["sm_permille"][d]) > fl["sm_cap_permille"]:
+            continue
+        fd = feasible_levels(inp, d)
+        both = fs & fd
+        if not both:
+            continue
+        kstar, kd0 = min(both), min(fd)
+        f = [float(x) for x in lut["freq_level"]]
+        us, ud, kd = float(fl["util"][s]), float(fl["util"][d]), float(fl["k_dyn_w"][d])
+        before = kd * f[kd0] ** 3 * ud                     # d's dynamic power alone
+        after = kd * f[kstar] ** 3 * (us + ud)             # merged load at the shared level
+        saving = lut["p0_w"] - (after - before)            # source's static power freed
+        if not np.float32(saving) > -np.inf:
+            continue
+        out.append((saving, d, kstar))
+    return out
+
+
+def brute_migrations(inp):
+    G = inp["fleet"]["n_gpus"]
+    best = np.full(G, -1, np.int32)
+    sav = np.full(G, -np.inf)
+    lev = np.full(G, -1, np.int32)
+    for s in range(G):
+        p = migration_pairs(inp, s)
+        if p:
+            # largest saving, then lowest d
+            sv, d, k = min(p, key=lambda t: (-t[0], t[1]))
+            best[s], sav[s], lev[s] = d, sv, k
+    return best, sav, lev

@@ -1,0 +1,94 @@
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+HERE = os.path.dirname(os.path.abspath(__file__))
+if HERE not in sys.path:
+    sys.path.insert(0, HERE)
+
+GOLDEN = os.path.join(HERE, "golden")
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+
+
+def load_golden(name):
+    with open(os.path.join(GOLDEN, name)) as fh:
+        return json.load(fh)
+
+
+def _tables(spec):
+    M, NS, NF = spec["n_models"], spec["n_sm"], spec["n_freq"]
+    pf = np.full((M, 32, NS, NF), spec["fill"], np.float32)
+    dc = np.full((M, 32, NS, NF), spec["fill"], np.float32)
+    for m, row, j, k, v in spec["pf_cells"]:
+        pf[m, row, j, k] = v
+    for m, row, j, k, v in spec["dc_cells"]:
+        dc[m, row, j, k] = v
+    return {"n_models": M, "n_rows": 32, "n_sm": NS, "n_freq": NF,
+            "sm_level": np.array(spec["sm_level"], np.float32),
+            "freq_level": np.array(spec["freq_level"], np.float32),
+            "pf": pf, "dc": dc, "p0_w": float(spec["p0_w"])}
+
+
+def golden_placement(variant=None):
+    """Inputs of the hand-worked placement example (optionally its capped variant)."""
+    d = load_golden("placement_worked_example.json")
+    lut = _tables(d["lut"])
+    G = d["gpus"]["n_gpus"]
+    batch = np.array(d["gpus"]["batch"], np.int32)
+    gpus = {"n_gpus": G, "n_waves": 1, "batch": batch,
+            "k_dyn_w": np.array(d["gpus"]["k_dyn_w"], np.float32),
+            "resident": np.ones((G, 1), np.uint32), "cap_pf": None, "cap_dc": None}
+    q = d["request"]
+    req = {"n_requests": 1, "model": np.array([q["model"]], np.int32), "wave": None,
+           "prompt_tokens": np.array([q["prompt_tokens"]], np.int32),
+           "pred_out_tokens": np.array([q["pred_out_tokens"]], np.int32),
+           "slo_ttft_ms": np.array([q["slo_ttft_ms"]], np.float32),
+           "slo_tbt_ms": np.array([q["slo_tbt_ms"]], np.float32)}
+    exp = d["expected"]
+    if variant == "capped":
+        v = d["capped_variant"]
+        gpus["cap_pf"] = np.array(v["cap_pf"], np.int8)
+        gpus["cap_dc"] = np.array(v["cap_dc"], np.int8)
+        if v["drop_gpu0"]:
+            gpus["batch"] = batch.copy()
+            gpus["batch"][0, 0] = -1
+        exp = v["expected"]
+    return {"lut": lut, "gpus": gpus, "requests": req}, exp, d
+
+
+def golden_migration():
+    d = load_golden("migration_worked_example.json")
+    lut = _tables(d["lut"])
+    fs = d["fleet"]
+    G, K = fs["n_gpus"], fs["max_inst"]
+    z = lambda dt: np.zeros((G, K), dt)
+    fl = {"n_gpus": G, "max_inst": K, "n_inst": np.zeros(G, np.int32), "inst_model": z(np.int32),
+          "inst_prompt_tokens": z(np.int32), "inst_batch": z(np.int32), "inst_sm": z(np.int32),
+          "inst_slo_ttft_ms": z(np.float32), "inst_slo_tbt_ms": z(np.float32),
+          "hbm_mib": np.array(fs["hbm_mib"], np.int32), "sm_permille": np.array(fs["sm_permille"], np.int32),
+          "util": np.array(fs["util"], np.float32), "k_dyn_w": np.array(fs["k_dyn_w"], np.float32),
+          "hbm_cap_mib": fs["hbm_cap_mib"], "sm_cap_permille": fs["sm_cap_permille"]}
+    for g, insts in enumerate(fs["instances"]):
+        fl["n_inst"][g] = len(insts)
+        for i, (m, pt, b, j, st, sb) in enumerate(insts):
+            fl["inst_model"][g, i] = m
+            fl["inst_prompt_tokens"][g, i] = pt
+            fl["inst_batch"][g, i] = b
+            fl["inst_sm"][g, i] = j
+            fl["inst_slo_ttft_ms"][g, i] = st
+            fl["inst_slo_tbt_ms"][g, i] = sb
+    return {"lut": lut, "fleet": fl}, d["expected"], d
+
+
+@pytest.fixture
+def rng():
+    return np.random.default_rng(12345)

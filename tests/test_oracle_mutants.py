@@ -1,0 +1,76 @@
+"""The oracle's pins must reject plausible mistakes.
+
+Each case plants one mistake in a copy of the oracle's C source (a dropped term, a
+wrong sign or index, an inclusive instead of a strict test, a swapped operand),
+compiles it on the CPU, and runs the pin suites against that library: they must
+fail.  Nothing here touches a GPU or the HIP library.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+SRC = os.path.join(ROOT, "oracle", "festina_oracle.c")
+
+PLACEMENT = [
+    ("dropped decode term", "const double E = Pp * (double)ttft + Lout * Pd * (double)tbt;",
+     "const double E = Pp * (double)ttft;"),
+    ("f instead of f^3", "const double f3 = or_cube((double)L->freq_level[k]);",
+     "const double f3 = (double)L->freq_level[k];"),
+    ("inclusive SLO test", "if (!(ttft < Q->slo_ttft_ms[r] && tbt < Q->slo_tbt_ms[r])) return 0;",
+     "if (!(ttft <= Q->slo_ttft_ms[r] && tbt <= Q->slo_tbt_ms[r])) return 0;"),
+    ("pre-admission batch in u", "const double u = (double)b / 32.0;", "const double u = (double)B / 32.0;"),
+    ("TTFT read from the batch row", "L->pf[or_cell(L, m, row_p, jp, k)]", "L->pf[or_cell(L, m, b - 1, jp, k)]"),
+    ("decode cap taken from prefill cap", "const int jd = j < cd ? j : cd;", "const int jd = j < cp ? j : cp;"),
+    ("highest index wins ties", "if (best_idx < 0 || e < best_e) {", "if (best_idx < 0 || e <= best_e) {"),
+    ("floor instead of ceil in the 5% pad", "((int64_t)predicted * 105 + 99) / 100", "((int64_t)predicted * 105) / 100"),
+    ("prompt bucket off by one", "((int64_t)tokens + OR_ROW_TOKENS - 1) / OR_ROW_TOKENS",
+     "((int64_t)tokens + OR_ROW_TOKENS) / OR_ROW_TOKENS"),
+    ("uncapped SM level in prefill power", "const double Pp = L->p0_w + kg * (double)L->sm_level[jp]",
+     "const double Pp = L->p0_w + kg * (double)L->sm_level[j]"),
+    ("wrong sign of dynamic power", "const double Pd = L->p0_w + kg", "const double Pd = L->p0_w - kg"),
+]
+
+MIGRATION = [
+    ("destination baseline level from the source", "if (or_gpu_ok(L, F, d, k)) kd0 = k;",
+     "if (or_gpu_ok(L, F, s, k)) kd0 = k;"),
+    ("strict HBM budget", "> (int64_t)F->hbm_cap_mib) return 0;", ">= (int64_t)F->hbm_cap_mib) return 0;"),
+    ("saving sign flipped", "const double sv = L->p0_w - kd * added;", "const double sv = L->p0_w + kd * added;"),
+    ("destination SLOs ignored", "if (or_gpu_ok(L, F, s, k) && or_gpu_ok(L, F, d, k)) kstar = k;",
+     "if (or_gpu_ok(L, F, s, k)) kstar = k;"),
+    ("instance TTFT read from the batch row", "L->pf[or_cell(L, m, row_p, j, k)]",
+     "L->pf[or_cell(L, m, b - 1, j, k)]"),
+    ("merged load drops u_d", "* (us + ud) - or_cube", "* us - or_cube"),
+    ("source may move onto itself", "if (s < 0 || d < 0 || s >= F->n_gpus || d >= F->n_gpus || s == d) return 0;",
+     "if (s < 0 || d < 0 || s >= F->n_gpus || d >= F->n_gpus) return 0;"),
+]
+
+
+def _run_pins(tmp_path, name, old, new, suite):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique/present: {name}"
+    mut = tmp_path / "mut.c"
+    mut.write_text(src.replace(old, new))
+    lib = tmp_path / "libmut.so"
+    subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fPIC", "-shared", "-o", str(lib), str(mut), "-lm"],
+                   check=True)
+    env = dict(os.environ, FESTINA_ORACLE_LIB=str(lib))
+    proc = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                           os.path.join(HERE, suite)], cwd=ROOT, env=env,
+                          stdout=subprocess.PIPE, stderr=subprocess.STDOUT, timeout=600)
+    return proc.returncode, proc.stdout.decode()[-400:]
+
+
+@pytest.mark.parametrize("name,old,new", PLACEMENT, ids=[p[0] for p in PLACEMENT])
+def test_placement_pins_reject_mutant(tmp_path, name, old, new):
+    rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_placement_pins.py")
+    assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
+
+
+@pytest.mark.parametrize("name,old,new", MIGRATION, ids=[p[0] for p in MIGRATION])
+def test_migration_pins_reject_mutant(tmp_path, name, old, new):
+    rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_migration_pins.py")
+    assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
