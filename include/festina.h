@@ -1,0 +1,188 @@
+/*
+ * festina.h -- C ABI of the batched energy-aware placement and migration search
+ * (Festina, "Energy-Aware Scheduling for Serverless LLM Serving on Shared GPUs").
+ *
+ * Two calls do the work:
+ *   festina_score_placements  -- for every pending request, score every
+ *       (GPU, SM-partition level, frequency level) candidate against the offline
+ *       profile tables, drop candidates that miss the TTFT/TBT SLO, and pick the
+ *       least-energy one (Sec. 3.3, Phase One feasibility and Phase Two
+ *       E^k = Power x Latency, argmin over the feasible set; Eq. energy).
+ *   festina_score_migrations  -- for consolidation (Sec. 3.5), score every ordered
+ *       source -> destination GPU pair for moving the whole source workload, and
+ *       return each source's best destination.
+ *
+ * Conventions shared by every entry point
+ *  - All array pointers inside the structs are DEVICE pointers (HIP global memory
+ *    of the current device), laid out as structures of arrays, row-major, with the
+ *    shapes given beside each field.  The caller owns every buffer, including the
+ *    workspace; the library allocates nothing and keeps no pointer after a call.
+ *  - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL = the null
+ *    stream).  Outputs are valid once the caller has synchronised that stream.
+ *    Calls are stateless and reentrant; concurrent calls need distinct workspaces.
+ *  - Errors: a NULL required pointer, a non-positive or inconsistent size, or a
+ *    workspace smaller than the matching *_workspace_bytes() value returns
+ *    FESTINA_ERR_INVALID before anything is launched.  A shape the kernels do not
+ *    support returns FESTINA_ERR_UNSUPPORTED before anything is launched.  A HIP
+ *    launch or runtime failure returns FESTINA_ERR_DEVICE.
+ *  - Bad per-element data never causes an out-of-bounds access: it only makes the
+ *    affected request, GPU or pair infeasible (see each struct).
+ *  - Units: latency ms, power W, energy mJ (W x ms), saving W.
+ */
+#ifndef FESTINA_H
+#define FESTINA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FESTINA_ABI_VERSION 1
+#define FESTINA_N_ROWS 32        /* rows of every profile table */
+#define FESTINA_MAX_CELLS 256    /* n_sm * n_freq limit of the placement kernels */
+#define FESTINA_MAX_FREQ_MIG 32  /* n_freq limit of the migration kernels (32-bit level masks) */
+
+typedef enum {
+  FESTINA_OK = 0,
+  FESTINA_ERR_INVALID = 1,
+  FESTINA_ERR_DEVICE = 2,
+  FESTINA_ERR_UNSUPPORTED = 3
+} festina_status;
+
+/* Offline profile look-up table (Sec. 3.2.1: latency per model under each frequency,
+ * SM share and input length / batch).  Power is the closed form
+ *   P(s, f, u) = p0_w + k_g * s * f^3 * u
+ * (static power plus dynamic power cubic in frequency, Sec. 3.5.1), so it needs no table.
+ *   pf[m][row][j][k]: prefill latency (TTFT, ms) of model m for a prompt in 256-token
+ *                     bucket `row` (tokens in (256*row, 256*(row+1)]), SM level j,
+ *                     frequency level k.
+ *   dc[m][row][j][k]: decode-step latency (TBT, ms) at batch row+1.
+ * NaN or +inf entries are never feasible. */
+typedef struct festina_lut {
+  int32_t n_models;          /* M >= 1 */
+  int32_t n_rows;            /* must be FESTINA_N_ROWS */
+  int32_t n_sm;              /* NS >= 1 */
+  int32_t n_freq;            /* NF >= 1; NS*NF <= FESTINA_MAX_CELLS */
+  const float *sm_level;     /* [NS] SM share s_j in (0, 1] */
+  const float *freq_level;   /* [NF] normalised frequency f_k */
+  const float *pf;           /* [M][32][NS][NF] */
+  const float *dc;           /* [M][32][NS][NF] */
+  float p0_w;                /* static power P0, W */
+} festina_lut;
+
+/* GPU state summaries (Sec. 3.3 Phase One: what each local scheduler reports).
+ * A request admitted to GPU g in wave w runs at batch b = min(batch[w][g] + 1, 32)
+ * and utilisation u = b / 32.  A GPU whose batch is negative (in that wave) or
+ * whose SM cap lies outside [0, NS-1] has no candidates. */
+typedef struct festina_gpus {
+  int32_t n_gpus;            /* G >= 1 */
+  int32_t n_waves;           /* W >= 1 independent snapshots (arrival waves) */
+  const int32_t *batch;      /* [W][G] current batch B_g */
+  const float *k_dyn_w;      /* [G] dynamic-power coefficient k_g, W */
+  const uint32_t *resident;  /* [G][(M+31)/32] bit m set = model m resident on g */
+  const int8_t *cap_pf;      /* [G] or NULL: prefill runs at SM level min(j, cap_pf[g]) */
+  const int8_t *cap_dc;      /* [G] or NULL: decode runs at SM level min(j, cap_dc[g]) */
+} festina_gpus;
+
+/* Pending requests (Sec. 3.3 Phase One: input length, predicted output length, SLOs).
+ * The library applies the 5% output-length safety pad, Lout = ceil(1.05 * pred)
+ * (Sec. 3.2.2), and buckets the prompt, row = min(ceil(tokens/256), 32) - 1; a request
+ * with 0 prompt tokens reads its TTFT from the decode batch row instead.  A model id
+ * outside [0, M), a wave outside [0, W), or negative token counts make the request
+ * infeasible. */
+typedef struct festina_requests {
+  int32_t n_requests;              /* R >= 0 */
+  const int32_t *model;            /* [R] */
+  const int32_t *wave;             /* [R] snapshot index, or NULL (all wave 0) */
+  const int32_t *prompt_tokens;    /* [R] */
+  const int32_t *pred_out_tokens;  /* [R] predicted output tokens (before the pad) */
+  const float *slo_ttft_ms;        /* [R] */
+  const float *slo_tbt_ms;         /* [R] */
+} festina_requests;
+
+/* Placement results, one entry per request (device memory, written by the call):
+ *   choice    = (g * NS + j) * NF + k of the least-energy feasible candidate; among
+ *               candidates of exactly equal energy the lowest index; -1 if none;
+ *   feasible  = 1 if a candidate was chosen, else 0 (the caller scales out,
+ *               Sec. 3.3 Phase Three);
+ *   energy_mj = Pp * TTFT + Lout * Pd * TBT of the choice (float32), +inf if none.
+ * A candidate is feasible when TTFT < slo_ttft and TBT < slo_tbt (strict). */
+typedef struct festina_placements {
+  int32_t *choice;
+  uint8_t *feasible;
+  float *energy_mj;
+} festina_placements;
+
+/* Bytes of device workspace festina_score_placements needs for these shapes
+ * (reads only the scalar fields).  Returns 0 for invalid shapes. */
+size_t festina_placements_workspace_bytes(const festina_lut *lut, const festina_gpus *gpus,
+                                          const festina_requests *req);
+
+/* Score all requests (Sec. 3.3 Phases One-Two; Eq. energy).  `workspace` is device
+ * memory of at least festina_placements_workspace_bytes() bytes, 256-byte aligned;
+ * its contents on entry do not matter and are clobbered. */
+festina_status festina_score_placements(const festina_lut *lut, const festina_gpus *gpus,
+                                        const festina_requests *req, festina_placements *out,
+                                        void *workspace, size_t workspace_bytes, void *stream);
+
+/* Consolidation fleet (Sec. 3.5.2; App. E): every GPU holds 1..max_inst resident
+ * model instances.  Instance i of GPU g meets its SLOs at frequency level k when
+ *   pf[model][prompt row][inst_sm][k] < slo_ttft  and  dc[model][batch row][inst_sm][k] < slo_tbt
+ * (rows as for requests: prompt bucket, or the batch row for 0 prompt tokens; batch row
+ * = min(inst_batch + 1, 32) - 1).  One frequency is shared by the whole GPU (Sec. 2.2),
+ * so a GPU is feasible at k when all of its instances are.  An n_inst outside
+ * [1, max_inst] or any instance field out of range makes the GPU infeasible. */
+typedef struct festina_fleet {
+  int32_t n_gpus;                    /* G >= 2 */
+  int32_t max_inst;                  /* instance slots per GPU, >= 1 */
+  const int32_t *n_inst;             /* [G] */
+  const int32_t *inst_model;         /* [G][max_inst] */
+  const int32_t *inst_prompt_tokens; /* [G][max_inst] */
+  const int32_t *inst_batch;         /* [G][max_inst] */
+  const int32_t *inst_sm;            /* [G][max_inst] SM level index the instance runs at */
+  const float *inst_slo_ttft_ms;     /* [G][max_inst] */
+  const float *inst_slo_tbt_ms;      /* [G][max_inst] */
+  const int32_t *hbm_mib;            /* [G] resident memory footprint, MiB */
+  const int32_t *sm_permille;        /* [G] SM demand (utilisation), per-mille */
+  const float *util;                 /* [G] utilisation u_g used in the power model */
+  const float *k_dyn_w;              /* [G] k_g, W */
+  int32_t hbm_cap_mib;               /* memory budget of one GPU (with any safety margin) */
+  int32_t sm_cap_permille;           /* SM budget, per-mille */
+} festina_fleet;
+
+/* Migration results, one entry per source GPU s (device memory):
+ *   best_dst   = destination d != s maximising saving_w; lowest d on exact ties; -1 if none;
+ *   saving_w   = P0 - k_d * (f[k*]^3 * (u_s + u_d) - f[kd0]^3 * u_d) (float32), -inf if none:
+ *                the source's static power freed minus the destination's added dynamic
+ *                power; may be negative (whether to move is the caller's decision);
+ *   freq_level = k*, the lowest level at which every instance of s and d meets its SLOs
+ *                (kd0 = d's own lowest such level); -1 if none.
+ * A pair is feasible when hbm_s + hbm_d <= hbm_cap, sm_s + sm_d <= sm_cap (inclusive)
+ * and such a k* exists. */
+typedef struct festina_migrations {
+  int32_t *best_dst;
+  float *saving_w;
+  int32_t *freq_level;
+} festina_migrations;
+
+size_t festina_migrations_workspace_bytes(const festina_lut *lut, const festina_fleet *fleet);
+
+/* Score all ordered pairs and reduce per source (Sec. 3.5; capacity check Sec. 3.5.2).
+ * Requires n_freq <= FESTINA_MAX_FREQ_MIG.  Workspace as for placements. */
+festina_status festina_score_migrations(const festina_lut *lut, const festina_fleet *fleet,
+                                        festina_migrations *out, void *workspace,
+                                        size_t workspace_bytes, void *stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char *festina_status_string(festina_status status);
+
+/* FESTINA_ABI_VERSION of the loaded library. */
+int32_t festina_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FESTINA_H */

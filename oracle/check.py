@@ -1,0 +1,105 @@
+"""Acceptance rule for a result under test against the oracle (test infrastructure only).
+
+Placement, per request:
+  * the feasibility flag must equal the oracle's exactly;
+  * when feasible, the tested energy must be within ``rtol`` (1e-5) of the oracle's
+    float64 energy *of the tested choice*, and that choice must be feasible under
+    the oracle;
+  * a choice other than the oracle's is accepted only as a near-tie: its oracle energy
+    is at most the oracle optimum times (1 + rtol).
+Migration, per source: the same on (saving, destination), with the tolerance taken
+relative to max(|saving|, P0), and the frequency level must be the oracle's k* for
+the tested pair exactly.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import candidate_energy, pair_saving
+
+RTOL = 1e-5
+
+
+@dataclass
+class Report:
+    n: int = 0
+    mismatches: list = field(default_factory=list)
+    near_ties: int = 0
+    max_rel_err: float = 0.0
+
+    @property
+    def ok(self):
+        return not self.mismatches
+
+    def __str__(self):
+        head = self.mismatches[:5]
+        return (f"{self.n} checked, {len(self.mismatches)} mismatches, {self.near_ties} near-ties, "
+                f"max rel err {self.max_rel_err:.3g}" + (f"; first: {head}" if head else ""))
+
+
+def check_placements(inp, sel, oracle_out, gpu_out, rtol=RTOL) -> Report:
+    """``sel``: request ids; ``oracle_out``/``gpu_out``: (choice, feasible, energy) for those ids."""
+    oc, of, oe = oracle_out
+    gc, gf, ge = gpu_out
+    rep = Report(n=len(sel))
+    for i, r in enumerate(sel):
+        r = int(r)
+        if int(gf[i]) != int(of[i]):
+            rep.mismatches.append((r, "feasible", int(gf[i]), int(of[i])))
+            continue
+        if not of[i]:
+            if int(gc[i]) != -1 or not np.isinf(ge[i]):
+                rep.mismatches.append((r, "infeasible output", int(gc[i]), float(ge[i])))
+            continue
+        ok, e_at_gpu = candidate_energy(inp, r, int(gc[i]))
+        if not ok:
+            rep.mismatches.append((r, "choice infeasible under the oracle", int(gc[i]), int(oc[i])))
+            continue
+        rel = abs(float(ge[i]) - e_at_gpu) / max(abs(e_at_gpu), 1e-30)
+        rep.max_rel_err = max(rep.max_rel_err, rel)
+        if rel > rtol:
+            rep.mismatches.append((r, "energy", float(ge[i]), e_at_gpu))
+            continue
+        if int(gc[i]) != int(oc[i]):
+            if e_at_gpu <= float(oe[i]) * (1 + rtol) + 1e-30:
+                rep.near_ties += 1
+            else:
+                rep.mismatches.append((r, "choice", int(gc[i]), int(oc[i]), e_at_gpu, float(oe[i])))
+    return rep
+
+
+def check_migrations(inp, sel, oracle_out, gpu_out, rtol=RTOL) -> Report:
+    ob, osv, ok_ = oracle_out
+    gb, gsv, gk = gpu_out
+    p0 = float(inp["lut"]["p0_w"])
+    rep = Report(n=len(sel))
+    for i, s in enumerate(sel):
+        s = int(s)
+        if (int(gb[i]) >= 0) != (int(ob[i]) >= 0):
+            rep.mismatches.append((s, "feasible", int(gb[i]), int(ob[i])))
+            continue
+        if int(ob[i]) < 0:
+            if int(gk[i]) != -1 or not (np.isinf(gsv[i]) and gsv[i] < 0):
+                rep.mismatches.append((s, "infeasible output", int(gk[i]), float(gsv[i])))
+            continue
+        ok, kstar, sv = pair_saving(inp, s, int(gb[i]))
+        if not ok:
+            rep.mismatches.append((s, "pair infeasible under the oracle", int(gb[i]), int(ob[i])))
+            continue
+        if int(gk[i]) != kstar:
+            rep.mismatches.append((s, "freq level", int(gk[i]), kstar))
+            continue
+        scale = max(abs(sv), abs(p0), 1e-30)
+        rel = abs(float(gsv[i]) - sv) / scale
+        rep.max_rel_err = max(rep.max_rel_err, rel)
+        if rel > rtol:
+            rep.mismatches.append((s, "saving", float(gsv[i]), sv))
+            continue
+        if int(gb[i]) != int(ob[i]):
+            if sv >= float(osv[i]) - rtol * max(abs(float(osv[i])), abs(p0)):
+                rep.near_ties += 1
+            else:
+                rep.mismatches.append((s, "destination", int(gb[i]), int(ob[i]), sv, float(osv[i])))
+    return rep

@@ -1,0 +1,839 @@
+// festina.hip -- MI355X (gfx950) kernels and C-ABI host dispatch of the batched
+// energy-aware placement and migration search (Festina, Sec. 3.3 and Sec. 3.5).
+//
+// Placement pipeline (one call, five launches on the caller's stream):
+//   k_zero      clear the bucket counters
+//   k_prep      requests: validity, 5% output pad, prompt bucket, bucket key (wave, model,
+//                 has-prompt) and a counter; hosts: per-model list of hosting GPUs in
+//                 ascending order; GPU records: per (wave, GPU) the post-admission batch
+//                 row, k_g * u_g and the SM caps
+//   k_scan      one block: bucket offsets and the tile table
+//   k_scatter   requests grouped by bucket
+//   k_score     one workgroup per tile (requests of one bucket): the model's decode table is
+//                 staged in LDS; each wave scores Q requests at once, lanes spanning the
+//                 (SM level, frequency level) cells, looping over the hosting GPUs; the
+//                 per-request argmin is fused (running minimum per lane, then a wavefront
+//                 reduction with lowest-index tie-break); only 9 bytes per request reach HBM
+// Migration pipeline:
+//   k_fleet     per GPU: bitmask of frequency levels at which all instances meet their SLOs,
+//                 its lowest level and the dynamic-power baseline f[kd0]^3 * u
+//   k_migrate   one wavefront per group of sources, lanes spanning destinations; fused
+//                 per-source argmax with lowest-destination tie-break
+//
+// Exactness: every SLO and budget test compares a table entry with an SLO, or integers,
+// so it is decided bit-identically to any other correct implementation.  Energies are
+// float32: Pp = fma(k_g*u_g, s*f^3, P0), X = Pp*TTFT, Y = Pd*TBT, E = fma(Lout, Y, X).
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+#include <cstddef>
+#include <cstdint>
+
+#include "festina.h"
+
+namespace {
+
+constexpr int kRows = FESTINA_N_ROWS;
+constexpr int kWave = 64;
+constexpr int kQ = 4;            // requests scored together by one wavefront
+constexpr int kPrepBlock = 256;
+constexpr float kInf = __builtin_huge_valf();
+
+struct HostRec {                 // per (wave, GPU), 16 bytes
+  int32_t row_off;               // (b - 1) * cells, or -1 when the GPU has no candidates
+  float kappa;                   // k_g * b / 32
+  int32_t caps;                  // cap_pf | cap_dc << 8
+  int32_t pad;
+};
+
+struct PlaceArgs {
+  // table
+  int32_t M, NS, NF, C;          // C = NS * NF
+  const float *sm_level, *freq_level, *pf, *dc;
+  float p0;
+  // gpus
+  int32_t G, W, words;
+  const int32_t *batch;
+  const float *kdyn;
+  const uint32_t *resident;
+  const int8_t *cap_pf, *cap_dc;
+  int32_t has_caps;
+  // requests
+  int32_t R;
+  const int32_t *model, *wave, *prompt, *pred;
+  const float *slo_ttft, *slo_tbt;
+  // outputs
+  int32_t *choice;
+  uint8_t *feasible;
+  float *energy;
+  // workspace
+  int32_t NB;                    // buckets = 2 * W * M
+  int32_t tile;                  // requests per tile
+  int32_t max_tiles;
+  int32_t *cnt;                  // [NB] counters, then scatter cursors
+  int32_t *bstart;               // [NB + 1]
+  int32_t *n_tiles;              // [1]
+  int2 *tiles;                   // [max_tiles] {bucket, first position}
+  int32_t *host_cnt;             // [M]
+  int32_t *host_list;            // [M][G]
+  HostRec *recs;                 // [W][G]
+  int32_t *perm;                 // [R]
+  int32_t *key;                  // [R]
+  int32_t *row;                  // [R] prompt row (-1: batch row)
+  float *lout;                   // [R] padded output tokens
+};
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ float cube(float f) { return f * f * f; }
+
+// Read-only view in the constant address space: buffers that a kernel never writes
+// (tables, request fields, the host lists and records made by earlier launches) are
+// then read with scalar loads into SGPRs wherever the address is wave-uniform.
+template <typename T>
+__device__ __forceinline__ const __attribute__((address_space(4))) T *ro(const T *p) {
+  return (const __attribute__((address_space(4))) T *)(p);
+}
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ HostRec load_rec(const __attribute__((address_space(4))) HostRec *rw, int g) {
+  const auto p = reinterpret_cast<const __attribute__((address_space(4))) v4i *>(rw) + g;
+  const v4i v = *p;
+  HostRec r;
+  r.row_off = v.x;
+  r.kappa = __int_as_float(v.y);
+  r.caps = v.z;
+  r.pad = v.w;
+  return r;
+}
+
+// ------------------------------------------------------------------ prologue kernels
+__global__ void k_zero(int32_t *p, int32_t n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+}
+
+// Blocks [0, nbr): requests.  Blocks [nbr, nbr + M): host list of model (block - nbr).
+// Blocks after: GPU records, one thread per (wave, GPU).
+__global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
+  const int b = blockIdx.x;
+  if (b < nbr) {
+    const int r = b * kPrepBlock + threadIdx.x;
+    if (r >= a.R) return;
+    const int m = a.model[r];
+    const int w = a.wave ? a.wave[r] : 0;
+    const int pt = a.prompt[r];
+    const int pr = a.pred[r];
+    const bool ok = m >= 0 && m < a.M && w >= 0 && w < a.W && pt >= 0 && pr >= 0;
+    if (!ok) {
+      a.key[r] = -1;
+      a.choice[r] = -1;
+      a.feasible[r] = 0;
+      a.energy[r] = kInf;
+      return;
+    }
+    // prompt bucket: min(ceil(tokens / 256), 32) - 1 (unsigned: no overflow for any
+    // int32 token count); 0 tokens -> the decode batch row is used
+    const int prow = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
+    // 5% safety pad: ceil(1.05 * pred) = (105 * pred + 99) / 100, in 64-bit
+    const long long lo = ((long long)pr * 105 + 99) / 100;
+    a.row[r] = prow;
+    a.lout[r] = (float)lo;
+    const int k = ((w * a.M + m) << 1) | (prow < 0 ? 1 : 0);
+    a.key[r] = k;
+    atomicAdd(&a.cnt[k], 1);
+    return;
+  }
+  if (b < nbr + a.M) {
+    // ascending list of GPUs whose resident mask has bit m
+    const int m = b - nbr;
+    __shared__ int wsum[kPrepBlock / kWave];
+    __shared__ int base_s;
+    if (threadIdx.x == 0) base_s = 0;
+    __syncthreads();
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x >> 6;
+    for (int g0 = 0; g0 < a.G; g0 += kPrepBlock) {
+      const int g = g0 + threadIdx.x;
+      const bool has = g < a.G && ((a.resident[(size_t)g * a.words + (m >> 5)] >> (m & 31)) & 1u);
+      const unsigned long long bal = __ballot(has);
+      const int before = __popcll(bal & ((1ull << lane) - 1ull));
+      if (lane == 0) wsum[wv] = __popcll(bal);
+      __syncthreads();
+      int off = base_s;
+      for (int i = 0; i < wv; ++i) off += wsum[i];
+      if (has) a.host_list[(size_t)m * a.G + off + before] = g;
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        int t = 0;
+        for (int i = 0; i < kPrepBlock / kWave; ++i) t += wsum[i];
+        base_s += t;
+      }
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) a.host_cnt[m] = base_s;
+    return;
+  }
+  const long long i = (long long)(b - nbr - a.M) * kPrepBlock + threadIdx.x;
+  if (i >= (long long)a.W * a.G) return;
+  const int g = (int)(i % a.G);
+  const int B = a.batch[i];
+  const int cp = a.cap_pf ? (int)a.cap_pf[g] : a.NS - 1;
+  const int cd = a.cap_dc ? (int)a.cap_dc[g] : a.NS - 1;
+  HostRec rec;
+  const bool ok = B >= 0 && cp >= 0 && cp < a.NS && cd >= 0 && cd < a.NS;
+  const int bb = B + 1 > kRows ? kRows : B + 1;
+  rec.row_off = ok ? (bb - 1) * a.C : -1;
+  rec.kappa = a.kdyn[g] * ((float)bb * 0.03125f);   // u = b / 32, exact
+  rec.caps = ok ? (cp | (cd << 8)) : 0;
+  rec.pad = 0;
+  a.recs[i] = rec;
+}
+
+// One block of 1024 threads: exclusive scans of bucket counts and tiles-per-bucket,
+// the tile table, and scatter cursors.
+__global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
+  __shared__ int s_cnt[1024];
+  __shared__ int s_til[1024];
+  const int T = blockDim.x;
+  const int per = (a.NB + T - 1) / T;
+  const int lo = threadIdx.x * per;
+  const int hi = min(lo + per, a.NB);
+  int c = 0, t = 0;
+  for (int i = lo; i < hi; ++i) {
+    const int n = a.cnt[i];
+    c += n;
+    t += (n + a.tile - 1) / a.tile;
+  }
+  s_cnt[threadIdx.x] = c;
+  s_til[threadIdx.x] = t;
+  __syncthreads();
+  for (int off = 1; off < T; off <<= 1) {      // Hillis-Steele inclusive scan
+    const int vc = threadIdx.x >= off ? s_cnt[threadIdx.x - off] : 0;
+    const int vt = threadIdx.x >= off ? s_til[threadIdx.x - off] : 0;
+    __syncthreads();
+    s_cnt[threadIdx.x] += vc;
+    s_til[threadIdx.x] += vt;
+    __syncthreads();
+  }
+  int pc = s_cnt[threadIdx.x] - c;             // exclusive prefix
+  int pt = s_til[threadIdx.x] - t;
+  for (int i = lo; i < hi; ++i) {
+    const int n = a.cnt[i];
+    a.bstart[i] = pc;
+    const int nt = (n + a.tile - 1) / a.tile;
+    for (int q = 0; q < nt; ++q) a.tiles[pt + q] = make_int2(i, pc + q * a.tile);
+    a.cnt[i] = pc;                             // cursor for the scatter
+    pc += n;
+    pt += nt;
+  }
+  if (threadIdx.x == T - 1) {
+    a.bstart[a.NB] = s_cnt[T - 1];
+    *a.n_tiles = s_til[T - 1];
+  }
+}
+
+__global__ void k_scatter(PlaceArgs a) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= a.R) return;
+  const int k = a.key[r];
+  if (k < 0) return;
+  const int pos = atomicAdd(&a.cnt[k], 1);
+  a.perm[pos] = r;
+}
+
+// ------------------------------------------------------------------ scoring kernel
+// (E, idx) lexicographic minimum across the wavefront; idx = INT_MAX means "none".
+__device__ __forceinline__ void wave_argmin(float &e, int &id) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float oe = __shfl_xor(e, off, kWave);
+    const int oi = __shfl_xor(id, off, kWave);
+    if (oe < e || (oe == e && oi < id)) {
+      e = oe;
+      id = oi;
+    }
+  }
+}
+
+// CPL = cells per lane (consecutive cells c = lane*CPL + t).
+// LDS floats needed by k_score<CPL>: the decode table plus a pad that lanes past the
+// last cell may read (their values are masked), s*f^3, and the per-wave prompt rows.
+__host__ __device__ constexpr size_t score_lds_floats(int C, int CPL, int waves) {
+  return (size_t)kRows * C + (size_t)kWave * CPL + C + (size_t)waves * kQ * C;
+}
+
+template <int CPL>
+__global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
+  extern __shared__ __align__(16) float lds[];
+  const int C = a.C, NF = a.NF;
+  float *dcs = lds;                                   // [32 * C + pad] decode table of the tile's model
+  float *pds = lds + kRows * C + kWave * CPL;         // [C] s_j * f_k^3
+  float *rows = pds + C;                              // [waves][Q][C] prompt rows (capped GPUs)
+
+  const int t = blockIdx.x;
+  if (t >= *ro(a.n_tiles)) return;
+  const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
+  const int bucket = tp[2 * t];
+  const bool noprompt = bucket & 1;
+  const int wm = bucket >> 1;
+  const int w = wm / a.M, m = wm - (wm / a.M) * a.M;
+  const int beg = tp[2 * t + 1];
+  const int end = min(beg + a.tile, ro(a.bstart)[bucket + 1]);
+
+  // stage the model's decode table and the dynamic-power factors
+  {
+    const float *src = a.dc + (size_t)m * kRows * C;
+    const int n = kRows * C;
+    if ((((uintptr_t)src) & 15) == 0) {
+      const float4 *s4 = reinterpret_cast<const float4 *>(src);
+      float4 *d4 = reinterpret_cast<float4 *>(dcs);
+      for (int i = threadIdx.x; i < n / 4; i += blockDim.x) d4[i] = s4[i];
+    } else {
+      for (int i = threadIdx.x; i < n; i += blockDim.x) dcs[i] = src[i];
+    }
+    for (int i = threadIdx.x; i < kWave * CPL; i += blockDim.x) dcs[n + i] = 0.f;
+    for (int i = threadIdx.x; i < C; i += blockDim.x) {
+      const int j = i / NF, k = i - (i / NF) * NF;
+      pds[i] = a.sm_level[j] * cube(a.freq_level[k]);
+    }
+  }
+  __syncthreads();
+
+  const int nwaves = blockDim.x / kWave;
+  const int wv = uniform(threadIdx.x >> 6);
+  const int lane = threadIdx.x & (kWave - 1);
+  float *myrows = rows + (size_t)wv * kQ * C;
+  const int hcnt = ro(a.host_cnt)[m];
+  const auto hl = ro(a.host_list + (size_t)m * a.G);
+  const auto rw = ro(a.recs + (size_t)w * a.G);
+  const float p0 = a.p0;
+  const bool caps = a.has_caps != 0;
+
+  int cj[CPL], ck[CPL];
+  bool live[CPL];
+  float pdl[CPL];
+#pragma unroll
+  for (int u = 0; u < CPL; ++u) {
+    const int c = lane * CPL + u;
+    live[u] = c < C;
+    const int cc = live[u] ? c : 0;
+    cj[u] = cc / NF;
+    ck[u] = cc - cj[u] * NF;
+    pdl[u] = pds[cc];
+  }
+
+  for (int base = beg + wv * kQ; base < end; base += nwaves * kQ) {
+    int rq[kQ];
+    float lo[kQ], st[kQ], sb[kQ];
+    int prw[kQ];
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      const int pos = base + q;
+      rq[q] = pos < end ? ro(a.perm)[pos] : -1;
+      if (rq[q] >= 0) {
+        lo[q] = ro(a.lout)[rq[q]];
+        st[q] = ro(a.slo_ttft)[rq[q]];
+        sb[q] = ro(a.slo_tbt)[rq[q]];
+        prw[q] = ro(a.row)[rq[q]];
+      } else {
+        lo[q] = 0.f;
+        st[q] = -kInf;                    // nothing is below -inf: never feasible
+        sb[q] = -kInf;
+        prw[q] = 0;
+      }
+    }
+    float be[kQ][CPL];
+    int bg[kQ][CPL];
+#pragma unroll
+    for (int q = 0; q < kQ; ++q)
+#pragma unroll
+      for (int u = 0; u < CPL; ++u) {
+        be[q][u] = kInf;
+        bg[q][u] = -1;
+      }
+
+    if (noprompt) {
+      // TTFT from the prefill table at the decode batch row (global, L2-resident)
+      const float *pfm = a.pf + (size_t)m * kRows * C;
+      for (int i = 0; i < hcnt; ++i) {
+        const int g = hl[i];
+        const HostRec rec = load_rec(rw, g);
+        if (rec.row_off < 0) continue;
+        const int cp = rec.caps & 0xff, cd = (rec.caps >> 8) & 0xff;
+#pragma unroll
+        for (int u = 0; u < CPL; ++u) {
+          const int cP = min(cj[u], cp) * NF + ck[u];
+          const int cD = min(cj[u], cd) * NF + ck[u];
+          const float tbt = dcs[rec.row_off + cD];
+          const float ttft = pfm[rec.row_off + cP];
+          const float Pp = fmaf(rec.kappa, pds[cP], p0);
+          const float Pd = fmaf(rec.kappa, pds[cD], p0);
+          const float X = Pp * ttft;
+          const float Y = Pd * tbt;
+#pragma unroll
+          for (int q = 0; q < kQ; ++q) {
+            const float E = fmaf(lo[q], Y, X);
+            const bool ok = live[u] && ttft < st[q] && tbt < sb[q] && E < be[q][u];
+            be[q][u] = ok ? E : be[q][u];
+            bg[q][u] = ok ? g : bg[q][u];
+          }
+        }
+      }
+    } else if (!caps) {
+      // uncapped: the request's TTFT cells stay in registers, masked by its TTFT SLO
+      float tt[kQ][CPL];
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        const float *pr = a.pf + ((size_t)m * kRows + prw[q]) * C;
+#pragma unroll
+        for (int u = 0; u < CPL; ++u) {
+          const float v = (rq[q] >= 0 && live[u]) ? pr[lane * CPL + u] : kInf;
+          tt[q][u] = v < st[q] ? v : kInf;
+        }
+      }
+      for (int i = 0; i < hcnt; ++i) {
+        const int g = hl[i];
+        const HostRec rec = load_rec(rw, g);
+        if (rec.row_off < 0) continue;
+        const float *drow = dcs + rec.row_off + lane * CPL;
+#pragma unroll
+        for (int u = 0; u < CPL; ++u) {
+          const float tbt = drow[u];
+          const float P = fmaf(rec.kappa, pdl[u], p0);
+          const float Y = P * tbt;
+#pragma unroll
+          for (int q = 0; q < kQ; ++q) {
+            const float X = P * tt[q][u];
+            const float E = fmaf(lo[q], Y, X);
+            const bool ok = tbt < sb[q] && E < be[q][u];
+            be[q][u] = ok ? E : be[q][u];
+            bg[q][u] = ok ? g : bg[q][u];
+          }
+        }
+      }
+    } else {
+      // capped GPUs: stage each request's masked prompt row in LDS, read at min(j, cap)
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        const float *pr = a.pf + ((size_t)m * kRows + prw[q]) * C;
+        for (int c = lane; c < C; c += kWave) {
+          const float v = rq[q] >= 0 ? pr[c] : kInf;
+          myrows[q * C + c] = v < st[q] ? v : kInf;
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      for (int i = 0; i < hcnt; ++i) {
+        const int g = hl[i];
+        const HostRec rec = load_rec(rw, g);
+        if (rec.row_off < 0) continue;
+        const int cp = rec.caps & 0xff, cd = (rec.caps >> 8) & 0xff;
+#pragma unroll
+        for (int u = 0; u < CPL; ++u) {
+          const int cP = min(cj[u], cp) * NF + ck[u];
+          const int cD = min(cj[u], cd) * NF + ck[u];
+          const float tbt = dcs[rec.row_off + cD];
+          const float Pp = fmaf(rec.kappa, pds[cP], p0);
+          const float Pd = fmaf(rec.kappa, pds[cD], p0);
+          const float Y = Pd * tbt;
+#pragma unroll
+          for (int q = 0; q < kQ; ++q) {
+            const float X = Pp * myrows[q * C + cP];
+            const float E = fmaf(lo[q], Y, X);
+            const bool ok = live[u] && tbt < sb[q] && E < be[q][u];
+            be[q][u] = ok ? E : be[q][u];
+            bg[q][u] = ok ? g : bg[q][u];
+          }
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+
+    // per request: lane minimum over its cells, then the wavefront argmin
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      float e = kInf;
+      int id = INT_MAX;
+#pragma unroll
+      for (int u = 0; u < CPL; ++u) {
+        if (bg[q][u] >= 0) {
+          const int cand = bg[q][u] * C + lane * CPL + u;
+          if (be[q][u] < e || (be[q][u] == e && cand < id)) {
+            e = be[q][u];
+            id = cand;
+          }
+        }
+      }
+      wave_argmin(e, id);
+      if (lane == 0 && rq[q] >= 0) {
+        const bool found = id != INT_MAX;
+        a.choice[rq[q]] = found ? id : -1;
+        a.feasible[rq[q]] = found ? 1 : 0;
+        a.energy[rq[q]] = found ? e : kInf;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ migration kernels
+struct MigArgs {
+  int32_t M, NS, NF, C;
+  const float *freq_level, *pf, *dc;
+  float p0;
+  int32_t G, K;
+  const int32_t *n_inst, *inst_model, *inst_prompt, *inst_batch, *inst_sm;
+  const float *inst_slo_ttft, *inst_slo_tbt;
+  const int32_t *hbm, *smpm;
+  const float *util, *kdyn;
+  int32_t hbm_cap, sm_cap;
+  int32_t *best_dst;
+  float *saving;
+  int32_t *level;
+  uint32_t *fm;                  // [G] feasible-level masks
+  float *base;                   // [G] f[kd0]^3 * u_d
+};
+
+__global__ void k_fleet(MigArgs a) {
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= a.G) return;
+  const int n = a.n_inst[g];
+  uint32_t fm = (n >= 1 && n <= a.K) ? (a.NF >= 32 ? 0xffffffffu : ((1u << a.NF) - 1u)) : 0u;
+  for (int i = 0; i < n && i < a.K && fm; ++i) {
+    const size_t at = (size_t)g * a.K + i;
+    const int m = a.inst_model[at], j = a.inst_sm[at], B = a.inst_batch[at], pt = a.inst_prompt[at];
+    if (m < 0 || m >= a.M || j < 0 || j >= a.NS || B < 0 || pt < 0) {
+      fm = 0;
+      break;
+    }
+    const int bb = B + 1 > kRows ? kRows : B + 1;
+    const int prow = pt == 0 ? bb - 1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
+    const float *pr = a.pf + (((size_t)m * kRows + prow) * a.NS + j) * a.NF;
+    const float *dr = a.dc + (((size_t)m * kRows + (bb - 1)) * a.NS + j) * a.NF;
+    const float st = a.inst_slo_ttft[at], sb = a.inst_slo_tbt[at];
+    uint32_t mk = 0;
+    for (int k = 0; k < a.NF; ++k)
+      if (pr[k] < st && dr[k] < sb) mk |= 1u << k;
+    fm &= mk;
+  }
+  a.fm[g] = fm;
+  a.base[g] = fm ? cube(a.freq_level[__builtin_ctz(fm)]) * a.util[g] : 0.f;
+}
+
+constexpr int kSrcPerWave = 2;
+
+__global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
+  __shared__ float f3[32];
+  if (threadIdx.x < 32) f3[threadIdx.x] = threadIdx.x < a.NF ? cube(a.freq_level[threadIdx.x]) : 0.f;
+  __syncthreads();
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = uniform(threadIdx.x >> 6);
+  const int s0 = (blockIdx.x * (blockDim.x / kWave) + wv) * kSrcPerWave;
+  if (s0 >= a.G) return;
+  int src[kSrcPerWave], remH[kSrcPerWave], remU[kSrcPerWave];
+  uint32_t fms[kSrcPerWave];
+  float us[kSrcPerWave];
+  bool any[kSrcPerWave];
+#pragma unroll
+  for (int q = 0; q < kSrcPerWave; ++q) {
+    src[q] = s0 + q;
+    const bool v = src[q] < a.G;
+    const int s = v ? src[q] : 0;
+    const long long rh = (long long)a.hbm_cap - a.hbm[s];
+    const long long ru = (long long)a.sm_cap - a.smpm[s];
+    any[q] = v && rh >= (long long)INT_MIN && ru >= (long long)INT_MIN;
+    remH[q] = (int)(rh > INT_MAX ? INT_MAX : (rh < INT_MIN ? INT_MIN : rh));
+    remU[q] = (int)(ru > INT_MAX ? INT_MAX : (ru < INT_MIN ? INT_MIN : ru));
+    fms[q] = v ? a.fm[s] : 0u;
+    us[q] = a.util[s];
+  }
+  float bs[kSrcPerWave];
+  int bd[kSrcPerWave], bk[kSrcPerWave];
+#pragma unroll
+  for (int q = 0; q < kSrcPerWave; ++q) {
+    bs[q] = -kInf;
+    bd[q] = INT_MAX;
+    bk[q] = -1;
+  }
+  for (int d = lane; d < a.G; d += kWave) {
+    const int hd = a.hbm[d], ud_pm = a.smpm[d];
+    const uint32_t fmd = a.fm[d];
+    const float ud = a.util[d], kd = a.kdyn[d], bb = a.base[d];
+#pragma unroll
+    for (int q = 0; q < kSrcPerWave; ++q) {
+      const uint32_t f = fms[q] & fmd;
+      const bool ok = any[q] && d != src[q] && hd <= remH[q] && ud_pm <= remU[q] && f != 0u;
+      const int k = __builtin_ctz(f | 0x80000000u);
+      const float added = f3[k] * (us[q] + ud) - bb;
+      const float sv = fmaf(-kd, added, a.p0);
+      const bool better = ok && sv > bs[q];
+      bs[q] = better ? sv : bs[q];
+      bd[q] = better ? d : bd[q];
+      bk[q] = better ? k : bk[q];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kSrcPerWave; ++q) {
+    float v = bs[q];
+    int d = bd[q], k = bk[q];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const float ov = __shfl_xor(v, off, kWave);
+      const int od = __shfl_xor(d, off, kWave);
+      const int ok2 = __shfl_xor(k, off, kWave);
+      if (ov > v || (ov == v && od < d)) {
+        v = ov;
+        d = od;
+        k = ok2;
+      }
+    }
+    if (lane == 0 && src[q] < a.G) {
+      const bool found = d != INT_MAX;
+      a.best_dst[src[q]] = found ? d : -1;
+      a.saving[src[q]] = found ? v : -kInf;
+      a.level[src[q]] = found ? k : -1;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ host helpers
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct PlaceLayout {
+  size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, perm, key, row, lout, total;
+  int32_t NB, tile, max_tiles, waves_per_block;
+};
+
+bool place_shapes_ok(const festina_lut *L, const festina_gpus *G, const festina_requests *Q) {
+  if (!L || !G || !Q) return false;
+  if (L->n_models < 1 || L->n_rows != kRows || L->n_sm < 1 || L->n_freq < 1) return false;
+  if (G->n_gpus < 1 || G->n_waves < 1 || Q->n_requests < 0) return false;
+  return true;
+}
+
+bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_requests *Q, PlaceLayout *o) {
+  if (!place_shapes_ok(L, G, Q)) return false;
+  const long long M = L->n_models, Gn = G->n_gpus, W = G->n_waves, R = Q->n_requests;
+  const long long C = (long long)L->n_sm * L->n_freq;
+  const long long NB = 2 * W * M;
+  if (NB > INT_MAX / 2 || Gn * C > INT_MAX || W * Gn > INT_MAX || M * Gn > INT_MAX) return false;
+  // tile size: large tiles amortise the table staging, small ones fill the chip
+  int wpb = 4, tile = 2 * 4 * kQ;
+  if (R < 2048LL * tile) {
+    tile = 4 * kQ;
+    if (R < 1024LL * tile) {
+      wpb = 1;
+      tile = kQ;
+    }
+  }
+  const long long max_tiles = (R + tile - 1) / tile + NB;
+  if (max_tiles > INT_MAX) return false;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align256(off + bytes);
+    return at;
+  };
+  o->cnt = take(sizeof(int32_t) * NB);
+  o->bstart = take(sizeof(int32_t) * (NB + 1));
+  o->ntiles = take(sizeof(int32_t));
+  o->tiles = take(sizeof(int2) * max_tiles);
+  o->host_cnt = take(sizeof(int32_t) * M);
+  o->host_list = take(sizeof(int32_t) * M * Gn);
+  o->recs = take(sizeof(HostRec) * W * Gn);
+  o->perm = take(sizeof(int32_t) * (R > 0 ? R : 1));
+  o->key = take(sizeof(int32_t) * (R > 0 ? R : 1));
+  o->row = take(sizeof(int32_t) * (R > 0 ? R : 1));
+  o->lout = take(sizeof(float) * (R > 0 ? R : 1));
+  o->total = off;
+  o->NB = (int32_t)NB;
+  o->tile = tile;
+  o->max_tiles = (int32_t)max_tiles;
+  o->waves_per_block = wpb;
+  return true;
+}
+
+template <int CPL>
+hipError_t launch_score(const PlaceArgs &a, int blocks, int wpb, size_t lds, hipStream_t st) {
+  k_score<CPL><<<blocks, wpb * kWave, lds, st>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+extern "C" {
+
+int32_t festina_abi_version(void) { return FESTINA_ABI_VERSION; }
+
+const char *festina_status_string(festina_status s) {
+  switch (s) {
+    case FESTINA_OK: return "ok";
+    case FESTINA_ERR_INVALID: return "invalid argument (null pointer, bad size or workspace too small)";
+    case FESTINA_ERR_DEVICE: return "HIP device error";
+    case FESTINA_ERR_UNSUPPORTED: return "shape not supported by the kernels";
+  }
+  return "unknown status";
+}
+
+size_t festina_placements_workspace_bytes(const festina_lut *lut, const festina_gpus *gpus,
+                                          const festina_requests *req) {
+  PlaceLayout lay;
+  if (!place_layout(lut, gpus, req, &lay)) return 0;
+  return lay.total;
+}
+
+festina_status festina_score_placements(const festina_lut *L, const festina_gpus *G,
+                                        const festina_requests *Q, festina_placements *out,
+                                        void *workspace, size_t workspace_bytes, void *stream) {
+  if (!place_shapes_ok(L, G, Q) || !out) return FESTINA_ERR_INVALID;
+  const long long C = (long long)L->n_sm * L->n_freq;
+  if (C > FESTINA_MAX_CELLS) return FESTINA_ERR_UNSUPPORTED;
+  if (!L->sm_level || !L->freq_level || !L->pf || !L->dc) return FESTINA_ERR_INVALID;
+  if (!G->batch || !G->k_dyn_w || !G->resident) return FESTINA_ERR_INVALID;
+  PlaceLayout lay;
+  if (!place_layout(L, G, Q, &lay)) return FESTINA_ERR_INVALID;
+  if (Q->n_requests == 0) return FESTINA_OK;
+  if (!Q->model || !Q->prompt_tokens || !Q->pred_out_tokens || !Q->slo_ttft_ms || !Q->slo_tbt_ms)
+    return FESTINA_ERR_INVALID;
+  if (!out->choice || !out->feasible || !out->energy_mj) return FESTINA_ERR_INVALID;
+  if (!workspace || workspace_bytes < lay.total || (((uintptr_t)workspace) & 255) != 0)
+    return FESTINA_ERR_INVALID;
+
+  char *ws = static_cast<char *>(workspace);
+  PlaceArgs a;
+  a.M = L->n_models;
+  a.NS = L->n_sm;
+  a.NF = L->n_freq;
+  a.C = (int32_t)C;
+  a.sm_level = L->sm_level;
+  a.freq_level = L->freq_level;
+  a.pf = L->pf;
+  a.dc = L->dc;
+  a.p0 = L->p0_w;
+  a.G = G->n_gpus;
+  a.W = G->n_waves;
+  a.words = (L->n_models + 31) / 32;
+  a.batch = G->batch;
+  a.kdyn = G->k_dyn_w;
+  a.resident = G->resident;
+  a.cap_pf = G->cap_pf;
+  a.cap_dc = G->cap_dc;
+  a.has_caps = (G->cap_pf || G->cap_dc) ? 1 : 0;
+  a.R = Q->n_requests;
+  a.model = Q->model;
+  a.wave = Q->wave;
+  a.prompt = Q->prompt_tokens;
+  a.pred = Q->pred_out_tokens;
+  a.slo_ttft = Q->slo_ttft_ms;
+  a.slo_tbt = Q->slo_tbt_ms;
+  a.choice = out->choice;
+  a.feasible = out->feasible;
+  a.energy = out->energy_mj;
+  a.NB = lay.NB;
+  a.tile = lay.tile;
+  a.max_tiles = lay.max_tiles;
+  a.cnt = reinterpret_cast<int32_t *>(ws + lay.cnt);
+  a.bstart = reinterpret_cast<int32_t *>(ws + lay.bstart);
+  a.n_tiles = reinterpret_cast<int32_t *>(ws + lay.ntiles);
+  a.tiles = reinterpret_cast<int2 *>(ws + lay.tiles);
+  a.host_cnt = reinterpret_cast<int32_t *>(ws + lay.host_cnt);
+  a.host_list = reinterpret_cast<int32_t *>(ws + lay.host_list);
+  a.recs = reinterpret_cast<HostRec *>(ws + lay.recs);
+  a.perm = reinterpret_cast<int32_t *>(ws + lay.perm);
+  a.key = reinterpret_cast<int32_t *>(ws + lay.key);
+  a.row = reinterpret_cast<int32_t *>(ws + lay.row);
+  a.lout = reinterpret_cast<float *>(ws + lay.lout);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int zb = (lay.NB + 255) / 256;
+  k_zero<<<zb < 1024 ? zb : 1024, 256, 0, st>>>(a.cnt, lay.NB);
+  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  const int nbr = (a.R + kPrepBlock - 1) / kPrepBlock;
+  const long long nrec = ((long long)a.W * a.G + kPrepBlock - 1) / kPrepBlock;
+  k_prep<<<(unsigned)(nbr + a.M + nrec), kPrepBlock, 0, st>>>(a, nbr);
+  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  k_scan<<<1, 1024, 0, st>>>(a);
+  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  k_scatter<<<nbr, kPrepBlock, 0, st>>>(a);
+  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  const int cpl = C <= 64 ? 1 : (C <= 128 ? 2 : 4);
+  const size_t lds = sizeof(float) * score_lds_floats((int)C, cpl, lay.waves_per_block);
+  hipError_t e;
+  if (cpl == 1)
+    e = launch_score<1>(a, lay.max_tiles, lay.waves_per_block, lds, st);
+  else if (cpl == 2)
+    e = launch_score<2>(a, lay.max_tiles, lay.waves_per_block, lds, st);
+  else
+    e = launch_score<4>(a, lay.max_tiles, lay.waves_per_block, lds, st);
+  return e == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
+}
+
+static bool mig_shapes_ok(const festina_lut *L, const festina_fleet *F) {
+  if (!L || !F) return false;
+  if (L->n_models < 1 || L->n_rows != kRows || L->n_sm < 1 || L->n_freq < 1) return false;
+  if (F->n_gpus < 2 || F->max_inst < 1) return false;
+  if ((long long)F->n_gpus * F->max_inst > INT_MAX) return false;
+  return true;
+}
+
+size_t festina_migrations_workspace_bytes(const festina_lut *lut, const festina_fleet *fleet) {
+  if (!mig_shapes_ok(lut, fleet)) return 0;
+  return align256(sizeof(uint32_t) * fleet->n_gpus) + align256(sizeof(float) * fleet->n_gpus);
+}
+
+festina_status festina_score_migrations(const festina_lut *L, const festina_fleet *F,
+                                        festina_migrations *out, void *workspace,
+                                        size_t workspace_bytes, void *stream) {
+  if (!mig_shapes_ok(L, F) || !out) return FESTINA_ERR_INVALID;
+  if (L->n_freq > FESTINA_MAX_FREQ_MIG) return FESTINA_ERR_UNSUPPORTED;
+  if (!L->freq_level || !L->pf || !L->dc) return FESTINA_ERR_INVALID;
+  if (!F->n_inst || !F->inst_model || !F->inst_prompt_tokens || !F->inst_batch || !F->inst_sm ||
+      !F->inst_slo_ttft_ms || !F->inst_slo_tbt_ms || !F->hbm_mib || !F->sm_permille || !F->util ||
+      !F->k_dyn_w)
+    return FESTINA_ERR_INVALID;
+  if (!out->best_dst || !out->saving_w || !out->freq_level) return FESTINA_ERR_INVALID;
+  const size_t need = festina_migrations_workspace_bytes(L, F);
+  if (!workspace || workspace_bytes < need || (((uintptr_t)workspace) & 255) != 0) return FESTINA_ERR_INVALID;
+  MigArgs a;
+  a.M = L->n_models;
+  a.NS = L->n_sm;
+  a.NF = L->n_freq;
+  a.C = L->n_sm * L->n_freq;
+  a.freq_level = L->freq_level;
+  a.pf = L->pf;
+  a.dc = L->dc;
+  a.p0 = L->p0_w;
+  a.G = F->n_gpus;
+  a.K = F->max_inst;
+  a.n_inst = F->n_inst;
+  a.inst_model = F->inst_model;
+  a.inst_prompt = F->inst_prompt_tokens;
+  a.inst_batch = F->inst_batch;
+  a.inst_sm = F->inst_sm;
+  a.inst_slo_ttft = F->inst_slo_ttft_ms;
+  a.inst_slo_tbt = F->inst_slo_tbt_ms;
+  a.hbm = F->hbm_mib;
+  a.smpm = F->sm_permille;
+  a.util = F->util;
+  a.kdyn = F->k_dyn_w;
+  a.hbm_cap = F->hbm_cap_mib;
+  a.sm_cap = F->sm_cap_permille;
+  a.best_dst = out->best_dst;
+  a.saving = out->saving_w;
+  a.level = out->freq_level;
+  char *ws = static_cast<char *>(workspace);
+  a.fm = reinterpret_cast<uint32_t *>(ws);
+  a.base = reinterpret_cast<float *>(ws + align256(sizeof(uint32_t) * F->n_gpus));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  k_fleet<<<(a.G + 255) / 256, 256, 0, st>>>(a);
+  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  const int per_block = 4 * kSrcPerWave;
+  k_migrate<<<(a.G + per_block - 1) / per_block, 256, 0, st>>>(a);
+  return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
+}
+
+}  // extern "C"

@@ -1,0 +1,229 @@
+"""Thin ctypes binding of the C ABI in include/festina.h.
+
+Argument marshalling only: every step of the search runs in the HIP library
+(``libfestina.so`` built from ``csrc/festina.hip``).  PyTorch provides device
+memory and streams.  There is no CPU fallback: if the library is missing this
+module raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfestina.so")
+
+FESTINA_OK = 0
+FESTINA_ERR_INVALID = 1
+FESTINA_ERR_DEVICE = 2
+FESTINA_ERR_UNSUPPORTED = 3
+
+
+class FestinaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {festina_status_string(status)} (status {status})")
+        self.status = status
+
+
+class festina_lut(C.Structure):
+    _fields_ = [("n_models", C.c_int32), ("n_rows", C.c_int32), ("n_sm", C.c_int32),
+                ("n_freq", C.c_int32), ("sm_level", C.c_void_p), ("freq_level", C.c_void_p),
+                ("pf", C.c_void_p), ("dc", C.c_void_p), ("p0_w", C.c_float)]
+
+
+class festina_gpus(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("n_waves", C.c_int32), ("batch", C.c_void_p),
+                ("k_dyn_w", C.c_void_p), ("resident", C.c_void_p), ("cap_pf", C.c_void_p),
+                ("cap_dc", C.c_void_p)]
+
+
+class festina_requests(C.Structure):
+    _fields_ = [("n_requests", C.c_int32), ("model", C.c_void_p), ("wave", C.c_void_p),
+                ("prompt_tokens", C.c_void_p), ("pred_out_tokens", C.c_void_p),
+                ("slo_ttft_ms", C.c_void_p), ("slo_tbt_ms", C.c_void_p)]
+
+
+class festina_placements(C.Structure):
+    _fields_ = [("choice", C.c_void_p), ("feasible", C.c_void_p), ("energy_mj", C.c_void_p)]
+
+
+class festina_fleet(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("max_inst", C.c_int32), ("n_inst", C.c_void_p),
+                ("inst_model", C.c_void_p), ("inst_prompt_tokens", C.c_void_p),
+                ("inst_batch", C.c_void_p), ("inst_sm", C.c_void_p),
+                ("inst_slo_ttft_ms", C.c_void_p), ("inst_slo_tbt_ms", C.c_void_p),
+                ("hbm_mib", C.c_void_p), ("sm_permille", C.c_void_p), ("util", C.c_void_p),
+                ("k_dyn_w", C.c_void_p), ("hbm_cap_mib", C.c_int32), ("sm_cap_permille", C.c_int32)]
+
+
+class festina_migrations(C.Structure):
+    _fields_ = [("best_dst", C.c_void_p), ("saving_w", C.c_void_p), ("freq_level", C.c_void_p)]
+
+
+EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_workspace_bytes",
+            "festina_score_placements", "festina_migrations_workspace_bytes", "festina_score_migrations")
+
+_lib = None
+
+
+def lib():
+    """Load the built HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"HIP library {LIB_PATH} is not built; run __graft_entry__.build()")
+        L = C.CDLL(LIB_PATH)
+        P = C.POINTER
+        L.festina_abi_version.restype = C.c_int32
+        L.festina_status_string.argtypes = [C.c_int]
+        L.festina_status_string.restype = C.c_char_p
+        L.festina_placements_workspace_bytes.argtypes = [P(festina_lut), P(festina_gpus), P(festina_requests)]
+        L.festina_placements_workspace_bytes.restype = C.c_size_t
+        L.festina_score_placements.argtypes = [P(festina_lut), P(festina_gpus), P(festina_requests),
+                                               P(festina_placements), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.festina_score_placements.restype = C.c_int
+        L.festina_migrations_workspace_bytes.argtypes = [P(festina_lut), P(festina_fleet)]
+        L.festina_migrations_workspace_bytes.restype = C.c_size_t
+        L.festina_score_migrations.argtypes = [P(festina_lut), P(festina_fleet), P(festina_migrations),
+                                               C.c_void_p, C.c_size_t, C.c_void_p]
+        L.festina_score_migrations.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def festina_abi_version() -> int:
+    return int(lib().festina_abi_version())
+
+
+def festina_status_string(status: int) -> str:
+    return lib().festina_status_string(int(status)).decode()
+
+
+# ------------------------------------------------------------------ device marshalling
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream_handle(stream):
+    if stream is None:
+        import torch
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return C.c_void_p(stream)
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _dev(a, dtype, device):
+    import torch
+    if a is None:
+        return None
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=dtype)).to(device)
+
+
+class DevicePlacement:
+    """Placement inputs copied to device memory once, with the ABI structs pointing at them."""
+
+    def __init__(self, inp: dict, device="cuda"):
+        import torch
+        lut, gp, rq = inp["lut"], inp["gpus"], inp["requests"]
+        d = lambda a, t: _dev(a, t, device)
+        self.t = {
+            "sm_level": d(lut["sm_level"], np.float32), "freq_level": d(lut["freq_level"], np.float32),
+            "pf": d(lut["pf"], np.float32), "dc": d(lut["dc"], np.float32),
+            "batch": d(gp["batch"], np.int32), "k_dyn_w": d(gp["k_dyn_w"], np.float32),
+            "resident": d(np.asarray(gp["resident"], np.uint32).view(np.int32), np.int32),
+            "cap_pf": d(gp.get("cap_pf"), np.int8), "cap_dc": d(gp.get("cap_dc"), np.int8),
+            "model": d(rq["model"], np.int32), "wave": d(rq.get("wave"), np.int32),
+            "prompt_tokens": d(rq["prompt_tokens"], np.int32),
+            "pred_out_tokens": d(rq["pred_out_tokens"], np.int32),
+            "slo_ttft_ms": d(rq["slo_ttft_ms"], np.float32), "slo_tbt_ms": d(rq["slo_tbt_ms"], np.float32),
+        }
+        t = self.t
+        self.lut = festina_lut(int(lut["n_models"]), int(lut["n_rows"]), int(lut["n_sm"]), int(lut["n_freq"]),
+                               _ptr(t["sm_level"]), _ptr(t["freq_level"]), _ptr(t["pf"]), _ptr(t["dc"]),
+                               float(lut["p0_w"]))
+        self.gpus = festina_gpus(int(gp["n_gpus"]), int(gp["n_waves"]), _ptr(t["batch"]), _ptr(t["k_dyn_w"]),
+                                 _ptr(t["resident"]), _ptr(t["cap_pf"]), _ptr(t["cap_dc"]))
+        self.R = int(rq["n_requests"])
+        self.req = festina_requests(self.R, _ptr(t["model"]), _ptr(t["wave"]), _ptr(t["prompt_tokens"]),
+                                    _ptr(t["pred_out_tokens"]), _ptr(t["slo_ttft_ms"]), _ptr(t["slo_tbt_ms"]))
+        n = max(self.R, 1)
+        self.choice = torch.empty(n, dtype=torch.int32, device=device)
+        self.feasible = torch.empty(n, dtype=torch.uint8, device=device)
+        self.energy = torch.empty(n, dtype=torch.float32, device=device)
+        self.out = festina_placements(_ptr(self.choice), _ptr(self.feasible), _ptr(self.energy))
+        self.ws_bytes = festina_placements_workspace_bytes(self.lut, self.gpus, self.req)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
+
+    def run(self, stream=None):
+        festina_score_placements(self.lut, self.gpus, self.req, self.out, self.workspace, self.ws_bytes, stream)
+
+    def results(self):
+        R = self.R
+        return (self.choice[:R].cpu().numpy(), self.feasible[:R].cpu().numpy(), self.energy[:R].cpu().numpy())
+
+
+class DeviceMigration:
+    """Consolidation fleet copied to device memory once, with the ABI structs pointing at it."""
+
+    def __init__(self, inp: dict, device="cuda"):
+        import torch
+        lut, fl = inp["lut"], inp["fleet"]
+        d = lambda a, t: _dev(a, t, device)
+        self.t = {
+            "freq_level": d(lut["freq_level"], np.float32), "sm_level": d(lut["sm_level"], np.float32),
+            "pf": d(lut["pf"], np.float32), "dc": d(lut["dc"], np.float32),
+        }
+        for k in ("n_inst", "inst_model", "inst_prompt_tokens", "inst_batch", "inst_sm", "hbm_mib", "sm_permille"):
+            self.t[k] = d(fl[k], np.int32)
+        for k in ("inst_slo_ttft_ms", "inst_slo_tbt_ms", "util", "k_dyn_w"):
+            self.t[k] = d(fl[k], np.float32)
+        t = self.t
+        self.lut = festina_lut(int(lut["n_models"]), int(lut["n_rows"]), int(lut["n_sm"]), int(lut["n_freq"]),
+                               _ptr(t["sm_level"]), _ptr(t["freq_level"]), _ptr(t["pf"]), _ptr(t["dc"]),
+                               float(lut["p0_w"]))
+        self.G = int(fl["n_gpus"])
+        self.fleet = festina_fleet(self.G, int(fl["max_inst"]), _ptr(t["n_inst"]), _ptr(t["inst_model"]),
+                                   _ptr(t["inst_prompt_tokens"]), _ptr(t["inst_batch"]), _ptr(t["inst_sm"]),
+                                   _ptr(t["inst_slo_ttft_ms"]), _ptr(t["inst_slo_tbt_ms"]), _ptr(t["hbm_mib"]),
+                                   _ptr(t["sm_permille"]), _ptr(t["util"]), _ptr(t["k_dyn_w"]),
+                                   int(fl["hbm_cap_mib"]), int(fl["sm_cap_permille"]))
+        self.best_dst = torch.empty(self.G, dtype=torch.int32, device=device)
+        self.saving = torch.empty(self.G, dtype=torch.float32, device=device)
+        self.level = torch.empty(self.G, dtype=torch.int32, device=device)
+        self.out = festina_migrations(_ptr(self.best_dst), _ptr(self.saving), _ptr(self.level))
+        self.ws_bytes = festina_migrations_workspace_bytes(self.lut, self.fleet)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
+
+    def run(self, stream=None):
+        festina_score_migrations(self.lut, self.fleet, self.out, self.workspace, self.ws_bytes, stream)
+
+    def results(self):
+        return self.best_dst.cpu().numpy(), self.saving.cpu().numpy(), self.level.cpu().numpy()
+
+
+# ------------------------------------------------------------------ the ABI calls
+def festina_placements_workspace_bytes(lut, gpus, req) -> int:
+    return int(lib().festina_placements_workspace_bytes(C.byref(lut), C.byref(gpus), C.byref(req)))
+
+
+def festina_score_placements(lut, gpus, req, out, workspace, workspace_bytes, stream=None) -> None:
+    ws = None if workspace is None else C.c_void_p(workspace.data_ptr())
+    st = lib().festina_score_placements(C.byref(lut), C.byref(gpus), C.byref(req), C.byref(out), ws,
+                                        int(workspace_bytes), _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_score_placements")
+
+
+def festina_migrations_workspace_bytes(lut, fleet) -> int:
+    return int(lib().festina_migrations_workspace_bytes(C.byref(lut), C.byref(fleet)))
+
+
+def festina_score_migrations(lut, fleet, out, workspace, workspace_bytes, stream=None) -> None:
+    ws = None if workspace is None else C.c_void_p(workspace.data_ptr())
+    st = lib().festina_score_migrations(C.byref(lut), C.byref(fleet), C.byref(out), ws,
+                                        int(workspace_bytes), _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_score_migrations")

@@ -1,0 +1,227 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Flags and indices must match exactly and energies within 1e-5 (relative); a
+different index is accepted only as a near-tie judged by the oracle's own float64
+energies (oracle/check.py).  Covers the five configurations (full sizes with
+sampled oracle checks, and oracle-sized runs spanning several tiles with ragged
+tails), extra seeds, odd table shapes, caps, prompt-less requests, NaN/inf tables,
+invalid per-element data, empty input, unaligned tables, determinism and streams.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.check import check_migrations, check_placements
+from paper_2606_30391_amd import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def festina():
+    from paper_2606_30391_amd import festina as F
+    F.lib()
+    return F
+
+
+def run_place(inp, stream=None):
+    dp = festina().DevicePlacement(inp, "cuda")
+    dp.run(stream)
+    torch.cuda.synchronize()
+    return dp.results()
+
+
+def parity_place(inp, sel=None, label=""):
+    R = inp["requests"]["n_requests"]
+    say(f"[gpu] placement {label}: R={R} G={inp['gpus']['n_gpus']} W={inp['gpus']['n_waves']} "
+        f"NS={inp['lut']['n_sm']} NF={inp['lut']['n_freq']}")
+    got = run_place(inp)
+    sel = np.arange(R) if sel is None else np.asarray(sel)
+    ref = oracle.score_placements(inp, sel)
+    rep = check_placements(inp, sel, ref, tuple(x[sel] for x in got))
+    say(f"      {rep}")
+    assert rep.ok, str(rep)
+    return got, rep
+
+
+def run_mig(inp):
+    dm = festina().DeviceMigration(inp, "cuda")
+    dm.run()
+    torch.cuda.synchronize()
+    return dm.results()
+
+
+def parity_mig(inp, sel=None, label=""):
+    G = inp["fleet"]["n_gpus"]
+    say(f"[gpu] migration {label}: G={G} NF={inp['lut']['n_freq']}")
+    got = run_mig(inp)
+    sel = np.arange(G) if sel is None else np.asarray(sel)
+    ref = oracle.score_migrations(inp, sel)
+    rep = check_migrations(inp, sel, ref, tuple(x[sel] for x in got))
+    say(f"      {rep}")
+    assert rep.ok, str(rep)
+    return got, rep
+
+
+# ------------------------------------------------------------------ the five configurations
+@pytest.mark.parametrize("cfg", [1, 2])
+@pytest.mark.parametrize("extra", [0, 100, 200, 300])
+def test_small_configs_full(cfg, extra):
+    parity_place(W.make_placement(cfg, seed=W.config_seed(cfg, extra)), label=f"cfg{cfg}+{extra}")
+
+
+@pytest.mark.parametrize("cfg,R", [(3, 5003), (3, 20011), (4, 3001), (4, 20011)])
+def test_large_configs_oracle_sized(cfg, R):
+    # all GPUs and tables of the configuration; fewer requests so the oracle checks every one
+    parity_place(W.make_placement(cfg, n_requests=R), label=f"cfg{cfg} R={R}")
+
+
+@pytest.mark.parametrize("cfg", [3, 4])
+@pytest.mark.parametrize("extra", [0, 100])
+def test_large_configs_full_size_sampled(cfg, extra):
+    inp = W.make_placement(cfg, seed=W.config_seed(cfg, extra))
+    R = inp["requests"]["n_requests"]
+    sel = np.random.default_rng(cfg + extra).choice(R, 2500, replace=False)
+    got, rep = parity_place(inp, sel, label=f"cfg{cfg}+{extra} full")
+    # properties over every request: choices in range and consistent with the flags
+    ch, fe, en = got
+    NS, NF, G = inp["lut"]["n_sm"], inp["lut"]["n_freq"], inp["gpus"]["n_gpus"]
+    assert np.all((fe == 1) == (ch >= 0))
+    assert np.all(ch < G * NS * NF)
+    assert np.all(np.isinf(en[fe == 0])) and np.all(np.isfinite(en[fe == 1]))
+    # the chosen GPU hosts the request's model
+    m = inp["requests"]["model"][fe == 1]
+    g = ch[fe == 1] // (NS * NF)
+    assert np.all((inp["gpus"]["resident"][g, m // 32] >> (m % 32).astype(np.uint32)) & 1)
+    if cfg == 3:
+        assert np.all(fe[inp["meta"]["planted"]] == 0)
+
+
+def test_config5_full():
+    parity_mig(W.make_fleet(), label="cfg5 full")
+
+
+@pytest.mark.parametrize("extra", [100, 200, 300])
+def test_config5_seeds(extra):
+    parity_mig(W.make_fleet(seed=W.config_seed(5, extra), n_gpus=700), label=f"cfg5+{extra} G=700")
+
+
+# ------------------------------------------------------------------ shapes and edge cases
+SHAPES = [(1, 1), (3, 5), (4, 8), (7, 9), (8, 8), (5, 13), (8, 12), (1, 127), (8, 16), (3, 43),
+          (8, 25), (16, 16)]
+
+
+@pytest.mark.parametrize("NS,NF", SHAPES)
+@pytest.mark.parametrize("caps", [False, True])
+def test_cell_shapes(NS, NF, caps):
+    rng = np.random.default_rng(NS * 100 + NF + (7 if caps else 0))
+    inp = W.make_tiny_placement(rng, R=61, G=9, M=3, NS=NS, NF=NF, W=2, caps=caps)
+    parity_place(inp, label=f"shape {NS}x{NF} caps={caps}")
+
+
+def test_many_gpus_and_models():
+    rng = np.random.default_rng(4)
+    inp = W.make_tiny_placement(rng, R=301, G=300, M=37, NS=8, NF=16, W=3, caps=True)
+    parity_place(inp, label="G=300 M=37 (two resident words)")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_ties_nan_and_bad_elements(seed):
+    rng = np.random.default_rng(900 + seed)
+    parity_place(W.make_tiny_placement(rng, R=40, G=6, M=2, NS=4, NF=6, ties=True), label="ties")
+    parity_place(W.make_tiny_placement(rng, R=40, G=6, M=2, NS=4, NF=6, nan_cells=True), label="nan/inf")
+    inp = W.make_tiny_placement(rng, R=80, G=7, M=3, NS=4, NF=8, W=2, caps=True)
+    q, g = inp["requests"], inp["gpus"]
+    q["model"][::7] = 5
+    q["model"][1::11] = -2
+    q["wave"][2::9] = 2
+    q["prompt_tokens"][3::8] = -1
+    q["pred_out_tokens"][4::10] = -3
+    g["batch"][0, 1] = -1
+    g["batch"][1, 2] = 77
+    g["cap_pf"][3] = 9
+    g["cap_dc"][4] = -1
+    parity_place(inp, label="bad elements")
+
+
+def test_all_infeasible_and_empty_and_unhosted():
+    inp = W.make_placement(2, n_requests=500)
+    inp["requests"]["slo_tbt_ms"][:] = 0.5
+    got, _ = parity_place(inp, label="all infeasible")
+    assert not got[1].any()
+    inp = W.make_placement(2, n_requests=300)
+    inp["gpus"]["resident"][:] = 1                      # only model 0 is hosted anywhere
+    got, _ = parity_place(inp, label="unhosted models")
+    assert np.all(got[1][inp["requests"]["model"] != 0] == 0)
+    inp = W.make_placement(2, n_requests=0)
+    say("[gpu] placement: zero requests")
+    got = run_place(inp)
+    assert all(len(x) == 0 for x in got)
+
+
+def test_unaligned_tables_and_side_stream():
+    F = festina()
+    inp = W.make_placement(2, n_requests=777)
+    dp = F.DevicePlacement(inp, "cuda")
+    for name in ("pf", "dc"):
+        t = dp.t[name].reshape(-1)
+        buf = torch.empty(t.numel() + 1, dtype=torch.float32, device="cuda")
+        buf[1:].copy_(t)
+        dp.t[name + "_unaligned"] = buf
+        setattr(dp.lut, name, buf[1:].data_ptr())
+    s = torch.cuda.Stream()
+    say("[gpu] placement: unaligned tables on a side stream")
+    dp.run(s)
+    s.synchronize()
+    got = dp.results()
+    sel = np.arange(777)
+    rep = check_placements(inp, sel, oracle.score_placements(inp, sel), got)
+    assert rep.ok, str(rep)
+
+
+def test_deterministic_reruns():
+    inp = W.make_placement(4)
+    say("[gpu] placement cfg4 full, twice")
+    a = run_place(inp)
+    b = run_place(inp)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    inp = W.make_fleet()
+    say("[gpu] migration cfg5 full, twice")
+    a = run_mig(inp)
+    b = run_mig(inp)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("G,NF", [(2, 1), (3, 5), (7, 16), (64, 31), (65, 32), (300, 16)])
+def test_migration_shapes(G, NF):
+    rng = np.random.default_rng(G * 7 + NF)
+    parity_mig(W.make_tiny_fleet(rng, G=G, M=3, NS=4, NF=NF), label=f"tiny G={G} NF={NF}")
+
+
+def test_migration_ties_and_bad_elements():
+    rng = np.random.default_rng(31)
+    inp = W.make_tiny_fleet(rng, G=40, M=2, NS=3, NF=6, loose=True, huge_budget=True)
+    inp["fleet"]["k_dyn_w"][:] = 400.0                  # every destination ties exactly:
+    inp["fleet"]["util"][:] = rng.integers(0, 40, 40) / 64.0   # dyadic u, f0 = 0.5: exact arithmetic
+    got, _ = parity_mig(inp, label="all destinations tie")
+    assert np.all(got[0][1:] == 0) and got[0][0] == 1
+    inp = W.make_tiny_fleet(rng, G=50, M=3, NS=4, NF=8)
+    fl = inp["fleet"]
+    fl["n_inst"][::9] = 0
+    fl["n_inst"][1::13] = 6
+    fl["inst_model"][2::7, 0] = 9
+    fl["inst_sm"][3::11, 0] = 4
+    fl["inst_batch"][4::5, 0] = -2
+    fl["inst_prompt_tokens"][5::6, 0] = -4
+    fl["hbm_mib"][6] = -2_000_000_000
+    parity_mig(inp, label="bad elements")
