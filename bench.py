@@ -1,0 +1,301 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched energy-aware placement and migration search on one GPU.
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+  * placement search of the phase-aware bursty workload: 262,144 requests in 64
+    arrival waves over 1,024 GPUs, 32 models, 8 SM x 16 frequency levels, capped
+    prefill/decode SM splits (every (hosting GPU, SM level, frequency level)
+    candidate of every request is scored, masked by SLO and reduced to the
+    least-energy feasible one);
+  * consolidation scoring of a 2,048-GPU fleet: all 4,192,256 ordered
+    source -> destination pairs and the per-source best destination.
+Inputs are resident in device memory before the timed region.  The metric is
+candidate evaluations per second (placement candidates plus migration pairs).
+
+Also reported: the roofline position of the dominant kernel (placement scoring,
+timed alone with HIP events recorded around it inside the library), and the CPU
+oracle timed on a bounded sample of the same workload on this host.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+       python bench.py --per-config     (one JSON line per configuration, then the step line)
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+# MI355X: 256 CUs x 4 SIMD x 16 lanes, 2.4 GHz peak engine clock -> 64 VALU lane-ops/clock/CU
+N_CU = 256
+LANES_PER_CU_CLOCK = 64
+SCLK_HZ = 2.4e9
+VALU_PEAK = N_CU * LANES_PER_CU_CLOCK * SCLK_HZ            # 39.32e12 lane-ops/s
+HBM_PEAK = 8.0e12                                           # B/s
+
+# Work a candidate needs that no other request or GPU can share:
+# energy (one multiply, one fused multiply-add), the TBT-SLO compare, and the running
+# argmin (compare + two selects).
+OPS_PER_CANDIDATE = 6
+# Migration pair: two budget compares, level-mask AND and test, self test, lowest set bit,
+# u_s + u_d, two multiplies, subtract, FMA, compare with the best, three selects.
+OPS_PER_PAIR = 15
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_score_config4_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "festina.hip")
+
+
+# ------------------------------------------------------------------ HIP events (ctypes)
+class Hip:
+    def __init__(self):
+        self.L = C.CDLL("libamdhip64.so")
+        self.L.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.L.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.L.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.L.hipEventDestroy.argtypes = [C.c_void_p]
+
+    def event(self):
+        e = C.c_void_p()
+        rc = self.L.hipEventCreate(C.byref(e))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed ({rc})")
+        return e.value
+
+    def elapsed_ms(self, a, b):
+        self.L.hipEventSynchronize(C.c_void_p(b))
+        ms = C.c_float()
+        rc = self.L.hipEventElapsedTime(C.byref(ms), C.c_void_p(a), C.c_void_p(b))
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(ms.value)
+
+    def destroy(self, e):
+        self.L.hipEventDestroy(C.c_void_p(e))
+
+
+# ------------------------------------------------------------------ work counts
+def placement_candidates(inp, sel=None):
+    """sum over (valid) requests of |hosts(model)| * NS * NF."""
+    lut, gp, rq = inp["lut"], inp["gpus"], inp["requests"]
+    M = lut["n_models"]
+    res = np.asarray(gp["resident"], np.uint32)
+    hosts = np.array([int(((res[:, m // 32] >> np.uint32(m % 32)) & 1).sum()) for m in range(M)])
+    model = rq["model"] if sel is None else rq["model"][sel]
+    ok = (model >= 0) & (model < M)
+    return int(hosts[model[ok]].sum()) * lut["n_sm"] * lut["n_freq"]
+
+
+def placement_bytes(inp):
+    """Algorithmic HBM bytes of one placement call: request fields in, results out,
+    GPU state and each model's tables read once."""
+    lut, gp, rq = inp["lut"], inp["gpus"], inp["requests"]
+    R, G, W, M = rq["n_requests"], gp["n_gpus"], gp["n_waves"], lut["n_models"]
+    req_in = R * (4 * 6)                       # model, wave, prompt, pred, two SLOs
+    out = R * (4 + 1 + 4)
+    state = W * G * 4 + G * (4 + 4 * ((M + 31) // 32) + (2 if gp.get("cap_pf") is not None else 0))
+    tables = 2 * lut["pf"].nbytes
+    return req_in + out + state + tables
+
+
+def src_hash():
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def load_traffic():
+    """HBM bytes per launch of the scoring kernel from the committed counter runs,
+    or None when the kernel source changed since they were taken."""
+    try:
+        d = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_src_sha256_16") != src_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+# ------------------------------------------------------------------ CPU baseline (oracle)
+def cpu_baseline(place_inp, fleet_inp, gpu_place, gpu_mig, stride=4):
+    import oracle
+    R = place_inp["requests"]["n_requests"]
+    sel = np.arange(0, R, stride, dtype=np.int32)
+    t0 = time.perf_counter()
+    oc, of, oe = oracle.score_placements(place_inp, sel)
+    t1 = time.perf_counter()
+    ob, osv, ok = oracle.score_migrations(fleet_inp)
+    t2 = time.perf_counter()
+    cand = placement_candidates(place_inp, sel)
+    G = fleet_inp["fleet"]["n_gpus"]
+    pairs = G * (G - 1)
+    gc, gf, _ = gpu_place
+    gb = gpu_mig[0]
+    return {
+        "value": (cand + pairs) / ((t1 - t0) + (t2 - t1)),
+        "unit": "candidate evaluations/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"every {stride}th request of the placement workload ({len(sel)} requests, {cand} "
+                   f"candidates, {t1 - t0:.2f} s) + all {pairs} migration pairs ({t2 - t1:.2f} s); "
+                   f"single-threaded C, float64, gcc -O2"),
+        "agreement": {"placement_flags_equal": float(np.mean(of == gf[sel])),
+                      "placement_choice_equal": float(np.mean(oc == gc[sel])),
+                      "migration_dst_equal": float(np.mean(ob == gb))},
+    }
+
+
+# ------------------------------------------------------------------ main
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--per-config", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} (WORLD_SIZE {world}) is not "
+              f"supported: the search shards without communication (see DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_30391_amd import festina as F
+    from paper_2606_30391_amd import workloads as W
+
+    F.lib()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    hip = Hip()
+
+    if args.per_config:
+        per_config(F, W, hip, torch)
+
+    place = W.make_placement(4)
+    fleet = W.make_fleet()
+    dp = F.DevicePlacement(place, "cuda")
+    dm = F.DeviceMigration(fleet, "cuda")
+    torch.cuda.synchronize()
+
+    n_cand = placement_candidates(place)
+    G = fleet["fleet"]["n_gpus"]
+    n_pairs = G * (G - 1)
+
+    for _ in range(args.warmup):
+        dp.run()
+        dm.run()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [[hip.event() for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        F.festina_set_timing_events(*evs[i])
+        dp.run()
+        dm.run()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    F.festina_set_timing_events()
+    score_ms = float(np.mean([hip.elapsed_ms(e[0], e[1]) for e in evs]))
+    pairs_ms = float(np.mean([hip.elapsed_ms(e[2], e[3]) for e in evs]))
+    for e in evs:
+        for x in e:
+            hip.destroy(x)
+
+    step_s = (t1 - t0) / K
+    value = (n_cand + n_pairs) / step_s
+    achieved = n_cand * OPS_PER_CANDIDATE / (score_ms * 1e-3)
+    gpu_place = dp.results()
+    gpu_mig = dm.results()
+
+    line = {
+        "metric": "candidate evaluations/sec + % of HBM/VALU roofline, 1 MI355X",
+        "value": value,
+        "unit": "candidate evaluations/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": ("phase-aware bursty placement (262144 requests in 64 waves, 1024 GPUs, 32 models, "
+                         "8 SM x 16 freq levels, capped prefill/decode SM splits) + consolidation scoring "
+                         "(2048 GPUs, 4192256 ordered pairs)"),
+            "placement_candidates": n_cand,
+            "migration_pairs": n_pairs,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "kernel": "k_score (placement scoring + fused argmin)",
+            "bound": "alu",
+            "achieved": achieved / 1e12,
+            "peak": VALU_PEAK / 1e12,
+            "unit": "T VALU lane-ops/s",
+            "frac": achieved / VALU_PEAK,
+            "traffic": load_traffic(),
+            "ops_per_candidate": OPS_PER_CANDIDATE,
+            "kernel_ms": score_ms,
+            "hbm_frac_algorithmic": placement_bytes(place) / (score_ms * 1e-3) / HBM_PEAK,
+        },
+        "kernels_ms": {"k_score": score_ms, "k_migrate": pairs_ms,
+                       "migration_pairs_per_s_kernel": n_pairs / (pairs_ms * 1e-3)},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(place, fleet, gpu_place, gpu_mig)
+    print(json.dumps(line), flush=True)
+
+
+def per_config(F, W, hip, torch):
+    """One JSON line per configuration: call time, kernel time, rates, VALU fraction."""
+    for cfg in (1, 2, 3, 4, 5):
+        if cfg < 5:
+            inp = W.make_placement(cfg)
+            dev = F.DevicePlacement(inp, "cuda")
+            work = placement_candidates(inp)
+            ops = work * OPS_PER_CANDIDATE
+            idx = (0, 1)
+        else:
+            inp = W.make_fleet()
+            dev = F.DeviceMigration(inp, "cuda")
+            G = inp["fleet"]["n_gpus"]
+            work = G * (G - 1)
+            ops = work * OPS_PER_PAIR
+            idx = (2, 3)
+        reps = 10 if cfg == 4 else 50
+        for _ in range(5):
+            dev.run()
+        torch.cuda.synchronize()
+        call_ms, kern_ms = [], []
+        for _ in range(reps):
+            ev = [hip.event() for _ in range(4)]
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            F.festina_set_timing_events(*ev)
+            a.record()
+            dev.run()
+            b.record()
+            torch.cuda.synchronize()
+            call_ms.append(a.elapsed_time(b))
+            kern_ms.append(hip.elapsed_ms(ev[idx[0]], ev[idx[1]]))
+            for e in ev:
+                hip.destroy(e)
+        F.festina_set_timing_events()
+        cm, km = float(np.median(call_ms)), float(np.median(kern_ms))
+        print(json.dumps({"config": cfg, "work": work, "call_ms": cm, "kernel_ms": km,
+                          "evals_per_s_call": work / (cm * 1e-3), "evals_per_s_kernel": work / (km * 1e-3),
+                          "valu_frac_kernel": ops / (km * 1e-3) / VALU_PEAK}), flush=True)
+
+
+if __name__ == "__main__":
+    main()

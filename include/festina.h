@@ -175,6 +175,16 @@ festina_status festina_score_migrations(const festina_lut *lut, const festina_fl
                                         festina_migrations *out, void *workspace,
                                         size_t workspace_bytes, void *stream);
 
+/* Measurement hook, not part of the search.  While set, festina_score_placements
+ * records `score_begin` on its stream immediately before its scoring kernel and
+ * `score_end` immediately after it, and festina_score_migrations does the same with
+ * `pairs_begin` / `pairs_end` around its pair-scoring kernel, so that a caller can time
+ * those kernels alone with hipEventElapsedTime.  Each argument is a hipEvent_t passed
+ * as void*, created by the caller on the device of the following calls; NULL leaves
+ * that point unrecorded.  The setting belongs to the calling host thread and stays in
+ * force until changed. */
+void festina_set_timing_events(void *score_begin, void *score_end, void *pairs_begin, void *pairs_end);
+
 /* Static, NUL-terminated description of a status code. */
 const char *festina_status_string(festina_status status);
 

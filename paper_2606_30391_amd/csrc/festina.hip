@@ -656,6 +656,13 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   return true;
 }
 
+// events recorded around the scoring kernels (measurement hook; per host thread)
+thread_local hipEvent_t t_events[4] = {nullptr, nullptr, nullptr, nullptr};
+
+hipError_t mark(int which, hipStream_t st) {
+  return t_events[which] ? hipEventRecord(t_events[which], st) : hipSuccess;
+}
+
 template <int CPL>
 hipError_t launch_score(const PlaceArgs &a, int blocks, int wpb, size_t lds, hipStream_t st) {
   k_score<CPL><<<blocks, wpb * kWave, lds, st>>>(a);
@@ -668,6 +675,13 @@ hipError_t launch_score(const PlaceArgs &a, int blocks, int wpb, size_t lds, hip
 extern "C" {
 
 int32_t festina_abi_version(void) { return FESTINA_ABI_VERSION; }
+
+void festina_set_timing_events(void *score_begin, void *score_end, void *pairs_begin, void *pairs_end) {
+  t_events[0] = static_cast<hipEvent_t>(score_begin);
+  t_events[1] = static_cast<hipEvent_t>(score_end);
+  t_events[2] = static_cast<hipEvent_t>(pairs_begin);
+  t_events[3] = static_cast<hipEvent_t>(pairs_end);
+}
 
 const char *festina_status_string(festina_status s) {
   switch (s) {
@@ -762,13 +776,15 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int cpl = C <= 64 ? 1 : (C <= 128 ? 2 : 4);
   const size_t lds = sizeof(float) * score_lds_floats((int)C, cpl, lay.waves_per_block);
-  hipError_t e;
+  hipError_t e = mark(0, st);
+  if (e != hipSuccess) return FESTINA_ERR_DEVICE;
   if (cpl == 1)
     e = launch_score<1>(a, lay.max_tiles, lay.waves_per_block, lds, st);
   else if (cpl == 2)
     e = launch_score<2>(a, lay.max_tiles, lay.waves_per_block, lds, st);
   else
     e = launch_score<4>(a, lay.max_tiles, lay.waves_per_block, lds, st);
+  if (e == hipSuccess) e = mark(1, st);
   return e == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
 }
 
@@ -832,8 +848,10 @@ festina_status festina_score_migrations(const festina_lut *L, const festina_flee
   k_fleet<<<(a.G + 255) / 256, 256, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int per_block = 4 * kSrcPerWave;
+  if (mark(2, st) != hipSuccess) return FESTINA_ERR_DEVICE;
   k_migrate<<<(a.G + per_block - 1) / per_block, 256, 0, st>>>(a);
-  return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
+  if (hipGetLastError() != hipSuccess || mark(3, st) != hipSuccess) return FESTINA_ERR_DEVICE;
+  return FESTINA_OK;
 }
 
 }  // extern "C"

@@ -63,7 +63,8 @@ class festina_migrations(C.Structure):
 
 
 EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_workspace_bytes",
-            "festina_score_placements", "festina_migrations_workspace_bytes", "festina_score_migrations")
+            "festina_score_placements", "festina_migrations_workspace_bytes", "festina_score_migrations",
+            "festina_set_timing_events")
 
 _lib = None
 
@@ -89,8 +90,16 @@ def lib():
         L.festina_score_migrations.argtypes = [P(festina_lut), P(festina_fleet), P(festina_migrations),
                                                C.c_void_p, C.c_size_t, C.c_void_p]
         L.festina_score_migrations.restype = C.c_int
+        L.festina_set_timing_events.argtypes = [C.c_void_p] * 4
+        L.festina_set_timing_events.restype = None
         _lib = L
     return _lib
+
+
+def festina_set_timing_events(score_begin=None, score_end=None, pairs_begin=None, pairs_end=None) -> None:
+    """Measurement hook: raw hipEvent_t handles (ints) recorded around the scoring kernels."""
+    lib().festina_set_timing_events(*(C.c_void_p(e) if e else None
+                                      for e in (score_begin, score_end, pairs_begin, pairs_end)))
 
 
 def festina_abi_version() -> int:
