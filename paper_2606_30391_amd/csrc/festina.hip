@@ -39,6 +39,9 @@ constexpr int kWave = 64;
 constexpr int kQ = 4;            // requests scored together by one wavefront
 constexpr int kPrepBlock = 256;
 constexpr float kInf = __builtin_huge_valf();
+// Value of a masked (SLO-missing) latency: a quiet NaN stays NaN through every multiply and
+// FMA whatever the sign of the power terms, and NaN < x is false, so it never wins.
+constexpr float kMask = __builtin_nanf("");
 
 struct HostRec {                 // per (wave, GPU), 16 bytes
   int32_t row_off;               // (b - 1) * cells, or -1 when the GPU has no candidates
@@ -184,7 +187,8 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
   const bool ok = B >= 0 && cp >= 0 && cp < a.NS && cd >= 0 && cd < a.NS;
   const int bb = B + 1 > kRows ? kRows : B + 1;
   rec.row_off = ok ? (bb - 1) * a.C : -1;
-  rec.kappa = a.kdyn[g] * ((float)bb * 0.03125f);   // u = b / 32, exact
+  // u = b / 32 is exact; a GPU without candidates gets NaN so that every energy on it is NaN
+  rec.kappa = ok ? a.kdyn[g] * ((float)bb * 0.03125f) : kMask;
   rec.caps = ok ? (cp | (cd << 8)) : 0;
   rec.pad = 0;
   a.recs[i] = rec;
@@ -264,15 +268,12 @@ __host__ __device__ constexpr size_t score_lds_floats(int C, int CPL, int waves)
 }
 
 template <int CPL>
-__global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
-  extern __shared__ __align__(16) float lds[];
+__device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
   const int C = a.C, NF = a.NF;
   float *dcs = lds;                                   // [32 * C + pad] decode table of the tile's model
   float *pds = lds + kRows * C + kWave * CPL;         // [C] s_j * f_k^3
   float *rows = pds + C;                              // [waves][Q][C] prompt rows (capped GPUs)
 
-  const int t = blockIdx.x;
-  if (t >= *ro(a.n_tiles)) return;
   const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
   const int bucket = tp[2 * t];
   const bool noprompt = bucket & 1;
@@ -389,7 +390,7 @@ __global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
 #pragma unroll
         for (int u = 0; u < CPL; ++u) {
           const float v = (rq[q] >= 0 && live[u]) ? pr[lane * CPL + u] : kInf;
-          tt[q][u] = v < st[q] ? v : kInf;
+          tt[q][u] = v < st[q] ? v : kMask;
         }
       }
       for (int i = 0; i < hcnt; ++i) {
@@ -419,7 +420,7 @@ __global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
         const float *pr = a.pf + ((size_t)m * kRows + prw[q]) * C;
         for (int c = lane; c < C; c += kWave) {
           const float v = rq[q] >= 0 ? pr[c] : kInf;
-          myrows[q * C + c] = v < st[q] ? v : kInf;
+          myrows[q * C + c] = v < st[q] ? v : kMask;
         }
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -479,6 +480,274 @@ __global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
   }
 }
 
+template <int CPL>
+__global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
+  extern __shared__ __align__(16) float lds[];
+  if ((int)blockIdx.x >= *ro(a.n_tiles)) return;
+  score_tile_generic<CPL>(a, blockIdx.x, lds);
+}
+
+// ------------------------------------------------------------------ 8 x 16 scoring kernel
+// Tables of 8 SM levels x 16 frequency levels (128 cells).  Lane l owns cells 2l and 2l+1,
+// which share SM level j = l / 8, so a capped cell offset is one min on byte offsets,
+// min(j * 64, cap * 64) + k * 4, and the LDS offsets below are compile-time immediates.
+//
+// A workgroup takes a tile of WPB * kQF requests of one (wave, model) bucket; each
+// wavefront scores its kQF requests together against every hosting GPU.
+//   pass 1: per (request, cell) the minimum energy over the GPUs: one multiply, one FMA
+//           and one min per candidate; the GPU terms (Pp, Pd * TBT, the TBT-SLO mask) are
+//           shared by the kQF requests, the TTFT-SLO mask is applied once per request;
+//   pass 2: E* = the wavefront minimum; among the cells whose minimum equals E*, in
+//           ascending cell order, the lowest GPU position whose energy -- recomputed with
+//           the same operations, hence bit-identical -- equals E*.  That is the
+//           (energy, index) lexicographic minimum.
+// Masked (SLO-missing) latencies are NaN, which min ignores and == never matches.
+constexpr int kQF = 8;
+constexpr int kC = 128;
+constexpr int kHcap = 256;                       // host records staged in LDS per chunk
+constexpr int kWblkB = (1 + kQF) * kC * 4;       // per wave: s*f^3 row + kQF prompt rows
+
+__host__ __device__ constexpr int fast_rec_off(int wpb) { return wpb * kWblkB; }
+__host__ __device__ constexpr int fast_dcs_off(int wpb) { return wpb * kWblkB + kHcap * 16; }
+__host__ __device__ constexpr size_t fast_lds_bytes(int wpb) {
+  return (size_t)fast_dcs_off(wpb) + (size_t)kRows * kC * 4;
+}
+
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v2f lds2(const char *base, uint32_t off) {
+  return *reinterpret_cast<const v2f *>(base + off);
+}
+__device__ __forceinline__ float lds1(const char *base, uint32_t off) {
+  return *reinterpret_cast<const float *>(base + off);
+}
+
+// v_min_f32 as one instruction.  Its operands are results of arithmetic or +inf, and a
+// quiet-NaN operand yields the other operand, which is the masking rule; fminf would make
+// the compiler add a canonicalising v_max_f32 per operand in IEEE mode.
+__device__ __forceinline__ float vmin(float x, float y) {
+  float r;
+  asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(x), "v"(y));
+  return r;
+}
+
+// Energy of one candidate.  Pass 1 and pass 2 both evaluate exactly this expression.
+__device__ __forceinline__ float cell_energy(float kap, float pdp, float pdd, float tbt, float tt,
+                                            float p0, float lo, float slo_tbt) {
+  const float Pp = fmaf(kap, pdp, p0);
+  const float Pd = fmaf(kap, pdd, p0);
+  const float Ym = tbt < slo_tbt ? Pd * tbt : kMask;
+  return fmaf(lo, Ym, Pp * tt);
+}
+
+// Pass 1 over host records [0, n) of the LDS record table.  SAME: the kQF requests share
+// their TBT SLO, so the TBT mask is applied once per (GPU, cell).
+template <bool SAME>
+__device__ __forceinline__ void fast_pass1(const char *L, uint32_t recB, uint32_t wblkB, int n,
+                                           uint32_t j64, uint32_t k04, float p0, const float (&lo)[kQF],
+                                           const float (&sb)[kQF], float (&mn)[kQF][2]) {
+  for (int i = 0; i < n; ++i) {
+    const v4u r = *reinterpret_cast<const v4u *>(L + recB + i * 16);
+    const uint32_t rowB = r.x;
+    const float kap = __uint_as_float(r.y);
+    const uint32_t aP = wblkB + min(j64, r.z) + k04;
+    const uint32_t mD = min(j64, r.w) + k04;
+    const v2f pdp = lds2(L, aP);
+    const v2f pdd = lds2(L, wblkB + mD);
+    const v2f tbt = lds2(L, rowB + mD);
+    float Pp[2], Y[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      Pp[c] = fmaf(kap, pdp[c], p0);
+      const float Pd = fmaf(kap, pdd[c], p0);
+      Y[c] = SAME ? (tbt[c] < sb[0] ? Pd * tbt[c] : kMask) : Pd * tbt[c];
+    }
+#pragma unroll
+    for (int q = 0; q < kQF; ++q) {
+      const v2f tt = lds2(L, aP + (1 + q) * kC * 4);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const float Ym = SAME ? Y[c] : (tbt[c] < sb[q] ? Y[c] : kMask);
+        mn[q][c] = vmin(mn[q][c], fmaf(lo[q], Ym, Pp[c] * tt[c]));
+      }
+    }
+  }
+}
+
+template <int WPB>
+__global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
+  extern __shared__ __align__(16) float lds[];
+  char *L = reinterpret_cast<char *>(lds);
+  constexpr uint32_t recB = fast_rec_off(WPB);
+  constexpr uint32_t dcsB = fast_dcs_off(WPB);
+  const int t = blockIdx.x;
+  if (t >= *ro(a.n_tiles)) return;
+  const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
+  const int bucket = tp[2 * t];
+  if (bucket & 1) {                       // prompt-less requests: TTFT from the batch row
+    score_tile_generic<2>(a, t, lds);
+    return;
+  }
+  const int wm = bucket >> 1;
+  const int w = wm / a.M, m = wm - (wm / a.M) * a.M;
+  const int beg = tp[2 * t + 1];
+  const int end = min(beg + a.tile, ro(a.bstart)[bucket + 1]);
+
+  {  // the model's decode table
+    const float *src = a.dc + (size_t)m * kRows * kC;
+    if ((((uintptr_t)src) & 15) == 0) {
+      const float4 *s4 = reinterpret_cast<const float4 *>(src);
+      float4 *d4 = reinterpret_cast<float4 *>(L + dcsB);
+      for (int i = threadIdx.x; i < kRows * kC / 4; i += WPB * 64) d4[i] = s4[i];
+    } else {
+      float *d1 = reinterpret_cast<float *>(L + dcsB);
+      for (int i = threadIdx.x; i < kRows * kC; i += WPB * 64) d1[i] = src[i];
+    }
+  }
+  const int wv = uniform(threadIdx.x >> 6);
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t wblkB = (uint32_t)wv * kWblkB;
+  const int j = lane >> 3;
+  const uint32_t j64 = (uint32_t)j * 64u;          // byte offset of SM level j in a row
+  const uint32_t k04 = (uint32_t)(lane & 7) * 8u;  // byte offset of frequency level 2 * (lane % 8)
+  {
+    v2f pd;
+    pd.x = a.sm_level[j] * cube(a.freq_level[2 * (lane & 7)]);
+    pd.y = a.sm_level[j] * cube(a.freq_level[2 * (lane & 7) + 1]);
+    *reinterpret_cast<v2f *>(L + wblkB + j64 + k04) = pd;
+  }
+
+  // this wavefront's requests, and their prompt rows (NaN where TTFT misses the SLO)
+  const int q0 = beg + wv * kQF;
+  const int nq = max(0, min(kQF, end - q0));
+  int rq[kQF];
+  float lo[kQF], sb[kQF];
+  bool same = true;
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) {
+    rq[q] = q < nq ? ro(a.perm)[q0 + q] : -1;
+    float st = -kInf;
+    int prw = 0;
+    lo[q] = 0.f;
+    sb[q] = -kInf;
+    if (rq[q] >= 0) {
+      lo[q] = ro(a.lout)[rq[q]];
+      st = ro(a.slo_ttft)[rq[q]];
+      sb[q] = ro(a.slo_tbt)[rq[q]];
+      prw = ro(a.row)[rq[q]];
+    }
+    if (q > 0 && rq[q] < 0) sb[q] = sb[0];
+    same = same && __float_as_int(sb[q]) == __float_as_int(sb[0]);
+    const float *pr = a.pf + ((size_t)m * kRows + prw) * kC + 2 * lane;
+    v2f v;
+    v.x = rq[q] >= 0 ? pr[0] : kMask;
+    v.y = rq[q] >= 0 ? pr[1] : kMask;
+    v.x = v.x < st ? v.x : kMask;
+    v.y = v.y < st ? v.y : kMask;
+    *reinterpret_cast<v2f *>(L + wblkB + (1 + q) * kC * 4 + j64 + k04) = v;
+  }
+
+  float mn[kQF][2];
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) mn[q][0] = mn[q][1] = kInf;
+
+  const int hcnt = ro(a.host_cnt)[m];
+  const int32_t *hl = a.host_list + (size_t)m * a.G;
+  const HostRec *rw = a.recs + (size_t)w * a.G;
+  const float p0 = a.p0;
+  for (int c0 = 0; c0 < hcnt; c0 += kHcap) {
+    const int n = min(kHcap, hcnt - c0);
+    __syncthreads();                      // previous records no longer in use; rows written
+    for (int i = threadIdx.x; i < n; i += WPB * 64) {
+      const HostRec r = rw[hl[c0 + i]];
+      v4u f;
+      f.x = dcsB + (uint32_t)max(r.row_off, 0) * 4u;
+      f.y = __float_as_uint(r.kappa);
+      f.z = (uint32_t)(r.caps & 0xff) * 64u;
+      f.w = (uint32_t)((r.caps >> 8) & 0xff) * 64u;
+      *reinterpret_cast<v4u *>(L + recB + i * 16) = f;
+    }
+    __syncthreads();
+    if (nq > 0) {
+      if (same)
+        fast_pass1<true>(L, recB, wblkB, n, j64, k04, p0, lo, sb, mn);
+      else
+        fast_pass1<false>(L, recB, wblkB, n, j64, k04, p0, lo, sb, mn);
+    }
+  }
+
+  // pass 2: the winning energy, then the lowest index that reaches it
+  const bool recs_in_lds = hcnt <= kHcap;
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) {
+    if (q >= nq) break;
+    float e = vmin(mn[q][0], mn[q][1]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) e = vmin(e, __shfl_xor(e, off, kWave));
+    const float est = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(e)));
+    int best = INT_MAX;
+    if (est < kInf) {
+      unsigned long long t0 = __ballot(mn[q][0] == est);
+      unsigned long long t1 = __ballot(mn[q][1] == est);
+      int ilim = hcnt;                    // positions >= ilim cannot improve the index
+      while ((t0 | t1) != 0ull) {
+        // next tied cell in ascending order: cell = 2 * lane + c
+        const int l0 = t0 ? __builtin_ctzll(t0) : 64;
+        const int l1 = t1 ? __builtin_ctzll(t1) : 64;
+        int cell;
+        if (l0 <= l1) {
+          cell = 2 * l0;
+          t0 &= t0 - 1ull;
+        } else {
+          cell = 2 * l1 + 1;
+          t1 &= t1 - 1ull;
+        }
+        const uint32_t cj64 = (uint32_t)(cell >> 4) * 64u, ck4 = (uint32_t)(cell & 15) * 4u;
+        for (int b0 = 0; b0 < ilim; b0 += kWave) {
+          const int i = b0 + lane;
+          bool hit = false;
+          if (i < ilim) {
+            uint32_t rowB, cpB, cdB;
+            float kap;
+            if (recs_in_lds) {
+              const v4u r = *reinterpret_cast<const v4u *>(L + recB + i * 16);
+              rowB = r.x;
+              kap = __uint_as_float(r.y);
+              cpB = r.z;
+              cdB = r.w;
+            } else {
+              const HostRec r = rw[hl[i]];
+              rowB = dcsB + (uint32_t)max(r.row_off, 0) * 4u;
+              kap = r.kappa;
+              cpB = (uint32_t)(r.caps & 0xff) * 64u;
+              cdB = (uint32_t)((r.caps >> 8) & 0xff) * 64u;
+            }
+            const uint32_t aP = wblkB + min(cj64, cpB) + ck4;
+            const uint32_t mD = min(cj64, cdB) + ck4;
+            const float E = cell_energy(kap, lds1(L, aP), lds1(L, wblkB + mD), lds1(L, rowB + mD),
+                                        lds1(L, aP + (1 + q) * kC * 4), p0, lo[q], same ? sb[0] : sb[q]);
+            hit = E == est;
+          }
+          const unsigned long long h = __ballot(hit);
+          if (h) {
+            const int i_hit = b0 + __builtin_ctzll(h);
+            best = min(best, ro(a.host_list + (size_t)m * a.G)[i_hit] * kC + cell);
+            ilim = i_hit;                 // later cells need a strictly lower position
+            break;
+          }
+        }
+      }
+    }
+    if (lane == 0) {
+      const bool found = best != INT_MAX;
+      a.choice[rq[q]] = found ? best : -1;
+      a.feasible[rq[q]] = found ? 1 : 0;
+      a.energy[rq[q]] = found ? est : kInf;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ migration kernels
 struct MigArgs {
   int32_t M, NS, NF, C;
@@ -497,14 +766,18 @@ struct MigArgs {
   float *base;                   // [G] f[kd0]^3 * u_d
 };
 
-__global__ void k_fleet(MigArgs a) {
-  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+// One wavefront per GPU: lane k tests frequency level k (NF <= 32) for each instance, a
+// ballot turns the tests into that instance's level mask, and the GPU's mask is the AND.
+__global__ void __launch_bounds__(256) k_fleet(MigArgs a) {
+  const int g = blockIdx.x * 4 + uniform(threadIdx.x >> 6);
+  const int lane = threadIdx.x & (kWave - 1);
   if (g >= a.G) return;
-  const int n = a.n_inst[g];
+  const int n = ro(a.n_inst)[g];
   uint32_t fm = (n >= 1 && n <= a.K) ? (a.NF >= 32 ? 0xffffffffu : ((1u << a.NF) - 1u)) : 0u;
   for (int i = 0; i < n && i < a.K && fm; ++i) {
     const size_t at = (size_t)g * a.K + i;
-    const int m = a.inst_model[at], j = a.inst_sm[at], B = a.inst_batch[at], pt = a.inst_prompt[at];
+    const int m = ro(a.inst_model)[at], j = ro(a.inst_sm)[at], B = ro(a.inst_batch)[at];
+    const int pt = ro(a.inst_prompt)[at];
     if (m < 0 || m >= a.M || j < 0 || j >= a.NS || B < 0 || pt < 0) {
       fm = 0;
       break;
@@ -513,14 +786,14 @@ __global__ void k_fleet(MigArgs a) {
     const int prow = pt == 0 ? bb - 1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
     const float *pr = a.pf + (((size_t)m * kRows + prow) * a.NS + j) * a.NF;
     const float *dr = a.dc + (((size_t)m * kRows + (bb - 1)) * a.NS + j) * a.NF;
-    const float st = a.inst_slo_ttft[at], sb = a.inst_slo_tbt[at];
-    uint32_t mk = 0;
-    for (int k = 0; k < a.NF; ++k)
-      if (pr[k] < st && dr[k] < sb) mk |= 1u << k;
-    fm &= mk;
+    const float st = ro(a.inst_slo_ttft)[at], sb = ro(a.inst_slo_tbt)[at];
+    const bool pass = lane < a.NF && pr[lane < a.NF ? lane : 0] < st && dr[lane < a.NF ? lane : 0] < sb;
+    fm &= (uint32_t)__ballot(pass);
   }
-  a.fm[g] = fm;
-  a.base[g] = fm ? cube(a.freq_level[__builtin_ctz(fm)]) * a.util[g] : 0.f;
+  if (lane == 0) {
+    a.fm[g] = fm;
+    a.base[g] = fm ? cube(a.freq_level[__builtin_ctz(fm)]) * a.util[g] : 0.f;
+  }
 }
 
 constexpr int kSrcPerWave = 2;
@@ -605,6 +878,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct PlaceLayout {
   size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, perm, key, row, lout, total;
   int32_t NB, tile, max_tiles, waves_per_block;
+  bool fast;                     // 8 SM x 16 frequency levels: the specialised kernel
 };
 
 bool place_shapes_ok(const festina_lut *L, const festina_gpus *G, const festina_requests *Q) {
@@ -621,14 +895,25 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   const long long NB = 2 * W * M;
   if (NB > INT_MAX / 2 || Gn * C > INT_MAX || W * Gn > INT_MAX || M * Gn > INT_MAX) return false;
   // tile size: large tiles amortise the table staging, small ones fill the chip
-  int wpb = 4, tile = 2 * 4 * kQ;
-  if (R < 2048LL * tile) {
-    tile = 4 * kQ;
+  const bool fast = L->n_sm == 8 && L->n_freq == 16;
+  int wpb = 4, tile;
+  if (fast) {                    // one group of kQF requests per wavefront
+    tile = 4 * kQF;
     if (R < 1024LL * tile) {
       wpb = 1;
-      tile = kQ;
+      tile = kQF;
+    }
+  } else {
+    tile = 2 * 4 * kQ;
+    if (R < 2048LL * tile) {
+      tile = 4 * kQ;
+      if (R < 1024LL * tile) {
+        wpb = 1;
+        tile = kQ;
+      }
     }
   }
+  o->fast = fast;
   const long long max_tiles = (R + tile - 1) / tile + NB;
   if (max_tiles > INT_MAX) return false;
   size_t off = 0;
@@ -775,15 +1060,26 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   k_scatter<<<nbr, kPrepBlock, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int cpl = C <= 64 ? 1 : (C <= 128 ? 2 : 4);
-  const size_t lds = sizeof(float) * score_lds_floats((int)C, cpl, lay.waves_per_block);
+  const int wpb = lay.waves_per_block;
+  size_t lds = sizeof(float) * score_lds_floats((int)C, cpl, wpb);
+  if (lay.fast) {
+    const size_t f = fast_lds_bytes(wpb);
+    lds = f > lds ? f : lds;
+  }
   hipError_t e = mark(0, st);
   if (e != hipSuccess) return FESTINA_ERR_DEVICE;
-  if (cpl == 1)
-    e = launch_score<1>(a, lay.max_tiles, lay.waves_per_block, lds, st);
+  if (lay.fast) {
+    if (wpb == 4)
+      k_score_c128<4><<<lay.max_tiles, 4 * kWave, lds, st>>>(a);
+    else
+      k_score_c128<1><<<lay.max_tiles, kWave, lds, st>>>(a);
+    e = hipGetLastError();
+  } else if (cpl == 1)
+    e = launch_score<1>(a, lay.max_tiles, wpb, lds, st);
   else if (cpl == 2)
-    e = launch_score<2>(a, lay.max_tiles, lay.waves_per_block, lds, st);
+    e = launch_score<2>(a, lay.max_tiles, wpb, lds, st);
   else
-    e = launch_score<4>(a, lay.max_tiles, lay.waves_per_block, lds, st);
+    e = launch_score<4>(a, lay.max_tiles, wpb, lds, st);
   if (e == hipSuccess) e = mark(1, st);
   return e == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
 }
@@ -845,7 +1141,7 @@ festina_status festina_score_migrations(const festina_lut *L, const festina_flee
   a.fm = reinterpret_cast<uint32_t *>(ws);
   a.base = reinterpret_cast<float *>(ws + align256(sizeof(uint32_t) * F->n_gpus));
   hipStream_t st = static_cast<hipStream_t>(stream);
-  k_fleet<<<(a.G + 255) / 256, 256, 0, st>>>(a);
+  k_fleet<<<(a.G + 3) / 4, 256, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int per_block = 4 * kSrcPerWave;
   if (mark(2, st) != hipSuccess) return FESTINA_ERR_DEVICE;

@@ -225,3 +225,21 @@ def test_migration_ties_and_bad_elements():
     fl["inst_prompt_tokens"][5::6, 0] = -4
     fl["hbm_mib"][6] = -2_000_000_000
     parity_mig(inp, label="bad elements")
+
+
+@pytest.mark.parametrize("NS,NF", [(8, 16), (4, 6)])
+def test_negative_power_terms(NS, NF):
+    """Negative k_g (and a small P0) make some powers negative; SLO-masked cells must
+    still never win, and the least (most negative) feasible energy is chosen."""
+    rng = np.random.default_rng(55 + NS)
+    inp = W.make_tiny_placement(rng, R=64, G=10, M=2, NS=NS, NF=NF, W=1, caps=True)
+    inp["gpus"]["k_dyn_w"][::2] *= np.float32(-1.0)
+    inp["lut"]["p0_w"] = 5.0
+    parity_place(inp, label=f"negative power {NS}x{NF}")
+
+
+def test_fast_kernel_mixed_slo_groups():
+    """8x16 tables with requests of one model carrying different TBT SLOs in a group."""
+    inp = W.make_placement(3, n_requests=4099)
+    inp["requests"]["slo_tbt_ms"][::3] *= np.float32(1.5)
+    parity_place(inp, label="cfg3 mixed TBT SLOs")
