@@ -58,14 +58,17 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "festina.hip")
 class Hip:
     def __init__(self):
         self.L = C.CDLL("libamdhip64.so")
-        self.L.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.L.hipEventCreateWithFlags.argtypes = [C.POINTER(C.c_void_p), C.c_uint]
         self.L.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
         self.L.hipEventSynchronize.argtypes = [C.c_void_p]
         self.L.hipEventDestroy.argtypes = [C.c_void_p]
 
+    # timing-only events: no system-scope fence (cache writeback/invalidate) on record
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
     def event(self):
         e = C.c_void_p()
-        rc = self.L.hipEventCreate(C.byref(e))
+        rc = self.L.hipEventCreateWithFlags(C.byref(e), self.DISABLE_SYSTEM_FENCE)
         if rc != 0:
             raise RuntimeError(f"hipEventCreate failed ({rc})")
         return e.value

@@ -117,35 +117,59 @@ __global__ void k_zero(int32_t *p, int32_t n) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
-// Blocks [0, nbr): requests.  Blocks [nbr, nbr + M): host list of model (block - nbr).
-// Blocks after: GPU records, one thread per (wave, GPU).
+// Request pre-processing of request r: validity, 5% output pad, prompt bucket, bucket key.
+// Returns the key, or -1 (and writes the infeasible result) for an invalid request.
+__device__ __forceinline__ int prep_request(const PlaceArgs &a, int r) {
+  const int m = a.model[r];
+  const int w = a.wave ? a.wave[r] : 0;
+  const int pt = a.prompt[r];
+  const int pr = a.pred[r];
+  const bool ok = m >= 0 && m < a.M && w >= 0 && w < a.W && pt >= 0 && pr >= 0;
+  if (!ok) {
+    a.key[r] = -1;
+    a.choice[r] = -1;
+    a.feasible[r] = 0;
+    a.energy[r] = kInf;
+    return -1;
+  }
+  // prompt bucket: min(ceil(tokens / 256), 32) - 1 (unsigned: no overflow for any
+  // int32 token count); 0 tokens -> the decode batch row is used
+  const int prow = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
+  // 5% safety pad: ceil(1.05 * pred) = (105 * pred + 99) / 100, in 64-bit
+  const long long lo = ((long long)pr * 105 + 99) / 100;
+  a.row[r] = prow;
+  a.lout[r] = (float)lo;
+  const int k = ((w * a.M + m) << 1) | (prow < 0 ? 1 : 0);
+  a.key[r] = k;
+  return k;
+}
+
+constexpr int kReqPerPrepBlock = 4 * kPrepBlock;  // requests per request block of k_prep / k_scatter
+constexpr int kHistMax = 8192;                    // buckets counted in LDS (else global atomics)
+
+// Blocks [0, nbr): kReqPerPrepBlock requests each, counted per bucket in an LDS histogram
+// and flushed with one global atomic per non-empty bucket.  Blocks [nbr, nbr + M): host
+// list of model (block - nbr).  Blocks after: GPU records, one thread per (wave, GPU).
 __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
+  __shared__ int hist[kHistMax];
   const int b = blockIdx.x;
   if (b < nbr) {
-    const int r = b * kPrepBlock + threadIdx.x;
-    if (r >= a.R) return;
-    const int m = a.model[r];
-    const int w = a.wave ? a.wave[r] : 0;
-    const int pt = a.prompt[r];
-    const int pr = a.pred[r];
-    const bool ok = m >= 0 && m < a.M && w >= 0 && w < a.W && pt >= 0 && pr >= 0;
-    if (!ok) {
-      a.key[r] = -1;
-      a.choice[r] = -1;
-      a.feasible[r] = 0;
-      a.energy[r] = kInf;
-      return;
+    const bool local = a.NB <= kHistMax;
+    if (local) {
+      for (int k = threadIdx.x; k < a.NB; k += kPrepBlock) hist[k] = 0;
+      __syncthreads();
     }
-    // prompt bucket: min(ceil(tokens / 256), 32) - 1 (unsigned: no overflow for any
-    // int32 token count); 0 tokens -> the decode batch row is used
-    const int prow = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
-    // 5% safety pad: ceil(1.05 * pred) = (105 * pred + 99) / 100, in 64-bit
-    const long long lo = ((long long)pr * 105 + 99) / 100;
-    a.row[r] = prow;
-    a.lout[r] = (float)lo;
-    const int k = ((w * a.M + m) << 1) | (prow < 0 ? 1 : 0);
-    a.key[r] = k;
-    atomicAdd(&a.cnt[k], 1);
+    for (int u = 0; u < kReqPerPrepBlock / kPrepBlock; ++u) {
+      const int r = b * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
+      if (r >= a.R) break;
+      const int k = prep_request(a, r);
+      if (k >= 0) atomicAdd(local ? &hist[k] : &a.cnt[k], 1);
+    }
+    if (local) {
+      __syncthreads();
+      for (int k = threadIdx.x; k < a.NB; k += kPrepBlock)
+        if (hist[k]) atomicAdd(&a.cnt[k], hist[k]);
+    }
     return;
   }
   if (b < nbr + a.M) {
@@ -194,36 +218,51 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
   a.recs[i] = rec;
 }
 
-// One block of 1024 threads: exclusive scans of bucket counts and tiles-per-bucket,
-// the tile table, and scatter cursors.
-__global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
-  __shared__ int s_cnt[1024];
-  __shared__ int s_til[1024];
+// Inclusive prefix sum over a wavefront.
+__device__ __forceinline__ int wave_scan(int v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int o = __shfl_up(v, off, kWave);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+constexpr int kScanLds = 16384;   // bucket counts staged in LDS by k_scan (64 KB)
+
+// Scan body over bucket counts `cnt` (LDS copy or the global counters themselves).
+template <typename P>
+__device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_cnt, int *s_til) {
   const int T = blockDim.x;
   const int per = (a.NB + T - 1) / T;
   const int lo = threadIdx.x * per;
   const int hi = min(lo + per, a.NB);
   int c = 0, t = 0;
   for (int i = lo; i < hi; ++i) {
-    const int n = a.cnt[i];
+    const int n = cnt[i];
     c += n;
     t += (n + a.tile - 1) / a.tile;
   }
-  s_cnt[threadIdx.x] = c;
-  s_til[threadIdx.x] = t;
-  __syncthreads();
-  for (int off = 1; off < T; off <<= 1) {      // Hillis-Steele inclusive scan
-    const int vc = threadIdx.x >= off ? s_cnt[threadIdx.x - off] : 0;
-    const int vt = threadIdx.x >= off ? s_til[threadIdx.x - off] : 0;
-    __syncthreads();
-    s_cnt[threadIdx.x] += vc;
-    s_til[threadIdx.x] += vt;
-    __syncthreads();
+  const int ic = wave_scan(c), it = wave_scan(t);
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  if (lane == kWave - 1) {
+    s_cnt[wv] = ic;
+    s_til[wv] = it;
   }
-  int pc = s_cnt[threadIdx.x] - c;             // exclusive prefix
-  int pt = s_til[threadIdx.x] - t;
+  __syncthreads();
+  int pc = ic - c, pt = it - t;                  // exclusive prefix within the wave
+  int tot_c = 0, tot_t = 0;
+  for (int i = 0; i < T / kWave; ++i) {
+    if (i < wv) {
+      pc += s_cnt[i];
+      pt += s_til[i];
+    }
+    tot_c += s_cnt[i];
+    tot_t += s_til[i];
+  }
   for (int i = lo; i < hi; ++i) {
-    const int n = a.cnt[i];
+    const int n = cnt[i];
     a.bstart[i] = pc;
     const int nt = (n + a.tile - 1) / a.tile;
     for (int q = 0; q < nt; ++q) a.tiles[pt + q] = make_int2(i, pc + q * a.tile);
@@ -231,19 +270,74 @@ __global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
     pc += n;
     pt += nt;
   }
-  if (threadIdx.x == T - 1) {
-    a.bstart[a.NB] = s_cnt[T - 1];
-    *a.n_tiles = s_til[T - 1];
+  if (threadIdx.x == 0) {
+    a.bstart[a.NB] = tot_c;
+    *a.n_tiles = tot_t;
   }
 }
 
-__global__ void k_scatter(PlaceArgs a) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= a.R) return;
-  const int k = a.key[r];
-  if (k < 0) return;
-  const int pos = atomicAdd(&a.cnt[k], 1);
-  a.perm[pos] = r;
+// One block of 1024 threads: exclusive scans of bucket counts and tiles-per-bucket,
+// the tile table, and scatter cursors.  Counts are first copied to LDS in one coalesced
+// pass when they fit, so the scan never waits on a global load after a global store.
+__global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
+  __shared__ int s_cnt[1024 / kWave];
+  __shared__ int s_til[1024 / kWave];
+  extern __shared__ int lcnt[];     // [NB] when NB <= kScanLds
+  if (a.NB <= kScanLds) {
+    constexpr int U = 4;            // loads in flight per thread before the first wait
+    for (int i0 = 0; i0 < a.NB; i0 += U * 1024) {
+      int v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * 1024 + threadIdx.x;
+        v[u] = i < a.NB ? __builtin_nontemporal_load(&a.cnt[i]) : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * 1024 + threadIdx.x;
+        if (i < a.NB) lcnt[i] = v[u];
+      }
+    }
+    __syncthreads();
+    scan_buckets(a, lcnt, s_cnt, s_til);
+  } else {
+    scan_buckets(a, a.cnt, s_cnt, s_til);
+  }
+}
+
+// Requests grouped by bucket: each block ranks its requests per bucket in LDS, reserves
+// one range per non-empty bucket with a global atomic, then writes the permutation.
+__global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
+  __shared__ int hist[kHistMax];
+  constexpr int U = kReqPerPrepBlock / kPrepBlock;
+  const bool local = a.NB <= kHistMax;
+  int key[U], rank[U];
+  if (local) {
+    for (int k = threadIdx.x; k < a.NB; k += kPrepBlock) hist[k] = 0;
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int r = blockIdx.x * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
+    key[u] = r < a.R ? a.key[r] : -1;
+    rank[u] = 0;
+    if (key[u] >= 0) {
+      if (local)
+        rank[u] = atomicAdd(&hist[key[u]], 1);
+      else
+        a.perm[atomicAdd(&a.cnt[key[u]], 1)] = r;
+    }
+  }
+  if (!local) return;
+  __syncthreads();
+  for (int k = threadIdx.x; k < a.NB; k += kPrepBlock)
+    if (hist[k]) hist[k] = atomicAdd(&a.cnt[k], hist[k]);
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int r = blockIdx.x * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
+    if (key[u] >= 0) a.perm[hist[key[u]] + rank[u]] = r;
+  }
 }
 
 // ------------------------------------------------------------------ scoring kernel
@@ -494,23 +588,32 @@ __global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
 //
 // A workgroup takes a tile of WPB * kQF requests of one (wave, model) bucket; each
 // wavefront scores its kQF requests together against every hosting GPU.
-//   pass 1: per (request, cell) the minimum energy over the GPUs: one multiply, one FMA
-//           and one min per candidate; the GPU terms (Pp, Pd * TBT, the TBT-SLO mask) are
-//           shared by the kQF requests, the TTFT-SLO mask is applied once per request;
-//   pass 2: E* = the wavefront minimum; among the cells whose minimum equals E*, in
-//           ascending cell order, the lowest GPU position whose energy -- recomputed with
-//           the same operations, hence bit-identical -- equals E*.  That is the
+//   pass 1: per (request, cell) the minimum energy over the GPUs.  The tile's GPU records
+//           are staged in LDS grouped by SM-cap class (cap_pf, cap_dc); per class the
+//           capped prompt-row values of the kQF requests and the power factors s*f^3 sit
+//           in registers, so each GPU costs one record and one TBT read.  Per candidate:
+//           one multiply, one FMA, and half a v_min3 (GPUs taken in pairs).  Cells above
+//           max(cap_pf, cap_dc) repeat that level's cell exactly (same latencies, same
+//           power) at a higher index, so they get NaN power and never compete.
+//   pass 2: E* = the wavefront minimum; for each cell whose minimum equals E*, the lowest
+//           GPU id whose energy -- recomputed with the same operations, hence bit-identical
+//           -- equals E*; the smallest index (g * 128 + cell) wins.  That is the
 //           (energy, index) lexicographic minimum.
 // Masked (SLO-missing) latencies are NaN, which min ignores and == never matches.
 constexpr int kQF = 8;
 constexpr int kC = 128;
+constexpr int kNS8 = 8;
+constexpr int kClasses = kNS8 * kNS8;            // (cap_pf, cap_dc) pairs
 constexpr int kHcap = 256;                       // host records staged in LDS per chunk
 constexpr int kWblkB = (1 + kQF) * kC * 4;       // per wave: s*f^3 row + kQF prompt rows
+// Decode-table rows are padded to 130 floats in LDS: row r starts at bank 2r, so pass-2
+// reads of one cell from many rows hit distinct banks, and rows stay 8-byte aligned.
+constexpr int kRowB = 130 * 4;
 
 __host__ __device__ constexpr int fast_rec_off(int wpb) { return wpb * kWblkB; }
 __host__ __device__ constexpr int fast_dcs_off(int wpb) { return wpb * kWblkB + kHcap * 16; }
 __host__ __device__ constexpr size_t fast_lds_bytes(int wpb) {
-  return (size_t)fast_dcs_off(wpb) + (size_t)kRows * kC * 4;
+  return (size_t)fast_dcs_off(wpb) + (size_t)kRows * kRowB;
 }
 
 typedef float v2f __attribute__((ext_vector_type(2)));
@@ -523,16 +626,21 @@ __device__ __forceinline__ float lds1(const char *base, uint32_t off) {
   return *reinterpret_cast<const float *>(base + off);
 }
 
-// v_min_f32 as one instruction.  Its operands are results of arithmetic or +inf, and a
-// quiet-NaN operand yields the other operand, which is the masking rule; fminf would make
-// the compiler add a canonicalising v_max_f32 per operand in IEEE mode.
+// v_min_f32 / v_min3_f32 as single instructions.  Operands are results of arithmetic or
+// +inf, and a quiet-NaN operand yields the other operands, which is the masking rule;
+// fminf would make the compiler add a canonicalising v_max_f32 per operand in IEEE mode.
 __device__ __forceinline__ float vmin(float x, float y) {
   float r;
   asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(x), "v"(y));
   return r;
 }
+__device__ __forceinline__ float vmin3(float x, float y, float z) {
+  float r;
+  asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(y), "v"(z));
+  return r;
+}
 
-// Energy of one candidate.  Pass 1 and pass 2 both evaluate exactly this expression.
+// Energy of one candidate.  Pass 1 and pass 2 both evaluate exactly these operations.
 __device__ __forceinline__ float cell_energy(float kap, float pdp, float pdd, float tbt, float tt,
                                             float p0, float lo, float slo_tbt) {
   const float Pp = fmaf(kap, pdp, p0);
@@ -541,46 +649,81 @@ __device__ __forceinline__ float cell_energy(float kap, float pdp, float pdd, fl
   return fmaf(lo, Ym, Pp * tt);
 }
 
-// Pass 1 over host records [0, n) of the LDS record table.  SAME: the kQF requests share
-// their TBT SLO, so the TBT mask is applied once per (GPU, cell).
-template <bool SAME>
-__device__ __forceinline__ void fast_pass1(const char *L, uint32_t recB, uint32_t wblkB, int n,
-                                           uint32_t j64, uint32_t k04, float p0, const float (&lo)[kQF],
-                                           const float (&sb)[kQF], float (&mn)[kQF][2]) {
-  for (int i = 0; i < n; ++i) {
-    const v4u r = *reinterpret_cast<const v4u *>(L + recB + i * 16);
-    const uint32_t rowB = r.x;
-    const float kap = __uint_as_float(r.y);
-    const uint32_t aP = wblkB + min(j64, r.z) + k04;
-    const uint32_t mD = min(j64, r.w) + k04;
-    const v2f pdp = lds2(L, aP);
-    const v2f pdd = lds2(L, wblkB + mD);
-    const v2f tbt = lds2(L, rowB + mD);
-    float Pp[2], Y[2];
+// TBT-SLO handling of pass 1:
+//   kPremasked  every live request of the tile has the same TBT SLO and the staged decode
+//               table already holds NaN where TBT misses it;
+//   kWaveSame   the wavefront's live requests share one TBT SLO: one test per (GPU, cell);
+//   kMixed      one test per (request, GPU, cell).
+enum { kPremasked = 0, kWaveSame = 1, kMixed = 2 };
+
+// Per-class registers of one wavefront: capped prompt-row values of its requests, the
+// power factors, and the decode-cell offset.
+struct ClassRegs {
+  v2f tt[kQF];
+  v2f pdp, pdd;
+  uint32_t mD;
+};
+
+template <int MODE>
+__device__ __forceinline__ void host_terms(const char *L, v4u r, const ClassRegs &cr, float p0, float sb0,
+                                           float (&Pp)[2], float (&Y)[2], float (&tbt)[2]) {
+  const float kap = __uint_as_float(r.y);
+  const v2f t = lds2(L, r.x + cr.mD);
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      Pp[c] = fmaf(kap, pdp[c], p0);
-      const float Pd = fmaf(kap, pdd[c], p0);
-      Y[c] = SAME ? (tbt[c] < sb[0] ? Pd * tbt[c] : kMask) : Pd * tbt[c];
-    }
+  for (int c = 0; c < 2; ++c) {
+    Pp[c] = fmaf(kap, cr.pdp[c], p0);
+    const float Pd = fmaf(kap, cr.pdd[c], p0);
+    tbt[c] = t[c];
+    Y[c] = MODE == kWaveSame ? (t[c] < sb0 ? Pd * t[c] : kMask) : Pd * t[c];
+  }
+}
+
+// Pass 1 over the records [cs, ce) of one class.
+template <int MODE>
+__device__ __forceinline__ void class_pass1(const char *L, uint32_t recB, int cs, int ce, const ClassRegs &cr,
+                                            float p0, const float (&lo)[kQF], const float (&sb)[kQF],
+                                            float sb0, float (&mn)[kQF][2]) {
+  int i = cs;
+  for (; i + 1 < ce; i += 2) {
+    const v4u r0 = *reinterpret_cast<const v4u *>(L + recB + i * 16);
+    const v4u r1 = *reinterpret_cast<const v4u *>(L + recB + (i + 1) * 16);
+    float Pp0[2], Y0[2], T0[2], Pp1[2], Y1[2], T1[2];
+    host_terms<MODE>(L, r0, cr, p0, sb0, Pp0, Y0, T0);
+    host_terms<MODE>(L, r1, cr, p0, sb0, Pp1, Y1, T1);
 #pragma unroll
-    for (int q = 0; q < kQF; ++q) {
-      const v2f tt = lds2(L, aP + (1 + q) * kC * 4);
+    for (int q = 0; q < kQF; ++q)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const float Ym = SAME ? Y[c] : (tbt[c] < sb[q] ? Y[c] : kMask);
-        mn[q][c] = vmin(mn[q][c], fmaf(lo[q], Ym, Pp[c] * tt[c]));
+        const float y0 = MODE == kMixed ? (T0[c] < sb[q] ? Y0[c] : kMask) : Y0[c];
+        const float y1 = MODE == kMixed ? (T1[c] < sb[q] ? Y1[c] : kMask) : Y1[c];
+        mn[q][c] = vmin3(mn[q][c], fmaf(lo[q], y0, Pp0[c] * cr.tt[q][c]), fmaf(lo[q], y1, Pp1[c] * cr.tt[q][c]));
       }
-    }
+  }
+  if (i < ce) {
+    const v4u r0 = *reinterpret_cast<const v4u *>(L + recB + i * 16);
+    float Pp0[2], Y0[2], T0[2];
+    host_terms<MODE>(L, r0, cr, p0, sb0, Pp0, Y0, T0);
+#pragma unroll
+    for (int q = 0; q < kQF; ++q)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const float y0 = MODE == kMixed ? (T0[c] < sb[q] ? Y0[c] : kMask) : Y0[c];
+        mn[q][c] = vmin(mn[q][c], fmaf(lo[q], y0, Pp0[c] * cr.tt[q][c]));
+      }
   }
 }
 
 template <int WPB>
 __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   extern __shared__ __align__(16) float lds[];
+  __shared__ int s_live[WPB], s_same[WPB], s_sb[WPB];
+  __shared__ int s_cls[kClasses + 1];     // class counts, then class starts
+  __shared__ int s_clist[kClasses + 1];   // non-empty classes: cls | start << 6 | end << 15; [64] = count
+  __shared__ float4 s_par[WPB][kQF];      // pass 2: per request {cell, E*, Lout, TBT SLO}
   char *L = reinterpret_cast<char *>(lds);
   constexpr uint32_t recB = fast_rec_off(WPB);
   constexpr uint32_t dcsB = fast_dcs_off(WPB);
+  constexpr int T = WPB * 64;
   const int t = blockIdx.x;
   if (t >= *ro(a.n_tiles)) return;
   const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
@@ -594,17 +737,6 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   const int beg = tp[2 * t + 1];
   const int end = min(beg + a.tile, ro(a.bstart)[bucket + 1]);
 
-  {  // the model's decode table
-    const float *src = a.dc + (size_t)m * kRows * kC;
-    if ((((uintptr_t)src) & 15) == 0) {
-      const float4 *s4 = reinterpret_cast<const float4 *>(src);
-      float4 *d4 = reinterpret_cast<float4 *>(L + dcsB);
-      for (int i = threadIdx.x; i < kRows * kC / 4; i += WPB * 64) d4[i] = s4[i];
-    } else {
-      float *d1 = reinterpret_cast<float *>(L + dcsB);
-      for (int i = threadIdx.x; i < kRows * kC; i += WPB * 64) d1[i] = src[i];
-    }
-  }
   const int wv = uniform(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t wblkB = (uint32_t)wv * kWblkB;
@@ -618,12 +750,15 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     *reinterpret_cast<v2f *>(L + wblkB + j64 + k04) = pd;
   }
 
-  // this wavefront's requests, and their prompt rows (NaN where TTFT misses the SLO)
+  // this wavefront's requests and their prompt rows (NaN where TTFT misses the SLO).  A
+  // request whose whole row is NaN is dead: infeasible whatever the TBT test says, so it
+  // takes no part in the TBT-SLO uniformity checks.
   const int q0 = beg + wv * kQF;
   const int nq = max(0, min(kQF, end - q0));
   int rq[kQF];
   float lo[kQF], sb[kQF];
-  bool same = true;
+  bool live_any = false, wsame = true;
+  float sb0 = 0.f;
 #pragma unroll
   for (int q = 0; q < kQF; ++q) {
     rq[q] = q < nq ? ro(a.perm)[q0 + q] : -1;
@@ -637,8 +772,6 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
       sb[q] = ro(a.slo_tbt)[rq[q]];
       prw = ro(a.row)[rq[q]];
     }
-    if (q > 0 && rq[q] < 0) sb[q] = sb[0];
-    same = same && __float_as_int(sb[q]) == __float_as_int(sb[0]);
     const float *pr = a.pf + ((size_t)m * kRows + prw) * kC + 2 * lane;
     v2f v;
     v.x = rq[q] >= 0 ? pr[0] : kMask;
@@ -646,105 +779,232 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     v.x = v.x < st ? v.x : kMask;
     v.y = v.y < st ? v.y : kMask;
     *reinterpret_cast<v2f *>(L + wblkB + (1 + q) * kC * 4 + j64 + k04) = v;
+    const bool live = __ballot(v.x == v.x || v.y == v.y) != 0ull;
+    if (live) {
+      if (!live_any) sb0 = sb[q];
+      wsame = wsame && __float_as_int(sb[q]) == __float_as_int(sb0);
+      live_any = true;
+    }
+  }
+  if (lane == 0) {
+    s_live[wv] = live_any;
+    s_same[wv] = wsame;
+    s_sb[wv] = __float_as_int(sb0);
+  }
+  __syncthreads();
+  bool tile_live = false, tile_same = true;
+  int tile_sb = 0;
+  for (int v = 0; v < WPB; ++v) {
+    if (!s_live[v]) continue;
+    if (!tile_live) tile_sb = s_sb[v];
+    tile_same = tile_same && s_same[v] && s_sb[v] == tile_sb;
+    tile_live = true;
+  }
+  const float tsb = __int_as_float(tile_sb);
+
+  {  // the model's decode table, rows padded to kRowB bytes; NaN where TBT misses the
+     // tile's common TBT SLO
+    const float *src = a.dc + (size_t)m * kRows * kC;
+    if ((((uintptr_t)src) & 15) == 0) {
+      const float4 *s4 = reinterpret_cast<const float4 *>(src);
+      for (int i = threadIdx.x; i < kRows * kC / 4; i += T) {
+        float4 v = s4[i];
+        if (tile_same) {
+          v.x = v.x < tsb ? v.x : kMask;
+          v.y = v.y < tsb ? v.y : kMask;
+          v.z = v.z < tsb ? v.z : kMask;
+          v.w = v.w < tsb ? v.w : kMask;
+        }
+        v2f *d = reinterpret_cast<v2f *>(L + dcsB + (i >> 5) * kRowB + (i & 31) * 16);
+        d[0] = v2f{v.x, v.y};
+        d[1] = v2f{v.z, v.w};
+      }
+    } else {
+      for (int i = threadIdx.x; i < kRows * kC; i += T) {
+        float v = src[i];
+        if (tile_same) v = v < tsb ? v : kMask;
+        *reinterpret_cast<float *>(L + dcsB + (i >> 7) * kRowB + (i & 127) * 4) = v;
+      }
+    }
   }
 
   float mn[kQF][2];
 #pragma unroll
   for (int q = 0; q < kQF; ++q) mn[q][0] = mn[q][1] = kInf;
 
-  const int hcnt = ro(a.host_cnt)[m];
+  const int hcnt = tile_live ? ro(a.host_cnt)[m] : 0;   // a tile of dead requests scores nothing
   const int32_t *hl = a.host_list + (size_t)m * a.G;
   const HostRec *rw = a.recs + (size_t)w * a.G;
   const float p0 = a.p0;
+  constexpr int kPer = kHcap / T > 0 ? kHcap / T : 1;  // host records per thread per chunk
   for (int c0 = 0; c0 < hcnt; c0 += kHcap) {
     const int n = min(kHcap, hcnt - c0);
-    __syncthreads();                      // previous records no longer in use; rows written
-    for (int i = threadIdx.x; i < n; i += WPB * 64) {
-      const HostRec r = rw[hl[c0 + i]];
-      v4u f;
-      f.x = dcsB + (uint32_t)max(r.row_off, 0) * 4u;
-      f.y = __float_as_uint(r.kappa);
-      f.z = (uint32_t)(r.caps & 0xff) * 64u;
-      f.w = (uint32_t)((r.caps >> 8) & 0xff) * 64u;
-      *reinterpret_cast<v4u *>(L + recB + i * 16) = f;
+    __syncthreads();                      // previous records no longer in use; table staged
+    for (int i = threadIdx.x; i < kClasses; i += T) s_cls[i] = 0;
+    __syncthreads();
+    // records of this chunk, grouped by (cap_pf, cap_dc) class with an LDS counting sort
+    v4u rec[kPer];
+    int key[kPer], rank[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int i = u * T + threadIdx.x;
+      key[u] = -1;
+      if (i < n) {
+        const int g = hl[c0 + i];
+        const HostRec r = rw[g];
+        rec[u].x = dcsB + (uint32_t)(max(r.row_off, 0) / kC) * kRowB;
+        rec[u].y = __float_as_uint(r.kappa);
+        rec[u].z = (uint32_t)g;
+        rec[u].w = (uint32_t)r.caps;
+        key[u] = (r.caps & 0xff) * kNS8 + ((r.caps >> 8) & 0xff);
+        rank[u] = atomicAdd(&s_cls[key[u]], 1);
+      }
     }
     __syncthreads();
-    if (nq > 0) {
-      if (same)
-        fast_pass1<true>(L, recB, wblkB, n, j64, k04, p0, lo, sb, mn);
-      else
-        fast_pass1<false>(L, recB, wblkB, n, j64, k04, p0, lo, sb, mn);
+    if (threadIdx.x < kWave) {            // exclusive prefix over the 64 classes, and the
+      const int cnt = s_cls[threadIdx.x];  // compact list of the non-empty ones
+      const int inc = wave_scan(cnt);
+      s_cls[threadIdx.x] = inc - cnt;
+      const unsigned long long ne = __ballot(cnt > 0);
+      const int pos = __popcll(ne & ((1ull << threadIdx.x) - 1ull));
+      if (cnt > 0) s_clist[pos] = threadIdx.x | ((inc - cnt) << 6) | (inc << 15);
+      if (threadIdx.x == kWave - 1) {
+        s_cls[kClasses] = inc;
+        s_clist[kClasses] = __popcll(ne);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kPer; ++u)
+      if (key[u] >= 0) *reinterpret_cast<v4u *>(L + recB + (s_cls[key[u]] + rank[u]) * 16) = rec[u];
+    __syncthreads();
+    if (live_any) {
+      const int ncls = uniform(s_clist[kClasses]);
+      for (int k = 0; k < ncls; ++k) {
+        const int packed = uniform(s_clist[k]);
+        const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
+        const uint32_t cpB = (uint32_t)(cls / kNS8) * 64u, cdB = (uint32_t)(cls % kNS8) * 64u;
+        ClassRegs cr;
+        const uint32_t aP = wblkB + min(j64, cpB) + k04;
+        cr.mD = min(j64, cdB) + k04;
+        cr.pdp = lds2(L, aP);
+        cr.pdd = lds2(L, wblkB + cr.mD);
+        if (j64 > max(cpB, cdB)) cr.pdp = v2f{kMask, kMask};   // repeated cells drop out
+#pragma unroll
+        for (int q = 0; q < kQF; ++q) cr.tt[q] = lds2(L, aP + (1 + q) * kC * 4);
+        if (tile_same)
+          class_pass1<kPremasked>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+        else if (wsame)
+          class_pass1<kWaveSame>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+        else
+          class_pass1<kMixed>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+      }
     }
   }
 
-  // pass 2: the winning energy, then the lowest index that reaches it
+  // pass 2: per request the winning energy E*, then the lowest index that reaches it.
+  // Requests are searched together: lane = (host i, request q) with q = lane % kQF, so a
+  // chunk covers 64 / kQF hosts of every request; one round per tied cell of a request
+  // (one round unless two different cells reach exactly E*).
   const bool recs_in_lds = hcnt <= kHcap;
+  float est[kQF];
+  unsigned long long t0[kQF], t1[kQF];
+  bool rounds = false;
 #pragma unroll
   for (int q = 0; q < kQF; ++q) {
-    if (q >= nq) break;
     float e = vmin(mn[q][0], mn[q][1]);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) e = vmin(e, __shfl_xor(e, off, kWave));
-    const float est = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(e)));
-    int best = INT_MAX;
-    if (est < kInf) {
-      unsigned long long t0 = __ballot(mn[q][0] == est);
-      unsigned long long t1 = __ballot(mn[q][1] == est);
-      int ilim = hcnt;                    // positions >= ilim cannot improve the index
-      while ((t0 | t1) != 0ull) {
-        // next tied cell in ascending order: cell = 2 * lane + c
-        const int l0 = t0 ? __builtin_ctzll(t0) : 64;
-        const int l1 = t1 ? __builtin_ctzll(t1) : 64;
-        int cell;
-        if (l0 <= l1) {
-          cell = 2 * l0;
-          t0 &= t0 - 1ull;
-        } else {
-          cell = 2 * l1 + 1;
-          t1 &= t1 - 1ull;
+    est[q] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(e)));
+    const bool feas = q < nq && est[q] < kInf;
+    t0[q] = __ballot(feas && mn[q][0] == est[q]);
+    t1[q] = __ballot(feas && mn[q][1] == est[q]);
+    rounds = rounds || (t0[q] | t1[q]) != 0ull;
+  }
+  const int myq = lane & (kQF - 1);
+  int bestl = INT_MAX;                    // lane q < kQF: best index of request q
+  while (rounds) {
+    rounds = false;
+    if (lane == 0) {
+#pragma unroll
+      for (int q = 0; q < kQF; ++q) {
+        int cell = -1;                    // next tied cell of request q, ascending
+        if ((t0[q] | t1[q]) != 0ull) {
+          const int l0 = t0[q] ? __builtin_ctzll(t0[q]) : 64;
+          const int l1 = t1[q] ? __builtin_ctzll(t1[q]) : 64;
+          cell = l0 <= l1 ? 2 * l0 : 2 * l1 + 1;
         }
-        const uint32_t cj64 = (uint32_t)(cell >> 4) * 64u, ck4 = (uint32_t)(cell & 15) * 4u;
-        for (int b0 = 0; b0 < ilim; b0 += kWave) {
-          const int i = b0 + lane;
-          bool hit = false;
-          if (i < ilim) {
-            uint32_t rowB, cpB, cdB;
-            float kap;
-            if (recs_in_lds) {
-              const v4u r = *reinterpret_cast<const v4u *>(L + recB + i * 16);
-              rowB = r.x;
-              kap = __uint_as_float(r.y);
-              cpB = r.z;
-              cdB = r.w;
-            } else {
-              const HostRec r = rw[hl[i]];
-              rowB = dcsB + (uint32_t)max(r.row_off, 0) * 4u;
-              kap = r.kappa;
-              cpB = (uint32_t)(r.caps & 0xff) * 64u;
-              cdB = (uint32_t)((r.caps >> 8) & 0xff) * 64u;
-            }
-            const uint32_t aP = wblkB + min(cj64, cpB) + ck4;
-            const uint32_t mD = min(cj64, cdB) + ck4;
-            const float E = cell_energy(kap, lds1(L, aP), lds1(L, wblkB + mD), lds1(L, rowB + mD),
-                                        lds1(L, aP + (1 + q) * kC * 4), p0, lo[q], same ? sb[0] : sb[q]);
-            hit = E == est;
+        s_par[wv][q] = make_float4(__int_as_float(cell), est[q], lo[q], sb[q]);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kQF; ++q) {       // consume the cell just published
+      if ((t0[q] | t1[q]) != 0ull) {
+        const int l0 = t0[q] ? __builtin_ctzll(t0[q]) : 64;
+        const int l1 = t1[q] ? __builtin_ctzll(t1[q]) : 64;
+        if (l0 <= l1)
+          t0[q] &= t0[q] - 1ull;
+        else
+          t1[q] &= t1[q] - 1ull;
+      }
+      rounds = rounds || (t0[q] | t1[q]) != 0ull;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const float4 par = s_par[wv][myq];
+    const int cell = __float_as_int(par.x);
+    int gmin = INT_MAX;                   // lowest GPU id reaching E* (per lane)
+    if (cell >= 0) {
+      const uint32_t cj64 = (uint32_t)(cell >> 4) * 64u, ck4 = (uint32_t)(cell & 15) * 4u;
+      const uint32_t ttB = wblkB + (1 + myq) * kC * 4;
+      for (int b0 = 0; b0 < hcnt * kQF; b0 += kWave) {
+        const int i = (b0 + lane) / kQF;
+        if (i < hcnt) {
+          uint32_t rowB;
+          int g, caps;
+          float kap;
+          if (recs_in_lds) {
+            const v4u r = *reinterpret_cast<const v4u *>(L + recB + i * 16);
+            rowB = r.x;
+            kap = __uint_as_float(r.y);
+            g = (int)r.z;
+            caps = (int)r.w;
+          } else {
+            g = hl[i];
+            const HostRec r = rw[g];
+            rowB = dcsB + (uint32_t)(max(r.row_off, 0) / kC) * kRowB;
+            kap = r.kappa;
+            caps = r.caps;
           }
-          const unsigned long long h = __ballot(hit);
-          if (h) {
-            const int i_hit = b0 + __builtin_ctzll(h);
-            best = min(best, ro(a.host_list + (size_t)m * a.G)[i_hit] * kC + cell);
-            ilim = i_hit;                 // later cells need a strictly lower position
-            break;
-          }
+          const uint32_t cpB = (uint32_t)(caps & 0xff) * 64u, cdB = (uint32_t)((caps >> 8) & 0xff) * 64u;
+          const uint32_t mP = min(cj64, cpB) + ck4;
+          const uint32_t mD = min(cj64, cdB) + ck4;
+          const float pdp = cj64 > max(cpB, cdB) ? kMask : lds1(L, wblkB + mP);
+          const float E = cell_energy(kap, pdp, lds1(L, wblkB + mD), lds1(L, rowB + mD), lds1(L, ttB + mP),
+                                      p0, par.z, par.w);
+          if (E == par.y) gmin = min(gmin, g);
         }
       }
     }
-    if (lane == 0) {
-      const bool found = best != INT_MAX;
-      a.choice[rq[q]] = found ? best : -1;
-      a.feasible[rq[q]] = found ? 1 : 0;
-      a.energy[rq[q]] = found ? est : kInf;
-    }
+#pragma unroll
+    for (int off = kQF; off < kWave; off <<= 1) gmin = min(gmin, __shfl_xor(gmin, off, kWave));
+    if (cell >= 0 && gmin != INT_MAX) bestl = min(bestl, gmin * kC + cell);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  if (lane < nq) {
+    float e = est[0];
+#pragma unroll
+    for (int q = 1; q < kQF; ++q) e = lane == q ? est[q] : e;
+    int r = rq[0];
+#pragma unroll
+    for (int q = 1; q < kQF; ++q) r = lane == q ? rq[q] : r;
+    const bool found = bestl != INT_MAX;
+    a.choice[r] = found ? bestl : -1;
+    a.feasible[r] = found ? 1 : 0;
+    a.energy[r] = found ? e : kInf;
   }
 }
 
@@ -797,15 +1057,18 @@ __global__ void __launch_bounds__(256) k_fleet(MigArgs a) {
 }
 
 constexpr int kSrcPerWave = 2;
+constexpr int kMigChunk = 2048;   // destination records staged in LDS per pass
 
+// Two sources per wavefront, four wavefronts per block; destination records are staged in
+// LDS in chunks (one coalesced pass over the fleet per block), lanes span destinations.
 __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
   __shared__ float f3[32];
+  __shared__ int4 drec[kMigChunk];       // hbm, SM per-mille, level mask, k_d
+  __shared__ float2 drec2[kMigChunk];    // u_d, f[kd0]^3 * u_d
   if (threadIdx.x < 32) f3[threadIdx.x] = threadIdx.x < a.NF ? cube(a.freq_level[threadIdx.x]) : 0.f;
-  __syncthreads();
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = uniform(threadIdx.x >> 6);
   const int s0 = (blockIdx.x * (blockDim.x / kWave) + wv) * kSrcPerWave;
-  if (s0 >= a.G) return;
   int src[kSrcPerWave], remH[kSrcPerWave], remU[kSrcPerWave];
   uint32_t fms[kSrcPerWave];
   float us[kSrcPerWave];
@@ -831,23 +1094,37 @@ __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
     bd[q] = INT_MAX;
     bk[q] = -1;
   }
-  for (int d = lane; d < a.G; d += kWave) {
-    const int hd = a.hbm[d], ud_pm = a.smpm[d];
-    const uint32_t fmd = a.fm[d];
-    const float ud = a.util[d], kd = a.kdyn[d], bb = a.base[d];
+  for (int d0 = 0; d0 < a.G; d0 += kMigChunk) {
+    const int n = min(kMigChunk, a.G - d0);
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+      const int d = d0 + i;
+      drec[i] = make_int4(a.hbm[d], a.smpm[d], (int)a.fm[d], __float_as_int(a.kdyn[d]));
+      drec2[i] = make_float2(a.util[d], a.base[d]);
+    }
+    __syncthreads();
+    if (s0 >= a.G) continue;
+    for (int i = lane; i < n; i += kWave) {
+      const int d = d0 + i;
+      const int4 r = drec[i];
+      const float2 r2 = drec2[i];
+      const uint32_t fmd = (uint32_t)r.z;
+      const float kd = __int_as_float(r.w);
 #pragma unroll
-    for (int q = 0; q < kSrcPerWave; ++q) {
-      const uint32_t f = fms[q] & fmd;
-      const bool ok = any[q] && d != src[q] && hd <= remH[q] && ud_pm <= remU[q] && f != 0u;
-      const int k = __builtin_ctz(f | 0x80000000u);
-      const float added = f3[k] * (us[q] + ud) - bb;
-      const float sv = fmaf(-kd, added, a.p0);
-      const bool better = ok && sv > bs[q];
-      bs[q] = better ? sv : bs[q];
-      bd[q] = better ? d : bd[q];
-      bk[q] = better ? k : bk[q];
+      for (int q = 0; q < kSrcPerWave; ++q) {
+        const uint32_t f = fms[q] & fmd;
+        const bool ok = any[q] && d != src[q] && r.x <= remH[q] && r.y <= remU[q] && f != 0u;
+        const int k = __builtin_ctz(f | 0x80000000u);
+        const float added = f3[k] * (us[q] + r2.x) - r2.y;
+        const float sv = fmaf(-kd, added, a.p0);
+        const bool better = ok && sv > bs[q];
+        bs[q] = better ? sv : bs[q];
+        bd[q] = better ? d : bd[q];
+        bk[q] = better ? k : bk[q];
+      }
     }
   }
+  if (s0 >= a.G) return;
 #pragma unroll
   for (int q = 0; q < kSrcPerWave; ++q) {
     float v = bs[q];
@@ -1051,11 +1328,11 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   const int zb = (lay.NB + 255) / 256;
   k_zero<<<zb < 1024 ? zb : 1024, 256, 0, st>>>(a.cnt, lay.NB);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  const int nbr = (a.R + kPrepBlock - 1) / kPrepBlock;
+  const int nbr = (a.R + kReqPerPrepBlock - 1) / kReqPerPrepBlock;
   const long long nrec = ((long long)a.W * a.G + kPrepBlock - 1) / kPrepBlock;
   k_prep<<<(unsigned)(nbr + a.M + nrec), kPrepBlock, 0, st>>>(a, nbr);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  k_scan<<<1, 1024, 0, st>>>(a);
+  k_scan<<<1, 1024, lay.NB <= kScanLds ? sizeof(int) * lay.NB : 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   k_scatter<<<nbr, kPrepBlock, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
