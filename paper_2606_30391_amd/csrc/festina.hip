@@ -50,6 +50,14 @@ struct HostRec {                 // per (wave, GPU), 16 bytes
   int32_t pad;
 };
 
+struct ReqRec {                  // one request in bucket order, 32 bytes
+  int32_t r;                     // request index
+  int32_t row;                   // prompt row (-1: the decode batch row)
+  float lout;                    // padded output tokens
+  float slo_ttft, slo_tbt;
+  int32_t pad[3];
+};
+
 struct PlaceArgs {
   // table
   int32_t M, NS, NF, C;          // C = NS * NF
@@ -81,10 +89,8 @@ struct PlaceArgs {
   int32_t *host_cnt;             // [M]
   int32_t *host_list;            // [M][G]
   HostRec *recs;                 // [W][G]
-  int32_t *perm;                 // [R]
+  ReqRec *preq;                  // [R] request records in bucket order
   int32_t *key;                  // [R]
-  int32_t *row;                  // [R] prompt row (-1: batch row)
-  float *lout;                   // [R] padded output tokens
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -112,13 +118,27 @@ __device__ __forceinline__ HostRec load_rec(const __attribute__((address_space(4
   return r;
 }
 
+// Request record at bucket position pos (wave-uniform): two scalar 16-byte loads.
+__device__ __forceinline__ ReqRec load_req(const PlaceArgs &a, int pos) {
+  const auto p = ro(reinterpret_cast<const v4i *>(a.preq + pos));
+  const v4i x = p[0], y = p[1];
+  ReqRec q;
+  q.r = x.x;
+  q.row = x.y;
+  q.lout = __int_as_float(x.z);
+  q.slo_ttft = __int_as_float(x.w);
+  q.slo_tbt = __int_as_float(y.x);
+  q.pad[0] = q.pad[1] = q.pad[2] = 0;
+  return q;
+}
+
 // ------------------------------------------------------------------ prologue kernels
 __global__ void k_zero(int32_t *p, int32_t n) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
-// Request pre-processing of request r: validity, 5% output pad, prompt bucket, bucket key.
-// Returns the key, or -1 (and writes the infeasible result) for an invalid request.
+// Validity and bucket key (wave, model, has-prompt) of request r.  Returns the key, or -1
+// (and writes the infeasible result) for an invalid request.
 __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r) {
   const int m = a.model[r];
   const int w = a.wave ? a.wave[r] : 0;
@@ -132,14 +152,7 @@ __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r) {
     a.energy[r] = kInf;
     return -1;
   }
-  // prompt bucket: min(ceil(tokens / 256), 32) - 1 (unsigned: no overflow for any
-  // int32 token count); 0 tokens -> the decode batch row is used
-  const int prow = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
-  // 5% safety pad: ceil(1.05 * pred) = (105 * pred + 99) / 100, in 64-bit
-  const long long lo = ((long long)pr * 105 + 99) / 100;
-  a.row[r] = prow;
-  a.lout[r] = (float)lo;
-  const int k = ((w * a.M + m) << 1) | (prow < 0 ? 1 : 0);
+  const int k = ((w * a.M + m) << 1) | (pt == 0 ? 1 : 0);
   a.key[r] = k;
   return k;
 }
@@ -305,6 +318,21 @@ __global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
   }
 }
 
+// Record of valid request r: prompt bucket min(ceil(tokens / 256), 32) - 1 (unsigned: no
+// overflow for any int32 token count; 0 tokens -> -1, the decode batch row), the 5% output
+// pad ceil(1.05 * pred) = (105 * pred + 99) / 100 in 64-bit, and the SLOs.
+__device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
+  const int pt = a.prompt[r];
+  ReqRec q;
+  q.r = r;
+  q.row = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
+  q.lout = (float)(((long long)a.pred[r] * 105 + 99) / 100);
+  q.slo_ttft = a.slo_ttft[r];
+  q.slo_tbt = a.slo_tbt[r];
+  q.pad[0] = q.pad[1] = q.pad[2] = 0;
+  return q;
+}
+
 // Requests grouped by bucket: each block ranks its requests per bucket in LDS, reserves
 // one range per non-empty bucket with a global atomic, then writes the permutation.
 __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
@@ -325,7 +353,7 @@ __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
       if (local)
         rank[u] = atomicAdd(&hist[key[u]], 1);
       else
-        a.perm[atomicAdd(&a.cnt[key[u]], 1)] = r;
+        a.preq[atomicAdd(&a.cnt[key[u]], 1)] = make_req_rec(a, r);
     }
   }
   if (!local) return;
@@ -336,7 +364,7 @@ __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int r = blockIdx.x * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
-    if (key[u] >= 0) a.perm[hist[key[u]] + rank[u]] = r;
+    if (key[u] >= 0) a.preq[hist[key[u]] + rank[u]] = make_req_rec(a, r);
   }
 }
 
@@ -425,12 +453,13 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
 #pragma unroll
     for (int q = 0; q < kQ; ++q) {
       const int pos = base + q;
-      rq[q] = pos < end ? ro(a.perm)[pos] : -1;
+      const ReqRec rr = load_req(a, pos < end ? pos : beg);
+      rq[q] = pos < end ? rr.r : -1;
       if (rq[q] >= 0) {
-        lo[q] = ro(a.lout)[rq[q]];
-        st[q] = ro(a.slo_ttft)[rq[q]];
-        sb[q] = ro(a.slo_tbt)[rq[q]];
-        prw[q] = ro(a.row)[rq[q]];
+        lo[q] = rr.lout;
+        st[q] = rr.slo_ttft;
+        sb[q] = rr.slo_tbt;
+        prw[q] = rr.row;
       } else {
         lo[q] = 0.f;
         st[q] = -kInf;                    // nothing is below -inf: never feasible
@@ -602,6 +631,7 @@ __global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
 // Masked (SLO-missing) latencies are NaN, which min ignores and == never matches.
 constexpr int kQF = 8;
 constexpr int kC = 128;
+constexpr int kXcds = 8;                         // MI355X: 8 XCDs, each with its own L2
 constexpr int kNS8 = 8;
 constexpr int kClasses = kNS8 * kNS8;            // (cap_pf, cap_dc) pairs
 constexpr int kHcap = 256;                       // host records staged in LDS per chunk
@@ -724,8 +754,14 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   constexpr uint32_t recB = fast_rec_off(WPB);
   constexpr uint32_t dcsB = fast_dcs_off(WPB);
   constexpr int T = WPB * 64;
-  const int t = blockIdx.x;
-  if (t >= *ro(a.n_tiles)) return;
+  // XCD-aware tile order: workgroups are dealt to the 8 XCDs round-robin, so XCD x takes
+  // the contiguous tile range [x * per, (x + 1) * per) -- the same arrival waves and GPU
+  // records -- instead of every eighth tile.  per = ceil(n_tiles / 8) <= grid / 8.
+  const int ntiles = *ro(a.n_tiles);
+  const int per = (ntiles + kXcds - 1) / kXcds;
+  const int idx = blockIdx.x / kXcds;
+  const int t = (blockIdx.x % kXcds) * per + idx;
+  if (idx >= per || t >= ntiles) return;
   const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
   const int bucket = tp[2 * t];
   if (bucket & 1) {                       // prompt-less requests: TTFT from the batch row
@@ -761,16 +797,17 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   float sb0 = 0.f;
 #pragma unroll
   for (int q = 0; q < kQF; ++q) {
-    rq[q] = q < nq ? ro(a.perm)[q0 + q] : -1;
+    const ReqRec rr = load_req(a, q < nq ? q0 + q : beg);
+    rq[q] = q < nq ? rr.r : -1;
     float st = -kInf;
     int prw = 0;
     lo[q] = 0.f;
     sb[q] = -kInf;
     if (rq[q] >= 0) {
-      lo[q] = ro(a.lout)[rq[q]];
-      st = ro(a.slo_ttft)[rq[q]];
-      sb[q] = ro(a.slo_tbt)[rq[q]];
-      prw = ro(a.row)[rq[q]];
+      lo[q] = rr.lout;
+      st = rr.slo_ttft;
+      sb[q] = rr.slo_tbt;
+      prw = rr.row;
     }
     const float *pr = a.pf + ((size_t)m * kRows + prw) * kC + 2 * lane;
     v2f v;
@@ -1153,7 +1190,7 @@ __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct PlaceLayout {
-  size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, perm, key, row, lout, total;
+  size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, preq, key, total;
   int32_t NB, tile, max_tiles, waves_per_block;
   bool fast;                     // 8 SM x 16 frequency levels: the specialised kernel
 };
@@ -1192,7 +1229,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   }
   o->fast = fast;
   const long long max_tiles = (R + tile - 1) / tile + NB;
-  if (max_tiles > INT_MAX) return false;
+  if (max_tiles > INT_MAX - 8) return false;   // the grid is rounded up to a multiple of 8
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -1206,10 +1243,8 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->host_cnt = take(sizeof(int32_t) * M);
   o->host_list = take(sizeof(int32_t) * M * Gn);
   o->recs = take(sizeof(HostRec) * W * Gn);
-  o->perm = take(sizeof(int32_t) * (R > 0 ? R : 1));
+  o->preq = take(sizeof(ReqRec) * (R > 0 ? R : 1));
   o->key = take(sizeof(int32_t) * (R > 0 ? R : 1));
-  o->row = take(sizeof(int32_t) * (R > 0 ? R : 1));
-  o->lout = take(sizeof(float) * (R > 0 ? R : 1));
   o->total = off;
   o->NB = (int32_t)NB;
   o->tile = tile;
@@ -1319,10 +1354,8 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   a.host_cnt = reinterpret_cast<int32_t *>(ws + lay.host_cnt);
   a.host_list = reinterpret_cast<int32_t *>(ws + lay.host_list);
   a.recs = reinterpret_cast<HostRec *>(ws + lay.recs);
-  a.perm = reinterpret_cast<int32_t *>(ws + lay.perm);
+  a.preq = reinterpret_cast<ReqRec *>(ws + lay.preq);
   a.key = reinterpret_cast<int32_t *>(ws + lay.key);
-  a.row = reinterpret_cast<int32_t *>(ws + lay.row);
-  a.lout = reinterpret_cast<float *>(ws + lay.lout);
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int zb = (lay.NB + 255) / 256;
@@ -1346,10 +1379,11 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   hipError_t e = mark(0, st);
   if (e != hipSuccess) return FESTINA_ERR_DEVICE;
   if (lay.fast) {
+    const int grid = (lay.max_tiles + kXcds - 1) / kXcds * kXcds;
     if (wpb == 4)
-      k_score_c128<4><<<lay.max_tiles, 4 * kWave, lds, st>>>(a);
+      k_score_c128<4><<<grid, 4 * kWave, lds, st>>>(a);
     else
-      k_score_c128<1><<<lay.max_tiles, kWave, lds, st>>>(a);
+      k_score_c128<1><<<grid, kWave, lds, st>>>(a);
     e = hipGetLastError();
   } else if (cpl == 1)
     e = launch_score<1>(a, lay.max_tiles, wpb, lds, st);
