@@ -243,3 +243,28 @@ def test_fast_kernel_mixed_slo_groups():
     inp = W.make_placement(3, n_requests=4099)
     inp["requests"]["slo_tbt_ms"][::3] *= np.float32(1.5)
     parity_place(inp, label="cfg3 mixed TBT SLOs")
+
+
+def test_fast_kernel_more_hosts_than_one_lds_chunk():
+    """8x16 tables with > 256 hosting GPUs per model: host records are staged in several
+    chunks and pass 2 reads them from global memory."""
+    rng = np.random.default_rng(606)
+    inp = W.make_tiny_placement(rng, R=203, G=700, M=2, NS=8, NF=16, W=2, caps=True)
+    hosts = [int(((inp["gpus"]["resident"][:, 0] >> m) & 1).sum()) for m in range(2)]
+    assert max(hosts) > 256
+    parity_place(inp, label=f"8x16 with {hosts} hosts per model")
+
+
+def test_generic_kernel_four_waves_per_block():
+    rng = np.random.default_rng(607)
+    inp = W.make_tiny_placement(rng, R=20011, G=50, M=3, NS=4, NF=6, W=2, caps=True)
+    sel = np.random.default_rng(1).choice(20011, 3000, replace=False)
+    parity_place(inp, sel, label="4x6 tables, 20011 requests")
+
+
+def test_fast_kernel_promptless_four_waves_per_block():
+    rng = np.random.default_rng(608)
+    inp = W.make_tiny_placement(rng, R=40009, G=40, M=3, NS=8, NF=16, W=3, caps=False)
+    assert (inp["requests"]["prompt_tokens"] == 0).mean() > 0.2
+    sel = np.random.default_rng(2).choice(40009, 3000, replace=False)
+    parity_place(inp, sel, label="8x16 tables, 40009 requests, 30% without prompt")
