@@ -82,7 +82,8 @@ struct PlaceArgs {
   int32_t NB;                    // buckets = 2 * W * M
   int32_t tile;                  // requests per tile
   int32_t max_tiles;
-  int32_t *cnt;                  // [NB] counters, then scatter cursors
+  int32_t *cnt;                  // [NB4] counters (cursors too when NB > kHistMax)
+  int32_t *cur;                  // [NB4] scatter cursors, from zero (NB <= kHistMax)
   int32_t *bstart;               // [NB + 1]
   int32_t *n_tiles;              // [1]
   int2 *tiles;                   // [max_tiles] {bucket, first position}
@@ -333,39 +334,111 @@ __device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
   return q;
 }
 
-// Requests grouped by bucket: each block ranks its requests per bucket in LDS, reserves
-// one range per non-empty bucket with a global atomic, then writes the permutation.
+// Exclusive scans of the bucket counts (requests and tiles) inside one block of k_scatter,
+// into the LDS array `start`.  Thread t holds buckets [t*per, t*per + per), per a multiple
+// of 4 (at most 32), read as up to 8 int4 loads that are all in flight before the first use;
+// the counter array is padded to a multiple of 4 with zeros.  Every block scans all buckets
+// (a few KB from L2); bucket i's global start and tiles are written by block i mod grid, so
+// the tile table is spread over the grid, and block 0 writes the totals.
+__device__ void block_scan_buckets(const PlaceArgs &a, int *start) {
+  __shared__ int s_c[kPrepBlock / kWave];
+  __shared__ int s_t[kPrepBlock / kWave];
+  constexpr int V = kHistMax / kPrepBlock / 4;
+  const int per = (((a.NB + kPrepBlock - 1) / kPrepBlock) + 3) & ~3;
+  const int lo = min((int)threadIdx.x * per, a.NB);
+  const int hi = min(lo + per, a.NB);
+  const v4i *c4 = reinterpret_cast<const v4i *>(a.cnt + lo);
+  v4i v[V];
+#pragma unroll
+  for (int q = 0; q < V; ++q) v[q] = lo + 4 * q < hi ? c4[q] : v4i{0, 0, 0, 0};
+  int c = 0, t = 0;
+#pragma unroll
+  for (int q = 0; q < V; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int n = v[q][e];
+      c += n;
+      t += (n + a.tile - 1) / a.tile;
+    }
+  const int ic = wave_scan(c), it = wave_scan(t);
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  if (lane == kWave - 1) {
+    s_c[wv] = ic;
+    s_t[wv] = it;
+  }
+  __syncthreads();
+  int pc = ic - c, pt = it - t;
+  int tot_c = 0, tot_t = 0;
+  for (int i = 0; i < kPrepBlock / kWave; ++i) {
+    if (i < wv) {
+      pc += s_c[i];
+      pt += s_t[i];
+    }
+    tot_c += s_c[i];
+    tot_t += s_t[i];
+  }
+#pragma unroll
+  for (int q = 0; q < V; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = lo + 4 * q + e;
+      if (i < hi) {
+        const int n = v[q][e];
+        const int nt = (n + a.tile - 1) / a.tile;
+        start[i] = pc;
+        if (i % (int)gridDim.x == (int)blockIdx.x) {
+          a.bstart[i] = pc;
+          for (int k = 0; k < nt; ++k) a.tiles[pt + k] = make_int2(i, pc + k * a.tile);
+        }
+        pc += n;
+        pt += nt;
+      }
+    }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    a.bstart[a.NB] = tot_c;
+    *a.n_tiles = tot_t;
+  }
+  __syncthreads();
+}
+
+// Requests grouped by bucket.  With at most kHistMax buckets, each block scans the bucket
+// counts itself (dynamic LDS: ranks [NB], starts [NB]), ranks its requests per bucket in
+// LDS, reserves one range per non-empty bucket with an atomic on a zeroed cursor, then
+// writes the permutation.  With more buckets, k_scan has turned the counters into
+// cursors and every request takes its slot with a global atomic.
 __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
-  __shared__ int hist[kHistMax];
+  extern __shared__ int sl[];
   constexpr int U = kReqPerPrepBlock / kPrepBlock;
   const bool local = a.NB <= kHistMax;
+  int *hist = sl, *start = sl + a.NB;
   int key[U], rank[U];
-  if (local) {
-    for (int k = threadIdx.x; k < a.NB; k += kPrepBlock) hist[k] = 0;
-    __syncthreads();
-  }
+  ReqRec rec[U];
+  // request loads first, so that their latency overlaps the bucket scan
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int r = blockIdx.x * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
     key[u] = r < a.R ? a.key[r] : -1;
     rank[u] = 0;
-    if (key[u] >= 0) {
-      if (local)
-        rank[u] = atomicAdd(&hist[key[u]], 1);
-      else
-        a.preq[atomicAdd(&a.cnt[key[u]], 1)] = make_req_rec(a, r);
-    }
+    if (key[u] >= 0) rec[u] = make_req_rec(a, r);
   }
-  if (!local) return;
+  if (!local) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (key[u] >= 0) a.preq[atomicAdd(&a.cnt[key[u]], 1)] = rec[u];
+    return;
+  }
+  for (int k = threadIdx.x; k < a.NB; k += kPrepBlock) hist[k] = 0;
+  block_scan_buckets(a, start);        // ends with a barrier
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (key[u] >= 0) rank[u] = atomicAdd(&hist[key[u]], 1);
   __syncthreads();
   for (int k = threadIdx.x; k < a.NB; k += kPrepBlock)
-    if (hist[k]) hist[k] = atomicAdd(&a.cnt[k], hist[k]);
+    if (hist[k]) hist[k] = start[k] + atomicAdd(&a.cur[k], hist[k]);
   __syncthreads();
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int r = blockIdx.x * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
-    if (key[u] >= 0) a.preq[hist[key[u]] + rank[u]] = make_req_rec(a, r);
-  }
+  for (int u = 0; u < U; ++u)
+    if (key[u] >= 0) a.preq[hist[key[u]] + rank[u]] = rec[u];
 }
 
 // ------------------------------------------------------------------ scoring kernel
@@ -1059,8 +1132,8 @@ struct MigArgs {
   int32_t *best_dst;
   float *saving;
   int32_t *level;
-  uint32_t *fm;                  // [G] feasible-level masks
-  float *base;                   // [G] f[kd0]^3 * u_d
+  v4i *drec;                     // [G][2] destination records from k_fleet:
+                                 // {hbm, SM per-mille, level mask, k_d}, {u, f[kd0]^3 * u, 0, 0}
 };
 
 // One wavefront per GPU: lane k tests frequency level k (NF <= 32) for each instance, a
@@ -1088,16 +1161,18 @@ __global__ void __launch_bounds__(256) k_fleet(MigArgs a) {
     fm &= (uint32_t)__ballot(pass);
   }
   if (lane == 0) {
-    a.fm[g] = fm;
-    a.base[g] = fm ? cube(a.freq_level[__builtin_ctz(fm)]) * a.util[g] : 0.f;
+    const float u = a.util[g];
+    const float base = fm ? cube(a.freq_level[__builtin_ctz(fm)]) * u : 0.f;
+    a.drec[2 * g] = v4i{a.hbm[g], a.smpm[g], (int)fm, __float_as_int(a.kdyn[g])};
+    a.drec[2 * g + 1] = v4i{__float_as_int(u), __float_as_int(base), 0, 0};
   }
 }
 
 constexpr int kSrcPerWave = 2;
 constexpr int kMigChunk = 2048;   // destination records staged in LDS per pass
 
-// Two sources per wavefront, four wavefronts per block; destination records are staged in
-// LDS in chunks (one coalesced pass over the fleet per block), lanes span destinations.
+// Two sources per wavefront, four wavefronts per block; the 32-byte destination records are
+// staged in LDS in chunks (all of a thread's loads in flight at once), lanes span destinations.
 __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
   __shared__ float f3[32];
   __shared__ int4 drec[kMigChunk];       // hbm, SM per-mille, level mask, k_d
@@ -1120,8 +1195,9 @@ __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
     any[q] = v && rh >= (long long)INT_MIN && ru >= (long long)INT_MIN;
     remH[q] = (int)(rh > INT_MAX ? INT_MAX : (rh < INT_MIN ? INT_MIN : rh));
     remU[q] = (int)(ru > INT_MAX ? INT_MAX : (ru < INT_MIN ? INT_MIN : ru));
-    fms[q] = v ? a.fm[s] : 0u;
-    us[q] = a.util[s];
+    const v4i x = a.drec[2 * s], y = a.drec[2 * s + 1];
+    fms[q] = v ? (uint32_t)x.z : 0u;
+    us[q] = __int_as_float(y.x);
   }
   float bs[kSrcPerWave];
   int bd[kSrcPerWave], bk[kSrcPerWave];
@@ -1134,10 +1210,23 @@ __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
   for (int d0 = 0; d0 < a.G; d0 += kMigChunk) {
     const int n = min(kMigChunk, a.G - d0);
     __syncthreads();
-    for (int i = threadIdx.x; i < n; i += blockDim.x) {
-      const int d = d0 + i;
-      drec[i] = make_int4(a.hbm[d], a.smpm[d], (int)a.fm[d], __float_as_int(a.kdyn[d]));
-      drec2[i] = make_float2(a.util[d], a.base[d]);
+    constexpr int U = kMigChunk / 256;
+    v4i x[U], y[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = u * 256 + threadIdx.x;
+      if (i < n) {
+        x[u] = a.drec[2 * (d0 + i)];
+        y[u] = a.drec[2 * (d0 + i) + 1];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = u * 256 + threadIdx.x;
+      if (i < n) {
+        drec[i] = make_int4(x[u].x, x[u].y, x[u].z, x[u].w);
+        drec2[i] = make_float2(__int_as_float(y[u].x), __int_as_float(y[u].y));
+      }
     }
     __syncthreads();
     if (s0 >= a.G) continue;
@@ -1207,7 +1296,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   const long long M = L->n_models, Gn = G->n_gpus, W = G->n_waves, R = Q->n_requests;
   const long long C = (long long)L->n_sm * L->n_freq;
   const long long NB = 2 * W * M;
-  if (NB > INT_MAX / 2 || Gn * C > INT_MAX || W * Gn > INT_MAX || M * Gn > INT_MAX) return false;
+  if (NB > INT_MAX / 2 - 4 || Gn * C > INT_MAX || W * Gn > INT_MAX || M * Gn > INT_MAX) return false;
   // tile size: large tiles amortise the table staging, small ones fill the chip
   const bool fast = L->n_sm == 8 && L->n_freq == 16;
   int wpb = 4, tile;
@@ -1236,7 +1325,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
     off = align256(off + bytes);
     return at;
   };
-  o->cnt = take(sizeof(int32_t) * NB);
+  o->cnt = take(sizeof(int32_t) * 2 * ((NB + 3) & ~3LL));   // counters, then cursors
   o->bstart = take(sizeof(int32_t) * (NB + 1));
   o->ntiles = take(sizeof(int32_t));
   o->tiles = take(sizeof(int2) * max_tiles);
@@ -1348,6 +1437,8 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   a.tile = lay.tile;
   a.max_tiles = lay.max_tiles;
   a.cnt = reinterpret_cast<int32_t *>(ws + lay.cnt);
+  const int nb4 = (lay.NB + 3) & ~3;      // counters padded with zeros to whole int4
+  a.cur = a.cnt + nb4;
   a.bstart = reinterpret_cast<int32_t *>(ws + lay.bstart);
   a.n_tiles = reinterpret_cast<int32_t *>(ws + lay.ntiles);
   a.tiles = reinterpret_cast<int2 *>(ws + lay.tiles);
@@ -1358,16 +1449,19 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   a.key = reinterpret_cast<int32_t *>(ws + lay.key);
 
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int zb = (lay.NB + 255) / 256;
-  k_zero<<<zb < 1024 ? zb : 1024, 256, 0, st>>>(a.cnt, lay.NB);
+  const int zb = (2 * nb4 + 255) / 256;
+  k_zero<<<zb < 1024 ? zb : 1024, 256, 0, st>>>(a.cnt, 2 * nb4);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int nbr = (a.R + kReqPerPrepBlock - 1) / kReqPerPrepBlock;
   const long long nrec = ((long long)a.W * a.G + kPrepBlock - 1) / kPrepBlock;
   k_prep<<<(unsigned)(nbr + a.M + nrec), kPrepBlock, 0, st>>>(a, nbr);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  k_scan<<<1, 1024, lay.NB <= kScanLds ? sizeof(int) * lay.NB : 0, st>>>(a);
-  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  k_scatter<<<nbr, kPrepBlock, 0, st>>>(a);
+  const bool local = lay.NB <= kHistMax;
+  if (!local) {
+    k_scan<<<1, 1024, lay.NB <= kScanLds ? sizeof(int) * lay.NB : 0, st>>>(a);
+    if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  }
+  k_scatter<<<nbr, kPrepBlock, local ? 2 * sizeof(int) * lay.NB : 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int cpl = C <= 64 ? 1 : (C <= 128 ? 2 : 4);
   const int wpb = lay.waves_per_block;
@@ -1405,7 +1499,7 @@ static bool mig_shapes_ok(const festina_lut *L, const festina_fleet *F) {
 
 size_t festina_migrations_workspace_bytes(const festina_lut *lut, const festina_fleet *fleet) {
   if (!mig_shapes_ok(lut, fleet)) return 0;
-  return align256(sizeof(uint32_t) * fleet->n_gpus) + align256(sizeof(float) * fleet->n_gpus);
+  return align256((size_t)32 * fleet->n_gpus);      // one 32-byte destination record per GPU
 }
 
 festina_status festina_score_migrations(const festina_lut *L, const festina_fleet *F,
@@ -1449,8 +1543,7 @@ festina_status festina_score_migrations(const festina_lut *L, const festina_flee
   a.saving = out->saving_w;
   a.level = out->freq_level;
   char *ws = static_cast<char *>(workspace);
-  a.fm = reinterpret_cast<uint32_t *>(ws);
-  a.base = reinterpret_cast<float *>(ws + align256(sizeof(uint32_t) * F->n_gpus));
+  a.drec = reinterpret_cast<v4i *>(ws);
   hipStream_t st = static_cast<hipStream_t>(stream);
   k_fleet<<<(a.G + 3) / 4, 256, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;

@@ -268,3 +268,13 @@ def test_fast_kernel_promptless_four_waves_per_block():
     assert (inp["requests"]["prompt_tokens"] == 0).mean() > 0.2
     sel = np.random.default_rng(2).choice(40009, 3000, replace=False)
     parity_place(inp, sel, label="8x16 tables, 40009 requests, 30% without prompt")
+
+
+@pytest.mark.parametrize("M,Wn,NS,NF", [(70, 60, 8, 16), (130, 70, 4, 6)])
+def test_more_buckets_than_the_lds_histogram(M, Wn, NS, NF):
+    """2*W*M buckets above 8192 (LDS-staged scan) and above 16384 (global counters): the
+    bucket scan runs in its own kernel and requests take their slots by global atomics."""
+    rng = np.random.default_rng(609 + M)
+    inp = W.make_tiny_placement(rng, R=6007, G=20, M=M, NS=NS, NF=NF, W=Wn, caps=True)
+    assert 2 * M * Wn > 8192
+    parity_place(inp, label=f"{2 * M * Wn} buckets, {NS}x{NF} tables")
