@@ -1,4 +1,5 @@
-"""CPU oracle of the batched energy-aware placement and migration search.
+"""CPU oracle of the batched energy-aware placement and migration search and of the
+local SM/frequency sweep.
 
 TEST INFRASTRUCTURE ONLY: the test suite, the package smoke check and the
 benchmark's CPU-baseline leg are the only callers.  The product path never
@@ -55,6 +56,13 @@ class _Fleet(C.Structure):
                 ("k_dyn_w", C.c_void_p), ("hbm_cap_mib", C.c_int32), ("sm_cap_permille", C.c_int32)]
 
 
+class _Batches(C.Structure):
+    _fields_ = [("n_batches", C.c_int32), ("max_tasks", C.c_int32), ("n_tasks", C.c_void_p),
+                ("task_model", C.c_void_p), ("task_phase", C.c_void_p), ("task_tokens", C.c_void_p),
+                ("task_slack_ms", C.c_void_p), ("k_dyn_w", C.c_void_p), ("util", C.c_void_p),
+                ("sm_units", C.c_void_p), ("sm_budget", C.c_int32)]
+
+
 def lib():
     global _lib
     if _lib is None:
@@ -79,6 +87,14 @@ def lib():
         L.festina_oracle_prompt_row.restype = C.c_int
         L.festina_oracle_padded_out.argtypes = [C.c_int32]
         L.festina_oracle_padded_out.restype = C.c_int64
+        L.festina_oracle_sweep.argtypes = [P(_Lut), P(_Batches), C.c_int32, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.festina_oracle_sweep.restype = C.c_int
+        L.festina_oracle_sweep_level.argtypes = [P(_Lut), P(_Batches), C.c_int32, C.c_int32,
+                                                 P(C.c_double)]
+        L.festina_oracle_sweep_level.restype = C.c_int
+        L.festina_oracle_min_sm.argtypes = [P(_Lut), P(_Batches), C.c_int32, C.c_int32, C.c_int32]
+        L.festina_oracle_min_sm.restype = C.c_int
         _lib = L
     return _lib
 
@@ -133,6 +149,14 @@ def _fleet(d, pin):
                   pin(d["hbm_mib"], np.int32), pin(d["sm_permille"], np.int32),
                   pin(d["util"], np.float32), pin(d["k_dyn_w"], np.float32),
                   int(d["hbm_cap_mib"]), int(d["sm_cap_permille"]))
+
+
+def _batches(d, pin):
+    return _Batches(int(d["n_batches"]), int(d["max_tasks"]), pin(d["n_tasks"], np.int32),
+                    pin(d["task_model"], np.int32), pin(d["task_phase"], np.int32),
+                    pin(d["task_tokens"], np.int32), pin(d["task_slack_ms"], np.float32),
+                    pin(d["k_dyn_w"], np.float32), pin(d["util"], np.float32),
+                    pin(d["sm_units"], np.int32), int(d["sm_budget"]))
 
 
 # ------------------------------------------------------------------ public API
@@ -200,3 +224,40 @@ def prompt_row(tokens: int) -> int:
 
 def padded_out(predicted: int) -> int:
     return int(lib().festina_oracle_padded_out(int(predicted)))
+
+
+def sweep(inp: dict, sel=None):
+    """Oracle local SM/frequency sweep for all batches (or the batch ids in ``sel``).
+
+    Returns (freq_level int32, feasible uint8, energy_mj float64, task_sm int32 [n, max_tasks]).
+    """
+    pin = _Pinned()
+    lut, bat = _lut(inp["lut"], pin), _batches(inp["batches"], pin)
+    n = int(inp["batches"]["n_batches"]) if sel is None else len(sel)
+    T = int(inp["batches"]["max_tasks"])
+    sel_a = None if sel is None else _arr(sel, np.int32)
+    lev = np.empty(n, np.int32)
+    feas = np.empty(n, np.uint8)
+    energy = np.empty(n, np.float64)
+    tsm = np.empty((n, T), np.int32)
+    rc = lib().festina_oracle_sweep(C.byref(lut), C.byref(bat), n, _p(sel_a), _p(lev), _p(feas),
+                                    _p(energy), _p(tsm))
+    if rc != 0:
+        raise ValueError("oracle rejected the sweep arguments")
+    return lev, feas, energy, tsm
+
+
+def sweep_level(inp: dict, b: int, k: int):
+    """(usable, energy_mj) of batch ``b`` at frequency level ``k``."""
+    pin = _Pinned()
+    lut, bat = _lut(inp["lut"], pin), _batches(inp["batches"], pin)
+    e = C.c_double(0.0)
+    ok = lib().festina_oracle_sweep_level(C.byref(lut), C.byref(bat), int(b), int(k), C.byref(e))
+    return bool(ok), float(e.value)
+
+
+def min_sm(inp: dict, b: int, t: int, k: int) -> int:
+    """Smallest SM level at which task ``t`` of batch ``b`` meets its slack at level ``k`` (-1: none)."""
+    pin = _Pinned()
+    lut, bat = _lut(inp["lut"], pin), _batches(inp["batches"], pin)
+    return int(lib().festina_oracle_min_sm(C.byref(lut), C.byref(bat), int(b), int(t), int(k)))

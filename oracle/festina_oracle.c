@@ -32,6 +32,15 @@
  *     saving = P0 - k_d * (f[k*]^3 * (u_s + u_d) - f[kd0]^3 * u_d), where kd0 is d's own
  *     lowest feasible level.  Per source: the largest saving, lowest d on exact ties.
  *
+ *   local SM/frequency sweep (Sec. 3.4, runtime resource allocation):
+ *     for every batch of tasks and every frequency level k: each task takes the smallest
+ *     SM level whose latency (PF row for a prefill unit, DC row for a decode step) is
+ *     strictly below its slack; k is usable when every task has one and the integer SM
+ *     shares sum to strictly less than the device budget; energy at k =
+ *        sum over tasks of (P0 + k_dyn * s_j * f_k^3 * u) * latency
+ *     (Power x Latency per task, the placement power model); the least-energy usable k
+ *     wins, the lowest k on exact ties.
+ *
  * Request pre-processing (Sec. 3.2.1 input-length axis 256..8192; Sec. 3.2.2 / 3.3 the
  * 5% output-length safety pad):
  *   Lout = ceil(1.05 * predicted_out)            (integer: (105*L + 99) / 100)
@@ -278,6 +287,126 @@ int festina_oracle_score_migrations(const or_lut *L, const or_fleet *F, int32_t 
     best_dst[i] = bd;
     saving_w[i] = bd >= 0 ? bs : -INFINITY;
     freq_level[i] = bk;
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------- local SM/frequency sweep */
+/* Sec. 3.4, "Runtime Resource Allocation": a local scheduler holds a batch of tasks
+ * (prefill units and decode steps) and picks one GPU frequency level for the batch.  At
+ * each level k, every task takes the smallest SM level whose profiled latency is strictly
+ * below the task's remaining slack; the level is usable only when every task has such an
+ * SM level and the SM shares sum to strictly less than the device budget ("< 100%");
+ * the batch's energy at k is the sum over its tasks of Power x Latency with the same
+ * closed-form power model as placement, P = P0 + k_dyn * s * f^3 * u.  The chosen level
+ * is the least-energy usable one, the lowest k on exact ties. */
+typedef struct {
+  int32_t n_batches, max_tasks;
+  const int32_t *n_tasks;        /* [B] */
+  const int32_t *task_model;     /* [B][T] */
+  const int32_t *task_phase;     /* [B][T] 0 = prefill (PF table), 1 = decode (DC table) */
+  const int32_t *task_tokens;    /* [B][T] prompt tokens (prefill) or decode batch size */
+  const float *task_slack_ms;    /* [B][T] */
+  const float *k_dyn_w;          /* [B] */
+  const float *util;             /* [B] */
+  const int32_t *sm_units;       /* [NS] integer SM share of each level */
+  int32_t sm_budget;
+} or_batches;
+
+/* Table row of task t of batch b, or -1 when the task is invalid.  Prefill rows are the
+ * 256-token prompt buckets; decode rows are batch sizes 1..32 (row = size - 1). */
+static int or_task_row(const or_lut *L, const or_batches *S, int b, int t) {
+  const size_t at = (size_t)b * S->max_tasks + (size_t)t;
+  const int m = S->task_model[at], ph = S->task_phase[at];
+  const int32_t tok = S->task_tokens[at];
+  if (m < 0 || m >= L->n_models || tok < 1) return -1;
+  if (ph == 0) return or_prompt_row(tok);
+  if (ph == 1) return (tok > OR_ROWS ? OR_ROWS : tok) - 1;
+  return -1;
+}
+
+static float or_task_latency(const or_lut *L, const or_batches *S, int b, int t, int row, int j, int k) {
+  const size_t at = (size_t)b * S->max_tasks + (size_t)t;
+  const int m = S->task_model[at];
+  const float *tab = S->task_phase[at] == 0 ? L->pf : L->dc;
+  return tab[or_cell(L, m, row, j, k)];
+}
+
+/* Smallest SM level at which task t meets its slack at frequency level k; -1 if none. */
+static int or_min_sm(const or_lut *L, const or_batches *S, int b, int t, int k) {
+  const int row = or_task_row(L, S, b, t);
+  if (row < 0) return -1;
+  const float slack = S->task_slack_ms[(size_t)b * S->max_tasks + (size_t)t];
+  for (int j = 0; j < L->n_sm; ++j)
+    if (or_task_latency(L, S, b, t, row, j, k) < slack) return j;
+  return -1;
+}
+
+static int or_batch_ok(const or_lut *L, const or_batches *S, int b) {
+  const int n = S->n_tasks[b];
+  if (n < 0 || n > S->max_tasks) return 0;
+  for (int t = 0; t < n; ++t)
+    if (or_task_row(L, S, b, t) < 0) return 0;
+  return 1;
+}
+
+/* Energy of batch b at frequency level k: 1 and *energy when level k is usable. */
+static int or_sweep_level(const or_lut *L, const or_batches *S, int b, int k, double *energy) {
+  if (b < 0 || b >= S->n_batches || k < 0 || k >= L->n_freq || !or_batch_ok(L, S, b)) return 0;
+  const double f3 = or_cube((double)L->freq_level[k]);
+  const double kg = (double)S->k_dyn_w[b], u = (double)S->util[b];
+  int64_t units = 0;
+  double E = 0.0;
+  for (int t = 0; t < S->n_tasks[b]; ++t) {
+    const int j = or_min_sm(L, S, b, t, k);
+    if (j < 0) return 0;
+    units += S->sm_units[j];
+    const double lat = (double)or_task_latency(L, S, b, t, or_task_row(L, S, b, t), j, k);
+    const double P = L->p0_w + kg * (double)L->sm_level[j] * f3 * u;
+    E += P * lat;
+  }
+  if (!(units < (int64_t)S->sm_budget)) return 0;
+  if (!((float)E < INFINITY)) return 0;
+  *energy = E;
+  return 1;
+}
+
+int festina_oracle_sweep_level(const or_lut *L, const or_batches *S, int32_t b, int32_t k, double *energy) {
+  if (!or_lut_ok(L) || !S || !energy) return 0;
+  return or_sweep_level(L, S, b, k, energy);
+}
+
+int festina_oracle_min_sm(const or_lut *L, const or_batches *S, int32_t b, int32_t t, int32_t k) {
+  if (!or_lut_ok(L) || !S || b < 0 || b >= S->n_batches || t < 0 || t >= S->max_tasks) return -1;
+  if (k < 0 || k >= L->n_freq) return -1;
+  return or_min_sm(L, S, b, t, k);
+}
+
+/* Sweep batches sel[0..n_sel) (all when sel == NULL).  Output i belongs to batch sel[i];
+ * task_sm is [n][max_tasks]: each task's SM level at the chosen frequency level, -1 for
+ * slots past n_tasks and for batches with no usable level. */
+int festina_oracle_sweep(const or_lut *L, const or_batches *S, int32_t n_sel, const int32_t *sel,
+                         int32_t *freq_level, uint8_t *feasible, double *energy_mj, int32_t *task_sm) {
+  if (!or_lut_ok(L) || !S || !freq_level || !feasible || !energy_mj || !task_sm) return 1;
+  if (S->n_batches < 0 || S->max_tasks < 1 || !S->sm_units) return 1;
+  const int32_t n = sel ? n_sel : S->n_batches;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t b = sel ? sel[i] : i;
+    int32_t bk = -1;
+    double be = INFINITY;
+    for (int k = 0; k < L->n_freq; ++k) {
+      double e;
+      if (!or_sweep_level(L, S, b, k, &e)) continue;
+      if (bk < 0 || e < be) {
+        bk = k;
+        be = e;
+      }
+    }
+    freq_level[i] = bk;
+    feasible[i] = bk >= 0 ? 1 : 0;
+    energy_mj[i] = bk >= 0 ? be : INFINITY;
+    for (int t = 0; t < S->max_tasks; ++t)
+      task_sm[(size_t)i * S->max_tasks + (size_t)t] = (bk >= 0 && t < S->n_tasks[b]) ? or_min_sm(L, S, b, t, bk) : -1;
   }
   return 0;
 }

@@ -346,3 +346,109 @@ def make_tiny_fleet(rng: np.random.Generator, G=None, M=None, NS=None, NF=None,
              "hbm_cap_mib": (1 << 30) if huge_budget else HBM_CAP_MIB,
              "sm_cap_permille": (1 << 30) if huge_budget else SM_CAP_PERMILLE}
     return {"lut": lut, "fleet": fleet, "meta": {}}
+
+
+# --------------------------------------------------------------------------- local sweep
+SWEEP_SEED = CONFIG_SEED_BASE + 50
+SWEEP_MAX_TASKS = 8
+PREFILL_CHUNK = 2048      # tokens per prefill unit in the sweep workload
+
+
+def sm_permille(s: np.ndarray) -> np.ndarray:
+    """Integer SM share of each level in per-mille of the device (125 per eighth)."""
+    return np.rint(1000.0 * s.astype(np.float64)).astype(np.int32)
+
+
+def make_sweep(seed: int | None = None, n_gpus: int = 1024, n_epochs: int = 64,
+               max_tasks: int = SWEEP_MAX_TASKS) -> dict:
+    """Batches for the local SM/frequency sweep: one batch per (epoch, GPU).
+
+    Tables as configuration 3 (32 models, 8 SM x 16 frequency levels, +-5% noise).  Each
+    GPU hosts 1-4 distinct models and has k ~ U(300, 500).  Per epoch, each hosted model
+    has a decode step in the batch with probability 0.7 (decode batch size
+    min(Poisson(4) + 1, 32)), and Poisson(0.7) prefill units of hosted models join: a
+    prompt from configuration 4's bimodal law (70% lognormal mu=5, 30% mu=8), prefilled in
+    chunks of at most 2048 tokens; tasks past max_tasks are dropped.  Slack: decode TBT
+    SLO x U(0.9, 1); prefill TTFT SLO x U(0.7, 1).  Utilisation u = min(1, total decode batch / 32).  SM shares in per-mille,
+    device budget 1000.
+    """
+    if seed is None:
+        seed = SWEEP_SEED
+    rng = np.random.default_rng(seed)
+    M, NS, NF, G, E, T = 32, 8, 16, int(n_gpus), int(n_epochs), int(max_tasks)
+    s, f = sm_levels(NS), freq_levels(NF)
+    a, c, cp = _latency_params(rng, M, prefill=True)
+    pf, dc = _tables(rng, M, s, f, a, c, cp, noise=True)
+    lut = _lut(pf, dc, s, f)
+    slo_m_ttft = rng.choice(TTFT_SLO_SET, M)
+    slo_m_tbt = rng.choice(TBT_SLO_SET, M)
+    nres = rng.integers(1, 5, size=G)
+    models_per_gpu = _distinct_models(rng, G, M, nres)
+    kdyn_g = rng.uniform(300.0, 500.0, G).astype(np.float32)
+
+    B = E * G
+    n_tasks = np.zeros(B, np.int32)
+    model = np.zeros((B, T), np.int32)
+    phase = np.zeros((B, T), np.int32)
+    tokens = np.zeros((B, T), np.int32)
+    slack = np.zeros((B, T), np.float32)
+    util = np.zeros(B, np.float32)
+    kdyn = np.tile(kdyn_g, E)
+    dec_on = rng.random((E, G, MAX_INST)) < 0.7
+    dec_b = np.minimum(rng.poisson(4.0, (E, G, MAX_INST)) + 1, N_ROWS)
+    n_pre = rng.poisson(0.7, (E, G))
+    for e in range(E):
+        for g in range(G):
+            b = e * G + g
+            ms = models_per_gpu[g]
+            t = 0
+            tot = 0
+            for i, mm in enumerate(ms):
+                if dec_on[e, g, i] and t < T:
+                    model[b, t], phase[b, t], tokens[b, t] = mm, 1, dec_b[e, g, i]
+                    slack[b, t] = slo_m_tbt[mm] * rng.uniform(0.9, 1.0)
+                    tot += int(dec_b[e, g, i])
+                    t += 1
+            for _ in range(int(n_pre[e, g])):
+                mm = ms[int(rng.integers(0, len(ms)))]
+                mu = 8.0 if rng.random() < 0.3 else 5.0
+                tok = min(int(np.clip(np.rint(rng.lognormal(mu, 1.0)), 16, 8192)), PREFILL_CHUNK)
+                sl = slo_m_ttft[mm] * rng.uniform(0.7, 1.0)
+                if t < T:
+                    model[b, t], phase[b, t], tokens[b, t], slack[b, t] = mm, 0, tok, sl
+                    t += 1
+            n_tasks[b] = t
+            util[b] = min(1.0, tot / 32.0)
+    batches = {"n_batches": B, "max_tasks": T, "n_tasks": n_tasks, "task_model": model,
+               "task_phase": phase, "task_tokens": tokens, "task_slack_ms": slack,
+               "k_dyn_w": kdyn, "util": util, "sm_units": sm_permille(s), "sm_budget": 1000}
+    meta = {"seed": seed, "n_gpus": G, "n_epochs": E, "models_per_gpu": models_per_gpu}
+    return {"lut": lut, "batches": batches, "meta": meta}
+
+
+def make_tiny_sweep(rng: np.random.Generator, B=None, T=None, M=None, NS=None, NF=None,
+                    nan_cells=False, zero_power=False) -> dict:
+    """Small random sweep instance for pins and parity edge cases."""
+    B = int(rng.integers(1, 6)) if B is None else B
+    T = int(rng.integers(1, 5)) if T is None else T
+    M = int(rng.integers(1, 4)) if M is None else M
+    NS = int(rng.integers(1, 5)) if NS is None else NS
+    NF = int(rng.integers(1, 7)) if NF is None else NF
+    s, f = sm_levels(NS), freq_levels(NF)
+    pf = rng.uniform(5.0, 60.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    dc = rng.uniform(2.0, 40.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    if nan_cells:
+        pf[rng.random(pf.shape) < 0.1] = np.nan
+        dc[rng.random(dc.shape) < 0.05] = np.inf
+    lut = _lut(pf, dc, s, f, p0=0.0 if zero_power else float(rng.uniform(0.0, 150.0)))
+    n_tasks = rng.integers(0, T + 1, B).astype(np.int32)
+    units = sm_permille(s)
+    batches = {"n_batches": B, "max_tasks": T, "n_tasks": n_tasks,
+               "task_model": rng.integers(0, M, (B, T)).astype(np.int32),
+               "task_phase": rng.integers(0, 2, (B, T)).astype(np.int32),
+               "task_tokens": rng.integers(1, 9000, (B, T)).astype(np.int32),
+               "task_slack_ms": rng.uniform(3.0, 60.0, (B, T)).astype(np.float32),
+               "k_dyn_w": (np.zeros(B) if zero_power else rng.uniform(0.0, 500.0, B)).astype(np.float32),
+               "util": rng.uniform(0.0, 1.0, B).astype(np.float32),
+               "sm_units": units, "sm_budget": int(rng.integers(1, 1000 * T + 2))}
+    return {"lut": lut, "batches": batches, "meta": {}}

@@ -151,3 +151,69 @@ def brute_migrations(inp):
             sv, d, k = min(p, key=lambda t: (-t[0], t[1]))
             best[s], sav[s], lev[s] = d, sv, k
     return best, sav, lev
+
+
+# ------------------------------------------------------------------ local sweep
+def task_rows(inp, b):
+    """Table and row of each task of batch b, or None when the batch holds an invalid task."""
+    lut, bt = inp["lut"], inp["batches"]
+    n = int(bt["n_tasks"][b])
+    if not 0 <= n <= bt["max_tasks"]:
+        return None
+    out = []
+    for t in range(n):
+        m, ph, tok = int(bt["task_model"][b, t]), int(bt["task_phase"][b, t]), int(bt["task_tokens"][b, t])
+        if not 0 <= m < lut["n_models"] or tok < 1 or ph not in (0, 1):
+            return None
+        if ph == 0:
+            out.append((lut["pf"], m, prompt_row(tok)))
+        else:
+            out.append((lut["dc"], m, min(tok, 32) - 1))
+    return out
+
+
+def sweep_levels(inp, b):
+    """All (energy, k, assignment) of usable frequency levels of batch b.
+
+    Every SM assignment that meets all slacks is listed; the per-task minimum SM level is
+    the componentwise minimum of that list, and the level is usable when that
+    assignment's integer SM shares sum to less than the budget.
+    """
+    lut, bt = inp["lut"], inp["batches"]
+    NS, NF = lut["n_sm"], lut["n_freq"]
+    rows = task_rows(inp, b)
+    if rows is None:
+        return []
+    n = len(rows)
+    out = []
+    for k in range(NF):
+        ok = [a for a in itertools.product(range(NS), repeat=n)
+              if all(tab[m, row, a[t], k] < bt["task_slack_ms"][b, t] for t, (tab, m, row) in enumerate(rows))]
+        if not ok:
+            continue
+        assign = tuple(min(a[t] for a in ok) for t in range(n))
+        if not sum(int(bt["sm_units"][j]) for j in assign) < int(bt["sm_budget"]):
+            continue
+        f = float(lut["freq_level"][k])
+        e = sum(power(lut["p0_w"], float(bt["k_dyn_w"][b]), float(lut["sm_level"][assign[t]]), f,
+                      float(bt["util"][b])) * float(tab[m, row, assign[t], k])
+                for t, (tab, m, row) in enumerate(rows))
+        if not np.float32(e) < np.inf:
+            continue
+        out.append((e, k, assign))
+    return out
+
+
+def brute_sweep(inp):
+    bt = inp["batches"]
+    B, T = bt["n_batches"], bt["max_tasks"]
+    lev = np.full(B, -1, np.int32)
+    energy = np.full(B, np.inf)
+    tsm = np.full((B, T), -1, np.int32)
+    for b in range(B):
+        c = sweep_levels(inp, b)
+        if c:
+            e, k, a = min(c)
+            lev[b], energy[b] = k, e
+            tsm[b, :len(a)] = a
+    return lev, (lev >= 0).astype(np.uint8), energy, tsm

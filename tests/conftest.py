@@ -92,3 +92,32 @@ def golden_migration():
 @pytest.fixture
 def rng():
     return np.random.default_rng(12345)
+
+
+def golden_sweep(variant=None):
+    """Inputs of the hand-worked sweep example (optionally one of its variants by name)."""
+    d = load_golden("sweep_worked_example.json")
+    spec = dict(d["lut"])
+    bt = dict(d["batch"])
+    exp = d["expected"]
+    slack = [t["slack_ms"] for t in bt["tasks"]]
+    if variant is not None:
+        v = [x for x in d["variants"] if x["name"] == variant][0]
+        ch = v["change"]
+        if "p0_w" in ch:
+            spec["p0_w"] = ch["p0_w"]
+        bt["sm_units"] = ch.get("sm_units", bt["sm_units"])
+        bt["sm_budget"] = ch.get("sm_budget", bt["sm_budget"])
+        slack = ch.get("slack_ms", slack)
+        exp = v["expected"]
+    lut = _tables(spec)
+    T = len(bt["tasks"])
+    batches = {"n_batches": 1, "max_tasks": T, "n_tasks": np.array([T], np.int32),
+               "task_model": np.array([[t["model"] for t in bt["tasks"]]], np.int32),
+               "task_phase": np.array([[t["phase"] for t in bt["tasks"]]], np.int32),
+               "task_tokens": np.array([[t["tokens"] for t in bt["tasks"]]], np.int32),
+               "task_slack_ms": np.array([slack], np.float32),
+               "k_dyn_w": np.array([bt["k_dyn_w"]], np.float32),
+               "util": np.array([bt["util"]], np.float32),
+               "sm_units": np.array(bt["sm_units"], np.int32), "sm_budget": int(bt["sm_budget"])}
+    return {"lut": lut, "batches": batches}, exp, d

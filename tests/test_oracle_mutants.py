@@ -49,6 +49,29 @@ MIGRATION = [
 ]
 
 
+SWEEP = [
+    ("inclusive slack test", "if (or_task_latency(L, S, b, t, row, j, k) < slack) return j;",
+     "if (or_task_latency(L, S, b, t, row, j, k) <= slack) return j;"),
+    ("inclusive SM budget", "if (!(units < (int64_t)S->sm_budget)) return 0;",
+     "if (!(units <= (int64_t)S->sm_budget)) return 0;"),
+    ("dropped static power", "const double P = L->p0_w + kg * (double)L->sm_level[j] * f3 * u;",
+     "const double P = kg * (double)L->sm_level[j] * f3 * u;"),
+    ("utilisation dropped", "const double P = L->p0_w + kg * (double)L->sm_level[j] * f3 * u;",
+     "const double P = L->p0_w + kg * (double)L->sm_level[j] * f3;"),
+    ("f instead of f^3", "const double f3 = or_cube((double)L->freq_level[k]);\n  const double kg = (double)S->k_dyn_w[b]",
+     "const double f3 = (double)L->freq_level[k];\n  const double kg = (double)S->k_dyn_w[b]"),
+    ("decode reads the prefill table", "const float *tab = S->task_phase[at] == 0 ? L->pf : L->dc;",
+     "const float *tab = L->pf;"),
+    ("largest SM level instead of smallest",
+     "for (int j = 0; j < L->n_sm; ++j)\n    if (or_task_latency",
+     "for (int j = L->n_sm - 1; j >= 0; --j)\n    if (or_task_latency"),
+    ("decode row off by one", "if (ph == 1) return (tok > OR_ROWS ? OR_ROWS : tok) - 1;",
+     "if (ph == 1) return tok >= OR_ROWS ? OR_ROWS - 1 : tok;"),
+    ("longest task instead of the sum", "    E += P * lat;", "    E = E > P * lat ? E : P * lat;"),
+    ("highest level wins ties", "if (bk < 0 || e < be) {", "if (bk < 0 || e <= be) {"),
+]
+
+
 def _run_pins(tmp_path, name, old, new, suite):
     src = open(SRC).read()
     assert src.count(old) == 1, f"mutation anchor not unique/present: {name}"
@@ -73,4 +96,10 @@ def test_placement_pins_reject_mutant(tmp_path, name, old, new):
 @pytest.mark.parametrize("name,old,new", MIGRATION, ids=[p[0] for p in MIGRATION])
 def test_migration_pins_reject_mutant(tmp_path, name, old, new):
     rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_migration_pins.py")
+    assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
+
+
+@pytest.mark.parametrize("name,old,new", SWEEP, ids=[p[0] for p in SWEEP])
+def test_sweep_pins_reject_mutant(tmp_path, name, old, new):
+    rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_sweep_pins.py")
     assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
