@@ -18,8 +18,8 @@ SRC = os.path.join(ROOT, "oracle", "festina_oracle.c")
 PLACEMENT = [
     ("dropped decode term", "const double E = Pp * (double)ttft + Lout * Pd * (double)tbt;",
      "const double E = Pp * (double)ttft;"),
-    ("f instead of f^3", "const double f3 = or_cube((double)L->freq_level[k]);",
-     "const double f3 = (double)L->freq_level[k];"),
+    ("f instead of f^3", "const double f3 = or_cube((double)L->freq_level[k]);\n  const double kg = (double)G->k_dyn_w[g];",
+     "const double f3 = (double)L->freq_level[k];\n  const double kg = (double)G->k_dyn_w[g];"),
     ("inclusive SLO test", "if (!(ttft < Q->slo_ttft_ms[r] && tbt < Q->slo_tbt_ms[r])) return 0;",
      "if (!(ttft <= Q->slo_ttft_ms[r] && tbt <= Q->slo_tbt_ms[r])) return 0;"),
     ("pre-admission batch in u", "const double u = (double)b / 32.0;", "const double u = (double)B / 32.0;"),
