@@ -14,7 +14,9 @@ candidate evaluations per second (placement candidates plus migration pairs).
 
 Also reported: the roofline position of the dominant kernel (placement scoring,
 timed alone with HIP events recorded around it inside the library), and the CPU
-oracle timed on a bounded sample of the same workload on this host.
+oracle timed on a bounded sample of the same workload on this host.  Outside the
+timed steps, ``next_rows`` measures the local schedulers' SM/frequency sweep over
+1,024 GPUs x 64 epochs of task batches (one kernel per call) the same way.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --per-config     (one JSON line per configuration, then the step line)
@@ -52,6 +54,12 @@ OPS_PER_PAIR = 15
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_score_config4_traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "festina.hip")
+SWEEP_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sweep_traffic.json")
+SWEEP_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "sweep.hip")
+# Sweep, per (task, SM level, frequency level) cell: one compare of the latency with the
+# slack; per (task, frequency level): the SM share add and two FMAs (power, energy).
+OPS_PER_SWEEP_CELL = 1
+OPS_PER_SWEEP_TASK_LEVEL = 3
 
 
 # ------------------------------------------------------------------ HIP events (ctypes)
@@ -62,6 +70,7 @@ class Hip:
         self.L.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
         self.L.hipEventSynchronize.argtypes = [C.c_void_p]
         self.L.hipEventDestroy.argtypes = [C.c_void_p]
+        self.L.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
 
     # timing-only events: no system-scope fence (cache writeback/invalidate) on record
     DISABLE_SYSTEM_FENCE = 0x20000000
@@ -83,6 +92,11 @@ class Hip:
 
     def destroy(self, e):
         self.L.hipEventDestroy(C.c_void_p(e))
+
+    def record(self, e, stream):
+        rc = self.L.hipEventRecord(C.c_void_p(e), C.c_void_p(stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
 
 
 # ------------------------------------------------------------------ work counts
@@ -109,20 +123,84 @@ def placement_bytes(inp):
     return req_in + out + state + tables
 
 
-def src_hash():
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+def sweep_bytes(inp):
+    """Algorithmic HBM bytes of one sweep call: every batch's count and GPU terms, every task
+    slot's four fields, the results, and the tables read once."""
+    bt, lut = inp["batches"], inp["lut"]
+    B, T = bt["n_batches"], bt["max_tasks"]
+    return B * 12 + B * T * 16 + B * (4 + 1 + 4) + B * T * 4 + 2 * lut["pf"].nbytes
 
 
-def load_traffic():
-    """HBM bytes per launch of the scoring kernel from the committed counter runs,
-    or None when the kernel source changed since they were taken."""
+def sweep_work(inp):
+    """(cells, algorithmic VALU lane-ops) of one sweep call."""
+    bt, lut = inp["batches"], inp["lut"]
+    n = np.asarray(bt["n_tasks"])
+    tasks = int(n[(n >= 0) & (n <= bt["max_tasks"])].sum())
+    cells = tasks * lut["n_sm"] * lut["n_freq"]
+    return cells, cells * OPS_PER_SWEEP_CELL + tasks * lut["n_freq"] * OPS_PER_SWEEP_TASK_LEVEL
+
+
+def src_hash(path=KERNEL_SRC):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def load_traffic(path=TRAFFIC_FILE, src=KERNEL_SRC):
+    """HBM bytes per launch of a kernel from the committed counter runs, or None when
+    the kernel source changed since they were taken."""
     try:
-        d = json.load(open(TRAFFIC_FILE))
+        d = json.load(open(path))
     except (OSError, ValueError):
         return None
-    if d.get("kernel_src_sha256_16") != src_hash():
+    if d.get("kernel_src_sha256_16") != src_hash(src):
         return None
     return d.get("hbm_bytes_per_launch")
+
+
+def sweep_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
+    """The local SM/frequency sweep: kernel time from HIP events around each call (one
+    launch per call), its roofline position, and the oracle on the same batches."""
+    inp = W.make_sweep()
+    ds = F.DeviceSweep(inp, "cuda")
+    for _ in range(warmup):
+        ds.run()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream().cuda_stream
+    evs = [(hip.event(), hip.event()) for _ in range(calls)]
+    for a, b in evs:
+        hip.record(a, st)
+        ds.run()
+        hip.record(b, st)
+    torch.cuda.synchronize()
+    ms = float(np.mean([hip.elapsed_ms(a, b) for a, b in evs]))
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    bt = inp["batches"]
+    cells, ops = sweep_work(inp)
+    nbytes = sweep_bytes(inp)
+    row = {
+        "workload": ("local SM/frequency sweep: 1024 GPUs x 64 epochs = 65536 task batches of up to 8 "
+                     "prefill units / decode steps, 32 models, 8 SM x 16 freq levels"),
+        "batches": int(bt["n_batches"]), "tasks": int(np.asarray(bt["n_tasks"]).sum()),
+        "cells": cells, "kernel_ms": ms, "cells_per_s": cells / (ms * 1e-3),
+        "roofline": {"kernel": "k_sweep_8x16", "bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9,
+                     "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / HBM_PEAK,
+                     "traffic": load_traffic(SWEEP_TRAFFIC_FILE, SWEEP_SRC), "algorithmic_bytes": nbytes,
+                     "valu_frac_algorithmic": ops / (ms * 1e-3) / VALU_PEAK},
+        "cpu_baseline": None,
+    }
+    if with_cpu:
+        import oracle
+        gl, gf, ge, gt = ds.results()
+        t0 = time.perf_counter()
+        ol, of, oe, ot = oracle.sweep(inp)
+        t1 = time.perf_counter()
+        row["cpu_baseline"] = {
+            "value": cells / (t1 - t0), "unit": "cells/s", "cores": 1, "kind": "oracle",
+            "sample": f"all {bt['n_batches']} batches ({t1 - t0:.3f} s); single-threaded C, float64, gcc -O2",
+            "agreement": {"flags_equal": float(np.mean(of == gf)), "levels_equal": float(np.mean(ol == gl)),
+                          "task_sm_equal": float(np.mean(ot == gt))}}
+    return row
 
 
 # ------------------------------------------------------------------ CPU baseline (oracle)
@@ -269,6 +347,7 @@ def main():
         "kernels_ms": {"k_score": score_ms, "k_migrate": pairs_ms,
                        "migration_pairs_per_s_kernel": n_pairs / (pairs_ms * 1e-3)},
         "cpu_baseline": None,
+        "next_rows": {"sweep": sweep_row(F, W, hip, torch, not args.no_cpu_baseline)},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(place, fleet, gpu_place, gpu_mig)

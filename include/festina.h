@@ -11,6 +11,11 @@
  *   festina_score_migrations  -- for consolidation (Sec. 3.5), score every ordered
  *       source -> destination GPU pair for moving the whole source workload, and
  *       return each source's best destination.
+ * and, for the per-GPU local schedulers:
+ *   festina_sweep_batches     -- the joint SM/frequency sweep of many task batches at
+ *       once (Sec. 3.4, runtime resource allocation): per batch, the least-energy
+ *       frequency level at which every task meets its deadline on its smallest
+ *       sufficient SM share and the shares fit the device.
  *
  * Conventions shared by every entry point
  *  - All array pointers inside the structs are DEVICE pointers (HIP global memory
@@ -43,6 +48,10 @@ extern "C" {
 #define FESTINA_N_ROWS 32        /* rows of every profile table */
 #define FESTINA_MAX_CELLS 256    /* n_sm * n_freq limit of the placement kernels */
 #define FESTINA_MAX_FREQ_MIG 32  /* n_freq limit of the migration kernels (32-bit level masks) */
+#define FESTINA_MAX_FREQ_SWEEP 64 /* n_freq limit of the sweep kernel (one lane per level) */
+#define FESTINA_MAX_TASKS 64     /* task slots per batch of the sweep kernel */
+#define FESTINA_PREFILL 0        /* task phases of the sweep */
+#define FESTINA_DECODE 1
 
 typedef enum {
   FESTINA_OK = 0,
@@ -174,6 +183,52 @@ size_t festina_migrations_workspace_bytes(const festina_lut *lut, const festina_
 festina_status festina_score_migrations(const festina_lut *lut, const festina_fleet *fleet,
                                         festina_migrations *out, void *workspace,
                                         size_t workspace_bytes, void *stream);
+
+/* Task batches of the local schedulers (Sec. 3.4): batch b holds n_tasks[b] tasks in
+ * slots 0..n_tasks[b]-1 of its max_tasks slots.  A task is a prefill unit (phase
+ * FESTINA_PREFILL: latency from pf at the prompt bucket of task_tokens, rows as for
+ * requests) or one decode step (phase FESTINA_DECODE: latency from dc at batch size
+ * task_tokens, row = min(task_tokens, 32) - 1), and must finish strictly within
+ * task_slack_ms, the remaining time to its SLO deadline.  SM level j takes sm_units[j]
+ * of the device (e.g. per-mille: 125 per eighth); the shares of a batch must sum to
+ * strictly less than sm_budget (Sec. 3.4: below 100% of the SMs).  A model id outside
+ * [0, M), task_tokens < 1, an unknown phase, or n_tasks outside [0, max_tasks] makes
+ * the batch infeasible. */
+typedef struct festina_batches {
+  int32_t n_batches;                 /* B >= 0 */
+  int32_t max_tasks;                 /* task slots per batch, 1..FESTINA_MAX_TASKS */
+  const int32_t *n_tasks;            /* [B] */
+  const int32_t *task_model;         /* [B][max_tasks] */
+  const int32_t *task_phase;         /* [B][max_tasks] FESTINA_PREFILL or FESTINA_DECODE */
+  const int32_t *task_tokens;        /* [B][max_tasks] prompt tokens (prefill) or batch size (decode) */
+  const float *task_slack_ms;        /* [B][max_tasks] */
+  const float *k_dyn_w;              /* [B] dynamic-power coefficient of the batch's GPU, W */
+  const float *util;                 /* [B] utilisation u of the batch's GPU in the power model */
+  const int32_t *sm_units;           /* [NS] integer SM share of each level */
+  int32_t sm_budget;                 /* shares must sum to < sm_budget */
+} festina_batches;
+
+/* Sweep results (device memory, written by the call):
+ *   freq_level[b] = least-energy usable frequency level, lowest on exact ties; -1 if none;
+ *   feasible[b]   = 1 if a level was chosen, else 0;
+ *   energy_mj[b]  = sum over tasks of (P0 + k_dyn * s_j * f^3 * u) * latency at that level
+ *                   (float32), +inf if none;
+ *   task_sm[b][t] = SM level of task t at that level (the smallest whose latency is below
+ *                   the slack); -1 for slots t >= n_tasks[b] and for infeasible batches. */
+typedef struct festina_sweep_result {
+  int32_t *freq_level;
+  uint8_t *feasible;
+  float *energy_mj;
+  int32_t *task_sm;
+} festina_sweep_result;
+
+/* Sweep every batch (Sec. 3.4, runtime resource allocation: per frequency, the minimum SM
+ * share per task that meets its deadline, the device SM budget, the least predicted
+ * energy).  Needs no workspace.  Requires n_freq <= FESTINA_MAX_FREQ_SWEEP,
+ * n_sm <= FESTINA_MAX_CELLS and max_tasks <= FESTINA_MAX_TASKS.  One kernel launch on
+ * `stream`. */
+festina_status festina_sweep_batches(const festina_lut *lut, const festina_batches *batches,
+                                     festina_sweep_result *out, void *stream);
 
 /* Measurement hook, not part of the search.  While set, festina_score_placements
  * records `score_begin` on its stream immediately before its scoring kernel and

@@ -10,6 +10,10 @@ Placement, per request:
 Migration, per source: the same on (saving, destination), with the tolerance taken
 relative to max(|saving|, P0), and the frequency level must be the oracle's k* for
 the tested pair exactly.
+Sweep, per batch: the flag exactly; the tested level must be usable under the oracle,
+its energy within ``rtol`` of the oracle's float64 energy at that level, a level other
+than the oracle's only as a near-tie, and every task's SM level equal to the oracle's
+smallest sufficient level at the tested frequency level.
 """
 from __future__ import annotations
 
@@ -17,7 +21,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-from . import candidate_energy, pair_saving
+from . import candidate_energy, min_sm, pair_saving, sweep_level
 
 RTOL = 1e-5
 
@@ -102,4 +106,46 @@ def check_migrations(inp, sel, oracle_out, gpu_out, rtol=RTOL) -> Report:
                 rep.near_ties += 1
             else:
                 rep.mismatches.append((s, "destination", int(gb[i]), int(ob[i]), sv, float(osv[i])))
+    return rep
+
+
+def check_sweep(inp, sel, oracle_out, gpu_out, rtol=RTOL) -> Report:
+    """``sel``: batch ids; outputs: (freq_level, feasible, energy, task_sm) for those ids."""
+    ol, of, oe, ot = oracle_out
+    gl, gf, ge, gt = gpu_out
+    bt = inp["batches"]
+    T = int(bt["max_tasks"])
+    rep = Report(n=len(sel))
+    for i, b in enumerate(sel):
+        b = int(b)
+        if int(gf[i]) != int(of[i]):
+            rep.mismatches.append((b, "feasible", int(gf[i]), int(of[i])))
+            continue
+        if not of[i]:
+            if int(gl[i]) != -1 or not np.isinf(ge[i]) or np.any(gt[i] != -1):
+                rep.mismatches.append((b, "infeasible output", int(gl[i]), float(ge[i])))
+            continue
+        k = int(gl[i])
+        if k == int(ol[i]):                  # the oracle's own level: its outputs apply
+            ok, e_at, exp_t = True, float(oe[i]), [int(x) for x in ot[i]]
+        else:
+            ok, e_at = sweep_level(inp, b, k)
+            n = int(bt["n_tasks"][b])
+            exp_t = [min_sm(inp, b, t, k) if t < n else -1 for t in range(T)] if ok else None
+        if not ok:
+            rep.mismatches.append((b, "level unusable under the oracle", k, int(ol[i])))
+            continue
+        rel = abs(float(ge[i]) - e_at) / max(abs(e_at), 1e-30)
+        rep.max_rel_err = max(rep.max_rel_err, rel)
+        if rel > rtol:
+            rep.mismatches.append((b, "energy", float(ge[i]), e_at))
+            continue
+        if list(gt[i]) != exp_t:
+            rep.mismatches.append((b, "task SM levels", list(gt[i]), exp_t))
+            continue
+        if k != int(ol[i]):
+            if e_at <= float(oe[i]) * (1 + rtol) + 1e-30:
+                rep.near_ties += 1
+            else:
+                rep.mismatches.append((b, "level", k, int(ol[i]), e_at, float(oe[i])))
     return rep

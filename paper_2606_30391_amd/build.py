@@ -6,7 +6,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "festina.hip")
+SRCS = [os.path.join(HERE, "csrc", n) for n in ("festina.hip", "sweep.hip")]
 LIB = os.path.join(HERE, "libfestina.so")
 
 # -packed-fp32-ops: no v_pk_*_f32 from the compiler (plain fp32 VALU only)
@@ -16,7 +16,7 @@ HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
 
 
 def build_hip(verbose: bool = False) -> str:
-    cmd = ["hipcc", *HIPCC_FLAGS, "-o", LIB + ".tmp", SRC]
+    cmd = ["hipcc", *HIPCC_FLAGS, "-o", LIB + ".tmp", *SRCS]
     proc = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
     out = proc.stdout.decode()
     noise = "packed-fp32-ops"

@@ -1,7 +1,7 @@
 """Thin ctypes binding of the C ABI in include/festina.h.
 
 Argument marshalling only: every step of the search runs in the HIP library
-(``libfestina.so`` built from ``csrc/festina.hip``).  PyTorch provides device
+(``libfestina.so`` built from ``csrc/festina.hip`` and ``csrc/sweep.hip``).  PyTorch provides device
 memory and streams.  There is no CPU fallback: if the library is missing this
 module raises.
 """
@@ -62,9 +62,21 @@ class festina_migrations(C.Structure):
     _fields_ = [("best_dst", C.c_void_p), ("saving_w", C.c_void_p), ("freq_level", C.c_void_p)]
 
 
+class festina_batches(C.Structure):
+    _fields_ = [("n_batches", C.c_int32), ("max_tasks", C.c_int32), ("n_tasks", C.c_void_p),
+                ("task_model", C.c_void_p), ("task_phase", C.c_void_p), ("task_tokens", C.c_void_p),
+                ("task_slack_ms", C.c_void_p), ("k_dyn_w", C.c_void_p), ("util", C.c_void_p),
+                ("sm_units", C.c_void_p), ("sm_budget", C.c_int32)]
+
+
+class festina_sweep_result(C.Structure):
+    _fields_ = [("freq_level", C.c_void_p), ("feasible", C.c_void_p), ("energy_mj", C.c_void_p),
+                ("task_sm", C.c_void_p)]
+
+
 EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_workspace_bytes",
             "festina_score_placements", "festina_migrations_workspace_bytes", "festina_score_migrations",
-            "festina_set_timing_events")
+            "festina_sweep_batches", "festina_set_timing_events")
 
 _lib = None
 
@@ -90,6 +102,9 @@ def lib():
         L.festina_score_migrations.argtypes = [P(festina_lut), P(festina_fleet), P(festina_migrations),
                                                C.c_void_p, C.c_size_t, C.c_void_p]
         L.festina_score_migrations.restype = C.c_int
+        L.festina_sweep_batches.argtypes = [P(festina_lut), P(festina_batches), P(festina_sweep_result),
+                                            C.c_void_p]
+        L.festina_sweep_batches.restype = C.c_int
         L.festina_set_timing_events.argtypes = [C.c_void_p] * 4
         L.festina_set_timing_events.restype = None
         _lib = L
@@ -213,6 +228,47 @@ class DeviceMigration:
         return self.best_dst.cpu().numpy(), self.saving.cpu().numpy(), self.level.cpu().numpy()
 
 
+class DeviceSweep:
+    """Local-scheduler task batches copied to device memory once, with the ABI structs."""
+
+    def __init__(self, inp: dict, device="cuda"):
+        import torch
+        lut, bt = inp["lut"], inp["batches"]
+        d = lambda a, t: _dev(a, t, device)
+        self.t = {
+            "freq_level": d(lut["freq_level"], np.float32), "sm_level": d(lut["sm_level"], np.float32),
+            "pf": d(lut["pf"], np.float32), "dc": d(lut["dc"], np.float32),
+        }
+        for k in ("n_tasks", "task_model", "task_phase", "task_tokens", "sm_units"):
+            self.t[k] = d(bt[k], np.int32)
+        for k in ("task_slack_ms", "k_dyn_w", "util"):
+            self.t[k] = d(bt[k], np.float32)
+        t = self.t
+        self.lut = festina_lut(int(lut["n_models"]), int(lut["n_rows"]), int(lut["n_sm"]), int(lut["n_freq"]),
+                               _ptr(t["sm_level"]), _ptr(t["freq_level"]), _ptr(t["pf"]), _ptr(t["dc"]),
+                               float(lut["p0_w"]))
+        self.B, self.T = int(bt["n_batches"]), int(bt["max_tasks"])
+        self.batches = festina_batches(self.B, self.T, _ptr(t["n_tasks"]), _ptr(t["task_model"]),
+                                       _ptr(t["task_phase"]), _ptr(t["task_tokens"]), _ptr(t["task_slack_ms"]),
+                                       _ptr(t["k_dyn_w"]), _ptr(t["util"]), _ptr(t["sm_units"]),
+                                       int(bt["sm_budget"]))
+        n = max(self.B, 1)
+        self.level = torch.empty(n, dtype=torch.int32, device=device)
+        self.feasible = torch.empty(n, dtype=torch.uint8, device=device)
+        self.energy = torch.empty(n, dtype=torch.float32, device=device)
+        self.task_sm = torch.empty((n, self.T), dtype=torch.int32, device=device)
+        self.out = festina_sweep_result(_ptr(self.level), _ptr(self.feasible), _ptr(self.energy),
+                                        _ptr(self.task_sm))
+
+    def run(self, stream=None):
+        festina_sweep_batches(self.lut, self.batches, self.out, stream)
+
+    def results(self):
+        B = self.B
+        return (self.level[:B].cpu().numpy(), self.feasible[:B].cpu().numpy(), self.energy[:B].cpu().numpy(),
+                self.task_sm[:B].cpu().numpy())
+
+
 # ------------------------------------------------------------------ the ABI calls
 def festina_placements_workspace_bytes(lut, gpus, req) -> int:
     return int(lib().festina_placements_workspace_bytes(C.byref(lut), C.byref(gpus), C.byref(req)))
@@ -236,3 +292,9 @@ def festina_score_migrations(lut, fleet, out, workspace, workspace_bytes, stream
                                         int(workspace_bytes), _stream_handle(stream))
     if st != FESTINA_OK:
         raise FestinaError(st, "festina_score_migrations")
+
+
+def festina_sweep_batches(lut, batches, out, stream=None) -> None:
+    st = lib().festina_sweep_batches(C.byref(lut), C.byref(batches), C.byref(out), _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_sweep_batches")

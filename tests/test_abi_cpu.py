@@ -148,3 +148,45 @@ def test_product_binding_does_not_touch_the_oracle():
     assert "oracle" not in src.replace("no CPU fallback", "")
     hip = open(os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "festina.hip")).read()
     assert "oracle" not in hip
+
+
+def _sweep_structs(M=2, NS=4, NF=8, B=16, T=4):
+    fake = C.c_void_p(0x1000)       # never dereferenced: the calls below fail validation first
+    lut = F.festina_lut(M, 32, NS, NF, fake, fake, fake, fake, 120.0)
+    bat = F.festina_batches(B, T, fake, fake, fake, fake, fake, fake, fake, fake, 1000)
+    out = F.festina_sweep_result(fake, fake, fake, fake)
+    return lut, bat, out
+
+
+def _sweep_status(lut, bat, out):
+    return F.lib().festina_sweep_batches(C.byref(lut), C.byref(bat), C.byref(out), None)
+
+
+@no_gpu
+def test_sweep_rejects_bad_arguments(lib):
+    lut, bat, out = _sweep_structs()
+    L = F.lib()
+    assert L.festina_sweep_batches(None, C.byref(bat), C.byref(out), None) == F.FESTINA_ERR_INVALID
+    assert L.festina_sweep_batches(C.byref(lut), None, C.byref(out), None) == F.FESTINA_ERR_INVALID
+    assert L.festina_sweep_batches(C.byref(lut), C.byref(bat), None, None) == F.FESTINA_ERR_INVALID
+    for field, value, status in [("n_rows", 31, F.FESTINA_ERR_INVALID), ("n_sm", 0, F.FESTINA_ERR_INVALID),
+                                 ("n_freq", 0, F.FESTINA_ERR_INVALID), ("n_models", 0, F.FESTINA_ERR_INVALID),
+                                 ("n_freq", 65, F.FESTINA_ERR_UNSUPPORTED),
+                                 ("n_sm", 257, F.FESTINA_ERR_UNSUPPORTED), ("pf", None, F.FESTINA_ERR_INVALID)]:
+        lut, bat, out = _sweep_structs()
+        setattr(lut, field, value)
+        assert _sweep_status(lut, bat, out) == status, field
+    for field, value in [("n_batches", -1), ("max_tasks", 0), ("sm_units", None), ("task_slack_ms", None),
+                         ("n_tasks", None), ("util", None)]:
+        lut, bat, out = _sweep_structs()
+        setattr(bat, field, value)
+        assert _sweep_status(lut, bat, out) == F.FESTINA_ERR_INVALID, field
+    for field in ("freq_level", "feasible", "energy_mj", "task_sm"):
+        lut, bat, out = _sweep_structs()
+        setattr(out, field, None)
+        assert _sweep_status(lut, bat, out) == F.FESTINA_ERR_INVALID, field
+    # no batches: nothing to do, nothing launched, outputs untouched
+    lut, bat, out = _sweep_structs(B=0)
+    bat.n_tasks = None
+    out.task_sm = None
+    assert _sweep_status(lut, bat, out) == F.FESTINA_OK
