@@ -262,6 +262,8 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep(SweepArgs a) {
 // to LDS; after the 16-lane (energy, level) minimum, lane t of the batch writes task t's
 // level at the chosen frequency.  Same arithmetic as k_sweep, so the same results.
 constexpr int kFNS = 8, kFNF = 16, kFT = 16;
+constexpr int kTasksInFlight = 2;             // 2 x 8 table loads issued together per lane
+constexpr long long kSweepGrid = 8192;        // blocks of the grid-stride loop (one pass up to 131072 batches)
 constexpr int kBatchesPerWave = kWave / kFNF;
 
 __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep_8x16(SweepArgs a) {
@@ -278,92 +280,97 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep_8x16(SweepArgs
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
   const int g = lane >> 4, k = lane & (kFNF - 1);
-  const int b = (blockIdx.x * kWavesPerBlock + wv) * kBatchesPerWave + g;
-  const bool live = b < a.B;
-  const size_t row0 = (size_t)(live ? b : 0) * a.T;
-
-  // one memory round trip: lane k of a batch's group loads slot k
-  int m = 0, ph = 0, tok = 0;
-  float sl = 0.f;
-  if (live && k < a.T) {
-    m = a.model[row0 + k];
-    ph = a.phase[row0 + k];
-    tok = a.tokens[row0 + k];
-    sl = a.slack[row0 + k];
-  }
-  const int n = live ? a.n_tasks[b] : 0;
-  const float kd = live ? a.kdyn[b] : 0.f, u = live ? a.util[b] : 0.f;
-  const bool n_ok = n >= 0 && n <= a.T;
-  const int nn = n_ok ? n : 0;
-  int row = 0;
-  if (k < nn) {
-    row = task_row(a, m, ph, tok);
-    s_col[wv][lane] = row >= 0 ? (m * kRows + row) * (kFNS * kFNF) : 0;
-    s_slack[wv][lane] = sl;
-    s_ph[wv][lane] = ph;
-  }
-  __syncthreads();
-  const unsigned long long badm = __ballot(k < nn && row < 0);
-  const bool bad = !live || !n_ok || ((badm >> (kFNF * g)) & 0xffffull) != 0;
-
-  const float f = a.freq_level[k];
-  const float c = kd * u * (f * f * f);
-  long long units = 0;
-  float E = 0.f;
-  int miss = 0;
   const int gs = g * kFNF;
-  for (int t = 0; !bad && t < nn; t += 2) {
-    const bool two = t + 1 < nn;
-    const int t1 = two ? t + 1 : t;
-    const float *c0 = (s_ph[wv][gs + t] == 0 ? a.pf : a.dc) + s_col[wv][gs + t] + k;
-    const float *c1 = (s_ph[wv][gs + t1] == 0 ? a.pf : a.dc) + s_col[wv][gs + t1] + k;
-    float v0[kJChunk], v1[kJChunk];
+  const float f = a.freq_level[k];
+  const float f3 = f * f * f;
+  constexpr int kPerBlock = kWavesPerBlock * kBatchesPerWave;
+  const int n_units = (a.B + kPerBlock - 1) / kPerBlock;
+  // grid-stride over groups of 16 batches (the loop count is uniform per block); a grid of
+  // one block per group measured fastest, so the loop only serves very large calls
+  for (int unit = blockIdx.x; unit < n_units; unit += gridDim.x) {
+    const int b = (unit * kWavesPerBlock + wv) * kBatchesPerWave + g;
+    const bool live = b < a.B;
+    const size_t row0 = (size_t)(live ? b : 0) * a.T;
+
+    // one memory round trip: lane k of a batch's group loads slot k
+    int m = 0, ph = 0, tok = 0;
+    float sl = 0.f;
+    if (live && k < a.T) {
+      m = a.model[row0 + k];
+      ph = a.phase[row0 + k];
+      tok = a.tokens[row0 + k];
+      sl = a.slack[row0 + k];
+    }
+    const int n = live ? a.n_tasks[b] : 0;
+    const float kd = live ? a.kdyn[b] : 0.f, u = live ? a.util[b] : 0.f;
+    const bool n_ok = n >= 0 && n <= a.T;
+    const int nn = n_ok ? n : 0;
+    int row = 0;
+    if (k < nn) {
+      row = task_row(a, m, ph, tok);
+      s_col[wv][lane] = row >= 0 ? (m * kRows + row) * (kFNS * kFNF) : 0;
+      s_slack[wv][lane] = sl;
+      s_ph[wv][lane] = ph;
+    }
+    __syncthreads();
+    const unsigned long long badm = __ballot(k < nn && row < 0);
+    const bool bad = !live || !n_ok || ((badm >> (kFNF * g)) & 0xffffull) != 0;
+
+    const float c = kd * u * f3;
+    long long units = 0;
+    float E = 0.f;
+    int miss = 0;
+    for (int t = 0; !bad && t < nn; t += kTasksInFlight) {
+      const float *cp[kTasksInFlight];
+      float slk[kTasksInFlight];
 #pragma unroll
-    for (int q = 0; q < kJChunk; ++q) {
-      v0[q] = c0[q * kFNF];
-      v1[q] = c1[q * kFNF];
-    }
-    float lat0, lat1;
-    const int j0 = first_below(v0, s_slack[wv][gs + t], lat0);
-    const int j1 = first_below(v1, s_slack[wv][gs + t1], lat1);
-    s_j[wv][g][t][k] = (int8_t)j0;
-    if (j0 < 0) {
-      miss = 1;
-    } else {
-      units += s_units[j0];
-      E = fmaf(fmaf(c, s_lev[j0], a.p0), lat0, E);
-    }
-    if (two) {
-      s_j[wv][g][t1][k] = (int8_t)j1;
-      if (j1 < 0) {
-        miss = 1;
-      } else {
-        units += s_units[j1];
-        E = fmaf(fmaf(c, s_lev[j1], a.p0), lat1, E);
+      for (int i = 0; i < kTasksInFlight; ++i) {
+        const int ti = t + i < nn ? t + i : t;   // a slot of this batch either way
+        cp[i] = (s_ph[wv][gs + ti] == 0 ? a.pf : a.dc) + s_col[wv][gs + ti] + k;
+        slk[i] = s_slack[wv][gs + ti];
+      }
+      float v[kTasksInFlight][kJChunk];
+#pragma unroll
+      for (int i = 0; i < kTasksInFlight; ++i)
+#pragma unroll
+        for (int q = 0; q < kJChunk; ++q) v[i][q] = cp[i][q * kFNF];
+#pragma unroll
+      for (int i = 0; i < kTasksInFlight; ++i) {
+        if (t + i >= nn) break;
+        float lat;
+        const int j = first_below(v[i], slk[i], lat);
+        s_j[wv][g][t + i][k] = (int8_t)j;
+        if (j < 0) {
+          miss = 1;
+        } else {
+          units += s_units[j];
+          E = fmaf(fmaf(c, s_lev[j], a.p0), lat, E);
+        }
       }
     }
-  }
-  const bool usable = !bad && !miss && units < (long long)a.budget && E < kInf;
-  float be = usable ? E : kInf;
-  int bk = usable ? k : INT_MAX;
+    const bool usable = !bad && !miss && units < (long long)a.budget && E < kInf;
+    float be = usable ? E : kInf;
+    int bk = usable ? k : INT_MAX;
 #pragma unroll
-  for (int off = kFNF / 2; off >= 1; off >>= 1) {
-    const float oe = __shfl_xor(be, off, kWave);
-    const int ok = __shfl_xor(bk, off, kWave);
-    if (oe < be || (oe == be && ok < bk)) {
-      be = oe;
-      bk = ok;
+    for (int off = kFNF / 2; off >= 1; off >>= 1) {
+      const float oe = __shfl_xor(be, off, kWave);
+      const int ok = __shfl_xor(bk, off, kWave);
+      if (oe < be || (oe == be && ok < bk)) {
+        be = oe;
+        bk = ok;
+      }
+    }
+    const bool found = bk != INT_MAX;
+    __syncthreads();                       // the SM levels in s_j are visible to every lane
+    if (live) {
+      if (k == 0) {
+        a.level[b] = found ? bk : -1;
+        a.feasible[b] = found ? 1 : 0;
+        a.energy[b] = found ? be : kInf;
+      }
+      if (k < a.T) a.task_sm[row0 + k] = (found && k < nn) ? (int)s_j[wv][g][k][bk] : -1;
     }
   }
-  const bool found = bk != INT_MAX;
-  __syncthreads();                       // the SM levels in s_j are visible to every lane
-  if (!live) return;
-  if (k == 0) {
-    a.level[b] = found ? bk : -1;
-    a.feasible[b] = found ? 1 : 0;
-    a.energy[b] = found ? be : kInf;
-  }
-  if (k < a.T) a.task_sm[row0 + k] = (found && k < nn) ? (int)s_j[wv][g][k][bk] : -1;
 }
 
 }  // namespace
@@ -412,7 +419,8 @@ extern "C" festina_status festina_sweep_batches(const festina_lut *L, const fest
   const bool fast = a.NS == kFNS && a.NF == kFNF && a.T <= kFT && a.M <= (INT_MAX / (kRows * kFNS * kFNF));
   if (fast) {
     const long long per = (long long)kWavesPerBlock * kBatchesPerWave;
-    const long long blocks = ((long long)a.B + per - 1) / per;
+    const long long units = ((long long)a.B + per - 1) / per;
+    const long long blocks = units < kSweepGrid ? units : kSweepGrid;
     k_sweep_8x16<<<(unsigned)blocks, kWavesPerBlock * kWave, 0, st>>>(a);
   } else {
     const long long blocks = ((long long)a.B + kWavesPerBlock - 1) / kWavesPerBlock;

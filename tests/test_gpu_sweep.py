@@ -130,3 +130,12 @@ def test_sweep_side_stream_and_repeat():
     b = run_sweep(inp)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
+
+
+def test_sweep_more_batches_than_one_grid_pass():
+    """Above 131072 batches the 8x16 kernel's blocks loop over several groups of 16."""
+    rng = np.random.default_rng(952)
+    inp = W.make_tiny_sweep(rng, B=140_011, T=3, M=3, NS=8, NF=16)
+    sel = np.concatenate([np.arange(200), np.random.default_rng(3).choice(140_011, 3000, replace=False),
+                          np.arange(140_011 - 200, 140_011)])
+    parity_sweep(inp, sel, label="140011 batches")
