@@ -63,6 +63,19 @@ class _Batches(C.Structure):
                 ("sm_units", C.c_void_p), ("sm_budget", C.c_int32)]
 
 
+class _Llms(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("max_inst", C.c_int32), ("n_inst", C.c_void_p),
+                ("model", C.c_void_p), ("avg_in_tokens", C.c_void_p), ("avg_out_tokens", C.c_void_p),
+                ("batch", C.c_void_p), ("slo_ttft_ms", C.c_void_p), ("slo_tbt_ms", C.c_void_p),
+                ("k_dyn_w", C.c_void_p)]
+
+
+class _Pref(C.Structure):
+    _fields_ = [("sm_p", C.c_int32), ("f_p", C.c_int32), ("sm_d", C.c_int32), ("f_d", C.c_int32),
+                ("t_p", C.c_double), ("t_d", C.c_double), ("p_p", C.c_double), ("p_d", C.c_double),
+                ("sm_pref", C.c_double), ("f_pref", C.c_double), ("feasible", C.c_int)]
+
+
 def lib():
     global _lib
     if _lib is None:
@@ -95,6 +108,14 @@ def lib():
         L.festina_oracle_sweep_level.restype = C.c_int
         L.festina_oracle_min_sm.argtypes = [P(_Lut), P(_Batches), C.c_int32, C.c_int32, C.c_int32]
         L.festina_oracle_min_sm.restype = C.c_int
+        L.festina_oracle_preferred.argtypes = [P(_Lut), P(_Llms), C.c_void_p]
+        L.festina_oracle_preferred.restype = C.c_int
+        L.festina_oracle_phase_cell.argtypes = [P(_Lut), P(_Llms), C.c_int32, C.c_int32, C.c_int32,
+                                                C.c_int32, C.c_int32, P(C.c_double), P(C.c_double)]
+        L.festina_oracle_phase_cell.restype = C.c_int
+        L.festina_oracle_fleet_ewr.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                               C.c_void_p, C.c_void_p, C.c_void_p]
+        L.festina_oracle_fleet_ewr.restype = C.c_int
         _lib = L
     return _lib
 
@@ -157,6 +178,13 @@ def _batches(d, pin):
                     pin(d["task_tokens"], np.int32), pin(d["task_slack_ms"], np.float32),
                     pin(d["k_dyn_w"], np.float32), pin(d["util"], np.float32),
                     pin(d["sm_units"], np.int32), int(d["sm_budget"]))
+
+
+def _llms(d, pin):
+    return _Llms(int(d["n_gpus"]), int(d["max_inst"]), pin(d["n_inst"], np.int32), pin(d["model"], np.int32),
+                 pin(d["avg_in_tokens"], np.int32), pin(d["avg_out_tokens"], np.int32),
+                 pin(d["batch"], np.int32), pin(d["slo_ttft_ms"], np.float32), pin(d["slo_tbt_ms"], np.float32),
+                 pin(d["k_dyn_w"], np.float32))
 
 
 # ------------------------------------------------------------------ public API
@@ -261,3 +289,50 @@ def min_sm(inp: dict, b: int, t: int, k: int) -> int:
     pin = _Pinned()
     lut, bat = _lut(inp["lut"], pin), _batches(inp["batches"], pin)
     return int(lib().festina_oracle_min_sm(C.byref(lut), C.byref(bat), int(b), int(t), int(k)))
+
+
+PREF_FIELDS = ("sm_p", "f_p", "sm_d", "f_d", "t_p", "t_d", "p_p", "p_d", "sm_pref", "f_pref", "feasible")
+
+
+def preferred(inp: dict) -> dict:
+    """Oracle preferred configuration of every instance slot: dict of [G][K] arrays
+    (levels int32, durations/powers/averages float64, feasible uint8)."""
+    pin = _Pinned()
+    lut, q = _lut(inp["lut"], pin), _llms(inp["llms"], pin)
+    G, K = int(inp["llms"]["n_gpus"]), int(inp["llms"]["max_inst"])
+    buf = (_Pref * max(G * K, 1))()
+    if lib().festina_oracle_preferred(C.byref(lut), C.byref(q), C.cast(buf, C.c_void_p)) != 0:
+        raise ValueError("oracle rejected the preferred-configuration arguments")
+    out = {}
+    for f in PREF_FIELDS:
+        dt = np.float64 if f in ("t_p", "t_d", "p_p", "p_d", "sm_pref", "f_pref") else np.int32
+        out[f] = np.array([getattr(buf[x], f) for x in range(G * K)], dt).reshape(G, K)
+    out["feasible"] = out["feasible"].astype(np.uint8)
+    return out
+
+
+def phase_cell(inp: dict, g: int, i: int, decode: bool, j: int, k: int):
+    """(feasible, duration_ms, power_w) of one phase of instance (g, i) at cell (j, k)."""
+    pin = _Pinned()
+    lut, q = _lut(inp["lut"], pin), _llms(inp["llms"], pin)
+    t, p = C.c_double(0.0), C.c_double(0.0)
+    ok = lib().festina_oracle_phase_cell(C.byref(lut), C.byref(q), int(g), int(i), int(bool(decode)),
+                                         int(j), int(k), C.byref(t), C.byref(p))
+    return bool(ok), float(t.value), float(p.value)
+
+
+def fleet_ewr(n_inst, f_pref, t_ms):
+    """Eq. energy_waste / energy_optimal / energy_waste_ratio over instance slots [G][K].
+
+    Returns (f_gpu float64 [G], waste_gpu float64 [G], (E_waste, E_optimal, EWR))."""
+    n_inst = _arr(n_inst, np.int32)
+    f = _arr(f_pref, np.float32)
+    t = _arr(t_ms, np.float32)
+    G, K = f.shape
+    fg = np.empty(G, np.float64)
+    wg = np.empty(G, np.float64)
+    tot = np.empty(3, np.float64)
+    rc = lib().festina_oracle_fleet_ewr(G, K, _p(n_inst), _p(f), _p(t), _p(fg), _p(wg), _p(tot))
+    if rc != 0:
+        raise ValueError("oracle rejected the EWR arguments")
+    return fg, wg, (float(tot[0]), float(tot[1]), float(tot[2]))

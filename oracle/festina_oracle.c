@@ -41,6 +41,13 @@
  *     (Power x Latency per task, the placement power model); the least-energy usable k
  *     wins, the lowest k on exact ties.
  *
+ *   preferred configuration (App. E) and energy waste ratio (Sec. 3.5.1):
+ *     per LLM instance, the least-energy SLO-feasible cell of the prefill phase
+ *     (duration TTFT at the average prompt's bucket) and of the decode phase (duration
+ *     avg_out x TBT at the batch row), then SM_l = (s_p T_p + s_d T_d) / (T_p + T_d) and
+ *     F_l = (P_p T_p f_p + P_d T_d f_d) / (P_p T_p + P_d T_d); per GPU F_g = max F_l,
+ *     E_waste = sum t_l (F_g^3 - F_l^3), E_optimal = sum t_l F_l^3, EWR = their ratio.
+ *
  * Request pre-processing (Sec. 3.2.1 input-length axis 256..8192; Sec. 3.2.2 / 3.3 the
  * 5% output-length safety pad):
  *   Lout = ceil(1.05 * predicted_out)            (integer: (105*L + 99) / 100)
@@ -408,5 +415,172 @@ int festina_oracle_sweep(const or_lut *L, const or_batches *S, int32_t n_sel, co
     for (int t = 0; t < S->max_tasks; ++t)
       task_sm[(size_t)i * S->max_tasks + (size_t)t] = (bk >= 0 && t < S->n_tasks[b]) ? or_min_sm(L, S, b, t, bk) : -1;
   }
+  return 0;
+}
+
+/* ---------------------------------------------------------------- preferred configuration, EWR */
+/* App. E, "Determining Preferred Configurations": per active LLM, the least-energy
+ * SLO-feasible (SM level, frequency level) of each phase from the look-up table, then
+ * Eq. preferred_sm (time-weighted SM share) and Eq. preferred_frequency (energy-weighted
+ * frequency).  Sec. 3.5.1, Eq. energy_waste / energy_optimal / energy_waste_ratio: per GPU
+ * the operating frequency F_g is the highest preferred frequency among its LLMs. */
+typedef struct {
+  int32_t n_gpus, max_inst;
+  const int32_t *n_inst;           /* [G] */
+  const int32_t *model;            /* [G][K] */
+  const int32_t *avg_in_tokens;    /* [G][K] */
+  const int32_t *avg_out_tokens;   /* [G][K] */
+  const int32_t *batch;            /* [G][K] current decode batch B */
+  const float *slo_ttft_ms, *slo_tbt_ms;  /* [G][K] */
+  const float *k_dyn_w;            /* [G] */
+} or_llms;
+
+typedef struct {
+  int32_t sm_p, f_p, sm_d, f_d;    /* chosen levels, -1 when the phase has no feasible cell */
+  double t_p, t_d, p_p, p_d;       /* phase duration (ms) and power (W) at those levels */
+  double sm_pref, f_pref;          /* Eq. preferred_sm, Eq. preferred_frequency */
+  int feasible;                    /* both phases have a feasible cell */
+} or_pref;
+
+/* Least-energy feasible cell of one phase of instance i of GPU g.  Prefill: duration
+ * TTFT = PF[prompt row][j][k] (< SLO), energy P * TTFT.  Decode: duration
+ * avg_out * TBT with TBT = DC[batch row][j][k] (< SLO), energy P * duration.  P is the
+ * placement power model with u = b / 32, b = min(B + 1, 32).  Returns the linear cell
+ * j*NF + k (lowest on exact ties) or -1. */
+static int or_phase_best(const or_lut *L, const or_llms *Q, int g, int i, int decode,
+                         double *t_out, double *p_out) {
+  const size_t at = (size_t)g * Q->max_inst + (size_t)i;
+  const int m = Q->model[at];
+  const int32_t B = Q->batch[at];
+  const int prow = or_prompt_row(Q->avg_in_tokens[at]);
+  if (m < 0 || m >= L->n_models || B < 0 || prow < 0 || Q->avg_out_tokens[at] < 0) return -1;
+  const int b = (B + 1 > OR_ROWS) ? OR_ROWS : B + 1;
+  const double u = (double)b / 32.0;
+  const double kg = (double)Q->k_dyn_w[g];
+  int best = -1;
+  double best_e = INFINITY, best_t = 0.0, best_p = 0.0;
+  for (int j = 0; j < L->n_sm; ++j)
+    for (int k = 0; k < L->n_freq; ++k) {
+      const float lat = decode ? L->dc[or_cell(L, m, b - 1, j, k)] : L->pf[or_cell(L, m, prow, j, k)];
+      const float slo = decode ? Q->slo_tbt_ms[at] : Q->slo_ttft_ms[at];
+      if (!(lat < slo)) continue;
+      const double P = L->p0_w + kg * (double)L->sm_level[j] * or_cube((double)L->freq_level[k]) * u;
+      const double t = decode ? (double)Q->avg_out_tokens[at] * (double)lat : (double)lat;
+      const double e = P * t;
+      if (!((float)e < INFINITY)) continue;
+      if (best < 0 || e < best_e) {
+        best = j * L->n_freq + k;
+        best_e = e;
+        best_t = t;
+        best_p = P;
+      }
+    }
+  *t_out = best_t;
+  *p_out = best_p;
+  return best;
+}
+
+static void or_preferred_one(const or_lut *L, const or_llms *Q, int g, int i, or_pref *o) {
+  double tp = 0, pp = 0, td = 0, pd = 0;
+  const int cp = or_phase_best(L, Q, g, i, 0, &tp, &pp);
+  const int cd = or_phase_best(L, Q, g, i, 1, &td, &pd);
+  o->sm_p = cp < 0 ? -1 : cp / L->n_freq;
+  o->f_p = cp < 0 ? -1 : cp % L->n_freq;
+  o->sm_d = cd < 0 ? -1 : cd / L->n_freq;
+  o->f_d = cd < 0 ? -1 : cd % L->n_freq;
+  o->t_p = tp;
+  o->p_p = pp;
+  o->t_d = td;
+  o->p_d = pd;
+  o->feasible = cp >= 0 && cd >= 0;
+  if (o->feasible) {
+    const double sp = (double)L->sm_level[o->sm_p], sd = (double)L->sm_level[o->sm_d];
+    const double fp = (double)L->freq_level[o->f_p], fd = (double)L->freq_level[o->f_d];
+    o->sm_pref = (sp * tp + sd * td) / (tp + td);
+    o->f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);
+  } else {
+    o->sm_pref = NAN;
+    o->f_pref = NAN;
+  }
+}
+
+/* Preferred configuration of every instance slot [G][K]; slots past n_inst (or a GPU with
+ * n_inst outside [0, K]) are infeasible. */
+int festina_oracle_preferred(const or_lut *L, const or_llms *Q, or_pref *out) {
+  if (!or_lut_ok(L) || !Q || !out || Q->n_gpus < 0 || Q->max_inst < 1) return 1;
+  for (int g = 0; g < Q->n_gpus; ++g)
+    for (int i = 0; i < Q->max_inst; ++i) {
+      or_pref *o = &out[(size_t)g * Q->max_inst + (size_t)i];
+      const int n = Q->n_inst[g];
+      if (n < 0 || n > Q->max_inst || i >= n) {
+        o->sm_p = o->f_p = o->sm_d = o->f_d = -1;
+        o->t_p = o->t_d = o->p_p = o->p_d = 0.0;
+        o->sm_pref = o->f_pref = NAN;
+        o->feasible = 0;
+        continue;
+      }
+      or_preferred_one(L, Q, g, i, o);
+    }
+  return 0;
+}
+
+/* Energy of one phase at a given cell (for checking another implementation's choice):
+ * 1 and the duration/power when the cell is feasible. */
+int festina_oracle_phase_cell(const or_lut *L, const or_llms *Q, int32_t g, int32_t i, int32_t decode,
+                              int32_t j, int32_t k, double *t_out, double *p_out) {
+  if (!or_lut_ok(L) || !Q || g < 0 || g >= Q->n_gpus || i < 0 || i >= Q->max_inst) return 0;
+  if (j < 0 || j >= L->n_sm || k < 0 || k >= L->n_freq) return 0;
+  const size_t at = (size_t)g * Q->max_inst + (size_t)i;
+  const int n = Q->n_inst[g];
+  if (n < 0 || n > Q->max_inst || i >= n) return 0;
+  const int m = Q->model[at];
+  const int32_t B = Q->batch[at];
+  const int prow = or_prompt_row(Q->avg_in_tokens[at]);
+  if (m < 0 || m >= L->n_models || B < 0 || prow < 0 || Q->avg_out_tokens[at] < 0) return 0;
+  const int b = (B + 1 > OR_ROWS) ? OR_ROWS : B + 1;
+  const float lat = decode ? L->dc[or_cell(L, m, b - 1, j, k)] : L->pf[or_cell(L, m, prow, j, k)];
+  const float slo = decode ? Q->slo_tbt_ms[at] : Q->slo_ttft_ms[at];
+  if (!(lat < slo)) return 0;
+  const double P = L->p0_w + (double)Q->k_dyn_w[g] * (double)L->sm_level[j] * or_cube((double)L->freq_level[k]) *
+                                 ((double)b / 32.0);
+  const double t = decode ? (double)Q->avg_out_tokens[at] * (double)lat : (double)lat;
+  if (!((float)(P * t) < INFINITY)) return 0;
+  *t_out = t;
+  *p_out = P;
+  return 1;
+}
+
+/* Eq. energy_waste, energy_optimal, energy_waste_ratio over a fleet of instance slots.
+ * Instances with a non-finite preferred frequency or execution time, or past n_inst, are
+ * left out.  F_g = the highest preferred frequency on GPU g (0 with no instance);
+ * waste_g = sum t_l (F_g^3 - F_l^3); totals[0] = sum waste_g, totals[1] = sum t_l F_l^3,
+ * totals[2] = totals[0] / totals[1]. */
+int festina_oracle_fleet_ewr(int32_t n_gpus, int32_t max_inst, const int32_t *n_inst, const float *f_pref,
+                             const float *t_ms, double *f_gpu, double *waste_gpu, double *totals) {
+  if (n_gpus < 0 || max_inst < 1 || !n_inst || !f_pref || !t_ms || !f_gpu || !waste_gpu || !totals) return 1;
+  double waste = 0.0, opt = 0.0;
+  for (int g = 0; g < n_gpus; ++g) {
+    const int n = n_inst[g];
+    double fg = 0.0;
+    for (int i = 0; i < max_inst; ++i) {
+      const size_t at = (size_t)g * max_inst + (size_t)i;
+      if (n < 0 || n > max_inst || i >= n || !isfinite(f_pref[at]) || !isfinite(t_ms[at])) continue;
+      if ((double)f_pref[at] > fg) fg = (double)f_pref[at];
+    }
+    double wg = 0.0;
+    for (int i = 0; i < max_inst; ++i) {
+      const size_t at = (size_t)g * max_inst + (size_t)i;
+      if (n < 0 || n > max_inst || i >= n || !isfinite(f_pref[at]) || !isfinite(t_ms[at])) continue;
+      const double fl = (double)f_pref[at], t = (double)t_ms[at];
+      wg += t * (or_cube(fg) - or_cube(fl));
+      opt += t * or_cube(fl);
+    }
+    f_gpu[g] = fg;
+    waste_gpu[g] = wg;
+    waste += wg;
+  }
+  totals[0] = waste;
+  totals[1] = opt;
+  totals[2] = waste / opt;
   return 0;
 }

@@ -452,3 +452,73 @@ def make_tiny_sweep(rng: np.random.Generator, B=None, T=None, M=None, NS=None, N
                "util": rng.uniform(0.0, 1.0, B).astype(np.float32),
                "sm_units": units, "sm_budget": int(rng.integers(1, 1000 * T + 2))}
     return {"lut": lut, "batches": batches, "meta": {}}
+
+
+# --------------------------------------------------------------------------- preferred configuration
+LLMS_SEED = CONFIG_SEED_BASE + 60
+
+
+def make_llms(seed: int | None = None, n_gpus: int = 2048) -> dict:
+    """Active LLM instances for the preferred-configuration search and the EWR reduction.
+
+    Configuration 5's fleet law: tables as configuration 3 (32 models, 8 SM x 16 frequency
+    levels, +-5% noise), each GPU hosts 1-4 distinct models with k ~ U(300, 500); per
+    instance the average prompt over the last window is lognormal(6, 1) tokens (clipped
+    16-8192), the average output lognormal(5, 1) (clipped 1-8192), the decode batch
+    min(Poisson(4), 31), and the SLOs are the model's.
+    """
+    if seed is None:
+        seed = LLMS_SEED
+    rng = np.random.default_rng(seed)
+    M, NS, NF, G, K = 32, 8, 16, int(n_gpus), MAX_INST
+    s, f = sm_levels(NS), freq_levels(NF)
+    a, c, cp = _latency_params(rng, M, prefill=True)
+    pf, dc = _tables(rng, M, s, f, a, c, cp, noise=True)
+    lut = _lut(pf, dc, s, f)
+    slo_m_ttft = rng.choice(TTFT_SLO_SET, M)
+    slo_m_tbt = rng.choice(TBT_SLO_SET, M)
+    n_inst = rng.integers(1, K + 1, size=G).astype(np.int32)
+    model = np.zeros((G, K), np.int32)
+    for g in range(G):
+        model[g, :n_inst[g]] = rng.choice(M, int(n_inst[g]), replace=False)
+    avg_in = _lognormal_tokens(rng, 6.0, G * K, 16, 8192).reshape(G, K)
+    avg_out = _lognormal_tokens(rng, 5.0, G * K, 1, 8192).reshape(G, K)
+    batch = np.minimum(rng.poisson(4.0, size=(G, K)), 31).astype(np.int32)
+    kdyn = rng.uniform(300.0, 500.0, G).astype(np.float32)
+    unused = np.arange(K)[None, :] >= n_inst[:, None]
+    for arr in (model, avg_in, avg_out, batch):
+        arr[unused] = 0
+    slo_ttft = slo_m_ttft[model].astype(np.float32)
+    slo_tbt = slo_m_tbt[model].astype(np.float32)
+    slo_ttft[unused] = 0.0
+    slo_tbt[unused] = 0.0
+    llms = {"n_gpus": G, "max_inst": K, "n_inst": n_inst, "model": model, "avg_in_tokens": avg_in,
+            "avg_out_tokens": avg_out, "batch": batch, "slo_ttft_ms": slo_ttft, "slo_tbt_ms": slo_tbt,
+            "k_dyn_w": kdyn}
+    return {"lut": lut, "llms": llms, "meta": {"seed": seed}}
+
+
+def make_tiny_llms(rng: np.random.Generator, G=None, K=None, M=None, NS=None, NF=None,
+                   nan_cells=False, zero_out=False) -> dict:
+    """Small random set of LLM instances for pins and parity edge cases."""
+    G = int(rng.integers(1, 5)) if G is None else G
+    K = int(rng.integers(1, 4)) if K is None else K
+    M = int(rng.integers(1, 4)) if M is None else M
+    NS = int(rng.integers(1, 5)) if NS is None else NS
+    NF = int(rng.integers(1, 7)) if NF is None else NF
+    s, f = sm_levels(NS), freq_levels(NF)
+    pf = rng.uniform(5.0, 60.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    dc = rng.uniform(2.0, 40.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    if nan_cells:
+        pf[rng.random(pf.shape) < 0.1] = np.nan
+        dc[rng.random(dc.shape) < 0.05] = np.inf
+    lut = _lut(pf, dc, s, f, p0=float(rng.uniform(0.0, 150.0)))
+    llms = {"n_gpus": G, "max_inst": K, "n_inst": rng.integers(0, K + 1, G).astype(np.int32),
+            "model": rng.integers(0, M, (G, K)).astype(np.int32),
+            "avg_in_tokens": rng.integers(1, 9000, (G, K)).astype(np.int32),
+            "avg_out_tokens": (np.zeros((G, K)) if zero_out else rng.integers(0, 400, (G, K))).astype(np.int32),
+            "batch": rng.integers(0, 32, (G, K)).astype(np.int32),
+            "slo_ttft_ms": rng.uniform(8.0, 70.0, (G, K)).astype(np.float32),
+            "slo_tbt_ms": rng.uniform(4.0, 45.0, (G, K)).astype(np.float32),
+            "k_dyn_w": rng.uniform(0.0, 500.0, G).astype(np.float32)}
+    return {"lut": lut, "llms": llms, "meta": {}}

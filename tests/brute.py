@@ -217,3 +217,70 @@ def brute_sweep(inp):
             lev[b], energy[b] = k, e
             tsm[b, :len(a)] = a
     return lev, (lev >= 0).astype(np.uint8), energy, tsm
+
+
+# ------------------------------------------------------------------ preferred configuration, EWR
+def phase_cells(inp, g, i, decode):
+    """All (energy, cell, duration, power) of the SLO-feasible cells of one phase."""
+    lut, q = inp["lut"], inp["llms"]
+    NS, NF = lut["n_sm"], lut["n_freq"]
+    m, B = int(q["model"][g, i]), int(q["batch"][g, i])
+    prow = prompt_row(int(q["avg_in_tokens"][g, i]))
+    out_tok = int(q["avg_out_tokens"][g, i])
+    if not 0 <= m < lut["n_models"] or B < 0 or prow is None or prow < 0 or out_tok < 0:
+        return []
+    b = min(B + 1, 32)
+    res = []
+    for j, k in itertools.product(range(NS), range(NF)):
+        lat = lut["dc"][m, b - 1, j, k] if decode else lut["pf"][m, prow, j, k]
+        slo = q["slo_tbt_ms"][g, i] if decode else q["slo_ttft_ms"][g, i]
+        if not lat < slo:
+            continue
+        p = power(lut["p0_w"], float(q["k_dyn_w"][g]), float(lut["sm_level"][j]), float(lut["freq_level"][k]),
+                  b / 32)
+        t = out_tok * float(lat) if decode else float(lat)
+        if not np.float32(p * t) < np.inf:
+            continue
+        res.append((p * t, j * NF + k, t, p))
+    return res
+
+
+def brute_preferred(inp):
+    q, lut = inp["llms"], inp["lut"]
+    G, K, NF = q["n_gpus"], q["max_inst"], lut["n_freq"]
+    out = {"sm_p": np.full((G, K), -1, np.int32), "f_p": np.full((G, K), -1, np.int32),
+           "sm_d": np.full((G, K), -1, np.int32), "f_d": np.full((G, K), -1, np.int32),
+           "sm_pref": np.full((G, K), np.nan), "f_pref": np.full((G, K), np.nan),
+           "feasible": np.zeros((G, K), np.uint8)}
+    for g in range(G):
+        n = int(q["n_inst"][g])
+        for i in range(K):
+            if not 0 <= n <= K or i >= n:
+                continue
+            cp, cd = phase_cells(inp, g, i, False), phase_cells(inp, g, i, True)
+            if cp:
+                _, c, tp, pp = min(cp)
+                out["sm_p"][g, i], out["f_p"][g, i] = divmod(c, NF)
+            if cd:
+                _, c, td, pd = min(cd)
+                out["sm_d"][g, i], out["f_d"][g, i] = divmod(c, NF)
+            if cp and cd:
+                sp, sd = float(lut["sm_level"][out["sm_p"][g, i]]), float(lut["sm_level"][out["sm_d"][g, i]])
+                fp, fd = float(lut["freq_level"][out["f_p"][g, i]]), float(lut["freq_level"][out["f_d"][g, i]])
+                out["sm_pref"][g, i] = (sp * tp + sd * td) / (tp + td)          # time-weighted SM share
+                out["f_pref"][g, i] = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td)   # energy-weighted
+                out["feasible"][g, i] = 1
+    return out
+
+
+def brute_ewr(n_inst, f_pref, t_ms):
+    """Per GPU: the highest preferred frequency, the waste sum t (F_g^3 - F_l^3); totals."""
+    G, K = f_pref.shape
+    fg, wg, opt = np.zeros(G), np.zeros(G), 0.0
+    for g in range(G):
+        ls = [(float(f_pref[g, i]), float(t_ms[g, i])) for i in range(K)
+              if 0 <= n_inst[g] <= K and i < n_inst[g] and np.isfinite(f_pref[g, i]) and np.isfinite(t_ms[g, i])]
+        fg[g] = max([f for f, _ in ls], default=0.0)
+        wg[g] = sum(t * (fg[g] ** 3 - f ** 3) for f, t in ls)
+        opt += sum(t * f ** 3 for f, t in ls)
+    return fg, wg, (wg.sum(), opt, wg.sum() / opt if opt else np.nan)

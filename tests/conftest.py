@@ -121,3 +121,23 @@ def golden_sweep(variant=None):
                "util": np.array([bt["util"]], np.float32),
                "sm_units": np.array(bt["sm_units"], np.int32), "sm_budget": int(bt["sm_budget"])}
     return {"lut": lut, "batches": batches}, exp, d
+
+
+def golden_preferred(variant=None):
+    """Inputs of the hand-worked preferred-configuration example (one instance), or of one
+    of its variants by name."""
+    d = load_golden("preferred_worked_example.json")
+    lut = _tables(d["lut"])
+    q = dict(d["instance"])
+    exp = d["expected"]
+    if variant is not None:
+        v = [x for x in d["variants"] if x["name"] == variant][0]
+        q.update(v["change"])
+        exp = v["expected"]
+    one = lambda v, dt: np.array([[v]], dt)
+    llms = {"n_gpus": 1, "max_inst": 1, "n_inst": np.array([1], np.int32),
+            "model": one(q["model"], np.int32), "avg_in_tokens": one(q["avg_in_tokens"], np.int32),
+            "avg_out_tokens": one(q["avg_out_tokens"], np.int32), "batch": one(q["batch"], np.int32),
+            "slo_ttft_ms": one(q["slo_ttft_ms"], np.float32), "slo_tbt_ms": one(q["slo_tbt_ms"], np.float32),
+            "k_dyn_w": np.array([q["k_dyn_w"]], np.float32)}
+    return {"lut": lut, "llms": llms}, exp, d

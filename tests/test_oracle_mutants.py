@@ -72,6 +72,26 @@ SWEEP = [
 ]
 
 
+PREFERRED = [
+    ("inclusive SLO in the phase search", "      if (!(lat < slo)) continue;", "      if (!(lat <= slo)) continue;"),
+    ("decode duration without the output length",
+     "const double t = decode ? (double)Q->avg_out_tokens[at] * (double)lat : (double)lat;\n      const double e",
+     "const double t = (double)lat;\n      const double e"),
+    ("time-weighted frequency", "o->f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);",
+     "o->f_pref = (tp * fp + td * fd) / (tp + td);"),
+    ("energy-weighted SM share", "o->sm_pref = (sp * tp + sd * td) / (tp + td);",
+     "o->sm_pref = (pp * tp * sp + pd * td * sd) / (pp * tp + pd * td);"),
+    ("decode reads the prompt row", "      const float lat = decode ? L->dc[or_cell(L, m, b - 1, j, k)]",
+     "      const float lat = decode ? L->dc[or_cell(L, m, prow, j, k)]"),
+    ("pre-admission batch in the phase power", "const double u = (double)b / 32.0;\n  const double kg = (double)Q->k_dyn_w[g];",
+     "const double u = (double)B / 32.0;\n  const double kg = (double)Q->k_dyn_w[g];"),
+    ("highest cell wins phase ties", "      if (best < 0 || e < best_e) {", "      if (best < 0 || e <= best_e) {"),
+    ("GPU frequency from the last LLM", "if ((double)f_pref[at] > fg) fg = (double)f_pref[at];", "fg = (double)f_pref[at];"),
+    ("optimal energy at the GPU frequency", "opt += t * or_cube(fl);", "opt += t * or_cube(fg);"),
+    ("waste without the cube", "wg += t * (or_cube(fg) - or_cube(fl));", "wg += t * (fg - fl);"),
+]
+
+
 def _run_pins(tmp_path, name, old, new, suite):
     src = open(SRC).read()
     assert src.count(old) == 1, f"mutation anchor not unique/present: {name}"
@@ -102,4 +122,10 @@ def test_migration_pins_reject_mutant(tmp_path, name, old, new):
 @pytest.mark.parametrize("name,old,new", SWEEP, ids=[p[0] for p in SWEEP])
 def test_sweep_pins_reject_mutant(tmp_path, name, old, new):
     rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_sweep_pins.py")
+    assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
+
+
+@pytest.mark.parametrize("name,old,new", PREFERRED, ids=[p[0] for p in PREFERRED])
+def test_preferred_pins_reject_mutant(tmp_path, name, old, new):
+    rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_preferred_pins.py")
     assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
