@@ -22,7 +22,8 @@ PLACEMENT = [
      "const double f3 = (double)L->freq_level[k];\n  const double kg = (double)G->k_dyn_w[g];"),
     ("inclusive SLO test", "if (!(ttft < Q->slo_ttft_ms[r] && tbt < Q->slo_tbt_ms[r])) return 0;",
      "if (!(ttft <= Q->slo_ttft_ms[r] && tbt <= Q->slo_tbt_ms[r])) return 0;"),
-    ("pre-admission batch in u", "const double u = (double)b / 32.0;", "const double u = (double)B / 32.0;"),
+    ("pre-admission batch in u", "const double u = (double)b / 32.0;\n  const double f3",
+     "const double u = (double)B / 32.0;\n  const double f3"),
     ("TTFT read from the batch row", "L->pf[or_cell(L, m, row_p, jp, k)]", "L->pf[or_cell(L, m, b - 1, jp, k)]"),
     ("decode cap taken from prefill cap", "const int jd = j < cd ? j : cd;", "const int jd = j < cp ? j : cp;"),
     ("highest index wins ties", "if (best_idx < 0 || e < best_e) {", "if (best_idx < 0 || e <= best_e) {"),
