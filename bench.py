@@ -16,7 +16,9 @@ Also reported: the roofline position of the dominant kernel (placement scoring,
 timed alone with HIP events recorded around it inside the library), and the CPU
 oracle timed on a bounded sample of the same workload on this host.  Outside the
 timed steps, ``next_rows`` measures the local schedulers' SM/frequency sweep over
-1,024 GPUs x 64 epochs of task batches (one kernel per call) the same way.
+1,024 GPUs x 64 epochs of task batches (one kernel per call), and the preferred
+configuration of every LLM instance on a 2,048-GPU fleet plus the fleet's energy waste
+ratio, the same way.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --per-config     (one JSON line per configuration, then the step line)
@@ -156,25 +158,69 @@ def load_traffic(path=TRAFFIC_FILE, src=KERNEL_SRC):
     return d.get("hbm_bytes_per_launch")
 
 
-def sweep_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
-    """The local SM/frequency sweep: kernel time from HIP events around each call (one
-    launch per call), its roofline position, and the oracle on the same batches."""
-    inp = W.make_sweep()
-    ds = F.DeviceSweep(inp, "cuda")
+def timed_calls(hip, torch, fn, calls, warmup):
+    """Mean duration (ms) of fn() over `calls` calls, HIP events recorded around each."""
     for _ in range(warmup):
-        ds.run()
+        fn()
     torch.cuda.synchronize()
     st = torch.cuda.current_stream().cuda_stream
     evs = [(hip.event(), hip.event()) for _ in range(calls)]
     for a, b in evs:
         hip.record(a, st)
-        ds.run()
+        fn()
         hip.record(b, st)
     torch.cuda.synchronize()
     ms = float(np.mean([hip.elapsed_ms(a, b) for a, b in evs]))
     for a, b in evs:
         hip.destroy(a)
         hip.destroy(b)
+    return ms
+
+
+def preferred_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
+    """Preferred configurations of every LLM instance (one launch) and the fleet's EWR
+    (two launches): durations from HIP events around each call, roofline position, and
+    the oracle on the same instances."""
+    inp = W.make_llms()
+    dp = F.DevicePreferred(inp, "cuda")
+    pref_ms = timed_calls(hip, torch, dp.run_preferred, calls, warmup)
+    ewr_ms = timed_calls(hip, torch, dp.run_ewr, calls, warmup)
+    q, lut = inp["llms"], inp["lut"]
+    G, K = q["n_gpus"], q["max_inst"]
+    live = int((np.arange(K)[None, :] < q["n_inst"][:, None]).sum())
+    cells = 2 * live * lut["n_sm"] * lut["n_freq"]           # both phases of every instance
+    nbytes = G * K * (6 * 4) + G * 8 + G * K * (4 * 4 + 7 * 4 + 1) + 2 * lut["pf"].nbytes
+    row = {
+        "workload": ("preferred configuration of every LLM instance on a 2048-GPU fleet (1-4 instances "
+                     "per GPU, 32 models, 8 SM x 16 freq levels, both phases) + the fleet's EWR"),
+        "instances": live, "cells": cells, "preferred_kernel_ms": pref_ms, "ewr_ms": ewr_ms,
+        "cells_per_s": cells / (pref_ms * 1e-3),
+        "roofline": {"kernel": "k_preferred", "bound": "hbm", "achieved": nbytes / (pref_ms * 1e-3) / 1e9,
+                     "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": nbytes / (pref_ms * 1e-3) / HBM_PEAK,
+                     "traffic": None, "algorithmic_bytes": nbytes},
+        "cpu_baseline": None,
+    }
+    if with_cpu:
+        import oracle
+        got = dp.results()
+        t0 = time.perf_counter()
+        ref = oracle.preferred(inp)
+        t1 = time.perf_counter()
+        row["cpu_baseline"] = {
+            "value": cells / (t1 - t0), "unit": "cells/s", "cores": 1, "kind": "oracle",
+            "sample": f"all {live} instances ({t1 - t0:.3f} s); single-threaded C, float64, gcc -O2",
+            "agreement": {"flags_equal": float(np.mean(got["feasible"] == ref["feasible"])),
+                          "cells_equal": float(np.mean((got["sm_p"] == ref["sm_p"]) & (got["f_p"] == ref["f_p"])
+                                                       & (got["sm_d"] == ref["sm_d"]) & (got["f_d"] == ref["f_d"])))}}
+    return row
+
+
+def sweep_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
+    """The local SM/frequency sweep: kernel time from HIP events around each call (one
+    launch per call), its roofline position, and the oracle on the same batches."""
+    inp = W.make_sweep()
+    ds = F.DeviceSweep(inp, "cuda")
+    ms = timed_calls(hip, torch, ds.run, calls, warmup)
     bt = inp["batches"]
     cells, ops = sweep_work(inp)
     nbytes = sweep_bytes(inp)
@@ -347,7 +393,8 @@ def main():
         "kernels_ms": {"k_score": score_ms, "k_migrate": pairs_ms,
                        "migration_pairs_per_s_kernel": n_pairs / (pairs_ms * 1e-3)},
         "cpu_baseline": None,
-        "next_rows": {"sweep": sweep_row(F, W, hip, torch, not args.no_cpu_baseline)},
+        "next_rows": {"sweep": sweep_row(F, W, hip, torch, not args.no_cpu_baseline),
+                      "preferred": preferred_row(F, W, hip, torch, not args.no_cpu_baseline)},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(place, fleet, gpu_place, gpu_mig)

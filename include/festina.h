@@ -16,6 +16,12 @@
  *       once (Sec. 3.4, runtime resource allocation): per batch, the least-energy
  *       frequency level at which every task meets its deadline on its smallest
  *       sufficient SM share and the shares fit the device.
+ * and, as inputs of the consolidation algorithm (App. E, Sec. 3.5.1):
+ *   festina_preferred_configs -- every active LLM's preferred configuration: the
+ *       least-energy SLO-feasible cell of each phase, then the time-weighted SM share
+ *       and energy-weighted frequency (Eq. preferred_sm, Eq. preferred_frequency);
+ *   festina_fleet_ewr         -- the fleet's energy waste, optimal energy and energy
+ *       waste ratio (Eq. energy_waste, energy_optimal, energy_waste_ratio).
  *
  * Conventions shared by every entry point
  *  - All array pointers inside the structs are DEVICE pointers (HIP global memory
@@ -229,6 +235,74 @@ typedef struct festina_sweep_result {
  * `stream`. */
 festina_status festina_sweep_batches(const festina_lut *lut, const festina_batches *batches,
                                      festina_sweep_result *out, void *stream);
+
+/* Active LLM instances (App. E: per LLM, the average input/output lengths over the last
+ * window; Sec. 3.5.2 Phase One).  Slot i of GPU g is an instance when i < n_inst[g].  Its
+ * prefill phase lasts TTFT = pf[model][prompt row of avg_in_tokens][j][k], its decode phase
+ * avg_out_tokens x TBT with TBT = dc[model][batch row][j][k] (batch row =
+ * min(batch + 1, 32) - 1); each must be strictly below its SLO.  Power is
+ * p0_w + k_dyn_w[g] * s_j * f_k^3 * u with u = min(batch + 1, 32) / 32.  A model id out of
+ * range, batch < 0, avg_in_tokens < 1, avg_out_tokens < 0, or n_inst outside
+ * [0, max_inst] makes the instance infeasible. */
+typedef struct festina_llms {
+  int32_t n_gpus;                    /* G >= 0 */
+  int32_t max_inst;                  /* K >= 1 slots per GPU */
+  const int32_t *n_inst;             /* [G] */
+  const int32_t *model;              /* [G][K] */
+  const int32_t *avg_in_tokens;      /* [G][K] */
+  const int32_t *avg_out_tokens;     /* [G][K] */
+  const int32_t *batch;              /* [G][K] current decode batch B */
+  const float *slo_ttft_ms;          /* [G][K] */
+  const float *slo_tbt_ms;           /* [G][K] */
+  const float *k_dyn_w;              /* [G] */
+} festina_llms;
+
+/* Preferred configurations, [G][K] each (device memory, written by the call):
+ *   sm_p, f_p / sm_d, f_d = SM and frequency level of the least-energy feasible cell of
+ *       the prefill / decode phase (energy = power x duration; lowest cell j*NF + k on
+ *       exact ties); -1 when the phase has no feasible cell;
+ *   t_p_ms, p_p_w / t_d_ms, p_d_w = that cell's duration and power (0 when none);
+ *   t_ms = t_p_ms + t_d_ms, the instance's execution time t_l of Eq. energy_waste;
+ *   sm_pref = (s_p t_p + s_d t_d) / (t_p + t_d)                    (Eq. preferred_sm),
+ *   f_pref  = (P_p t_p f_p + P_d t_d f_d) / (P_p t_p + P_d t_d)    (Eq. preferred_frequency),
+ *       as SM share and normalised frequency, NaN unless both phases have a cell;
+ *   feasible = 1 when both phases have a cell. */
+typedef struct festina_preferred {
+  int32_t *sm_p, *f_p, *sm_d, *f_d;
+  float *t_p_ms, *t_d_ms, *p_p_w, *p_d_w;
+  float *t_ms;
+  float *sm_pref, *f_pref;
+  uint8_t *feasible;
+} festina_preferred;
+
+/* Preferred configuration of every instance slot (App. E).  Needs no workspace; requires
+ * n_sm * n_freq <= FESTINA_MAX_CELLS.  One kernel launch on `stream`. */
+festina_status festina_preferred_configs(const festina_lut *lut, const festina_llms *llms,
+                                         festina_preferred *out, void *stream);
+
+/* Energy waste of a fleet (Sec. 3.5.1), device memory written by the call:
+ *   f_gpu[g]     = F_g, the highest preferred frequency among GPU g's instances (0 if none);
+ *   waste_gpu[g] = sum over its instances of t_l * (F_g^3 - F_l^3), float64;
+ *   totals[0]    = E_waste = sum of waste_gpu; totals[1] = E_optimal = sum of t_l * F_l^3;
+ *   totals[2]    = EWR = E_waste / E_optimal. */
+typedef struct festina_ewr {
+  float *f_gpu;
+  double *waste_gpu;
+  double *totals;
+} festina_ewr;
+
+/* Bytes of device workspace festina_fleet_ewr needs (0 for n_gpus < 1). */
+size_t festina_ewr_workspace_bytes(int32_t n_gpus);
+
+/* EWR of the fleet whose instance slots [n_gpus][max_inst] hold preferred frequencies
+ * f_pref and execution times t_ms (device pointers; e.g. festina_preferred_configs'
+ * f_pref and t_ms).  Slots past n_inst[g], and slots whose frequency or time is
+ * not finite, are left out.  Workspace 256-byte aligned, contents clobbered; one kernel
+ * launch on `stream` up to 16,384 GPUs, two beyond; the totals are summed in a fixed
+ * order (deterministic). */
+festina_status festina_fleet_ewr(int32_t n_gpus, int32_t max_inst, const int32_t *n_inst,
+                                 const float *f_pref, const float *t_ms, festina_ewr *out,
+                                 void *workspace, size_t workspace_bytes, void *stream);
 
 /* Measurement hook, not part of the search.  While set, festina_score_placements
  * records `score_begin` on its stream immediately before its scoring kernel and

@@ -113,6 +113,9 @@ def lib():
         L.festina_oracle_phase_cell.argtypes = [P(_Lut), P(_Llms), C.c_int32, C.c_int32, C.c_int32,
                                                 C.c_int32, C.c_int32, P(C.c_double), P(C.c_double)]
         L.festina_oracle_phase_cell.restype = C.c_int
+        L.festina_oracle_preferred_at.argtypes = [P(_Lut), P(_Llms), C.c_int32, C.c_int32, C.c_int32,
+                                                  C.c_int32, C.c_int32, C.c_int32, P(C.c_double), P(C.c_double)]
+        L.festina_oracle_preferred_at.restype = C.c_int
         L.festina_oracle_fleet_ewr.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                                C.c_void_p, C.c_void_p, C.c_void_p]
         L.festina_oracle_fleet_ewr.restype = C.c_int
@@ -336,3 +339,13 @@ def fleet_ewr(n_inst, f_pref, t_ms):
     if rc != 0:
         raise ValueError("oracle rejected the EWR arguments")
     return fg, wg, (float(tot[0]), float(tot[1]), float(tot[2]))
+
+
+def preferred_at(inp: dict, g: int, i: int, jp: int, kp: int, jd: int, kd: int):
+    """(feasible, sm_pref, f_pref) of instance (g, i) at the given prefill and decode cells."""
+    pin = _Pinned()
+    lut, q = _lut(inp["lut"], pin), _llms(inp["llms"], pin)
+    sm, f = C.c_double(0.0), C.c_double(0.0)
+    ok = lib().festina_oracle_preferred_at(C.byref(lut), C.byref(q), int(g), int(i), int(jp), int(kp), int(jd),
+                                           int(kd), C.byref(sm), C.byref(f))
+    return bool(ok), float(sm.value), float(f.value)

@@ -14,6 +14,10 @@ Sweep, per batch: the flag exactly; the tested level must be usable under the or
 its energy within ``rtol`` of the oracle's float64 energy at that level, a level other
 than the oracle's only as a near-tie, and every task's SM level equal to the oracle's
 smallest sufficient level at the tested frequency level.
+Preferred configuration, per instance slot: the flag exactly; each phase's tested cell
+feasible under the oracle, at most the oracle's least energy times (1 + rtol), with its
+duration and power within ``rtol``; the two averages within ``rtol`` of the oracle's at
+the tested cells.  EWR: per-GPU frequencies exactly, waste and totals within 1e-9.
 """
 from __future__ import annotations
 
@@ -21,7 +25,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-from . import candidate_energy, min_sm, pair_saving, sweep_level
+from . import candidate_energy, min_sm, pair_saving, phase_cell, preferred_at, sweep_level
 
 RTOL = 1e-5
 
@@ -148,4 +152,90 @@ def check_sweep(inp, sel, oracle_out, gpu_out, rtol=RTOL) -> Report:
                 rep.near_ties += 1
             else:
                 rep.mismatches.append((b, "level", k, int(ol[i]), e_at, float(oe[i])))
+    return rep
+
+
+def _rel(a, b):
+    return abs(float(a) - float(b)) / max(abs(float(b)), 1e-30)
+
+
+def check_preferred(inp, oracle_out, gpu_out, rtol=RTOL) -> Report:
+    """``oracle_out``: oracle.preferred(inp); ``gpu_out``: the same keys from the device
+    (t_p_ms/t_d_ms/p_p_w/p_d_w/t_ms names for durations and powers)."""
+    q = inp["llms"]
+    G, K = int(q["n_gpus"]), int(q["max_inst"])
+    o, d = oracle_out, gpu_out
+    rep = Report(n=G * K)
+    for g in range(G):
+        for i in range(K):
+            if int(d["feasible"][g, i]) != int(o["feasible"][g, i]):
+                rep.mismatches.append(((g, i), "feasible", int(d["feasible"][g, i]), int(o["feasible"][g, i])))
+                continue
+            bad = False
+            same = True
+            for decode, js, ks, tk, pk, ot, op in ((False, "sm_p", "f_p", "t_p_ms", "p_p_w", "t_p", "p_p"),
+                                                    (True, "sm_d", "f_d", "t_d_ms", "p_d_w", "t_d", "p_d")):
+                gj, gk, oj = int(d[js][g, i]), int(d[ks][g, i]), int(o[js][g, i])
+                if (gj < 0) != (oj < 0):
+                    rep.mismatches.append(((g, i), f"{js} presence", gj, oj))
+                    bad = True
+                    break
+                if gj < 0:
+                    continue
+                ok, t, p = phase_cell(inp, g, i, decode, gj, gk)
+                if not ok:
+                    rep.mismatches.append(((g, i), f"{js} cell infeasible under the oracle", (gj, gk)))
+                    bad = True
+                    break
+                for got, want, what in ((d[tk][g, i], t, tk), (d[pk][g, i], p, pk)):
+                    r = _rel(got, want)
+                    rep.max_rel_err = max(rep.max_rel_err, r)
+                    if r > rtol:
+                        rep.mismatches.append(((g, i), what, float(got), want))
+                        bad = True
+                if (gj, gk) != (oj, int(o[ks][g, i])):
+                    same = False
+                    if p * t <= float(o[op][g, i] * o[ot][g, i]) * (1 + rtol) + 1e-30:
+                        rep.near_ties += 1
+                    else:
+                        rep.mismatches.append(((g, i), f"{js} cell", (gj, gk), (oj, int(o[ks][g, i]))))
+                        bad = True
+            if bad or not o["feasible"][g, i]:
+                if not bad and not (np.isnan(d["sm_pref"][g, i]) and np.isnan(d["f_pref"][g, i])):
+                    rep.mismatches.append(((g, i), "averages of an infeasible slot", float(d["sm_pref"][g, i])))
+                continue
+            if same:
+                want_sm, want_f, want_t = o["sm_pref"][g, i], o["f_pref"][g, i], o["t_p"][g, i] + o["t_d"][g, i]
+            else:
+                _, want_sm, want_f = preferred_at(inp, g, i, d["sm_p"][g, i], d["f_p"][g, i], d["sm_d"][g, i],
+                                                  d["f_d"][g, i])
+                want_t = phase_cell(inp, g, i, False, d["sm_p"][g, i], d["f_p"][g, i])[1] + \
+                    phase_cell(inp, g, i, True, d["sm_d"][g, i], d["f_d"][g, i])[1]
+            for got, want, what in ((d["sm_pref"][g, i], want_sm, "sm_pref"), (d["f_pref"][g, i], want_f, "f_pref"),
+                                    (d["t_ms"][g, i], want_t, "t_ms")):
+                r = _rel(got, want)
+                rep.max_rel_err = max(rep.max_rel_err, r)
+                if r > rtol:
+                    rep.mismatches.append(((g, i), what, float(got), float(want)))
+    return rep
+
+
+def check_ewr(oracle_out, gpu_out, rtol=1e-9) -> Report:
+    """``oracle_out``: oracle.fleet_ewr(...) on the same inputs; ``gpu_out``:
+    (f_gpu, waste_gpu, totals[3]) from the device."""
+    of, ow, ot = oracle_out
+    gf, gw, gt = gpu_out
+    rep = Report(n=len(of))
+    if not np.array_equal(np.asarray(gf, np.float64), np.asarray(of, np.float64)):
+        bad = np.flatnonzero(np.asarray(gf, np.float64) != np.asarray(of, np.float64))[:5]
+        rep.mismatches.append(("f_gpu", [(int(b), float(gf[b]), float(of[b])) for b in bad]))
+    scale = max(abs(ot[0]), abs(ot[1]) * 1e-6, 1e-30)
+    dw = np.abs(np.asarray(gw) - np.asarray(ow))
+    if np.any(dw > rtol * scale):
+        rep.mismatches.append(("waste_gpu", float(dw.max())))
+    for k, name in enumerate(("e_waste", "e_optimal", "ewr")):
+        r = _rel(gt[k], ot[k]) if ot[k] != 0 else abs(float(gt[k]))
+        rep.max_rel_err = max(rep.max_rel_err, r)
+        if not (r <= rtol or (np.isnan(gt[k]) and np.isnan(ot[k]))):
+            rep.mismatches.append((name, float(gt[k]), float(ot[k])))
     return rep

@@ -584,3 +584,17 @@ int festina_oracle_fleet_ewr(int32_t n_gpus, int32_t max_inst, const int32_t *n_
   totals[2] = waste / opt;
   return 0;
 }
+
+/* The two averages of instance (g, i) at given cells of each phase (for checking another
+ * implementation's near-tie choice): 1 when both cells are feasible. */
+int festina_oracle_preferred_at(const or_lut *L, const or_llms *Q, int32_t g, int32_t i, int32_t jp, int32_t kp,
+                                int32_t jd, int32_t kd, double *sm_pref, double *f_pref) {
+  double tp, pp, td, pd;
+  if (!festina_oracle_phase_cell(L, Q, g, i, 0, jp, kp, &tp, &pp)) return 0;
+  if (!festina_oracle_phase_cell(L, Q, g, i, 1, jd, kd, &td, &pd)) return 0;
+  const double sp = (double)L->sm_level[jp], sd = (double)L->sm_level[jd];
+  const double fp = (double)L->freq_level[kp], fd = (double)L->freq_level[kd];
+  *sm_pref = (sp * tp + sd * td) / (tp + td);
+  *f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);
+  return 1;
+}

@@ -1,7 +1,8 @@
 """Thin ctypes binding of the C ABI in include/festina.h.
 
 Argument marshalling only: every step of the search runs in the HIP library
-(``libfestina.so`` built from ``csrc/festina.hip`` and ``csrc/sweep.hip``).  PyTorch provides device
+(``libfestina.so`` built from ``csrc/festina.hip``, ``csrc/sweep.hip`` and
+``csrc/preferred.hip``).  PyTorch provides device
 memory and streams.  There is no CPU fallback: if the library is missing this
 module raises.
 """
@@ -74,9 +75,27 @@ class festina_sweep_result(C.Structure):
                 ("task_sm", C.c_void_p)]
 
 
+class festina_llms(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("max_inst", C.c_int32), ("n_inst", C.c_void_p),
+                ("model", C.c_void_p), ("avg_in_tokens", C.c_void_p), ("avg_out_tokens", C.c_void_p),
+                ("batch", C.c_void_p), ("slo_ttft_ms", C.c_void_p), ("slo_tbt_ms", C.c_void_p),
+                ("k_dyn_w", C.c_void_p)]
+
+
+class festina_preferred(C.Structure):
+    _fields_ = [("sm_p", C.c_void_p), ("f_p", C.c_void_p), ("sm_d", C.c_void_p), ("f_d", C.c_void_p),
+                ("t_p_ms", C.c_void_p), ("t_d_ms", C.c_void_p), ("p_p_w", C.c_void_p), ("p_d_w", C.c_void_p),
+                ("t_ms", C.c_void_p), ("sm_pref", C.c_void_p), ("f_pref", C.c_void_p), ("feasible", C.c_void_p)]
+
+
+class festina_ewr(C.Structure):
+    _fields_ = [("f_gpu", C.c_void_p), ("waste_gpu", C.c_void_p), ("totals", C.c_void_p)]
+
+
 EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_workspace_bytes",
             "festina_score_placements", "festina_migrations_workspace_bytes", "festina_score_migrations",
-            "festina_sweep_batches", "festina_set_timing_events")
+            "festina_sweep_batches", "festina_preferred_configs", "festina_ewr_workspace_bytes",
+            "festina_fleet_ewr", "festina_set_timing_events")
 
 _lib = None
 
@@ -105,6 +124,14 @@ def lib():
         L.festina_sweep_batches.argtypes = [P(festina_lut), P(festina_batches), P(festina_sweep_result),
                                             C.c_void_p]
         L.festina_sweep_batches.restype = C.c_int
+        L.festina_preferred_configs.argtypes = [P(festina_lut), P(festina_llms), P(festina_preferred),
+                                                C.c_void_p]
+        L.festina_preferred_configs.restype = C.c_int
+        L.festina_ewr_workspace_bytes.argtypes = [C.c_int32]
+        L.festina_ewr_workspace_bytes.restype = C.c_size_t
+        L.festina_fleet_ewr.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                        P(festina_ewr), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.festina_fleet_ewr.restype = C.c_int
         L.festina_set_timing_events.argtypes = [C.c_void_p] * 4
         L.festina_set_timing_events.restype = None
         _lib = L
@@ -269,6 +296,72 @@ class DeviceSweep:
                 self.task_sm[:B].cpu().numpy())
 
 
+PREF_INT = ("sm_p", "f_p", "sm_d", "f_d")
+PREF_FLOAT = ("t_p_ms", "t_d_ms", "p_p_w", "p_d_w", "t_ms", "sm_pref", "f_pref")
+
+
+class DevicePreferred:
+    """Active LLM instances copied to device memory once; run() computes every preferred
+    configuration and then the fleet's EWR from them (execution time t_ms = t_p + t_d)."""
+
+    def __init__(self, inp: dict, device="cuda"):
+        import torch
+        lut, q = inp["lut"], inp["llms"]
+        d = lambda a, t: _dev(a, t, device)
+        self.t = {
+            "freq_level": d(lut["freq_level"], np.float32), "sm_level": d(lut["sm_level"], np.float32),
+            "pf": d(lut["pf"], np.float32), "dc": d(lut["dc"], np.float32),
+        }
+        for k in ("n_inst", "model", "avg_in_tokens", "avg_out_tokens", "batch"):
+            self.t[k] = d(q[k], np.int32)
+        for k in ("slo_ttft_ms", "slo_tbt_ms", "k_dyn_w"):
+            self.t[k] = d(q[k], np.float32)
+        t = self.t
+        self.lut = festina_lut(int(lut["n_models"]), int(lut["n_rows"]), int(lut["n_sm"]), int(lut["n_freq"]),
+                               _ptr(t["sm_level"]), _ptr(t["freq_level"]), _ptr(t["pf"]), _ptr(t["dc"]),
+                               float(lut["p0_w"]))
+        self.G, self.K = int(q["n_gpus"]), int(q["max_inst"])
+        self.llms = festina_llms(self.G, self.K, _ptr(t["n_inst"]), _ptr(t["model"]), _ptr(t["avg_in_tokens"]),
+                                 _ptr(t["avg_out_tokens"]), _ptr(t["batch"]), _ptr(t["slo_ttft_ms"]),
+                                 _ptr(t["slo_tbt_ms"]), _ptr(t["k_dyn_w"]))
+        n = max(self.G * self.K, 1)
+        self.o = {k: torch.empty(n, dtype=torch.int32, device=device) for k in PREF_INT}
+        self.o.update({k: torch.empty(n, dtype=torch.float32, device=device) for k in PREF_FLOAT})
+        self.o["feasible"] = torch.empty(n, dtype=torch.uint8, device=device)
+        self.out = festina_preferred(*(_ptr(self.o[k]) for k in PREF_INT + PREF_FLOAT + ("feasible",)))
+        g = max(self.G, 1)
+        self.f_gpu = torch.empty(g, dtype=torch.float32, device=device)
+        self.waste_gpu = torch.empty(g, dtype=torch.float64, device=device)
+        self.totals = torch.empty(3, dtype=torch.float64, device=device)
+        self.ewr = festina_ewr(_ptr(self.f_gpu), _ptr(self.waste_gpu), _ptr(self.totals))
+        self.ws_bytes = festina_ewr_workspace_bytes(self.G)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
+
+    def run_preferred(self, stream=None):
+        festina_preferred_configs(self.lut, self.llms, self.out, stream)
+
+    def run_ewr(self, f_pref=None, t_ms=None, stream=None):
+        """EWR from device tensors f_pref/t_ms [G*K] (default: this object's own results)."""
+        if f_pref is None:
+            f_pref = self.o["f_pref"]
+            t_ms = self.o["t_ms"]
+        festina_fleet_ewr(self.G, self.K, self.t["n_inst"], f_pref, t_ms, self.ewr, self.workspace,
+                          self.ws_bytes, stream)
+
+    def run(self, stream=None):
+        """Preferred configurations, then the EWR of the fleet from them."""
+        self.run_preferred(stream)
+        self.run_ewr(stream=stream)
+
+    def results(self):
+        G, K = self.G, self.K
+        r = {k: self.o[k][:G * K].cpu().numpy().reshape(G, K) for k in PREF_INT + PREF_FLOAT + ("feasible",)}
+        return r
+
+    def ewr_results(self):
+        return self.f_gpu[:self.G].cpu().numpy(), self.waste_gpu[:self.G].cpu().numpy(), self.totals.cpu().numpy()
+
+
 # ------------------------------------------------------------------ the ABI calls
 def festina_placements_workspace_bytes(lut, gpus, req) -> int:
     return int(lib().festina_placements_workspace_bytes(C.byref(lut), C.byref(gpus), C.byref(req)))
@@ -298,3 +391,21 @@ def festina_sweep_batches(lut, batches, out, stream=None) -> None:
     st = lib().festina_sweep_batches(C.byref(lut), C.byref(batches), C.byref(out), _stream_handle(stream))
     if st != FESTINA_OK:
         raise FestinaError(st, "festina_sweep_batches")
+
+
+def festina_preferred_configs(lut, llms, out, stream=None) -> None:
+    st = lib().festina_preferred_configs(C.byref(lut), C.byref(llms), C.byref(out), _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_preferred_configs")
+
+
+def festina_ewr_workspace_bytes(n_gpus: int) -> int:
+    return int(lib().festina_ewr_workspace_bytes(int(n_gpus)))
+
+
+def festina_fleet_ewr(n_gpus, max_inst, n_inst, f_pref, t_ms, out, workspace, workspace_bytes, stream=None) -> None:
+    ws = None if workspace is None else C.c_void_p(workspace.data_ptr())
+    st = lib().festina_fleet_ewr(int(n_gpus), int(max_inst), _ptr(n_inst), _ptr(f_pref), _ptr(t_ms), C.byref(out),
+                                 ws, int(workspace_bytes), _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_fleet_ewr")

@@ -190,3 +190,50 @@ def test_sweep_rejects_bad_arguments(lib):
     bat.n_tasks = None
     out.task_sm = None
     assert _sweep_status(lut, bat, out) == F.FESTINA_OK
+
+
+@no_gpu
+def test_preferred_and_ewr_reject_bad_arguments(lib):
+    fake = C.c_void_p(0x1000)
+    L = F.lib()
+
+    def structs(NS=4, NF=8, G=4, K=2):
+        lut = F.festina_lut(2, 32, NS, NF, fake, fake, fake, fake, 120.0)
+        q = F.festina_llms(G, K, *([fake] * 8))
+        out = F.festina_preferred(*([fake] * 12))
+        return lut, q, out
+
+    call = lambda lut, q, out: L.festina_preferred_configs(C.byref(lut), C.byref(q), C.byref(out), None)
+    lut, q, out = structs()
+    assert L.festina_preferred_configs(None, C.byref(q), C.byref(out), None) == F.FESTINA_ERR_INVALID
+    assert L.festina_preferred_configs(C.byref(lut), None, C.byref(out), None) == F.FESTINA_ERR_INVALID
+    assert call(*structs(NS=16, NF=17)) == F.FESTINA_ERR_UNSUPPORTED
+    for field in ("n_inst", "avg_out_tokens", "k_dyn_w"):
+        lut, q, out = structs()
+        setattr(q, field, None)
+        assert call(lut, q, out) == F.FESTINA_ERR_INVALID, field
+    for field in ("sm_p", "t_ms", "f_pref", "feasible"):
+        lut, q, out = structs()
+        setattr(out, field, None)
+        assert call(lut, q, out) == F.FESTINA_ERR_INVALID, field
+    lut, q, out = structs()
+    q.max_inst = 0
+    assert call(lut, q, out) == F.FESTINA_ERR_INVALID
+    lut, q, out = structs(G=0)
+    q.n_inst = None
+    assert call(lut, q, out) == F.FESTINA_OK
+
+    assert F.festina_ewr_workspace_bytes(0) == 0
+    assert F.festina_ewr_workspace_bytes(1) == 256 and F.festina_ewr_workspace_bytes(257) == 256
+    assert F.festina_ewr_workspace_bytes(256 * 17) == 512
+    ewr = F.festina_ewr(fake, fake, fake)
+    ws = C.c_void_p(0x100000)
+    ecall = lambda G, K, n, out, w, nb: L.festina_fleet_ewr(G, K, n, fake, fake, C.byref(out) if out else None,
+                                                            w, nb, None)
+    assert ecall(0, 4, fake, ewr, ws, 256) == F.FESTINA_ERR_INVALID
+    assert ecall(8, 0, fake, ewr, ws, 256) == F.FESTINA_ERR_INVALID
+    assert ecall(8, 4, None, ewr, ws, 256) == F.FESTINA_ERR_INVALID
+    assert ecall(8, 4, fake, None, ws, 256) == F.FESTINA_ERR_INVALID
+    assert ecall(8, 4, fake, ewr, ws, 255) == F.FESTINA_ERR_INVALID
+    assert ecall(8, 4, fake, ewr, C.c_void_p(0x100010), 256) == F.FESTINA_ERR_INVALID
+    assert ecall(8, 4, fake, ewr, None, 256) == F.FESTINA_ERR_INVALID
