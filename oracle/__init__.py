@@ -76,6 +76,18 @@ class _Pref(C.Structure):
                 ("sm_pref", C.c_double), ("f_pref", C.c_double), ("feasible", C.c_int)]
 
 
+class _Avail(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("n_steps", C.c_int32), ("freq_cur", C.c_void_p), ("batch", C.c_void_p),
+                ("k_dyn_w", C.c_void_p), ("resident", C.c_void_p), ("t_avail_ms", C.c_void_p),
+                ("mem_free_mib", C.c_void_p), ("sm_free", C.c_void_p), ("kv_kib_per_token", C.c_void_p),
+                ("k_new_w", C.c_float)]
+
+
+class _Dispatch(C.Structure):
+    _fields_ = [("gpu", C.c_int32), ("freq_level", C.c_int32), ("sm_level", C.c_int32), ("phase", C.c_int32),
+                ("energy", C.c_double)]
+
+
 def lib():
     global _lib
     if _lib is None:
@@ -116,6 +128,8 @@ def lib():
         L.festina_oracle_preferred_at.argtypes = [P(_Lut), P(_Llms), C.c_int32, C.c_int32, C.c_int32,
                                                   C.c_int32, C.c_int32, C.c_int32, P(C.c_double), P(C.c_double)]
         L.festina_oracle_preferred_at.restype = C.c_int
+        L.festina_oracle_dispatch.argtypes = [P(_Lut), P(_Avail), P(_Requests), C.c_int32, C.c_void_p, C.c_void_p]
+        L.festina_oracle_dispatch.restype = C.c_int
         L.festina_oracle_fleet_ewr.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                                C.c_void_p, C.c_void_p, C.c_void_p]
         L.festina_oracle_fleet_ewr.restype = C.c_int
@@ -188,6 +202,13 @@ def _llms(d, pin):
                  pin(d["avg_in_tokens"], np.int32), pin(d["avg_out_tokens"], np.int32),
                  pin(d["batch"], np.int32), pin(d["slo_ttft_ms"], np.float32), pin(d["slo_tbt_ms"], np.float32),
                  pin(d["k_dyn_w"], np.float32))
+
+
+def _avail(d, pin):
+    return _Avail(int(d["n_gpus"]), int(d["n_steps"]), pin(d["freq_cur"], np.int32), pin(d["batch"], np.int32),
+                  pin(d["k_dyn_w"], np.float32), pin(d["resident"], np.uint32), pin(d["t_avail_ms"], np.float32),
+                  pin(d["mem_free_mib"], np.int32), pin(d["sm_free"], np.int32),
+                  pin(d["kv_kib_per_token"], np.int32), float(d["k_new_w"]))
 
 
 # ------------------------------------------------------------------ public API
@@ -349,3 +370,19 @@ def preferred_at(inp: dict, g: int, i: int, jp: int, kp: int, jd: int, kd: int):
     ok = lib().festina_oracle_preferred_at(C.byref(lut), C.byref(q), int(g), int(i), int(jp), int(kp), int(jd),
                                            int(kd), C.byref(sm), C.byref(f))
     return bool(ok), float(sm.value), float(f.value)
+
+
+def dispatch(inp: dict, sel=None):
+    """Oracle current-frequency dispatch (Sec. 3.3, Phases One to Three) of all requests (or
+    the ids in ``sel``).  Returns (gpu, freq_level, sm_level, phase int32, energy float64)."""
+    pin = _Pinned()
+    lut, av, req = _lut(inp["lut"], pin), _avail(inp["avail"], pin), _requests(inp["requests"], pin)
+    n = int(inp["requests"]["n_requests"]) if sel is None else len(sel)
+    sel_a = None if sel is None else _arr(sel, np.int32)
+    buf = (_Dispatch * max(n, 1))()
+    rc = lib().festina_oracle_dispatch(C.byref(lut), C.byref(av), C.byref(req), n, _p(sel_a), C.cast(buf, C.c_void_p))
+    if rc != 0:
+        raise ValueError("oracle rejected the dispatch arguments")
+    a = np.frombuffer(buf, dtype=np.dtype([("gpu", "<i4"), ("freq_level", "<i4"), ("sm_level", "<i4"),
+                                           ("phase", "<i4"), ("energy", "<f8")]), count=n)
+    return (a["gpu"].copy(), a["freq_level"].copy(), a["sm_level"].copy(), a["phase"].copy(), a["energy"].copy())

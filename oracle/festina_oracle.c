@@ -48,6 +48,9 @@
  *     F_l = (P_p T_p f_p + P_d T_d f_d) / (P_p T_p + P_d T_d); per GPU F_g = max F_l,
  *     E_waste = sum t_l (F_g^3 - F_l^3), E_optimal = sum t_l F_l^3, EWR = their ratio.
  *
+ *   current-frequency dispatch (Sec. 3.3 as the paper runs it, Phases One to Three with
+ *   the 2% stability tie-break and the F_max fallback): see the section at the end.
+ *
  * Request pre-processing (Sec. 3.2.1 input-length axis 256..8192; Sec. 3.2.2 / 3.3 the
  * 5% output-length safety pad):
  *   Lout = ceil(1.05 * predicted_out)            (integer: (105*L + 99) / 100)
@@ -597,4 +600,186 @@ int festina_oracle_preferred_at(const or_lut *L, const or_llms *Q, int32_t g, in
   *sm_pref = (sp * tp + sd * td) / (tp + td);
   *f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);
   return 1;
+}
+
+/* ---------------------------------------------------------------- current-frequency dispatch */
+/* Sec. 3.3 as the paper runs it: every GPU offers one operating point, its current
+ * frequency F_curr and the SMs free when the request's memory becomes available.
+ * Phase One: GPU g's local scheduler reports a free-memory profile (from time t_s on,
+ * mem_s MiB and SM level sm_s are free; t_s non-decreasing); the request needs
+ * Req_mem = kv_kib_per_token[m] * (prompt + Lout) KiB; T_avail is the first t_s whose
+ * mem_s covers it and SM_free that step's SM level.  g is feasible when
+ * T_avail + TTFT(SM_free, F_curr) < slo_ttft and TBT(SM_free, F_curr) < slo_tbt.
+ * Phase Two: E_g = Power(F_curr) x Latency = P * (TTFT + Lout * TBT); the least E wins,
+ * but every candidate within 2% of it (E_g <= 1.02 E_min) ties, and among those the most
+ * free memory, then the most free SMs, then the lowest GPU id wins.
+ * Phase Three: no candidate -> GPUs ordered by T_avail (then id); the first that meets
+ * the SLO at F_max (the top level) with its SM_free takes the request.  Else a new GPU
+ * (batch 1, every SM, available now, k = k_new) at its least-energy feasible level.
+ * Energies are float64 in a fixed order (the kernels use the same order, so both sides
+ * take the 2% decision on identical values). */
+typedef struct {
+  int32_t n_gpus, n_steps;
+  const int32_t *freq_cur;         /* [G] */
+  const int32_t *batch;            /* [G] */
+  const float *k_dyn_w;            /* [G] */
+  const uint32_t *resident;        /* [G][words] */
+  const float *t_avail_ms;         /* [G][S] */
+  const int32_t *mem_free_mib;     /* [G][S] */
+  const int32_t *sm_free;          /* [G][S] SM level index, -1 = none */
+  const int32_t *kv_kib_per_token; /* [M] */
+  float k_new_w;                   /* k of a newly activated GPU */
+} or_avail;
+
+typedef struct {
+  int32_t gpu, freq_level, sm_level, phase;   /* phase: 1 = Phase Two, 2 = F_max fallback,
+                                                 3 = new GPU, 0 = nothing feasible */
+  double energy;
+} or_dispatch;
+
+#define OR_STABILITY 1.02
+
+/* Energy of the request on one operating point; the order of operations is fixed. */
+static double or_dispatch_energy(double p0, double kg, double s, double f, double u, double ttft, double lout,
+                                 double tbt) {
+  const double P = p0 + kg * s * (f * f * f) * u;
+  return P * (ttft + lout * tbt);
+}
+
+/* Phase One for GPU g: 1 when g hosts the model and some profile step holds the memory;
+ * then the step's time and SM level. */
+static int or_avail_step(const or_lut *L, const or_avail *A, int g, int m, int64_t need_kib, double *t_avail,
+                         int *sm, int *mem) {
+  const int words = (L->n_models + 31) / 32;
+  if (!((A->resident[(size_t)g * words + (size_t)(m / 32)] >> (m % 32)) & 1u)) return 0;
+  for (int s = 0; s < A->n_steps; ++s) {
+    const size_t at = (size_t)g * A->n_steps + (size_t)s;
+    if ((int64_t)A->mem_free_mib[at] * 1024 >= need_kib) {
+      *t_avail = (double)A->t_avail_ms[at];
+      *sm = A->sm_free[at];
+      *mem = A->mem_free_mib[at];
+      return 1;
+    }
+  }
+  return 0;
+}
+
+/* Does the request meet both SLOs on GPU g's point (level j, frequency k, start t_avail)?
+ * Sets the energy when it does. */
+static int or_point_ok(const or_lut *L, const or_requests *Q, int r, int m, int prow, int b, int j, int k,
+                       double t_avail, double kg, double *energy) {
+  if (j < 0 || j >= L->n_sm || k < 0 || k >= L->n_freq) return 0;
+  const float ttft = L->pf[or_cell(L, m, prow >= 0 ? prow : b - 1, j, k)];
+  const float tbt = L->dc[or_cell(L, m, b - 1, j, k)];
+  if (!(t_avail + (double)ttft < (double)Q->slo_ttft_ms[r] && tbt < Q->slo_tbt_ms[r])) return 0;
+  const double lout = (double)or_padded_out(Q->pred_out_tokens[r]);
+  const double e = or_dispatch_energy(L->p0_w, kg, (double)L->sm_level[j], (double)L->freq_level[k],
+                                      (double)b / 32.0, (double)ttft, lout, (double)tbt);
+  if (!((float)e < INFINITY)) return 0;
+  *energy = e;
+  return 1;
+}
+
+static void or_dispatch_one(const or_lut *L, const or_avail *A, const or_requests *Q, int r, or_dispatch *o) {
+  o->gpu = o->freq_level = o->sm_level = -1;
+  o->phase = 0;
+  o->energy = INFINITY;
+  const int m = (r >= 0 && r < Q->n_requests) ? Q->model[r] : -1;
+  if (m < 0 || m >= L->n_models || Q->pred_out_tokens[r] < 0) return;
+  const int prow = or_prompt_row(Q->prompt_tokens[r]);
+  if (prow == -2) return;
+  const int64_t need = (int64_t)A->kv_kib_per_token[m] * ((int64_t)Q->prompt_tokens[r] + or_padded_out(Q->pred_out_tokens[r]));
+  /* Phase One and the least energy */
+  double emin = INFINITY;
+  int any = 0;
+  for (int g = 0; g < A->n_gpus; ++g) {
+    double ta, e;
+    int sm, mem;
+    if (!or_avail_step(L, A, g, m, need, &ta, &sm, &mem)) continue;
+    const int32_t B = A->batch[g];
+    if (B < 0) continue;
+    const int b = B + 1 > OR_ROWS ? OR_ROWS : B + 1;
+    if (!or_point_ok(L, Q, r, m, prow, b, sm, A->freq_cur[g], ta, (double)A->k_dyn_w[g], &e)) continue;
+    if (!any || e < emin) emin = e;
+    any = 1;
+  }
+  if (any) {
+    /* Phase Two with the stability tie-break */
+    const double bound = OR_STABILITY * emin;
+    int bg = -1, bmem = 0, bsm = 0;
+    double be = 0.0;
+    for (int g = 0; g < A->n_gpus; ++g) {
+      double ta, e;
+      int sm, mem;
+      if (!or_avail_step(L, A, g, m, need, &ta, &sm, &mem)) continue;
+      const int32_t B = A->batch[g];
+      if (B < 0) continue;
+      const int b = B + 1 > OR_ROWS ? OR_ROWS : B + 1;
+      if (!or_point_ok(L, Q, r, m, prow, b, sm, A->freq_cur[g], ta, (double)A->k_dyn_w[g], &e)) continue;
+      if (!(e <= bound)) continue;
+      if (bg < 0 || mem > bmem || (mem == bmem && sm > bsm)) {
+        bg = g;
+        bmem = mem;
+        bsm = sm;
+        be = e;
+      }
+    }
+    o->gpu = bg;
+    o->freq_level = A->freq_cur[bg];
+    o->sm_level = bsm;
+    o->phase = 1;
+    o->energy = be;
+    return;
+  }
+  /* Phase Three: the earliest available GPU that meets the SLO at F_max */
+  const int kmax = L->n_freq - 1;
+  int bg = -1, bsm = -1;
+  double bt = INFINITY, be = 0.0;
+  for (int g = 0; g < A->n_gpus; ++g) {
+    double ta, e;
+    int sm, mem;
+    if (!or_avail_step(L, A, g, m, need, &ta, &sm, &mem)) continue;
+    const int32_t B = A->batch[g];
+    if (B < 0) continue;
+    const int b = B + 1 > OR_ROWS ? OR_ROWS : B + 1;
+    if (!or_point_ok(L, Q, r, m, prow, b, sm, kmax, ta, (double)A->k_dyn_w[g], &e)) continue;
+    if (bg < 0 || ta < bt) {
+      bg = g;
+      bt = ta;
+      bsm = sm;
+      be = e;
+    }
+  }
+  if (bg >= 0) {
+    o->gpu = bg;
+    o->freq_level = kmax;
+    o->sm_level = bsm;
+    o->phase = 2;
+    o->energy = be;
+    return;
+  }
+  /* scale out: a new GPU, every SM free now, batch 1, its least-energy feasible level */
+  int bk = -1;
+  for (int k = 0; k < L->n_freq; ++k) {
+    double e;
+    if (!or_point_ok(L, Q, r, m, prow, 1, L->n_sm - 1, k, 0.0, (double)A->k_new_w, &e)) continue;
+    if (bk < 0 || e < be) {
+      bk = k;
+      be = e;
+    }
+  }
+  if (bk >= 0) {
+    o->freq_level = bk;
+    o->sm_level = L->n_sm - 1;
+    o->phase = 3;
+    o->energy = be;
+  }
+}
+
+int festina_oracle_dispatch(const or_lut *L, const or_avail *A, const or_requests *Q, int32_t n_sel,
+                            const int32_t *sel, or_dispatch *out) {
+  if (!or_lut_ok(L) || !A || !Q || !out || A->n_gpus < 0 || A->n_steps < 1 || Q->n_requests < 0) return 1;
+  const int32_t n = sel ? n_sel : Q->n_requests;
+  for (int32_t i = 0; i < n; ++i) or_dispatch_one(L, A, Q, sel ? sel[i] : i, &out[i]);
+  return 0;
 }

@@ -522,3 +522,98 @@ def make_tiny_llms(rng: np.random.Generator, G=None, K=None, M=None, NS=None, NF
             "slo_tbt_ms": rng.uniform(4.0, 45.0, (G, K)).astype(np.float32),
             "k_dyn_w": rng.uniform(0.0, 500.0, G).astype(np.float32)}
     return {"lut": lut, "llms": llms, "meta": {}}
+
+
+# --------------------------------------------------------------------------- current-frequency dispatch
+DISPATCH_SEED = CONFIG_SEED_BASE + 70
+N_AVAIL_STEPS = 4
+
+
+def make_dispatch(seed: int | None = None, n_requests: int = 65536, n_gpus: int = 512) -> dict:
+    """Requests and GPU state for the paper's own dispatcher (current frequency, one
+    operating point per GPU, 2% stability tie-break, F_max fallback).
+
+    Configuration 3's laws for the tables (32 models, 8 SM x 16 frequency levels, +-5%
+    noise), the GPUs (1-4 models, k ~ U(300, 500), batch min(Poisson(4), 31)) and the
+    requests (prompts lognormal(6, 1), outputs lognormal(5, 1), model SLOs).  Added: each
+    GPU's current frequency level (uniform), a 4-step free-memory profile from its local
+    scheduler (now: U(0, 2048) MiB free; each later step after Exp(30 ms) frees U(256, 4096)
+    MiB more, up to 288 GiB) with its free SM level (now: uniform in -1..7, -1 = none;
+    each step frees 0-3 levels more, up to 7), a KV-cache size per model of 128-640 KiB per
+    token, and k = 400 W for a newly activated GPU.
+    """
+    if seed is None:
+        seed = DISPATCH_SEED
+    rng = np.random.default_rng(seed)
+    M, NS, NF, G, R, S = 32, 8, 16, int(n_gpus), int(n_requests), N_AVAIL_STEPS
+    s, f = sm_levels(NS), freq_levels(NF)
+    a, c, cp = _latency_params(rng, M, prefill=True)
+    pf, dc = _tables(rng, M, s, f, a, c, cp, noise=True)
+    lut = _lut(pf, dc, s, f)
+    slo_m_ttft = rng.choice(TTFT_SLO_SET, M)
+    slo_m_tbt = rng.choice(TBT_SLO_SET, M)
+    nres = rng.integers(1, 5, size=G)
+    models_per_gpu = _distinct_models(rng, G, M, nres)
+    kdyn = rng.uniform(300.0, 500.0, G).astype(np.float32)
+    batch = np.minimum(rng.poisson(4.0, size=G), 31).astype(np.int32)
+    freq_cur = rng.integers(0, NF, G).astype(np.int32)
+    t = np.zeros((G, S))
+    mem = np.zeros((G, S), np.int64)
+    sm = np.zeros((G, S), np.int32)
+    mem[:, 0] = rng.integers(0, 2049, G)
+    sm[:, 0] = rng.integers(-1, NS, G)
+    for k in range(1, S):
+        t[:, k] = t[:, k - 1] + rng.exponential(30.0, G)
+        mem[:, k] = np.minimum(mem[:, k - 1] + rng.integers(256, 4097, G), HBM_CAP_MIB)
+        sm[:, k] = np.minimum(sm[:, k - 1] + rng.integers(0, 4, G), NS - 1)
+    avail = {"n_gpus": G, "n_steps": S, "freq_cur": freq_cur, "batch": batch, "k_dyn_w": kdyn,
+             "resident": _resident_bits(models_per_gpu, M), "t_avail_ms": t.astype(np.float32),
+             "mem_free_mib": mem.astype(np.int32), "sm_free": sm,
+             "kv_kib_per_token": rng.integers(128, 641, M).astype(np.int32), "k_new_w": 400.0}
+    model = rng.integers(0, M, size=R, dtype=np.int32)
+    prompt = _lognormal_tokens(rng, 6.0, R, 16, 8192)
+    pred_out = _lognormal_tokens(rng, 5.0, R, 1, 8192)
+    requests = {"n_requests": R, "model": model, "wave": None, "prompt_tokens": prompt,
+                "pred_out_tokens": pred_out, "slo_ttft_ms": slo_m_ttft[model].astype(np.float32),
+                "slo_tbt_ms": slo_m_tbt[model].astype(np.float32)}
+    return {"lut": lut, "avail": avail, "requests": requests,
+            "meta": {"seed": seed, "models_per_gpu": models_per_gpu}}
+
+
+def make_tiny_dispatch(rng: np.random.Generator, R=None, G=None, M=None, NS=None, NF=None, S=None,
+                       ties=False) -> dict:
+    """Small random dispatch instance for pins and parity edge cases.  With ``ties`` every
+    GPU shares one table value and power coefficient, so energies tie exactly or lie
+    within 2% and the stability tie-break decides."""
+    R = int(rng.integers(1, 9)) if R is None else R
+    G = int(rng.integers(1, 7)) if G is None else G
+    M = int(rng.integers(1, 3)) if M is None else M
+    NS = int(rng.integers(1, 5)) if NS is None else NS
+    NF = int(rng.integers(1, 6)) if NF is None else NF
+    S = int(rng.integers(1, 4)) if S is None else S
+    s, f = sm_levels(NS), freq_levels(NF)
+    pf = rng.uniform(5.0, 60.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    dc = rng.uniform(2.0, 40.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    kd = rng.uniform(0.0, 500.0, G)
+    if ties:
+        pf[:] = np.float32(rng.uniform(5, 30))
+        dc[:] = np.float32(rng.uniform(2, 20))
+        kd = np.full(G, rng.uniform(0.0, 5.0))      # dynamic power small: energies within 2%
+    lut = _lut(pf, dc, s, f, p0=float(rng.uniform(50.0, 150.0)))
+    t = np.cumsum(rng.exponential(10.0, (G, S)), axis=1)
+    t[:, 0] = 0.0
+    mem = np.cumsum(rng.integers(0, 400, (G, S)), axis=1)
+    sm = np.minimum(np.cumsum(rng.integers(0, 2, (G, S)), axis=1) + rng.integers(-1, NS, G)[:, None], NS - 1)
+    models_per_gpu = [np.flatnonzero(rng.random(M) < 0.8) for _ in range(G)]
+    avail = {"n_gpus": G, "n_steps": S, "freq_cur": rng.integers(0, NF, G).astype(np.int32),
+             "batch": rng.integers(0, 32, G).astype(np.int32), "k_dyn_w": kd.astype(np.float32),
+             "resident": _resident_bits(models_per_gpu, M), "t_avail_ms": t.astype(np.float32),
+             "mem_free_mib": mem.astype(np.int32), "sm_free": sm.astype(np.int32),
+             "kv_kib_per_token": rng.integers(1, 200, M).astype(np.int32),
+             "k_new_w": float(np.float32(rng.uniform(0, 500)))}
+    requests = {"n_requests": R, "model": rng.integers(0, M, R).astype(np.int32), "wave": None,
+                "prompt_tokens": np.where(rng.random(R) < 0.2, 0, rng.integers(1, 3000, R)).astype(np.int32),
+                "pred_out_tokens": rng.integers(0, 300, R).astype(np.int32),
+                "slo_ttft_ms": rng.uniform(10.0, 90.0, R).astype(np.float32),
+                "slo_tbt_ms": rng.uniform(5.0, 45.0, R).astype(np.float32)}
+    return {"lut": lut, "avail": avail, "requests": requests, "meta": {}}

@@ -284,3 +284,82 @@ def brute_ewr(n_inst, f_pref, t_ms):
         wg[g] = sum(t * (fg[g] ** 3 - f ** 3) for f, t in ls)
         opt += sum(t * f ** 3 for f, t in ls)
     return fg, wg, (wg.sum(), opt, wg.sum() / opt if opt else np.nan)
+
+
+# ------------------------------------------------------------------ current-frequency dispatch
+def dispatch_energy(p0, k, s, f, u, ttft, lout, tbt):
+    """Power x latency on one operating point, in the fixed float64 order of the oracle."""
+    P = p0 + k * s * (f * f * f) * u
+    return P * (ttft + lout * tbt)
+
+
+def dispatch_points(inp, r):
+    """Per hosting GPU with memory for request r: (g, T_avail, SM_free, free memory, b)."""
+    lut, av, rq = inp["lut"], inp["avail"], inp["requests"]
+    m = int(rq["model"][r])
+    need = int(av["kv_kib_per_token"][m]) * (int(rq["prompt_tokens"][r]) + padded_out(int(rq["pred_out_tokens"][r])))
+    out = []
+    for g in range(av["n_gpus"]):
+        if not (int(av["resident"][g, m // 32]) >> (m % 32)) & 1 or int(av["batch"][g]) < 0:
+            continue
+        steps = [s for s in range(av["n_steps"]) if int(av["mem_free_mib"][g, s]) * 1024 >= need]
+        if steps:
+            s = steps[0]
+            out.append((g, float(av["t_avail_ms"][g, s]), int(av["sm_free"][g, s]), int(av["mem_free_mib"][g, s]),
+                        min(int(av["batch"][g]) + 1, 32)))
+    return out
+
+
+def point_energy(inp, r, j, k, t_avail, b, kg):
+    """Energy of request r on (j, k) starting at t_avail with batch b, or None if an SLO misses."""
+    lut, rq = inp["lut"], inp["requests"]
+    NS, NF = lut["n_sm"], lut["n_freq"]
+    if not (0 <= j < NS and 0 <= k < NF):
+        return None
+    m = int(rq["model"][r])
+    prow = prompt_row(int(rq["prompt_tokens"][r]))
+    ttft = lut["pf"][m, b - 1 if prow < 0 else prow, j, k]
+    tbt = lut["dc"][m, b - 1, j, k]
+    if not (t_avail + float(ttft) < float(rq["slo_ttft_ms"][r]) and tbt < rq["slo_tbt_ms"][r]):
+        return None
+    e = dispatch_energy(float(lut["p0_w"]), kg, float(lut["sm_level"][j]), float(lut["freq_level"][k]), b / 32,
+                        float(ttft), float(padded_out(int(rq["pred_out_tokens"][r]))), float(tbt))
+    return e if np.float32(e) < np.inf else None
+
+
+def brute_dispatch(inp):
+    lut, av, rq = inp["lut"], inp["avail"], inp["requests"]
+    R, NS, NF = rq["n_requests"], lut["n_sm"], lut["n_freq"]
+    res = []
+    for r in range(R):
+        pts = dispatch_points(inp, r)
+        cands = []
+        for g, ta, sm, mem, b in pts:
+            e = point_energy(inp, r, sm, int(av["freq_cur"][g]), ta, b, float(av["k_dyn_w"][g]))
+            if e is not None:
+                cands.append((e, g, sm, mem))
+        if cands:
+            emin = min(c[0] for c in cands)
+            tied = [c for c in cands if c[0] <= 1.02 * emin]                 # within 2%
+            e, g, sm, mem = min(tied, key=lambda c: (-c[3], -c[2], c[1]))   # memory, SMs, id
+            res.append((g, int(av["freq_cur"][g]), sm, 1, e))
+            continue
+        fb = []
+        for g, ta, sm, mem, b in pts:
+            e = point_energy(inp, r, sm, NF - 1, ta, b, float(av["k_dyn_w"][g]))
+            if e is not None:
+                fb.append((ta, g, sm, e))
+        if fb:
+            ta, g, sm, e = min(fb)                                          # earliest, then id
+            res.append((g, NF - 1, sm, 2, e))
+            continue
+        knew = float(np.float32(av["k_new_w"]))                          # a float32 field of the ABI
+        new = [(point_energy(inp, r, NS - 1, k, 0.0, 1, knew), k) for k in range(NF)]
+        new = [(e, k) for e, k in new if e is not None]
+        if new:
+            e, k = min(new)
+            res.append((-1, k, NS - 1, 3, e))
+        else:
+            res.append((-1, -1, -1, 0, np.inf))
+    a = np.array([x[:4] for x in res], np.int32).reshape(-1, 4)
+    return a[:, 0], a[:, 1], a[:, 2], a[:, 3], np.array([x[4] for x in res])

@@ -141,3 +141,29 @@ def golden_preferred(variant=None):
             "slo_ttft_ms": one(q["slo_ttft_ms"], np.float32), "slo_tbt_ms": one(q["slo_tbt_ms"], np.float32),
             "k_dyn_w": np.array([q["k_dyn_w"]], np.float32)}
     return {"lut": lut, "llms": llms}, exp, d
+
+
+def golden_dispatch(variant=None):
+    """Inputs of the hand-worked dispatch example (optionally one of its variants by name)."""
+    d = load_golden("dispatch_worked_example.json")
+    lut = _tables(d["lut"])
+    av = dict(d["avail"])
+    q = dict(d["request"])
+    exp = d["expected"]
+    if variant is not None:
+        v = [x for x in d["variants"] if x["name"] == variant][0]
+        for k, val in v["change"].items():
+            (q if k in q else av)[k] = val
+        exp = v["expected"]
+    G = len(av["freq_cur"])
+    avail = {"n_gpus": G, "n_steps": len(av["t_avail_ms"][0]), "freq_cur": np.array(av["freq_cur"], np.int32),
+             "batch": np.array(av["batch"], np.int32), "k_dyn_w": np.array(av["k_dyn_w"], np.float32),
+             "resident": np.ones((G, 1), np.uint32), "t_avail_ms": np.array(av["t_avail_ms"], np.float32),
+             "mem_free_mib": np.array(av["mem_free_mib"], np.int32), "sm_free": np.array(av["sm_free"], np.int32),
+             "kv_kib_per_token": np.array(av["kv_kib_per_token"], np.int32), "k_new_w": float(av["k_new_w"])}
+    req = {"n_requests": 1, "model": np.array([q["model"]], np.int32), "wave": None,
+           "prompt_tokens": np.array([q["prompt_tokens"]], np.int32),
+           "pred_out_tokens": np.array([q["pred_out_tokens"]], np.int32),
+           "slo_ttft_ms": np.array([q["slo_ttft_ms"]], np.float32),
+           "slo_tbt_ms": np.array([q["slo_tbt_ms"]], np.float32)}
+    return {"lut": lut, "avail": avail, "requests": req}, exp, d

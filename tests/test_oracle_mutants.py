@@ -93,6 +93,28 @@ PREFERRED = [
 ]
 
 
+DISPATCH = [
+    ("no stability margin", "#define OR_STABILITY 1.02", "#define OR_STABILITY 1.0"),
+    ("least memory wins the tie", "if (bg < 0 || mem > bmem || (mem == bmem && sm > bsm)) {",
+     "if (bg < 0 || mem < bmem || (mem == bmem && sm > bsm)) {"),
+    ("free SMs ignored in the tie", "if (bg < 0 || mem > bmem || (mem == bmem && sm > bsm)) {",
+     "if (bg < 0 || mem > bmem) {"),
+    ("memory demand without the output",
+     "((int64_t)Q->prompt_tokens[r] + or_padded_out(Q->pred_out_tokens[r]))", "((int64_t)Q->prompt_tokens[r])"),
+    ("waiting time ignored", "if (!(t_avail + (double)ttft < (double)Q->slo_ttft_ms[r]",
+     "if (!((double)ttft < (double)Q->slo_ttft_ms[r]"),
+    ("fallback at the current frequency", "if (!or_point_ok(L, Q, r, m, prow, b, sm, kmax, ta,",
+     "if (!or_point_ok(L, Q, r, m, prow, b, sm, A->freq_cur[g], ta,"),
+    ("fallback to the latest GPU", "if (bg < 0 || ta < bt) {", "if (bg < 0 || ta >= bt) {"),
+    ("new GPU at full batch", "if (!or_point_ok(L, Q, r, m, prow, 1, L->n_sm - 1, k, 0.0,",
+     "if (!or_point_ok(L, Q, r, m, prow, 32, L->n_sm - 1, k, 0.0,"),
+    ("first profile step whatever its memory", "if ((int64_t)A->mem_free_mib[at] * 1024 >= need_kib) {",
+     "if (1) {"),
+    ("dispatch power without utilisation", "const double P = p0 + kg * s * (f * f * f) * u;",
+     "const double P = p0 + kg * s * (f * f * f);"),
+]
+
+
 def _run_pins(tmp_path, name, old, new, suite):
     src = open(SRC).read()
     assert src.count(old) == 1, f"mutation anchor not unique/present: {name}"
@@ -129,4 +151,10 @@ def test_sweep_pins_reject_mutant(tmp_path, name, old, new):
 @pytest.mark.parametrize("name,old,new", PREFERRED, ids=[p[0] for p in PREFERRED])
 def test_preferred_pins_reject_mutant(tmp_path, name, old, new):
     rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_preferred_pins.py")
+    assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
+
+
+@pytest.mark.parametrize("name,old,new", DISPATCH, ids=[p[0] for p in DISPATCH])
+def test_dispatch_pins_reject_mutant(tmp_path, name, old, new):
+    rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_dispatch_pins.py")
     assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
