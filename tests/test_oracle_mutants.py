@@ -69,7 +69,7 @@ SWEEP = [
     ("decode row off by one", "if (ph == 1) return (tok > OR_ROWS ? OR_ROWS : tok) - 1;",
      "if (ph == 1) return tok >= OR_ROWS ? OR_ROWS - 1 : tok;"),
     ("longest task instead of the sum", "    E += P * lat;", "    E = E > P * lat ? E : P * lat;"),
-    ("highest level wins ties", "if (bk < 0 || e < be) {", "if (bk < 0 || e <= be) {"),
+    ("highest level wins ties", "      if (bk < 0 || e < be) {", "      if (bk < 0 || e <= be) {"),
 ]
 
 
