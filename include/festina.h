@@ -21,7 +21,10 @@
  *       least-energy SLO-feasible cell of each phase, then the time-weighted SM share
  *       and energy-weighted frequency (Eq. preferred_sm, Eq. preferred_frequency);
  *   festina_fleet_ewr         -- the fleet's energy waste, optimal energy and energy
- *       waste ratio (Eq. energy_waste, energy_optimal, energy_waste_ratio).
+ *       waste ratio (Eq. energy_waste, energy_optimal, energy_waste_ratio);
+ * and the paper's own dispatcher, for comparison with the exhaustive search:
+ *   festina_dispatch_requests -- one operating point per GPU (its current frequency),
+ *       the 2% stability tie-break, the F_max fallback and scale-out (Sec. 3.3).
  *
  * Conventions shared by every entry point
  *  - All array pointers inside the structs are DEVICE pointers (HIP global memory
@@ -303,6 +306,55 @@ size_t festina_ewr_workspace_bytes(int32_t n_gpus);
 festina_status festina_fleet_ewr(int32_t n_gpus, int32_t max_inst, const int32_t *n_inst,
                                  const float *f_pref, const float *t_ms, festina_ewr *out,
                                  void *workspace, size_t workspace_bytes, void *stream);
+
+/* The paper's own dispatcher (Sec. 3.3): each GPU offers one operating point, its current
+ * frequency level freq_cur and the SMs free once the request's memory is available.  Its
+ * local scheduler reports a free-memory profile of n_steps steps: from t_avail_ms[g][s] on
+ * (non-decreasing in s), mem_free_mib[g][s] MiB and SM level sm_free[g][s] (-1 = none) are
+ * free.  A request needs Req_mem = kv_kib_per_token[model] * (prompt + Lout) KiB (Lout the
+ * padded output); T_avail and SM_free come from the first step whose memory holds it.  A GPU
+ * with a negative batch, not hosting the model, or without such a step is no candidate. */
+typedef struct festina_gpu_avail {
+  int32_t n_gpus;                    /* G >= 1 */
+  int32_t n_steps;                   /* S >= 1 */
+  const int32_t *freq_cur;           /* [G] current frequency level F_curr */
+  const int32_t *batch;              /* [G] current batch B (b = min(B+1, 32), u = b/32) */
+  const float *k_dyn_w;              /* [G] */
+  const uint32_t *resident;          /* [G][(M+31)/32] */
+  const float *t_avail_ms;           /* [G][S] */
+  const int32_t *mem_free_mib;       /* [G][S] */
+  const int32_t *sm_free;            /* [G][S] SM level index, -1 = none */
+  const int32_t *kv_kib_per_token;   /* [M] KV-cache KiB per token of each model */
+  float k_new_w;                     /* k of a newly activated GPU */
+} festina_gpu_avail;
+
+/* Dispatch results, one entry per request (device memory, written by the call):
+ *   phase 1 (Phase Two): among the GPUs whose point meets both SLOs (T_avail + TTFT <
+ *     slo_ttft, TBT < slo_tbt at (SM_free, freq_cur)), every one with energy
+ *     E = (P0 + k*s*f^3*u) * (TTFT + Lout*TBT) within 2% of the least (E <= 1.02 E_min)
+ *     ties, and the one with the most free memory, then the most free SMs, then the
+ *     lowest id wins;
+ *   phase 2 (Phase Three): no such GPU; the earliest-available GPU (then lowest id) whose
+ *     point meets the SLOs at the top frequency level;
+ *   phase 3 (scale-out): a new GPU (batch 1, every SM, available now, k = k_new_w) at its
+ *     least-energy feasible level (lowest on ties); gpu = -1;
+ *   phase 0: nothing feasible (also for an invalid request); gpu, levels -1, energy +inf.
+ * Energies are evaluated in float64, each operation rounded in the order written above,
+ * and returned as float32. */
+typedef struct festina_dispatches {
+  int32_t *gpu, *freq_level, *sm_level;
+  uint8_t *phase;
+  float *energy_mj;
+} festina_dispatches;
+
+size_t festina_dispatch_workspace_bytes(const festina_lut *lut, const festina_gpu_avail *avail);
+
+/* Dispatch every request against one snapshot of the GPUs' answers (Sec. 3.3, Phases One
+ * to Three; requests' wave field is ignored).  Workspace as for placements; two kernel
+ * launches on `stream`. */
+festina_status festina_dispatch_requests(const festina_lut *lut, const festina_gpu_avail *avail,
+                                         const festina_requests *req, festina_dispatches *out,
+                                         void *workspace, size_t workspace_bytes, void *stream);
 
 /* Measurement hook, not part of the search.  While set, festina_score_placements
  * records `score_begin` on its stream immediately before its scoring kernel and

@@ -18,6 +18,9 @@ Preferred configuration, per instance slot: the flag exactly; each phase's teste
 feasible under the oracle, at most the oracle's least energy times (1 + rtol), with its
 duration and power within ``rtol``; the two averages within ``rtol`` of the oracle's at
 the tested cells.  EWR: per-GPU frequencies exactly, waste and totals within 1e-9.
+Dispatch, per request: GPU, levels and phase exactly, and the float32 energy equal to the
+oracle's float64 energy rounded to float32 (both sides evaluate the same float64
+expression, so the 2% decision is taken on identical values).
 """
 from __future__ import annotations
 
@@ -238,4 +241,19 @@ def check_ewr(oracle_out, gpu_out, rtol=1e-9) -> Report:
         rep.max_rel_err = max(rep.max_rel_err, r)
         if not (r <= rtol or (np.isnan(gt[k]) and np.isnan(ot[k]))):
             rep.mismatches.append((name, float(gt[k]), float(ot[k])))
+    return rep
+
+
+def check_dispatch(oracle_out, gpu_out) -> Report:
+    og, ok, oj, oph, oe = oracle_out
+    gg, gk, gj, gph, ge = gpu_out
+    rep = Report(n=len(og))
+    for i in range(len(og)):
+        a = (int(gg[i]), int(gk[i]), int(gj[i]), int(gph[i]))
+        b = (int(og[i]), int(ok[i]), int(oj[i]), int(oph[i]))
+        if a != b:
+            rep.mismatches.append((i, "choice", a, b))
+            continue
+        if not (np.float32(oe[i]) == ge[i]):
+            rep.mismatches.append((i, "energy", float(ge[i]), float(oe[i])))
     return rep

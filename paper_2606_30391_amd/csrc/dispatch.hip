@@ -1,0 +1,355 @@
+// dispatch.hip -- MI355X (gfx950) kernels and C-ABI host dispatch of the paper's own
+// request dispatcher (Festina, Sec. 3.3 as the paper runs it): one operating point per GPU
+// (its current frequency and the SMs free when the request's memory is available), the
+// 2% stability tie-break, the F_max fallback ordered by availability, and a new GPU's
+// least-energy level.
+//
+// k_dsp_hosts  one block per model: ascending list of the GPUs hosting it (wavefront
+//                ballots), in the caller's workspace.
+// k_dispatch   one wavefront per request; lanes stride over the model's hosts.  Per host:
+//                the first free-memory profile step that holds Req_mem gives T_avail and
+//                SM_free; the point (SM_free, F_curr) is feasible when T_avail + TTFT and
+//                TBT meet the SLOs; E = P * (TTFT + Lout * TBT) in float64.  Pass 1: the
+//                wavefront minimum E_min.  Pass 2: among hosts with E <= 1.02 E_min, the
+//                lexicographic best (most memory, most SMs, lowest id).  With no
+//                candidate: the hosts feasible at the top level, earliest T_avail (then
+//                lowest id).  Else lane k scores a new GPU at level k and the least energy
+//                (lowest k on ties) wins.
+//
+// Exactness: the energies are float64 in the same order of operations as any float64
+// evaluation of P0 + k*s*f^3*u and P * (TTFT + Lout*TBT) without contraction, so the 2%
+// test and every comparison are decided on identical values; the SLO tests add or compare
+// float32 inputs exactly.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstddef>
+#include <cstdint>
+
+#include "festina.h"
+
+namespace {
+
+constexpr int kRows = FESTINA_N_ROWS;
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;
+constexpr int kHostBlock = 256;
+constexpr int kMaxSteps = 8;                 // profile steps loaded at once
+constexpr double kStability = 1.02;          // energies within 2% of the least tie
+
+struct DspArgs {
+  int32_t M, NS, NF, C, words;
+  const float *sm_level, *freq_level, *pf, *dc;
+  double p0;
+  int32_t G, S;
+  const int32_t *freq_cur, *batch;
+  const float *kdyn;
+  const uint32_t *resident;
+  const float *t_avail;
+  const int32_t *mem_free, *sm_free, *kv;
+  double k_new;
+  int32_t R;
+  const int32_t *model, *prompt, *pred;
+  const float *slo_ttft, *slo_tbt;
+  int32_t *out_gpu, *out_freq, *out_sm;
+  uint8_t *out_phase;
+  float *out_energy;
+  int32_t *host_cnt, *host_list;     // workspace: [M], [M][G]
+};
+
+// Energy on one operating point: P = p0 + k*s*f^3*u, E = P * (ttft + lout*tbt), each
+// operation rounded separately (no fused multiply-add).
+__device__ __noinline__ double point_energy(double p0, double kg, double s, double f, double u, double ttft,
+                                            double lout, double tbt) {
+#pragma clang fp contract(off)
+  const double f3 = f * f * f;
+  const double P = p0 + kg * s * f3 * u;
+  return P * (ttft + lout * tbt);
+}
+
+__global__ void __launch_bounds__(kHostBlock) k_dsp_hosts(DspArgs a) {
+  const int m = blockIdx.x;
+  __shared__ int wsum[kHostBlock / kWave];
+  __shared__ int base_s;
+  if (threadIdx.x == 0) base_s = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x >> 6;
+  for (int g0 = 0; g0 < a.G; g0 += kHostBlock) {
+    const int g = g0 + threadIdx.x;
+    const bool has = g < a.G && ((a.resident[(size_t)g * a.words + (m >> 5)] >> (m & 31)) & 1u);
+    const unsigned long long bal = __ballot(has);
+    const int before = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wv] = __popcll(bal);
+    __syncthreads();
+    int off = base_s;
+    for (int i = 0; i < wv; ++i) off += wsum[i];
+    if (has) a.host_list[(size_t)m * a.G + off + before] = g;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int t = 0;
+      for (int i = 0; i < kHostBlock / kWave; ++i) t += wsum[i];
+      base_s += t;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) a.host_cnt[m] = base_s;
+}
+
+struct Point {
+  int ok;                        // the host has a profile step holding the memory
+  double ta;                     // T_avail
+  int sm, mem, b;
+};
+
+// Phase One for host g: first profile step whose free memory holds `need` KiB.
+__device__ __forceinline__ Point host_point(const DspArgs &a, int g, long long need) {
+  Point p{0, 0.0, -1, 0, 1};
+  const int B = a.batch[g];
+  if (B < 0) return p;
+  p.b = B + 1 > kRows ? kRows : B + 1;
+  const size_t base = (size_t)g * a.S;
+  if (a.S <= kMaxSteps) {
+    int mem[kMaxSteps];
+#pragma unroll
+    for (int s = 0; s < kMaxSteps; ++s) mem[s] = s < a.S ? a.mem_free[base + s] : 0;
+    int st = -1;
+#pragma unroll
+    for (int s = kMaxSteps - 1; s >= 0; --s)
+      if (s < a.S && (long long)mem[s] * 1024 >= need) st = s;
+    if (st < 0) return p;
+    p.ok = 1;
+    p.ta = (double)a.t_avail[base + st];
+    p.sm = a.sm_free[base + st];
+    p.mem = a.mem_free[base + st];
+    return p;
+  }
+  for (int s = 0; s < a.S; ++s)
+    if ((long long)a.mem_free[base + s] * 1024 >= need) {
+      p.ok = 1;
+      p.ta = (double)a.t_avail[base + s];
+      p.sm = a.sm_free[base + s];
+      p.mem = a.mem_free[base + s];
+      return p;
+    }
+  return p;
+}
+
+// Does request r meet its SLOs on (j, k) starting at ta with batch b?  Energy if so.
+__device__ __forceinline__ bool point_ok(const DspArgs &a, int r, int m, int prow, int b, int j, int k, double ta,
+                                         double kg, double lout, double &e) {
+  if (j < 0 || j >= a.NS || k < 0 || k >= a.NF) return false;
+  const size_t cell = (size_t)j * a.NF + k;
+  const float ttft = a.pf[((size_t)m * kRows + (prow >= 0 ? prow : b - 1)) * a.C + cell];
+  const float tbt = a.dc[((size_t)m * kRows + (b - 1)) * a.C + cell];
+  if (!(ta + (double)ttft < (double)a.slo_ttft[r] && tbt < a.slo_tbt[r])) return false;
+  e = point_energy(a.p0, kg, (double)a.sm_level[j], (double)a.freq_level[k], (double)b / 32.0, (double)ttft, lout,
+                   (double)tbt);
+  return (float)e < __builtin_huge_valf();
+}
+
+__global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) {
+  const int r = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  if (r >= a.R) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const double inf = __builtin_huge_val();
+  const int m = a.model[r];
+  const int pt = a.prompt[r], pd = a.pred[r];
+  int gsel = -1, ksel = -1, jsel = -1, phase = 0;
+  double esel = inf;
+  if (m >= 0 && m < a.M && pd >= 0 && pt >= 0) {
+    const int prow = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
+    const long long lout_i = ((long long)pd * 105 + 99) / 100;
+    const double lout = (double)lout_i;
+    const long long need = (long long)a.kv[m] * ((long long)pt + lout_i);
+    const int nh = a.host_cnt[m];
+    const int *hl = a.host_list + (size_t)m * a.G;
+    // pass 1: least energy at the current operating points
+    double emin = inf;
+    for (int h = lane; h < nh; h += kWave) {
+      const int g = hl[h];
+      const Point p = host_point(a, g, need);
+      double e;
+      if (p.ok && point_ok(a, r, m, prow, p.b, p.sm, a.freq_cur[g], p.ta, (double)a.kdyn[g], lout, e) && e < emin)
+        emin = e;
+    }
+    for (int off = 32; off >= 1; off >>= 1) emin = fmin(emin, __shfl_xor(emin, off, kWave));
+    if (emin < inf) {
+      // pass 2: the stability order over the candidates within 2% of the least energy
+      const double bound = kStability * emin;
+      int bg = INT_MAX, bmem = INT_MIN, bsm = INT_MIN;
+      double be = inf;
+      for (int h = lane; h < nh; h += kWave) {
+        const int g = hl[h];
+        const Point p = host_point(a, g, need);
+        double e;
+        if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, a.freq_cur[g], p.ta, (double)a.kdyn[g], lout, e))) continue;
+        if (!(e <= bound)) continue;
+        if (p.mem > bmem || (p.mem == bmem && (p.sm > bsm || (p.sm == bsm && g < bg)))) {
+          bg = g;
+          bmem = p.mem;
+          bsm = p.sm;
+          be = e;
+        }
+      }
+      for (int off = 32; off >= 1; off >>= 1) {
+        const int og = __shfl_xor(bg, off, kWave), om = __shfl_xor(bmem, off, kWave);
+        const int os = __shfl_xor(bsm, off, kWave);
+        const double oe = __shfl_xor(be, off, kWave);
+        if (om > bmem || (om == bmem && (os > bsm || (os == bsm && og < bg)))) {
+          bg = og;
+          bmem = om;
+          bsm = os;
+          be = oe;
+        }
+      }
+      gsel = bg;
+      ksel = a.freq_cur[bg];
+      jsel = bsm;
+      phase = 1;
+      esel = be;
+    } else {
+      // Phase Three: the earliest available host that meets the SLOs at the top level
+      const int kmax = a.NF - 1;
+      int bg = INT_MAX, bsm = -1;
+      double bt = inf, be = inf;
+      for (int h = lane; h < nh; h += kWave) {
+        const int g = hl[h];
+        const Point p = host_point(a, g, need);
+        double e;
+        if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, kmax, p.ta, (double)a.kdyn[g], lout, e))) continue;
+        if (p.ta < bt || (p.ta == bt && g < bg)) {
+          bg = g;
+          bt = p.ta;
+          bsm = p.sm;
+          be = e;
+        }
+      }
+      for (int off = 32; off >= 1; off >>= 1) {
+        const int og = __shfl_xor(bg, off, kWave), os = __shfl_xor(bsm, off, kWave);
+        const double ot = __shfl_xor(bt, off, kWave), oe = __shfl_xor(be, off, kWave);
+        if (ot < bt || (ot == bt && og < bg)) {
+          bg = og;
+          bt = ot;
+          bsm = os;
+          be = oe;
+        }
+      }
+      if (bg != INT_MAX) {
+        gsel = bg;
+        ksel = kmax;
+        jsel = bsm;
+        phase = 2;
+        esel = be;
+      } else {
+        // scale out: a new GPU (batch 1, every SM, available now), lane k scores level k
+        int bk = INT_MAX;
+        double bke = inf;
+        for (int k = lane; k < a.NF; k += kWave) {
+          double e;
+          if (point_ok(a, r, m, prow, 1, a.NS - 1, k, 0.0, a.k_new, lout, e) && (e < bke || (e == bke && k < bk))) {
+            bke = e;
+            bk = k;
+          }
+        }
+        for (int off = 32; off >= 1; off >>= 1) {
+          const int ok = __shfl_xor(bk, off, kWave);
+          const double oe = __shfl_xor(bke, off, kWave);
+          if (oe < bke || (oe == bke && ok < bk)) {
+            bke = oe;
+            bk = ok;
+          }
+        }
+        if (bk != INT_MAX) {
+          ksel = bk;
+          jsel = a.NS - 1;
+          phase = 3;
+          esel = bke;
+        }
+      }
+    }
+  }
+  if (lane == 0) {
+    a.out_gpu[r] = gsel;
+    a.out_freq[r] = ksel;
+    a.out_sm[r] = jsel;
+    a.out_phase[r] = (uint8_t)phase;
+    a.out_energy[r] = (float)esel;
+  }
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool dsp_shapes_ok(const festina_lut *L, const festina_gpu_avail *A) {
+  if (!L || !A) return false;
+  if (L->n_models < 1 || L->n_rows != kRows || L->n_sm < 1 || L->n_freq < 1) return false;
+  if (A->n_gpus < 1 || A->n_steps < 1) return false;
+  if ((long long)L->n_models * A->n_gpus > INT_MAX) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" size_t festina_dispatch_workspace_bytes(const festina_lut *L, const festina_gpu_avail *A) {
+  if (!dsp_shapes_ok(L, A)) return 0;
+  return align256(sizeof(int32_t) * L->n_models) + align256(sizeof(int32_t) * (size_t)L->n_models * A->n_gpus);
+}
+
+extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const festina_gpu_avail *A,
+                                                    const festina_requests *Q, festina_dispatches *out,
+                                                    void *workspace, size_t workspace_bytes, void *stream) {
+  if (!dsp_shapes_ok(L, A) || !Q || !out || Q->n_requests < 0) return FESTINA_ERR_INVALID;
+  const long long C = (long long)L->n_sm * L->n_freq;
+  if (C > FESTINA_MAX_CELLS) return FESTINA_ERR_UNSUPPORTED;
+  if (!L->sm_level || !L->freq_level || !L->pf || !L->dc) return FESTINA_ERR_INVALID;
+  if (!A->freq_cur || !A->batch || !A->k_dyn_w || !A->resident || !A->t_avail_ms || !A->mem_free_mib ||
+      !A->sm_free || !A->kv_kib_per_token)
+    return FESTINA_ERR_INVALID;
+  const size_t need = festina_dispatch_workspace_bytes(L, A);
+  if (!workspace || workspace_bytes < need || (((uintptr_t)workspace) & 255) != 0) return FESTINA_ERR_INVALID;
+  if (Q->n_requests == 0) return FESTINA_OK;
+  if (!Q->model || !Q->prompt_tokens || !Q->pred_out_tokens || !Q->slo_ttft_ms || !Q->slo_tbt_ms)
+    return FESTINA_ERR_INVALID;
+  if (!out->gpu || !out->freq_level || !out->sm_level || !out->phase || !out->energy_mj) return FESTINA_ERR_INVALID;
+  DspArgs a;
+  a.M = L->n_models;
+  a.NS = L->n_sm;
+  a.NF = L->n_freq;
+  a.C = (int32_t)C;
+  a.words = (L->n_models + 31) / 32;
+  a.sm_level = L->sm_level;
+  a.freq_level = L->freq_level;
+  a.pf = L->pf;
+  a.dc = L->dc;
+  a.p0 = (double)L->p0_w;
+  a.G = A->n_gpus;
+  a.S = A->n_steps;
+  a.freq_cur = A->freq_cur;
+  a.batch = A->batch;
+  a.kdyn = A->k_dyn_w;
+  a.resident = A->resident;
+  a.t_avail = A->t_avail_ms;
+  a.mem_free = A->mem_free_mib;
+  a.sm_free = A->sm_free;
+  a.kv = A->kv_kib_per_token;
+  a.k_new = (double)A->k_new_w;
+  a.R = Q->n_requests;
+  a.model = Q->model;
+  a.prompt = Q->prompt_tokens;
+  a.pred = Q->pred_out_tokens;
+  a.slo_ttft = Q->slo_ttft_ms;
+  a.slo_tbt = Q->slo_tbt_ms;
+  a.out_gpu = out->gpu;
+  a.out_freq = out->freq_level;
+  a.out_sm = out->sm_level;
+  a.out_phase = out->phase;
+  a.out_energy = out->energy_mj;
+  char *ws = static_cast<char *>(workspace);
+  a.host_cnt = reinterpret_cast<int32_t *>(ws);
+  a.host_list = reinterpret_cast<int32_t *>(ws + align256(sizeof(int32_t) * L->n_models));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  k_dsp_hosts<<<a.M, kHostBlock, 0, st>>>(a);
+  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  const long long blocks = ((long long)a.R + kWavesPerBlock - 1) / kWavesPerBlock;
+  k_dispatch<<<(unsigned)blocks, kWavesPerBlock * kWave, 0, st>>>(a);
+  return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
+}

@@ -1,8 +1,8 @@
 """Thin ctypes binding of the C ABI in include/festina.h.
 
 Argument marshalling only: every step of the search runs in the HIP library
-(``libfestina.so`` built from ``csrc/festina.hip``, ``csrc/sweep.hip`` and
-``csrc/preferred.hip``).  PyTorch provides device
+(``libfestina.so`` built from ``csrc/festina.hip``, ``csrc/sweep.hip``,
+``csrc/preferred.hip`` and ``csrc/dispatch.hip``).  PyTorch provides device
 memory and streams.  There is no CPU fallback: if the library is missing this
 module raises.
 """
@@ -92,10 +92,23 @@ class festina_ewr(C.Structure):
     _fields_ = [("f_gpu", C.c_void_p), ("waste_gpu", C.c_void_p), ("totals", C.c_void_p)]
 
 
+class festina_gpu_avail(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("n_steps", C.c_int32), ("freq_cur", C.c_void_p), ("batch", C.c_void_p),
+                ("k_dyn_w", C.c_void_p), ("resident", C.c_void_p), ("t_avail_ms", C.c_void_p),
+                ("mem_free_mib", C.c_void_p), ("sm_free", C.c_void_p), ("kv_kib_per_token", C.c_void_p),
+                ("k_new_w", C.c_float)]
+
+
+class festina_dispatches(C.Structure):
+    _fields_ = [("gpu", C.c_void_p), ("freq_level", C.c_void_p), ("sm_level", C.c_void_p),
+                ("phase", C.c_void_p), ("energy_mj", C.c_void_p)]
+
+
 EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_workspace_bytes",
             "festina_score_placements", "festina_migrations_workspace_bytes", "festina_score_migrations",
             "festina_sweep_batches", "festina_preferred_configs", "festina_ewr_workspace_bytes",
-            "festina_fleet_ewr", "festina_set_timing_events")
+            "festina_fleet_ewr", "festina_dispatch_workspace_bytes", "festina_dispatch_requests",
+            "festina_set_timing_events")
 
 _lib = None
 
@@ -132,6 +145,11 @@ def lib():
         L.festina_fleet_ewr.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                         P(festina_ewr), C.c_void_p, C.c_size_t, C.c_void_p]
         L.festina_fleet_ewr.restype = C.c_int
+        L.festina_dispatch_workspace_bytes.argtypes = [P(festina_lut), P(festina_gpu_avail)]
+        L.festina_dispatch_workspace_bytes.restype = C.c_size_t
+        L.festina_dispatch_requests.argtypes = [P(festina_lut), P(festina_gpu_avail), P(festina_requests),
+                                                P(festina_dispatches), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.festina_dispatch_requests.restype = C.c_int
         L.festina_set_timing_events.argtypes = [C.c_void_p] * 4
         L.festina_set_timing_events.restype = None
         _lib = L
@@ -362,6 +380,54 @@ class DevicePreferred:
         return self.f_gpu[:self.G].cpu().numpy(), self.waste_gpu[:self.G].cpu().numpy(), self.totals.cpu().numpy()
 
 
+class DeviceDispatch:
+    """Requests and the GPUs' answers for the paper's own dispatcher, on the device."""
+
+    def __init__(self, inp: dict, device="cuda"):
+        import torch
+        lut, av, rq = inp["lut"], inp["avail"], inp["requests"]
+        d = lambda a, t: _dev(a, t, device)
+        self.t = {
+            "sm_level": d(lut["sm_level"], np.float32), "freq_level": d(lut["freq_level"], np.float32),
+            "pf": d(lut["pf"], np.float32), "dc": d(lut["dc"], np.float32),
+            "resident": d(np.asarray(av["resident"], np.uint32).view(np.int32), np.int32),
+        }
+        for k in ("freq_cur", "batch", "mem_free_mib", "sm_free", "kv_kib_per_token"):
+            self.t[k] = d(av[k], np.int32)
+        for k in ("k_dyn_w", "t_avail_ms"):
+            self.t[k] = d(av[k], np.float32)
+        for k in ("model", "prompt_tokens", "pred_out_tokens"):
+            self.t[k] = d(rq[k], np.int32)
+        for k in ("slo_ttft_ms", "slo_tbt_ms"):
+            self.t[k] = d(rq[k], np.float32)
+        t = self.t
+        self.lut = festina_lut(int(lut["n_models"]), int(lut["n_rows"]), int(lut["n_sm"]), int(lut["n_freq"]),
+                               _ptr(t["sm_level"]), _ptr(t["freq_level"]), _ptr(t["pf"]), _ptr(t["dc"]),
+                               float(lut["p0_w"]))
+        self.avail = festina_gpu_avail(int(av["n_gpus"]), int(av["n_steps"]), _ptr(t["freq_cur"]), _ptr(t["batch"]),
+                                       _ptr(t["k_dyn_w"]), _ptr(t["resident"]), _ptr(t["t_avail_ms"]),
+                                       _ptr(t["mem_free_mib"]), _ptr(t["sm_free"]), _ptr(t["kv_kib_per_token"]),
+                                       float(av["k_new_w"]))
+        self.R = int(rq["n_requests"])
+        self.req = festina_requests(self.R, _ptr(t["model"]), None, _ptr(t["prompt_tokens"]),
+                                    _ptr(t["pred_out_tokens"]), _ptr(t["slo_ttft_ms"]), _ptr(t["slo_tbt_ms"]))
+        n = max(self.R, 1)
+        self.o = {k: torch.empty(n, dtype=torch.int32, device=device) for k in ("gpu", "freq_level", "sm_level")}
+        self.o["phase"] = torch.empty(n, dtype=torch.uint8, device=device)
+        self.o["energy_mj"] = torch.empty(n, dtype=torch.float32, device=device)
+        self.out = festina_dispatches(*(_ptr(self.o[k]) for k in ("gpu", "freq_level", "sm_level", "phase",
+                                                                  "energy_mj")))
+        self.ws_bytes = festina_dispatch_workspace_bytes(self.lut, self.avail)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
+
+    def run(self, stream=None):
+        festina_dispatch_requests(self.lut, self.avail, self.req, self.out, self.workspace, self.ws_bytes, stream)
+
+    def results(self):
+        R = self.R
+        return tuple(self.o[k][:R].cpu().numpy() for k in ("gpu", "freq_level", "sm_level", "phase", "energy_mj"))
+
+
 # ------------------------------------------------------------------ the ABI calls
 def festina_placements_workspace_bytes(lut, gpus, req) -> int:
     return int(lib().festina_placements_workspace_bytes(C.byref(lut), C.byref(gpus), C.byref(req)))
@@ -409,3 +475,15 @@ def festina_fleet_ewr(n_gpus, max_inst, n_inst, f_pref, t_ms, out, workspace, wo
                                  ws, int(workspace_bytes), _stream_handle(stream))
     if st != FESTINA_OK:
         raise FestinaError(st, "festina_fleet_ewr")
+
+
+def festina_dispatch_workspace_bytes(lut, avail) -> int:
+    return int(lib().festina_dispatch_workspace_bytes(C.byref(lut), C.byref(avail)))
+
+
+def festina_dispatch_requests(lut, avail, req, out, workspace, workspace_bytes, stream=None) -> None:
+    ws = None if workspace is None else C.c_void_p(workspace.data_ptr())
+    st = lib().festina_dispatch_requests(C.byref(lut), C.byref(avail), C.byref(req), C.byref(out), ws,
+                                         int(workspace_bytes), _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_dispatch_requests")

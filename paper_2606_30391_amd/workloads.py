@@ -599,7 +599,7 @@ def make_tiny_dispatch(rng: np.random.Generator, R=None, G=None, M=None, NS=None
         pf[:] = np.float32(rng.uniform(5, 30))
         dc[:] = np.float32(rng.uniform(2, 20))
         kd = np.full(G, rng.uniform(0.0, 5.0))      # dynamic power small: energies within 2%
-    lut = _lut(pf, dc, s, f, p0=float(rng.uniform(50.0, 150.0)))
+    lut = _lut(pf, dc, s, f, p0=float(np.float32(rng.uniform(50.0, 150.0))))   # the ABI's P0 is float32
     t = np.cumsum(rng.exponential(10.0, (G, S)), axis=1)
     t[:, 0] = 0.0
     mem = np.cumsum(rng.integers(0, 400, (G, S)), axis=1)

@@ -1,0 +1,101 @@
+"""GPU parity of the paper's own dispatcher (Sec. 3.3: current frequency, 2% stability
+tie-break, F_max fallback, scale-out): the HIP path through the C ABI against the CPU
+oracle.  Both evaluate the same float64 energies in the same order, so every output must
+match exactly: GPU, levels, phase, and the energy rounded to float32."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from conftest import golden_dispatch, load_golden
+from oracle.check import check_dispatch
+from paper_2606_30391_amd import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+VARIANTS = [v["name"] for v in load_golden("dispatch_worked_example.json")["variants"]]
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run(inp):
+    from paper_2606_30391_amd import festina as F
+    F.lib()
+    dd = F.DeviceDispatch(inp, "cuda")
+    dd.run()
+    torch.cuda.synchronize()
+    return dd.results()
+
+
+def parity(inp, label=""):
+    say(f"[gpu] dispatch {label}: R={inp['requests']['n_requests']} G={inp['avail']['n_gpus']} "
+        f"S={inp['avail']['n_steps']} NS={inp['lut']['n_sm']} NF={inp['lut']['n_freq']}")
+    got = run(inp)
+    ref = oracle.dispatch(inp)
+    rep = check_dispatch(ref, got)
+    say(f"      {rep}; phases {np.bincount(got[3], minlength=4).tolist()}")
+    assert rep.ok, str(rep)
+    return got
+
+
+def test_dispatch_workload_full_size():
+    got = parity(W.make_dispatch(), label="65536 requests, 512 GPUs")
+    ph = np.bincount(got[3], minlength=4)
+    assert ph[1] > 0.5 * ph.sum() and ph[2] > 0 and ph[3] > 0 and ph[0] > 0
+
+
+@pytest.mark.parametrize("extra", [100, 200])
+def test_dispatch_workload_seeds(extra):
+    parity(W.make_dispatch(seed=W.DISPATCH_SEED + extra, n_requests=8000, n_gpus=1024), label=f"seed +{extra}")
+
+
+@pytest.mark.parametrize("variant", [None] + VARIANTS)
+def test_dispatch_worked_example(variant):
+    inp, exp, d = golden_dispatch(variant)
+    g, k, j, ph, e = run(inp)
+    assert (int(g[0]), int(k[0]), int(j[0]), int(ph[0])) == (exp["gpu"], exp["freq_level"], exp["sm_level"],
+                                                              exp["phase"])
+    assert e[0] == (np.inf if exp["energy_mj"] is None else np.float32(exp["energy_mj"]))
+
+
+@pytest.mark.parametrize("NS,NF,S", [(1, 1, 1), (3, 5, 2), (4, 8, 3), (8, 16, 9), (16, 16, 4), (2, 70, 1)])
+def test_dispatch_shapes(NS, NF, S):
+    rng = np.random.default_rng(1500 + NS * 100 + NF)
+    parity(W.make_tiny_dispatch(rng, R=3000, G=150, M=3, NS=NS, NF=NF, S=S), label="shapes")
+
+
+def test_dispatch_exact_and_near_ties():
+    rng = np.random.default_rng(1600)
+    inp = W.make_tiny_dispatch(rng, R=4000, G=90, M=2, NS=3, NF=4, S=2, ties=True)
+    parity(inp, label="ties")
+    inp["avail"]["k_dyn_w"][:] = 0.0
+    inp["avail"]["mem_free_mib"][:] = inp["avail"]["mem_free_mib"][:1]
+    parity(inp, label="exact ties, equal memory")
+
+
+def test_dispatch_invalid_elements():
+    rng = np.random.default_rng(1700)
+    inp = W.make_tiny_dispatch(rng, R=500, G=40, M=3, NS=4, NF=6, S=3)
+    rq, av = inp["requests"], inp["avail"]
+    rq["model"][:20] = 3
+    rq["model"][20:30] = -1
+    rq["prompt_tokens"][30:40] = -5
+    rq["pred_out_tokens"][40:50] = -1
+    av["batch"][:5] = -1
+    av["freq_cur"][5:10] = 9
+    av["sm_free"][10:15] = 7
+    av["sm_free"][15:20] = -1
+    got = parity(inp, label="invalid elements")
+    assert np.all(got[3][:50] == 0)
+
+
+def test_dispatch_many_hosts():
+    """More hosting GPUs than lanes in a wavefront: several hosts per lane."""
+    rng = np.random.default_rng(1800)
+    parity(W.make_tiny_dispatch(rng, R=700, G=700, M=2, NS=4, NF=6, S=2), label="700 GPUs")
