@@ -18,7 +18,8 @@ oracle timed on a bounded sample of the same workload on this host.  Outside the
 timed steps, ``next_rows`` measures the local schedulers' SM/frequency sweep over
 1,024 GPUs x 64 epochs of task batches (one kernel per call), and the preferred
 configuration of every LLM instance on a 2,048-GPU fleet plus the fleet's energy waste
-ratio, the same way.
+ratio, and the paper's own current-frequency dispatcher (65,536 requests, 512 GPUs), the
+same way.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --per-config     (one JSON line per configuration, then the step line)
@@ -215,6 +216,43 @@ def preferred_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
     return row
 
 
+def dispatch_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
+    """The paper's own dispatcher (one operating point per GPU, 2% stability tie-break,
+    F_max fallback): call time from HIP events, roofline position, and the oracle."""
+    inp = W.make_dispatch()
+    dd = F.DeviceDispatch(inp, "cuda")
+    ms = timed_calls(hip, torch, dd.run, calls, warmup)
+    lut, av, rq = inp["lut"], inp["avail"], inp["requests"]
+    M, G, R, S = lut["n_models"], av["n_gpus"], rq["n_requests"], av["n_steps"]
+    res = np.asarray(av["resident"], np.uint32)
+    hosts = np.array([int(((res[:, m // 32] >> np.uint32(m % 32)) & 1).sum()) for m in range(M)])
+    evals = int(hosts[rq["model"]].sum())                    # (request, hosting GPU) operating points
+    nbytes = R * (5 * 4) + R * (3 * 4 + 1 + 4) + G * (4 * 3 + 4 * ((M + 31) // 32) + S * 12) + M * 4 \
+        + 2 * lut["pf"].nbytes
+    row = {
+        "workload": ("paper's current-frequency dispatcher: 65536 requests, 512 GPUs (1-4 of 32 models each), "
+                     "4-step free-memory profiles, 8 SM x 16 freq levels"),
+        "requests": R, "evaluations": evals, "kernel_ms": ms, "evaluations_per_s": evals / (ms * 1e-3),
+        "roofline": {"kernel": "k_dispatch", "bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9,
+                     "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / HBM_PEAK,
+                     "traffic": None, "algorithmic_bytes": nbytes},
+        "cpu_baseline": None,
+    }
+    if with_cpu:
+        import oracle
+        got = dd.results()
+        t0 = time.perf_counter()
+        ref = oracle.dispatch(inp)
+        t1 = time.perf_counter()
+        row["cpu_baseline"] = {
+            "value": evals / (t1 - t0), "unit": "evaluations/s", "cores": 1, "kind": "oracle",
+            "sample": f"all {R} requests ({t1 - t0:.3f} s); single-threaded C, float64, gcc -O2",
+            "agreement": {"all_outputs_equal": float(np.mean(
+                (got[0] == ref[0]) & (got[1] == ref[1]) & (got[2] == ref[2]) & (got[3] == ref[3])
+                & (got[4] == ref[4].astype(np.float32))))}}
+    return row
+
+
 def sweep_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
     """The local SM/frequency sweep: kernel time from HIP events around each call (one
     launch per call), its roofline position, and the oracle on the same batches."""
@@ -394,7 +432,8 @@ def main():
                        "migration_pairs_per_s_kernel": n_pairs / (pairs_ms * 1e-3)},
         "cpu_baseline": None,
         "next_rows": {"sweep": sweep_row(F, W, hip, torch, not args.no_cpu_baseline),
-                      "preferred": preferred_row(F, W, hip, torch, not args.no_cpu_baseline)},
+                      "preferred": preferred_row(F, W, hip, torch, not args.no_cpu_baseline),
+                      "dispatch": dispatch_row(F, W, hip, torch, not args.no_cpu_baseline)},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(place, fleet, gpu_place, gpu_mig)

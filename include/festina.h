@@ -313,7 +313,8 @@ festina_status festina_fleet_ewr(int32_t n_gpus, int32_t max_inst, const int32_t
  * (non-decreasing in s), mem_free_mib[g][s] MiB and SM level sm_free[g][s] (-1 = none) are
  * free.  A request needs Req_mem = kv_kib_per_token[model] * (prompt + Lout) KiB (Lout the
  * padded output); T_avail and SM_free come from the first step whose memory holds it.  A GPU
- * with a negative batch, not hosting the model, or without such a step is no candidate. */
+ * with a negative batch, not hosting the model, or without such a step is no candidate.
+ * n_gpus must be below 2^24 and n_sm * n_freq at most FESTINA_MAX_CELLS. */
 typedef struct festina_gpu_avail {
   int32_t n_gpus;                    /* G >= 1 */
   int32_t n_steps;                   /* S >= 1 */
@@ -331,7 +332,7 @@ typedef struct festina_gpu_avail {
 /* Dispatch results, one entry per request (device memory, written by the call):
  *   phase 1 (Phase Two): among the GPUs whose point meets both SLOs (T_avail + TTFT <
  *     slo_ttft, TBT < slo_tbt at (SM_free, freq_cur)), every one with energy
- *     E = (P0 + k*s*f^3*u) * (TTFT + Lout*TBT) within 2% of the least (E <= 1.02 E_min)
+ *     E = (P0 + k*s*f^3*u) * (TTFT + Lout*TBT) within 2% of the least (E <= E_min + 0.02|E_min|)
  *     ties, and the one with the most free memory, then the most free SMs, then the
  *     lowest id wins;
  *   phase 2 (Phase Three): no such GPU; the earliest-available GPU (then lowest id) whose

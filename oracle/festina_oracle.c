@@ -611,7 +611,7 @@ int festina_oracle_preferred_at(const or_lut *L, const or_llms *Q, int32_t g, in
  * mem_s covers it and SM_free that step's SM level.  g is feasible when
  * T_avail + TTFT(SM_free, F_curr) < slo_ttft and TBT(SM_free, F_curr) < slo_tbt.
  * Phase Two: E_g = Power(F_curr) x Latency = P * (TTFT + Lout * TBT); the least E wins,
- * but every candidate within 2% of it (E_g <= 1.02 E_min) ties, and among those the most
+ * but every candidate within 2% of it (E_g <= E_min + 0.02 |E_min|) ties, and among those the most
  * free memory, then the most free SMs, then the lowest GPU id wins.
  * Phase Three: no candidate -> GPUs ordered by T_avail (then id); the first that meets
  * the SLO at F_max (the top level) with its SM_free takes the request.  Else a new GPU
@@ -637,7 +637,7 @@ typedef struct {
   double energy;
 } or_dispatch;
 
-#define OR_STABILITY 1.02
+#define OR_STABILITY 0.02
 
 /* Energy of the request on one operating point; the order of operations is fixed. */
 static double or_dispatch_energy(double p0, double kg, double s, double f, double u, double ttft, double lout,
@@ -705,7 +705,7 @@ static void or_dispatch_one(const or_lut *L, const or_avail *A, const or_request
   }
   if (any) {
     /* Phase Two with the stability tie-break */
-    const double bound = OR_STABILITY * emin;
+    const double bound = emin + OR_STABILITY * fabs(emin);
     int bg = -1, bmem = 0, bsm = 0;
     double be = 0.0;
     for (int g = 0; g < A->n_gpus; ++g) {

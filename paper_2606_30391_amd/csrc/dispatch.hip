@@ -9,9 +9,11 @@
 // k_dispatch   one wavefront per request; lanes stride over the model's hosts.  Per host:
 //                the first free-memory profile step that holds Req_mem gives T_avail and
 //                SM_free; the point (SM_free, F_curr) is feasible when T_avail + TTFT and
-//                TBT meet the SLOs; E = P * (TTFT + Lout * TBT) in float64.  Pass 1: the
-//                wavefront minimum E_min.  Pass 2: among hosts with E <= 1.02 E_min, the
-//                lexicographic best (most memory, most SMs, lowest id).  With no
+//                TBT meet the SLOs; E = P * (TTFT + Lout * TBT) in float64.  One pass
+//                evaluates every host (a lane's first two hosts stay in registers) and
+//                the wavefront takes E_min; among hosts with E <= E_min + 0.02 |E_min| the largest
+//                stability key (most memory, most SMs, lowest id packed in 64 bits) wins,
+//                and the lane holding it writes the result.  With no
 //                candidate: the hosts feasible at the top level, earliest T_avail (then
 //                lowest id).  Else lane k scores a new GPU at level k and the least energy
 //                (lowest k on ties) wins.
@@ -35,7 +37,7 @@ constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kHostBlock = 256;
 constexpr int kMaxSteps = 8;                 // profile steps loaded at once
-constexpr double kStability = 1.02;          // energies within 2% of the least tie
+constexpr double kStability = 0.02;          // energies within 2% of the least tie
 
 struct DspArgs {
   int32_t M, NS, NF, C, words;
@@ -147,6 +149,20 @@ __device__ __forceinline__ bool point_ok(const DspArgs &a, int r, int m, int pro
   return (float)e < __builtin_huge_valf();
 }
 
+// Stability order as one integer: more free memory, then more free SMs, then a lower GPU id
+// is a larger key (memory biased to unsigned; SM level < 256; id < 2^24); 0 = no candidate.
+__device__ __forceinline__ unsigned long long stability_key(int mem, int sm, int g) {
+  return ((unsigned long long)((unsigned)mem ^ 0x80000000u) << 32) | ((unsigned long long)(sm & 0xff) << 24) |
+         (unsigned long long)(0xffffffu - (unsigned)g);
+}
+
+__device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int off) {
+  const unsigned lo = __shfl_xor((unsigned)v, off, kWave), hi = __shfl_xor((unsigned)(v >> 32), off, kWave);
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+constexpr int kCached = 2;       // hosts per lane whose Phase One result stays in registers
+
 __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) {
   const int r = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   if (r >= a.R) return;
@@ -156,6 +172,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
   const int pt = a.prompt[r], pd = a.pred[r];
   int gsel = -1, ksel = -1, jsel = -1, phase = 0;
   double esel = inf;
+  bool writer = lane == 0;
   if (m >= 0 && m < a.M && pd >= 0 && pt >= 0) {
     const int prow = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
     const long long lout_i = ((long long)pd * 105 + 99) / 100;
@@ -163,50 +180,64 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
     const long long need = (long long)a.kv[m] * ((long long)pt + lout_i);
     const int nh = a.host_cnt[m];
     const int *hl = a.host_list + (size_t)m * a.G;
-    // pass 1: least energy at the current operating points
+    // Phase One at every host, least energy; the first kCached hosts of a lane are kept
     double emin = inf;
-    for (int h = lane; h < nh; h += kWave) {
+    double ec[kCached];
+    unsigned long long kc[kCached];
+#pragma unroll
+    for (int i = 0; i < kCached; ++i) {
+      ec[i] = inf;
+      kc[i] = 0ull;
+    }
+    for (int i = 0, h = lane; h < nh; ++i, h += kWave) {
       const int g = hl[h];
       const Point p = host_point(a, g, need);
       double e;
-      if (p.ok && point_ok(a, r, m, prow, p.b, p.sm, a.freq_cur[g], p.ta, (double)a.kdyn[g], lout, e) && e < emin)
-        emin = e;
+      if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, a.freq_cur[g], p.ta, (double)a.kdyn[g], lout, e))) continue;
+      emin = fmin(emin, e);
+#pragma unroll
+      for (int c = 0; c < kCached; ++c)
+        if (i == c) {
+          ec[c] = e;
+          kc[c] = stability_key(p.mem, p.sm, g);
+        }
     }
     for (int off = 32; off >= 1; off >>= 1) emin = fmin(emin, __shfl_xor(emin, off, kWave));
     if (emin < inf) {
-      // pass 2: the stability order over the candidates within 2% of the least energy
-      const double bound = kStability * emin;
-      int bg = INT_MAX, bmem = INT_MIN, bsm = INT_MIN;
-      double be = inf;
-      for (int h = lane; h < nh; h += kWave) {
+      // Phase Two: the largest stability key among the hosts within 2% of the least energy
+      const double bound = emin + kStability * fabs(emin);
+      unsigned long long best = 0ull;
+      double ebest = inf;
+#pragma unroll
+      for (int c = 0; c < kCached; ++c)
+        if (kc[c] > best && ec[c] <= bound) {
+          best = kc[c];
+          ebest = ec[c];
+        }
+      for (int h = lane + kCached * kWave; h < nh; h += kWave) {   // hosts past the cached ones
         const int g = hl[h];
         const Point p = host_point(a, g, need);
         double e;
         if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, a.freq_cur[g], p.ta, (double)a.kdyn[g], lout, e))) continue;
-        if (!(e <= bound)) continue;
-        if (p.mem > bmem || (p.mem == bmem && (p.sm > bsm || (p.sm == bsm && g < bg)))) {
-          bg = g;
-          bmem = p.mem;
-          bsm = p.sm;
-          be = e;
+        const unsigned long long key = stability_key(p.mem, p.sm, g);
+        if (e <= bound && key > best) {
+          best = key;
+          ebest = e;
         }
       }
+      unsigned long long wbest = best;
       for (int off = 32; off >= 1; off >>= 1) {
-        const int og = __shfl_xor(bg, off, kWave), om = __shfl_xor(bmem, off, kWave);
-        const int os = __shfl_xor(bsm, off, kWave);
-        const double oe = __shfl_xor(be, off, kWave);
-        if (om > bmem || (om == bmem && (os > bsm || (os == bsm && og < bg)))) {
-          bg = og;
-          bmem = om;
-          bsm = os;
-          be = oe;
-        }
+        const unsigned long long o = shfl_xor_u64(wbest, off);
+        wbest = o > wbest ? o : wbest;
       }
-      gsel = bg;
-      ksel = a.freq_cur[bg];
-      jsel = bsm;
-      phase = 1;
-      esel = be;
+      if (wbest != 0ull) {                 // the least-energy host is always within the bound
+        writer = best == wbest;            // exactly one lane holds the winning key
+        gsel = (int)(0xffffffu - (unsigned)(wbest & 0xffffffull));
+        jsel = (int)((wbest >> 24) & 0xffull);
+        ksel = a.freq_cur[gsel];
+        phase = 1;
+        esel = ebest;
+      }
     } else {
       // Phase Three: the earliest available host that meets the SLOs at the top level
       const int kmax = a.NF - 1;
@@ -268,7 +299,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       }
     }
   }
-  if (lane == 0) {
+  if (writer) {
     a.out_gpu[r] = gsel;
     a.out_freq[r] = ksel;
     a.out_sm[r] = jsel;
@@ -284,6 +315,7 @@ bool dsp_shapes_ok(const festina_lut *L, const festina_gpu_avail *A) {
   if (L->n_models < 1 || L->n_rows != kRows || L->n_sm < 1 || L->n_freq < 1) return false;
   if (A->n_gpus < 1 || A->n_steps < 1) return false;
   if ((long long)L->n_models * A->n_gpus > INT_MAX) return false;
+  if (A->n_gpus > 0xffffff) return false;       // GPU ids are packed in 24 bits
   return true;
 }
 

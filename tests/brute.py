@@ -340,7 +340,7 @@ def brute_dispatch(inp):
                 cands.append((e, g, sm, mem))
         if cands:
             emin = min(c[0] for c in cands)
-            tied = [c for c in cands if c[0] <= 1.02 * emin]                 # within 2%
+            tied = [c for c in cands if c[0] <= emin + 0.02 * abs(emin)]    # within 2%
             e, g, sm, mem = min(tied, key=lambda c: (-c[3], -c[2], c[1]))   # memory, SMs, id
             res.append((g, int(av["freq_cur"][g]), sm, 1, e))
             continue

@@ -99,3 +99,12 @@ def test_dispatch_many_hosts():
     """More hosting GPUs than lanes in a wavefront: several hosts per lane."""
     rng = np.random.default_rng(1800)
     parity(W.make_tiny_dispatch(rng, R=700, G=700, M=2, NS=4, NF=6, S=2), label="700 GPUs")
+
+
+def test_dispatch_negative_energies():
+    rng = np.random.default_rng(1900)
+    inp = W.make_tiny_dispatch(rng, R=2000, G=60, M=2, NS=3, NF=4, S=2)
+    inp["lut"]["p0_w"] = float(np.float32(2.0))
+    inp["avail"]["k_dyn_w"] = (-rng.uniform(0.0, 500.0, 60)).astype(np.float32)
+    got = parity(inp, label="negative energies")
+    assert np.any(got[4][got[3] == 1] < 0)

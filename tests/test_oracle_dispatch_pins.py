@@ -89,3 +89,17 @@ def test_dispatch_workload_invariants():
     for x, y in zip((g, k, j, ph), b[:4]):
         assert np.array_equal(x, y)
     assert np.array_equal(e, b[4])
+
+
+def test_dispatch_negative_energies():
+    """Negative power terms: the 2% band is taken on |E_min|, so the least-energy GPU is
+    always inside it and the stability order still decides among its neighbours."""
+    rng = np.random.default_rng(93)
+    for _ in range(30):
+        inp = W.make_tiny_dispatch(rng, R=30, G=8, M=2, NS=3, NF=4, S=2)
+        inp["lut"]["p0_w"] = float(np.float32(rng.uniform(0.0, 5.0)))
+        inp["avail"]["k_dyn_w"] = (-rng.uniform(0.0, 500.0, 8)).astype(np.float32)
+        o, b = oracle.dispatch(inp), brute_dispatch(inp)
+        for x, y in zip(o, b):
+            assert np.array_equal(x, y)
+        assert np.any(o[4][o[3] == 1] < 0)

@@ -94,7 +94,7 @@ PREFERRED = [
 
 
 DISPATCH = [
-    ("no stability margin", "#define OR_STABILITY 1.02", "#define OR_STABILITY 1.0"),
+    ("no stability margin", "#define OR_STABILITY 0.02", "#define OR_STABILITY 0.0"),
     ("least memory wins the tie", "if (bg < 0 || mem > bmem || (mem == bmem && sm > bsm)) {",
      "if (bg < 0 || mem < bmem || (mem == bmem && sm > bsm)) {"),
     ("free SMs ignored in the tie", "if (bg < 0 || mem > bmem || (mem == bmem && sm > bsm)) {",
