@@ -88,6 +88,22 @@ class _Dispatch(C.Structure):
                 ("energy", C.c_double)]
 
 
+class _Transfer(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("words", C.c_int32), ("resident", C.c_void_p), ("weights_mib", C.c_void_p),
+                ("state_mib", C.c_void_p), ("node", C.c_void_p), ("bw_intra_gbs", C.c_float),
+                ("bw_inter_gbs", C.c_float)]
+
+
+class _Moves(C.Structure):
+    _fields_ = [("n_requests", C.c_int32), ("src", C.c_void_p), ("model", C.c_void_p),
+                ("context_tokens", C.c_void_p), ("remaining_tokens", C.c_void_p), ("kv_kib", C.c_void_p),
+                ("token_kib", C.c_void_p)]
+
+
+class _Plan(C.Structure):
+    _fields_ = [("dest", C.c_void_p), ("freq_cur", C.c_void_p), ("sm_cur", C.c_void_p), ("batch", C.c_void_p)]
+
+
 def lib():
     global _lib
     if _lib is None:
@@ -130,6 +146,11 @@ def lib():
         L.festina_oracle_preferred_at.restype = C.c_int
         L.festina_oracle_dispatch.argtypes = [P(_Lut), P(_Avail), P(_Requests), C.c_int32, C.c_void_p, C.c_void_p]
         L.festina_oracle_dispatch.restype = C.c_int
+        L.festina_oracle_transfer_costs.argtypes = [P(_Transfer), C.c_int32, C.c_void_p]
+        L.festina_oracle_transfer_costs.restype = C.c_int
+        L.festina_oracle_request_moves.argtypes = [P(_Lut), P(_Transfer), P(_Plan), P(_Moves), C.c_void_p,
+                                                   C.c_void_p, C.c_void_p]
+        L.festina_oracle_request_moves.restype = C.c_int
         L.festina_oracle_fleet_ewr.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                                C.c_void_p, C.c_void_p, C.c_void_p]
         L.festina_oracle_fleet_ewr.restype = C.c_int
@@ -209,6 +230,12 @@ def _avail(d, pin):
                   pin(d["k_dyn_w"], np.float32), pin(d["resident"], np.uint32), pin(d["t_avail_ms"], np.float32),
                   pin(d["mem_free_mib"], np.int32), pin(d["sm_free"], np.int32),
                   pin(d["kv_kib_per_token"], np.int32), float(d["k_new_w"]))
+
+
+def _transfer(d, pin):
+    return _Transfer(int(d["n_gpus"]), int(d["words"]), pin(d["resident"], np.uint32), pin(d["weights_mib"], np.int32),
+                     pin(d["state_mib"], np.int32), pin(d["node"], np.int32), float(d["bw_intra_gbs"]),
+                     float(d["bw_inter_gbs"]))
 
 
 # ------------------------------------------------------------------ public API
@@ -386,3 +413,36 @@ def dispatch(inp: dict, sel=None):
     a = np.frombuffer(buf, dtype=np.dtype([("gpu", "<i4"), ("freq_level", "<i4"), ("sm_level", "<i4"),
                                            ("phase", "<i4"), ("energy", "<f8")]), count=n)
     return (a["gpu"].copy(), a["freq_level"].copy(), a["sm_level"].copy(), a["phase"].copy(), a["energy"].copy())
+
+
+def transfer_costs(inp: dict) -> np.ndarray:
+    """Oracle transfer-cost matrix e_uv (ms, float64, [G][G]) of App. F's device mapping."""
+    pin = _Pinned()
+    t = _transfer(inp["transfer"], pin)
+    G = int(inp["transfer"]["n_gpus"])
+    out = np.empty((G, G), np.float64)
+    if lib().festina_oracle_transfer_costs(C.byref(t), int(inp["n_models"]), _p(out)) != 0:
+        raise ValueError("oracle rejected the transfer arguments")
+    return out
+
+
+def request_moves(inp: dict):
+    """Oracle per-request decisions (finish in place / move with KV / move and recompute).
+
+    Returns (decision int32, remaining_ms float64, migrate_ms float64)."""
+    pin = _Pinned()
+    lut, t = _lut(inp["lut"], pin), _transfer(inp["transfer"], pin)
+    pl, mv = inp["plan"], inp["moves"]
+    plan = _Plan(pin(pl["dest"], np.int32), pin(pl["freq_cur"], np.int32), pin(pl["sm_cur"], np.int32),
+                 pin(pl["batch"], np.int32))
+    moves = _Moves(int(mv["n_requests"]), pin(mv["src"], np.int32), pin(mv["model"], np.int32),
+                   pin(mv["context_tokens"], np.int32), pin(mv["remaining_tokens"], np.int32),
+                   pin(mv["kv_kib"], np.int32), pin(mv["token_kib"], np.int32))
+    n = int(mv["n_requests"])
+    dec = np.empty(max(n, 1), np.int32)
+    rem = np.empty(max(n, 1), np.float64)
+    mig = np.empty(max(n, 1), np.float64)
+    if lib().festina_oracle_request_moves(C.byref(lut), C.byref(t), C.byref(plan), C.byref(moves), _p(dec), _p(rem),
+                                          _p(mig)) != 0:
+        raise ValueError("oracle rejected the request-move arguments")
+    return dec[:n], rem[:n], mig[:n]

@@ -51,6 +51,10 @@
  *   current-frequency dispatch (Sec. 3.3 as the paper runs it, Phases One to Three with
  *   the 2% stability tie-break and the F_max fallback): see the section at the end.
  *
+ *   transfer plan (App. F): the cost matrix e_uv = Bytes(u -> v) / BW(u, v) of the
+ *   minimum-cost device mapping, and the per-request choice to finish in place or move
+ *   (with the KV cache or a recompute of it): see the section at the end.
+ *
  * Request pre-processing (Sec. 3.2.1 input-length axis 256..8192; Sec. 3.2.2 / 3.3 the
  * 5% output-length safety pad):
  *   Lout = ceil(1.05 * predicted_out)            (integer: (105*L + 99) / 100)
@@ -781,5 +785,102 @@ int festina_oracle_dispatch(const or_lut *L, const or_avail *A, const or_request
   if (!or_lut_ok(L) || !A || !Q || !out || A->n_gpus < 0 || A->n_steps < 1 || Q->n_requests < 0) return 1;
   const int32_t n = sel ? n_sel : Q->n_requests;
   for (int32_t i = 0; i < n; ++i) or_dispatch_one(L, A, Q, sel ? sel[i] : i, &out[i]);
+  return 0;
+}
+
+/* ---------------------------------------------------------------- transfer plan (App. F) */
+/* "Transmission plan (device mapping)": the cost of sending the state now on GPU u to GPU v
+ * is e_uv = Bytes(u -> v) / BW(u, v), the input of the minimum-cost assignment.  Bytes
+ * counts the weights of u's resident models that v does not already hold plus u's request
+ * state selected for migration; keeping the state in place costs nothing (e_uu = 0).  BW
+ * is the intra-node link bandwidth between GPUs of one node, else the inter-node one.
+ * Times in ms: e = bytes * ms_per_byte, ms_per_byte = 1e3 / (GB/s * 1e9), in float64.
+ * "Selective request migration" and "what to transfer": an in-flight request on source u
+ * whose state goes to v = dest[u] moves only when its remaining decode time at u exceeds
+ * its migration time; it then moves its tokens plus either its KV cache or a recompute of
+ * it on v, whichever is faster. */
+typedef struct {
+  int32_t n_gpus, words;
+  const uint32_t *resident;        /* [G][words] models resident now */
+  const int32_t *weights_mib;      /* [M] */
+  const int32_t *state_mib;        /* [G] request state selected for migration */
+  const int32_t *node;             /* [G] */
+  float bw_intra_gbs, bw_inter_gbs;
+} or_transfer;
+
+static double or_ms_per_byte(double gbs) { return 1e3 / (gbs * 1e9); }
+
+static double or_link_ms_per_byte(const or_transfer *T, int u, int v) {
+  return T->node[u] == T->node[v] ? or_ms_per_byte((double)T->bw_intra_gbs) : or_ms_per_byte((double)T->bw_inter_gbs);
+}
+
+int festina_oracle_transfer_costs(const or_transfer *T, int32_t n_models, double *cost) {
+  if (!T || !cost || T->n_gpus < 0 || T->words < (n_models + 31) / 32 || n_models < 1) return 1;
+  for (int u = 0; u < T->n_gpus; ++u)
+    for (int v = 0; v < T->n_gpus; ++v) {
+      double e = 0.0;
+      if (u != v) {
+        int64_t mib = T->state_mib[u];
+        for (int m = 0; m < n_models; ++m) {
+          const int on_u = (T->resident[(size_t)u * T->words + (size_t)(m / 32)] >> (m % 32)) & 1u;
+          const int on_v = (T->resident[(size_t)v * T->words + (size_t)(m / 32)] >> (m % 32)) & 1u;
+          if (on_u && !on_v) mib += T->weights_mib[m];
+        }
+        e = (double)(mib * 1048576) * or_link_ms_per_byte(T, u, v);
+      }
+      cost[(size_t)u * T->n_gpus + (size_t)v] = e;
+    }
+  return 0;
+}
+
+typedef struct {
+  int32_t n_requests;
+  const int32_t *src;              /* [Q] source GPU */
+  const int32_t *model;            /* [Q] */
+  const int32_t *context_tokens;   /* [Q] prompt + generated so far */
+  const int32_t *remaining_tokens; /* [Q] predicted tokens still to generate */
+  const int32_t *kv_kib;           /* [Q] KV-cache size */
+  const int32_t *token_kib;        /* [Q] token state (prompt and generated ids) */
+} or_moves;
+
+typedef struct {
+  const int32_t *dest;             /* [G] destination of each GPU's state (the plan) */
+  const int32_t *freq_cur, *sm_cur, *batch;   /* [G] operating point and decode batch */
+} or_plan;
+
+/* decision: 0 = finish on the source (or the state stays), 1 = move with the KV cache,
+ * 2 = move the tokens and recompute the KV cache on the destination, -1 = invalid request
+ * (GPU, model, level or token count out of range); times 0 unless computed. */
+int festina_oracle_request_moves(const or_lut *L, const or_transfer *T, const or_plan *P, const or_moves *Q,
+                                 int32_t *decision, double *remaining_ms, double *migrate_ms) {
+  if (!or_lut_ok(L) || !T || !P || !Q || !decision || !remaining_ms || !migrate_ms) return 1;
+  for (int q = 0; q < Q->n_requests; ++q) {
+    decision[q] = -1;
+    remaining_ms[q] = 0.0;
+    migrate_ms[q] = 0.0;
+    const int u = Q->src[q], m = Q->model[q];
+    if (u < 0 || u >= T->n_gpus || m < 0 || m >= L->n_models) continue;
+    const int v = P->dest[u];
+    if (v < 0 || v >= T->n_gpus) continue;
+    const int ju = P->sm_cur[u], ku = P->freq_cur[u], jv = P->sm_cur[v], kv = P->freq_cur[v];
+    const int32_t Bu = P->batch[u];
+    const int crow = or_prompt_row(Q->context_tokens[q]);
+    if (ju < 0 || ju >= L->n_sm || ku < 0 || ku >= L->n_freq || jv < 0 || jv >= L->n_sm || kv < 0 ||
+        kv >= L->n_freq || Bu < 0 || crow < 0 || Q->remaining_tokens[q] < 0 || Q->kv_kib[q] < 0 || Q->token_kib[q] < 0)
+      continue;
+    decision[q] = 0;
+    const int bu = Bu + 1 > OR_ROWS ? OR_ROWS : Bu + 1;
+    const double rem = (double)Q->remaining_tokens[q] * (double)L->dc[or_cell(L, m, bu - 1, ju, ku)];
+    remaining_ms[q] = rem;
+    if (v == u) continue;                        /* the state stays: nothing to move */
+    const double mpb = or_link_ms_per_byte(T, u, v);
+    const double kv_ms = (double)((int64_t)Q->kv_kib[q] * 1024) * mpb;
+    const double tok_ms = (double)((int64_t)Q->token_kib[q] * 1024) * mpb;
+    const double rec_ms = (double)L->pf[or_cell(L, m, crow, jv, kv)];
+    const int use_kv = kv_ms < rec_ms;
+    const double mig = tok_ms + (use_kv ? kv_ms : rec_ms);
+    migrate_ms[q] = mig;
+    if (rem > mig) decision[q] = use_kv ? 1 : 2;
+  }
   return 0;
 }

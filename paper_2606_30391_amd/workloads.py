@@ -617,3 +617,86 @@ def make_tiny_dispatch(rng: np.random.Generator, R=None, G=None, M=None, NS=None
                 "slo_ttft_ms": rng.uniform(10.0, 90.0, R).astype(np.float32),
                 "slo_tbt_ms": rng.uniform(5.0, 45.0, R).astype(np.float32)}
     return {"lut": lut, "avail": avail, "requests": requests, "meta": {}}
+
+
+# --------------------------------------------------------------------------- transfer plan
+TRANSFER_SEED = CONFIG_SEED_BASE + 80
+GPUS_PER_NODE = 8
+XGMI_LINK_GBS = 153.6      # one GPU-to-GPU xGMI link inside a node
+NIC_GBS = 50.0             # 400 Gb/s between nodes
+
+
+def make_transfer(seed: int | None = None, n_gpus: int = 2048, requests_per_gpu: int = 8) -> dict:
+    """A 2,048-GPU fleet about to be reconfigured (configuration 5's shape), for the transfer
+    cost matrix of the device mapping and the per-request move decisions.
+
+    Tables as configuration 3; each GPU hosts 1-4 distinct models of 32, whose weights take
+    U(8, 80) GiB; GPUs sit 8 to a node (xGMI links of 153.6 GB/s inside a node, 50 GB/s
+    between nodes); each GPU has U(0, 16) GiB of request state selected for migration.  The
+    plan keeps half of the GPUs' state in place and sends the other half to a random
+    permutation of those GPUs.  Each GPU has ~8 in-flight requests of its models: context
+    lognormal(6, 1) prompt tokens plus U{0..500} generated, remaining tokens lognormal(5, 1),
+    KV cache 128-640 KiB per token by model, 4 bytes per token of token state, and each GPU
+    an operating point (uniform SM and frequency level) and decode batch min(Poisson(4), 31).
+    """
+    if seed is None:
+        seed = TRANSFER_SEED
+    rng = np.random.default_rng(seed)
+    M, NS, NF, G = 32, 8, 16, int(n_gpus)
+    s, f = sm_levels(NS), freq_levels(NF)
+    a, c, cp = _latency_params(rng, M, prefill=True)
+    pf, dc = _tables(rng, M, s, f, a, c, cp, noise=True)
+    lut = _lut(pf, dc, s, f)
+    nres = rng.integers(1, 5, size=G)
+    models_per_gpu = _distinct_models(rng, G, M, nres)
+    weights = np.rint(rng.uniform(8.0, 80.0, M) * 1024).astype(np.int32)
+    state = rng.integers(0, 16 * 1024 + 1, G).astype(np.int32)
+    transfer = {"n_gpus": G, "words": (M + 31) // 32, "resident": _resident_bits(models_per_gpu, M),
+                "weights_mib": weights, "state_mib": state,
+                "node": (np.arange(G) // GPUS_PER_NODE).astype(np.int32),
+                "bw_intra_gbs": XGMI_LINK_GBS, "bw_inter_gbs": NIC_GBS}
+    dest = np.arange(G, dtype=np.int32)
+    moving = np.flatnonzero(rng.random(G) < 0.5)
+    dest[moving] = moving[rng.permutation(len(moving))]
+    plan = {"dest": dest, "freq_cur": rng.integers(0, NF, G).astype(np.int32),
+            "sm_cur": rng.integers(0, NS, G).astype(np.int32),
+            "batch": np.minimum(rng.poisson(4.0, G), 31).astype(np.int32)}
+    Q = G * int(requests_per_gpu)
+    src = rng.integers(0, G, Q).astype(np.int32)
+    model = np.array([models_per_gpu[g][int(rng.integers(0, len(models_per_gpu[g])))] for g in src], np.int32)
+    ctx = (_lognormal_tokens(rng, 6.0, Q, 16, 8192) + rng.integers(0, 501, Q)).clip(1, 8192).astype(np.int32)
+    kv_tok = rng.integers(128, 641, M)
+    moves = {"n_requests": Q, "src": src, "model": model, "context_tokens": ctx,
+             "remaining_tokens": _lognormal_tokens(rng, 5.0, Q, 0, 8192),
+             "kv_kib": (kv_tok[model] * ctx).astype(np.int32), "token_kib": ((ctx * 4 + 1023) // 1024).astype(np.int32)}
+    return {"lut": lut, "n_models": M, "transfer": transfer, "plan": plan, "moves": moves,
+            "meta": {"seed": seed, "models_per_gpu": models_per_gpu}}
+
+
+def make_tiny_transfer(rng: np.random.Generator, G=None, M=None, NS=None, NF=None, Q=None) -> dict:
+    """Small random transfer instance for pins and parity edge cases."""
+    G = int(rng.integers(1, 9)) if G is None else G
+    M = int(rng.integers(1, 5)) if M is None else M
+    NS = int(rng.integers(1, 5)) if NS is None else NS
+    NF = int(rng.integers(1, 6)) if NF is None else NF
+    Q = int(rng.integers(0, 20)) if Q is None else Q
+    s, f = sm_levels(NS), freq_levels(NF)
+    pf = rng.uniform(5.0, 600.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    dc = rng.uniform(2.0, 40.0, (M, N_ROWS, NS, NF)).astype(np.float32)
+    lut = _lut(pf, dc, s, f)
+    models_per_gpu = [np.flatnonzero(rng.random(M) < 0.5) for _ in range(G)]
+    transfer = {"n_gpus": G, "words": (M + 31) // 32, "resident": _resident_bits(models_per_gpu, M),
+                "weights_mib": rng.integers(0, 90000, M).astype(np.int32),
+                "state_mib": rng.integers(0, 20000, G).astype(np.int32),
+                "node": (np.arange(G) // int(rng.integers(1, 5))).astype(np.int32),
+                "bw_intra_gbs": float(np.float32(rng.uniform(50, 400))),
+                "bw_inter_gbs": float(np.float32(rng.uniform(5, 100)))}
+    plan = {"dest": rng.permutation(G).astype(np.int32), "freq_cur": rng.integers(0, NF, G).astype(np.int32),
+            "sm_cur": rng.integers(0, NS, G).astype(np.int32), "batch": rng.integers(0, 32, G).astype(np.int32)}
+    ctx = rng.integers(1, 9000, Q).astype(np.int32)
+    moves = {"n_requests": Q, "src": rng.integers(0, G, Q).astype(np.int32),
+             "model": rng.integers(0, M, Q).astype(np.int32), "context_tokens": ctx,
+             "remaining_tokens": rng.integers(0, 600, Q).astype(np.int32),
+             "kv_kib": (rng.integers(0, 800, Q) * ctx // 8).astype(np.int32),
+             "token_kib": ((ctx * 4 + 1023) // 1024).astype(np.int32)}
+    return {"lut": lut, "n_models": M, "transfer": transfer, "plan": plan, "moves": moves, "meta": {}}

@@ -363,3 +363,55 @@ def brute_dispatch(inp):
             res.append((-1, -1, -1, 0, np.inf))
     a = np.array([x[:4] for x in res], np.int32).reshape(-1, 4)
     return a[:, 0], a[:, 1], a[:, 2], a[:, 3], np.array([x[4] for x in res])
+
+
+# ------------------------------------------------------------------ transfer plan
+def transfer_mib(inp):
+    """Bytes(u -> v) in MiB from Python sets: u's models that v lacks plus u's state; 0 on the diagonal."""
+    t = inp["transfer"]
+    G, M = t["n_gpus"], inp["n_models"]
+    sets = [{m for m in range(M) if (int(t["resident"][g, m // 32]) >> (m % 32)) & 1} for g in range(G)]
+    out = np.zeros((G, G), np.int64)
+    for u in range(G):
+        for v in range(G):
+            if u != v:
+                out[u, v] = int(t["state_mib"][u]) + sum(int(t["weights_mib"][m]) for m in sets[u] - sets[v])
+    return out
+
+
+def link_ms_per_byte(inp, u, v):
+    t = inp["transfer"]
+    gbs = float(np.float32(t["bw_intra_gbs"] if t["node"][u] == t["node"][v] else t["bw_inter_gbs"]))
+    return 1e3 / (gbs * 1e9)
+
+
+def brute_moves(inp):
+    """Per request: -1 invalid, 0 finish in place, 1 move with the KV cache, 2 move and recompute."""
+    lut, t, pl, mv = inp["lut"], inp["transfer"], inp["plan"], inp["moves"]
+    NS, NF, M, G = lut["n_sm"], lut["n_freq"], lut["n_models"], t["n_gpus"]
+    res = []
+    for q in range(mv["n_requests"]):
+        u, m = int(mv["src"][q]), int(mv["model"][q])
+        ok = 0 <= u < G and 0 <= m < M
+        v = int(pl["dest"][u]) if ok else -1
+        ok = ok and 0 <= v < G
+        if ok:
+            ju, ku, jv, kv = (int(pl["sm_cur"][u]), int(pl["freq_cur"][u]), int(pl["sm_cur"][v]), int(pl["freq_cur"][v]))
+            row = prompt_row(int(mv["context_tokens"][q]))
+            ok = (0 <= ju < NS and 0 <= ku < NF and 0 <= jv < NS and 0 <= kv < NF and int(pl["batch"][u]) >= 0
+                  and row is not None and row >= 0 and min(int(mv["remaining_tokens"][q]), int(mv["kv_kib"][q]),
+                                                           int(mv["token_kib"][q])) >= 0)
+        if not ok:
+            res.append((-1, 0.0, 0.0))
+            continue
+        b = min(int(pl["batch"][u]) + 1, 32)
+        remaining = int(mv["remaining_tokens"][q]) * float(lut["dc"][m, b - 1, ju, ku])
+        if v == u:
+            res.append((0, remaining, 0.0))
+            continue
+        mpb = link_ms_per_byte(inp, u, v)
+        kv_ms = (int(mv["kv_kib"][q]) * 1024) * mpb
+        rec_ms = float(lut["pf"][m, row, jv, kv])
+        mig = (int(mv["token_kib"][q]) * 1024) * mpb + min(kv_ms, rec_ms)
+        res.append(((1 if kv_ms < rec_ms else 2) if remaining > mig else 0, remaining, mig))
+    return (np.array([r[0] for r in res], np.int32), np.array([r[1] for r in res]), np.array([r[2] for r in res]))

@@ -167,3 +167,23 @@ def golden_dispatch(variant=None):
            "slo_ttft_ms": np.array([q["slo_ttft_ms"]], np.float32),
            "slo_tbt_ms": np.array([q["slo_tbt_ms"]], np.float32)}
     return {"lut": lut, "avail": avail, "requests": req}, exp, d
+
+
+def golden_transfer():
+    """Inputs of the hand-worked transfer example."""
+    d = load_golden("transfer_worked_example.json")
+    M = d["n_models"]
+    G = len(d["resident"])
+    res = np.zeros((G, 1), np.uint32)
+    for g, ms in enumerate(d["resident"]):
+        for m in ms:
+            res[g, 0] |= np.uint32(1 << m)
+    transfer = {"n_gpus": G, "words": 1, "resident": res, "weights_mib": np.array(d["weights_mib"], np.int32),
+                "state_mib": np.array(d["state_mib"], np.int32), "node": np.array(d["node"], np.int32),
+                "bw_intra_gbs": d["bw_intra_gbs"], "bw_inter_gbs": d["bw_inter_gbs"]}
+    plan = {k: np.array(v, np.int32) for k, v in d["plan"].items()}
+    mv = d["moves"]
+    moves = {"n_requests": len(mv)}
+    for k in ("src", "model", "context_tokens", "remaining_tokens", "kv_kib", "token_kib"):
+        moves[k] = np.array([x[k] for x in mv], np.int32)
+    return {"lut": _tables(d["lut"]), "n_models": M, "transfer": transfer, "plan": plan, "moves": moves}, d

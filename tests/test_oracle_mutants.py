@@ -115,6 +115,21 @@ DISPATCH = [
 ]
 
 
+TRANSFER = [
+    ("weights the destination already holds", "if (on_u && !on_v) mib += T->weights_mib[m];",
+     "if (on_u) mib += T->weights_mib[m];"),
+    ("request state not counted", "int64_t mib = T->state_mib[u];", "int64_t mib = 0;"),
+    ("link classes swapped", "return T->node[u] == T->node[v] ?", "return T->node[u] != T->node[v] ?"),
+    ("cost on the diagonal", "      if (u != v) {\n        int64_t mib", "      if (1) {\n        int64_t mib"),
+    ("remaining time at the destination", "L->dc[or_cell(L, m, bu - 1, ju, ku)]", "L->dc[or_cell(L, m, bu - 1, jv, kv)]"),
+    ("recompute at the source", "L->pf[or_cell(L, m, crow, jv, kv)]", "L->pf[or_cell(L, m, crow, ju, ku)]"),
+    ("always the KV cache", "const int use_kv = kv_ms < rec_ms;", "const int use_kv = 1;"),
+    ("token state forgotten", "const double mig = tok_ms + (use_kv ? kv_ms : rec_ms);",
+     "const double mig = (use_kv ? kv_ms : rec_ms);"),
+    ("move at equal times", "if (rem > mig) decision[q]", "if (rem >= mig) decision[q]"),
+]
+
+
 def _run_pins(tmp_path, name, old, new, suite):
     src = open(SRC).read()
     assert src.count(old) == 1, f"mutation anchor not unique/present: {name}"
@@ -157,4 +172,10 @@ def test_preferred_pins_reject_mutant(tmp_path, name, old, new):
 @pytest.mark.parametrize("name,old,new", DISPATCH, ids=[p[0] for p in DISPATCH])
 def test_dispatch_pins_reject_mutant(tmp_path, name, old, new):
     rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_dispatch_pins.py")
+    assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
+
+
+@pytest.mark.parametrize("name,old,new", TRANSFER, ids=[p[0] for p in TRANSFER])
+def test_transfer_pins_reject_mutant(tmp_path, name, old, new):
+    rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_transfer_pins.py")
     assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
