@@ -22,6 +22,10 @@
  *       and energy-weighted frequency (Eq. preferred_sm, Eq. preferred_frequency);
  *   festina_fleet_ewr         -- the fleet's energy waste, optimal energy and energy
  *       waste ratio (Eq. energy_waste, energy_optimal, energy_waste_ratio);
+ * the transfer plan after a reconfiguration (App. F):
+ *   festina_transfer_costs    -- the device-mapping cost matrix e_uv = Bytes / BW;
+ *   festina_request_moves     -- per in-flight request: finish in place, or move with the
+ *       KV cache, or move the tokens and recompute;
  * and the paper's own dispatcher, for comparison with the exhaustive search:
  *   festina_dispatch_requests -- one operating point per GPU (its current frequency),
  *       the 2% stability tie-break, the F_max fallback and scale-out (Sec. 3.3).
@@ -356,6 +360,62 @@ size_t festina_dispatch_workspace_bytes(const festina_lut *lut, const festina_gp
 festina_status festina_dispatch_requests(const festina_lut *lut, const festina_gpu_avail *avail,
                                          const festina_requests *req, festina_dispatches *out,
                                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* Transfer plan after a reconfiguration (App. F).  A GPU's state is its resident models'
+ * weights plus its request state selected for migration.  Sending GPU u's state to GPU v
+ * moves state_mib[u] plus the weights of u's resident models that v does not hold; it
+ * runs at bw_intra_gbs between GPUs of one node (equal node ids), else at bw_inter_gbs. */
+typedef struct festina_transfer {
+  int32_t n_gpus;                    /* G >= 1 */
+  int32_t n_models;                  /* M >= 1 */
+  const uint32_t *resident;          /* [G][(M+31)/32] models resident now */
+  const int32_t *weights_mib;        /* [M] */
+  const int32_t *state_mib;          /* [G] */
+  const int32_t *node;               /* [G] */
+  float bw_intra_gbs, bw_inter_gbs;  /* GB/s, > 0 */
+} festina_transfer;
+
+/* Device-mapping cost matrix: cost[u][v] = e_uv = Bytes(u -> v) / BW(u, v) in ms (float32,
+ * row-major [G][G], device memory written by the call), e_uu = 0; Bytes in bytes (MiB =
+ * 2^20 B), time = bytes * 1e3 / (GB/s * 1e9) evaluated in float64 and rounded once.  This
+ * is the input of the minimum-cost assignment (Kuhn-Munkres), which this library does not
+ * solve.  One kernel launch on `stream`. */
+festina_status festina_transfer_costs(const festina_transfer *transfer, float *cost, void *stream);
+
+/* The plan: dest[u] = the GPU that receives GPU u's state (u itself: it stays), and each
+ * GPU's operating point (SM level, frequency level) and decode batch. */
+typedef struct festina_plan {
+  const int32_t *dest, *freq_cur, *sm_cur, *batch;   /* [G] */
+} festina_plan;
+
+/* In-flight requests whose GPU is being reconfigured. */
+typedef struct festina_inflight {
+  int32_t n_requests;                /* Q >= 0 */
+  const int32_t *src;                /* [Q] GPU now serving the request */
+  const int32_t *model;              /* [Q] */
+  const int32_t *context_tokens;     /* [Q] prompt plus tokens generated so far, >= 1 */
+  const int32_t *remaining_tokens;   /* [Q] tokens still to generate (predicted) */
+  const int32_t *kv_kib;             /* [Q] KV-cache size */
+  const int32_t *token_kib;          /* [Q] token state (prompt and generated ids) */
+} festina_inflight;
+
+/* Per request (device memory, written by the call):
+ *   remaining_ms = remaining_tokens * TBT at the source (dc at its batch row and point);
+ *   migrate_ms   = token transfer + the faster of KV transfer and recompute (pf at the
+ *                  context's prompt bucket at the destination's point), 0 when the
+ *                  source's state stays (dest[src] == src);
+ *   decision     = 1 move with the KV cache, 2 move the tokens and recompute, when
+ *                  remaining_ms > migrate_ms; 0 finish in place (or the state stays);
+ *                  -1 invalid request (GPU, model, level or token count out of range).
+ * Times evaluated in float64 and rounded once to float32. */
+typedef struct festina_moves {
+  int32_t *decision;
+  float *remaining_ms, *migrate_ms;
+} festina_moves;
+
+festina_status festina_request_moves(const festina_lut *lut, const festina_transfer *transfer,
+                                     const festina_plan *plan, const festina_inflight *req,
+                                     festina_moves *out, void *stream);
 
 /* Measurement hook, not part of the search.  While set, festina_score_placements
  * records `score_begin` on its stream immediately before its scoring kernel and

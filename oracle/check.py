@@ -21,6 +21,9 @@ the tested cells.  EWR: per-GPU frequencies exactly, waste and totals within 1e-
 Dispatch, per request: GPU, levels and phase exactly, and the float32 energy equal to the
 oracle's float64 energy rounded to float32 (both sides evaluate the same float64
 expression, so the 2% decision is taken on identical values).
+Transfer plan: every cost equal to the oracle's float64 cost rounded to float32; every
+decision equal, and both times equal to the oracle's rounded to float32 (same float64
+evaluation order on both sides).
 """
 from __future__ import annotations
 
@@ -256,4 +259,21 @@ def check_dispatch(oracle_out, gpu_out) -> Report:
             continue
         if not (np.float32(oe[i]) == ge[i]):
             rep.mismatches.append((i, "energy", float(ge[i]), float(oe[i])))
+    return rep
+
+
+def check_transfer(oracle_costs, oracle_moves, gpu_costs, gpu_moves) -> Report:
+    rep = Report(n=oracle_costs.size + len(oracle_moves[0]))
+    want = oracle_costs.astype(np.float32)
+    bad = np.argwhere(want != gpu_costs)
+    if len(bad):
+        u, v = bad[0]
+        rep.mismatches.append(("cost", len(bad), (int(u), int(v)), float(gpu_costs[u, v]), float(oracle_costs[u, v])))
+    od, orem, omig = oracle_moves
+    gd, grem, gmig = gpu_moves
+    for name, a, b in (("decision", gd, od), ("remaining_ms", grem, orem.astype(np.float32)),
+                       ("migrate_ms", gmig, omig.astype(np.float32))):
+        bad = np.flatnonzero(a != b)
+        if len(bad):
+            rep.mismatches.append((name, len(bad), int(bad[0]), float(a[bad[0]]), float(b[bad[0]])))
     return rep

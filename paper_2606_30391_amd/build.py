@@ -6,7 +6,8 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", n) for n in ("festina.hip", "sweep.hip", "preferred.hip", "dispatch.hip")]
+SRCS = [os.path.join(HERE, "csrc", n) for n in ("festina.hip", "sweep.hip", "preferred.hip", "dispatch.hip",
+                                                       "transfer.hip")]
 LIB = os.path.join(HERE, "libfestina.so")
 
 # -packed-fp32-ops: no v_pk_*_f32 from the compiler (plain fp32 VALU only)

@@ -2,7 +2,7 @@
 
 Argument marshalling only: every step of the search runs in the HIP library
 (``libfestina.so`` built from ``csrc/festina.hip``, ``csrc/sweep.hip``,
-``csrc/preferred.hip`` and ``csrc/dispatch.hip``).  PyTorch provides device
+``csrc/preferred.hip``, ``csrc/dispatch.hip`` and ``csrc/transfer.hip``).  PyTorch provides device
 memory and streams.  There is no CPU fallback: if the library is missing this
 module raises.
 """
@@ -104,11 +104,31 @@ class festina_dispatches(C.Structure):
                 ("phase", C.c_void_p), ("energy_mj", C.c_void_p)]
 
 
+class festina_transfer(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("n_models", C.c_int32), ("resident", C.c_void_p),
+                ("weights_mib", C.c_void_p), ("state_mib", C.c_void_p), ("node", C.c_void_p),
+                ("bw_intra_gbs", C.c_float), ("bw_inter_gbs", C.c_float)]
+
+
+class festina_plan(C.Structure):
+    _fields_ = [("dest", C.c_void_p), ("freq_cur", C.c_void_p), ("sm_cur", C.c_void_p), ("batch", C.c_void_p)]
+
+
+class festina_inflight(C.Structure):
+    _fields_ = [("n_requests", C.c_int32), ("src", C.c_void_p), ("model", C.c_void_p),
+                ("context_tokens", C.c_void_p), ("remaining_tokens", C.c_void_p), ("kv_kib", C.c_void_p),
+                ("token_kib", C.c_void_p)]
+
+
+class festina_moves(C.Structure):
+    _fields_ = [("decision", C.c_void_p), ("remaining_ms", C.c_void_p), ("migrate_ms", C.c_void_p)]
+
+
 EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_workspace_bytes",
             "festina_score_placements", "festina_migrations_workspace_bytes", "festina_score_migrations",
             "festina_sweep_batches", "festina_preferred_configs", "festina_ewr_workspace_bytes",
             "festina_fleet_ewr", "festina_dispatch_workspace_bytes", "festina_dispatch_requests",
-            "festina_set_timing_events")
+            "festina_transfer_costs", "festina_request_moves", "festina_set_timing_events")
 
 _lib = None
 
@@ -150,6 +170,11 @@ def lib():
         L.festina_dispatch_requests.argtypes = [P(festina_lut), P(festina_gpu_avail), P(festina_requests),
                                                 P(festina_dispatches), C.c_void_p, C.c_size_t, C.c_void_p]
         L.festina_dispatch_requests.restype = C.c_int
+        L.festina_transfer_costs.argtypes = [P(festina_transfer), C.c_void_p, C.c_void_p]
+        L.festina_transfer_costs.restype = C.c_int
+        L.festina_request_moves.argtypes = [P(festina_lut), P(festina_transfer), P(festina_plan),
+                                            P(festina_inflight), P(festina_moves), C.c_void_p]
+        L.festina_request_moves.restype = C.c_int
         L.festina_set_timing_events.argtypes = [C.c_void_p] * 4
         L.festina_set_timing_events.restype = None
         _lib = L
@@ -428,6 +453,56 @@ class DeviceDispatch:
         return tuple(self.o[k][:R].cpu().numpy() for k in ("gpu", "freq_level", "sm_level", "phase", "energy_mj"))
 
 
+class DeviceTransfer:
+    """A reconfiguring fleet on the device: the device-mapping cost matrix and the
+    in-flight requests' finish-or-move decisions."""
+
+    def __init__(self, inp: dict, device="cuda"):
+        import torch
+        lut, tr, pl, mv = inp["lut"], inp["transfer"], inp["plan"], inp["moves"]
+        d = lambda a, t: _dev(a, t, device)
+        self.t = {"sm_level": d(lut["sm_level"], np.float32), "freq_level": d(lut["freq_level"], np.float32),
+                  "pf": d(lut["pf"], np.float32), "dc": d(lut["dc"], np.float32),
+                  "resident": d(np.asarray(tr["resident"], np.uint32).view(np.int32), np.int32)}
+        for k in ("weights_mib", "state_mib", "node"):
+            self.t[k] = d(tr[k], np.int32)
+        for k in ("dest", "freq_cur", "sm_cur", "batch"):
+            self.t["plan_" + k] = d(pl[k], np.int32)
+        for k in ("src", "model", "context_tokens", "remaining_tokens", "kv_kib", "token_kib"):
+            self.t["req_" + k] = d(mv[k], np.int32)
+        t = self.t
+        self.lut = festina_lut(int(lut["n_models"]), int(lut["n_rows"]), int(lut["n_sm"]), int(lut["n_freq"]),
+                               _ptr(t["sm_level"]), _ptr(t["freq_level"]), _ptr(t["pf"]), _ptr(t["dc"]),
+                               float(lut["p0_w"]))
+        self.G = int(tr["n_gpus"])
+        self.transfer = festina_transfer(self.G, int(inp["n_models"]), _ptr(t["resident"]), _ptr(t["weights_mib"]),
+                                         _ptr(t["state_mib"]), _ptr(t["node"]), float(tr["bw_intra_gbs"]),
+                                         float(tr["bw_inter_gbs"]))
+        self.plan = festina_plan(_ptr(t["plan_dest"]), _ptr(t["plan_freq_cur"]), _ptr(t["plan_sm_cur"]),
+                                 _ptr(t["plan_batch"]))
+        self.Q = int(mv["n_requests"])
+        self.req = festina_inflight(self.Q, *(_ptr(t["req_" + k]) for k in ("src", "model", "context_tokens",
+                                                                           "remaining_tokens", "kv_kib",
+                                                                           "token_kib")))
+        self.cost = torch.empty((self.G, self.G), dtype=torch.float32, device=device)
+        n = max(self.Q, 1)
+        self.decision = torch.empty(n, dtype=torch.int32, device=device)
+        self.remaining = torch.empty(n, dtype=torch.float32, device=device)
+        self.migrate = torch.empty(n, dtype=torch.float32, device=device)
+        self.moves = festina_moves(_ptr(self.decision), _ptr(self.remaining), _ptr(self.migrate))
+
+    def run_costs(self, stream=None):
+        festina_transfer_costs(self.transfer, self.cost, stream)
+
+    def run_moves(self, stream=None):
+        festina_request_moves(self.lut, self.transfer, self.plan, self.req, self.moves, stream)
+
+    def results(self):
+        Q = self.Q
+        return (self.cost.cpu().numpy(), self.decision[:Q].cpu().numpy(), self.remaining[:Q].cpu().numpy(),
+                self.migrate[:Q].cpu().numpy())
+
+
 # ------------------------------------------------------------------ the ABI calls
 def festina_placements_workspace_bytes(lut, gpus, req) -> int:
     return int(lib().festina_placements_workspace_bytes(C.byref(lut), C.byref(gpus), C.byref(req)))
@@ -487,3 +562,16 @@ def festina_dispatch_requests(lut, avail, req, out, workspace, workspace_bytes, 
                                          int(workspace_bytes), _stream_handle(stream))
     if st != FESTINA_OK:
         raise FestinaError(st, "festina_dispatch_requests")
+
+
+def festina_transfer_costs(transfer, cost, stream=None) -> None:
+    st = lib().festina_transfer_costs(C.byref(transfer), _ptr(cost), _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_transfer_costs")
+
+
+def festina_request_moves(lut, transfer, plan, req, out, stream=None) -> None:
+    st = lib().festina_request_moves(C.byref(lut), C.byref(transfer), C.byref(plan), C.byref(req), C.byref(out),
+                                     _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_request_moves")
