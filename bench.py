@@ -18,8 +18,9 @@ oracle timed on a bounded sample of the same workload on this host.  Outside the
 timed steps, ``next_rows`` measures the local schedulers' SM/frequency sweep over
 1,024 GPUs x 64 epochs of task batches (one kernel per call), and the preferred
 configuration of every LLM instance on a 2,048-GPU fleet plus the fleet's energy waste
-ratio, and the paper's own current-frequency dispatcher (65,536 requests, 512 GPUs), the
-same way.
+ratio, the paper's own current-frequency dispatcher (65,536 requests, 512 GPUs), and the
+transfer plan of a 2,048-GPU reconfiguration (cost matrix, per-request moves), the same
+way.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --per-config     (one JSON line per configuration, then the step line)
@@ -253,6 +254,40 @@ def dispatch_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
     return row
 
 
+def transfer_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
+    """The transfer plan (App. F): the dense device-mapping cost matrix (the dominant,
+    store-bound kernel) and the in-flight requests' decisions."""
+    inp = W.make_transfer()
+    dt = F.DeviceTransfer(inp, "cuda")
+    cost_ms = timed_calls(hip, torch, dt.run_costs, calls, warmup)
+    moves_ms = timed_calls(hip, torch, dt.run_moves, calls, warmup)
+    tr, M, Q = inp["transfer"], inp["n_models"], inp["moves"]["n_requests"]
+    G = tr["n_gpus"]
+    nbytes = G * G * 4 + G * (4 * ((M + 31) // 32) + 8) + M * 4     # the matrix written, the fleet read
+    row = {
+        "workload": "transfer plan of a 2048-GPU reconfiguration: 2048 x 2048 cost matrix, 16384 in-flight requests",
+        "pairs": G * G, "requests": Q, "cost_kernel_ms": cost_ms, "moves_ms": moves_ms,
+        "pairs_per_s": G * G / (cost_ms * 1e-3),
+        "roofline": {"kernel": "k_transfer_costs", "bound": "hbm", "achieved": nbytes / (cost_ms * 1e-3) / 1e9,
+                     "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": nbytes / (cost_ms * 1e-3) / HBM_PEAK,
+                     "traffic": None, "algorithmic_bytes": nbytes},
+        "cpu_baseline": None,
+    }
+    if with_cpu:
+        import oracle
+        c, d, r, m = dt.results()
+        t0 = time.perf_counter()
+        oc = oracle.transfer_costs(inp)
+        t1 = time.perf_counter()
+        od, orem, omig = oracle.request_moves(inp)
+        row["cpu_baseline"] = {
+            "value": G * G / (t1 - t0), "unit": "pairs/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole {G} x {G} matrix ({t1 - t0:.3f} s); single-threaded C, float64, gcc -O2",
+            "agreement": {"costs_equal": float(np.mean(oc.astype(np.float32) == c)),
+                          "decisions_equal": float(np.mean(od == d))}}
+    return row
+
+
 def sweep_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
     """The local SM/frequency sweep: kernel time from HIP events around each call (one
     launch per call), its roofline position, and the oracle on the same batches."""
@@ -433,7 +468,8 @@ def main():
         "cpu_baseline": None,
         "next_rows": {"sweep": sweep_row(F, W, hip, torch, not args.no_cpu_baseline),
                       "preferred": preferred_row(F, W, hip, torch, not args.no_cpu_baseline),
-                      "dispatch": dispatch_row(F, W, hip, torch, not args.no_cpu_baseline)},
+                      "dispatch": dispatch_row(F, W, hip, torch, not args.no_cpu_baseline),
+                      "transfer": transfer_row(F, W, hip, torch, not args.no_cpu_baseline)},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(place, fleet, gpu_place, gpu_mig)

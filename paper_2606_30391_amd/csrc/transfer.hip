@@ -6,9 +6,9 @@
 //   dense [G][G] float32 matrix (the input of the minimum-cost assignment).  Bytes = u's
 //   request state plus the weights of u's resident models that v lacks; e_uu = 0; BW is
 //   the intra-node link inside a node, else the inter-node one.  A block owns a stretch of
-//   row u (u's residency and state are wave-uniform); each thread makes four consecutive
-//   entries from the set bits of (u's models & ~v's models) and stores them as one 16-byte
-//   vector, so the kernel is a coalesced stream of stores.
+//   row u (u's residency and state are wave-uniform); each thread makes two groups of four
+//   consecutive entries from the set bits of (u's models & ~v's models) and stores each as
+//   one 16-byte vector, so the kernel is a coalesced stream of stores.
 // k_request_moves   one thread per in-flight request: remaining decode time at the source
 //   against token transfer plus the faster of KV-cache transfer and recompute on the
 //   destination of the plan.
@@ -39,39 +39,89 @@ struct CostArgs {
   float *cost;
 };
 
+// Cost of sending u's state (state_mib, residency word pointer ru) to v.
+__device__ __forceinline__ float pair_cost(const CostArgs &a, int u, int v, long long state, int node_u,
+                                           const uint32_t *ru) {
+  if (v == u) return 0.f;
+  long long mib = state;
+  for (int w = 0; w < a.words; ++w) {
+    unsigned bits = ru[w] & ~a.resident[(size_t)v * a.words + w];     // u's models that v lacks
+    while (bits) {
+      const int m = w * 32 + __builtin_ctz(bits);
+      bits &= bits - 1;
+      if (m < a.M) mib += a.weights[m];
+    }
+  }
+  const double mpb = a.node[v] == node_u ? a.mpb_intra : a.mpb_inter;
+  return (float)((double)(mib * 1048576) * mpb);
+}
+
+// Thread t of a block makes entries v = base + 4t .. 4t+3 and base + 4(t + kCostBlock) ..
+// of row u: kCostVecs 16-byte stores per thread, each coalesced across the block.
+constexpr int kCostVecs = 2;
+
 __global__ void __launch_bounds__(kCostBlock) k_transfer_costs(CostArgs a, int32_t blocks_per_row, int32_t vec) {
   const int u = blockIdx.x / blocks_per_row;
   const int part = blockIdx.x - u * blocks_per_row;
   const long long state = a.state[u];
   const int node_u = a.node[u];
   const uint32_t *ru = a.resident + (size_t)u * a.words;
-  const int v0 = (part * kCostBlock + threadIdx.x) * 4;
-  if (v0 >= a.G) return;
-  float e[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int v = v0 + q;
-    e[q] = 0.f;
-    if (v >= a.G || v == u) continue;
-    long long mib = state;
-    for (int w = 0; w < a.words; ++w) {
-      unsigned bits = ru[w] & ~a.resident[(size_t)v * a.words + w];     // u's models that v lacks
-      while (bits) {
-        const int m = w * 32 + __builtin_ctz(bits);
-        bits &= bits - 1;
-        if (m < a.M) mib += a.weights[m];
-      }
-    }
-    const double mpb = a.node[v] == node_u ? a.mpb_intra : a.mpb_inter;
-    e[q] = (float)((double)(mib * 1048576) * mpb);
-  }
   float *row = a.cost + (size_t)u * a.G;
-  if (vec && v0 + 3 < a.G) {
-    *reinterpret_cast<float4 *>(row + v0) = make_float4(e[0], e[1], e[2], e[3]);
-  } else {
+  const int base = part * kCostBlock * 4 * kCostVecs;
+#pragma unroll
+  for (int c = 0; c < kCostVecs; ++c) {
+    const int v0 = base + (c * kCostBlock + threadIdx.x) * 4;
+    if (v0 >= a.G) break;
+    float e[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) e[q] = v0 + q < a.G ? pair_cost(a, u, v0 + q, state, node_u, ru) : 0.f;
+    if (vec && v0 + 3 < a.G) {
+      *reinterpret_cast<float4 *>(row + v0) = make_float4(e[0], e[1], e[2], e[3]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (v0 + q < a.G) row[v0 + q] = e[q];
+    }
+  }
+}
+
+// Fleets of at most 32 models with rows of whole 16-byte vectors: u's models are walked as
+// a wave-uniform bit loop, and per destination a model costs one bit test, a select and a
+// float64 add (byte counts are whole MiB, exact in float64); e = MiB * (2^20 * ms_per_byte),
+// the same value as bytes * ms_per_byte since scaling by 2^20 is exact.
+__global__ void __launch_bounds__(kCostBlock) k_transfer_costs_w1(CostArgs a, int32_t blocks_per_row) {
+  const int u = blockIdx.x / blocks_per_row;
+  const int part = blockIdx.x - u * blocks_per_row;
+  const double state = (double)a.state[u];
+  const int node_u = a.node[u];
+  const unsigned cu = __builtin_amdgcn_readfirstlane(a.resident[u]);
+  const double mib_intra = a.mpb_intra * 1048576.0, mib_inter = a.mpb_inter * 1048576.0;
+  float *row = a.cost + (size_t)u * a.G;
+  const int base = part * kCostBlock * 4 * kCostVecs;
+#pragma unroll
+  for (int c = 0; c < kCostVecs; ++c) {
+    const int v0 = base + (c * kCostBlock + threadIdx.x) * 4;
+    if (v0 >= a.G) break;
+    const uint4 cv = *reinterpret_cast<const uint4 *>(a.resident + v0);
+    const int4 nv = *reinterpret_cast<const int4 *>(a.node + v0);
+    double acc[4] = {state, state, state, state};
+    for (unsigned bits = cu; bits; bits &= bits - 1) {          // u's models, wave-uniform
+      const int m = __builtin_ctz(bits);
+      if (m >= a.M) break;
+      const double w = (double)a.weights[m];
+      acc[0] += ((cv.x >> m) & 1u) ? 0.0 : w;
+      acc[1] += ((cv.y >> m) & 1u) ? 0.0 : w;
+      acc[2] += ((cv.z >> m) & 1u) ? 0.0 : w;
+      acc[3] += ((cv.w >> m) & 1u) ? 0.0 : w;
+    }
+    const int nvv[4] = {nv.x, nv.y, nv.z, nv.w};
+    float e[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      if (v0 + q < a.G) row[v0 + q] = e[q];
+      e[q] = v0 + q == u ? 0.f : (float)(acc[q] * (nvv[q] == node_u ? mib_intra : mib_inter));
+    // streaming store: the matrix is written once and not read back by this kernel
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(v4f{e[0], e[1], e[2], e[3]}, reinterpret_cast<v4f *>(row + v0));
   }
 }
 
@@ -151,14 +201,19 @@ extern "C" festina_status festina_transfer_costs(const festina_transfer *T, floa
   a.mpb_intra = ms_per_byte(T->bw_intra_gbs);
   a.mpb_inter = ms_per_byte(T->bw_inter_gbs);
   a.cost = cost;
-  const int per_block = kCostBlock * 4;
+  const int per_block = kCostBlock * 4 * kCostVecs;
   const int bpr = (a.G + per_block - 1) / per_block;
   const long long blocks = (long long)a.G * bpr;
   if (blocks > INT_MAX) return FESTINA_ERR_UNSUPPORTED;
   hipStream_t st = static_cast<hipStream_t>(stream);
   // 16-byte row stores when every row starts 16-byte aligned
   const int vec = (a.G % 4 == 0) && ((reinterpret_cast<uintptr_t>(cost) & 15) == 0);
-  k_transfer_costs<<<(unsigned)blocks, kCostBlock, 0, st>>>(a, bpr, vec);
+  const bool aligned_in = ((reinterpret_cast<uintptr_t>(T->resident) & 15) == 0) &&
+                          ((reinterpret_cast<uintptr_t>(T->node) & 15) == 0);
+  if (vec && a.words == 1 && aligned_in)
+    k_transfer_costs_w1<<<(unsigned)blocks, kCostBlock, 0, st>>>(a, bpr);
+  else
+    k_transfer_costs<<<(unsigned)blocks, kCostBlock, 0, st>>>(a, bpr, vec);
   return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
 }
 

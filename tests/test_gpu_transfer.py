@@ -48,7 +48,7 @@ def test_transfer_worked_example():
     assert list(d) == [m["decision"] for m in g["moves"]]
 
 
-@pytest.mark.parametrize("G,M", [(1, 1), (3, 2), (5, 7), (129, 33), (1001, 70), (2050, 32)])
+@pytest.mark.parametrize("G,M", [(1, 1), (3, 2), (4, 1), (5, 7), (129, 33), (1000, 31), (1001, 70), (2050, 32)])
 def test_transfer_shapes(G, M):
     """Row lengths not a multiple of 4 (scalar stores), several residency words, one GPU."""
     rng = np.random.default_rng(2000 + G)
