@@ -6,12 +6,12 @@
 //
 // k_dsp_hosts  one block per model: ascending list of the GPUs hosting it (wavefront
 //                ballots), in the caller's workspace.
-// k_dispatch   one wavefront per request; lanes stride over the model's hosts.  Per host:
+// k_dispatch   16 lanes per request (four per wavefront) stride over the model's hosts.  Per host:
 //                the first free-memory profile step that holds Req_mem gives T_avail and
 //                SM_free; the point (SM_free, F_curr) is feasible when T_avail + TTFT and
 //                TBT meet the SLOs; E = P * (TTFT + Lout * TBT) in float64.  One pass
-//                evaluates every host (a lane's first two hosts stay in registers) and
-//                the wavefront takes E_min; among hosts with E <= E_min + 0.02 |E_min| the largest
+//                evaluates every host (a lane's first four hosts stay in registers) and
+//                the group takes E_min; among hosts with E <= E_min + 0.02 |E_min| the largest
 //                stability key (most memory, most SMs, lowest id packed in 64 bits) wins,
 //                and the lane holding it writes the result.  With no
 //                candidate: the hosts feasible at the top level, earliest T_avail (then
@@ -61,7 +61,7 @@ struct DspArgs {
 
 // Energy on one operating point: P = p0 + k*s*f^3*u, E = P * (ttft + lout*tbt), each
 // operation rounded separately (no fused multiply-add).
-__device__ __noinline__ double point_energy(double p0, double kg, double s, double f, double u, double ttft,
+__device__ __forceinline__ double point_energy(double p0, double kg, double s, double f, double u, double ttft,
                                             double lout, double tbt) {
 #pragma clang fp contract(off)
   const double f3 = f * f * f;
@@ -156,23 +156,29 @@ __device__ __forceinline__ unsigned long long stability_key(int mem, int sm, int
          (unsigned long long)(0xffffffu - (unsigned)g);
 }
 
+constexpr int kGroup = 16;                       // lanes per request
+constexpr int kReqPerWave = kWave / kGroup;
+constexpr int kCached = 4;                       // hosts per lane whose Phase One result stays in registers
+
 __device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int off) {
-  const unsigned lo = __shfl_xor((unsigned)v, off, kWave), hi = __shfl_xor((unsigned)(v >> 32), off, kWave);
+  const unsigned lo = __shfl_xor((unsigned)v, off, kGroup), hi = __shfl_xor((unsigned)(v >> 32), off, kGroup);
   return ((unsigned long long)hi << 32) | lo;
 }
 
-constexpr int kCached = 2;       // hosts per lane whose Phase One result stays in registers
-
+// Four requests per wavefront, 16 lanes each; lane s of a request strides over its
+// model's hosts (s, s + 16, ...), all reductions stay inside the 16-lane group.
 __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) {
-  const int r = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-  if (r >= a.R) return;
+#pragma clang fp contract(off)
   const int lane = threadIdx.x & (kWave - 1);
+  const int sub = lane & (kGroup - 1);
+  const int r = (blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kReqPerWave + (lane >> 4);
+  if (r >= a.R) return;
   const double inf = __builtin_huge_val();
   const int m = a.model[r];
   const int pt = a.prompt[r], pd = a.pred[r];
   int gsel = -1, ksel = -1, jsel = -1, phase = 0;
   double esel = inf;
-  bool writer = lane == 0;
+  bool writer = sub == 0;
   if (m >= 0 && m < a.M && pd >= 0 && pt >= 0) {
     const int prow = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
     const long long lout_i = ((long long)pd * 105 + 99) / 100;
@@ -189,7 +195,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       ec[i] = inf;
       kc[i] = 0ull;
     }
-    for (int i = 0, h = lane; h < nh; ++i, h += kWave) {
+    for (int i = 0, h = sub; h < nh; ++i, h += kGroup) {
       const int g = hl[h];
       const Point p = host_point(a, g, need);
       double e;
@@ -202,7 +208,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
           kc[c] = stability_key(p.mem, p.sm, g);
         }
     }
-    for (int off = 32; off >= 1; off >>= 1) emin = fmin(emin, __shfl_xor(emin, off, kWave));
+    for (int off = kGroup / 2; off >= 1; off >>= 1) emin = fmin(emin, __shfl_xor(emin, off, kGroup));
     if (emin < inf) {
       // Phase Two: the largest stability key among the hosts within 2% of the least energy
       const double bound = emin + kStability * fabs(emin);
@@ -214,7 +220,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
           best = kc[c];
           ebest = ec[c];
         }
-      for (int h = lane + kCached * kWave; h < nh; h += kWave) {   // hosts past the cached ones
+      for (int h = sub + kCached * kGroup; h < nh; h += kGroup) {   // hosts past the cached ones
         const int g = hl[h];
         const Point p = host_point(a, g, need);
         double e;
@@ -226,12 +232,12 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
         }
       }
       unsigned long long wbest = best;
-      for (int off = 32; off >= 1; off >>= 1) {
+      for (int off = kGroup / 2; off >= 1; off >>= 1) {
         const unsigned long long o = shfl_xor_u64(wbest, off);
         wbest = o > wbest ? o : wbest;
       }
       if (wbest != 0ull) {                 // the least-energy host is always within the bound
-        writer = best == wbest;            // exactly one lane holds the winning key
+        writer = best == wbest;            // exactly one lane of the group holds the winning key
         gsel = (int)(0xffffffu - (unsigned)(wbest & 0xffffffull));
         jsel = (int)((wbest >> 24) & 0xffull);
         ksel = a.freq_cur[gsel];
@@ -243,7 +249,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       const int kmax = a.NF - 1;
       int bg = INT_MAX, bsm = -1;
       double bt = inf, be = inf;
-      for (int h = lane; h < nh; h += kWave) {
+      for (int h = sub; h < nh; h += kGroup) {
         const int g = hl[h];
         const Point p = host_point(a, g, need);
         double e;
@@ -255,9 +261,9 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
           be = e;
         }
       }
-      for (int off = 32; off >= 1; off >>= 1) {
-        const int og = __shfl_xor(bg, off, kWave), os = __shfl_xor(bsm, off, kWave);
-        const double ot = __shfl_xor(bt, off, kWave), oe = __shfl_xor(be, off, kWave);
+      for (int off = kGroup / 2; off >= 1; off >>= 1) {
+        const int og = __shfl_xor(bg, off, kGroup), os = __shfl_xor(bsm, off, kGroup);
+        const double ot = __shfl_xor(bt, off, kGroup), oe = __shfl_xor(be, off, kGroup);
         if (ot < bt || (ot == bt && og < bg)) {
           bg = og;
           bt = ot;
@@ -272,19 +278,19 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
         phase = 2;
         esel = be;
       } else {
-        // scale out: a new GPU (batch 1, every SM, available now), lane k scores level k
+        // scale out: a new GPU (batch 1, every SM, available now), lane s scores levels s, s + 16, ...
         int bk = INT_MAX;
         double bke = inf;
-        for (int k = lane; k < a.NF; k += kWave) {
+        for (int k = sub; k < a.NF; k += kGroup) {
           double e;
           if (point_ok(a, r, m, prow, 1, a.NS - 1, k, 0.0, a.k_new, lout, e) && (e < bke || (e == bke && k < bk))) {
             bke = e;
             bk = k;
           }
         }
-        for (int off = 32; off >= 1; off >>= 1) {
-          const int ok = __shfl_xor(bk, off, kWave);
-          const double oe = __shfl_xor(bke, off, kWave);
+        for (int off = kGroup / 2; off >= 1; off >>= 1) {
+          const int ok = __shfl_xor(bk, off, kGroup);
+          const double oe = __shfl_xor(bke, off, kGroup);
           if (oe < bke || (oe == bke && ok < bk)) {
             bke = oe;
             bk = ok;
@@ -381,7 +387,8 @@ extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const 
   hipStream_t st = static_cast<hipStream_t>(stream);
   k_dsp_hosts<<<a.M, kHostBlock, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  const long long blocks = ((long long)a.R + kWavesPerBlock - 1) / kWavesPerBlock;
+  const long long per_block = (long long)kWavesPerBlock * kReqPerWave;
+  const long long blocks = ((long long)a.R + per_block - 1) / per_block;
   k_dispatch<<<(unsigned)blocks, kWavesPerBlock * kWave, 0, st>>>(a);
   return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
 }

@@ -137,7 +137,7 @@ struct MoveArgs {
 };
 
 // ms for `bytes` over the link u -> v, one rounding per operation.
-__device__ __noinline__ double link_ms(long long bytes, double mpb) {
+__device__ __forceinline__ double link_ms(long long bytes, double mpb) {
 #pragma clang fp contract(off)
   return (double)bytes * mpb;
 }
