@@ -5,7 +5,9 @@
 // least-energy level.
 //
 // k_dsp_hosts  one block per model: ascending list of the GPUs hosting it (wavefront
-//                ballots), in the caller's workspace.
+//                ballots), in the caller's workspace; with at most 4 profile steps, also a
+//                64-byte record per (model, host) with everything Phase One reads, so that
+//                the 16 lanes of a request load their hosts with coalesced 16-byte loads.
 // k_dispatch   16 lanes per request (four per wavefront) stride over the model's hosts.  Per host:
 //                the first free-memory profile step that holds Req_mem gives T_avail and
 //                SM_free; the point (SM_free, F_curr) is feasible when T_avail + TTFT and
@@ -57,7 +59,11 @@ struct DspArgs {
   uint8_t *out_phase;
   float *out_energy;
   int32_t *host_cnt, *host_list;     // workspace: [M], [M][G]
+  int4 *hrec;                        // workspace: [M][G][4] host records when S <= 4
+  int32_t packed;
 };
+
+typedef int v4i __attribute__((ext_vector_type(4)));
 
 // Energy on one operating point: P = p0 + k*s*f^3*u, E = P * (ttft + lout*tbt), each
 // operation rounded separately (no fused multiply-add).
@@ -85,7 +91,27 @@ __global__ void __launch_bounds__(kHostBlock) k_dsp_hosts(DspArgs a) {
     __syncthreads();
     int off = base_s;
     for (int i = 0; i < wv; ++i) off += wsum[i];
-    if (has) a.host_list[(size_t)m * a.G + off + before] = g;
+    if (has) {
+      const size_t at = (size_t)m * a.G + off + before;
+      a.host_list[at] = g;
+      if (a.packed) {
+        // one 64-byte record per (model, host): id, batch row + 1 (-1: no candidate),
+        // current level, k; the profile's free memory, times and SM levels
+        const int B = a.batch[g];
+        int4 r0 = make_int4(g, B < 0 ? -1 : (B + 1 > kRows ? kRows : B + 1), a.freq_cur[g], __float_as_int(a.kdyn[g]));
+        int mem[4] = {0, 0, 0, 0}, tt[4] = {0, 0, 0, 0}, sm[4] = {-1, -1, -1, -1};
+        for (int s = 0; s < a.S; ++s) {
+          mem[s] = a.mem_free[(size_t)g * a.S + s];
+          tt[s] = __float_as_int(a.t_avail[(size_t)g * a.S + s]);
+          sm[s] = a.sm_free[(size_t)g * a.S + s];
+        }
+        int4 *rec = a.hrec + at * 4;
+        rec[0] = r0;
+        rec[1] = make_int4(mem[0], mem[1], mem[2], mem[3]);
+        rec[2] = make_int4(tt[0], tt[1], tt[2], tt[3]);
+        rec[3] = make_int4(sm[0], sm[1], sm[2], sm[3]);
+      }
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
       int t = 0;
@@ -134,6 +160,41 @@ __device__ __forceinline__ Point host_point(const DspArgs &a, int g, long long n
       return p;
     }
   return p;
+}
+
+struct Host {
+  int g, kcur;
+  double kd;
+  Point p;
+};
+
+// Phase One inputs of host number h of model m: from the packed record, or gathered.
+__device__ __forceinline__ Host load_host(const DspArgs &a, int m, int h, const int *hl, long long need) {
+  Host o;
+  if (a.packed) {
+    const v4i *rec = reinterpret_cast<const v4i *>(a.hrec + ((size_t)m * a.G + h) * 4);
+    const v4i r0 = rec[0], mem = rec[1], tt = rec[2], sm = rec[3];
+    o.g = r0.x;
+    o.kcur = r0.z;
+    o.kd = (double)__int_as_float(r0.w);
+    o.p = Point{0, 0.0, -1, 0, r0.y};
+    if (r0.y < 0) return o;
+    int st = -1;
+#pragma unroll
+    for (int s = 3; s >= 0; --s)
+      if (s < a.S && (long long)mem[s] * 1024 >= need) st = s;
+    if (st < 0) return o;
+    o.p.ok = 1;
+    o.p.ta = (double)__int_as_float(st == 0 ? tt.x : st == 1 ? tt.y : st == 2 ? tt.z : tt.w);
+    o.p.sm = st == 0 ? sm.x : st == 1 ? sm.y : st == 2 ? sm.z : sm.w;
+    o.p.mem = st == 0 ? mem.x : st == 1 ? mem.y : st == 2 ? mem.z : mem.w;
+    return o;
+  }
+  o.g = hl[h];
+  o.kcur = a.freq_cur[o.g];
+  o.kd = (double)a.kdyn[o.g];
+  o.p = host_point(a, o.g, need);
+  return o;
 }
 
 // Does request r meet its SLOs on (j, k) starting at ta with batch b?  Energy if so.
@@ -196,10 +257,11 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       kc[i] = 0ull;
     }
     for (int i = 0, h = sub; h < nh; ++i, h += kGroup) {
-      const int g = hl[h];
-      const Point p = host_point(a, g, need);
+      const Host H = load_host(a, m, h, hl, need);
+      const int g = H.g;
+      const Point &p = H.p;
       double e;
-      if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, a.freq_cur[g], p.ta, (double)a.kdyn[g], lout, e))) continue;
+      if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, H.kcur, p.ta, H.kd, lout, e))) continue;
       emin = fmin(emin, e);
 #pragma unroll
       for (int c = 0; c < kCached; ++c)
@@ -221,10 +283,11 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
           ebest = ec[c];
         }
       for (int h = sub + kCached * kGroup; h < nh; h += kGroup) {   // hosts past the cached ones
-        const int g = hl[h];
-        const Point p = host_point(a, g, need);
+        const Host H = load_host(a, m, h, hl, need);
+        const int g = H.g;
+        const Point &p = H.p;
         double e;
-        if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, a.freq_cur[g], p.ta, (double)a.kdyn[g], lout, e))) continue;
+        if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, H.kcur, p.ta, H.kd, lout, e))) continue;
         const unsigned long long key = stability_key(p.mem, p.sm, g);
         if (e <= bound && key > best) {
           best = key;
@@ -240,7 +303,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
         writer = best == wbest;            // exactly one lane of the group holds the winning key
         gsel = (int)(0xffffffu - (unsigned)(wbest & 0xffffffull));
         jsel = (int)((wbest >> 24) & 0xffull);
-        ksel = a.freq_cur[gsel];
+        ksel = a.freq_cur[gsel];        // the winner's current level
         phase = 1;
         esel = ebest;
       }
@@ -250,10 +313,11 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       int bg = INT_MAX, bsm = -1;
       double bt = inf, be = inf;
       for (int h = sub; h < nh; h += kGroup) {
-        const int g = hl[h];
-        const Point p = host_point(a, g, need);
+        const Host H = load_host(a, m, h, hl, need);
+        const int g = H.g;
+        const Point &p = H.p;
         double e;
-        if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, kmax, p.ta, (double)a.kdyn[g], lout, e))) continue;
+        if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, kmax, p.ta, H.kd, lout, e))) continue;
         if (p.ta < bt || (p.ta == bt && g < bg)) {
           bg = g;
           bt = p.ta;
@@ -329,7 +393,9 @@ bool dsp_shapes_ok(const festina_lut *L, const festina_gpu_avail *A) {
 
 extern "C" size_t festina_dispatch_workspace_bytes(const festina_lut *L, const festina_gpu_avail *A) {
   if (!dsp_shapes_ok(L, A)) return 0;
-  return align256(sizeof(int32_t) * L->n_models) + align256(sizeof(int32_t) * (size_t)L->n_models * A->n_gpus);
+  size_t bytes = align256(sizeof(int32_t) * L->n_models) + align256(sizeof(int32_t) * (size_t)L->n_models * A->n_gpus);
+  if (A->n_steps <= 4) bytes += align256((size_t)64 * L->n_models * A->n_gpus);     // host records
+  return bytes;
 }
 
 extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const festina_gpu_avail *A,
@@ -384,6 +450,9 @@ extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const 
   char *ws = static_cast<char *>(workspace);
   a.host_cnt = reinterpret_cast<int32_t *>(ws);
   a.host_list = reinterpret_cast<int32_t *>(ws + align256(sizeof(int32_t) * L->n_models));
+  a.packed = A->n_steps <= 4 ? 1 : 0;
+  a.hrec = reinterpret_cast<int4 *>(ws + align256(sizeof(int32_t) * L->n_models) +
+                                    align256(sizeof(int32_t) * (size_t)L->n_models * A->n_gpus));
   hipStream_t st = static_cast<hipStream_t>(stream);
   k_dsp_hosts<<<a.M, kHostBlock, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
