@@ -60,6 +60,8 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_score_config4_traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "festina.hip")
 SWEEP_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sweep_traffic.json")
 SWEEP_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "sweep.hip")
+TRANSFER_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_transfer_costs_traffic.json")
+TRANSFER_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "transfer.hip")
 # Sweep, per (task, SM level, frequency level) cell: one compare of the latency with the
 # slack; per (task, frequency level): the SM share add and two FMAs (power, energy).
 OPS_PER_SWEEP_CELL = 1
@@ -270,7 +272,7 @@ def transfer_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
         "pairs_per_s": G * G / (cost_ms * 1e-3),
         "roofline": {"kernel": "k_transfer_costs", "bound": "hbm", "achieved": nbytes / (cost_ms * 1e-3) / 1e9,
                      "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": nbytes / (cost_ms * 1e-3) / HBM_PEAK,
-                     "traffic": None, "algorithmic_bytes": nbytes},
+                     "traffic": load_traffic(TRANSFER_TRAFFIC_FILE, TRANSFER_SRC), "algorithmic_bytes": nbytes},
         "cpu_baseline": None,
     }
     if with_cpu:
