@@ -823,6 +823,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   __shared__ int s_cls[kClasses + 1];     // class counts, then class starts
   __shared__ int s_clist[kClasses + 1];   // non-empty classes: cls | start << 6 | end << 15; [64] = count
   __shared__ float4 s_par[WPB][kQF];      // pass 2: per request {cell, E*, Lout, TBT SLO}
+  __shared__ short s_pos[kHcap];          // slot of host i's record after the class sort
   char *L = reinterpret_cast<char *>(lds);
   constexpr uint32_t recB = fast_rec_off(WPB);
   constexpr uint32_t dcsB = fast_dcs_off(WPB);
@@ -986,7 +987,11 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < kPer; ++u)
-      if (key[u] >= 0) *reinterpret_cast<v4u *>(L + recB + (s_cls[key[u]] + rank[u]) * 16) = rec[u];
+      if (key[u] >= 0) {
+        const int pos = s_cls[key[u]] + rank[u];
+        *reinterpret_cast<v4u *>(L + recB + pos * 16) = rec[u];
+        s_pos[u * T + threadIdx.x] = (short)pos;
+      }
     __syncthreads();
     if (live_any) {
       const int ncls = uniform(s_clist[kClasses]);
@@ -1065,17 +1070,28 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     const float4 par = s_par[wv][myq];
     const int cell = __float_as_int(par.x);
     int gmin = INT_MAX;                   // lowest GPU id reaching E* (per lane)
+    // requests with a cell this round, as an 8-bit mask (lane q of each group of kQF lanes)
+    const unsigned need = (unsigned)(__ballot(cell >= 0) & ((1ull << kQF) - 1ull));
     if (cell >= 0) {
       const uint32_t cj64 = (uint32_t)(cell >> 4) * 64u, ck4 = (uint32_t)(cell & 15) * 4u;
       const uint32_t ttB = wblkB + (1 + myq) * kC * 4;
+      // hosts ascend by GPU id, so once every request of the round has found E* no later
+      // host can lower its index: stop there
       for (int b0 = 0; b0 < hcnt * kQF; b0 += kWave) {
+        if (b0 > 0) {
+          unsigned long long f = __ballot(gmin != INT_MAX);
+          f |= f >> 32;
+          f |= f >> 16;
+          f |= f >> 8;
+          if ((((unsigned)f & 0xffu) & need) == need) break;
+        }
         const int i = (b0 + lane) / kQF;
         if (i < hcnt) {
           uint32_t rowB;
           int g, caps;
           float kap;
-          if (recs_in_lds) {
-            const v4u r = *reinterpret_cast<const v4u *>(L + recB + i * 16);
+          if (recs_in_lds) {           // host i (ascending GPU id) sits at slot s_pos[i]
+            const v4u r = *reinterpret_cast<const v4u *>(L + recB + (int)s_pos[i] * 16);
             rowB = r.x;
             kap = __uint_as_float(r.y);
             g = (int)r.z;
