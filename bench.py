@@ -47,11 +47,13 @@ SCLK_HZ = 2.4e9
 VALU_PEAK = N_CU * LANES_PER_CU_CLOCK * SCLK_HZ            # 39.32e12 lane-ops/s
 HBM_PEAK = 8.0e12                                           # B/s
 
-# Least VALU work per candidate of any exhaustive search: the energy mixes
-# two request terms (Lout, TTFT) with two GPU terms (Pp, Pd*TBT) -- one multiply and one
-# fused multiply-add -- and the argmin needs one min.  SLO masks, power terms and the
-# index of the winner are shared or recovered once per request, so they are not counted.
-OPS_PER_CANDIDATE = 3
+# Least VALU work per candidate of any exhaustive search: divided by the
+# request's Lout, a candidate's energy is Pp * (TTFT / Lout) + Pd * TBT, one fused
+# multiply-add of a request term and two GPU terms, and a three-way min folds two
+# candidates into the running minimum, half an instruction each.  SLO masks, power terms,
+# the per-request scale and the index of the winner are shared or recovered once per
+# request or GPU, so they are not counted.
+OPS_PER_CANDIDATE = 1.5
 # Migration pair: two budget compares, level-mask AND and test, self test, lowest set bit,
 # u_s + u_d, two multiplies, subtract, FMA, compare with the best, three selects.
 OPS_PER_PAIR = 15

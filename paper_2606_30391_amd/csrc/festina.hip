@@ -55,7 +55,8 @@ struct ReqRec {                  // one request in bucket order, 32 bytes
   int32_t row;                   // prompt row (-1: the decode batch row)
   float lout;                    // padded output tokens
   float slo_ttft, slo_tbt;
-  int32_t pad[3];
+  float rlout;                   // 1 / lout when lout is in [1, 2^40], else 0
+  int32_t pad[2];
 };
 
 struct PlaceArgs {
@@ -129,7 +130,8 @@ __device__ __forceinline__ ReqRec load_req(const PlaceArgs &a, int pos) {
   q.lout = __int_as_float(x.z);
   q.slo_ttft = __int_as_float(x.w);
   q.slo_tbt = __int_as_float(y.x);
-  q.pad[0] = q.pad[1] = q.pad[2] = 0;
+  q.rlout = __int_as_float(y.y);
+  q.pad[0] = q.pad[1] = 0;
   return q;
 }
 
@@ -321,7 +323,8 @@ __global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
 
 // Record of valid request r: prompt bucket min(ceil(tokens / 256), 32) - 1 (unsigned: no
 // overflow for any int32 token count; 0 tokens -> -1, the decode batch row), the 5% output
-// pad ceil(1.05 * pred) = (105 * pred + 99) / 100 in 64-bit, and the SLOs.
+// pad ceil(1.05 * pred) = (105 * pred + 99) / 100 in 64-bit, its reciprocal (0 outside
+// [1, 2^40]), and the SLOs.
 __device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
   const int pt = a.prompt[r];
   ReqRec q;
@@ -330,7 +333,8 @@ __device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
   q.lout = (float)(((long long)a.pred[r] * 105 + 99) / 100);
   q.slo_ttft = a.slo_ttft[r];
   q.slo_tbt = a.slo_tbt[r];
-  q.pad[0] = q.pad[1] = q.pad[2] = 0;
+  q.rlout = q.lout >= 1.f && q.lout <= 0x1p40f ? 1.f / q.lout : 0.f;
+  q.pad[0] = q.pad[1] = 0;
   return q;
 }
 
@@ -690,17 +694,21 @@ __global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
 //
 // A workgroup takes a tile of WPB * kQF requests of one (wave, model) bucket; each
 // wavefront scores its kQF requests together against every hosting GPU.
-//   pass 1: per (request, cell) the minimum energy over the GPUs.  The tile's GPU records
-//           are staged in LDS grouped by SM-cap class (cap_pf, cap_dc); per class the
-//           capped prompt-row values of the kQF requests and the power factors s*f^3 sit
-//           in registers, so each GPU costs one record and one TBT read.  Per candidate:
-//           one multiply, one FMA, and half a v_min3 (GPUs taken in pairs).  Cells above
-//           max(cap_pf, cap_dc) repeat that level's cell exactly (same latencies, same
-//           power) at a higher index, so they get NaN power and never compete.
-//   pass 2: E* = the wavefront minimum; for each cell whose minimum equals E*, the lowest
-//           GPU id whose energy -- recomputed with the same operations, hence bit-identical
-//           -- equals E*; the smallest index (g * 128 + cell) wins.  That is the
-//           (energy, index) lexicographic minimum.
+//   pass 1: per (request, cell) the minimum key over the GPUs, where a candidate's key is
+//           its energy divided by the request's Lout, Pp * (TT / Lout) + Pd * TBT (Eq.
+//           energy, Sec. 3.3).  The tile's GPU records are staged in LDS grouped by SM-cap
+//           class (cap_pf, cap_dc); the prompt rows are staged already divided by Lout,
+//           and per class the capped row values of the kQF requests and the power factors
+//           s*f^3 sit in registers, so each GPU costs one record and one TBT read.  Per candidate: one FMA and half a v_min3 (GPUs taken in pairs).
+//           Cells above max(cap_pf, cap_dc) repeat that level's cell exactly (same
+//           latencies, same power) at a higher index, so they get NaN power and never
+//           compete.  A wavefront with a request whose Lout is below 1 (or a prompt
+//           latency far outside the float range that division keeps normal) keeps TT and
+//           evaluates the energy itself: one multiply and one FMA per candidate.
+//   pass 2: K* = the wavefront minimum; for each cell whose minimum equals K*, the lowest
+//           GPU id whose key -- recomputed with the same operations, hence bit-identical
+//           -- equals K*; the smallest index (g * 128 + cell) wins.  That is the
+//           (key, index) lexicographic minimum, and the energy is Lout * K*.
 // Masked (SLO-missing) latencies are NaN, which min ignores and == never matches.
 constexpr int kQF = 8;
 constexpr int kC = 128;
@@ -752,6 +760,25 @@ __device__ __forceinline__ float cell_energy(float kap, float pdp, float pdd, fl
   return fmaf(lo, Ym, Pp * tt);
 }
 
+// The same candidate's energy divided by Lout (Lout >= 1): the key Pp * (TT / Lout) + Pd * TBT,
+// one FMA once TT / Lout is staged.  Lout is one positive scale per request, so the
+// request's keys are ordered as its energies (up to rounding), and its energy is Lout times
+// its least key.  Pass 1 and pass 2 both evaluate exactly these operations.
+__device__ __forceinline__ float cell_key(float kap, float pdp, float pdd, float tbt, float ttl, float p0,
+                                         float slo_tbt) {
+  const float Pp = fmaf(kap, pdp, p0);
+  const float Pd = fmaf(kap, pdd, p0);
+  const float Ym = tbt < slo_tbt ? Pd * tbt : kMask;
+  return fmaf(Pp, ttl, Ym);
+}
+
+// A prompt latency x scaled to s = x / Lout keeps its precision: s is NaN, infinite or
+// normal, or zero because x is.  (Class mask: signaling and quiet NaN, +-infinity,
+// +-normal.)
+__device__ __forceinline__ bool scaled_ok(float s, float x) {
+  return __builtin_amdgcn_classf(s, 0x30f) | (x == 0.f);
+}
+
 // TBT-SLO handling of pass 1:
 //   kPremasked  every live request of the tile has the same TBT SLO and the staged decode
 //               table already holds NaN where TBT misses it;
@@ -781,8 +808,10 @@ __device__ __forceinline__ void host_terms(const char *L, v4u r, const ClassRegs
   }
 }
 
-// Pass 1 over the records [cs, ce) of one class.
-template <int MODE>
+// Pass 1 over the records [cs, ce) of one class.  NORM: the staged prompt rows hold TT / Lout
+// and a candidate costs one FMA (its key); otherwise they hold TT and the candidate is its
+// energy.
+template <int MODE, bool NORM>
 __device__ __forceinline__ void class_pass1(const char *L, uint32_t recB, int cs, int ce, const ClassRegs &cr,
                                             float p0, const float (&lo)[kQF], const float (&sb)[kQF],
                                             float sb0, float (&mn)[kQF][2]) {
@@ -799,7 +828,10 @@ __device__ __forceinline__ void class_pass1(const char *L, uint32_t recB, int cs
       for (int c = 0; c < 2; ++c) {
         const float y0 = MODE == kMixed ? (T0[c] < sb[q] ? Y0[c] : kMask) : Y0[c];
         const float y1 = MODE == kMixed ? (T1[c] < sb[q] ? Y1[c] : kMask) : Y1[c];
-        mn[q][c] = vmin3(mn[q][c], fmaf(lo[q], y0, Pp0[c] * cr.tt[q][c]), fmaf(lo[q], y1, Pp1[c] * cr.tt[q][c]));
+        if (NORM)
+          mn[q][c] = vmin3(mn[q][c], fmaf(Pp0[c], cr.tt[q][c], y0), fmaf(Pp1[c], cr.tt[q][c], y1));
+        else
+          mn[q][c] = vmin3(mn[q][c], fmaf(lo[q], y0, Pp0[c] * cr.tt[q][c]), fmaf(lo[q], y1, Pp1[c] * cr.tt[q][c]));
       }
   }
   if (i < ce) {
@@ -811,9 +843,51 @@ __device__ __forceinline__ void class_pass1(const char *L, uint32_t recB, int cs
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const float y0 = MODE == kMixed ? (T0[c] < sb[q] ? Y0[c] : kMask) : Y0[c];
-        mn[q][c] = vmin(mn[q][c], fmaf(lo[q], y0, Pp0[c] * cr.tt[q][c]));
+        mn[q][c] = vmin(mn[q][c], NORM ? fmaf(Pp0[c], cr.tt[q][c], y0) : fmaf(lo[q], y0, Pp0[c] * cr.tt[q][c]));
       }
   }
+}
+
+// DPP lane moves within rows of 16 lanes (every source lane exists).
+constexpr int kDppRor8 = 0x128;        // row_ror:8: lane i reads lane i ^ 8 of its row
+constexpr int kDppHalfMirror = 0x141;  // lane i reads lane 7 - i of its group of 8
+constexpr int kDppQuad2301 = 0x4E;     // lane i reads lane i ^ 2 of its quad
+constexpr int kDppQuad1032 = 0xB1;     // lane i reads lane i ^ 1 of its quad
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+
+// est[q] = min over the wavefront's lanes of min(m[q][0], m[q][1]), for the kQF = 8
+// requests at once, as a transposing reduction: each exchange halves the values a lane
+// holds (xor 32 and xor 16 by permlane swaps, xor 8 by DPP) until lane l holds request
+// l / 8's partial minimum, then three DPP steps reduce each group of 8 lanes.
+__device__ __forceinline__ void wave_min8(const float (&m)[kQF][2], float (&est)[kQF]) {
+  static_assert(kQF == 8, "the exchange pattern is written for 8 requests per wavefront");
+  float v[8], u[4], w[2];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) v[q] = vmin(m[q][0], m[q][1]);
+  // lanes 0-31 keep requests 0-3, lanes 32-63 requests 4-7
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[p]), __float_as_uint(v[p + 4]), false, false);
+    u[p] = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  }
+  // even rows of 16 lanes keep the first two of their half's four, odd rows the last two
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(u[p]), __float_as_uint(u[p + 2]), false, false);
+    w[p] = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  }
+  // lanes with bit 3 clear keep the first of the two, the others the second
+  const bool hi = (__lane_id() & 8) != 0;
+  float c = vmin(hi ? w[1] : w[0], dpp<kDppRor8>(hi ? w[0] : w[1]));
+  c = vmin(c, dpp<kDppHalfMirror>(c));
+  c = vmin(c, dpp<kDppQuad2301>(c));
+  c = vmin(c, dpp<kDppQuad1032>(c));
+#pragma unroll
+  for (int q = 0; q < 8; ++q) est[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(c), 8 * q));
 }
 
 template <int WPB>
@@ -869,27 +943,42 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   float lo[kQF], sb[kQF];
   bool live_any = false, wsame = true;
   float sb0 = 0.f;
+  // All request records, then all prompt-row loads, in flight before the first use.  A
+  // missing request reads the tile's first record and row 0, and is masked below.
+  ReqRec rr[kQF];
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) rr[q] = load_req(a, q < nq ? q0 + q : beg);
+  float raw[kQF][2];
 #pragma unroll
   for (int q = 0; q < kQF; ++q) {
-    const ReqRec rr = load_req(a, q < nq ? q0 + q : beg);
-    rq[q] = q < nq ? rr.r : -1;
-    float st = -kInf;
-    int prw = 0;
-    lo[q] = 0.f;
-    sb[q] = -kInf;
-    if (rq[q] >= 0) {
-      lo[q] = rr.lout;
-      st = rr.slo_ttft;
-      sb[q] = rr.slo_tbt;
-      prw = rr.row;
-    }
-    const float *pr = a.pf + ((size_t)m * kRows + prw) * kC + 2 * lane;
-    v2f v;
-    v.x = rq[q] >= 0 ? pr[0] : kMask;
-    v.y = rq[q] >= 0 ? pr[1] : kMask;
-    v.x = v.x < st ? v.x : kMask;
-    v.y = v.y < st ? v.y : kMask;
-    *reinterpret_cast<v2f *>(L + wblkB + (1 + q) * kC * 4 + j64 + k04) = v;
+    rq[q] = q < nq ? rr[q].r : -1;
+    const float *pr = a.pf + ((size_t)m * kRows + (rq[q] >= 0 ? rr[q].row : 0)) * kC + 2 * lane;
+    raw[q][0] = pr[0];
+    raw[q][1] = pr[1];
+  }
+  // Prompt rows: NaN where TTFT misses the SLO, scaled by 1 / Lout when every request of the
+  // wavefront has a usable reciprocal and every scaled value stays normal (or NaN), or is
+  // zero because the latency is.
+  v2f pv[kQF], ps[kQF];
+  bool nrm = true;
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) {
+    const bool has = rq[q] >= 0;
+    lo[q] = has ? rr[q].lout : 0.f;
+    sb[q] = has ? rr[q].slo_tbt : -kInf;
+    const float st = has ? rr[q].slo_ttft : -kInf;
+    const float rl = has ? rr[q].rlout : 1.f;
+    pv[q].x = raw[q][0] < st ? raw[q][0] : kMask;
+    pv[q].y = raw[q][1] < st ? raw[q][1] : kMask;
+    ps[q].x = pv[q].x * rl;
+    ps[q].y = pv[q].y * rl;
+    nrm = nrm & (rl > 0.f) & scaled_ok(ps[q].x, pv[q].x) & scaled_ok(ps[q].y, pv[q].y);
+  }
+  nrm = __ballot(!nrm) == 0ull;
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) {
+    const v2f v = pv[q];
+    *reinterpret_cast<v2f *>(L + wblkB + (1 + q) * kC * 4 + j64 + k04) = nrm ? ps[q] : v;
     const bool live = __ballot(v.x == v.x || v.y == v.y) != 0ull;
     if (live) {
       if (!live_any) sb0 = sb[q];
@@ -1007,17 +1096,27 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
         if (j64 > max(cpB, cdB)) cr.pdp = v2f{kMask, kMask};   // repeated cells drop out
 #pragma unroll
         for (int q = 0; q < kQF; ++q) cr.tt[q] = lds2(L, aP + (1 + q) * kC * 4);
-        if (tile_same)
-          class_pass1<kPremasked>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-        else if (wsame)
-          class_pass1<kWaveSame>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-        else
-          class_pass1<kMixed>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+        if (nrm) {
+          if (tile_same)
+            class_pass1<kPremasked, true>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+          else if (wsame)
+            class_pass1<kWaveSame, true>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+          else
+            class_pass1<kMixed, true>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+        } else {
+          if (tile_same)
+            class_pass1<kPremasked, false>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+          else if (wsame)
+            class_pass1<kWaveSame, false>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+          else
+            class_pass1<kMixed, false>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+        }
       }
     }
   }
 
-  // pass 2: per request the winning energy E*, then the lowest index that reaches it.
+  // pass 2: per request the winning energy E* (key K*: E* = Lout * K*), then the lowest index
+  // that reaches it.
   // Requests are searched together: lane = (host i, request q) with q = lane % kQF, so a
   // chunk covers 64 / kQF hosts of every request; one round per tied cell of a request
   // (one round unless two different cells reach exactly E*).
@@ -1025,13 +1124,10 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   float est[kQF];
   unsigned long long t0[kQF], t1[kQF];
   bool rounds = false;
+  wave_min8(mn, est);
 #pragma unroll
   for (int q = 0; q < kQF; ++q) {
-    float e = vmin(mn[q][0], mn[q][1]);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) e = vmin(e, __shfl_xor(e, off, kWave));
-    est[q] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(e)));
-    const bool feas = q < nq && est[q] < kInf;
+    const bool feas = q < nq && (nrm ? lo[q] * est[q] : est[q]) < kInf;
     t0[q] = __ballot(feas && mn[q][0] == est[q]);
     t1[q] = __ballot(feas && mn[q][1] == est[q]);
     rounds = rounds || (t0[q] | t1[q]) != 0ull;
@@ -1107,8 +1203,9 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
           const uint32_t mP = min(cj64, cpB) + ck4;
           const uint32_t mD = min(cj64, cdB) + ck4;
           const float pdp = cj64 > max(cpB, cdB) ? kMask : lds1(L, wblkB + mP);
-          const float E = cell_energy(kap, pdp, lds1(L, wblkB + mD), lds1(L, rowB + mD), lds1(L, ttB + mP),
-                                      p0, par.z, par.w);
+          const float pdd = lds1(L, wblkB + mD), tbt = lds1(L, rowB + mD), tt = lds1(L, ttB + mP);
+          const float E = nrm ? cell_key(kap, pdp, pdd, tbt, tt, p0, par.w)
+                              : cell_energy(kap, pdp, pdd, tbt, tt, p0, par.z, par.w);
           if (E == par.y) gmin = min(gmin, g);
         }
       }
@@ -1121,9 +1218,9 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   if (lane < nq) {
-    float e = est[0];
+    float e = nrm ? lo[0] * est[0] : est[0];
 #pragma unroll
-    for (int q = 1; q < kQF; ++q) e = lane == q ? est[q] : e;
+    for (int q = 1; q < kQF; ++q) e = lane == q ? (nrm ? lo[q] * est[q] : est[q]) : e;
     int r = rq[0];
 #pragma unroll
     for (int q = 1; q < kQF; ++q) r = lane == q ? rq[q] : r;
