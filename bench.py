@@ -52,7 +52,8 @@ HBM_PEAK = 8.0e12                                           # B/s
 # multiply-add of a request term and two GPU terms, and a three-way min folds two
 # candidates into the running minimum, half an instruction each.  SLO masks, power terms,
 # the per-request scale and the index of the winner are shared or recovered once per
-# request or GPU, so they are not counted.
+# request or GPU, so they are not counted.  The count runs over distinct candidates: the
+# cells of a capped GPU above max(cap_pf, cap_dc) repeat lower cells and need no work.
 OPS_PER_CANDIDATE = 1.5
 # Migration pair: two budget compares, level-mask AND and test, self test, lowest set bit,
 # u_s + u_d, two multiplies, subtract, FMA, compare with the best, three selects.
@@ -117,6 +118,26 @@ def placement_candidates(inp, sel=None):
     model = rq["model"] if sel is None else rq["model"][sel]
     ok = (model >= 0) & (model < M)
     return int(hosts[model[ok]].sum()) * lut["n_sm"] * lut["n_freq"]
+
+
+def distinct_candidates(inp):
+    """Candidates that are not repeats: a capped GPU's SM levels above max(cap_pf, cap_dc)
+    repeat that level's cells exactly at a higher index (never the lowest-index minimum), so
+    only levels 0..max(cap_pf, cap_dc) of each hosting GPU count."""
+    lut, gp, rq = inp["lut"], inp["gpus"], inp["requests"]
+    M, NS, NF = lut["n_models"], lut["n_sm"], lut["n_freq"]
+    G = gp["n_gpus"]
+    res = np.asarray(gp["resident"], np.uint32)
+    if gp.get("cap_pf") is not None or gp.get("cap_dc") is not None:
+        cp = np.full(G, NS - 1) if gp.get("cap_pf") is None else np.asarray(gp["cap_pf"], np.int64)
+        cd = np.full(G, NS - 1) if gp.get("cap_dc") is None else np.asarray(gp["cap_dc"], np.int64)
+        levels = np.minimum(np.maximum(cp, cd), NS - 1) + 1
+    else:
+        levels = np.full(G, NS)
+    per_model = np.array([int(levels[((res[:, m // 32] >> np.uint32(m % 32)) & 1) == 1].sum()) for m in range(M)])
+    model = rq["model"]
+    ok = (model >= 0) & (model < M)
+    return int(per_model[model[ok]].sum()) * NF
 
 
 def placement_bytes(inp):
@@ -392,6 +413,7 @@ def main():
     torch.cuda.synchronize()
 
     n_cand = placement_candidates(place)
+    n_distinct = distinct_candidates(place)
     G = fleet["fleet"]["n_gpus"]
     n_pairs = G * (G - 1)
 
@@ -430,7 +452,7 @@ def main():
 
     step_s = (t1 - t0) / K
     value = (n_cand + n_pairs) / step_s
-    achieved = n_cand * OPS_PER_CANDIDATE / (score_ms * 1e-3)
+    achieved = n_distinct * OPS_PER_CANDIDATE / (score_ms * 1e-3)
     gpu_place = dp.results()
     gpu_mig = dm.results()
 
@@ -452,6 +474,7 @@ def main():
                          "8 SM x 16 freq levels, capped prefill/decode SM splits) + consolidation scoring "
                          "(2048 GPUs, 4192256 ordered pairs)"),
             "placement_candidates": n_cand,
+            "distinct_placement_candidates": n_distinct,
             "migration_pairs": n_pairs,
             "parallelism": "single GPU",
         },
@@ -464,6 +487,7 @@ def main():
             "frac": achieved / VALU_PEAK,
             "traffic": load_traffic(),
             "ops_per_candidate": OPS_PER_CANDIDATE,
+            "candidates_counted": "distinct (capped GPUs' repeated SM levels excluded)",
             "kernel_ms": score_ms,
             "hbm_frac_algorithmic": placement_bytes(place) / (score_ms * 1e-3) / HBM_PEAK,
         },
@@ -495,7 +519,7 @@ def per_config(F, W, hip, torch):
             inp = W.make_placement(cfg)
             dev = F.DevicePlacement(inp, "cuda")
             work = placement_candidates(inp)
-            ops = work * OPS_PER_CANDIDATE
+            ops = distinct_candidates(inp) * OPS_PER_CANDIDATE
             idx = (0, 1)
         else:
             inp = W.make_fleet()

@@ -848,6 +848,138 @@ __device__ __forceinline__ void class_pass1(const char *L, uint32_t recB, int cs
   }
 }
 
+// SM-cap classes are numbered so that ascending number means ascending
+// m = max(cap_pf, cap_dc): the 2m + 1 classes of m take the numbers m^2 .. (m + 1)^2 - 1.
+__device__ __forceinline__ int class_id(int p, int d) {
+  const int m = max(p, d);
+  return m * m + (p == m ? d : m + 1 + p);
+}
+// The inverse, as cap_pf * 8 + cap_dc.
+__device__ __forceinline__ int class_caps(int t) {
+  int m = 0;
+#pragma unroll
+  for (int k = 1; k < kNS8; ++k) m += t >= k * k;
+  const int r = t - m * m;
+  return r <= m ? m * kNS8 + r : (r - m - 1) * kNS8 + m;
+}
+
+// Per-class registers for the SM level at byte offset je64 of this lane; a level above
+// max(cap_pf, cap_dc) only repeats the class's top level, so its power is NaN.
+__device__ __forceinline__ ClassRegs class_regs(const char *L, uint32_t wblkB, uint32_t je64, uint32_t k04,
+                                                uint32_t cpB, uint32_t cdB) {
+  ClassRegs cr;
+  const uint32_t aP = wblkB + min(je64, cpB) + k04;
+  cr.mD = min(je64, cdB) + k04;
+  cr.pdp = lds2(L, aP);
+  cr.pdd = lds2(L, wblkB + cr.mD);
+  if (je64 > max(cpB, cdB)) cr.pdp = v2f{kMask, kMask};
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) cr.tt[q] = lds2(L, aP + (1 + q) * kC * 4);
+  return cr;
+}
+
+// Pass 1 over one class in the common mode (premasked TBT, keys), H GPUs per step: H = 1
+// is the plain layout; H = 2 or 4 packs a class whose SM levels above m = max(cap_pf,
+// cap_dc) only repeat level m, with 8 / H levels per GPU (a power of two >= m + 1), so
+// lane l works on GPU (step start + slot), slot = (l / 8) / (8 / H), at SM level
+// (l / 8) % (8 / H).  The partial minima of one cell then sit in the lanes that share its
+// level until fold_levels gathers them.  A lane past the class's last GPU reads that GPU's
+// record with NaN power.
+__device__ __forceinline__ void class_pass1_common(const char *L, uint32_t recB, int cs, int ce,
+                                                   const ClassRegs &cr, float p0, int slot, int H,
+                                                   float (&mn)[kQF][2]) {
+  int i = cs;
+  for (; i + H < ce; i += 2 * H) {
+    const int h1 = i + H + slot;
+    const v4u r0 = *reinterpret_cast<const v4u *>(L + recB + (i + slot) * 16);
+    v4u r1 = *reinterpret_cast<const v4u *>(L + recB + min(h1, ce - 1) * 16);
+    r1.y = h1 < ce ? r1.y : __float_as_uint(kMask);
+    float Pp0[2], Y0[2], T0[2], Pp1[2], Y1[2], T1[2];
+    host_terms<kPremasked>(L, r0, cr, p0, 0.f, Pp0, Y0, T0);
+    host_terms<kPremasked>(L, r1, cr, p0, 0.f, Pp1, Y1, T1);
+#pragma unroll
+    for (int q = 0; q < kQF; ++q)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        mn[q][c] = vmin3(mn[q][c], fmaf(Pp0[c], cr.tt[q][c], Y0[c]), fmaf(Pp1[c], cr.tt[q][c], Y1[c]));
+  }
+  if (i < ce) {
+    const int h0 = i + slot;
+    v4u r0 = *reinterpret_cast<const v4u *>(L + recB + min(h0, ce - 1) * 16);
+    r0.y = h0 < ce ? r0.y : __float_as_uint(kMask);
+    float Pp0[2], Y0[2], T0[2];
+    host_terms<kPremasked>(L, r0, cr, p0, 0.f, Pp0, Y0, T0);
+#pragma unroll
+    for (int q = 0; q < kQF; ++q)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) mn[q][c] = vmin(mn[q][c], fmaf(Pp0[c], cr.tt[q][c], Y0[c]));
+  }
+}
+
+// Gathers packed partial minima: lanes whose SM levels agree modulo NLP combine (xor 16
+// and xor 32 over the lane index for NLP = 2, xor 32 for NLP = 4), lanes at levels below
+// NLP keep the result, and the others restart from +inf for the classes still to come.
+template <int NLP>
+__device__ __forceinline__ void fold_levels(float (&mn)[kQF][2], int j) {
+#pragma unroll
+  for (int q = 0; q < kQF; ++q)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float v = mn[q][c];
+      if (NLP <= 2) {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        v = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
+      }
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+      v = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
+      mn[q][c] = j < NLP ? v : kInf;
+    }
+}
+
+// Pass 1 over the class list of one chunk, every class in the plain layout.
+template <int MODE, bool NORM>
+__device__ __forceinline__ void pass1_classes(const char *L, uint32_t recB, uint32_t wblkB, const int *clist,
+                                              int ncls, uint32_t j64, uint32_t k04, float p0,
+                                              const float (&lo)[kQF], const float (&sb)[kQF], float sb0,
+                                              float (&mn)[kQF][2]) {
+  for (int k = 0; k < ncls; ++k) {
+    const int packed = uniform(clist[k]);
+    const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
+    const ClassRegs cr = class_regs(L, wblkB, j64, k04, (uint32_t)(cls / kNS8) * 64u, (uint32_t)(cls % kNS8) * 64u);
+    class_pass1<MODE, NORM>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
+  }
+}
+
+// Pass 1 over the class list of one chunk in the common mode.  With pk (the tile's GPUs fit
+// one chunk) capped classes are packed: classes come in ascending max cap, so the levels
+// per GPU never decrease and each packed group is folded once, when the next starts.
+__device__ __forceinline__ void pass1_common(const char *L, uint32_t recB, uint32_t wblkB, const int *clist,
+                                             int ncls, bool pk, int j, uint32_t k04, float p0,
+                                             float (&mn)[kQF][2]) {
+  int grp = kNS8;
+  for (int k = 0; k < ncls; ++k) {
+    const int packed = uniform(clist[k]);
+    const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
+    const int mc = max(cls / kNS8, cls % kNS8);
+    const int lg = !pk ? 3 : mc < 2 ? 1 : mc < 4 ? 2 : 3;   // log2 of the levels per GPU
+    const int nlp = 1 << lg;
+    if (nlp != grp) {
+      if (grp == 2)
+        fold_levels<2>(mn, j);
+      else if (grp == 4)
+        fold_levels<4>(mn, j);
+      grp = nlp;
+    }
+    const ClassRegs cr = class_regs(L, wblkB, (uint32_t)(j & (nlp - 1)) * 64u, k04, (uint32_t)(cls / kNS8) * 64u,
+                                    (uint32_t)(cls % kNS8) * 64u);
+    class_pass1_common(L, recB, cs, ce, cr, p0, j >> lg, kNS8 >> lg, mn);
+  }
+  if (grp == 2)
+    fold_levels<2>(mn, j);
+  else if (grp == 4)
+    fold_levels<4>(mn, j);
+}
+
 // DPP lane moves within rows of 16 lanes (every source lane exists).
 constexpr int kDppRor8 = 0x128;        // row_ror:8: lane i reads lane i ^ 8 of its row
 constexpr int kDppHalfMirror = 0x141;  // lane i reads lane 7 - i of its group of 8
@@ -1042,7 +1174,8 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     __syncthreads();                      // previous records no longer in use; table staged
     for (int i = threadIdx.x; i < kClasses; i += T) s_cls[i] = 0;
     __syncthreads();
-    // records of this chunk, grouped by (cap_pf, cap_dc) class with an LDS counting sort
+    // records of this chunk, grouped by (cap_pf, cap_dc) class with an LDS counting sort,
+    // classes in ascending max(cap_pf, cap_dc)
     v4u rec[kPer];
     int key[kPer], rank[kPer];
 #pragma unroll
@@ -1056,7 +1189,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
         rec[u].y = __float_as_uint(r.kappa);
         rec[u].z = (uint32_t)g;
         rec[u].w = (uint32_t)r.caps;
-        key[u] = (r.caps & 0xff) * kNS8 + ((r.caps >> 8) & 0xff);
+        key[u] = class_id(r.caps & 0xff, (r.caps >> 8) & 0xff);
         rank[u] = atomicAdd(&s_cls[key[u]], 1);
       }
     }
@@ -1067,7 +1200,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
       s_cls[threadIdx.x] = inc - cnt;
       const unsigned long long ne = __ballot(cnt > 0);
       const int pos = __popcll(ne & ((1ull << threadIdx.x) - 1ull));
-      if (cnt > 0) s_clist[pos] = threadIdx.x | ((inc - cnt) << 6) | (inc << 15);
+      if (cnt > 0) s_clist[pos] = class_caps(threadIdx.x) | ((inc - cnt) << 6) | (inc << 15);
       if (threadIdx.x == kWave - 1) {
         s_cls[kClasses] = inc;
         s_clist[kClasses] = __popcll(ne);
@@ -1084,34 +1217,18 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     __syncthreads();
     if (live_any) {
       const int ncls = uniform(s_clist[kClasses]);
-      for (int k = 0; k < ncls; ++k) {
-        const int packed = uniform(s_clist[k]);
-        const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
-        const uint32_t cpB = (uint32_t)(cls / kNS8) * 64u, cdB = (uint32_t)(cls % kNS8) * 64u;
-        ClassRegs cr;
-        const uint32_t aP = wblkB + min(j64, cpB) + k04;
-        cr.mD = min(j64, cdB) + k04;
-        cr.pdp = lds2(L, aP);
-        cr.pdd = lds2(L, wblkB + cr.mD);
-        if (j64 > max(cpB, cdB)) cr.pdp = v2f{kMask, kMask};   // repeated cells drop out
-#pragma unroll
-        for (int q = 0; q < kQF; ++q) cr.tt[q] = lds2(L, aP + (1 + q) * kC * 4);
-        if (nrm) {
-          if (tile_same)
-            class_pass1<kPremasked, true>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-          else if (wsame)
-            class_pass1<kWaveSame, true>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-          else
-            class_pass1<kMixed, true>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-        } else {
-          if (tile_same)
-            class_pass1<kPremasked, false>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-          else if (wsame)
-            class_pass1<kWaveSame, false>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-          else
-            class_pass1<kMixed, false>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-        }
-      }
+      if (tile_same && nrm)
+        pass1_common(L, recB, wblkB, s_clist, ncls, hcnt <= kHcap, j, k04, p0, mn);
+      else if (nrm && wsame)
+        pass1_classes<kWaveSame, true>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
+      else if (nrm)
+        pass1_classes<kMixed, true>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
+      else if (tile_same)
+        pass1_classes<kPremasked, false>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
+      else if (wsame)
+        pass1_classes<kWaveSame, false>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
+      else
+        pass1_classes<kMixed, false>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
     }
   }
 

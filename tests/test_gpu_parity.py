@@ -255,6 +255,32 @@ def test_fast_kernel_more_hosts_than_one_lds_chunk():
     parity_place(inp, label=f"8x16 with {hosts} hosts per model")
 
 
+@pytest.mark.parametrize("seed,variant", [(0, "plain"), (1, "plain"), (2, "ties"), (3, "ties"),
+                                          (4, "negative"), (5, "low caps")])
+def test_fast_kernel_packed_capped_classes(seed, variant):
+    """8x16 tables, one SLO pair per model and Lout >= 1 (the common scoring mode), every
+    (cap_pf, cap_dc) pair: GPUs whose caps leave repeated SM levels are scored several per
+    wavefront step, classes of every size leave partial steps, and the partial minima are
+    folded back per level.  'ties' makes every GPU of a request equal (the lowest id must
+    win across packed and unpacked classes), 'negative' flips half the power slopes,
+    'low caps' keeps every cap at 0..3 (packed classes only)."""
+    rng = np.random.default_rng(9100 + seed)
+    R, G, M = 700, 90, 3
+    inp = W.make_tiny_placement(rng, R=R, G=G, M=M, NS=8, NF=16, W=2, caps=True, ties=variant == "ties")
+    q, g = inp["requests"], inp["gpus"]
+    m = q["model"]
+    q["slo_ttft_ms"] = rng.uniform(20.0, 70.0, M).astype(np.float32)[m]
+    q["slo_tbt_ms"] = rng.uniform(10.0, 45.0, M).astype(np.float32)[m]
+    q["pred_out_tokens"] = rng.integers(1, 300, R).astype(np.int32)
+    if variant == "negative":
+        g["k_dyn_w"][::2] *= np.float32(-1.0)
+        inp["lut"]["p0_w"] = 5.0
+    if variant == "low caps":
+        g["cap_pf"] = (g["cap_pf"] % 4).astype(np.int8)
+        g["cap_dc"] = (g["cap_dc"] % 4).astype(np.int8)
+    parity_place(inp, label=f"8x16 packed capped classes ({variant}, seed {seed})")
+
+
 def test_generic_kernel_four_waves_per_block():
     rng = np.random.default_rng(607)
     inp = W.make_tiny_placement(rng, R=20011, G=50, M=3, NS=4, NF=6, W=2, caps=True)
