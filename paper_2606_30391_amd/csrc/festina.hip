@@ -135,6 +135,21 @@ __device__ __forceinline__ ReqRec load_req(const PlaceArgs &a, int pos) {
   return q;
 }
 
+// Request record at bucket position pos, per lane (vector loads).
+__device__ __forceinline__ ReqRec load_req_lane(const PlaceArgs &a, int pos) {
+  const v4i *p = reinterpret_cast<const v4i *>(a.preq + pos);
+  const v4i x = p[0], y = p[1];
+  ReqRec q;
+  q.r = x.x;
+  q.row = x.y;
+  q.lout = __int_as_float(x.z);
+  q.slo_ttft = __int_as_float(x.w);
+  q.slo_tbt = __int_as_float(y.x);
+  q.rlout = __int_as_float(y.y);
+  q.pad[0] = q.pad[1] = 0;
+  return q;
+}
+
 // ------------------------------------------------------------------ prologue kernels
 __global__ void k_zero(int32_t *p, int32_t n) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
@@ -994,8 +1009,9 @@ __device__ __forceinline__ float dpp(float x) {
 // est[q] = min over the wavefront's lanes of min(m[q][0], m[q][1]), for the kQF = 8
 // requests at once, as a transposing reduction: each exchange halves the values a lane
 // holds (xor 32 and xor 16 by permlane swaps, xor 8 by DPP) until lane l holds request
-// l / 8's partial minimum, then three DPP steps reduce each group of 8 lanes.
-__device__ __forceinline__ void wave_min8(const float (&m)[kQF][2], float (&est)[kQF]) {
+// l / 8's partial minimum, then three DPP steps reduce each group of 8 lanes.  Returns
+// est[l / 8] in lane l.
+__device__ __forceinline__ float wave_min8(const float (&m)[kQF][2], float (&est)[kQF]) {
   static_assert(kQF == 8, "the exchange pattern is written for 8 requests per wavefront");
   float v[8], u[4], w[2];
 #pragma unroll
@@ -1020,6 +1036,17 @@ __device__ __forceinline__ void wave_min8(const float (&m)[kQF][2], float (&est)
   c = vmin(c, dpp<kDppQuad1032>(c));
 #pragma unroll
   for (int q = 0; q < 8; ++q) est[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(c), 8 * q));
+  return c;
+}
+
+// Minimum of g over the lanes that share lane % 8 (xor 8 by DPP, xor 16 and xor 32 by
+// permlane swaps); every lane receives its group's minimum.
+__device__ __forceinline__ int min_over_lane_bits_345(int g) {
+  g = min(g, __builtin_amdgcn_update_dpp(0, g, kDppRor8, 0xf, 0xf, false));
+  auto r = __builtin_amdgcn_permlane16_swap((unsigned)g, (unsigned)g, false, false);
+  g = min((int)r[0], (int)r[1]);
+  r = __builtin_amdgcn_permlane32_swap((unsigned)g, (unsigned)g, false, false);
+  return min((int)r[0], (int)r[1]);
 }
 
 template <int WPB>
@@ -1066,53 +1093,71 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     *reinterpret_cast<v2f *>(L + wblkB + j64 + k04) = pd;
   }
 
-  // this wavefront's requests and their prompt rows (NaN where TTFT misses the SLO).  A
-  // request whose whole row is NaN is dead: infeasible whatever the TBT test says, so it
-  // takes no part in the TBT-SLO uniformity checks.
+  // this wavefront's requests and their prompt rows
   const int q0 = beg + wv * kQF;
   const int nq = max(0, min(kQF, end - q0));
-  int rq[kQF];
+  // Lane l stages SM level l % 8 (16 cells) of request l / 8's prompt row and keeps that
+  // request's fields; a missing request reads the tile's first record and row 0 and is
+  // masked.  Rows: NaN where TTFT misses the SLO, scaled by 1 / Lout when every request of
+  // the wavefront has a usable reciprocal and every scaled value stays normal (or NaN), or
+  // is zero because the latency is.
+  const int sq = lane >> 3;
+  const bool shas = sq < nq;
+  bool nrm;
+  unsigned long long livem;
+  const ReqRec myr = load_req_lane(a, shas ? q0 + sq : beg);
+  const int r_l = shas ? myr.r : -1;
+  const float lo_l = shas ? myr.lout : 0.f;
+  const float sb_l = shas ? myr.slo_tbt : -kInf;
+  {
+    const float st = shas ? myr.slo_ttft : -kInf;
+    const float rl = shas ? myr.rlout : 1.f;
+    const float *pr = a.pf + ((size_t)m * kRows + (shas ? myr.row : 0)) * kC + (lane & 7) * 16;
+    float v[16];
+    if ((reinterpret_cast<uintptr_t>(a.pf) & 15) == 0) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float4 x = reinterpret_cast<const float4 *>(pr)[u];
+        v[4 * u] = x.x;
+        v[4 * u + 1] = x.y;
+        v[4 * u + 2] = x.z;
+        v[4 * u + 3] = x.w;
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = pr[u];
+    }
+    bool ok = rl > 0.f, any = false;
+    float sc[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      v[u] = v[u] < st ? v[u] : kMask;
+      sc[u] = v[u] * rl;
+      ok = ok & scaled_ok(sc[u], v[u]);
+      any = any | (v[u] == v[u]);
+    }
+    nrm = __ballot(!ok) == 0ull;
+    float4 *d = reinterpret_cast<float4 *>(L + wblkB + (1 + sq) * kC * 4 + (lane & 7) * 64);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      d[u] = nrm ? make_float4(sc[4 * u], sc[4 * u + 1], sc[4 * u + 2], sc[4 * u + 3])
+                 : make_float4(v[4 * u], v[4 * u + 1], v[4 * u + 2], v[4 * u + 3]);
+    livem = __ballot(any);
+  }
+  // per-request uniform values: Lout and the TBT SLO from lane 8q
   float lo[kQF], sb[kQF];
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) {
+    lo[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lo_l), 8 * q));
+    sb[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sb_l), 8 * q));
+  }
+  // a request whose whole row is NaN is dead: infeasible whatever the TBT test says, so it
+  // takes no part in the TBT-SLO uniformity checks
   bool live_any = false, wsame = true;
   float sb0 = 0.f;
-  // All request records, then all prompt-row loads, in flight before the first use.  A
-  // missing request reads the tile's first record and row 0, and is masked below.
-  ReqRec rr[kQF];
-#pragma unroll
-  for (int q = 0; q < kQF; ++q) rr[q] = load_req(a, q < nq ? q0 + q : beg);
-  float raw[kQF][2];
 #pragma unroll
   for (int q = 0; q < kQF; ++q) {
-    rq[q] = q < nq ? rr[q].r : -1;
-    const float *pr = a.pf + ((size_t)m * kRows + (rq[q] >= 0 ? rr[q].row : 0)) * kC + 2 * lane;
-    raw[q][0] = pr[0];
-    raw[q][1] = pr[1];
-  }
-  // Prompt rows: NaN where TTFT misses the SLO, scaled by 1 / Lout when every request of the
-  // wavefront has a usable reciprocal and every scaled value stays normal (or NaN), or is
-  // zero because the latency is.
-  v2f pv[kQF], ps[kQF];
-  bool nrm = true;
-#pragma unroll
-  for (int q = 0; q < kQF; ++q) {
-    const bool has = rq[q] >= 0;
-    lo[q] = has ? rr[q].lout : 0.f;
-    sb[q] = has ? rr[q].slo_tbt : -kInf;
-    const float st = has ? rr[q].slo_ttft : -kInf;
-    const float rl = has ? rr[q].rlout : 1.f;
-    pv[q].x = raw[q][0] < st ? raw[q][0] : kMask;
-    pv[q].y = raw[q][1] < st ? raw[q][1] : kMask;
-    ps[q].x = pv[q].x * rl;
-    ps[q].y = pv[q].y * rl;
-    nrm = nrm & (rl > 0.f) & scaled_ok(ps[q].x, pv[q].x) & scaled_ok(ps[q].y, pv[q].y);
-  }
-  nrm = __ballot(!nrm) == 0ull;
-#pragma unroll
-  for (int q = 0; q < kQF; ++q) {
-    const v2f v = pv[q];
-    *reinterpret_cast<v2f *>(L + wblkB + (1 + q) * kC * 4 + j64 + k04) = nrm ? ps[q] : v;
-    const bool live = __ballot(v.x == v.x || v.y == v.y) != 0ull;
-    if (live) {
+    if ((livem >> (8 * q)) & 0xffull) {
       if (!live_any) sb0 = sb[q];
       wsame = wsame && __float_as_int(sb[q]) == __float_as_int(sb0);
       live_any = true;
@@ -1241,7 +1286,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   float est[kQF];
   unsigned long long t0[kQF], t1[kQF];
   bool rounds = false;
-  wave_min8(mn, est);
+  const float cmin = wave_min8(mn, est);   // request sq's minimum
 #pragma unroll
   for (int q = 0; q < kQF; ++q) {
     const bool feas = q < nq && (nrm ? lo[q] * est[q] : est[q]) < kInf;
@@ -1250,7 +1295,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     rounds = rounds || (t0[q] | t1[q]) != 0ull;
   }
   const int myq = lane & (kQF - 1);
-  int bestl = INT_MAX;                    // lane q < kQF: best index of request q
+  int bestl = INT_MAX;                    // lanes l % 8 = q: best index of request q
   while (rounds) {
     rounds = false;
     if (lane == 0) {
@@ -1327,24 +1372,19 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
         }
       }
     }
-#pragma unroll
-    for (int off = kQF; off < kWave; off <<= 1) gmin = min(gmin, __shfl_xor(gmin, off, kWave));
+    gmin = min_over_lane_bits_345(gmin);
     if (cell >= 0 && gmin != INT_MAX) bestl = min(bestl, gmin * kC + cell);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  if (lane < nq) {
-    float e = nrm ? lo[0] * est[0] : est[0];
-#pragma unroll
-    for (int q = 1; q < kQF; ++q) e = lane == q ? (nrm ? lo[q] * est[q] : est[q]) : e;
-    int r = rq[0];
-#pragma unroll
-    for (int q = 1; q < kQF; ++q) r = lane == q ? rq[q] : r;
+  // lane 9q writes request q: its minimum sits in lanes l / 8 = q, its index in lanes
+  // l % 8 = q, its record in lanes l / 8 = q
+  if ((lane & 7) == sq && shas) {
     const bool found = bestl != INT_MAX;
-    a.choice[r] = found ? bestl : -1;
-    a.feasible[r] = found ? 1 : 0;
-    a.energy[r] = found ? e : kInf;
+    a.choice[r_l] = found ? bestl : -1;
+    a.feasible[r_l] = found ? 1 : 0;
+    a.energy[r_l] = found ? (nrm ? lo_l * cmin : cmin) : kInf;
   }
 }
 
