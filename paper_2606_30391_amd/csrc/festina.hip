@@ -1096,11 +1096,11 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   // this wavefront's requests and their prompt rows
   const int q0 = beg + wv * kQF;
   const int nq = max(0, min(kQF, end - q0));
-  // Lane l stages SM level l % 8 (16 cells) of request l / 8's prompt row and keeps that
-  // request's fields; a missing request reads the tile's first record and row 0 and is
-  // masked.  Rows: NaN where TTFT misses the SLO, scaled by 1 / Lout when every request of
-  // the wavefront has a usable reciprocal and every scaled value stays normal (or NaN), or
-  // is zero because the latency is.
+  // Lane l stages 16 cells of request l / 8's prompt row and keeps that request's fields;
+  // a missing request reads the tile's first record and row 0 and is masked.  Rows: NaN
+  // where TTFT misses the SLO, scaled by 1 / Lout when every request of the wavefront has a
+  // usable reciprocal and every scaled value stays normal (or NaN), or is zero because the
+  // latency is.
   const int sq = lane >> 3;
   const bool shas = sq < nq;
   bool nrm;
@@ -1112,12 +1112,15 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   {
     const float st = shas ? myr.slo_ttft : -kInf;
     const float rl = shas ? myr.rlout : 1.f;
-    const float *pr = a.pf + ((size_t)m * kRows + (shas ? myr.row : 0)) * kC + (lane & 7) * 16;
+    // lane l takes the 16-byte chunks l % 8 + 8u (u < 4) of the row, so each load and each
+    // store of a request's 8 lanes covers 128 contiguous bytes
+    const float *pr = a.pf + ((size_t)m * kRows + (shas ? myr.row : 0)) * kC;
+    const int x8 = lane & 7;
     float v[16];
     if ((reinterpret_cast<uintptr_t>(a.pf) & 15) == 0) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const float4 x = reinterpret_cast<const float4 *>(pr)[u];
+        const float4 x = reinterpret_cast<const float4 *>(pr)[8 * u + x8];
         v[4 * u] = x.x;
         v[4 * u + 1] = x.y;
         v[4 * u + 2] = x.z;
@@ -1125,7 +1128,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
       }
     } else {
 #pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = pr[u];
+      for (int u = 0; u < 16; ++u) v[u] = pr[(8 * (u >> 2) + x8) * 4 + (u & 3)];
     }
     bool ok = rl > 0.f, any = false;
     float sc[16];
@@ -1137,10 +1140,10 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
       any = any | (v[u] == v[u]);
     }
     nrm = __ballot(!ok) == 0ull;
-    float4 *d = reinterpret_cast<float4 *>(L + wblkB + (1 + sq) * kC * 4 + (lane & 7) * 64);
+    float4 *d = reinterpret_cast<float4 *>(L + wblkB + (1 + sq) * kC * 4);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      d[u] = nrm ? make_float4(sc[4 * u], sc[4 * u + 1], sc[4 * u + 2], sc[4 * u + 3])
+      d[8 * u + x8] = nrm ? make_float4(sc[4 * u], sc[4 * u + 1], sc[4 * u + 2], sc[4 * u + 3])
                  : make_float4(v[4 * u], v[4 * u + 1], v[4 * u + 2], v[4 * u + 3]);
     livem = __ballot(any);
   }
