@@ -1039,14 +1039,71 @@ __device__ __forceinline__ float wave_min8(const float (&m)[kQF][2], float (&est
   return c;
 }
 
-// Minimum of g over the lanes that share lane % 8 (xor 8 by DPP, xor 16 and xor 32 by
-// permlane swaps); every lane receives its group's minimum.
-__device__ __forceinline__ int min_over_lane_bits_345(int g) {
-  g = min(g, __builtin_amdgcn_update_dpp(0, g, kDppRor8, 0xf, 0xf, false));
-  auto r = __builtin_amdgcn_permlane16_swap((unsigned)g, (unsigned)g, false, false);
-  g = min((int)r[0], (int)r[1]);
-  r = __builtin_amdgcn_permlane32_swap((unsigned)g, (unsigned)g, false, false);
-  return min((int)r[0], (int)r[1]);
+// One pass-2 round: for each request q with cell[q] >= 0, the lowest GPU id whose candidate at
+// that cell reaches the request's minimum est[q], recomputed with the operations of pass 1
+// (hence bit-identical); best[q] = min(best[q], g * 128 + cell).  Lane l takes host b0 + l of
+// the model's ascending host list, reads its record once and evaluates every request's
+// cell; the first set lane of a request's match mask is its lowest GPU id, so a request
+// stops at the first block of 64 hosts with a match.
+template <bool NRM>
+__device__ __forceinline__ void pass2_round(const PlaceArgs &a, const char *L, uint32_t recB, uint32_t dcsB,
+                                            uint32_t wblkB, const short *s_pos, const int32_t *hl, const HostRec *rw,
+                                            bool recs_in_lds, int hcnt, float p0, const int (&cell)[kQF],
+                                            const float (&est)[kQF], const float (&lo)[kQF], const float (&sb)[kQF],
+                                            int (&best)[kQF]) {
+  const int lane = __lane_id();
+  uint32_t cj64[kQF], ck4[kQF], base[kQF];
+  unsigned pending = 0;
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) {
+    const int c = cell[q] >= 0 ? cell[q] : 0;
+    cj64[q] = (uint32_t)(c >> 4) * 64u;
+    ck4[q] = (uint32_t)(c & 15) * 4u;
+    base[q] = wblkB + ck4[q];
+    pending |= cell[q] >= 0 ? 1u << q : 0u;
+  }
+  for (int b0 = 0; b0 < hcnt && pending != 0u; b0 += kWave) {
+    const int i = b0 + lane;
+    const bool valid = i < hcnt;
+    const int ic = valid ? i : hcnt - 1;
+    uint32_t rowB;
+    int g, caps;
+    float kap;
+    if (recs_in_lds) {                    // host i (ascending GPU id) sits at slot s_pos[i]
+      const v4u r = *reinterpret_cast<const v4u *>(L + recB + (int)s_pos[ic] * 16);
+      rowB = r.x;
+      kap = __uint_as_float(r.y);
+      g = (int)r.z;
+      caps = (int)r.w;
+    } else {
+      g = hl[ic];
+      const HostRec r = rw[g];
+      rowB = dcsB + (uint32_t)(max(r.row_off, 0) / kC) * kRowB;
+      kap = r.kappa;
+      caps = r.caps;
+    }
+    const uint32_t cpB = (uint32_t)(caps & 0xff) * 64u, cdB = (uint32_t)((caps >> 8) & 0xff) * 64u;
+    const uint32_t mxB = max(cpB, cdB);
+#pragma unroll
+    for (int q = 0; q < kQF; ++q) {
+      // a cell above max(cap_pf, cap_dc) repeats a lower cell of the same GPU: pass 1 gave it
+      // NaN power, so it never matches
+      const uint32_t jP = min(cj64[q], cpB), jD = min(cj64[q], cdB);
+      const uint32_t aP = base[q] + jP, aD = base[q] + jD;
+      const float pdp = lds1(L, aP), pdd = lds1(L, aD);
+      const float tbt = lds1(L, rowB + jD + ck4[q]);
+      const float tt = lds1(L, aP + (1 + q) * kC * 4);
+      const float E = NRM ? cell_key(kap, pdp, pdd, tbt, tt, p0, sb[q])
+                          : cell_energy(kap, pdp, pdd, tbt, tt, p0, lo[q], sb[q]);
+      const bool hit = (E == est[q]) & valid & (cj64[q] <= mxB);
+      const unsigned long long m = __ballot(hit);
+      if (((pending >> q) & 1u) && m != 0ull) {
+        const int gw = __builtin_amdgcn_readlane(g, __builtin_ctzll(m));
+        best[q] = min(best[q], gw * kC + cell[q]);
+        pending &= ~(1u << q);
+      }
+    }
+  }
 }
 
 template <int WPB>
@@ -1055,7 +1112,6 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   __shared__ int s_live[WPB], s_same[WPB], s_sb[WPB];
   __shared__ int s_cls[kClasses + 1];     // class counts, then class starts
   __shared__ int s_clist[kClasses + 1];   // non-empty classes: cls | start << 6 | end << 15; [64] = count
-  __shared__ float4 s_par[WPB][kQF];      // pass 2: per request {cell, E*, Lout, TBT SLO}
   __shared__ short s_pos[kHcap];          // slot of host i's record after the class sort
   char *L = reinterpret_cast<char *>(lds);
   constexpr uint32_t recB = fast_rec_off(WPB);
@@ -1281,10 +1337,8 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   }
 
   // pass 2: per request the winning energy E* (key K*: E* = Lout * K*), then the lowest index
-  // that reaches it.
-  // Requests are searched together: lane = (host i, request q) with q = lane % kQF, so a
-  // chunk covers 64 / kQF hosts of every request; one round per tied cell of a request
-  // (one round unless two different cells reach exactly E*).
+  // that reaches it.  One round per tied cell of a request (one round unless two different
+  // cells reach exactly E*); in a round every lane takes one host, in ascending GPU id.
   const bool recs_in_lds = hcnt <= kHcap;
   float est[kQF];
   unsigned long long t0[kQF], t1[kQF];
@@ -1297,27 +1351,19 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
     t1[q] = __ballot(feas && mn[q][1] == est[q]);
     rounds = rounds || (t0[q] | t1[q]) != 0ull;
   }
-  const int myq = lane & (kQF - 1);
-  int bestl = INT_MAX;                    // lanes l % 8 = q: best index of request q
+  int best[kQF];                          // lowest index reaching E*, per request
+#pragma unroll
+  for (int q = 0; q < kQF; ++q) best[q] = INT_MAX;
   while (rounds) {
     rounds = false;
-    if (lane == 0) {
+    int cell[kQF];                        // next tied cell of each request, ascending; -1: none
 #pragma unroll
-      for (int q = 0; q < kQF; ++q) {
-        int cell = -1;                    // next tied cell of request q, ascending
-        if ((t0[q] | t1[q]) != 0ull) {
-          const int l0 = t0[q] ? __builtin_ctzll(t0[q]) : 64;
-          const int l1 = t1[q] ? __builtin_ctzll(t1[q]) : 64;
-          cell = l0 <= l1 ? 2 * l0 : 2 * l1 + 1;
-        }
-        s_par[wv][q] = make_float4(__int_as_float(cell), est[q], lo[q], sb[q]);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < kQF; ++q) {       // consume the cell just published
+    for (int q = 0; q < kQF; ++q) {
+      cell[q] = -1;
       if ((t0[q] | t1[q]) != 0ull) {
         const int l0 = t0[q] ? __builtin_ctzll(t0[q]) : 64;
         const int l1 = t1[q] ? __builtin_ctzll(t1[q]) : 64;
+        cell[q] = l0 <= l1 ? 2 * l0 : 2 * l1 + 1;
         if (l0 <= l1)
           t0[q] &= t0[q] - 1ull;
         else
@@ -1325,67 +1371,18 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
       }
       rounds = rounds || (t0[q] | t1[q]) != 0ull;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const float4 par = s_par[wv][myq];
-    const int cell = __float_as_int(par.x);
-    int gmin = INT_MAX;                   // lowest GPU id reaching E* (per lane)
-    // requests with a cell this round, as an 8-bit mask (lane q of each group of kQF lanes)
-    const unsigned need = (unsigned)(__ballot(cell >= 0) & ((1ull << kQF) - 1ull));
-    if (cell >= 0) {
-      const uint32_t cj64 = (uint32_t)(cell >> 4) * 64u, ck4 = (uint32_t)(cell & 15) * 4u;
-      const uint32_t ttB = wblkB + (1 + myq) * kC * 4;
-      // hosts ascend by GPU id, so once every request of the round has found E* no later
-      // host can lower its index: stop there
-      for (int b0 = 0; b0 < hcnt * kQF; b0 += kWave) {
-        if (b0 > 0) {
-          unsigned long long f = __ballot(gmin != INT_MAX);
-          f |= f >> 32;
-          f |= f >> 16;
-          f |= f >> 8;
-          if ((((unsigned)f & 0xffu) & need) == need) break;
-        }
-        const int i = (b0 + lane) / kQF;
-        if (i < hcnt) {
-          uint32_t rowB;
-          int g, caps;
-          float kap;
-          if (recs_in_lds) {           // host i (ascending GPU id) sits at slot s_pos[i]
-            const v4u r = *reinterpret_cast<const v4u *>(L + recB + (int)s_pos[i] * 16);
-            rowB = r.x;
-            kap = __uint_as_float(r.y);
-            g = (int)r.z;
-            caps = (int)r.w;
-          } else {
-            g = hl[i];
-            const HostRec r = rw[g];
-            rowB = dcsB + (uint32_t)(max(r.row_off, 0) / kC) * kRowB;
-            kap = r.kappa;
-            caps = r.caps;
-          }
-          const uint32_t cpB = (uint32_t)(caps & 0xff) * 64u, cdB = (uint32_t)((caps >> 8) & 0xff) * 64u;
-          const uint32_t mP = min(cj64, cpB) + ck4;
-          const uint32_t mD = min(cj64, cdB) + ck4;
-          const float pdp = cj64 > max(cpB, cdB) ? kMask : lds1(L, wblkB + mP);
-          const float pdd = lds1(L, wblkB + mD), tbt = lds1(L, rowB + mD), tt = lds1(L, ttB + mP);
-          const float E = nrm ? cell_key(kap, pdp, pdd, tbt, tt, p0, par.w)
-                              : cell_energy(kap, pdp, pdd, tbt, tt, p0, par.z, par.w);
-          if (E == par.y) gmin = min(gmin, g);
-        }
-      }
-    }
-    gmin = min_over_lane_bits_345(gmin);
-    if (cell >= 0 && gmin != INT_MAX) bestl = min(bestl, gmin * kC + cell);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (nrm)
+      pass2_round<true>(a, L, recB, dcsB, wblkB, s_pos, hl, rw, recs_in_lds, hcnt, p0, cell, est, lo, sb, best);
+    else
+      pass2_round<false>(a, L, recB, dcsB, wblkB, s_pos, hl, rw, recs_in_lds, hcnt, p0, cell, est, lo, sb, best);
   }
-  // lane 9q writes request q: its minimum sits in lanes l / 8 = q, its index in lanes
-  // l % 8 = q, its record in lanes l / 8 = q
-  if ((lane & 7) == sq && shas) {
-    const bool found = bestl != INT_MAX;
-    a.choice[r_l] = found ? bestl : -1;
+  // lane 8q writes request q: its record and minimum sit in lanes l / 8 = q
+  int myb = best[0];
+#pragma unroll
+  for (int q = 1; q < kQF; ++q) myb = sq == q ? best[q] : myb;
+  if ((lane & 7) == 0 && shas) {
+    const bool found = myb != INT_MAX;
+    a.choice[r_l] = found ? myb : -1;
     a.feasible[r_l] = found ? 1 : 0;
     a.energy[r_l] = found ? (nrm ? lo_l * cmin : cmin) : kInf;
   }
