@@ -899,16 +899,21 @@ __device__ __forceinline__ ClassRegs class_regs(const char *L, uint32_t wblkB, u
 // lane l works on GPU (step start + slot), slot = (l / 8) / (8 / H), at SM level
 // (l / 8) % (8 / H).  The partial minima of one cell then sit in the lanes that share its
 // level until fold_levels gathers them.  A lane past the class's last GPU reads that GPU's
-// record with NaN power.
+// record with NaN power.  ONE: H = 1, where every step's GPU exists and no lane needs the clamp.
+template <bool ONE>
 __device__ __forceinline__ void class_pass1_common(const char *L, uint32_t recB, int cs, int ce,
                                                    const ClassRegs &cr, float p0, int slot, int H,
                                                    float (&mn)[kQF][2]) {
+  if (ONE) {
+    slot = 0;
+    H = 1;
+  }
   int i = cs;
   for (; i + H < ce; i += 2 * H) {
     const int h1 = i + H + slot;
     const v4u r0 = *reinterpret_cast<const v4u *>(L + recB + (i + slot) * 16);
-    v4u r1 = *reinterpret_cast<const v4u *>(L + recB + min(h1, ce - 1) * 16);
-    r1.y = h1 < ce ? r1.y : __float_as_uint(kMask);
+    v4u r1 = *reinterpret_cast<const v4u *>(L + recB + (ONE ? h1 : min(h1, ce - 1)) * 16);
+    if (!ONE) r1.y = h1 < ce ? r1.y : __float_as_uint(kMask);
     float Pp0[2], Y0[2], T0[2], Pp1[2], Y1[2], T1[2];
     host_terms<kPremasked>(L, r0, cr, p0, 0.f, Pp0, Y0, T0);
     host_terms<kPremasked>(L, r1, cr, p0, 0.f, Pp1, Y1, T1);
@@ -920,8 +925,8 @@ __device__ __forceinline__ void class_pass1_common(const char *L, uint32_t recB,
   }
   if (i < ce) {
     const int h0 = i + slot;
-    v4u r0 = *reinterpret_cast<const v4u *>(L + recB + min(h0, ce - 1) * 16);
-    r0.y = h0 < ce ? r0.y : __float_as_uint(kMask);
+    v4u r0 = *reinterpret_cast<const v4u *>(L + recB + (ONE ? h0 : min(h0, ce - 1)) * 16);
+    if (!ONE) r0.y = h0 < ce ? r0.y : __float_as_uint(kMask);
     float Pp0[2], Y0[2], T0[2];
     host_terms<kPremasked>(L, r0, cr, p0, 0.f, Pp0, Y0, T0);
 #pragma unroll
@@ -967,32 +972,40 @@ __device__ __forceinline__ void pass1_classes(const char *L, uint32_t recB, uint
 
 // Pass 1 over the class list of one chunk in the common mode.  With pk (the tile's GPUs fit
 // one chunk) capped classes are packed: classes come in ascending max cap, so the levels
-// per GPU never decrease and each packed group is folded once, when the next starts.
+// per GPU never decrease and each packed group is folded once, when the next starts; the
+// classes with one GPU per step (every class without pk) come last and run in a loop of
+// their own.
 __device__ __forceinline__ void pass1_common(const char *L, uint32_t recB, uint32_t wblkB, const int *clist,
                                              int ncls, bool pk, int j, uint32_t k04, float p0,
                                              float (&mn)[kQF][2]) {
   int grp = kNS8;
-  for (int k = 0; k < ncls; ++k) {
+  int k = 0;
+  for (; k < ncls; ++k) {
     const int packed = uniform(clist[k]);
     const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
     const int mc = max(cls / kNS8, cls % kNS8);
     const int lg = !pk ? 3 : mc < 2 ? 1 : mc < 4 ? 2 : 3;   // log2 of the levels per GPU
+    if (lg == 3) break;
     const int nlp = 1 << lg;
     if (nlp != grp) {
-      if (grp == 2)
-        fold_levels<2>(mn, j);
-      else if (grp == 4)
-        fold_levels<4>(mn, j);
+      if (grp == 2) fold_levels<2>(mn, j);
       grp = nlp;
     }
     const ClassRegs cr = class_regs(L, wblkB, (uint32_t)(j & (nlp - 1)) * 64u, k04, (uint32_t)(cls / kNS8) * 64u,
                                     (uint32_t)(cls % kNS8) * 64u);
-    class_pass1_common(L, recB, cs, ce, cr, p0, j >> lg, kNS8 >> lg, mn);
+    class_pass1_common<false>(L, recB, cs, ce, cr, p0, j >> lg, kNS8 >> lg, mn);
   }
   if (grp == 2)
     fold_levels<2>(mn, j);
   else if (grp == 4)
     fold_levels<4>(mn, j);
+  for (; k < ncls; ++k) {
+    const int packed = uniform(clist[k]);
+    const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
+    const ClassRegs cr = class_regs(L, wblkB, (uint32_t)j * 64u, k04, (uint32_t)(cls / kNS8) * 64u,
+                                    (uint32_t)(cls % kNS8) * 64u);
+    class_pass1_common<true>(L, recB, cs, ce, cr, p0, 0, 1, mn);
+  }
 }
 
 // DPP lane moves within rows of 16 lanes (every source lane exists).
