@@ -899,15 +899,13 @@ __device__ __forceinline__ ClassRegs class_regs(const char *L, uint32_t wblkB, u
 // lane l works on GPU (step start + slot), slot = (l / 8) / (8 / H), at SM level
 // (l / 8) % (8 / H).  The partial minima of one cell then sit in the lanes that share its
 // level until fold_levels gathers them.  A lane past the class's last GPU reads that GPU's
-// record with NaN power.  ONE: H = 1, where every step's GPU exists and no lane needs the clamp.
-template <bool ONE>
+// record with NaN power (with H = 1 every step's GPU exists and no lane needs the clamp).
+template <int H>
 __device__ __forceinline__ void class_pass1_common(const char *L, uint32_t recB, int cs, int ce,
-                                                   const ClassRegs &cr, float p0, int slot, int H,
+                                                   const ClassRegs &cr, float p0, int slot,
                                                    float (&mn)[kQF][2]) {
-  if (ONE) {
-    slot = 0;
-    H = 1;
-  }
+  constexpr bool ONE = H == 1;
+  if (ONE) slot = 0;
   int i = cs;
   for (; i + H < ce; i += 2 * H) {
     const int h1 = i + H + slot;
@@ -970,42 +968,41 @@ __device__ __forceinline__ void pass1_classes(const char *L, uint32_t recB, uint
   }
 }
 
-// Pass 1 over the class list of one chunk in the common mode.  With pk (the tile's GPUs fit
-// one chunk) capped classes are packed: classes come in ascending max cap, so the levels
-// per GPU never decrease and each packed group is folded once, when the next starts; the
-// classes with one GPU per step (every class without pk) come last and run in a loop of
-// their own.
-__device__ __forceinline__ void pass1_common(const char *L, uint32_t recB, uint32_t wblkB, const int *clist,
-                                             int ncls, bool pk, int j, uint32_t k04, float p0,
-                                             float (&mn)[kQF][2]) {
-  int grp = kNS8;
-  int k = 0;
+// Pass 1 over the classes [k, ncls) of one chunk in the common mode that have 8 / H levels per
+// GPU, H GPUs per step; returns the first class with more levels.
+template <int H>
+__device__ __forceinline__ int pass1_group(const char *L, uint32_t recB, uint32_t wblkB, const int *clist, int k,
+                                           int ncls, bool pk, int j, uint32_t k04, float p0, float (&mn)[kQF][2]) {
+  constexpr int lg = H == 4 ? 1 : H == 2 ? 2 : 3;   // log2 of the levels per GPU
   for (; k < ncls; ++k) {
     const int packed = uniform(clist[k]);
     const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
     const int mc = max(cls / kNS8, cls % kNS8);
-    const int lg = !pk ? 3 : mc < 2 ? 1 : mc < 4 ? 2 : 3;   // log2 of the levels per GPU
-    if (lg == 3) break;
-    const int nlp = 1 << lg;
-    if (nlp != grp) {
-      if (grp == 2) fold_levels<2>(mn, j);
-      grp = nlp;
-    }
-    const ClassRegs cr = class_regs(L, wblkB, (uint32_t)(j & (nlp - 1)) * 64u, k04, (uint32_t)(cls / kNS8) * 64u,
-                                    (uint32_t)(cls % kNS8) * 64u);
-    class_pass1_common<false>(L, recB, cs, ce, cr, p0, j >> lg, kNS8 >> lg, mn);
+    if (H > 1 && (!pk || (mc < 2 ? 1 : mc < 4 ? 2 : 3) != lg)) break;
+    const ClassRegs cr = class_regs(L, wblkB, (uint32_t)(j & ((1 << lg) - 1)) * 64u, k04,
+                                    (uint32_t)(cls / kNS8) * 64u, (uint32_t)(cls % kNS8) * 64u);
+    class_pass1_common<H>(L, recB, cs, ce, cr, p0, j >> lg, mn);
   }
-  if (grp == 2)
-    fold_levels<2>(mn, j);
-  else if (grp == 4)
-    fold_levels<4>(mn, j);
-  for (; k < ncls; ++k) {
-    const int packed = uniform(clist[k]);
-    const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
-    const ClassRegs cr = class_regs(L, wblkB, (uint32_t)j * 64u, k04, (uint32_t)(cls / kNS8) * 64u,
-                                    (uint32_t)(cls % kNS8) * 64u);
-    class_pass1_common<true>(L, recB, cs, ce, cr, p0, 0, 1, mn);
+  return k;
+}
+
+// Pass 1 over the class list of one chunk in the common mode.  With pk (the tile's GPUs fit
+// one chunk) capped classes are packed.  Classes come in ascending max cap m, so they form
+// three groups in order, each run by a loop of its own: m <= 1 (2 levels, 4 GPUs per step),
+// m = 2 or 3 (4 levels, 2 GPUs per step), each folded into the plain layout when it ends, and
+// m >= 4 (one GPU per step; every class without pk).
+__device__ __forceinline__ void pass1_common(const char *L, uint32_t recB, uint32_t wblkB, const int *clist,
+                                             int ncls, bool pk, int j, uint32_t k04, float p0,
+                                             float (&mn)[kQF][2]) {
+  int k = 0;
+  if (pk) {
+    const int k1 = pass1_group<4>(L, recB, wblkB, clist, 0, ncls, pk, j, k04, p0, mn);
+    if (k1 > 0) fold_levels<2>(mn, j);
+    const int k2 = pass1_group<2>(L, recB, wblkB, clist, k1, ncls, pk, j, k04, p0, mn);
+    if (k2 > k1) fold_levels<4>(mn, j);
+    k = k2;
   }
+  pass1_group<1>(L, recB, wblkB, clist, k, ncls, pk, j, k04, p0, mn);
 }
 
 // DPP lane moves within rows of 16 lanes (every source lane exists).
