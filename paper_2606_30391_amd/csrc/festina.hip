@@ -83,8 +83,7 @@ struct PlaceArgs {
   int32_t NB;                    // buckets = 2 * W * M
   int32_t tile;                  // requests per tile
   int32_t max_tiles;
-  int32_t *cnt;                  // [NB4] counters (cursors too when NB > kHistMax)
-  int32_t *cur;                  // [NB4] scatter cursors, from zero (NB <= kHistMax)
+  int32_t *cnt;                  // [NB4] counters
   int32_t *bstart;               // [NB + 1]
   int32_t *n_tiles;              // [1]
   int2 *tiles;                   // [max_tiles] {bucket, first position}
@@ -93,6 +92,7 @@ struct PlaceArgs {
   HostRec *recs;                 // [W][G]
   ReqRec *preq;                  // [R] request records in bucket order
   int32_t *key;                  // [R]
+  int32_t *off;                  // [R] position of request r within its bucket
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -179,8 +179,10 @@ constexpr int kReqPerPrepBlock = 4 * kPrepBlock;  // requests per request block 
 constexpr int kHistMax = 8192;                    // buckets counted in LDS (else global atomics)
 
 // Blocks [0, nbr): kReqPerPrepBlock requests each, counted per bucket in an LDS histogram
-// and flushed with one global atomic per non-empty bucket.  Blocks [nbr, nbr + M): host
-// list of model (block - nbr).  Blocks after: GPU records, one thread per (wave, GPU).
+// and flushed with one global atomic per non-empty bucket; the atomics' old values give each
+// request its position within its bucket (its rank in the block's count plus the block's
+// base), so the scatter needs no further atomics.  Blocks [nbr, nbr + M): host list of model
+// (block - nbr).  Blocks after: GPU records, one thread per (wave, GPU).
 __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
   __shared__ int hist[kHistMax];
   const int b = blockIdx.x;
@@ -190,17 +192,26 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
       for (int k = threadIdx.x; k < a.NB; k += kPrepBlock) hist[k] = 0;
       __syncthreads();
     }
-    for (int u = 0; u < kReqPerPrepBlock / kPrepBlock; ++u) {
+    constexpr int U = kReqPerPrepBlock / kPrepBlock;
+    int key[U], pos[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
       const int r = b * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
-      if (r >= a.R) break;
-      const int k = prep_request(a, r);
-      if (k >= 0) atomicAdd(local ? &hist[k] : &a.cnt[k], 1);
+      key[u] = r < a.R ? prep_request(a, r) : -1;
+      pos[u] = key[u] >= 0 ? atomicAdd(local ? &hist[key[u]] : &a.cnt[key[u]], 1) : 0;
     }
     if (local) {
       __syncthreads();
       for (int k = threadIdx.x; k < a.NB; k += kPrepBlock)
-        if (hist[k]) atomicAdd(&a.cnt[k], hist[k]);
+        if (hist[k]) hist[k] = atomicAdd(&a.cnt[k], hist[k]);   // this block's base in bucket k
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (key[u] >= 0) pos[u] += hist[key[u]];
     }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (key[u] >= 0) a.off[b * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x] = pos[u];
     return;
   }
   if (b < nbr + a.M) {
@@ -297,7 +308,6 @@ __device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_c
     a.bstart[i] = pc;
     const int nt = (n + a.tile - 1) / a.tile;
     for (int q = 0; q < nt; ++q) a.tiles[pt + q] = make_int2(i, pc + q * a.tile);
-    a.cnt[i] = pc;                             // cursor for the scatter
     pc += n;
     pt += nt;
   }
@@ -307,8 +317,8 @@ __device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_c
   }
 }
 
-// One block of 1024 threads: exclusive scans of bucket counts and tiles-per-bucket,
-// the tile table, and scatter cursors.  Counts are first copied to LDS in one coalesced
+// One block of 1024 threads: exclusive scans of bucket counts and tiles-per-bucket, and
+// the tile table.  Counts are first copied to LDS in one coalesced
 // pass when they fit, so the scan never waits on a global load after a global store.
 __global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
   __shared__ int s_cnt[1024 / kWave];
@@ -420,44 +430,35 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start) {
   __syncthreads();
 }
 
-// Requests grouped by bucket.  With at most kHistMax buckets, each block scans the bucket
-// counts itself (dynamic LDS: ranks [NB], starts [NB]), ranks its requests per bucket in
-// LDS, reserves one range per non-empty bucket with an atomic on a zeroed cursor, then
-// writes the permutation.  With more buckets, k_scan has turned the counters into
-// cursors and every request takes its slot with a global atomic.
+// Requests grouped by bucket: request r goes to its bucket's start plus its position from
+// k_prep.  With at most kHistMax buckets each block scans the bucket counts itself (dynamic
+// LDS: starts [NB]); with more, k_scan has written the bucket starts.
 __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
-  extern __shared__ int sl[];
+  extern __shared__ int start[];
   constexpr int U = kReqPerPrepBlock / kPrepBlock;
-  const bool local = a.NB <= kHistMax;
-  int *hist = sl, *start = sl + a.NB;
-  int key[U], rank[U];
+  int key[U], pos[U];
   ReqRec rec[U];
   // request loads first, so that their latency overlaps the bucket scan
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int r = blockIdx.x * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
     key[u] = r < a.R ? a.key[r] : -1;
-    rank[u] = 0;
-    if (key[u] >= 0) rec[u] = make_req_rec(a, r);
+    pos[u] = 0;
+    if (key[u] >= 0) {
+      rec[u] = make_req_rec(a, r);
+      pos[u] = a.off[r];
+    }
   }
-  if (!local) {
+  if (a.NB <= kHistMax) {
+    block_scan_buckets(a, start);        // ends with a barrier
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (key[u] >= 0) a.preq[atomicAdd(&a.cnt[key[u]], 1)] = rec[u];
-    return;
+      if (key[u] >= 0) a.preq[start[key[u]] + pos[u]] = rec[u];
+  } else {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (key[u] >= 0) a.preq[a.bstart[key[u]] + pos[u]] = rec[u];
   }
-  for (int k = threadIdx.x; k < a.NB; k += kPrepBlock) hist[k] = 0;
-  block_scan_buckets(a, start);        // ends with a barrier
-#pragma unroll
-  for (int u = 0; u < U; ++u)
-    if (key[u] >= 0) rank[u] = atomicAdd(&hist[key[u]], 1);
-  __syncthreads();
-  for (int k = threadIdx.x; k < a.NB; k += kPrepBlock)
-    if (hist[k]) hist[k] = start[k] + atomicAdd(&a.cur[k], hist[k]);
-  __syncthreads();
-#pragma unroll
-  for (int u = 0; u < U; ++u)
-    if (key[u] >= 0) a.preq[hist[key[u]] + rank[u]] = rec[u];
 }
 
 // ------------------------------------------------------------------ scoring kernel
@@ -1559,7 +1560,7 @@ __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct PlaceLayout {
-  size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, preq, key, total;
+  size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, preq, key, off, total;
   int32_t NB, tile, max_tiles, waves_per_block;
   bool fast;                     // 8 SM x 16 frequency levels: the specialised kernel
 };
@@ -1605,7 +1606,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
     off = align256(off + bytes);
     return at;
   };
-  o->cnt = take(sizeof(int32_t) * 2 * ((NB + 3) & ~3LL));   // counters, then cursors
+  o->cnt = take(sizeof(int32_t) * ((NB + 3) & ~3LL));       // counters
   o->bstart = take(sizeof(int32_t) * (NB + 1));
   o->ntiles = take(sizeof(int32_t));
   o->tiles = take(sizeof(int2) * max_tiles);
@@ -1614,6 +1615,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->recs = take(sizeof(HostRec) * W * Gn);
   o->preq = take(sizeof(ReqRec) * (R > 0 ? R : 1));
   o->key = take(sizeof(int32_t) * (R > 0 ? R : 1));
+  o->off = take(sizeof(int32_t) * (R > 0 ? R : 1));
   o->total = off;
   o->NB = (int32_t)NB;
   o->tile = tile;
@@ -1718,7 +1720,6 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   a.max_tiles = lay.max_tiles;
   a.cnt = reinterpret_cast<int32_t *>(ws + lay.cnt);
   const int nb4 = (lay.NB + 3) & ~3;      // counters padded with zeros to whole int4
-  a.cur = a.cnt + nb4;
   a.bstart = reinterpret_cast<int32_t *>(ws + lay.bstart);
   a.n_tiles = reinterpret_cast<int32_t *>(ws + lay.ntiles);
   a.tiles = reinterpret_cast<int2 *>(ws + lay.tiles);
@@ -1727,10 +1728,11 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   a.recs = reinterpret_cast<HostRec *>(ws + lay.recs);
   a.preq = reinterpret_cast<ReqRec *>(ws + lay.preq);
   a.key = reinterpret_cast<int32_t *>(ws + lay.key);
+  a.off = reinterpret_cast<int32_t *>(ws + lay.off);
 
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int zb = (2 * nb4 + 255) / 256;
-  k_zero<<<zb < 1024 ? zb : 1024, 256, 0, st>>>(a.cnt, 2 * nb4);
+  const int zb = (nb4 + 255) / 256;
+  k_zero<<<zb < 1024 ? zb : 1024, 256, 0, st>>>(a.cnt, nb4);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int nbr = (a.R + kReqPerPrepBlock - 1) / kReqPerPrepBlock;
   const long long nrec = ((long long)a.W * a.G + kPrepBlock - 1) / kPrepBlock;
@@ -1741,7 +1743,7 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
     k_scan<<<1, 1024, lay.NB <= kScanLds ? sizeof(int) * lay.NB : 0, st>>>(a);
     if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   }
-  k_scatter<<<nbr, kPrepBlock, local ? 2 * sizeof(int) * lay.NB : 0, st>>>(a);
+  k_scatter<<<nbr, kPrepBlock, local ? sizeof(int) * lay.NB : 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int cpl = C <= 64 ? 1 : (C <= 128 ? 2 : 4);
   const int wpb = lay.waves_per_block;
