@@ -1449,110 +1449,74 @@ __global__ void __launch_bounds__(256) k_fleet(MigArgs a) {
   }
 }
 
-constexpr int kSrcPerWave = 2;
-constexpr int kMigChunk = 2048;   // destination records staged in LDS per pass
+constexpr int kMigSrcPerBlock = 2;   // sources per block; each source's destinations in 2 halves
 
-// Two sources per wavefront, four wavefronts per block; the 32-byte destination records are
-// staged in LDS in chunks (all of a thread's loads in flight at once), lanes span destinations.
+// Best (largest saving, then lowest destination) of two candidates.
+__device__ __forceinline__ void keep_best(float &v, int &d, int &k, float ov, int od, int ok) {
+  if (ov > v || (ov == v && od < d)) {
+    v = ov;
+    d = od;
+    k = ok;
+  }
+}
+
+// Four wavefronts per block: wavefront w scores source blockIdx.x * 2 + w / 2 against the
+// destinations of half w % 2, lanes spanning destinations, reading the 32-byte destination
+// records straight from the cache (the whole fleet's records, 32 B per GPU, stay in L2).  The
+// two halves' bests meet in LDS: largest saving, ties to the lowest destination.
 __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
   __shared__ float f3[32];
-  __shared__ int4 drec[kMigChunk];       // hbm, SM per-mille, level mask, k_d
-  __shared__ float2 drec2[kMigChunk];    // u_d, f[kd0]^3 * u_d
+  __shared__ float s_v[4];
+  __shared__ int s_d[4], s_k[4];
   if (threadIdx.x < 32) f3[threadIdx.x] = threadIdx.x < a.NF ? cube(a.freq_level[threadIdx.x]) : 0.f;
+  __syncthreads();
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = uniform(threadIdx.x >> 6);
-  const int s0 = (blockIdx.x * (blockDim.x / kWave) + wv) * kSrcPerWave;
-  int src[kSrcPerWave], remH[kSrcPerWave], remU[kSrcPerWave];
-  uint32_t fms[kSrcPerWave];
-  float us[kSrcPerWave];
-  bool any[kSrcPerWave];
-#pragma unroll
-  for (int q = 0; q < kSrcPerWave; ++q) {
-    src[q] = s0 + q;
-    const bool v = src[q] < a.G;
-    const int s = v ? src[q] : 0;
-    const long long rh = (long long)a.hbm_cap - a.hbm[s];
-    const long long ru = (long long)a.sm_cap - a.smpm[s];
-    any[q] = v && rh >= (long long)INT_MIN && ru >= (long long)INT_MIN;
-    remH[q] = (int)(rh > INT_MAX ? INT_MAX : (rh < INT_MIN ? INT_MIN : rh));
-    remU[q] = (int)(ru > INT_MAX ? INT_MAX : (ru < INT_MIN ? INT_MIN : ru));
-    const v4i x = a.drec[2 * s], y = a.drec[2 * s + 1];
-    fms[q] = v ? (uint32_t)x.z : 0u;
-    us[q] = __int_as_float(y.x);
-  }
-  float bs[kSrcPerWave];
-  int bd[kSrcPerWave], bk[kSrcPerWave];
-#pragma unroll
-  for (int q = 0; q < kSrcPerWave; ++q) {
-    bs[q] = -kInf;
-    bd[q] = INT_MAX;
-    bk[q] = -1;
-  }
-  for (int d0 = 0; d0 < a.G; d0 += kMigChunk) {
-    const int n = min(kMigChunk, a.G - d0);
-    __syncthreads();
-    constexpr int U = kMigChunk / 256;
-    v4i x[U], y[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int i = u * 256 + threadIdx.x;
-      if (i < n) {
-        x[u] = a.drec[2 * (d0 + i)];
-        y[u] = a.drec[2 * (d0 + i) + 1];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int i = u * 256 + threadIdx.x;
-      if (i < n) {
-        drec[i] = make_int4(x[u].x, x[u].y, x[u].z, x[u].w);
-        drec2[i] = make_float2(__int_as_float(y[u].x), __int_as_float(y[u].y));
-      }
-    }
-    __syncthreads();
-    if (s0 >= a.G) continue;
-    for (int i = lane; i < n; i += kWave) {
-      const int d = d0 + i;
-      const int4 r = drec[i];
-      const float2 r2 = drec2[i];
-      const uint32_t fmd = (uint32_t)r.z;
-      const float kd = __int_as_float(r.w);
-#pragma unroll
-      for (int q = 0; q < kSrcPerWave; ++q) {
-        const uint32_t f = fms[q] & fmd;
-        const bool ok = any[q] && d != src[q] && r.x <= remH[q] && r.y <= remU[q] && f != 0u;
-        const int k = __builtin_ctz(f | 0x80000000u);
-        const float added = f3[k] * (us[q] + r2.x) - r2.y;
-        const float sv = fmaf(-kd, added, a.p0);
-        const bool better = ok && sv > bs[q];
-        bs[q] = better ? sv : bs[q];
-        bd[q] = better ? d : bd[q];
-        bk[q] = better ? k : bk[q];
-      }
+  const int src = blockIdx.x * kMigSrcPerBlock + (wv >> 1);
+  const bool valid = src < a.G;
+  const int s = valid ? src : 0;
+  const long long rh = (long long)a.hbm_cap - a.hbm[s];
+  const long long ru = (long long)a.sm_cap - a.smpm[s];
+  const bool any = valid && rh >= (long long)INT_MIN && ru >= (long long)INT_MIN;
+  const int remH = (int)(rh > INT_MAX ? INT_MAX : (rh < INT_MIN ? INT_MIN : rh));
+  const int remU = (int)(ru > INT_MAX ? INT_MAX : (ru < INT_MIN ? INT_MIN : ru));
+  const v4i sx = ro(a.drec)[2 * (size_t)s], sy = ro(a.drec)[2 * (size_t)s + 1];
+  const uint32_t fms = any ? (uint32_t)sx.z : 0u;
+  const float us = __int_as_float(sy.x);
+  const int per = (a.G + 1) >> 1;
+  const int lo = (wv & 1) * per, hi = min(a.G, lo + per);
+  float bs = -kInf;
+  int bd = INT_MAX, bk = -1;
+  if (fms != 0u) {
+#pragma unroll 4
+    for (int d = lo + lane; d < hi; d += kWave) {
+      const v4i r = a.drec[2 * (size_t)d], r2 = a.drec[2 * (size_t)d + 1];
+      const uint32_t f = fms & (uint32_t)r.z;
+      const bool ok = d != src && r.x <= remH && r.y <= remU && f != 0u;
+      const int k = __builtin_ctz(f | 0x80000000u);
+      const float added = f3[k] * (us + __int_as_float(r2.x)) - __int_as_float(r2.y);
+      const float sv = fmaf(-__int_as_float(r.w), added, a.p0);
+      const bool better = ok && sv > bs;
+      bs = better ? sv : bs;
+      bd = better ? d : bd;
+      bk = better ? k : bk;
     }
   }
-  if (s0 >= a.G) return;
 #pragma unroll
-  for (int q = 0; q < kSrcPerWave; ++q) {
-    float v = bs[q];
-    int d = bd[q], k = bk[q];
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      const float ov = __shfl_xor(v, off, kWave);
-      const int od = __shfl_xor(d, off, kWave);
-      const int ok2 = __shfl_xor(k, off, kWave);
-      if (ov > v || (ov == v && od < d)) {
-        v = ov;
-        d = od;
-        k = ok2;
-      }
-    }
-    if (lane == 0 && src[q] < a.G) {
-      const bool found = d != INT_MAX;
-      a.best_dst[src[q]] = found ? d : -1;
-      a.saving[src[q]] = found ? v : -kInf;
-      a.level[src[q]] = found ? k : -1;
-    }
+  for (int off = 32; off >= 1; off >>= 1)
+    keep_best(bs, bd, bk, __shfl_xor(bs, off, kWave), __shfl_xor(bd, off, kWave), __shfl_xor(bk, off, kWave));
+  if (lane == 0) {
+    s_v[wv] = bs;
+    s_d[wv] = bd;
+    s_k[wv] = bk;
+  }
+  __syncthreads();
+  if ((wv & 1) == 0 && lane == 0 && valid) {
+    keep_best(bs, bd, bk, s_v[wv + 1], s_d[wv + 1], s_k[wv + 1]);
+    const bool found = bd != INT_MAX;
+    a.best_dst[src] = found ? bd : -1;
+    a.saving[src] = found ? bs : -kInf;
+    a.level[src] = found ? bk : -1;
   }
 }
 
@@ -1829,9 +1793,8 @@ festina_status festina_score_migrations(const festina_lut *L, const festina_flee
   hipStream_t st = static_cast<hipStream_t>(stream);
   k_fleet<<<(a.G + 3) / 4, 256, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  const int per_block = 4 * kSrcPerWave;
   if (mark(2, st) != hipSuccess) return FESTINA_ERR_DEVICE;
-  k_migrate<<<(a.G + per_block - 1) / per_block, 256, 0, st>>>(a);
+  k_migrate<<<(a.G + kMigSrcPerBlock - 1) / kMigSrcPerBlock, 256, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess || mark(3, st) != hipSuccess) return FESTINA_ERR_DEVICE;
   return FESTINA_OK;
 }
