@@ -206,6 +206,27 @@ def timed_calls(hip, torch, fn, calls, warmup):
     return ms
 
 
+def timed_batch(hip, torch, fn, calls, head=None):
+    """Mean duration (ms) of fn() over `calls` back-to-back calls, one HIP event pair around
+    the batch.  `head` enqueues work first so that the device is still busy while the host
+    enqueues the batch (the calls then run back to back, not at the host's pace)."""
+    fn()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream().cuda_stream
+    a, b = hip.event(), hip.event()
+    if head is not None:
+        head()
+    hip.record(a, st)
+    for _ in range(calls):
+        fn()
+    hip.record(b, st)
+    torch.cuda.synchronize()
+    ms = hip.elapsed_ms(a, b) / calls
+    hip.destroy(a)
+    hip.destroy(b)
+    return ms
+
+
 def preferred_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
     """Preferred configurations of every LLM instance (one launch) and the fleet's EWR
     (two launches): durations from HIP events around each call, roofline position, and
@@ -427,7 +448,7 @@ def main():
 
     # Timed steps: placement on the current stream, consolidation on the side stream; events
     # are recorded around the scoring kernel only (each record costs a few microseconds of
-    # stream time); the migration kernel is timed afterwards on its own.
+    # stream time); the consolidation call is timed afterwards on its own, as a batch.
     K = args.steps
     evs = [[hip.event() for _ in range(2)] for _ in range(K)]
     torch.cuda.synchronize()
@@ -443,16 +464,7 @@ def main():
     for e in evs:
         for x in e:
             hip.destroy(x)
-    pevs = [[hip.event() for _ in range(2)] for _ in range(50)]
-    for e in pevs:
-        F.festina_set_timing_events(None, None, e[0], e[1])
-        dm.run()
-    torch.cuda.synchronize()
-    F.festina_set_timing_events()
-    pairs_ms = float(np.mean([hip.elapsed_ms(e[0], e[1]) for e in pevs]))
-    for e in pevs:
-        for x in e:
-            hip.destroy(x)
+    mig_ms = timed_batch(hip, torch, dm.run, 50, head=lambda: [dp.run() for _ in range(4)])
 
     step_s = (t1 - t0) / K
     value = (n_cand + n_pairs) / step_s
@@ -495,8 +507,8 @@ def main():
             "kernel_ms": score_ms,
             "hbm_frac_algorithmic": placement_bytes(place) / (score_ms * 1e-3) / HBM_PEAK,
         },
-        "kernels_ms": {"k_score": score_ms, "k_migrate": pairs_ms,
-                       "migration_pairs_per_s_kernel": n_pairs / (pairs_ms * 1e-3)},
+        "kernels_ms": {"k_score": score_ms, "migration_call": mig_ms,
+                       "migration_pairs_per_s_call": n_pairs / (mig_ms * 1e-3)},
         "cpu_baseline": None,
         "next_rows": {"sweep": sweep_row(F, W, hip, torch, not args.no_cpu_baseline),
                       "preferred": preferred_row(F, W, hip, torch, not args.no_cpu_baseline),
@@ -551,7 +563,13 @@ def per_config(F, W, hip, torch):
                 hip.destroy(e)
         F.festina_set_timing_events()
         cm, km = float(np.median(call_ms)), float(np.median(kern_ms))
-        print(json.dumps({"config": cfg, "work": work, "call_ms": cm, "kernel_ms": km,
+        timed = "k_score (HIP events around the kernel inside the library)"
+        if cfg == 5:
+            # an event between the two migration kernels costs several microseconds of stream
+            # time, more than the kernel itself: time a batch of whole calls instead
+            km = timed_batch(hip, torch, dev.run, 50)
+            timed = "k_fleet + k_migrate (batch of 50 calls, one event pair)"
+        print(json.dumps({"config": cfg, "work": work, "call_ms": cm, "kernel_ms": km, "kernel_timed": timed,
                           "evals_per_s_call": work / (cm * 1e-3), "evals_per_s_kernel": work / (km * 1e-3),
                           "valu_frac_kernel": ops / (km * 1e-3) / VALU_PEAK}), flush=True)
 
