@@ -1419,27 +1419,67 @@ struct MigArgs {
 
 // One wavefront per GPU: lane k tests frequency level k (NF <= 32) for each instance, a
 // ballot turns the tests into that instance's level mask, and the GPU's mask is the AND.
+// With at most kFleetUnroll instances per GPU every instance's fields, then every table
+// value, are requested before the first is used (two memory round trips per GPU).
+constexpr int kFleetUnroll = 4;
+
+__device__ __forceinline__ bool inst_ok(int m, int j, int B, int pt, const MigArgs &a) {
+  return m >= 0 && m < a.M && j >= 0 && j < a.NS && B >= 0 && pt >= 0;
+}
+
+// Level mask of instance (m, j, B, pt) with SLOs (st, sb): lane k's test, as a ballot.
+__device__ __forceinline__ uint32_t inst_mask(const MigArgs &a, int lane, int m, int j, int B, int pt, float st,
+                                              float sb) {
+  const int bb = B + 1 > kRows ? kRows : B + 1;
+  const int prow = pt == 0 ? bb - 1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
+  const float *pr = a.pf + (((size_t)m * kRows + prow) * a.NS + j) * a.NF;
+  const float *dr = a.dc + (((size_t)m * kRows + (bb - 1)) * a.NS + j) * a.NF;
+  const int k = lane < a.NF ? lane : 0;
+  const bool pass = lane < a.NF && pr[k] < st && dr[k] < sb;
+  return (uint32_t)__ballot(pass);
+}
+
 __global__ void __launch_bounds__(256) k_fleet(MigArgs a) {
   const int g = blockIdx.x * 4 + uniform(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
   if (g >= a.G) return;
   const int n = ro(a.n_inst)[g];
   uint32_t fm = (n >= 1 && n <= a.K) ? (a.NF >= 32 ? 0xffffffffu : ((1u << a.NF) - 1u)) : 0u;
-  for (int i = 0; i < n && i < a.K && fm; ++i) {
-    const size_t at = (size_t)g * a.K + i;
-    const int m = ro(a.inst_model)[at], j = ro(a.inst_sm)[at], B = ro(a.inst_batch)[at];
-    const int pt = ro(a.inst_prompt)[at];
-    if (m < 0 || m >= a.M || j < 0 || j >= a.NS || B < 0 || pt < 0) {
-      fm = 0;
-      break;
+  if (a.K <= kFleetUnroll) {
+    int m[kFleetUnroll], j[kFleetUnroll], B[kFleetUnroll], pt[kFleetUnroll];
+    float st[kFleetUnroll], sb[kFleetUnroll];
+#pragma unroll
+    for (int i = 0; i < kFleetUnroll; ++i) {
+      const size_t at = (size_t)g * a.K + (i < n ? i : 0);
+      m[i] = ro(a.inst_model)[at];
+      j[i] = ro(a.inst_sm)[at];
+      B[i] = ro(a.inst_batch)[at];
+      pt[i] = ro(a.inst_prompt)[at];
+      st[i] = ro(a.inst_slo_ttft)[at];
+      sb[i] = ro(a.inst_slo_tbt)[at];
     }
-    const int bb = B + 1 > kRows ? kRows : B + 1;
-    const int prow = pt == 0 ? bb - 1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
-    const float *pr = a.pf + (((size_t)m * kRows + prow) * a.NS + j) * a.NF;
-    const float *dr = a.dc + (((size_t)m * kRows + (bb - 1)) * a.NS + j) * a.NF;
-    const float st = ro(a.inst_slo_ttft)[at], sb = ro(a.inst_slo_tbt)[at];
-    const bool pass = lane < a.NF && pr[lane < a.NF ? lane : 0] < st && dr[lane < a.NF ? lane : 0] < sb;
-    fm &= (uint32_t)__ballot(pass);
+    // every instance's mask without an early exit (an AND that reached 0 stays 0), so that
+    // no instance's table loads wait for another's ballot
+#pragma unroll
+    for (int i = 0; i < kFleetUnroll; ++i) {
+      if (i >= n) continue;
+      if (!inst_ok(m[i], j[i], B[i], pt[i], a)) {   // never read the tables at a bad index
+        fm = 0;
+        continue;
+      }
+      fm &= inst_mask(a, lane, m[i], j[i], B[i], pt[i], st[i], sb[i]);
+    }
+  } else {
+    for (int i = 0; i < n && i < a.K && fm; ++i) {
+      const size_t at = (size_t)g * a.K + i;
+      const int m = ro(a.inst_model)[at], j = ro(a.inst_sm)[at], B = ro(a.inst_batch)[at];
+      const int pt = ro(a.inst_prompt)[at];
+      if (!inst_ok(m, j, B, pt, a)) {
+        fm = 0;
+        break;
+      }
+      fm &= inst_mask(a, lane, m, j, B, pt, ro(a.inst_slo_ttft)[at], ro(a.inst_slo_tbt)[at]);
+    }
   }
   if (lane == 0) {
     const float u = a.util[g];
