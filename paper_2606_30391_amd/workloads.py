@@ -313,13 +313,12 @@ def make_tiny_placement(rng: np.random.Generator, R=None, G=None, M=None, NS=Non
 
 
 def make_tiny_fleet(rng: np.random.Generator, G=None, M=None, NS=None, NF=None,
-                    loose=False, huge_budget=False) -> dict:
-    """Small random consolidation fleet for brute-force comparison."""
+                    loose=False, huge_budget=False, K=MAX_INST) -> dict:
+    """Small random consolidation fleet for brute-force comparison (K instance slots per GPU)."""
     G = int(rng.integers(2, 7)) if G is None else G
     M = int(rng.integers(1, 4)) if M is None else M
     NS = int(rng.integers(1, 5)) if NS is None else NS
     NF = int(rng.integers(1, 9)) if NF is None else NF
-    K = MAX_INST
     s, f = sm_levels(NS), freq_levels(NF)
     pf = rng.uniform(5.0, 60.0, (M, N_ROWS, NS, NF)).astype(np.float32)
     dc = rng.uniform(2.0, 40.0, (M, N_ROWS, NS, NF)).astype(np.float32)

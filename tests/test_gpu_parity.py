@@ -208,6 +208,14 @@ def test_migration_shapes(G, NF):
     parity_mig(W.make_tiny_fleet(rng, G=G, M=3, NS=4, NF=NF), label=f"tiny G={G} NF={NF}")
 
 
+@pytest.mark.parametrize("K", [1, 6])
+def test_migration_instance_slots(K):
+    """Fleets with one instance slot per GPU, and with more slots than the fleet-mask kernel
+    unrolls (its loop form)."""
+    rng = np.random.default_rng(400 + K)
+    parity_mig(W.make_tiny_fleet(rng, G=150, M=4, NS=4, NF=16, K=K), label=f"tiny G=150 K={K}")
+
+
 def test_migration_ties_and_bad_elements():
     rng = np.random.default_rng(31)
     inp = W.make_tiny_fleet(rng, G=40, M=2, NS=3, NF=6, loose=True, huge_budget=True)

@@ -46,6 +46,18 @@ def test_brute_force_random(seed):
                 assert abs(s1[s] - s2[s]) <= 1e-12 * max(abs(s2[s]), 1.0)
 
 
+@pytest.mark.parametrize("K", [1, 2, 6])
+def test_brute_force_instance_slots(K):
+    rng = np.random.default_rng(2200 + K)
+    for _ in range(30):
+        inp = W.make_tiny_fleet(rng, K=K)
+        b1, s1, k1 = oracle.score_migrations(inp)
+        b2, s2, k2 = brute_migrations(inp)
+        assert np.array_equal(k1 >= 0, k2 >= 0)
+        assert np.array_equal(b1, b2) and np.array_equal(k1, k2)
+        assert np.allclose(s1, s2, rtol=1e-12, atol=1e-12) or np.array_equal(s1, s2)
+
+
 def test_brute_force_bad_elements():
     rng = np.random.default_rng(2100)
     for _ in range(30):
