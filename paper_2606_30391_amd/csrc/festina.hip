@@ -3,12 +3,13 @@
 //
 // Placement pipeline (one call, five launches on the caller's stream):
 //   k_zero      clear the bucket counters
-//   k_prep      requests: validity, 5% output pad, prompt bucket, bucket key (wave, model,
-//                 has-prompt) and a counter; hosts: per-model list of hosting GPUs in
-//                 ascending order; GPU records: per (wave, GPU) the post-admission batch
-//                 row, k_g * u_g and the SM caps
-//   k_scan      one block: bucket offsets and the tile table
-//   k_scatter   requests grouped by bucket
+//   k_prep      requests: validity, bucket key (wave, model, has-prompt), the bucket count
+//                 and the request's position within its bucket; hosts: per-model list of
+//                 hosting GPUs in ascending order; GPU records: per (wave, GPU) the
+//                 post-admission batch row, k_g * u_g and the SM caps
+//   k_scan      one block: bucket offsets and the tile table (only with more buckets than
+//                 an LDS histogram holds)
+//   k_scatter   request records (5% output pad, prompt bucket, SLOs) grouped by bucket
 //   k_score     one workgroup per tile (requests of one bucket): the model's decode table is
 //                 staged in LDS; each wave scores Q requests at once, lanes spanning the
 //                 (SM level, frequency level) cells, looping over the hosting GPUs; the
@@ -17,8 +18,9 @@
 // Migration pipeline:
 //   k_fleet     per GPU: bitmask of frequency levels at which all instances meet their SLOs,
 //                 its lowest level and the dynamic-power baseline f[kd0]^3 * u
-//   k_migrate   one wavefront per group of sources, lanes spanning destinations; fused
-//                 per-source argmax with lowest-destination tie-break
+//   k_migrate   two sources per block, each source's destinations split over two
+//                 wavefronts, lanes spanning destinations; fused per-source argmax with
+//                 lowest-destination tie-break
 //
 // Exactness: every SLO and budget test compares a table entry with an SLO, or integers,
 // so it is decided bit-identically to any other correct implementation.  Energies are
