@@ -10,6 +10,8 @@
 """
 import numpy as np
 import pytest
+from hypothesis import given, settings
+from hypothesis import strategies as st
 
 import oracle
 from brute import brute_placements, padded_out as bpad, prompt_row as brow
@@ -74,11 +76,21 @@ def _agree(inp):
             assert ok and abs(e - e1[r]) <= 1e-12 * abs(e1[r])
 
 
-@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("seed", range(10))
 def test_brute_force_random(seed):
+    """2,000 random tiny instances (R <= 8, G <= 5, NS <= 4, NF <= 6, M <= 3)."""
     rng = np.random.default_rng(1000 + seed)
-    for _ in range(60):
+    for _ in range(200):
         _agree(W.make_tiny_placement(rng))
+
+
+@settings(max_examples=300, deadline=None)
+@given(seed=st.integers(0, 2**32 - 1), caps=st.booleans(), ties=st.booleans(), nan_cells=st.booleans(),
+       waves=st.integers(1, 2))
+def test_brute_force_search(seed, caps, ties, nan_cells, waves):
+    """Hypothesis explores generator seeds and flags (and shrinks a failure to a small one)."""
+    inp = W.make_tiny_placement(np.random.default_rng(seed), caps=caps, ties=ties, nan_cells=nan_cells, W=waves)
+    _agree(inp)
 
 
 def test_brute_force_ties():
