@@ -62,6 +62,7 @@ OPS_PER_CANDIDATE = 1.5
 OPS_PER_PAIR = 15
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_score_config4_traffic.json")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_score_config4_counters.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "festina.hip")
 SWEEP_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sweep_traffic.json")
 SWEEP_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "sweep.hip")
@@ -185,6 +186,19 @@ def load_traffic(path=TRAFFIC_FILE, src=KERNEL_SRC):
     if d.get("kernel_src_sha256_16") != src_hash(src):
         return None
     return d.get("hbm_bytes_per_launch")
+
+
+def load_counters(path=COUNTERS_FILE, src=KERNEL_SRC):
+    """VALU issue figures of the scoring kernel from the committed counter run, or None when
+    the kernel source changed since it was taken."""
+    try:
+        d = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_src_sha256_16") != src_hash(src):
+        return None
+    return {"valu_issue_busy": d["valu_issue_busy"],
+            "valu_lane_ops_per_distinct_candidate": d["valu_lane_ops_per_distinct_candidate"]}
 
 
 def timed_calls(hip, torch, fn, calls, warmup):
@@ -506,6 +520,7 @@ def main():
             "candidates_counted": "distinct (capped GPUs' repeated SM levels excluded)",
             "kernel_ms": score_ms,
             "hbm_frac_algorithmic": placement_bytes(place) / (score_ms * 1e-3) / HBM_PEAK,
+            "counters": load_counters(),
         },
         "kernels_ms": {"k_score": score_ms, "migration_call": mig_ms,
                        "migration_pairs_per_s_call": n_pairs / (mig_ms * 1e-3)},
