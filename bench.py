@@ -68,6 +68,10 @@ SWEEP_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sweep_traffic.json")
 SWEEP_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "sweep.hip")
 TRANSFER_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_transfer_costs_traffic.json")
 TRANSFER_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "transfer.hip")
+DISPATCH_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_dispatch_traffic.json")
+DISPATCH_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "dispatch.hip")
+PREFERRED_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_preferred_traffic.json")
+PREFERRED_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "preferred.hip")
 # Sweep, per (task, SM level, frequency level) cell: one compare of the latency with the
 # slack; per (task, frequency level): the SM share add and two FMAs (power, energy).
 OPS_PER_SWEEP_CELL = 1
@@ -261,7 +265,7 @@ def preferred_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
         "cells_per_s": cells / (pref_ms * 1e-3),
         "roofline": {"kernel": "k_preferred", "bound": "hbm", "achieved": nbytes / (pref_ms * 1e-3) / 1e9,
                      "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": nbytes / (pref_ms * 1e-3) / HBM_PEAK,
-                     "traffic": None, "algorithmic_bytes": nbytes},
+                     "traffic": load_traffic(PREFERRED_TRAFFIC_FILE, PREFERRED_SRC), "algorithmic_bytes": nbytes},
         "cpu_baseline": None,
     }
     if with_cpu:
@@ -298,7 +302,7 @@ def dispatch_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
         "requests": R, "evaluations": evals, "kernel_ms": ms, "evaluations_per_s": evals / (ms * 1e-3),
         "roofline": {"kernel": "k_dispatch", "bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9,
                      "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / HBM_PEAK,
-                     "traffic": None, "algorithmic_bytes": nbytes},
+                     "traffic": load_traffic(DISPATCH_TRAFFIC_FILE, DISPATCH_SRC), "algorithmic_bytes": nbytes},
         "cpu_baseline": None,
     }
     if with_cpu:
