@@ -105,6 +105,22 @@ def test_large_configs_full_size_sampled(cfg, extra):
         assert np.all(fe[inp["meta"]["planted"]] == 0)
 
 
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_large_configs_every_request(cfg):
+    """Every request of the full-size configuration against the oracle (run on chunks of
+    the requests in parallel processes)."""
+    import oracle_pool
+    inp = W.make_placement(cfg)
+    R = inp["requests"]["n_requests"]
+    say(f"[gpu] placement cfg{cfg} full size, every request: R={R}")
+    got = run_place(inp)
+    ref = oracle_pool.score_placements(inp)
+    sel = np.arange(R)
+    rep = check_placements(inp, sel, ref, got)
+    say(f"      {rep}")
+    assert rep.ok, str(rep)
+
+
 def test_config5_full():
     parity_mig(W.make_fleet(), label="cfg5 full")
 
