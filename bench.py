@@ -202,7 +202,8 @@ def load_counters(path=COUNTERS_FILE, src=KERNEL_SRC):
     if d.get("kernel_src_sha256_16") != src_hash(src):
         return None
     return {"valu_issue_busy": d["valu_issue_busy"],
-            "valu_lane_ops_per_distinct_candidate": d["valu_lane_ops_per_distinct_candidate"]}
+            "valu_lane_ops_per_distinct_candidate": d["valu_lane_ops_per_distinct_candidate"],
+            "sclk_ghz_effective": d.get("sclk_ghz_effective")}
 
 
 def timed_calls(hip, torch, fn, calls, warmup):
