@@ -203,7 +203,7 @@ def load_counters(path=COUNTERS_FILE, src=KERNEL_SRC):
         return None
     return {"valu_issue_busy": d["valu_issue_busy"],
             "valu_lane_ops_per_distinct_candidate": d["valu_lane_ops_per_distinct_candidate"],
-            "sclk_ghz_effective": d.get("sclk_ghz_effective")}
+            "sclk_ghz_effective": d["sclk_ghz_effective"]}
 
 
 def timed_calls(hip, torch, fn, calls, warmup):
@@ -422,6 +422,20 @@ def oracle_all_cores(place_inp, sel, workers):
     return t1 - t0
 
 
+def host_cpu():
+    """The host's CPU model (first `model name` of /proc/cpuinfo) and its logical CPU counts."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable": len(os.sched_getaffinity(0))}
+
+
 def cpu_baseline(place_inp, fleet_inp, gpu_place, gpu_mig, stride=4):
     import oracle
     R = place_inp["requests"]["n_requests"]
@@ -449,6 +463,7 @@ def cpu_baseline(place_inp, fleet_inp, gpu_place, gpu_mig, stride=4):
         "all_cores": {"value": cand / t_all, "cores": workers,
                       "sample": f"the same {len(sel)} placement requests in chunks over {workers} processes "
                                 f"({t_all:.2f} s), placement only"},
+        "host": host_cpu(),
         "agreement": {"placement_flags_equal": float(np.mean(of == gf[sel])),
                       "placement_choice_equal": float(np.mean(oc == gc[sel])),
                       "migration_dst_equal": float(np.mean(ob == gb))},
@@ -528,6 +543,7 @@ def main():
     gpu_place = dp.results()
     gpu_mig = dm.results()
 
+    counters = load_counters()
     line = {
         "metric": "candidate evaluations/sec + % of HBM/VALU roofline, 1 MI355X",
         "value": value,
@@ -562,9 +578,13 @@ def main():
             "candidates_counted": "distinct (capped GPUs' repeated SM levels excluded)",
             "kernel_ms": score_ms,
             "hbm_frac_algorithmic": placement_bytes(place) / (score_ms * 1e-3) / HBM_PEAK,
-            "counters": load_counters(),
+            "counters": counters,
+            # the same fraction against the peak at the engine clock the counter run measured
+            "frac_at_measured_sclk": (None if counters is None else
+                                      achieved / (VALU_PEAK * counters["sclk_ghz_effective"] * 1e9 / SCLK_HZ)),
         },
-        "kernels_ms": {"k_score": score_ms, "migration_call": mig_ms,
+        "kernels_ms": {"k_score": score_ms, "k_score_candidates_per_s": n_cand / (score_ms * 1e-3),
+                       "migration_call": mig_ms,
                        "migration_pairs_per_s_call": n_pairs / (mig_ms * 1e-3)},
         "cpu_baseline": None,
         "next_rows": {"sweep": sweep_row(F, W, hip, torch, not args.no_cpu_baseline),

@@ -55,8 +55,15 @@ def test_short_run_prints_one_line_with_the_contract_fields():
     assert abs(r["achieved"] * 1e12 * r["kernel_ms"] * 1e-3
                - r["ops_per_candidate"] * cfg["distinct_placement_candidates"]) < 1e-3 * r["achieved"] * 1e12 * r["kernel_ms"] * 1e-3
     assert r["traffic"] is None or r["traffic"] > 0
+    if r["counters"] is not None:
+        clk = r["counters"]["sclk_ghz_effective"]
+        assert 0.5 < clk < 3.0
+        assert abs(r["frac_at_measured_sclk"] - r["frac"] * 2.4 / clk) < 1e-9
+    ks = b["kernels_ms"]
+    assert abs(ks["k_score_candidates_per_s"] * ks["k_score"] * 1e-3 / cfg["placement_candidates"] - 1) < 1e-6
     c = b["cpu_baseline"]
     assert c["kind"] == "oracle" and c["cores"] >= 1 and c["value"] > 0 and c["unit"] == b["unit"]
     assert c["agreement"]["placement_flags_equal"] == 1.0 and c["agreement"]["migration_dst_equal"] == 1.0
+    assert c["host"]["nproc"] >= c["host"]["usable"] >= 1
     for row in ("sweep", "preferred", "dispatch", "transfer"):
         assert row in b["next_rows"] and b["next_rows"][row]["roofline"]["frac"] > 0
