@@ -153,18 +153,33 @@ __device__ __forceinline__ ReqRec load_req_lane(const PlaceArgs &a, int pos) {
 }
 
 // ------------------------------------------------------------------ prologue kernels
+// Inclusive prefix sum over a wavefront.
+__device__ __forceinline__ int wave_scan(int v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int o = __shfl_up(v, off, kWave);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
 __global__ void k_zero(int32_t *p, int32_t n) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
-// Validity and bucket key (wave, model, has-prompt) of request r.  Returns the key, or -1
-// (and writes the infeasible result) for an invalid request.
-__device__ __forceinline__ int prep_request(const PlaceArgs &a, int r) {
-  const int m = a.model[r];
-  const int w = a.wave ? a.wave[r] : 0;
-  const int pt = a.prompt[r];
-  const int pr = a.pred[r];
-  const bool ok = m >= 0 && m < a.M && w >= 0 && w < a.W && pt >= 0 && pr >= 0;
+// The fields of request r that decide its bucket.
+struct ReqKeyFields {
+  int m, w, pt, pr;
+};
+__device__ __forceinline__ ReqKeyFields load_key_fields(const PlaceArgs &a, int r) {
+  return ReqKeyFields{a.model[r], a.wave ? a.wave[r] : 0, a.prompt[r], a.pred[r]};
+}
+
+// Validity and bucket key (wave, model, has-prompt) of request r from its fields.  Returns
+// the key, or -1 (and writes the infeasible result) for an invalid request.
+__device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const ReqKeyFields &f) {
+  const bool ok = f.m >= 0 && f.m < a.M && f.w >= 0 && f.w < a.W && f.pt >= 0 && f.pr >= 0;
   if (!ok) {
     a.key[r] = -1;
     a.choice[r] = -1;
@@ -172,10 +187,12 @@ __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r) {
     a.energy[r] = kInf;
     return -1;
   }
-  const int k = ((w * a.M + m) << 1) | (pt == 0 ? 1 : 0);
+  const int k = ((f.w * a.M + f.m) << 1) | (f.pt == 0 ? 1 : 0);
   a.key[r] = k;
   return k;
 }
+
+__device__ const int8_t kNoCap = 0;                // read in place of absent cap arrays
 
 constexpr int kReqPerPrepBlock = 4 * kPrepBlock;  // requests per request block of k_prep / k_scatter
 constexpr int kHistMax = 8192;                    // buckets counted in LDS (else global atomics)
@@ -190,16 +207,23 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
   const int b = blockIdx.x;
   if (b < nbr) {
     const bool local = a.NB <= kHistMax;
+    constexpr int U = kReqPerPrepBlock / kPrepBlock;
+    // every request's fields are requested before the first is used (one memory round trip);
+    // a thread past the last request reads the last one (R >= 1 in a request block) and
+    // drops it
+    ReqKeyFields f[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      f[u] = load_key_fields(a, min(b * kReqPerPrepBlock + u * kPrepBlock + (int)threadIdx.x, a.R - 1));
     if (local) {
       for (int k = threadIdx.x; k < a.NB; k += kPrepBlock) hist[k] = 0;
       __syncthreads();
     }
-    constexpr int U = kReqPerPrepBlock / kPrepBlock;
     int key[U], pos[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = b * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
-      key[u] = r < a.R ? prep_request(a, r) : -1;
+      key[u] = r < a.R ? prep_request(a, r, f[u]) : -1;
       pos[u] = key[u] >= 0 ? atomicAdd(local ? &hist[key[u]] : &a.cnt[key[u]], 1) : 0;
     }
     if (local) {
@@ -221,9 +245,9 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
     const int m = b - nbr;
     __shared__ int wsum[kPrepBlock / kWave];
     __shared__ int base_s;
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x >> 6;
     if (threadIdx.x == 0) base_s = 0;
     __syncthreads();
-    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x >> 6;
     for (int g0 = 0; g0 < a.G; g0 += kPrepBlock) {
       const int g = g0 + threadIdx.x;
       const bool has = g < a.G && ((a.resident[(size_t)g * a.words + (m >> 5)] >> (m & 31)) & 1u);
@@ -248,29 +272,23 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
   const long long i = (long long)(b - nbr - a.M) * kPrepBlock + threadIdx.x;
   if (i >= (long long)a.W * a.G) return;
   const int g = (int)(i % a.G);
+  // all four loads in flight together: without caps the cap loads read a constant in
+  // device memory and are replaced by NS - 1
   const int B = a.batch[i];
-  const int cp = a.cap_pf ? (int)a.cap_pf[g] : a.NS - 1;
-  const int cd = a.cap_dc ? (int)a.cap_dc[g] : a.NS - 1;
+  const float kd = a.kdyn[g];
+  const int8_t cpv = *(a.cap_pf ? a.cap_pf + g : &kNoCap);
+  const int8_t cdv = *(a.cap_dc ? a.cap_dc + g : &kNoCap);
+  const int cp = a.cap_pf ? (int)cpv : a.NS - 1;
+  const int cd = a.cap_dc ? (int)cdv : a.NS - 1;
   HostRec rec;
   const bool ok = B >= 0 && cp >= 0 && cp < a.NS && cd >= 0 && cd < a.NS;
   const int bb = B + 1 > kRows ? kRows : B + 1;
   rec.row_off = ok ? (bb - 1) * a.C : -1;
   // u = b / 32 is exact; a GPU without candidates gets NaN so that every energy on it is NaN
-  rec.kappa = ok ? a.kdyn[g] * ((float)bb * 0.03125f) : kMask;
+  rec.kappa = ok ? kd * ((float)bb * 0.03125f) : kMask;
   rec.caps = ok ? (cp | (cd << 8)) : 0;
   rec.pad = 0;
   a.recs[i] = rec;
-}
-
-// Inclusive prefix sum over a wavefront.
-__device__ __forceinline__ int wave_scan(int v) {
-  const int lane = threadIdx.x & (kWave - 1);
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int o = __shfl_up(v, off, kWave);
-    if (lane >= off) v += o;
-  }
-  return v;
 }
 
 constexpr int kScanLds = 16384;   // bucket counts staged in LDS by k_scan (64 KB)
@@ -367,21 +385,38 @@ __device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
 
 // Exclusive scans of the bucket counts (requests and tiles) inside one block of k_scatter,
 // into the LDS array `start`.  Thread t holds buckets [t*per, t*per + per), per a multiple
-// of 4 (at most 32), read as up to 8 int4 loads that are all in flight before the first use;
-// the counter array is padded to a multiple of 4 with zeros.  Every block scans all buckets
-// (a few KB from L2); bucket i's global start and tiles are written by block i mod grid, so
-// the tile table is spread over the grid, and block 0 writes the totals.
-__device__ void block_scan_buckets(const PlaceArgs &a, int *start) {
-  __shared__ int s_c[kPrepBlock / kWave];
-  __shared__ int s_t[kPrepBlock / kWave];
-  constexpr int V = kHistMax / kPrepBlock / 4;
+// of 4 (at most 32), loaded by load_scan_counts as 8 int4 loads that are all in flight
+// before the first use; the counter array is padded to a multiple of 4 with zeros.  Every block scans all buckets
+// (a few KB from L2); the global starts and tiles of thread t's buckets are written by block
+// t mod grid, so the tile table is spread over the grid, and block 0 writes the totals.
+constexpr int kScanChunks = kHistMax / kPrepBlock / 4;   // int4 chunks of counts per thread
+
+// Thread t's bucket range [lo, hi) of the block scan: per buckets, a multiple of 4.
+__device__ __forceinline__ int2 scan_range(const PlaceArgs &a) {
   const int per = (((a.NB + kPrepBlock - 1) / kPrepBlock) + 3) & ~3;
   const int lo = min((int)threadIdx.x * per, a.NB);
-  const int hi = min(lo + per, a.NB);
-  const v4i *c4 = reinterpret_cast<const v4i *>(a.cnt + lo);
-  v4i v[V];
+  return make_int2(lo, min(lo + per, a.NB));
+}
+
+// Thread t's bucket counts for the block scan, requested without waiting: chunk q is read at
+// min(lo + 4q, NB4 - 4), always inside the padded counter array, and block_scan_buckets
+// counts it as zero past hi.
+__device__ __forceinline__ void load_scan_counts(const PlaceArgs &a, v4i (&v)[kScanChunks]) {
+  const int lo = scan_range(a).x;
+  const int last4 = ((a.NB + 3) & ~3) - 4;
 #pragma unroll
-  for (int q = 0; q < V; ++q) v[q] = lo + 4 * q < hi ? c4[q] : v4i{0, 0, 0, 0};
+  for (int q = 0; q < kScanChunks; ++q) v[q] = *reinterpret_cast<const v4i *>(a.cnt + min(lo + 4 * q, last4));
+}
+
+__device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kScanChunks]) {
+  __shared__ int s_c[kPrepBlock / kWave];
+  __shared__ int s_t[kPrepBlock / kWave];
+  constexpr int V = kScanChunks;
+  const int lo = scan_range(a).x, hi = scan_range(a).y;
+  const int tsh = __builtin_ctz((unsigned)a.tile);   // the tile size is a power of two
+#pragma unroll
+  for (int q = 0; q < V; ++q)
+    if (lo + 4 * q >= hi) v[q] = v4i{0, 0, 0, 0};
   int c = 0, t = 0;
 #pragma unroll
   for (int q = 0; q < V; ++q)
@@ -389,7 +424,7 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start) {
     for (int e = 0; e < 4; ++e) {
       const int n = v[q][e];
       c += n;
-      t += (n + a.tile - 1) / a.tile;
+      t += (n + a.tile - 1) >> tsh;
     }
   const int ic = wave_scan(c), it = wave_scan(t);
   const int wv = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
@@ -408,6 +443,8 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start) {
     tot_c += s_c[i];
     tot_t += s_t[i];
   }
+  // thread t's buckets are published by block t mod grid (every t < 256 names one block)
+  const bool writer = (int)threadIdx.x % (int)gridDim.x == (int)blockIdx.x;
 #pragma unroll
   for (int q = 0; q < V; ++q)
 #pragma unroll
@@ -415,9 +452,9 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start) {
       const int i = lo + 4 * q + e;
       if (i < hi) {
         const int n = v[q][e];
-        const int nt = (n + a.tile - 1) / a.tile;
+        const int nt = (n + a.tile - 1) >> tsh;
         start[i] = pc;
-        if (i % (int)gridDim.x == (int)blockIdx.x) {
+        if (writer) {
           a.bstart[i] = pc;
           for (int k = 0; k < nt; ++k) a.tiles[pt + k] = make_int2(i, pc + k * a.tile);
         }
@@ -435,30 +472,42 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start) {
 // Requests grouped by bucket: request r goes to its bucket's start plus its position from
 // k_prep.  With at most kHistMax buckets each block scans the bucket counts itself (dynamic
 // LDS: starts [NB]); with more, k_scan has written the bucket starts.
+constexpr int kScatterU = kReqPerPrepBlock / kPrepBlock;
+
+// Request u of this thread: bucket key (-1: none), position and record.  Every load is issued
+// before the first use; a thread past the last request reads the last one (R >= 1) and drops
+// it, and an invalid request's position (never written) is not used.
+__device__ __forceinline__ void scatter_loads(const PlaceArgs &a, int (&key)[kScatterU], int (&pos)[kScatterU],
+                                              ReqRec (&rec)[kScatterU]) {
+#pragma unroll
+  for (int u = 0; u < kScatterU; ++u) {
+    const int r = blockIdx.x * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
+    const int rc = min(r, a.R - 1);
+    key[u] = a.key[rc];
+    pos[u] = a.off[rc];
+    rec[u] = make_req_rec(a, rc);
+    if (r >= a.R) key[u] = -1;
+  }
+}
+
 __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
   extern __shared__ int start[];
-  constexpr int U = kReqPerPrepBlock / kPrepBlock;
-  int key[U], pos[U];
-  ReqRec rec[U];
-  // request loads first, so that their latency overlaps the bucket scan
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int r = blockIdx.x * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
-    key[u] = r < a.R ? a.key[r] : -1;
-    pos[u] = 0;
-    if (key[u] >= 0) {
-      rec[u] = make_req_rec(a, r);
-      pos[u] = a.off[r];
-    }
-  }
+  int key[kScatterU], pos[kScatterU];
+  ReqRec rec[kScatterU];
   if (a.NB <= kHistMax) {
-    block_scan_buckets(a, start);        // ends with a barrier
+    // the bucket counts are requested together with the request fields: one round trip
+    v4i cv[kScanChunks];
+    load_scan_counts(a, cv);
+    scatter_loads(a, key, pos, rec);
+    __builtin_amdgcn_sched_barrier(0);   // no use of a loaded value is scheduled before a load
+    block_scan_buckets(a, start, cv);    // ends with a barrier
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < kScatterU; ++u)
       if (key[u] >= 0) a.preq[start[key[u]] + pos[u]] = rec[u];
   } else {
+    scatter_loads(a, key, pos, rec);
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < kScatterU; ++u)
       if (key[u] >= 0) a.preq[a.bstart[key[u]] + pos[u]] = rec[u];
   }
 }
@@ -1624,7 +1673,8 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->off = take(sizeof(int32_t) * (R > 0 ? R : 1));
   o->total = off;
   o->NB = (int32_t)NB;
-  o->tile = tile;
+  static_assert((kQF & (kQF - 1)) == 0 && (kQ & (kQ - 1)) == 0, "tile sizes are powers of two");
+  o->tile = tile;                       // a power of two: the bucket scans shift by its log2
   o->max_tiles = (int32_t)max_tiles;
   o->waves_per_block = wpb;
   return true;

@@ -149,6 +149,14 @@ def test_many_gpus_and_models():
     parity_place(inp, label="G=300 M=37 (two resident words)")
 
 
+@pytest.mark.parametrize("G", [4096, 4097])
+def test_host_lists_at_the_one_pass_limit(G):
+    """Host lists built in 16 chunks of 256 GPUs, and one GPU more (a 17th chunk of one)."""
+    rng = np.random.default_rng(G)
+    inp = W.make_tiny_placement(rng, R=96, G=G, M=3, NS=4, NF=8, W=1, caps=True)
+    parity_place(inp, label=f"G={G} M=3 host lists")
+
+
 @pytest.mark.parametrize("seed", range(3))
 def test_ties_nan_and_bad_elements(seed):
     rng = np.random.default_rng(900 + seed)
