@@ -174,6 +174,7 @@ __device__ __forceinline__ Host load_host(const DspArgs &a, int m, int h, const 
   if (a.packed) {
     const v4i *rec = reinterpret_cast<const v4i *>(a.hrec + ((size_t)m * a.G + h) * 4);
     const v4i r0 = rec[0], mem = rec[1], tt = rec[2], sm = rec[3];
+    __builtin_amdgcn_sched_barrier(0);   // the four loads in flight together, before any test
     o.g = r0.x;
     o.kcur = r0.z;
     o.kd = (double)__int_as_float(r0.w);
@@ -197,17 +198,23 @@ __device__ __forceinline__ Host load_host(const DspArgs &a, int m, int h, const 
   return o;
 }
 
-// Does request r meet its SLOs on (j, k) starting at ta with batch b?  Energy if so.
-__device__ __forceinline__ bool point_ok(const DspArgs &a, int r, int m, int prow, int b, int j, int k, double ta,
-                                         double kg, double lout, double &e) {
+// The SLO test and energy of one operating point from its gathered values: does the request
+// (SLOs slo_ttft, slo_tbt) meet both starting at ta with batch b?  Energy if so.
+__device__ __forceinline__ bool point_test(const DspArgs &a, float ttft, float tbt, float s, float f, int b, double ta,
+                                           double kg, double lout, float slo_ttft, float slo_tbt, double &e) {
+  if (!(ta + (double)ttft < (double)slo_ttft && tbt < slo_tbt)) return false;
+  e = point_energy(a.p0, kg, (double)s, (double)f, (double)b / 32.0, (double)ttft, lout, (double)tbt);
+  return (float)e < __builtin_huge_valf();
+}
+
+// Does the request meet its SLOs on (j, k) starting at ta with batch b?  Energy if so.
+__device__ __forceinline__ bool point_ok(const DspArgs &a, int m, int prow, int b, int j, int k, double ta,
+                                         double kg, double lout, float slo_ttft, float slo_tbt, double &e) {
   if (j < 0 || j >= a.NS || k < 0 || k >= a.NF) return false;
   const size_t cell = (size_t)j * a.NF + k;
   const float ttft = a.pf[((size_t)m * kRows + (prow >= 0 ? prow : b - 1)) * a.C + cell];
   const float tbt = a.dc[((size_t)m * kRows + (b - 1)) * a.C + cell];
-  if (!(ta + (double)ttft < (double)a.slo_ttft[r] && tbt < a.slo_tbt[r])) return false;
-  e = point_energy(a.p0, kg, (double)a.sm_level[j], (double)a.freq_level[k], (double)b / 32.0, (double)ttft, lout,
-                   (double)tbt);
-  return (float)e < __builtin_huge_valf();
+  return point_test(a, ttft, tbt, a.sm_level[j], a.freq_level[k], b, ta, kg, lout, slo_ttft, slo_tbt, e);
 }
 
 // Stability order as one integer: more free memory, then more free SMs, then a lower GPU id
@@ -237,6 +244,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
   const double inf = __builtin_huge_val();
   const int m = a.model[r];
   const int pt = a.prompt[r], pd = a.pred[r];
+  const float slo_ttft = a.slo_ttft[r], slo_tbt = a.slo_tbt[r];
   int gsel = -1, ksel = -1, jsel = -1, phase = 0;
   double esel = inf;
   bool writer = sub == 0;
@@ -261,7 +269,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       const int g = H.g;
       const Point &p = H.p;
       double e;
-      if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, H.kcur, p.ta, H.kd, lout, e))) continue;
+      if (!(p.ok && point_ok(a, m, prow, p.b, p.sm, H.kcur, p.ta, H.kd, lout, slo_ttft, slo_tbt, e))) continue;
       emin = fmin(emin, e);
 #pragma unroll
       for (int c = 0; c < kCached; ++c)
@@ -287,7 +295,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
         const int g = H.g;
         const Point &p = H.p;
         double e;
-        if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, H.kcur, p.ta, H.kd, lout, e))) continue;
+        if (!(p.ok && point_ok(a, m, prow, p.b, p.sm, H.kcur, p.ta, H.kd, lout, slo_ttft, slo_tbt, e))) continue;
         const unsigned long long key = stability_key(p.mem, p.sm, g);
         if (e <= bound && key > best) {
           best = key;
@@ -317,7 +325,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
         const int g = H.g;
         const Point &p = H.p;
         double e;
-        if (!(p.ok && point_ok(a, r, m, prow, p.b, p.sm, kmax, p.ta, H.kd, lout, e))) continue;
+        if (!(p.ok && point_ok(a, m, prow, p.b, p.sm, kmax, p.ta, H.kd, lout, slo_ttft, slo_tbt, e))) continue;
         if (p.ta < bt || (p.ta == bt && g < bg)) {
           bg = g;
           bt = p.ta;
@@ -347,7 +355,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
         double bke = inf;
         for (int k = sub; k < a.NF; k += kGroup) {
           double e;
-          if (point_ok(a, r, m, prow, 1, a.NS - 1, k, 0.0, a.k_new, lout, e) && (e < bke || (e == bke && k < bk))) {
+          if (point_ok(a, m, prow, 1, a.NS - 1, k, 0.0, a.k_new, lout, slo_ttft, slo_tbt, e) && (e < bke || (e == bke && k < bk))) {
             bke = e;
             bk = k;
           }
