@@ -239,7 +239,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
 #pragma clang fp contract(off)
   const int lane = threadIdx.x & (kWave - 1);
   const int sub = lane & (kGroup - 1);
-  const int r = (blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kReqPerWave + (lane >> 4);
+  const int r = (blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kReqPerWave + lane / kGroup;
   if (r >= a.R) return;
   const double inf = __builtin_huge_val();
   const int m = a.model[r];
