@@ -1198,6 +1198,10 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   const int beg = tp[2 * t + 1];
   const int end = min(beg + a.tile, ro(a.bstart)[bucket + 1]);
 
+  // Staging and the class sort wait on memory and barriers while other workgroups' pass 1
+  // keeps the VALU busy: at a raised wavefront priority their instructions issue first, and
+  // pass 1 runs at the normal priority.
+  __builtin_amdgcn_s_setprio(2);
   const int wv = uniform(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t wblkB = (uint32_t)wv * kWblkB;
@@ -1338,6 +1342,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   for (int c0 = 0; c0 < hcnt; c0 += kHcap) {
     const int n = min(kHcap, hcnt - c0);
     __syncthreads();                      // previous records no longer in use; table staged
+    __builtin_amdgcn_s_setprio(2);          // the next chunk's class sort
     for (int i = threadIdx.x; i < kClasses; i += T) s_cls[i] = 0;
     __syncthreads();
     // records of this chunk, grouped by (cap_pf, cap_dc) class with an LDS counting sort,
@@ -1381,6 +1386,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
         s_pos[u * T + threadIdx.x] = (short)pos;
       }
     __syncthreads();
+    __builtin_amdgcn_s_setprio(0);
     if (live_any) {
       const int ncls = uniform(s_clist[kClasses]);
       if (tile_same && nrm)
