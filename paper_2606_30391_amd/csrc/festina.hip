@@ -780,7 +780,6 @@ __global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
 constexpr int kQF = 8;
 constexpr int kC = 128;
 constexpr int kXcds = 8;                         // MI355X: 8 XCDs, each with its own L2
-constexpr int kXcdChunk = 16;                     // consecutive tiles one XCD takes at a time
 constexpr int kNS8 = 8;
 constexpr int kClasses = kNS8 * kNS8;            // (cap_pf, cap_dc) pairs
 constexpr int kHcap = 256;                       // host records staged in LDS per chunk
@@ -1180,15 +1179,14 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   constexpr uint32_t recB = fast_rec_off(WPB);
   constexpr uint32_t dcsB = fast_dcs_off(WPB);
   constexpr int T = WPB * 64;
-  // XCD-aware tile order: workgroups are dealt to the 8 XCDs round-robin, so the idx-th
-  // workgroup of XCD x takes tile idx % C of chunk (idx / C) * 8 + x, chunks of C = kXcdChunk
-  // consecutive tiles (the same bucket's requests and GPU records stay on one L2) dealt to
-  // the XCDs in turn, so that no XCD is left with a heavier contiguous range.  The grid is a
-  // multiple of 8 * C, so every tile below n_tiles is some workgroup's.
+  // XCD-aware tile order: workgroups are dealt to the 8 XCDs round-robin, so XCD x takes
+  // the contiguous tile range [x * per, (x + 1) * per) -- the same arrival waves and GPU
+  // records -- instead of every eighth tile.  per = ceil(n_tiles / 8) <= grid / 8.
   const int ntiles = *ro(a.n_tiles);
+  const int per = (ntiles + kXcds - 1) / kXcds;
   const int idx = blockIdx.x / kXcds;
-  const int t = ((idx / kXcdChunk) * kXcds + (int)(blockIdx.x % kXcds)) * kXcdChunk + idx % kXcdChunk;
-  if (t >= ntiles) return;
+  const int t = (blockIdx.x % kXcds) * per + idx;
+  if (idx >= per || t >= ntiles) return;
   const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
   const int bucket = tp[2 * t];
   if (bucket & 1) {                       // prompt-less requests: TTFT from the batch row
@@ -1662,7 +1660,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   }
   o->fast = fast;
   const long long max_tiles = (R + tile - 1) / tile + NB;
-  if (max_tiles > INT_MAX - 128) return false;   // the grid is rounded up to a multiple of 8 * 16
+  if (max_tiles > INT_MAX - 8) return false;   // the grid is rounded up to a multiple of 8
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -1819,8 +1817,7 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
   hipError_t e = mark(0, st);
   if (e != hipSuccess) return FESTINA_ERR_DEVICE;
   if (lay.fast) {
-    static_assert(kXcds * kXcdChunk <= 128, "the layout's tile bound leaves room for this rounding");
-    const int grid = (lay.max_tiles + kXcds * kXcdChunk - 1) / (kXcds * kXcdChunk) * (kXcds * kXcdChunk);
+    const int grid = (lay.max_tiles + kXcds - 1) / kXcds * kXcds;
     if (wpb == 4)
       k_score_c128<4><<<grid, 4 * kWave, lds, st>>>(a);
     else
