@@ -49,7 +49,7 @@ SCLK_HZ = 2.4e9
 VALU_PEAK = N_CU * LANES_PER_CU_CLOCK * SCLK_HZ            # 39.32e12 lane-ops/s
 HBM_PEAK = 8.0e12                                           # B/s
 
-# Least VALU work per candidate of any exhaustive search (see DESIGN.md): divided by the
+# Least VALU work per candidate of any exhaustive search: divided by the
 # request's Lout, a candidate's energy is Pp * (TTFT / Lout) + Pd * TBT, one fused
 # multiply-add of a request term and two GPU terms, and a three-way min folds two
 # candidates into the running minimum, half an instruction each.  SLO masks, power terms,
@@ -485,7 +485,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} (WORLD_SIZE {world}) is not "
-              f"supported: the search shards without communication (see DESIGN.md).", file=sys.stderr)
+              f"supported: requests are independent, so the search shards by requests across devices "
+              f"without communication, and one device's share is what this measures.", file=sys.stderr)
         sys.exit(2)
 
     import torch
