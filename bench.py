@@ -478,6 +478,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-config", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="first print one line comparing the step (consolidation forked onto a second "
+                         "stream and joined back) launched eagerly and replayed from one HIP graph")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the run, copy MIB MiB device-to-device 5 times (a plain copy of known "
                          "size, to scale the HBM byte counters)")
@@ -500,6 +503,8 @@ def main():
 
     if args.per_config:
         per_config(F, W, hip, torch)
+    if args.graph:
+        graph_compare(F, W, torch)
 
     place = W.make_placement(4)
     fleet = W.make_fleet()
@@ -604,6 +609,46 @@ def main():
             y.copy_(x)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n * 4, "copies": 5}), flush=True)
+
+
+def graph_compare(F, W, torch, steps=200, rounds=3):
+    """The bench step with the consolidation call forked onto a second stream and joined back,
+    timed with events over `steps` steps: launched eagerly, and replayed from one HIP graph
+    capture of the same step; `rounds` alternating rounds."""
+    dp = F.DevicePlacement(W.make_placement(4), "cuda")
+    dm = F.DeviceMigration(W.make_fleet(), "cuda")
+    side = torch.cuda.Stream()
+
+    def step():
+        cur = torch.cuda.current_stream()
+        side.wait_stream(cur)
+        dp.run()
+        dm.run(side)
+        cur.wait_stream(side)
+
+    def per_step_us(fn):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record()
+        for _ in range(steps):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / steps * 1e3
+
+    for _ in range(10):
+        step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    eager, graph = [], []
+    for _ in range(rounds):
+        eager.append(per_step_us(step))
+        graph.append(per_step_us(g.replay))
+    print(json.dumps({"graph_compare": "config-4 placement + config-5 consolidation, forked and joined",
+                      "steps": steps, "eager_us_per_step": eager, "graph_replay_us_per_step": graph}), flush=True)
 
 
 def per_config(F, W, hip, torch):
