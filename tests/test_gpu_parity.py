@@ -85,7 +85,7 @@ def test_large_configs_oracle_sized(cfg, R):
 
 
 @pytest.mark.parametrize("cfg", [3, 4])
-@pytest.mark.parametrize("extra", [0, 100])
+@pytest.mark.parametrize("extra", [0, 100, 200, 300])
 def test_large_configs_full_size_sampled(cfg, extra):
     inp = W.make_placement(cfg, seed=W.config_seed(cfg, extra))
     R = inp["requests"]["n_requests"]
