@@ -69,6 +69,7 @@ SWEEP_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "sweep.hip")
 TRANSFER_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_transfer_costs_traffic.json")
 TRANSFER_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "transfer.hip")
 DISPATCH_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_dispatch_traffic.json")
+MIGRATE_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_migrate_traffic.json")
 DISPATCH_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "dispatch.hip")
 PREFERRED_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_preferred_traffic.json")
 PREFERRED_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "preferred.hip")
@@ -588,6 +589,16 @@ def main():
             # the same fraction against the peak at the engine clock the counter run measured
             "frac_at_measured_sclk": (None if counters is None else
                                       achieved / (VALU_PEAK * counters["sclk_ghz_effective"] * 1e9 / SCLK_HZ)),
+        },
+        # the consolidation scoring (the second scoring call), timed alone as a batch of calls
+        "migration": {
+            "kernel": "k_fleet + k_migrate (consolidation pair scoring + fused per-source argmax)",
+            "pairs": n_pairs, "call_ms": mig_ms,
+            "roofline": {"bound": "alu", "achieved": n_pairs * OPS_PER_PAIR / (mig_ms * 1e-3) / 1e12,
+                         "peak": VALU_PEAK / 1e12, "unit": "T VALU lane-ops/s",
+                         "frac": n_pairs * OPS_PER_PAIR / (mig_ms * 1e-3) / VALU_PEAK,
+                         "ops_per_pair": OPS_PER_PAIR,
+                         "traffic": load_traffic(MIGRATE_TRAFFIC_FILE, KERNEL_SRC)},   # both launches
         },
         "kernels_ms": {"k_score": score_ms, "k_score_candidates_per_s": n_cand / (score_ms * 1e-3),
                        "migration_call": mig_ms,

@@ -61,6 +61,11 @@ def test_short_run_prints_one_line_with_the_contract_fields():
         assert abs(r["frac_at_measured_sclk"] - r["frac"] * 2.4 / clk) < 1e-9
     ks = b["kernels_ms"]
     assert abs(ks["k_score_candidates_per_s"] * ks["k_score"] * 1e-3 / cfg["placement_candidates"] - 1) < 1e-6
+    mg = b["migration"]
+    assert mg["pairs"] == cfg["migration_pairs"] and mg["call_ms"] > 0
+    mr = mg["roofline"]
+    assert mr["bound"] == "alu" and 0 < mr["frac"] <= 1 and abs(mr["frac"] - mr["achieved"] / mr["peak"]) < 1e-9
+    assert mr["traffic"] is None or mr["traffic"] > 0
     c = b["cpu_baseline"]
     assert c["kind"] == "oracle" and c["cores"] >= 1 and c["value"] > 0 and c["unit"] == b["unit"]
     assert c["agreement"]["placement_flags_equal"] == 1.0 and c["agreement"]["migration_dst_equal"] == 1.0
