@@ -105,6 +105,23 @@ def test_large_configs_full_size_sampled(cfg, extra):
         assert np.all(fe[inp["meta"]["planted"]] == 0)
 
 
+def test_four_million_requests_sampled():
+    """Config 4's fleet and tables with 2^22 requests (65,536 per arrival wave): buckets of
+    about a thousand requests, a grid of 131,000 tiles; 2,000 sampled requests against the
+    oracle, flags and ranges over all of them."""
+    inp = W.make_placement(4, n_requests=1 << 22)
+    R = inp["requests"]["n_requests"]
+    sel = np.random.default_rng(22).choice(R, 2000, replace=False)
+    got, rep = parity_place(inp, sel, label="cfg4 tables, R=2^22")
+    ch, fe, en = got
+    NS, NF, G = inp["lut"]["n_sm"], inp["lut"]["n_freq"], inp["gpus"]["n_gpus"]
+    assert np.all((fe == 1) == (ch >= 0)) and np.all(ch < G * NS * NF)
+    assert np.all(np.isinf(en[fe == 0])) and np.all(np.isfinite(en[fe == 1]))
+    m = inp["requests"]["model"][fe == 1]
+    g = ch[fe == 1] // (NS * NF)
+    assert np.all((inp["gpus"]["resident"][g, m // 32] >> (m % 32).astype(np.uint32)) & 1)
+
+
 @pytest.mark.parametrize("cfg", [3, 4])
 def test_large_configs_every_request(cfg):
     """Every request of the full-size configuration against the oracle (run on chunks of
