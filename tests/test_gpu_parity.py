@@ -138,6 +138,16 @@ def test_large_configs_every_request(cfg):
     assert rep.ok, str(rep)
 
 
+def test_consolidation_of_16384_gpus_sampled():
+    """A fleet 8 times config 5's (16,384 GPUs, 268 M ordered pairs): 100 sampled sources, each
+    against all its destinations, checked against the oracle."""
+    inp = W.make_fleet(n_gpus=16384)
+    sel = np.random.default_rng(16384).choice(16384, 100, replace=False)
+    got, rep = parity_mig(inp, sel, label="16384 GPUs")
+    b, sv, k = got
+    assert np.all((b >= 0) == (k >= 0)) and np.all(b < 16384) and np.all(b != np.arange(16384))
+
+
 def test_config5_full():
     parity_mig(W.make_fleet(), label="cfg5 full")
 
