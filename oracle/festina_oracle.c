@@ -487,6 +487,18 @@ static int or_phase_best(const or_lut *L, const or_llms *Q, int g, int i, int de
   return best;
 }
 
+/* App. E, Eq. preferred_sm: SM_l = (s_p T_p + s_d T_d) / (T_p + T_d), the SM shares of the
+ * two phases' cells weighted by their durations; Eq. preferred_frequency:
+ * F_l = (E_p f_p + E_d f_d) / (E_p + E_d) with E = P * T, the frequencies weighted by
+ * the phases' energies. */
+static void or_averages(const or_lut *L, int jp, int kp, int jd, int kd, double tp, double pp, double td,
+                        double pd, double *sm_pref, double *f_pref) {
+  const double sp = (double)L->sm_level[jp], sd = (double)L->sm_level[jd];
+  const double fp = (double)L->freq_level[kp], fd = (double)L->freq_level[kd];
+  *sm_pref = (sp * tp + sd * td) / (tp + td);
+  *f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);
+}
+
 static void or_preferred_one(const or_lut *L, const or_llms *Q, int g, int i, or_pref *o) {
   double tp = 0, pp = 0, td = 0, pd = 0;
   const int cp = or_phase_best(L, Q, g, i, 0, &tp, &pp);
@@ -501,10 +513,7 @@ static void or_preferred_one(const or_lut *L, const or_llms *Q, int g, int i, or
   o->p_d = pd;
   o->feasible = cp >= 0 && cd >= 0;
   if (o->feasible) {
-    const double sp = (double)L->sm_level[o->sm_p], sd = (double)L->sm_level[o->sm_d];
-    const double fp = (double)L->freq_level[o->f_p], fd = (double)L->freq_level[o->f_d];
-    o->sm_pref = (sp * tp + sd * td) / (tp + td);
-    o->f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);
+    or_averages(L, o->sm_p, o->f_p, o->sm_d, o->f_d, tp, pp, td, pd, &o->sm_pref, &o->f_pref);
   } else {
     o->sm_pref = NAN;
     o->f_pref = NAN;
@@ -599,10 +608,7 @@ int festina_oracle_preferred_at(const or_lut *L, const or_llms *Q, int32_t g, in
   double tp, pp, td, pd;
   if (!festina_oracle_phase_cell(L, Q, g, i, 0, jp, kp, &tp, &pp)) return 0;
   if (!festina_oracle_phase_cell(L, Q, g, i, 1, jd, kd, &td, &pd)) return 0;
-  const double sp = (double)L->sm_level[jp], sd = (double)L->sm_level[jd];
-  const double fp = (double)L->freq_level[kp], fd = (double)L->freq_level[kd];
-  *sm_pref = (sp * tp + sd * td) / (tp + td);
-  *f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);
+  or_averages(L, jp, kp, jd, kd, tp, pp, td, pd, sm_pref, f_pref);
   return 1;
 }
 

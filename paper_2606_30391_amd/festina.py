@@ -133,12 +133,27 @@ EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_
 _lib = None
 
 
+def _check_fresh():
+    """Raise unless the library was built from the sources now in the tree."""
+    from .build import HASH_FILE, source_hash
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"HIP library {LIB_PATH} is not built; run __graft_entry__.build()")
+    try:
+        with open(HASH_FILE) as f:
+            built = f.read().strip()
+    except OSError:
+        built = ""
+    if built != source_hash():
+        raise RuntimeError(f"HIP library {LIB_PATH} was not built from the sources in this tree "
+                           "(csrc/, include/festina.h or the flags changed); run __graft_entry__.build()")
+
+
 def lib():
-    """Load the built HIP library (raises if it has not been built)."""
+    """Load the built HIP library (raises if it has not been built, or was built from other
+    sources than the ones in the tree)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"HIP library {LIB_PATH} is not built; run __graft_entry__.build()")
+        _check_fresh()
         L = C.CDLL(LIB_PATH)
         P = C.POINTER
         L.festina_abi_version.restype = C.c_int32

@@ -237,3 +237,113 @@ def test_preferred_and_ewr_reject_bad_arguments(lib):
     assert ecall(8, 4, fake, ewr, ws, 255) == F.FESTINA_ERR_INVALID
     assert ecall(8, 4, fake, ewr, C.c_void_p(0x100010), 256) == F.FESTINA_ERR_INVALID
     assert ecall(8, 4, fake, ewr, None, 256) == F.FESTINA_ERR_INVALID
+
+
+@no_gpu
+def test_dispatch_rejects_bad_arguments(lib):
+    fake = C.c_void_p(0x1000)
+    L = F.lib()
+
+    def structs(NS=8, NF=16, G=64, S=4, R=512):
+        lut = F.festina_lut(32, 32, NS, NF, fake, fake, fake, fake, 120.0)
+        av = F.festina_gpu_avail(G, S, *([fake] * 8), 400.0)
+        req = F.festina_requests(R, fake, None, fake, fake, fake, fake)
+        out = F.festina_dispatches(*([fake] * 5))
+        return lut, av, req, out
+
+    def call(lut, av, req, out, ws, nbytes):
+        return L.festina_dispatch_requests(C.byref(lut), C.byref(av), C.byref(req), C.byref(out), ws, nbytes, None)
+
+    lut, av, req, out = structs()
+    need = F.festina_dispatch_workspace_bytes(lut, av)
+    assert need > 0 and need % 256 == 0
+    ws = C.c_void_p(0x100000)
+    assert L.festina_dispatch_requests(None, C.byref(av), C.byref(req), C.byref(out), ws, need, None) == \
+        F.FESTINA_ERR_INVALID
+    assert L.festina_dispatch_requests(C.byref(lut), None, C.byref(req), C.byref(out), ws, need, None) == \
+        F.FESTINA_ERR_INVALID
+    assert L.festina_dispatch_requests(C.byref(lut), C.byref(av), None, C.byref(out), ws, need, None) == \
+        F.FESTINA_ERR_INVALID
+    assert call(lut, av, req, out, None, need) == F.FESTINA_ERR_INVALID
+    assert call(lut, av, req, out, ws, need - 1) == F.FESTINA_ERR_INVALID
+    assert call(lut, av, req, out, C.c_void_p(0x100008), need) == F.FESTINA_ERR_INVALID
+    assert call(*structs(NS=16, NF=17), ws, 1 << 30) == F.FESTINA_ERR_UNSUPPORTED
+    for obj, field, value in [("lut", "n_rows", 31), ("lut", "n_models", 0), ("lut", "pf", None),
+                              ("av", "n_gpus", 0), ("av", "n_gpus", 1 << 24), ("av", "n_steps", 0),
+                              ("av", "sm_free", None), ("av", "kv_kib_per_token", None),
+                              ("req", "n_requests", -1), ("req", "slo_tbt_ms", None),
+                              ("out", "phase", None), ("out", "energy_mj", None)]:
+        s = dict(zip(("lut", "av", "req", "out"), structs()))
+        setattr(s[obj], field, value)
+        assert call(s["lut"], s["av"], s["req"], s["out"], ws, 1 << 30) == F.FESTINA_ERR_INVALID, (obj, field)
+    assert F.festina_dispatch_workspace_bytes(*structs()[:1], F.festina_gpu_avail(0, 4, *([fake] * 8), 1.0)) == 0
+    # no requests: nothing launched, outputs untouched
+    lut, av, req, out = structs(R=0)
+    req.model = None
+    out.gpu = None
+    assert call(lut, av, req, out, ws, need) == F.FESTINA_OK
+
+
+@no_gpu
+def test_transfer_costs_and_moves_reject_bad_arguments(lib):
+    fake = C.c_void_p(0x1000)
+    L = F.lib()
+
+    def structs(G=64, M=32, Q=128):
+        tr = F.festina_transfer(G, M, fake, fake, fake, fake, 153.6, 50.0)
+        lut = F.festina_lut(M, 32, 8, 16, fake, fake, fake, fake, 120.0)
+        plan = F.festina_plan(fake, fake, fake, fake)
+        req = F.festina_inflight(Q, *([fake] * 6))
+        out = F.festina_moves(fake, fake, fake)
+        return tr, lut, plan, req, out
+
+    cost = lambda tr, c: L.festina_transfer_costs(C.byref(tr) if tr is not None else None, c, None)
+    tr, *_ = structs()
+    assert cost(None, fake) == F.FESTINA_ERR_INVALID
+    assert cost(tr, None) == F.FESTINA_ERR_INVALID
+    for field, value in [("n_gpus", 0), ("n_models", 0), ("resident", None), ("weights_mib", None),
+                         ("state_mib", None), ("node", None), ("bw_intra_gbs", 0.0), ("bw_inter_gbs", -1.0),
+                         ("bw_intra_gbs", float("nan"))]:
+        tr, *_ = structs()
+        setattr(tr, field, value)
+        assert cost(tr, fake) == F.FESTINA_ERR_INVALID, field
+    tr, *_ = structs(G=(1 << 20) + 1)
+    assert cost(tr, fake) == F.FESTINA_ERR_UNSUPPORTED          # more than 2^40 matrix entries
+
+    def moves(tr, lut, plan, req, out):
+        return L.festina_request_moves(C.byref(lut), C.byref(tr), C.byref(plan), C.byref(req), C.byref(out), None)
+
+    assert L.festina_request_moves(None, *(C.byref(x) for x in structs()[:1]), *(
+        C.byref(x) for x in structs()[2:]), None) == F.FESTINA_ERR_INVALID
+    for obj, field, value in [("tr", "bw_inter_gbs", 0.0), ("lut", "n_rows", 16), ("lut", "n_sm", 0),
+                              ("lut", "dc", None), ("plan", "dest", None), ("plan", "batch", None),
+                              ("req", "n_requests", -1), ("req", "kv_kib", None), ("req", "src", None),
+                              ("out", "decision", None), ("out", "migrate_ms", None)]:
+        s = dict(zip(("tr", "lut", "plan", "req", "out"), structs()))
+        setattr(s[obj], field, value)
+        assert moves(s["tr"], s["lut"], s["plan"], s["req"], s["out"]) == F.FESTINA_ERR_INVALID, (obj, field)
+    s = dict(zip(("tr", "lut", "plan", "req", "out"), structs()))
+    s["lut"].n_sm, s["lut"].n_freq = 16, 17
+    assert moves(s["tr"], s["lut"], s["plan"], s["req"], s["out"]) == F.FESTINA_ERR_UNSUPPORTED
+    # no in-flight requests: nothing launched
+    s = dict(zip(("tr", "lut", "plan", "req", "out"), structs(Q=0)))
+    s["req"].src = None
+    s["out"].decision = None
+    assert moves(s["tr"], s["lut"], s["plan"], s["req"], s["out"]) == F.FESTINA_OK
+
+
+def test_binding_refuses_a_library_built_from_other_sources(tmp_path, monkeypatch):
+    """festina.lib() loads the library only while its recorded source hash matches the tree."""
+    import paper_2606_30391_amd.build as B
+    if not os.path.exists(F.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    F._check_fresh()                                         # the built library matches
+    stale = tmp_path / "libfestina.so.sources"
+    stale.write_text("0" * 64 + "\n")
+    monkeypatch.setattr(B, "HASH_FILE", str(stale))
+    with pytest.raises(RuntimeError, match="not built from the sources"):
+        F._check_fresh()
+    monkeypatch.setattr(B, "HASH_FILE", str(tmp_path / "missing"))
+    with pytest.raises(RuntimeError, match="not built from the sources"):
+        F._check_fresh()

@@ -39,7 +39,9 @@ def run_place(inp, stream=None):
     return dp.results()
 
 
-def parity_place(inp, sel=None, label=""):
+def parity_place(inp, sel=None, label="", exact=False):
+    """GPU placements against the oracle.  With ``exact`` every choice must be the oracle's
+    own index: no near-tie acceptance, so exact ties must go to the lowest index."""
     R = inp["requests"]["n_requests"]
     say(f"[gpu] placement {label}: R={R} G={inp['gpus']['n_gpus']} W={inp['gpus']['n_waves']} "
         f"NS={inp['lut']['n_sm']} NF={inp['lut']['n_freq']}")
@@ -49,6 +51,9 @@ def parity_place(inp, sel=None, label=""):
     rep = check_placements(inp, sel, ref, tuple(x[sel] for x in got))
     say(f"      {rep}")
     assert rep.ok, str(rep)
+    if exact:
+        assert rep.near_ties == 0, f"{label}: {rep.near_ties} choices differ from the oracle's lowest index"
+        assert np.array_equal(got[0][sel], ref[0]), label
     return got, rep
 
 
@@ -187,7 +192,9 @@ def test_host_lists_at_the_one_pass_limit(G):
 @pytest.mark.parametrize("seed", range(3))
 def test_ties_nan_and_bad_elements(seed):
     rng = np.random.default_rng(900 + seed)
-    parity_place(W.make_tiny_placement(rng, R=40, G=6, M=2, NS=4, NF=6, ties=True), label="ties")
+    parity_place(W.make_tiny_placement(rng, R=40, G=6, M=2, NS=4, NF=6, ties=True), label="ties", exact=True)
+    parity_place(W.make_tiny_placement(rng, R=40, G=6, M=2, NS=8, NF=16, ties=True), label="ties 8x16",
+                 exact=True)
     parity_place(W.make_tiny_placement(rng, R=40, G=6, M=2, NS=4, NF=6, nan_cells=True), label="nan/inf")
     inp = W.make_tiny_placement(rng, R=80, G=7, M=3, NS=4, NF=8, W=2, caps=True)
     q, g = inp["requests"], inp["gpus"]
@@ -337,7 +344,7 @@ def test_fast_kernel_packed_capped_classes(seed, variant):
     if variant == "low caps":
         g["cap_pf"] = (g["cap_pf"] % 4).astype(np.int8)
         g["cap_dc"] = (g["cap_dc"] % 4).astype(np.int8)
-    parity_place(inp, label=f"8x16 packed capped classes ({variant}, seed {seed})")
+    parity_place(inp, label=f"8x16 packed capped classes ({variant}, seed {seed})", exact=variant == "ties")
 
 
 def test_generic_kernel_four_waves_per_block():

@@ -78,10 +78,18 @@ PREFERRED = [
     ("decode duration without the output length",
      "const double t = decode ? (double)Q->avg_out_tokens[at] * (double)lat : (double)lat;\n      const double e",
      "const double t = (double)lat;\n      const double e"),
-    ("time-weighted frequency", "o->f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);",
-     "o->f_pref = (tp * fp + td * fd) / (tp + td);"),
-    ("energy-weighted SM share", "o->sm_pref = (sp * tp + sd * td) / (tp + td);",
-     "o->sm_pref = (pp * tp * sp + pd * td * sd) / (pp * tp + pd * td);"),
+    ("time-weighted frequency", "*f_pref = (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td);",
+     "*f_pref = (tp * fp + td * fd) / (tp + td);"),
+    ("energy-weighted SM share", "*sm_pref = (sp * tp + sd * td) / (tp + td);",
+     "*sm_pref = (pp * tp * sp + pd * td * sd) / (pp * tp + pd * td);"),
+    ("averages at given cells take the decode cell for both phases",
+     "or_averages(L, jp, kp, jd, kd, tp, pp, td, pd, sm_pref, f_pref);",
+     "or_averages(L, jd, kd, jd, kd, tp, pp, td, pd, sm_pref, f_pref);"),
+    ("averages at given cells swap the phases' durations",
+     "or_averages(L, jp, kp, jd, kd, tp, pp, td, pd, sm_pref, f_pref);",
+     "or_averages(L, jp, kp, jd, kd, td, pp, tp, pd, sm_pref, f_pref);"),
+    ("decode cell tested as a prefill cell", "if (!festina_oracle_phase_cell(L, Q, g, i, 1, jd, kd, &td, &pd)) return 0;",
+     "if (!festina_oracle_phase_cell(L, Q, g, i, 0, jd, kd, &td, &pd)) return 0;"),
     ("decode reads the prompt row", "      const float lat = decode ? L->dc[or_cell(L, m, b - 1, j, k)]",
      "      const float lat = decode ? L->dc[or_cell(L, m, prow, j, k)]"),
     ("pre-admission batch in the phase power", "const double u = (double)b / 32.0;\n  const double kg = (double)Q->k_dyn_w[g];",

@@ -207,3 +207,70 @@ def test_preferred_workload_invariants():
             lo = float(min(lut["freq_level"][o["f_p"][g, i]], lut["freq_level"][o["f_d"][g, i]]))
             hi = float(max(lut["freq_level"][o["f_p"][g, i]], lut["freq_level"][o["f_d"][g, i]]))
             assert lo - 1e-12 <= o["f_pref"][g, i] <= hi + 1e-12
+
+
+# ------------------------------------------------------------------ averages at given cells
+def test_preferred_at_worked_example():
+    """The two averages at hand-chosen cells of the worked example, as exact fractions."""
+    inp, _, d = golden_preferred()
+    for case in d["at_cells"]["cases"]:
+        (jp, kp), (jd, kd) = case["prefill"], case["decode"]
+        ok, sm, f = oracle.preferred_at(inp, 0, 0, jp, kp, jd, kd)
+        assert ok == bool(case["feasible"]), case
+        if ok:
+            for got, (num, den) in ((sm, case["sm_pref"]), (f, case["f_pref"])):
+                assert got == pytest.approx(float(Fraction(num) / Fraction(den)), rel=1e-15), case
+
+
+def _averages_from_cells(inp, g, i, jp, kp, jd, kd):
+    """Eq. preferred_sm / preferred_frequency at the given cells, from brute.phase_cells."""
+    from brute import phase_cells
+    NF = inp["lut"]["n_freq"]
+    P = {c: (t, p) for _, c, t, p in phase_cells(inp, g, i, False)}
+    D = {c: (t, p) for _, c, t, p in phase_cells(inp, g, i, True)}
+    if jp * NF + kp not in P or jd * NF + kd not in D:
+        return None
+    (tp, pp), (td, pd) = P[jp * NF + kp], D[jd * NF + kd]
+    sp, sd = float(inp["lut"]["sm_level"][jp]), float(inp["lut"]["sm_level"][jd])
+    fp, fd = float(inp["lut"]["freq_level"][kp]), float(inp["lut"]["freq_level"][kd])
+    return (sp * tp + sd * td) / (tp + td), (pp * tp * fp + pd * td * fd) / (pp * tp + pd * td)
+
+
+def test_preferred_at_brute_force():
+    """Every cell pair of tiny random fleets: feasible exactly when both cells meet their
+    SLOs, and the averages equal the enumeration's."""
+    rng = np.random.default_rng(30391700)
+    n = 0
+    for _ in range(60):
+        inp = W.make_tiny_llms(rng)
+        lut, q = inp["lut"], inp["llms"]
+        NS, NF = lut["n_sm"], lut["n_freq"]
+        for g in range(q["n_gpus"]):
+            for i in range(int(q["n_inst"][g]) if 0 <= q["n_inst"][g] <= q["max_inst"] else 0):
+                for _ in range(6):
+                    jp, jd = rng.integers(0, NS, 2)
+                    kp, kd = rng.integers(0, NF, 2)
+                    ok, sm, f = oracle.preferred_at(inp, g, i, jp, kp, jd, kd)
+                    want = _averages_from_cells(inp, g, i, jp, kp, jd, kd)
+                    assert ok == (want is not None)
+                    if ok:
+                        assert sm == pytest.approx(want[0], rel=1e-12) and f == pytest.approx(want[1], rel=1e-12)
+                        n += 1
+    assert n > 100
+
+
+def test_preferred_at_reproduces_preferred_on_the_fleet_workload():
+    """At the oracle's own preferred cells the averages are the preferred configuration's."""
+    inp = W.make_llms(n_gpus=256)
+    o = oracle.preferred(inp)
+    q = inp["llms"]
+    checked = 0
+    for g in range(q["n_gpus"]):
+        for i in range(int(q["n_inst"][g])):
+            ok, sm, f = oracle.preferred_at(inp, g, i, o["sm_p"][g, i], o["f_p"][g, i], o["sm_d"][g, i],
+                                            o["f_d"][g, i])
+            assert ok == bool(o["feasible"][g, i])
+            if ok:
+                assert sm == o["sm_pref"][g, i] and f == o["f_pref"][g, i]
+                checked += 1
+    assert checked > 300
