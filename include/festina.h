@@ -65,12 +65,16 @@ extern "C" {
 #define FESTINA_MAX_TASKS 64     /* task slots per batch of the sweep kernel */
 #define FESTINA_PREFILL 0        /* task phases of the sweep */
 #define FESTINA_DECODE 1
+/* Device scratch that festina_score_placements_noalloc holds per GPU (32 MiB: the
+ * 262,144-request, 1,024-GPU, 64-wave placement search needs 11.3 MiB of it). */
+#define FESTINA_NOALLOC_WORKSPACE_BYTES ((size_t)32 << 20)
 
 typedef enum {
   FESTINA_OK = 0,
   FESTINA_ERR_INVALID = 1,
   FESTINA_ERR_DEVICE = 2,
-  FESTINA_ERR_UNSUPPORTED = 3
+  FESTINA_ERR_UNSUPPORTED = 3,
+  FESTINA_ERR_TOO_LARGE = 4     /* input exceeds the fixed scratch of an allocation-free entry point */
 } festina_status;
 
 /* Offline profile look-up table (Sec. 3.2.1: latency per model under each frequency,
@@ -148,6 +152,22 @@ size_t festina_placements_workspace_bytes(const festina_lut *lut, const festina_
 festina_status festina_score_placements(const festina_lut *lut, const festina_gpus *gpus,
                                         const festina_requests *req, festina_placements *out,
                                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* For callers that cannot allocate device memory -- code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc: festina_score_placements with its
+ * workspace taken from a fixed device array of FESTINA_NOALLOC_WORKSPACE_BYTES that the
+ * library holds on every GPU it runs on until the process ends.  The call allocates
+ * nothing; the caller passes inputs and outputs as for festina_score_placements, and gets
+ * the same outputs.  The array's address on the current device is looked up on the first
+ * call made with that device current.  Shapes whose festina_placements_workspace_bytes()
+ * exceeds FESTINA_NOALLOC_WORKSPACE_BYTES return FESTINA_ERR_TOO_LARGE before anything is
+ * launched.  Every call on one GPU shares that GPU's array: calls that overlap in time on
+ * one GPU (on different streams or from different host threads) race and their results
+ * are undefined; calls ordered on one stream are safe, since each call clears what it
+ * needs cleared with a kernel (no memset) before it uses it. */
+festina_status festina_score_placements_noalloc(const festina_lut *lut, const festina_gpus *gpus,
+                                                const festina_requests *req, festina_placements *out,
+                                                void *stream);
 
 /* Consolidation fleet (Sec. 3.5.2; App. E): every GPU holds 1..max_inst resident
  * model instances.  Instance i of GPU g meets its SLOs at frequency level k when

@@ -27,10 +27,12 @@
 // float32: Pp = fma(k_g*u_g, s*f^3, P0), X = Pp*TTFT, Y = Pd*TBT, E = fma(Lout, Y, X).
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
+#include <mutex>
 
 #include "festina.h"
 
@@ -1719,6 +1721,8 @@ const char *festina_status_string(festina_status s) {
     case FESTINA_ERR_INVALID: return "invalid argument (null pointer, bad size or workspace too small)";
     case FESTINA_ERR_DEVICE: return "HIP device error";
     case FESTINA_ERR_UNSUPPORTED: return "shape not supported by the kernels";
+    case FESTINA_ERR_TOO_LARGE:
+      return "input needs more workspace than the library's fixed device scratch holds";
   }
   return "unknown status";
 }
@@ -1730,24 +1734,31 @@ size_t festina_placements_workspace_bytes(const festina_lut *lut, const festina_
   return lay.total;
 }
 
-festina_status festina_score_placements(const festina_lut *L, const festina_gpus *G,
-                                        const festina_requests *Q, festina_placements *out,
-                                        void *workspace, size_t workspace_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks of a placement call that need no workspace; on success `lay` holds the workspace
+// layout.  FESTINA_OK with n_requests == 0 means there is nothing to launch.
+festina_status place_args(const festina_lut *L, const festina_gpus *G, const festina_requests *Q,
+                          const festina_placements *out, PlaceLayout *lay) {
   if (!place_shapes_ok(L, G, Q) || !out) return FESTINA_ERR_INVALID;
   const long long C = (long long)L->n_sm * L->n_freq;
   if (C > FESTINA_MAX_CELLS) return FESTINA_ERR_UNSUPPORTED;
   if (!L->sm_level || !L->freq_level || !L->pf || !L->dc) return FESTINA_ERR_INVALID;
   if (!G->batch || !G->k_dyn_w || !G->resident) return FESTINA_ERR_INVALID;
-  PlaceLayout lay;
-  if (!place_layout(L, G, Q, &lay)) return FESTINA_ERR_INVALID;
+  if (!place_layout(L, G, Q, lay)) return FESTINA_ERR_INVALID;
   if (Q->n_requests == 0) return FESTINA_OK;
   if (!Q->model || !Q->prompt_tokens || !Q->pred_out_tokens || !Q->slo_ttft_ms || !Q->slo_tbt_ms)
     return FESTINA_ERR_INVALID;
   if (!out->choice || !out->feasible || !out->energy_mj) return FESTINA_ERR_INVALID;
-  if (!workspace || workspace_bytes < lay.total || (((uintptr_t)workspace) & 255) != 0)
-    return FESTINA_ERR_INVALID;
+  return FESTINA_OK;
+}
 
-  char *ws = static_cast<char *>(workspace);
+// The launches of one placement call on a checked workspace of lay.total bytes.
+festina_status place_launch(const festina_lut *L, const festina_gpus *G, const festina_requests *Q,
+                            const festina_placements *out, const PlaceLayout &lay, char *ws, void *stream) {
+  const long long C = (long long)L->n_sm * L->n_freq;
   PlaceArgs a;
   a.M = L->n_models;
   a.NS = L->n_sm;
@@ -1831,6 +1842,61 @@ festina_status festina_score_placements(const festina_lut *L, const festina_gpus
     e = launch_score<4>(a, lay.max_tiles, wpb, lds, st);
   if (e == hipSuccess) e = mark(1, st);
   return e == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
+}
+
+// Workspace of the allocation-free placement entry point: one array per GPU, held by the
+// library for the life of the process.  In host code `scratch` names a host-side stand-in;
+// the array's device address on each GPU comes from hipGetSymbolAddress, looked up once per
+// device (on the first call with that device current) and kept in scratch_dev.
+constexpr size_t kScratchBytes = FESTINA_NOALLOC_WORKSPACE_BYTES;
+static_assert(kScratchBytes % 256 == 0, "the scratch size is a multiple of the workspace alignment");
+__device__ __align__(256) char scratch[kScratchBytes];
+constexpr int kScratchDevices = 64;
+std::atomic<char *> scratch_dev[kScratchDevices];
+std::mutex scratch_mu;
+
+// Device address of the current device's scratch array, or nullptr on a HIP error.
+char *scratch_for_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return nullptr;
+  char *p = scratch_dev[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  p = scratch_dev[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    void *addr = nullptr;
+    if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) return nullptr;
+    p = static_cast<char *>(addr);
+    scratch_dev[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+festina_status festina_score_placements(const festina_lut *L, const festina_gpus *G,
+                                        const festina_requests *Q, festina_placements *out,
+                                        void *workspace, size_t workspace_bytes, void *stream) {
+  PlaceLayout lay;
+  const festina_status s = place_args(L, G, Q, out, &lay);
+  if (s != FESTINA_OK || Q->n_requests == 0) return s;
+  if (!workspace || workspace_bytes < lay.total || (((uintptr_t)workspace) & 255) != 0)
+    return FESTINA_ERR_INVALID;
+  return place_launch(L, G, Q, out, lay, static_cast<char *>(workspace), stream);
+}
+
+festina_status festina_score_placements_noalloc(const festina_lut *L, const festina_gpus *G,
+                                                const festina_requests *Q, festina_placements *out,
+                                                void *stream) {
+  PlaceLayout lay;
+  const festina_status s = place_args(L, G, Q, out, &lay);
+  if (s != FESTINA_OK || Q->n_requests == 0) return s;
+  if (lay.total > kScratchBytes) return FESTINA_ERR_TOO_LARGE;
+  char *ws = scratch_for_current_device();
+  if (!ws) return FESTINA_ERR_DEVICE;
+  return place_launch(L, G, Q, out, lay, ws, stream);
 }
 
 static bool mig_shapes_ok(const festina_lut *L, const festina_fleet *F) {

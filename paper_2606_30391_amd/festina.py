@@ -20,6 +20,8 @@ FESTINA_OK = 0
 FESTINA_ERR_INVALID = 1
 FESTINA_ERR_DEVICE = 2
 FESTINA_ERR_UNSUPPORTED = 3
+FESTINA_ERR_TOO_LARGE = 4
+FESTINA_NOALLOC_WORKSPACE_BYTES = 32 << 20
 
 
 class FestinaError(RuntimeError):
@@ -125,7 +127,8 @@ class festina_moves(C.Structure):
 
 
 EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_workspace_bytes",
-            "festina_score_placements", "festina_migrations_workspace_bytes", "festina_score_migrations",
+            "festina_score_placements", "festina_score_placements_noalloc", "festina_migrations_workspace_bytes",
+            "festina_score_migrations",
             "festina_sweep_batches", "festina_preferred_configs", "festina_ewr_workspace_bytes",
             "festina_fleet_ewr", "festina_dispatch_workspace_bytes", "festina_dispatch_requests",
             "festina_transfer_costs", "festina_request_moves", "festina_set_timing_events")
@@ -164,6 +167,9 @@ def lib():
         L.festina_score_placements.argtypes = [P(festina_lut), P(festina_gpus), P(festina_requests),
                                                P(festina_placements), C.c_void_p, C.c_size_t, C.c_void_p]
         L.festina_score_placements.restype = C.c_int
+        L.festina_score_placements_noalloc.argtypes = [P(festina_lut), P(festina_gpus), P(festina_requests),
+                                                       P(festina_placements), C.c_void_p]
+        L.festina_score_placements_noalloc.restype = C.c_int
         L.festina_migrations_workspace_bytes.argtypes = [P(festina_lut), P(festina_fleet)]
         L.festina_migrations_workspace_bytes.restype = C.c_size_t
         L.festina_score_migrations.argtypes = [P(festina_lut), P(festina_fleet), P(festina_migrations),
@@ -268,6 +274,10 @@ class DevicePlacement:
 
     def run(self, stream=None):
         festina_score_placements(self.lut, self.gpus, self.req, self.out, self.workspace, self.ws_bytes, stream)
+
+    def run_noalloc(self, stream=None):
+        """The same search through the allocation-free entry point (the library's scratch)."""
+        festina_score_placements_noalloc(self.lut, self.gpus, self.req, self.out, stream)
 
     def results(self):
         R = self.R
@@ -529,6 +539,13 @@ def festina_score_placements(lut, gpus, req, out, workspace, workspace_bytes, st
                                         int(workspace_bytes), _stream_handle(stream))
     if st != FESTINA_OK:
         raise FestinaError(st, "festina_score_placements")
+
+
+def festina_score_placements_noalloc(lut, gpus, req, out, stream=None) -> None:
+    st = lib().festina_score_placements_noalloc(C.byref(lut), C.byref(gpus), C.byref(req), C.byref(out),
+                                                _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_score_placements_noalloc")
 
 
 def festina_migrations_workspace_bytes(lut, fleet) -> int:

@@ -48,8 +48,9 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_version_and_status_strings(lib):
     assert F.festina_abi_version() == 1
-    for s in range(4):
+    for s in range(5):
         assert F.festina_status_string(s)
+    assert "scratch" in F.festina_status_string(F.FESTINA_ERR_TOO_LARGE)
     assert "unknown" in F.festina_status_string(99)
 
 
@@ -347,3 +348,27 @@ def test_binding_refuses_a_library_built_from_other_sources(tmp_path, monkeypatc
     monkeypatch.setattr(B, "HASH_FILE", str(tmp_path / "missing"))
     with pytest.raises(RuntimeError, match="not built from the sources"):
         F._check_fresh()
+
+
+@no_gpu
+def test_noalloc_placement_rejects_bad_arguments_and_oversized_inputs(lib):
+    """The allocation-free entry point checks its arguments like festina_score_placements and
+    refuses, before any launch, shapes whose workspace exceeds its fixed scratch."""
+    L = F.lib()
+    call = lambda l, g, r, o: L.festina_score_placements_noalloc(C.byref(l), C.byref(g), C.byref(r),
+                                                                 C.byref(o), None)
+    lut, gpus, req, out = _structs(M=32, NS=8, NF=16, G=1024, W=64, R=1 << 22)
+    assert F.festina_placements_workspace_bytes(lut, gpus, req) > F.FESTINA_NOALLOC_WORKSPACE_BYTES
+    assert call(lut, gpus, req, out) == F.FESTINA_ERR_TOO_LARGE
+    lut, gpus, req, out = _structs(M=32, NS=8, NF=16, G=1024, W=64, R=262144)
+    assert F.festina_placements_workspace_bytes(lut, gpus, req) <= F.FESTINA_NOALLOC_WORKSPACE_BYTES
+    assert call(lut, gpus, req, out) == F.FESTINA_ERR_DEVICE          # fits, but there is no device here
+    for obj, field, value in [("lut", "n_rows", 16), ("lut", "pf", None), ("gpus", "n_gpus", 0),
+                              ("req", "model", None), ("out", "choice", None)]:
+        s = dict(zip(("lut", "gpus", "req", "out"), _structs()))
+        setattr(s[obj], field, value)
+        assert call(s["lut"], s["gpus"], s["req"], s["out"]) == F.FESTINA_ERR_INVALID, (obj, field)
+    assert call(*_structs(NS=16, NF=17)) == F.FESTINA_ERR_UNSUPPORTED
+    assert L.festina_score_placements_noalloc(None, C.byref(gpus), C.byref(req), C.byref(out), None) == \
+        F.FESTINA_ERR_INVALID
+    assert call(*_structs(R=0)) == F.FESTINA_OK                           # nothing to do
