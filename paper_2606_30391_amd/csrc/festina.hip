@@ -41,7 +41,14 @@ namespace {
 constexpr int kRows = FESTINA_N_ROWS;
 constexpr int kWave = 64;
 constexpr int kQ = 4;            // requests scored together by one wavefront
+constexpr int kNS8 = 8;
+constexpr int kClasses = kNS8 * kNS8;            // (cap_pf, cap_dc) pairs of 8 SM levels
+constexpr int kHcap = 256;                       // host records staged in LDS per chunk
+// A prompt latency at least this large keeps a normal value when divided by any Lout up to
+// 2^40 (2^-86 * 2^-40 = 2^-126, the least normal float).
+constexpr float kTinyLatency = 0x1p-86f;
 constexpr int kPrepBlock = 256;
+static_assert(kHcap == kPrepBlock, "a chunk's class sort takes one host per thread");
 constexpr float kInf = __builtin_huge_valf();
 // Value of a masked (SLO-missing) latency: a quiet NaN stays NaN through every multiply and
 // FMA whatever the sign of the power terms, and NaN < x is false, so it never wins.
@@ -97,6 +104,16 @@ struct PlaceArgs {
   ReqRec *preq;                  // [R] request records in bucket order
   int32_t *key;                  // [R]
   int32_t *off;                  // [R] position of request r within its bucket
+  // 8 x 16 tables: per model, its host list in chunks of kHcap hosts, each chunk grouped
+  // by SM-cap class
+  int32_t fast;
+  int32_t nch;                   // chunks per model, ceil(G / kHcap)
+  int32_t *host_pos;             // [M][G] slot of host i within its chunk's class order
+  int32_t *cls_tab;              // [M][nch][kClasses + 1] the chunk's non-empty classes
+  // table minima (for requests that no candidate can serve)
+  float *pf_rowmin;              // [M][32] least prefill entry of each row (NaN ignored)
+  float *pf_rowtiny;             // [M][32] least nonzero magnitude in each prefill row
+  float *dc_min;                 // [M] least decode entry of each model
 };
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -166,22 +183,85 @@ __device__ __forceinline__ int wave_scan(int v) {
   return v;
 }
 
-__global__ void k_zero(int32_t *p, int32_t n) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+__device__ __forceinline__ float wave_minf(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float o = __shfl_xor(v, off, kWave);
+    v = o < v ? o : v;
+  }
+  return v;
+}
+
+// Blocks [0, zb): clear the bucket counters.  Blocks [zb, zb + 8M): four prefill-table rows
+// each, one per wavefront: the least entry (NaN ignored) and the least nonzero magnitude.
+// Blocks [zb + 8M, zb + 9M): the least entry of one model's decode table.
+__global__ void __launch_bounds__(256) k_init(PlaceArgs a, int32_t zb, int32_t nb4) {
+  const int b = blockIdx.x;
+  if (b < zb) {
+    for (int i = b * 256 + (int)threadIdx.x; i < nb4; i += zb * 256) a.cnt[i] = 0;
+    return;
+  }
+  const int lane = threadIdx.x & (kWave - 1);
+  if (b < zb + 8 * a.M) {
+    const int row = (b - zb) * 4 + (int)(threadIdx.x >> 6);        // m * 32 + prompt row
+    const float *p = a.pf + (size_t)row * a.C;
+    float mn = kInf, tiny = kInf;
+    for (int c = lane; c < a.C; c += kWave) {
+      const float v = p[c], av = fabsf(v);
+      mn = v < mn ? v : mn;
+      tiny = av > 0.f && av < tiny ? av : tiny;
+    }
+    mn = wave_minf(mn);
+    tiny = wave_minf(tiny);
+    if (lane == 0) {
+      a.pf_rowmin[row] = mn;
+      a.pf_rowtiny[row] = tiny;
+    }
+    return;
+  }
+  __shared__ float part[256 / kWave];
+  const int m = b - zb - 8 * a.M;
+  const float *p = a.dc + (size_t)m * kRows * a.C;
+  float mn = kInf;
+  for (int c = threadIdx.x; c < kRows * a.C; c += 256) {
+    const float v = p[c];
+    mn = v < mn ? v : mn;
+  }
+  mn = wave_minf(mn);
+  if (lane == 0) part[threadIdx.x >> 6] = mn;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < 256 / kWave; ++i) mn = part[i] < mn ? part[i] : mn;
+    a.dc_min[m] = mn;
+  }
 }
 
 // The fields of request r that decide its bucket.
 struct ReqKeyFields {
   int m, w, pt, pr;
+  float st, sb;
 };
 __device__ __forceinline__ ReqKeyFields load_key_fields(const PlaceArgs &a, int r) {
-  return ReqKeyFields{a.model[r], a.wave ? a.wave[r] : 0, a.prompt[r], a.pred[r]};
+  return ReqKeyFields{a.model[r], a.wave ? a.wave[r] : 0, a.prompt[r], a.pred[r], a.slo_ttft[r], a.slo_tbt[r]};
+}
+
+// Prompt bucket of a token count: min(ceil(tokens / 256), 32) - 1 (unsigned: no overflow for
+// any int32 count; 0 tokens give -1, the decode batch row).
+__device__ __forceinline__ int prompt_row(int pt) {
+  return pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
 }
 
 // Validity and bucket key (wave, model, has-prompt) of request r from its fields.  Returns
-// the key, or -1 (and writes the infeasible result) for an invalid request.
+// the key, or -1 (and writes the infeasible result) for an invalid request and for one that
+// no candidate can serve: no entry of its model's decode table is below its TBT SLO, or no
+// entry of its prefill row is below its TTFT SLO (the SLO test of every candidate reads one
+// of those entries, so none can pass).
 __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const ReqKeyFields &f) {
-  const bool ok = f.m >= 0 && f.m < a.M && f.w >= 0 && f.w < a.W && f.pt >= 0 && f.pr >= 0;
+  bool ok = f.m >= 0 && f.m < a.M && f.w >= 0 && f.w < a.W && f.pt >= 0 && f.pr >= 0;
+  if (ok) {
+    const int row = prompt_row(f.pt);
+    ok = a.dc_min[f.m] < f.sb && (row < 0 || a.pf_rowmin[f.m * kRows + row] < f.st);
+  }
   if (!ok) {
     a.key[r] = -1;
     a.choice[r] = -1;
@@ -192,6 +272,58 @@ __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const Req
   const int k = ((f.w * a.M + f.m) << 1) | (f.pt == 0 ? 1 : 0);
   a.key[r] = k;
   return k;
+}
+
+// SM-cap classes are numbered so that ascending number means ascending
+// m = max(cap_pf, cap_dc): the 2m + 1 classes of m take the numbers m^2 .. (m + 1)^2 - 1.
+__device__ __forceinline__ int class_id(int p, int d) {
+  const int m = max(p, d);
+  return m * m + (p == m ? d : m + 1 + p);
+}
+// The inverse, as cap_pf * 8 + cap_dc.
+__device__ __forceinline__ int class_caps(int t) {
+  int m = 0;
+#pragma unroll
+  for (int k = 1; k < kNS8; ++k) m += t >= k * k;
+  const int r = t - m * m;
+  return r <= m ? m * kNS8 + r : (r - m - 1) * kNS8 + m;
+}
+
+// Model m's host list, in chunks of kHcap hosts, grouped by SM-cap class within each chunk
+// (8 x 16 tables): host_pos[m][i] = slot of host i within its chunk, and per chunk the list
+// of non-empty classes in ascending class number, each as cap_pf * 8 + cap_dc | first slot
+// << 6 | end slot << 15, with the count at [kClasses].  Caps outside [0, 7] (a GPU without
+// candidates) are clamped; absent cap arrays mean 7.  One block of kPrepBlock threads;
+// `cnt` is LDS scratch of kClasses ints.
+__device__ void sort_host_chunks(const PlaceArgs &a, int m, int hcnt, int *cnt) {
+  const int t = threadIdx.x;
+  for (int c0 = 0, ch = 0; c0 < hcnt; c0 += kHcap, ++ch) {
+    __syncthreads();                      // the host list is written; the counts are free
+    if (t < kClasses) cnt[t] = 0;
+    __syncthreads();
+    const int i = c0 + t;
+    int key = -1, rank = 0;
+    if (t < kHcap && i < hcnt) {
+      const int g = a.host_list[(size_t)m * a.G + i];
+      const int cp = a.cap_pf ? min(max((int)a.cap_pf[g], 0), kNS8 - 1) : kNS8 - 1;
+      const int cd = a.cap_dc ? min(max((int)a.cap_dc[g], 0), kNS8 - 1) : kNS8 - 1;
+      key = class_id(cp, cd);
+      rank = atomicAdd(&cnt[key], 1);
+    }
+    __syncthreads();
+    int *tab = a.cls_tab + ((size_t)m * a.nch + ch) * (kClasses + 1);
+    if (t < kWave) {                      // exclusive prefix over the 64 classes, compact list
+      const int n = cnt[t];
+      const int inc = wave_scan(n);
+      const unsigned long long ne = __ballot(n > 0);
+      const int pos = __popcll(ne & ((1ull << t) - 1ull));
+      if (n > 0) tab[pos] = class_caps(t) | ((inc - n) << 6) | (inc << 15);
+      if (t == kWave - 1) tab[kClasses] = __popcll(ne);
+      cnt[t] = inc - n;
+    }
+    __syncthreads();
+    if (key >= 0) a.host_pos[(size_t)m * a.G + i] = cnt[key] + rank;
+  }
 }
 
 __device__ const int8_t kNoCap = 0;                // read in place of absent cap arrays
@@ -269,6 +401,7 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
       __syncthreads();
     }
     if (threadIdx.x == 0) a.host_cnt[m] = base_s;
+    if (a.fast) sort_host_chunks(a, m, base_s, hist);
     return;
   }
   const long long i = (long long)(b - nbr - a.M) * kPrepBlock + threadIdx.x;
@@ -374,13 +507,17 @@ __global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
 // [1, 2^40]), and the SLOs.
 __device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
   const int pt = a.prompt[r];
+  const int m = a.model[r];
   ReqRec q;
   q.r = r;
-  q.row = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
+  q.row = prompt_row(pt);
   q.lout = (float)(((long long)a.pred[r] * 105 + 99) / 100);
   q.slo_ttft = a.slo_ttft[r];
   q.slo_tbt = a.slo_tbt[r];
-  q.rlout = q.lout >= 1.f && q.lout <= 0x1p40f ? 1.f / q.lout : 0.f;
+  // the 8 x 16 kernel scores prompt latencies divided by Lout: only while every entry of the
+  // prompt row keeps a normal value after the division (or is zero)
+  const bool tiny = a.fast && q.row >= 0 && m >= 0 && m < a.M && a.pf_rowtiny[m * kRows + q.row] < kTinyLatency;
+  q.rlout = q.lout >= 1.f && q.lout <= 0x1p40f && !tiny ? 1.f / q.lout : 0.f;
   q.pad[0] = q.pad[1] = 0;
   return q;
 }
@@ -756,55 +893,12 @@ __global__ void __launch_bounds__(256) k_score(PlaceArgs a) {
   score_tile_generic<CPL>(a, blockIdx.x, lds);
 }
 
-// ------------------------------------------------------------------ 8 x 16 scoring kernel
-// Tables of 8 SM levels x 16 frequency levels (128 cells).  Lane l owns cells 2l and 2l+1,
-// which share SM level j = l / 8, so a capped cell offset is one min on byte offsets,
-// min(j * 64, cap * 64) + k * 4, and the LDS offsets below are compile-time immediates.
-//
-// A workgroup takes a tile of WPB * kQF requests of one (wave, model) bucket; each
-// wavefront scores its kQF requests together against every hosting GPU.
-//   pass 1: per (request, cell) the minimum key over the GPUs, where a candidate's key is
-//           its energy divided by the request's Lout, Pp * (TT / Lout) + Pd * TBT (Eq.
-//           energy, Sec. 3.3).  The tile's GPU records are staged in LDS grouped by SM-cap
-//           class (cap_pf, cap_dc); the prompt rows are staged already divided by Lout,
-//           and per class the capped row values of the kQF requests and the power factors
-//           s*f^3 sit in registers, so each GPU costs one record and one TBT read.  Per candidate: one FMA and half a v_min3 (GPUs taken in pairs).
-//           Cells above max(cap_pf, cap_dc) repeat that level's cell exactly (same
-//           latencies, same power) at a higher index, so they get NaN power and never
-//           compete.  A wavefront with a request whose Lout is below 1 (or a prompt
-//           latency far outside the float range that division keeps normal) keeps TT and
-//           evaluates the energy itself: one multiply and one FMA per candidate.
-//   pass 2: K* = the wavefront minimum; for each cell whose minimum equals K*, the lowest
-//           GPU id whose key -- recomputed with the same operations, hence bit-identical
-//           -- equals K*; the smallest index (g * 128 + cell) wins.  That is the
-//           (key, index) lexicographic minimum, and the energy is Lout * K*.
-// Masked (SLO-missing) latencies are NaN, which min ignores and == never matches.
-constexpr int kQF = 8;
-constexpr int kC = 128;
+// ------------------------------------------------------------------ helpers of the 8 x 16 kernel
 constexpr int kXcds = 8;                         // MI355X: 8 XCDs, each with its own L2
-constexpr int kNS8 = 8;
-constexpr int kClasses = kNS8 * kNS8;            // (cap_pf, cap_dc) pairs
-constexpr int kHcap = 256;                       // host records staged in LDS per chunk
-constexpr int kWblkB = (1 + kQF) * kC * 4;       // per wave: s*f^3 row + kQF prompt rows
-// Decode-table rows are padded to 130 floats in LDS: row r starts at bank 2r, so pass-2
-// reads of one cell from many rows hit distinct banks, and rows stay 8-byte aligned.
-constexpr int kRowB = 130 * 4;
-
-__host__ __device__ constexpr int fast_rec_off(int wpb) { return wpb * kWblkB; }
-__host__ __device__ constexpr int fast_dcs_off(int wpb) { return wpb * kWblkB + kHcap * 16; }
-__host__ __device__ constexpr size_t fast_lds_bytes(int wpb) {
-  return (size_t)fast_dcs_off(wpb) + (size_t)kRows * kRowB;
-}
 
 typedef float v2f __attribute__((ext_vector_type(2)));
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ v2f lds2(const char *base, uint32_t off) {
-  return *reinterpret_cast<const v2f *>(base + off);
-}
-__device__ __forceinline__ float lds1(const char *base, uint32_t off) {
-  return *reinterpret_cast<const float *>(base + off);
-}
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 
 // v_min_f32 / v_min3_f32 as single instructions.  Operands are results of arithmetic or
 // +inf, and a quiet-NaN operand yields the other operands, which is the masking rule;
@@ -820,245 +914,6 @@ __device__ __forceinline__ float vmin3(float x, float y, float z) {
   return r;
 }
 
-// Energy of one candidate.  Pass 1 and pass 2 both evaluate exactly these operations.
-__device__ __forceinline__ float cell_energy(float kap, float pdp, float pdd, float tbt, float tt,
-                                            float p0, float lo, float slo_tbt) {
-  const float Pp = fmaf(kap, pdp, p0);
-  const float Pd = fmaf(kap, pdd, p0);
-  const float Ym = tbt < slo_tbt ? Pd * tbt : kMask;
-  return fmaf(lo, Ym, Pp * tt);
-}
-
-// The same candidate's energy divided by Lout (Lout >= 1): the key Pp * (TT / Lout) + Pd * TBT,
-// one FMA once TT / Lout is staged.  Lout is one positive scale per request, so the
-// request's keys are ordered as its energies (up to rounding), and its energy is Lout times
-// its least key.  Pass 1 and pass 2 both evaluate exactly these operations.
-__device__ __forceinline__ float cell_key(float kap, float pdp, float pdd, float tbt, float ttl, float p0,
-                                         float slo_tbt) {
-  const float Pp = fmaf(kap, pdp, p0);
-  const float Pd = fmaf(kap, pdd, p0);
-  const float Ym = tbt < slo_tbt ? Pd * tbt : kMask;
-  return fmaf(Pp, ttl, Ym);
-}
-
-// A prompt latency x scaled to s = x / Lout keeps its precision: s is NaN, infinite or
-// normal, or zero because x is.  (Class mask: signaling and quiet NaN, +-infinity,
-// +-normal.)
-__device__ __forceinline__ bool scaled_ok(float s, float x) {
-  return __builtin_amdgcn_classf(s, 0x30f) | (x == 0.f);
-}
-
-// TBT-SLO handling of pass 1:
-//   kPremasked  every live request of the tile has the same TBT SLO and the staged decode
-//               table already holds NaN where TBT misses it;
-//   kWaveSame   the wavefront's live requests share one TBT SLO: one test per (GPU, cell);
-//   kMixed      one test per (request, GPU, cell).
-enum { kPremasked = 0, kWaveSame = 1, kMixed = 2 };
-
-// Per-class registers of one wavefront: capped prompt-row values of its requests, the
-// power factors, and the decode-cell offset.
-struct ClassRegs {
-  v2f tt[kQF];
-  v2f pdp, pdd;
-  uint32_t mD;
-};
-
-template <int MODE>
-__device__ __forceinline__ void host_terms(const char *L, v4u r, const ClassRegs &cr, float p0, float sb0,
-                                           float (&Pp)[2], float (&Y)[2], float (&tbt)[2]) {
-  const float kap = __uint_as_float(r.y);
-  const v2f t = lds2(L, r.x + cr.mD);
-#pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    Pp[c] = fmaf(kap, cr.pdp[c], p0);
-    const float Pd = fmaf(kap, cr.pdd[c], p0);
-    tbt[c] = t[c];
-    Y[c] = MODE == kWaveSame ? (t[c] < sb0 ? Pd * t[c] : kMask) : Pd * t[c];
-  }
-}
-
-// Pass 1 over the records [cs, ce) of one class.  NORM: the staged prompt rows hold TT / Lout
-// and a candidate costs one FMA (its key); otherwise they hold TT and the candidate is its
-// energy.
-template <int MODE, bool NORM>
-__device__ __forceinline__ void class_pass1(const char *L, uint32_t recB, int cs, int ce, const ClassRegs &cr,
-                                            float p0, const float (&lo)[kQF], const float (&sb)[kQF],
-                                            float sb0, float (&mn)[kQF][2]) {
-  int i = cs;
-  for (; i + 1 < ce; i += 2) {
-    const v4u r0 = *reinterpret_cast<const v4u *>(L + recB + i * 16);
-    const v4u r1 = *reinterpret_cast<const v4u *>(L + recB + (i + 1) * 16);
-    float Pp0[2], Y0[2], T0[2], Pp1[2], Y1[2], T1[2];
-    host_terms<MODE>(L, r0, cr, p0, sb0, Pp0, Y0, T0);
-    host_terms<MODE>(L, r1, cr, p0, sb0, Pp1, Y1, T1);
-#pragma unroll
-    for (int q = 0; q < kQF; ++q)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const float y0 = MODE == kMixed ? (T0[c] < sb[q] ? Y0[c] : kMask) : Y0[c];
-        const float y1 = MODE == kMixed ? (T1[c] < sb[q] ? Y1[c] : kMask) : Y1[c];
-        if (NORM)
-          mn[q][c] = vmin3(mn[q][c], fmaf(Pp0[c], cr.tt[q][c], y0), fmaf(Pp1[c], cr.tt[q][c], y1));
-        else
-          mn[q][c] = vmin3(mn[q][c], fmaf(lo[q], y0, Pp0[c] * cr.tt[q][c]), fmaf(lo[q], y1, Pp1[c] * cr.tt[q][c]));
-      }
-  }
-  if (i < ce) {
-    const v4u r0 = *reinterpret_cast<const v4u *>(L + recB + i * 16);
-    float Pp0[2], Y0[2], T0[2];
-    host_terms<MODE>(L, r0, cr, p0, sb0, Pp0, Y0, T0);
-#pragma unroll
-    for (int q = 0; q < kQF; ++q)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const float y0 = MODE == kMixed ? (T0[c] < sb[q] ? Y0[c] : kMask) : Y0[c];
-        mn[q][c] = vmin(mn[q][c], NORM ? fmaf(Pp0[c], cr.tt[q][c], y0) : fmaf(lo[q], y0, Pp0[c] * cr.tt[q][c]));
-      }
-  }
-}
-
-// SM-cap classes are numbered so that ascending number means ascending
-// m = max(cap_pf, cap_dc): the 2m + 1 classes of m take the numbers m^2 .. (m + 1)^2 - 1.
-__device__ __forceinline__ int class_id(int p, int d) {
-  const int m = max(p, d);
-  return m * m + (p == m ? d : m + 1 + p);
-}
-// The inverse, as cap_pf * 8 + cap_dc.
-__device__ __forceinline__ int class_caps(int t) {
-  int m = 0;
-#pragma unroll
-  for (int k = 1; k < kNS8; ++k) m += t >= k * k;
-  const int r = t - m * m;
-  return r <= m ? m * kNS8 + r : (r - m - 1) * kNS8 + m;
-}
-
-// Per-class registers for the SM level at byte offset je64 of this lane; a level above
-// max(cap_pf, cap_dc) only repeats the class's top level, so its power is NaN.
-__device__ __forceinline__ ClassRegs class_regs(const char *L, uint32_t wblkB, uint32_t je64, uint32_t k04,
-                                                uint32_t cpB, uint32_t cdB) {
-  ClassRegs cr;
-  const uint32_t aP = wblkB + min(je64, cpB) + k04;
-  cr.mD = min(je64, cdB) + k04;
-  cr.pdp = lds2(L, aP);
-  cr.pdd = lds2(L, wblkB + cr.mD);
-  if (je64 > max(cpB, cdB)) cr.pdp = v2f{kMask, kMask};
-#pragma unroll
-  for (int q = 0; q < kQF; ++q) cr.tt[q] = lds2(L, aP + (1 + q) * kC * 4);
-  return cr;
-}
-
-// Pass 1 over one class in the common mode (premasked TBT, keys), H GPUs per step: H = 1
-// is the plain layout; H = 2 or 4 packs a class whose SM levels above m = max(cap_pf,
-// cap_dc) only repeat level m, with 8 / H levels per GPU (a power of two >= m + 1), so
-// lane l works on GPU (step start + slot), slot = (l / 8) / (8 / H), at SM level
-// (l / 8) % (8 / H).  The partial minima of one cell then sit in the lanes that share its
-// level until fold_levels gathers them.  A lane past the class's last GPU reads that GPU's
-// record with NaN power (with H = 1 every step's GPU exists and no lane needs the clamp).
-template <int H>
-__device__ __forceinline__ void class_pass1_common(const char *L, uint32_t recB, int cs, int ce,
-                                                   const ClassRegs &cr, float p0, int slot,
-                                                   float (&mn)[kQF][2]) {
-  constexpr bool ONE = H == 1;
-  if (ONE) slot = 0;
-  int i = cs;
-  for (; i + H < ce; i += 2 * H) {
-    const int h1 = i + H + slot;
-    const v4u r0 = *reinterpret_cast<const v4u *>(L + recB + (i + slot) * 16);
-    v4u r1 = *reinterpret_cast<const v4u *>(L + recB + (ONE ? h1 : min(h1, ce - 1)) * 16);
-    if (!ONE) r1.y = h1 < ce ? r1.y : __float_as_uint(kMask);
-    float Pp0[2], Y0[2], T0[2], Pp1[2], Y1[2], T1[2];
-    host_terms<kPremasked>(L, r0, cr, p0, 0.f, Pp0, Y0, T0);
-    host_terms<kPremasked>(L, r1, cr, p0, 0.f, Pp1, Y1, T1);
-#pragma unroll
-    for (int q = 0; q < kQF; ++q)
-#pragma unroll
-      for (int c = 0; c < 2; ++c)
-        mn[q][c] = vmin3(mn[q][c], fmaf(Pp0[c], cr.tt[q][c], Y0[c]), fmaf(Pp1[c], cr.tt[q][c], Y1[c]));
-  }
-  if (i < ce) {
-    const int h0 = i + slot;
-    v4u r0 = *reinterpret_cast<const v4u *>(L + recB + (ONE ? h0 : min(h0, ce - 1)) * 16);
-    if (!ONE) r0.y = h0 < ce ? r0.y : __float_as_uint(kMask);
-    float Pp0[2], Y0[2], T0[2];
-    host_terms<kPremasked>(L, r0, cr, p0, 0.f, Pp0, Y0, T0);
-#pragma unroll
-    for (int q = 0; q < kQF; ++q)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) mn[q][c] = vmin(mn[q][c], fmaf(Pp0[c], cr.tt[q][c], Y0[c]));
-  }
-}
-
-// Gathers packed partial minima: lanes whose SM levels agree modulo NLP combine (xor 16
-// and xor 32 over the lane index for NLP = 2, xor 32 for NLP = 4), lanes at levels below
-// NLP keep the result, and the others restart from +inf for the classes still to come.
-template <int NLP>
-__device__ __forceinline__ void fold_levels(float (&mn)[kQF][2], int j) {
-#pragma unroll
-  for (int q = 0; q < kQF; ++q)
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      float v = mn[q][c];
-      if (NLP <= 2) {
-        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-        v = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
-      }
-      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-      v = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
-      mn[q][c] = j < NLP ? v : kInf;
-    }
-}
-
-// Pass 1 over the class list of one chunk, every class in the plain layout.
-template <int MODE, bool NORM>
-__device__ __forceinline__ void pass1_classes(const char *L, uint32_t recB, uint32_t wblkB, const int *clist,
-                                              int ncls, uint32_t j64, uint32_t k04, float p0,
-                                              const float (&lo)[kQF], const float (&sb)[kQF], float sb0,
-                                              float (&mn)[kQF][2]) {
-  for (int k = 0; k < ncls; ++k) {
-    const int packed = uniform(clist[k]);
-    const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
-    const ClassRegs cr = class_regs(L, wblkB, j64, k04, (uint32_t)(cls / kNS8) * 64u, (uint32_t)(cls % kNS8) * 64u);
-    class_pass1<MODE, NORM>(L, recB, cs, ce, cr, p0, lo, sb, sb0, mn);
-  }
-}
-
-// Pass 1 over the classes [k, ncls) of one chunk in the common mode that have 8 / H levels per
-// GPU, H GPUs per step; returns the first class with more levels.
-template <int H>
-__device__ __forceinline__ int pass1_group(const char *L, uint32_t recB, uint32_t wblkB, const int *clist, int k,
-                                           int ncls, bool pk, int j, uint32_t k04, float p0, float (&mn)[kQF][2]) {
-  constexpr int lg = H == 4 ? 1 : H == 2 ? 2 : 3;   // log2 of the levels per GPU
-  for (; k < ncls; ++k) {
-    const int packed = uniform(clist[k]);
-    const int cls = packed & 63, cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
-    const int mc = max(cls / kNS8, cls % kNS8);
-    if (H > 1 && (!pk || (mc < 2 ? 1 : mc < 4 ? 2 : 3) != lg)) break;
-    const ClassRegs cr = class_regs(L, wblkB, (uint32_t)(j & ((1 << lg) - 1)) * 64u, k04,
-                                    (uint32_t)(cls / kNS8) * 64u, (uint32_t)(cls % kNS8) * 64u);
-    class_pass1_common<H>(L, recB, cs, ce, cr, p0, j >> lg, mn);
-  }
-  return k;
-}
-
-// Pass 1 over the class list of one chunk in the common mode.  With pk (the tile's GPUs fit
-// one chunk) capped classes are packed.  Classes come in ascending max cap m, so they form
-// three groups in order, each run by a loop of its own: m <= 1 (2 levels, 4 GPUs per step),
-// m = 2 or 3 (4 levels, 2 GPUs per step), each folded into the plain layout when it ends, and
-// m >= 4 (one GPU per step; every class without pk).
-__device__ __forceinline__ void pass1_common(const char *L, uint32_t recB, uint32_t wblkB, const int *clist,
-                                             int ncls, bool pk, int j, uint32_t k04, float p0,
-                                             float (&mn)[kQF][2]) {
-  int k = 0;
-  if (pk) {
-    const int k1 = pass1_group<4>(L, recB, wblkB, clist, 0, ncls, pk, j, k04, p0, mn);
-    if (k1 > 0) fold_levels<2>(mn, j);
-    const int k2 = pass1_group<2>(L, recB, wblkB, clist, k1, ncls, pk, j, k04, p0, mn);
-    if (k2 > k1) fold_levels<4>(mn, j);
-    k = k2;
-  }
-  pass1_group<1>(L, recB, wblkB, clist, k, ncls, pk, j, k04, p0, mn);
-}
-
 // DPP lane moves within rows of 16 lanes (every source lane exists).
 constexpr int kDppRor8 = 0x128;        // row_ror:8: lane i reads lane i ^ 8 of its row
 constexpr int kDppHalfMirror = 0x141;  // lane i reads lane 7 - i of its group of 8
@@ -1070,116 +925,316 @@ __device__ __forceinline__ float dpp(float x) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
 }
 
-// est[q] = min over the wavefront's lanes of min(m[q][0], m[q][1]), for the kQF = 8
-// requests at once, as a transposing reduction: each exchange halves the values a lane
-// holds (xor 32 and xor 16 by permlane swaps, xor 8 by DPP) until lane l holds request
-// l / 8's partial minimum, then three DPP steps reduce each group of 8 lanes.  Returns
-// est[l / 8] in lane l.
-__device__ __forceinline__ float wave_min8(const float (&m)[kQF][2], float (&est)[kQF]) {
-  static_assert(kQF == 8, "the exchange pattern is written for 8 requests per wavefront");
-  float v[8], u[4], w[2];
+// ------------------------------------------------------------------ 8 x 16 scoring kernel
+// Tables of 8 SM levels x 16 frequency levels (128 cells).  A workgroup takes a tile of
+// WPB * kR requests of one (wave, model) bucket; each wavefront scores its kR = 16
+// requests against every GPU hosting the model.
+//
+// A candidate's key is its energy divided by the request's Lout (Eq. energy, Sec. 3.3):
+//   key = Pp * (TTFT / Lout) + Pd * TBT,  Pp = P0 + k_g u_g s_jp f_k^3,  Pd = P0 + k_g u_g s_jd f_k^3,
+// one FMA once the request term x = TTFT / Lout is staged; Lout is one positive scale per
+// request, so its keys order as its energies (up to rounding) and its energy is Lout times
+// its least key.
+//
+// Lane l owns one cell of each of two ranges of SM levels, (j, k) = (l / 16, l % 16) in
+// range A (levels 0-3) and (4 + l / 16, l % 16) in range B (levels 4-7), and keeps the
+// request terms of both cells for the 16 requests in registers (xA, xB; NaN where TTFT misses
+// the SLO).  Pass 1 runs range A, then range B, over the tile's GPUs, which k_prep grouped by
+// SM-cap class (cap_pf, cap_dc) in ascending m = max(cap_pf, cap_dc); a GPU's cells above
+// level m repeat its level-m cells at a higher index, so they need no work.  Per class the
+// lanes fetch the capped request terms x(q, min(j, cap_pf), k) from xA / xB (ds_bpermute)
+// and the power factors; per GPU a lane reads one TBT value and forms Pp and Pd * TBT, shared
+// by its 16 requests: 16 FMA and 8 v_min3 per GPU for 16 candidates.  A class with one or two
+// levels in the range packs 4 or 2 GPUs per step (lane row l / 16 = GPU slot and level), and
+// the partial minima are folded back onto the level's own lanes when the group ends.
+//
+// Pass 2: K* = the request's least key (a transposing wavefront reduction over both ranges);
+// its tied cells are the lanes whose minimum equals K*, lowest first.  For each such cell the
+// lanes take (request l / 4, host 4 i + l % 4) and recompute the key with the operations of
+// pass 1 (hence bit-identical) in ascending host order; the first host reaching K* has the
+// lowest GPU id, giving the index g * 128 + cell, and the least index over tied cells wins:
+// the (key, index) lexicographic minimum.  The energy written is Lout * K*.
+//
+// Tiles whose requests mix TBT SLOs, or whose Lout or prompt latencies would lose precision
+// in the division (a request record with a zero reciprocal), run the generic kernel's tile
+// code instead; NaN is the mask value: a multiply or FMA with NaN stays NaN, v_min ignores it
+// and == never matches it.
+constexpr int kR = 16;                           // requests per wavefront
+constexpr int kRowPad = 130 * 4;                 // bytes per decode-table row in LDS
+constexpr uint32_t kL_dcs = 0;                                  // [32][130] decode table
+constexpr uint32_t kL_pd = kRows * kRowPad;                     // [128] s_j * f_k^3
+constexpr uint32_t kL_rec = kL_pd + 128 * 4;                    // [kHcap] records, class order
+constexpr uint32_t kL_rid = kL_rec + kHcap * 16;                // [kHcap] records, host order
+constexpr uint32_t kL_cls = kL_rid + kHcap * 16;                // [kClasses + 1] class list
+constexpr uint32_t kL_T = kL_cls + (kClasses + 1) * 4 + 12;     // per wave: [kR][8] pass-2 terms, then
+constexpr uint32_t kL_Tw = kR * 8 * 4 + kR * 8;                 // [kR] {K*, tied cell}; bytes per wave
+static_assert(kL_T % 16 == 0, "pass-2 tables start 16-byte aligned");
+__host__ __device__ constexpr size_t r16_lds_bytes(int wpb) { return kL_T + (size_t)wpb * kL_Tw; }
+
+__device__ __forceinline__ float bperm(uint32_t addr, float v) {
+  return __int_as_float(__builtin_amdgcn_ds_bpermute((int)addr, __float_as_int(v)));
+}
+
+// The key of one candidate; pass 1 and pass 2 both evaluate exactly these operations.
+__device__ __forceinline__ float r16_key(float kap, float pdp, float pdd, float tbt, float x, float p0) {
+  const float Pp = fmaf(kap, pdp, p0);
+  const float Y = fmaf(kap, pdd, p0) * tbt;
+  return fmaf(Pp, x, Y);
+}
+
+// Request terms and power factors of one class for this lane: level jl of the lane (range
+// start JB plus its row within the GPU's levels), capped at cap_pf for the prefill term and
+// power and at cap_dc for the decode latency and power; a level above max(cap_pf, cap_dc)
+// gets NaN power.
+struct R16Class {
+  float x[kR];
+  float pdp, pdd;
+  uint32_t mD;                   // byte offset of the decode cell within a table row
+};
+
+template <int JB>
+__device__ __forceinline__ void r16_class(const char *L, int jl, int kf, int cp, int cd, const float (&xA)[kR],
+                                          const float (&xB)[kR], R16Class &c) {
+  const int jp = min(jl, cp), jd = min(jl, cd);
+  c.pdp = jl > max(cp, cd) ? kMask : *reinterpret_cast<const float *>(L + kL_pd + (jp * 16 + kf) * 4);
+  c.pdd = *reinterpret_cast<const float *>(L + kL_pd + (jd * 16 + kf) * 4);
+  c.mD = (uint32_t)(jd * 16 + kf) * 4u;
+  const uint32_t src = (uint32_t)((jp & 3) * 16 + kf) * 4u;
+  if (JB == 0 || cp < 4) {               // the capped level lies in range A (uniform per class)
 #pragma unroll
-  for (int q = 0; q < 8; ++q) v[q] = vmin(m[q][0], m[q][1]);
-  // lanes 0-31 keep requests 0-3, lanes 32-63 requests 4-7
+    for (int q = 0; q < kR; ++q) c.x[q] = bperm(src, xA[q]);
+  } else {
+#pragma unroll
+    for (int q = 0; q < kR; ++q) c.x[q] = bperm(src, xB[q]);
+  }
+}
+
+// One GPU's shared terms for this lane: Pp and Pd * TBT (TBT premasked: NaN above the SLO).
+__device__ __forceinline__ void r16_gpu(const char *L, v4u r, const R16Class &c, float p0, float &Pp, float &Y) {
+  const float kap = __uint_as_float(r.y);
+  const float t = *reinterpret_cast<const float *>(L + r.x + c.mD);
+  Pp = fmaf(kap, c.pdp, p0);
+  Y = fmaf(kap, c.pdd, p0) * t;
+}
+
+// Pass 1 over the records [cs, ce) of one class, H GPUs per step (lane row / (4 / H) = slot).
+template <int H>
+__device__ __forceinline__ void r16_steps(const char *L, int cs, int ce, int slot, const R16Class &c, float p0,
+                                          float (&acc)[kR]) {
+  constexpr bool ONE = H == 1;
+  if (ONE) slot = 0;
+  int i = cs;
+  for (; i + H < ce; i += 2 * H) {
+    const int h1 = i + H + slot;
+    const v4u r0 = *reinterpret_cast<const v4u *>(L + kL_rec + (i + slot) * 16);
+    v4u r1 = *reinterpret_cast<const v4u *>(L + kL_rec + (ONE ? h1 : min(h1, ce - 1)) * 16);
+    if (!ONE) r1.y = h1 < ce ? r1.y : __float_as_uint(kMask);
+    float Pp0, Y0, Pp1, Y1;
+    r16_gpu(L, r0, c, p0, Pp0, Y0);
+    r16_gpu(L, r1, c, p0, Pp1, Y1);
+#pragma unroll
+    for (int q = 0; q < kR; ++q) acc[q] = vmin3(acc[q], fmaf(Pp0, c.x[q], Y0), fmaf(Pp1, c.x[q], Y1));
+  }
+  if (i < ce) {
+    const int h0 = i + slot;
+    v4u r0 = *reinterpret_cast<const v4u *>(L + kL_rec + (ONE ? h0 : min(h0, ce - 1)) * 16);
+    if (!ONE) r0.y = h0 < ce ? r0.y : __float_as_uint(kMask);
+    float Pp0, Y0;
+    r16_gpu(L, r0, c, p0, Pp0, Y0);
+#pragma unroll
+    for (int q = 0; q < kR; ++q) acc[q] = vmin(acc[q], fmaf(Pp0, c.x[q], Y0));
+  }
+}
+
+// Pass 1 over the classes [k, ncls) of one chunk that have n levels in range JB..JB+3, where n
+// = 1 (H = 4 GPUs per step), 2 (H = 2) or at least 3 (H = 1); returns the first other class.
+template <int JB, int H>
+__device__ __forceinline__ int r16_group(const char *L, int k, int ncls, const float (&xA)[kR],
+                                         const float (&xB)[kR], float p0, float (&acc)[kR]) {
+  constexpr int LP = 4 / H;                       // levels per GPU in a step
+  const int lane = __lane_id();
+  const int row = lane >> 4, kf = lane & 15;
+  const int jl = JB + row % LP;
+  const int slot = row / LP;
+  const int *cls = reinterpret_cast<const int *>(L + kL_cls);
+  for (; k < ncls; ++k) {
+    const int packed = uniform(cls[k]);
+    const int cp = (packed >> 3) & 7, cd = packed & 7;
+    const int cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
+    const int n = max(cp, cd) - JB + 1;           // levels of the range this class needs
+    if ((H == 4 && n != 1) || (H == 2 && n != 2)) break;
+    R16Class c;
+    r16_class<JB>(L, jl, kf, cp, cd, xA, xB, c);
+    r16_steps<H>(L, cs, ce, slot, c, p0, acc);
+  }
+  return k;
+}
+
+// Folds a packed group's partial minima onto the lanes of the levels they belong to: with
+// H = 4 rows 0-3 all hold level JB (row 0 takes the minimum of the four), with H = 2 rows
+// {0, 2} and {1, 3} hold levels JB and JB + 1 (rows 0 and 1 take the pairs' minima); the
+// other rows restart from +inf.  The other rows' values come by ds_bpermute (LDS pipe), so
+// a fold costs 2-3 VALU instructions per accumulator.
+template <int H>
+__device__ __forceinline__ void r16_fold(float (&acc)[kR]) {
+  const int row = __lane_id() >> 4;
+#pragma unroll
+  for (int q = 0; q < kR; ++q) {
+    float v = acc[q];
+    if (H == 4) {
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+      v = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    acc[q] = row < 4 / H ? v : kInf;
+  }
+}
+
+// Pass 1 of one chunk over range JB..JB+3 (classes in ascending m, so the groups come in the
+// order n = 1, 2, then more; classes with no level in the range come first and are skipped).
+template <int JB>
+__device__ __forceinline__ void r16_range(const char *L, int ncls, const float (&xA)[kR], const float (&xB)[kR],
+                                          float p0, float (&acc)[kR]) {
+  const int *cls = reinterpret_cast<const int *>(L + kL_cls);
+  int k = 0;
+  if (JB > 0)
+    while (k < ncls) {
+      const int packed = uniform(cls[k]);
+      if (max((packed >> 3) & 7, packed & 7) >= JB) break;
+      ++k;
+    }
+  const int k1 = r16_group<JB, 4>(L, k, ncls, xA, xB, p0, acc);
+  if (k1 > k) r16_fold<4>(acc);
+  const int k2 = r16_group<JB, 2>(L, k1, ncls, xA, xB, p0, acc);
+  if (k2 > k1) r16_fold<2>(acc);
+  r16_group<JB, 1>(L, k2, ncls, xA, xB, p0, acc);
+}
+
+// One value per request for the 16 requests at once: the reduction (OP) over the wavefront's
+// lanes of v[q], returned in lane l for request l / 4.  Each exchange halves the values a lane
+// holds: permlane32 pairs requests q and q + 8 (lanes 0-31 keep q, 32-63 keep q + 8),
+// permlane16 pairs q and q + 4 (row r keeps request 4r + q), a row rotation by 8 pairs q and
+// q + 2 (lane bit 3), the row half mirror pairs q and q + 1 (lane bit 2); two quad
+// permutations finish each group of 4.
+struct OpMinF {
+  __device__ static float f(float x, float y) { return vmin(x, y); }
+};
+struct OpMinI {
+  __device__ static int f(int x, int y) { return min(x, y); }
+};
+struct OpMaxI {
+  __device__ static int f(int x, int y) { return max(x, y); }
+};
+template <typename T>
+__device__ __forceinline__ unsigned bits_of(T x) {
+  unsigned u;
+  __builtin_memcpy(&u, &x, 4);
+  return u;
+}
+template <typename T>
+__device__ __forceinline__ T from_bits(unsigned u) {
+  T x;
+  __builtin_memcpy(&x, &u, 4);
+  return x;
+}
+template <typename T>
+__device__ __forceinline__ T dpp_t(T x, int) = delete;
+template <int CTRL, typename T>
+__device__ __forceinline__ T dppv(T x) {
+  return from_bits<T>((unsigned)__builtin_amdgcn_update_dpp(0, (int)bits_of(x), CTRL, 0xf, 0xf, false));
+}
+template <typename OP, typename T>
+__device__ __forceinline__ T wave_red16(const T (&v)[kR]) {
+  T u[8], w[4], c[2];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    const auto r = __builtin_amdgcn_permlane32_swap(bits_of(v[p]), bits_of(v[p + 8]), false, false);
+    u[p] = OP::f(from_bits<T>(r[0]), from_bits<T>(r[1]));
+  }
 #pragma unroll
   for (int p = 0; p < 4; ++p) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[p]), __float_as_uint(v[p + 4]), false, false);
-    u[p] = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    const auto r = __builtin_amdgcn_permlane16_swap(bits_of(u[p]), bits_of(u[p + 4]), false, false);
+    w[p] = OP::f(from_bits<T>(r[0]), from_bits<T>(r[1]));
   }
-  // even rows of 16 lanes keep the first two of their half's four, odd rows the last two
+  const int lane = __lane_id();
+  const bool b3 = (lane & 8) != 0, b2 = (lane & 4) != 0;
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(u[p]), __float_as_uint(u[p + 2]), false, false);
-    w[p] = vmin(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  for (int p = 0; p < 2; ++p) c[p] = OP::f(b3 ? w[p + 2] : w[p], dppv<kDppRor8>(b3 ? w[p] : w[p + 2]));
+  T d = OP::f(b2 ? c[1] : c[0], dppv<kDppHalfMirror>(b2 ? c[0] : c[1]));
+  d = OP::f(d, dppv<kDppQuad2301>(d));
+  d = OP::f(d, dppv<kDppQuad1032>(d));
+  return d;
+}
+
+// K* of the 16 requests: the minimum over both ranges' accumulators (lane l: request l / 4).
+__device__ __forceinline__ float wave_min16(const float (&a)[kR], const float (&b)[kR]) {
+  float v[kR];
+#pragma unroll
+  for (int q = 0; q < kR; ++q) v[q] = vmin(a[q], b[q]);
+  return wave_red16<OpMinF>(v);
+}
+
+// Cell value meaning "no tied cell left" (cells are 0-127).
+constexpr int kNoCell = 128;
+
+// v with lane LANE set to the wave-uniform value x (v_writelane_b32, the lane an immediate).
+// The compiler does not insert hazard wait states around inline assembly, so the asm brings
+// its own: five before (x may have just been written by a VALU instruction, e.g. a compare
+// writing VCC) and two after (the next instruction may read v through DPP).
+template <int LANE>
+__device__ __forceinline__ int writelane_imm(int v, int x) {
+  asm volatile("s_nop 4\n\tv_writelane_b32 %0, %1, %2\n\ts_nop 1" : "+v"(v) : "s"(x), "n"(LANE));
+  return v;
+}
+
+// Wave-level LDS barrier: stores by any lane of the wavefront are visible to its loads after.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Lanes 4q store request q's {K*, cell} at Qi + 8q, for the lanes' broadcast reads.
+__device__ __forceinline__ void r16_store_q(char *L, uint32_t Qi, float Kl, int cellv) {
+  const int lane = __lane_id();
+  if ((lane & 3) == 0) *reinterpret_cast<v2u *>(L + Qi + (lane >> 2) * 8) = v2u{__float_as_uint(Kl), (unsigned)cellv};
+  wave_sync();
+}
+
+// For each request q, its least tied cell above its previous one (the cell stored at Qi + 8q;
+// -1 before the first round): among the cells whose minimum equals K* (lane l of range A is
+// cell l, of range B cell 64 + l), the least one above it, for every request at once by a
+// wavefront min-reduction of (tied ? cell : kNoCell); an infeasible request has NaN stored as
+// its K*, which no minimum equals, so it gets kNoCell.  `more` tells whether some request has
+// a tied cell above the one returned (a max-reduction of the same cells).  Returns the cell in
+// every lane of request q's quad.  K* and the previous cell come from LDS as broadcast reads,
+// so that no per-request value occupies a scalar register.
+__device__ __forceinline__ int r16_next_cells(const char *L, uint32_t Qi, const float (&accA)[kR],
+                                              const float (&accB)[kR], bool &more) {
+  const int lane = __lane_id();
+  int lo[kR], hi[kR];
+#pragma unroll
+  for (int q = 0; q < kR; ++q) {
+    const v2u qi = *reinterpret_cast<const v2u *>(L + Qi + q * 8);
+    const float K = __uint_as_float(qi.x);
+    const int pv = (int)qi.y;
+    const int ca = accA[q] == K && lane > pv ? lane : kNoCell;
+    const int cb = accB[q] == K && 64 + lane > pv ? 64 + lane : kNoCell;
+    lo[q] = min(ca, cb);
+    hi[q] = max(ca == kNoCell ? -1 : ca, cb == kNoCell ? -1 : cb);
   }
-  // lanes with bit 3 clear keep the first of the two, the others the second
-  const bool hi = (__lane_id() & 8) != 0;
-  float c = vmin(hi ? w[1] : w[0], dpp<kDppRor8>(hi ? w[0] : w[1]));
-  c = vmin(c, dpp<kDppHalfMirror>(c));
-  c = vmin(c, dpp<kDppQuad2301>(c));
-  c = vmin(c, dpp<kDppQuad1032>(c));
-#pragma unroll
-  for (int q = 0; q < 8; ++q) est[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(c), 8 * q));
+  const int c = wave_red16<OpMinI>(lo);
+  const int top = wave_red16<OpMaxI>(hi);
+  more = __ballot(c < kNoCell && top > c) != 0ull;
   return c;
 }
 
-// One pass-2 round: for each request q with cell[q] >= 0, the lowest GPU id whose candidate at
-// that cell reaches the request's minimum est[q], recomputed with the operations of pass 1
-// (hence bit-identical); best[q] = min(best[q], g * 128 + cell).  Lane l takes host b0 + l of
-// the model's ascending host list, reads its record once and evaluates every request's
-// cell; the first set lane of a request's match mask is its lowest GPU id, so a request
-// stops at the first block of 64 hosts with a match.
-template <bool NRM>
-__device__ __forceinline__ void pass2_round(const PlaceArgs &a, const char *L, uint32_t recB, uint32_t dcsB,
-                                            uint32_t wblkB, const short *s_pos, const int32_t *hl, const HostRec *rw,
-                                            bool recs_in_lds, int hcnt, float p0, const int (&cell)[kQF],
-                                            const float (&est)[kQF], const float (&lo)[kQF], const float (&sb)[kQF],
-                                            int (&best)[kQF]) {
-  const int lane = __lane_id();
-  uint32_t cj64[kQF], ck4[kQF], base[kQF];
-  unsigned pending = 0;
-#pragma unroll
-  for (int q = 0; q < kQF; ++q) {
-    const int c = cell[q] >= 0 ? cell[q] : 0;
-    cj64[q] = (uint32_t)(c >> 4) * 64u;
-    ck4[q] = (uint32_t)(c & 15) * 4u;
-    base[q] = wblkB + ck4[q];
-    pending |= cell[q] >= 0 ? 1u << q : 0u;
-  }
-  for (int b0 = 0; b0 < hcnt && pending != 0u; b0 += kWave) {
-    const int i = b0 + lane;
-    const bool valid = i < hcnt;
-    const int ic = valid ? i : hcnt - 1;
-    uint32_t rowB;
-    int g, caps;
-    float kap;
-    if (recs_in_lds) {                    // host i (ascending GPU id) sits at slot s_pos[i]
-      const v4u r = *reinterpret_cast<const v4u *>(L + recB + (int)s_pos[ic] * 16);
-      rowB = r.x;
-      kap = __uint_as_float(r.y);
-      g = (int)r.z;
-      caps = (int)r.w;
-    } else {
-      g = hl[ic];
-      const HostRec r = rw[g];
-      rowB = dcsB + (uint32_t)(max(r.row_off, 0) / kC) * kRowB;
-      kap = r.kappa;
-      caps = r.caps;
-    }
-    const uint32_t cpB = (uint32_t)(caps & 0xff) * 64u, cdB = (uint32_t)((caps >> 8) & 0xff) * 64u;
-    const uint32_t mxB = max(cpB, cdB);
-#pragma unroll
-    for (int q = 0; q < kQF; ++q) {
-      // a cell above max(cap_pf, cap_dc) repeats a lower cell of the same GPU: pass 1 gave it
-      // NaN power, so it never matches
-      const uint32_t jP = min(cj64[q], cpB), jD = min(cj64[q], cdB);
-      const uint32_t aP = base[q] + jP, aD = base[q] + jD;
-      const float pdp = lds1(L, aP), pdd = lds1(L, aD);
-      const float tbt = lds1(L, rowB + jD + ck4[q]);
-      const float tt = lds1(L, aP + (1 + q) * kC * 4);
-      const float E = NRM ? cell_key(kap, pdp, pdd, tbt, tt, p0, sb[q])
-                          : cell_energy(kap, pdp, pdd, tbt, tt, p0, lo[q], sb[q]);
-      const bool hit = (E == est[q]) & valid & (cj64[q] <= mxB);
-      const unsigned long long m = __ballot(hit);
-      if (((pending >> q) & 1u) && m != 0ull) {
-        const int gw = __builtin_amdgcn_readlane(g, __builtin_ctzll(m));
-        best[q] = min(best[q], gw * kC + cell[q]);
-        pending &= ~(1u << q);
-      }
-    }
-  }
-}
-
 template <int WPB>
-__global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
+__global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
   extern __shared__ __align__(16) float lds[];
-  __shared__ int s_live[WPB], s_same[WPB], s_sb[WPB];
-  __shared__ int s_cls[kClasses + 1];     // class counts, then class starts
-  __shared__ int s_clist[kClasses + 1];   // non-empty classes: cls | start << 6 | end << 15; [64] = count
-  __shared__ short s_pos[kHcap];          // slot of host i's record after the class sort
+  __shared__ int s_ok[WPB];
   char *L = reinterpret_cast<char *>(lds);
-  constexpr uint32_t recB = fast_rec_off(WPB);
-  constexpr uint32_t dcsB = fast_dcs_off(WPB);
   constexpr int T = WPB * 64;
   // XCD-aware tile order: workgroups are dealt to the 8 XCDs round-robin, so XCD x takes
   // the contiguous tile range [x * per, (x + 1) * per) -- the same arrival waves and GPU
@@ -1200,261 +1255,216 @@ __global__ void __launch_bounds__(WPB * 64) k_score_c128(PlaceArgs a) {
   const int beg = tp[2 * t + 1];
   const int end = min(beg + a.tile, ro(a.bstart)[bucket + 1]);
 
-  // Staging and the class sort wait on memory and barriers while other workgroups' pass 1
-  // keeps the VALU busy: at a raised wavefront priority their instructions issue first, and
-  // pass 1 runs at the normal priority.
+  // Staging waits on memory and barriers while other workgroups' pass 1 keeps the VALU busy:
+  // at a raised wavefront priority its instructions issue first.
   __builtin_amdgcn_s_setprio(2);
   const int wv = uniform(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
-  const uint32_t wblkB = (uint32_t)wv * kWblkB;
-  const int j = lane >> 3;
-  const uint32_t j64 = (uint32_t)j * 64u;          // byte offset of SM level j in a row
-  const uint32_t k04 = (uint32_t)(lane & 7) * 8u;  // byte offset of frequency level 2 * (lane % 8)
+  const int q0 = beg + wv * kR;
+  const int nq = max(0, min(kR, end - q0));
+  // lane l holds the fields of request l / 4 (a missing request reads the tile's first
+  // record and is masked)
+  const bool has = (lane >> 2) < nq;
+  const ReqRec rq = load_req_lane(a, has ? q0 + (lane >> 2) : beg);
+  const float lo_has = has ? rq.lout : 0.f;
+  const ReqRec r0 = load_req(a, beg);     // the tile's first request (scalar)
   {
-    v2f pd;
-    pd.x = a.sm_level[j] * cube(a.freq_level[2 * (lane & 7)]);
-    pd.y = a.sm_level[j] * cube(a.freq_level[2 * (lane & 7) + 1]);
-    *reinterpret_cast<v2f *>(L + wblkB + j64 + k04) = pd;
-  }
-
-  // this wavefront's requests and their prompt rows
-  const int q0 = beg + wv * kQF;
-  const int nq = max(0, min(kQF, end - q0));
-  // Lane l stages 16 cells of request l / 8's prompt row and keeps that request's fields;
-  // a missing request reads the tile's first record and row 0 and is masked.  Rows: NaN
-  // where TTFT misses the SLO, scaled by 1 / Lout when every request of the wavefront has a
-  // usable reciprocal and every scaled value stays normal (or NaN), or is zero because the
-  // latency is.
-  const int sq = lane >> 3;
-  const bool shas = sq < nq;
-  bool nrm;
-  unsigned long long livem;
-  const ReqRec myr = load_req_lane(a, shas ? q0 + sq : beg);
-  const int r_l = shas ? myr.r : -1;
-  const float lo_l = shas ? myr.lout : 0.f;
-  const float sb_l = shas ? myr.slo_tbt : -kInf;
-  {
-    const float st = shas ? myr.slo_ttft : -kInf;
-    const float rl = shas ? myr.rlout : 1.f;
-    // lane l takes the 16-byte chunks l % 8 + 8u (u < 4) of the row, so each load and each
-    // store of a request's 8 lanes covers 128 contiguous bytes
-    const float *pr = a.pf + ((size_t)m * kRows + (shas ? myr.row : 0)) * kC;
-    const int x8 = lane & 7;
-    float v[16];
-    if ((reinterpret_cast<uintptr_t>(a.pf) & 15) == 0) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float4 x = reinterpret_cast<const float4 *>(pr)[8 * u + x8];
-        v[4 * u] = x.x;
-        v[4 * u + 1] = x.y;
-        v[4 * u + 2] = x.z;
-        v[4 * u + 3] = x.w;
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = pr[(8 * (u >> 2) + x8) * 4 + (u & 3)];
-    }
-    bool ok = rl > 0.f, any = false;
-    float sc[16];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      v[u] = v[u] < st ? v[u] : kMask;
-      sc[u] = v[u] * rl;
-      ok = ok & scaled_ok(sc[u], v[u]);
-      any = any | (v[u] == v[u]);
-    }
-    nrm = __ballot(!ok) == 0ull;
-    float4 *d = reinterpret_cast<float4 *>(L + wblkB + (1 + sq) * kC * 4);
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      d[8 * u + x8] = nrm ? make_float4(sc[4 * u], sc[4 * u + 1], sc[4 * u + 2], sc[4 * u + 3])
-                 : make_float4(v[4 * u], v[4 * u + 1], v[4 * u + 2], v[4 * u + 3]);
-    livem = __ballot(any);
-  }
-  // per-request uniform values: Lout and the TBT SLO from lane 8q
-  float lo[kQF], sb[kQF];
-#pragma unroll
-  for (int q = 0; q < kQF; ++q) {
-    lo[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lo_l), 8 * q));
-    sb[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sb_l), 8 * q));
-  }
-  // a request whose whole row is NaN is dead: infeasible whatever the TBT test says, so it
-  // takes no part in the TBT-SLO uniformity checks
-  bool live_any = false, wsame = true;
-  float sb0 = 0.f;
-#pragma unroll
-  for (int q = 0; q < kQF; ++q) {
-    if ((livem >> (8 * q)) & 0xffull) {
-      if (!live_any) sb0 = sb[q];
-      wsame = wsame && __float_as_int(sb[q]) == __float_as_int(sb0);
-      live_any = true;
-    }
-  }
-  if (lane == 0) {
-    s_live[wv] = live_any;
-    s_same[wv] = wsame;
-    s_sb[wv] = __float_as_int(sb0);
+    const bool ok = !has || (rq.rlout > 0.f && __float_as_int(rq.slo_tbt) == __float_as_int(r0.slo_tbt));
+    const unsigned long long bad = __ballot(!ok);
+    if (lane == 0) s_ok[wv] = bad == 0ull;
   }
   __syncthreads();
-  bool tile_live = false, tile_same = true;
-  int tile_sb = 0;
-  for (int v = 0; v < WPB; ++v) {
-    if (!s_live[v]) continue;
-    if (!tile_live) tile_sb = s_sb[v];
-    tile_same = tile_same && s_same[v] && s_sb[v] == tile_sb;
-    tile_live = true;
+  bool tile_ok = true;
+#pragma unroll
+  for (int v = 0; v < WPB; ++v) tile_ok = tile_ok && s_ok[v];
+  if (!tile_ok) {                         // mixed TBT SLOs or an unscalable request
+    score_tile_generic<2>(a, t, lds);
+    return;
   }
-  const float tsb = __int_as_float(tile_sb);
+  const float tsb = r0.slo_tbt;           // every request of the tile has this TBT SLO
 
-  {  // the model's decode table, rows padded to kRowB bytes; NaN where TBT misses the
-     // tile's common TBT SLO
-    const float *src = a.dc + (size_t)m * kRows * kC;
+  for (int c = threadIdx.x; c < 128; c += T)   // s_j * f_k^3 of cell j * 16 + k
+    *reinterpret_cast<float *>(L + kL_pd + c * 4) = a.sm_level[c >> 4] * cube(a.freq_level[c & 15]);
+  // request terms: x = TTFT / Lout where TTFT < the TTFT SLO, else NaN, at this lane's cell of
+  // each range, for the 16 requests (all loads requested before the first use).  Each
+  // request's prompt-row offset, SLO and 1 / Lout reach every lane by broadcast reads of the
+  // wavefront's LDS scratch (free until pass 2), not through scalar registers.
+  float xA[kR], xB[kR];
+  const uint32_t Tw = kL_T + (uint32_t)wv * kL_Tw;
+  if (nq > 0) {
+    if ((lane & 3) == 0)
+      *reinterpret_cast<v4u *>(L + Tw + (lane >> 2) * 16) =
+          v4u{(unsigned)((m * kRows + (has ? rq.row : 0)) * 128), has ? __float_as_uint(rq.slo_ttft) : __float_as_uint(-kInf),
+              has ? __float_as_uint(rq.rlout) : __float_as_uint(1.f), 0u};
+    wave_sync();
+#pragma unroll
+    for (int q = 0; q < kR; ++q) {
+      const unsigned off = reinterpret_cast<const v4u *>(L + Tw)[q].x;
+      xA[q] = a.pf[off + lane];
+      xB[q] = a.pf[off + 64 + lane];
+    }
+#pragma unroll
+    for (int q = 0; q < kR; ++q) {
+      const v4u f = reinterpret_cast<const v4u *>(L + Tw)[q];
+      const float st = __uint_as_float(f.y), rl = __uint_as_float(f.z);
+      xA[q] = xA[q] < st ? xA[q] * rl : kMask;
+      xB[q] = xB[q] < st ? xB[q] * rl : kMask;
+    }
+    wave_sync();                          // the scratch is reused by pass 2
+  }
+  {  // the model's decode table, rows padded to kRowPad bytes, NaN where TBT misses the SLO
+    const float *src = a.dc + (size_t)m * kRows * 128;
     if ((((uintptr_t)src) & 15) == 0) {
       const float4 *s4 = reinterpret_cast<const float4 *>(src);
-      for (int i = threadIdx.x; i < kRows * kC / 4; i += T) {
-        float4 v = s4[i];
-        if (tile_same) {
-          v.x = v.x < tsb ? v.x : kMask;
-          v.y = v.y < tsb ? v.y : kMask;
-          v.z = v.z < tsb ? v.z : kMask;
-          v.w = v.w < tsb ? v.w : kMask;
-        }
-        v2f *d = reinterpret_cast<v2f *>(L + dcsB + (i >> 5) * kRowB + (i & 31) * 16);
-        d[0] = v2f{v.x, v.y};
-        d[1] = v2f{v.z, v.w};
+#pragma unroll 4
+      for (int i = threadIdx.x; i < kRows * 128 / 4; i += T) {
+        const float4 v = s4[i];
+        v2f *d = reinterpret_cast<v2f *>(L + kL_dcs + (i >> 5) * kRowPad + (i & 31) * 16);
+        d[0] = v2f{v.x < tsb ? v.x : kMask, v.y < tsb ? v.y : kMask};
+        d[1] = v2f{v.z < tsb ? v.z : kMask, v.w < tsb ? v.w : kMask};
       }
     } else {
-      for (int i = threadIdx.x; i < kRows * kC; i += T) {
-        float v = src[i];
-        if (tile_same) v = v < tsb ? v : kMask;
-        *reinterpret_cast<float *>(L + dcsB + (i >> 7) * kRowB + (i & 127) * 4) = v;
+      for (int i = threadIdx.x; i < kRows * 128; i += T) {
+        const float v = src[i];
+        *reinterpret_cast<float *>(L + kL_dcs + (i >> 7) * kRowPad + (i & 127) * 4) = v < tsb ? v : kMask;
       }
     }
   }
 
-  float mn[kQF][2];
+  float accA[kR], accB[kR];
 #pragma unroll
-  for (int q = 0; q < kQF; ++q) mn[q][0] = mn[q][1] = kInf;
-
-  const int hcnt = tile_live ? ro(a.host_cnt)[m] : 0;   // a tile of dead requests scores nothing
-  const int32_t *hl = a.host_list + (size_t)m * a.G;
-  const HostRec *rw = a.recs + (size_t)w * a.G;
+  for (int q = 0; q < kR; ++q) accA[q] = accB[q] = kInf;
+  const int hcnt = ro(a.host_cnt)[m];
   const float p0 = a.p0;
-  constexpr int kPer = kHcap / T > 0 ? kHcap / T : 1;  // host records per thread per chunk
-  for (int c0 = 0; c0 < hcnt; c0 += kHcap) {
+  for (int c0 = 0, ch = 0; c0 < hcnt; c0 += kHcap, ++ch) {
     const int n = min(kHcap, hcnt - c0);
-    __syncthreads();                      // previous records no longer in use; table staged
-    __builtin_amdgcn_s_setprio(2);          // the next chunk's class sort
-    for (int i = threadIdx.x; i < kClasses; i += T) s_cls[i] = 0;
-    __syncthreads();
-    // records of this chunk, grouped by (cap_pf, cap_dc) class with an LDS counting sort,
-    // classes in ascending max(cap_pf, cap_dc)
-    v4u rec[kPer];
-    int key[kPer], rank[kPer];
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int i = u * T + threadIdx.x;
-      key[u] = -1;
-      if (i < n) {
-        const int g = hl[c0 + i];
-        const HostRec r = rw[g];
-        rec[u].x = dcsB + (uint32_t)(max(r.row_off, 0) / kC) * kRowB;
-        rec[u].y = __float_as_uint(r.kappa);
-        rec[u].z = (uint32_t)g;
-        rec[u].w = (uint32_t)r.caps;
-        key[u] = class_id(r.caps & 0xff, (r.caps >> 8) & 0xff);
-        rank[u] = atomicAdd(&s_cls[key[u]], 1);
-      }
+    __syncthreads();                      // the previous chunk's records are no longer read
+    __builtin_amdgcn_s_setprio(2);
+    for (int i = threadIdx.x; i < n; i += T) {   // this chunk's records, in class and host order
+      const int g = a.host_list[(size_t)m * a.G + c0 + i];
+      const int pos = a.host_pos[(size_t)m * a.G + c0 + i];
+      const HostRec h = a.recs[(size_t)w * a.G + g];
+      v4u e;
+      e.x = kL_dcs + (uint32_t)(max(h.row_off, 0) / 128) * kRowPad;
+      e.y = __float_as_uint(h.kappa);
+      e.z = (uint32_t)g;
+      e.w = (uint32_t)h.caps;
+      *reinterpret_cast<v4u *>(L + kL_rec + pos * 16) = e;
+      *reinterpret_cast<v4u *>(L + kL_rid + i * 16) = e;
     }
-    __syncthreads();
-    if (threadIdx.x < kWave) {            // exclusive prefix over the 64 classes, and the
-      const int cnt = s_cls[threadIdx.x];  // compact list of the non-empty ones
-      const int inc = wave_scan(cnt);
-      s_cls[threadIdx.x] = inc - cnt;
-      const unsigned long long ne = __ballot(cnt > 0);
-      const int pos = __popcll(ne & ((1ull << threadIdx.x) - 1ull));
-      if (cnt > 0) s_clist[pos] = class_caps(threadIdx.x) | ((inc - cnt) << 6) | (inc << 15);
-      if (threadIdx.x == kWave - 1) {
-        s_cls[kClasses] = inc;
-        s_clist[kClasses] = __popcll(ne);
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < kPer; ++u)
-      if (key[u] >= 0) {
-        const int pos = s_cls[key[u]] + rank[u];
-        *reinterpret_cast<v4u *>(L + recB + pos * 16) = rec[u];
-        s_pos[u * T + threadIdx.x] = (short)pos;
-      }
+    for (int i = threadIdx.x; i <= kClasses; i += T)
+      reinterpret_cast<int *>(L + kL_cls)[i] = a.cls_tab[((size_t)m * a.nch + ch) * (kClasses + 1) + i];
     __syncthreads();
     __builtin_amdgcn_s_setprio(0);
-    if (live_any) {
-      const int ncls = uniform(s_clist[kClasses]);
-      if (tile_same && nrm)
-        pass1_common(L, recB, wblkB, s_clist, ncls, hcnt <= kHcap, j, k04, p0, mn);
-      else if (nrm && wsame)
-        pass1_classes<kWaveSame, true>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
-      else if (nrm)
-        pass1_classes<kMixed, true>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
-      else if (tile_same)
-        pass1_classes<kPremasked, false>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
-      else if (wsame)
-        pass1_classes<kWaveSame, false>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
-      else
-        pass1_classes<kMixed, false>(L, recB, wblkB, s_clist, ncls, j64, k04, p0, lo, sb, sb0, mn);
+    if (nq > 0) {
+      const int ncls = uniform(reinterpret_cast<const int *>(L + kL_cls)[kClasses]);
+      r16_range<0>(L, ncls, xA, xB, p0, accA);
+      r16_range<4>(L, ncls, xA, xB, p0, accB);
     }
   }
+  if (nq == 0) return;
 
-  // pass 2: per request the winning energy E* (key K*: E* = Lout * K*), then the lowest index
-  // that reaches it.  One round per tied cell of a request (one round unless two different
-  // cells reach exactly E*); in a round every lane takes one host, in ascending GPU id.
-  const bool recs_in_lds = hcnt <= kHcap;
-  float est[kQF];
-  unsigned long long t0[kQF], t1[kQF];
-  bool rounds = false;
-  const float cmin = wave_min8(mn, est);   // request sq's minimum
+  // pass 2: per request the least key K* and, per tied cell in ascending order, the first host
+  // (ascending GPU id) reaching it
+  const float Kl = wave_min16(accA, accB);          // request lane / 4
+  // Lout of request lane / 4, 0 for a missing request (tested as a vector value so that no
+  // lane mask stays live in scalar registers across pass 1)
+  const float lo_l = lo_has;
+  const float Ks = lo_l > 0.f && Kl < kInf && lo_l * Kl < kInf ? Kl : kMask;   // NaN: infeasible
+  const bool recs_in_lds = hcnt <= kHcap;                     // T[q][j] at Tw + (8q + j) * 4
+  const uint32_t Qi = Tw + kR * 8 * 4;                        // {K*, cell} of request q at Qi + 8q
+  int best = INT_MAX;                                         // lanes of request q: its least index
+  bool more;
+  r16_store_q(L, Qi, Ks, -1);
+  int cellv = r16_next_cells(L, Qi, accA, accB, more);
+  while (__ballot(cellv < kNoCell) != 0ull) {
+    r16_store_q(L, Qi, Ks, cellv);
+    // T[q][j] = request q's term at level j and its tied cell's frequency level: lanes j < 8
+    // read lane (j % 4) * 16 + k of xA[q] (j < 4) or xB[q]; every request at once
 #pragma unroll
-  for (int q = 0; q < kQF; ++q) {
-    const bool feas = q < nq && (nrm ? lo[q] * est[q] : est[q]) < kInf;
-    t0[q] = __ballot(feas && mn[q][0] == est[q]);
-    t1[q] = __ballot(feas && mn[q][1] == est[q]);
-    rounds = rounds || (t0[q] | t1[q]) != 0ull;
-  }
-  int best[kQF];                          // lowest index reaching E*, per request
-#pragma unroll
-  for (int q = 0; q < kQF; ++q) best[q] = INT_MAX;
-  while (rounds) {
-    rounds = false;
-    int cell[kQF];                        // next tied cell of each request, ascending; -1: none
-#pragma unroll
-    for (int q = 0; q < kQF; ++q) {
-      cell[q] = -1;
-      if ((t0[q] | t1[q]) != 0ull) {
-        const int l0 = t0[q] ? __builtin_ctzll(t0[q]) : 64;
-        const int l1 = t1[q] ? __builtin_ctzll(t1[q]) : 64;
-        cell[q] = l0 <= l1 ? 2 * l0 : 2 * l1 + 1;
-        if (l0 <= l1)
-          t0[q] &= t0[q] - 1ull;
-        else
-          t1[q] &= t1[q] - 1ull;
-      }
-      rounds = rounds || (t0[q] | t1[q]) != 0ull;
+    for (int q = 0; q < kR; ++q) {
+      const int ck = (int)reinterpret_cast<const v2u *>(L + Qi + q * 8)->y & 15;
+      const uint32_t src = (uint32_t)((lane & 3) * 16 + ck) * 4u;
+      const float xa = bperm(src, xA[q]), xb = bperm(src, xB[q]);
+      if (lane < 8) *reinterpret_cast<float *>(L + Tw + (q * 8 + lane) * 4) = lane < 4 ? xa : xb;
     }
-    if (nrm)
-      pass2_round<true>(a, L, recB, dcsB, wblkB, s_pos, hl, rw, recs_in_lds, hcnt, p0, cell, est, lo, sb, best);
-    else
-      pass2_round<false>(a, L, recB, dcsB, wblkB, s_pos, hl, rw, recs_in_lds, hcnt, p0, cell, est, lo, sb, best);
-  }
-  // lane 8q writes request q: its record and minimum sit in lanes l / 8 = q
-  int myb = best[0];
+    wave_sync();
+    // Lanes take 64 hosts at a time in ascending order; each pending request is evaluated at
+    // its tied cell on all of them (four requests at a time, their LDS reads together), and
+    // its first matching lane is its lowest GPU id, so a request is done at the first block
+    // with a match.
+    unsigned long long pend = __ballot((lane & 3) == 0 && cellv < kNoCell);   // bit 4q: request q
+    for (int b0 = 0; b0 < hcnt && pend != 0ull; b0 += kWave) {
+      asm volatile("" ::: "memory");      // per-request values are reloaded in every block
+      const int i = b0 + lane;
+      const bool valid = i < hcnt;
+      const int ic = valid ? i : hcnt - 1;
+      uint32_t rowB;
+      float kap;
+      int g, caps;
+      if (recs_in_lds) {
+        const v4u r = *reinterpret_cast<const v4u *>(L + kL_rid + ic * 16);
+        rowB = r.x;
+        kap = __uint_as_float(r.y);
+        g = (int)r.z;
+        caps = (int)r.w;
+      } else {
+        g = a.host_list[(size_t)m * a.G + ic];
+        const HostRec hr = a.recs[(size_t)w * a.G + g];
+        rowB = kL_dcs + (uint32_t)(max(hr.row_off, 0) / 128) * kRowPad;
+        kap = hr.kappa;
+        caps = hr.caps;
+      }
+      const int cp = caps & 0xff, cd = (caps >> 8) & 0xff, mx = max(cp, cd);
 #pragma unroll
-  for (int q = 1; q < kQF; ++q) myb = sq == q ? best[q] : myb;
-  if ((lane & 7) == 0 && shas) {
-    const bool found = myb != INT_MAX;
-    a.choice[r_l] = found ? myb : -1;
-    a.feasible[r_l] = found ? 1 : 0;
-    a.energy[r_l] = found ? (nrm ? lo_l * cmin : cmin) : kInf;
+      for (int q0 = 0; q0 < kR; q0 += 4) {
+        if (((pend >> (4 * q0)) & 0x1111ull) == 0ull) continue;
+        bool hit[4];
+        int cq[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int q = q0 + t;
+          const v2u qi = *reinterpret_cast<const v2u *>(L + Qi + q * 8);
+          const float K = __uint_as_float(qi.x);
+          const int c = (int)qi.y;
+          cq[t] = c;
+          const int cj = c >> 4, ck = c & 15;
+          const int jp = min(cj, cp), jd = min(cj, cd);
+          const float pdp = *reinterpret_cast<const float *>(L + kL_pd + (jp * 16 + ck) * 4);
+          const float pdd = *reinterpret_cast<const float *>(L + kL_pd + (jd * 16 + ck) * 4);
+          const float tbt = *reinterpret_cast<const float *>(L + rowB + (uint32_t)(jd * 16 + ck) * 4u);
+          const float x = *reinterpret_cast<const float *>(L + Tw + (uint32_t)(q * 8 + jp) * 4u);
+          // a cell above max(cap_pf, cap_dc) repeats a lower cell of the same GPU: pass 1 gave
+          // it NaN power, so it never matches
+          hit[t] = valid && cj <= mx && r16_key(kap, pdp, pdd, tbt, x, p0) == K;
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int q = q0 + t;
+          const unsigned long long mk = __ballot(hit[t]);
+          if (((pend >> (4 * q)) & 1ull) && mk != 0ull) {
+            const int first = __builtin_ctzll(mk);
+            const int gw = __builtin_amdgcn_readlane(g, first);
+            best = (lane >> 2) == q ? min(best, gw * 128 + cq[t]) : best;
+            pend &= ~(1ull << (4 * q));
+          }
+        }
+      }
+    }
+    if (!more) break;
+    cellv = r16_next_cells(L, Qi, accA, accB, more);
+    wave_sync();                          // T is rewritten next round
+  }
+  // fresh copies of the lane id and Lout: tests on them are made here, not kept as lane masks
+  // in scalar registers through pass 2
+  int ln = lane;
+  float lo_w = lo_l;
+  asm volatile("" : "+v"(ln), "+v"(lo_w));
+  if ((ln & 3) == 0 && lo_w > 0.f) {
+    const bool found = best != INT_MAX;
+    a.choice[rq.r] = found ? best : -1;
+    a.feasible[rq.r] = found ? 1 : 0;
+    a.energy[rq.r] = found ? lo_l * Kl : kInf;
   }
 }
 
@@ -1623,8 +1633,9 @@ __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct PlaceLayout {
-  size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, preq, key, off, total;
-  int32_t NB, tile, max_tiles, waves_per_block;
+  size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, preq, key, off;
+  size_t host_pos, cls_tab, pf_rowmin, pf_rowtiny, dc_min, total;
+  int32_t NB, tile, max_tiles, waves_per_block, nch;
   bool fast;                     // 8 SM x 16 frequency levels: the specialised kernel
 };
 
@@ -1644,11 +1655,11 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   // tile size: large tiles amortise the table staging, small ones fill the chip
   const bool fast = L->n_sm == 8 && L->n_freq == 16;
   int wpb = 4, tile;
-  if (fast) {                    // one group of kQF requests per wavefront
-    tile = 4 * kQF;
+  if (fast) {                    // one group of kR requests per wavefront
+    tile = 4 * kR;
     if (R < 1024LL * tile) {
       wpb = 1;
-      tile = kQF;
+      tile = kR;
     }
   } else {
     tile = 2 * 4 * kQ;
@@ -1679,9 +1690,16 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->preq = take(sizeof(ReqRec) * (R > 0 ? R : 1));
   o->key = take(sizeof(int32_t) * (R > 0 ? R : 1));
   o->off = take(sizeof(int32_t) * (R > 0 ? R : 1));
+  const long long nch = fast ? (Gn + kHcap - 1) / kHcap : 0;
+  o->host_pos = take(sizeof(int32_t) * (fast ? M * Gn : 1));
+  o->cls_tab = take(sizeof(int32_t) * (fast ? M * nch * (kClasses + 1) : 1));
+  o->pf_rowmin = take(sizeof(float) * M * kRows);
+  o->pf_rowtiny = take(sizeof(float) * M * kRows);
+  o->dc_min = take(sizeof(float) * M);
   o->total = off;
+  o->nch = (int32_t)nch;
   o->NB = (int32_t)NB;
-  static_assert((kQF & (kQF - 1)) == 0 && (kQ & (kQ - 1)) == 0, "tile sizes are powers of two");
+  static_assert((kR & (kR - 1)) == 0 && (kQ & (kQ - 1)) == 0, "tile sizes are powers of two");
   o->tile = tile;                       // a power of two: the bucket scans shift by its log2
   o->max_tiles = (int32_t)max_tiles;
   o->waves_per_block = wpb;
@@ -1802,10 +1820,18 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
   a.preq = reinterpret_cast<ReqRec *>(ws + lay.preq);
   a.key = reinterpret_cast<int32_t *>(ws + lay.key);
   a.off = reinterpret_cast<int32_t *>(ws + lay.off);
+  a.fast = lay.fast ? 1 : 0;
+  a.nch = lay.nch;
+  a.host_pos = reinterpret_cast<int32_t *>(ws + lay.host_pos);
+  a.cls_tab = reinterpret_cast<int32_t *>(ws + lay.cls_tab);
+  a.pf_rowmin = reinterpret_cast<float *>(ws + lay.pf_rowmin);
+  a.pf_rowtiny = reinterpret_cast<float *>(ws + lay.pf_rowtiny);
+  a.dc_min = reinterpret_cast<float *>(ws + lay.dc_min);
 
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int zb = (nb4 + 255) / 256;
-  k_zero<<<zb < 1024 ? zb : 1024, 256, 0, st>>>(a.cnt, nb4);
+  int zb = (nb4 + 255) / 256;
+  zb = zb < 1024 ? zb : 1024;
+  k_init<<<zb + 9 * a.M, 256, 0, st>>>(a, zb, nb4);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int nbr = (a.R + kReqPerPrepBlock - 1) / kReqPerPrepBlock;
   const long long nrec = ((long long)a.W * a.G + kPrepBlock - 1) / kPrepBlock;
@@ -1822,7 +1848,7 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
   const int wpb = lay.waves_per_block;
   size_t lds = sizeof(float) * score_lds_floats((int)C, cpl, wpb);
   if (lay.fast) {
-    const size_t f = fast_lds_bytes(wpb);
+    const size_t f = r16_lds_bytes(wpb);
     lds = f > lds ? f : lds;
   }
   hipError_t e = mark(0, st);
@@ -1830,9 +1856,9 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
   if (lay.fast) {
     const int grid = (lay.max_tiles + kXcds - 1) / kXcds * kXcds;
     if (wpb == 4)
-      k_score_c128<4><<<grid, 4 * kWave, lds, st>>>(a);
+      k_score_r16<4><<<grid, 4 * kWave, lds, st>>>(a);
     else
-      k_score_c128<1><<<grid, kWave, lds, st>>>(a);
+      k_score_r16<1><<<grid, kWave, lds, st>>>(a);
     e = hipGetLastError();
   } else if (cpl == 1)
     e = launch_score<1>(a, lay.max_tiles, wpb, lds, st);
