@@ -91,13 +91,18 @@ struct PlaceArgs {
   uint8_t *feasible;
   float *energy;
   // workspace
-  int32_t NB;                    // buckets = 2 * W * M
+  int32_t NB;                    // buckets = 2 * W * M, numbered (2 m + prompt-less) * W + w
   int32_t tile;                  // requests per tile
   int32_t max_tiles;
+  int32_t gpad;                  // tiles per workgroup of the 8 x 16 kernel: the tiles of each
+                                 // (model, prompt kind) group are padded to a multiple of it
+                                 // with empty tiles (1: no padding)
+  int32_t scan_local;            // k_scatter scans the bucket counts itself (else k_scan)
   int32_t *cnt;                  // [NB4] counters
   int32_t *bstart;               // [NB + 1]
   int32_t *n_tiles;              // [1]
-  int2 *tiles;                   // [max_tiles] {bucket, first position}
+  int2 *tiles;                   // [max_tiles] {bucket, first position}; bucket -1: empty tile
+  int32_t *gscan;                // [2][2M + 1] group tile prefixes and pad prefixes (k_scan)
   int32_t *host_cnt;             // [M]
   int32_t *host_list;            // [M][G]
   HostRec *recs;                 // [W][G]
@@ -169,6 +174,20 @@ __device__ __forceinline__ ReqRec load_req_lane(const PlaceArgs &a, int pos) {
   q.rlout = __int_as_float(y.y);
   q.pad[0] = q.pad[1] = 0;
   return q;
+}
+
+// Buckets: the requests of one (wave, model, prompt kind).  The W buckets of a (model, prompt
+// kind) group are consecutive, so a group's tiles are contiguous in the tile table.
+__device__ __forceinline__ int bucket_of(const PlaceArgs &a, int w, int m, bool noprompt) {
+  return ((m << 1) | (noprompt ? 1 : 0)) * a.W + w;
+}
+struct BucketId {
+  int w, m;
+  bool noprompt;
+};
+__device__ __forceinline__ BucketId bucket_id(const PlaceArgs &a, int bucket) {
+  const int g = bucket / a.W;
+  return BucketId{bucket - g * a.W, g >> 1, (g & 1) != 0};
 }
 
 // ------------------------------------------------------------------ prologue kernels
@@ -269,7 +288,7 @@ __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const Req
     a.energy[r] = kInf;
     return -1;
   }
-  const int k = ((f.w * a.M + f.m) << 1) | (f.pt == 0 ? 1 : 0);
+  const int k = bucket_of(a, f.w, f.m, f.pt == 0);
   a.key[r] = k;
   return k;
 }
@@ -353,21 +372,28 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
       for (int k = threadIdx.x; k < a.NB; k += kPrepBlock) hist[k] = 0;
       __syncthreads();
     }
-    int key[U], pos[U];
+    // The LDS histogram is indexed wave-major, h = w * 2M + (2 m + prompt-less): requests that
+    // arrive together share w and spread over consecutive words (banks), where the bucket
+    // numbers, W apart, would all fall on one bank.
+    int key[U], pos[U], hk[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = b * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
       key[u] = r < a.R ? prep_request(a, r, f[u]) : -1;
-      pos[u] = key[u] >= 0 ? atomicAdd(local ? &hist[key[u]] : &a.cnt[key[u]], 1) : 0;
+      hk[u] = f[u].w * (2 * a.M) + ((f[u].m << 1) | (f[u].pt == 0 ? 1 : 0));
+      pos[u] = key[u] >= 0 ? atomicAdd(local ? &hist[hk[u]] : &a.cnt[key[u]], 1) : 0;
     }
     if (local) {
       __syncthreads();
-      for (int k = threadIdx.x; k < a.NB; k += kPrepBlock)
-        if (hist[k]) hist[k] = atomicAdd(&a.cnt[k], hist[k]);   // this block's base in bucket k
+      for (int h = threadIdx.x; h < a.NB; h += kPrepBlock)
+        if (hist[h]) {                  // this block's base in the bucket of histogram slot h
+          const int w = h / (2 * a.M), g = h - w * (2 * a.M);
+          hist[h] = atomicAdd(&a.cnt[g * a.W + w], hist[h]);
+        }
       __syncthreads();
 #pragma unroll
       for (int u = 0; u < U; ++u)
-        if (key[u] >= 0) pos[u] += hist[key[u]];
+        if (key[u] >= 0) pos[u] += hist[hk[u]];
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -428,12 +454,48 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
 
 constexpr int kScanLds = 16384;   // bucket counts staged in LDS by k_scan (64 KB)
 
+// Group padding: the 2M (model, prompt kind) groups each end with (gP[g] - gP[g + 1]) mod gpad
+// empty tiles.  gP holds the unpadded tile index of each group's first bucket, with the tile
+// total at [2M]; the scan writes pp[g] = the padded index of group g's first tile (gP[g] plus
+// the pads of the groups before it), pp[2M] = the padded total.  The whole block takes part;
+// s_a is LDS scratch of blockDim / 64 ints that no thread still reads; ends with a barrier.
+template <typename P>
+__device__ void scan_group_pads(const PlaceArgs &a, P gP, P pp, int *s_a) {
+  const int NG = 2 * a.M, T = blockDim.x, gm = a.gpad - 1;
+  const int per = (NG + T - 1) / T;
+  const int lo = min((int)threadIdx.x * per, NG), hi = min(lo + per, NG);
+  int s = 0;
+  for (int g = lo; g < hi; ++g) s += (gP[g] - gP[g + 1]) & gm;
+  const int is = wave_scan(s);
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  if (lane == kWave - 1) s_a[wv] = is;
+  __syncthreads();
+  int p = is - s, tot = 0;
+  for (int i = 0; i < T / kWave; ++i) {
+    if (i < wv) p += s_a[i];
+    tot += s_a[i];
+  }
+  for (int g = lo; g < hi; ++g) {
+    pp[g] = gP[g] + p;
+    p += (gP[g] - gP[g + 1]) & gm;
+  }
+  if (threadIdx.x == 0) pp[NG] = gP[NG] + tot;
+  __syncthreads();
+}
+
+// Table entries of bucket i (n requests from position pc; its first tile at index t): one per
+// tile of a.tile requests.
+__device__ __forceinline__ void put_tiles(const PlaceArgs &a, int i, int n, int pc, int t) {
+  const int nt = (n + a.tile - 1) >> __builtin_ctz((unsigned)a.tile);
+  for (int k = 0; k < nt; ++k) a.tiles[t + k] = make_int2(i, pc + k * a.tile);
+}
+
 // Scan body over bucket counts `cnt` (LDS copy or the global counters themselves).
 template <typename P>
 __device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_cnt, int *s_til) {
   const int T = blockDim.x;
   const int per = (a.NB + T - 1) / T;
-  const int lo = threadIdx.x * per;
+  const int lo = min((int)threadIdx.x * per, a.NB);
   const int hi = min(lo + per, a.NB);
   int c = 0, t = 0;
   for (int i = lo; i < hi; ++i) {
@@ -448,27 +510,60 @@ __device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_c
     s_til[wv] = it;
   }
   __syncthreads();
-  int pc = ic - c, pt = it - t;                  // exclusive prefix within the wave
+  int pc0 = ic - c, pt0 = it - t;                // exclusive prefix within the wave
   int tot_c = 0, tot_t = 0;
   for (int i = 0; i < T / kWave; ++i) {
     if (i < wv) {
-      pc += s_cnt[i];
-      pt += s_til[i];
+      pc0 += s_cnt[i];
+      pt0 += s_til[i];
     }
     tot_c += s_cnt[i];
     tot_t += s_til[i];
   }
-  for (int i = lo; i < hi; ++i) {
-    const int n = cnt[i];
-    a.bstart[i] = pc;
-    const int nt = (n + a.tile - 1) / a.tile;
-    for (int q = 0; q < nt; ++q) a.tiles[pt + q] = make_int2(i, pc + q * a.tile);
-    pc += n;
-    pt += nt;
+  const bool pad = a.gpad > 1;
+  int *gP = a.gscan, *pp = a.gscan + 2 * a.M + 1;
+  const int g0 = lo / a.W, w0 = lo - g0 * a.W;
+  {
+    int pc = pc0, pt = pt0, g = g0, wi = w0;
+    for (int i = lo; i < hi; ++i) {
+      const int n = cnt[i];
+      a.bstart[i] = pc;
+      if (!pad)
+        put_tiles(a, i, n, pc, pt);
+      else if (wi == 0)
+        gP[g] = pt;
+      pc += n;
+      pt += (n + a.tile - 1) / a.tile;
+      if (++wi == a.W) {
+        wi = 0;
+        ++g;
+      }
+    }
+  }
+  int pads = 0;
+  if (pad) {
+    if (threadIdx.x == 0) gP[2 * a.M] = tot_t;
+    __syncthreads();
+    scan_group_pads(a, gP, pp, s_cnt);
+    int pc = pc0, pt = pt0, g = g0, wi = w0;
+    for (int i = lo; i < hi; ++i) {
+      const int n = cnt[i];
+      const int nt = (n + a.tile - 1) / a.tile;
+      put_tiles(a, i, n, pc, pt - gP[g] + pp[g]);
+      if (wi == a.W - 1)                  // the group's empty tiles follow its last bucket
+        for (int k = pt + nt - gP[g] + pp[g]; k < pp[g + 1]; ++k) a.tiles[k] = make_int2(-1, 0);
+      pc += n;
+      pt += nt;
+      if (++wi == a.W) {
+        wi = 0;
+        ++g;
+      }
+    }
+    pads = pp[2 * a.M] - tot_t;
   }
   if (threadIdx.x == 0) {
     a.bstart[a.NB] = tot_c;
-    *a.n_tiles = tot_t;
+    *a.n_tiles = tot_t + pads;
   }
 }
 
@@ -525,9 +620,11 @@ __device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
 // Exclusive scans of the bucket counts (requests and tiles) inside one block of k_scatter,
 // into the LDS array `start`.  Thread t holds buckets [t*per, t*per + per), per a multiple
 // of 4 (at most 32), loaded by load_scan_counts as 8 int4 loads that are all in flight
-// before the first use; the counter array is padded to a multiple of 4 with zeros.  Every block scans all buckets
-// (a few KB from L2); the global starts and tiles of thread t's buckets are written by block
-// t mod grid, so the tile table is spread over the grid, and block 0 writes the totals.
+// before the first use; the counter array is padded to a multiple of 4 with zeros.  Every
+// block scans all buckets (a few KB from L2); the global starts of thread t's buckets are
+// written by block t mod grid, the tile table by every thread of the grid (one entry each,
+// its bucket found by a binary search over the buckets' first tiles in LDS), and block 0
+// writes the totals.
 constexpr int kScanChunks = kHistMax / kPrepBlock / 4;   // int4 chunks of counts per thread
 
 // Thread t's bucket range [lo, hi) of the block scan: per buckets, a multiple of 4.
@@ -545,6 +642,12 @@ __device__ __forceinline__ void load_scan_counts(const PlaceArgs &a, v4i (&v)[kS
   const int last4 = ((a.NB + 3) & ~3) - 4;
 #pragma unroll
   for (int q = 0; q < kScanChunks; ++q) v[q] = *reinterpret_cast<const v4i *>(a.cnt + min(lo + 4 * q, last4));
+}
+
+// LDS of block_scan_buckets (ints): [NB] bucket starts, [NB + 1] first tile of each bucket
+// and the tile total, then with group padding [2][2M + 1] group tables.
+__host__ __device__ constexpr long long block_scan_ints(long long NB, long long M, bool pad) {
+  return 2 * NB + 1 + (pad ? 2 * (2 * M + 1) : 0);
 }
 
 __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kScanChunks]) {
@@ -572,45 +675,98 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
     s_t[wv] = it;
   }
   __syncthreads();
-  int pc = ic - c, pt = it - t;
+  int pc0 = ic - c, pt0 = it - t;
   int tot_c = 0, tot_t = 0;
   for (int i = 0; i < kPrepBlock / kWave; ++i) {
     if (i < wv) {
-      pc += s_c[i];
-      pt += s_t[i];
+      pc0 += s_c[i];
+      pt0 += s_t[i];
     }
     tot_c += s_c[i];
     tot_t += s_t[i];
   }
-  // thread t's buckets are published by block t mod grid (every t < 256 names one block)
+  // thread t's bucket starts are published by block t mod grid (every t < 256 names one block)
   const bool writer = (int)threadIdx.x % (int)gridDim.x == (int)blockIdx.x;
+  const bool pad = a.gpad > 1;
+  int *ts = start + a.NB;                            // [NB + 1] unpadded first tile of each bucket
+  int *gP = ts + a.NB + 1, *pp = gP + 2 * a.M + 1;   // [2M + 1] each, with group padding
+  const int g0 = lo / a.W, w0 = lo - g0 * a.W;
+  {
+    int pc = pc0, pt = pt0, g = g0, wi = w0;
 #pragma unroll
-  for (int q = 0; q < V; ++q)
+    for (int q = 0; q < V; ++q)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int i = lo + 4 * q + e;
-      if (i < hi) {
-        const int n = v[q][e];
-        const int nt = (n + a.tile - 1) >> tsh;
-        start[i] = pc;
-        if (writer) {
-          a.bstart[i] = pc;
-          for (int k = 0; k < nt; ++k) a.tiles[pt + k] = make_int2(i, pc + k * a.tile);
+      for (int e = 0; e < 4; ++e) {
+        const int i = lo + 4 * q + e;
+        if (i < hi) {
+          const int n = v[q][e];
+          start[i] = pc;
+          ts[i] = pt;
+          if (writer) a.bstart[i] = pc;
+          if (pad && wi == 0) gP[g] = pt;
+          pc += n;
+          pt += (n + a.tile - 1) >> tsh;
+          if (++wi == a.W) {
+            wi = 0;
+            ++g;
+          }
         }
-        pc += n;
-        pt += nt;
+      }
+  }
+  if (threadIdx.x == 0) ts[a.NB] = tot_t;
+  int total = tot_t;
+  if (pad) {
+    if (threadIdx.x == 0) gP[2 * a.M] = tot_t;
+    __syncthreads();
+    scan_group_pads(a, gP, pp, s_c);
+    total = pp[2 * a.M];
+  } else {
+    __syncthreads();
+  }
+  // Padded tile k: its group g (pp[g] <= k < pp[g + 1]; an empty group's range is empty), its
+  // unpadded index u within the group's tiles, and the bucket l of the group with ts[l] <= u <
+  // ts[l + 1]; u past the group's tiles is one of its empty tiles.  Without padding the
+  // bucket is searched among all buckets.
+  for (int k = blockIdx.x * kPrepBlock + threadIdx.x; k < total; k += gridDim.x * kPrepBlock) {
+    int u = k, l = 0, h = a.NB;                      // ts[l] <= u < ts[h]
+    bool empty = false;
+    if (pad) {
+      int gl = 0, gh = 2 * a.M;                      // pp[gl] <= k < pp[gh]
+      while (gh - gl > 1) {
+        const int mid = (gl + gh) >> 1;
+        if (pp[mid] <= k)
+          gl = mid;
+        else
+          gh = mid;
+      }
+      u = k - pp[gl] + gP[gl];
+      empty = u >= gP[gl + 1];
+      l = gl * a.W;
+      h = l + a.W;
+    }
+    if (!empty) {
+      while (h - l > 1) {
+        const int mid = (l + h) >> 1;
+        if (ts[mid] <= u)
+          l = mid;
+        else
+          h = mid;
       }
     }
+    const int off = u - ts[l];
+    const int n = (l + 1 < a.NB ? start[l + 1] : tot_c) - start[l];
+    a.tiles[k] = !empty && off < ((n + a.tile - 1) >> tsh) ? make_int2(l, start[l] + off * a.tile) : make_int2(-1, 0);
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     a.bstart[a.NB] = tot_c;
-    *a.n_tiles = tot_t;
+    *a.n_tiles = total;
   }
-  __syncthreads();
 }
 
 // Requests grouped by bucket: request r goes to its bucket's start plus its position from
-// k_prep.  With at most kHistMax buckets each block scans the bucket counts itself (dynamic
-// LDS: starts [NB]); with more, k_scan has written the bucket starts.
+// k_prep.  With a.scan_local (at most kHistMax buckets, and the group tables fit beside the
+// starts in kScanLds ints of LDS) each block scans the bucket counts itself; otherwise k_scan
+// has written the bucket starts and the tile table.
 constexpr int kScatterU = kReqPerPrepBlock / kPrepBlock;
 
 // Request u of this thread: bucket key (-1: none), position and record.  Every load is issued
@@ -630,16 +786,16 @@ __device__ __forceinline__ void scatter_loads(const PlaceArgs &a, int (&key)[kSc
 }
 
 __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
-  extern __shared__ int start[];
+  extern __shared__ int start[];   // [NB] bucket starts, then with group padding [2][2M + 1]
   int key[kScatterU], pos[kScatterU];
   ReqRec rec[kScatterU];
-  if (a.NB <= kHistMax) {
+  if (a.scan_local) {
     // the bucket counts are requested together with the request fields: one round trip
     v4i cv[kScanChunks];
     load_scan_counts(a, cv);
     scatter_loads(a, key, pos, rec);
     __builtin_amdgcn_sched_barrier(0);   // no use of a loaded value is scheduled before a load
-    block_scan_buckets(a, start, cv);    // ends with a barrier
+    block_scan_buckets(a, start, cv);    // the bucket starts are complete on return
 #pragma unroll
     for (int u = 0; u < kScatterU; ++u)
       if (key[u] >= 0) a.preq[start[key[u]] + pos[u]] = rec[u];
@@ -672,41 +828,16 @@ __host__ __device__ constexpr size_t score_lds_floats(int C, int CPL, int waves)
   return (size_t)kRows * C + (size_t)kWave * CPL + C + (size_t)waves * kQ * C;
 }
 
-template <int CPL>
-__device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
+// The scoring loop of score_requests_generic for one kind of tile: MODE 0 prompt-less
+// requests, 1 GPUs without SM caps, 2 capped GPUs (one loop per kind keeps the kind's branch
+// out of the loop body).
+template <int CPL, int MODE>
+__device__ void generic_loop(const PlaceArgs &a, int m, int w, int beg, int end, int stride, float *lds) {
   const int C = a.C, NF = a.NF;
-  float *dcs = lds;                                   // [32 * C + pad] decode table of the tile's model
-  float *pds = lds + kRows * C + kWave * CPL;         // [C] s_j * f_k^3
-  float *rows = pds + C;                              // [waves][Q][C] prompt rows (capped GPUs)
+  float *dcs = lds;
+  float *pds = lds + kRows * C + kWave * CPL;
+  float *rows = pds + C;
 
-  const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
-  const int bucket = tp[2 * t];
-  const bool noprompt = bucket & 1;
-  const int wm = bucket >> 1;
-  const int w = wm / a.M, m = wm - (wm / a.M) * a.M;
-  const int beg = tp[2 * t + 1];
-  const int end = min(beg + a.tile, ro(a.bstart)[bucket + 1]);
-
-  // stage the model's decode table and the dynamic-power factors
-  {
-    const float *src = a.dc + (size_t)m * kRows * C;
-    const int n = kRows * C;
-    if ((((uintptr_t)src) & 15) == 0) {
-      const float4 *s4 = reinterpret_cast<const float4 *>(src);
-      float4 *d4 = reinterpret_cast<float4 *>(dcs);
-      for (int i = threadIdx.x; i < n / 4; i += blockDim.x) d4[i] = s4[i];
-    } else {
-      for (int i = threadIdx.x; i < n; i += blockDim.x) dcs[i] = src[i];
-    }
-    for (int i = threadIdx.x; i < kWave * CPL; i += blockDim.x) dcs[n + i] = 0.f;
-    for (int i = threadIdx.x; i < C; i += blockDim.x) {
-      const int j = i / NF, k = i - (i / NF) * NF;
-      pds[i] = a.sm_level[j] * cube(a.freq_level[k]);
-    }
-  }
-  __syncthreads();
-
-  const int nwaves = blockDim.x / kWave;
   const int wv = uniform(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
   float *myrows = rows + (size_t)wv * kQ * C;
@@ -714,29 +845,28 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
   const auto hl = ro(a.host_list + (size_t)m * a.G);
   const auto rw = ro(a.recs + (size_t)w * a.G);
   const float p0 = a.p0;
-  const bool caps = a.has_caps != 0;
 
   int cj[CPL], ck[CPL];
-  bool live[CPL];
+  int livev[CPL];                 // 1: a cell of the table, 0: a slot past the last cell
   float pdl[CPL];
 #pragma unroll
   for (int u = 0; u < CPL; ++u) {
     const int c = lane * CPL + u;
-    live[u] = c < C;
-    const int cc = live[u] ? c : 0;
+    livev[u] = c < C ? 1 : 0;
+    const int cc = c < C ? c : 0;
     cj[u] = cc / NF;
     ck[u] = cc - cj[u] * NF;
     pdl[u] = pds[cc];
   }
 
-  for (int base = beg + wv * kQ; base < end; base += nwaves * kQ) {
+  for (int base = beg; base < end; base += stride) {
     int rq[kQ];
     float lo[kQ], st[kQ], sb[kQ];
     int prw[kQ];
 #pragma unroll
     for (int q = 0; q < kQ; ++q) {
       const int pos = base + q;
-      const ReqRec rr = load_req(a, pos < end ? pos : beg);
+      const ReqRec rr = load_req_lane(a, pos < end ? pos : beg);   // in VGPRs: frees scalar registers
       rq[q] = pos < end ? rr.r : -1;
       if (rq[q] >= 0) {
         lo[q] = rr.lout;
@@ -760,7 +890,7 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
         bg[q][u] = -1;
       }
 
-    if (noprompt) {
+    if constexpr (MODE == 0) {
       // TTFT from the prefill table at the decode batch row (global, L2-resident)
       const float *pfm = a.pf + (size_t)m * kRows * C;
       for (int i = 0; i < hcnt; ++i) {
@@ -768,6 +898,14 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
         const HostRec rec = load_rec(rw, g);
         if (rec.row_off < 0) continue;
         const int cp = rec.caps & 0xff, cd = (rec.caps >> 8) & 0xff;
+        // the cell tests are remade per GPU from vector values, not held as lane masks in
+        // scalar registers across the loop
+        int lv[CPL];
+#pragma unroll
+        for (int u = 0; u < CPL; ++u) {
+          lv[u] = livev[u];
+          asm volatile("" : "+v"(lv[u]));
+        }
 #pragma unroll
         for (int u = 0; u < CPL; ++u) {
           const int cP = min(cj[u], cp) * NF + ck[u];
@@ -781,13 +919,13 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
 #pragma unroll
           for (int q = 0; q < kQ; ++q) {
             const float E = fmaf(lo[q], Y, X);
-            const bool ok = live[u] && ttft < st[q] && tbt < sb[q] && E < be[q][u];
+            const bool ok = lv[u] != 0 && ttft < st[q] && tbt < sb[q] && E < be[q][u];
             be[q][u] = ok ? E : be[q][u];
             bg[q][u] = ok ? g : bg[q][u];
           }
         }
       }
-    } else if (!caps) {
+    } else if constexpr (MODE == 1) {
       // uncapped: the request's TTFT cells stay in registers, masked by its TTFT SLO
       float tt[kQ][CPL];
 #pragma unroll
@@ -795,7 +933,7 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
         const float *pr = a.pf + ((size_t)m * kRows + prw[q]) * C;
 #pragma unroll
         for (int u = 0; u < CPL; ++u) {
-          const float v = (rq[q] >= 0 && live[u]) ? pr[lane * CPL + u] : kInf;
+          const float v = (rq[q] >= 0 && livev[u] != 0) ? pr[lane * CPL + u] : kInf;
           tt[q][u] = v < st[q] ? v : kMask;
         }
       }
@@ -837,6 +975,14 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
         const HostRec rec = load_rec(rw, g);
         if (rec.row_off < 0) continue;
         const int cp = rec.caps & 0xff, cd = (rec.caps >> 8) & 0xff;
+        // the cell tests are remade per GPU from vector values, not held as lane masks in
+        // scalar registers across the loop
+        int lv[CPL];
+#pragma unroll
+        for (int u = 0; u < CPL; ++u) {
+          lv[u] = livev[u];
+          asm volatile("" : "+v"(lv[u]));
+        }
 #pragma unroll
         for (int u = 0; u < CPL; ++u) {
           const int cP = min(cj[u], cp) * NF + ck[u];
@@ -849,7 +995,7 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
           for (int q = 0; q < kQ; ++q) {
             const float X = Pp * myrows[q * C + cP];
             const float E = fmaf(lo[q], Y, X);
-            const bool ok = live[u] && tbt < sb[q] && E < be[q][u];
+            const bool ok = lv[u] != 0 && tbt < sb[q] && E < be[q][u];
             be[q][u] = ok ? E : be[q][u];
             bg[q][u] = ok ? g : bg[q][u];
           }
@@ -884,6 +1030,57 @@ __device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
       }
     }
   }
+}
+
+// Requests [beg, end) of bucket positions, read by this wavefront kQ at a time from beg with
+// step `stride`, of model m and arrival wave w (both wave-uniform; beg = end: no requests).
+// The whole workgroup calls it (it stages the model's decode table in LDS).
+template <int CPL>
+__device__ void score_requests_generic(const PlaceArgs &a, int m, bool noprompt, int w, int beg, int end,
+                                       int stride, float *lds) {
+  const int C = a.C, NF = a.NF;
+  float *dcs = lds;                                   // [32 * C + pad] decode table of the tile's model
+  float *pds = lds + kRows * C + kWave * CPL;         // [C] s_j * f_k^3
+  float *rows = pds + C;                              // [waves][Q][C] prompt rows (capped GPUs)
+
+  // stage the model's decode table and the dynamic-power factors
+  {
+    const float *src = a.dc + (size_t)m * kRows * C;
+    const int n = kRows * C;
+    if ((((uintptr_t)src) & 15) == 0) {
+      const float4 *s4 = reinterpret_cast<const float4 *>(src);
+      float4 *d4 = reinterpret_cast<float4 *>(dcs);
+      for (int i = threadIdx.x; i < n / 4; i += blockDim.x) d4[i] = s4[i];
+    } else {
+      for (int i = threadIdx.x; i < n; i += blockDim.x) dcs[i] = src[i];
+    }
+    for (int i = threadIdx.x; i < kWave * CPL; i += blockDim.x) dcs[n + i] = 0.f;
+    for (int i = threadIdx.x; i < C; i += blockDim.x) {
+      const int j = i / NF, k = i - (i / NF) * NF;
+      pds[i] = a.sm_level[j] * cube(a.freq_level[k]);
+    }
+  }
+  __syncthreads();
+  if (noprompt)
+    generic_loop<CPL, 0>(a, m, w, beg, end, stride, lds);
+  else if (a.has_caps == 0)
+    generic_loop<CPL, 1>(a, m, w, beg, end, stride, lds);
+  else
+    generic_loop<CPL, 2>(a, m, w, beg, end, stride, lds);
+}
+
+// Tile t of the tile table: its bucket's requests [first, first + tile), wavefront v taking
+// kQ of them at positions first + v * kQ + i * waves * kQ.
+template <int CPL>
+__device__ void score_tile_generic(const PlaceArgs &a, int t, float *lds) {
+  const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
+  const int bucket = tp[2 * t];
+  const BucketId id = bucket_id(a, bucket);
+  const int first = tp[2 * t + 1];
+  const int end = min(first + a.tile, ro(a.bstart)[bucket + 1]);
+  const int nwaves = blockDim.x / kWave;
+  const int wv = uniform(threadIdx.x >> 6);
+  score_requests_generic<CPL>(a, id.m, id.noprompt, id.w, first + wv * kQ, end, nwaves * kQ, lds);
 }
 
 template <int CPL>
@@ -961,15 +1158,20 @@ __device__ __forceinline__ float dpp(float x) {
 // and == never matches it.
 constexpr int kR = 16;                           // requests per wavefront
 constexpr int kRowPad = 130 * 4;                 // bytes per decode-table row in LDS
+// Workgroup LDS: the model's decode table, the power factors, the chunk's class list and the
+// class-order slot of each host; then per wavefront its arrival wave's GPU records (class
+// order) and the pass-2 tables.
 constexpr uint32_t kL_dcs = 0;                                  // [32][130] decode table
 constexpr uint32_t kL_pd = kRows * kRowPad;                     // [128] s_j * f_k^3
-constexpr uint32_t kL_rec = kL_pd + 128 * 4;                    // [kHcap] records, class order
-constexpr uint32_t kL_rid = kL_rec + kHcap * 16;                // [kHcap] records, host order
-constexpr uint32_t kL_cls = kL_rid + kHcap * 16;                // [kClasses + 1] class list
-constexpr uint32_t kL_T = kL_cls + (kClasses + 1) * 4 + 12;     // per wave: [kR][8] pass-2 terms, then
-constexpr uint32_t kL_Tw = kR * 8 * 4 + kR * 8;                 // [kR] {K*, tied cell}; bytes per wave
-static_assert(kL_T % 16 == 0, "pass-2 tables start 16-byte aligned");
-__host__ __device__ constexpr size_t r16_lds_bytes(int wpb) { return kL_T + (size_t)wpb * kL_Tw; }
+constexpr uint32_t kL_cls = kL_pd + 128 * 4;                    // [kClasses + 1] class list
+constexpr uint32_t kL_hpos = kL_cls + (kClasses + 1) * 4 + 12;  // [kHcap] slot of chunk host i
+constexpr uint32_t kL_W = kL_hpos + kHcap * 4;                  // per wavefront, kLw bytes each:
+constexpr uint32_t kLw_rec = 0;                                 //   [kHcap] records, class order
+constexpr uint32_t kLw_T = kHcap * 16;                          //   [kR][8] pass-2 terms
+constexpr uint32_t kLw_Q = kLw_T + kR * 8 * 4;                  //   [kR] {K*, tied cell}
+constexpr uint32_t kLw = kLw_Q + kR * 8;
+static_assert(kL_W % 16 == 0 && kLw % 16 == 0, "per-wave tables start 16-byte aligned");
+__host__ __device__ constexpr size_t r16_lds_bytes(int wpb) { return kL_W + (size_t)wpb * kLw; }
 
 __device__ __forceinline__ float bperm(uint32_t addr, float v) {
   return __int_as_float(__builtin_amdgcn_ds_bpermute((int)addr, __float_as_int(v)));
@@ -1019,15 +1221,15 @@ __device__ __forceinline__ void r16_gpu(const char *L, v4u r, const R16Class &c,
 
 // Pass 1 over the records [cs, ce) of one class, H GPUs per step (lane row / (4 / H) = slot).
 template <int H>
-__device__ __forceinline__ void r16_steps(const char *L, int cs, int ce, int slot, const R16Class &c, float p0,
-                                          float (&acc)[kR]) {
+__device__ __forceinline__ void r16_steps(const char *L, const char *Rw, int cs, int ce, int slot, const R16Class &c,
+                                          float p0, float (&acc)[kR]) {
   constexpr bool ONE = H == 1;
   if (ONE) slot = 0;
   int i = cs;
   for (; i + H < ce; i += 2 * H) {
     const int h1 = i + H + slot;
-    const v4u r0 = *reinterpret_cast<const v4u *>(L + kL_rec + (i + slot) * 16);
-    v4u r1 = *reinterpret_cast<const v4u *>(L + kL_rec + (ONE ? h1 : min(h1, ce - 1)) * 16);
+    const v4u r0 = *reinterpret_cast<const v4u *>(Rw + (i + slot) * 16);
+    v4u r1 = *reinterpret_cast<const v4u *>(Rw + (ONE ? h1 : min(h1, ce - 1)) * 16);
     if (!ONE) r1.y = h1 < ce ? r1.y : __float_as_uint(kMask);
     float Pp0, Y0, Pp1, Y1;
     r16_gpu(L, r0, c, p0, Pp0, Y0);
@@ -1037,7 +1239,7 @@ __device__ __forceinline__ void r16_steps(const char *L, int cs, int ce, int slo
   }
   if (i < ce) {
     const int h0 = i + slot;
-    v4u r0 = *reinterpret_cast<const v4u *>(L + kL_rec + (ONE ? h0 : min(h0, ce - 1)) * 16);
+    v4u r0 = *reinterpret_cast<const v4u *>(Rw + (ONE ? h0 : min(h0, ce - 1)) * 16);
     if (!ONE) r0.y = h0 < ce ? r0.y : __float_as_uint(kMask);
     float Pp0, Y0;
     r16_gpu(L, r0, c, p0, Pp0, Y0);
@@ -1049,7 +1251,7 @@ __device__ __forceinline__ void r16_steps(const char *L, int cs, int ce, int slo
 // Pass 1 over the classes [k, ncls) of one chunk that have n levels in range JB..JB+3, where n
 // = 1 (H = 4 GPUs per step), 2 (H = 2) or at least 3 (H = 1); returns the first other class.
 template <int JB, int H>
-__device__ __forceinline__ int r16_group(const char *L, int k, int ncls, const float (&xA)[kR],
+__device__ __forceinline__ int r16_group(const char *L, const char *Rw, int k, int ncls, const float (&xA)[kR],
                                          const float (&xB)[kR], float p0, float (&acc)[kR]) {
   constexpr int LP = 4 / H;                       // levels per GPU in a step
   const int lane = __lane_id();
@@ -1065,7 +1267,7 @@ __device__ __forceinline__ int r16_group(const char *L, int k, int ncls, const f
     if ((H == 4 && n != 1) || (H == 2 && n != 2)) break;
     R16Class c;
     r16_class<JB>(L, jl, kf, cp, cd, xA, xB, c);
-    r16_steps<H>(L, cs, ce, slot, c, p0, acc);
+    r16_steps<H>(L, Rw, cs, ce, slot, c, p0, acc);
   }
   return k;
 }
@@ -1094,8 +1296,8 @@ __device__ __forceinline__ void r16_fold(float (&acc)[kR]) {
 // Pass 1 of one chunk over range JB..JB+3 (classes in ascending m, so the groups come in the
 // order n = 1, 2, then more; classes with no level in the range come first and are skipped).
 template <int JB>
-__device__ __forceinline__ void r16_range(const char *L, int ncls, const float (&xA)[kR], const float (&xB)[kR],
-                                          float p0, float (&acc)[kR]) {
+__device__ __forceinline__ void r16_range(const char *L, const char *Rw, int ncls, const float (&xA)[kR],
+                                          const float (&xB)[kR], float p0, float (&acc)[kR]) {
   const int *cls = reinterpret_cast<const int *>(L + kL_cls);
   int k = 0;
   if (JB > 0)
@@ -1104,11 +1306,11 @@ __device__ __forceinline__ void r16_range(const char *L, int ncls, const float (
       if (max((packed >> 3) & 7, packed & 7) >= JB) break;
       ++k;
     }
-  const int k1 = r16_group<JB, 4>(L, k, ncls, xA, xB, p0, acc);
+  const int k1 = r16_group<JB, 4>(L, Rw, k, ncls, xA, xB, p0, acc);
   if (k1 > k) r16_fold<4>(acc);
-  const int k2 = r16_group<JB, 2>(L, k1, ncls, xA, xB, p0, acc);
+  const int k2 = r16_group<JB, 2>(L, Rw, k1, ncls, xA, xB, p0, acc);
   if (k2 > k1) r16_fold<2>(acc);
-  r16_group<JB, 1>(L, k2, ncls, xA, xB, p0, acc);
+  r16_group<JB, 1>(L, Rw, k2, ncls, xA, xB, p0, acc);
 }
 
 // One value per request for the 16 requests at once: the reduction (OP) over the wavefront's
@@ -1236,38 +1438,48 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
   __shared__ int s_ok[WPB];
   char *L = reinterpret_cast<char *>(lds);
   constexpr int T = WPB * 64;
-  // XCD-aware tile order: workgroups are dealt to the 8 XCDs round-robin, so XCD x takes
-  // the contiguous tile range [x * per, (x + 1) * per) -- the same arrival waves and GPU
-  // records -- instead of every eighth tile.  per = ceil(n_tiles / 8) <= grid / 8.
-  const int ntiles = *ro(a.n_tiles);
-  const int per = (ntiles + kXcds - 1) / kXcds;
+  // Workgroup t takes tiles [WPB t, WPB t + WPB) of the table, all of one (model, prompt
+  // kind) group: the tiles of a group are contiguous and padded to a multiple of WPB, so the
+  // first is never empty.  Wavefront v scores tile WPB t + v: up to kR requests of one
+  // (arrival wave, model) bucket.
+  // XCD-aware order: workgroups are dealt to the 8 XCDs round-robin, so XCD x takes the
+  // contiguous range [x * per, (x + 1) * per) -- the same models -- instead of every eighth.
+  const int nblk = *ro(a.n_tiles) / WPB;
+  const int per = (nblk + kXcds - 1) / kXcds;
   const int idx = blockIdx.x / kXcds;
   const int t = (blockIdx.x % kXcds) * per + idx;
-  if (idx >= per || t >= ntiles) return;
+  if (idx >= per || t >= nblk) return;
   const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
-  const int bucket = tp[2 * t];
-  if (bucket & 1) {                       // prompt-less requests: TTFT from the batch row
-    score_tile_generic<2>(a, t, lds);
+  const int beg = tp[2 * WPB * t + 1];    // the workgroup's first request
+  const BucketId grp = bucket_id(a, tp[2 * WPB * t]);
+  const int m = grp.m;
+  const int wv = uniform(threadIdx.x >> 6);
+  const int bk = tp[2 * (WPB * t + wv)];  // this wavefront's bucket (-1: an empty tile)
+  const int q0 = bk >= 0 ? tp[2 * (WPB * t + wv) + 1] : beg;
+  const int nq = bk >= 0 ? min(kR, ro(a.bstart)[bk + 1] - q0) : 0;
+  const int w = bk >= 0 ? bucket_id(a, bk).w : 0;
+  if (grp.noprompt) {                     // prompt-less requests: TTFT from the batch row
+    score_requests_generic<2>(a, m, true, w, q0, q0 + nq, kQ, lds);
     return;
   }
-  const int wm = bucket >> 1;
-  const int w = wm / a.M, m = wm - (wm / a.M) * a.M;
-  const int beg = tp[2 * t + 1];
-  const int end = min(beg + a.tile, ro(a.bstart)[bucket + 1]);
 
   // Staging waits on memory and barriers while other workgroups' pass 1 keeps the VALU busy:
   // at a raised wavefront priority its instructions issue first.
   __builtin_amdgcn_s_setprio(2);
-  const int wv = uniform(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
-  const int q0 = beg + wv * kR;
-  const int nq = max(0, min(kR, end - q0));
-  // lane l holds the fields of request l / 4 (a missing request reads the tile's first
+  // lane l holds the fields of request l / 4 (a missing request reads the workgroup's first
   // record and is masked)
   const bool has = (lane >> 2) < nq;
   const ReqRec rq = load_req_lane(a, has ? q0 + (lane >> 2) : beg);
-  const float lo_has = has ? rq.lout : 0.f;
-  const ReqRec r0 = load_req(a, beg);     // the tile's first request (scalar)
+  float lo_has = has ? rq.lout : 0.f;
+  // the request's prompt-row offset, TTFT SLO and 1 / Lout for the request-term staging
+  // (a missing request: row 0, SLO -inf, so every term is masked)
+  v4u stage_rec = v4u{(unsigned)((m * kRows + (has ? rq.row : 0)) * 128),
+                      has ? __float_as_uint(rq.slo_ttft) : __float_as_uint(-kInf),
+                      has ? __float_as_uint(rq.rlout) : __float_as_uint(1.f), 0u};
+  // made here, not at their uses: the lane mask `has` is then dead before pass 1
+  asm volatile("" : "+v"(lo_has), "+v"(stage_rec));
+  const ReqRec r0 = load_req(a, beg);     // the workgroup's first request (scalar)
   {
     const bool ok = !has || (rq.rlout > 0.f && __float_as_int(rq.slo_tbt) == __float_as_int(r0.slo_tbt));
     const unsigned long long bad = __ballot(!ok);
@@ -1278,10 +1490,10 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
 #pragma unroll
   for (int v = 0; v < WPB; ++v) tile_ok = tile_ok && s_ok[v];
   if (!tile_ok) {                         // mixed TBT SLOs or an unscalable request
-    score_tile_generic<2>(a, t, lds);
+    score_requests_generic<2>(a, m, false, w, q0, q0 + nq, kQ, lds);
     return;
   }
-  const float tsb = r0.slo_tbt;           // every request of the tile has this TBT SLO
+  const float tsb = r0.slo_tbt;           // every request of the workgroup has this TBT SLO
 
   for (int c = threadIdx.x; c < 128; c += T)   // s_j * f_k^3 of cell j * 16 + k
     *reinterpret_cast<float *>(L + kL_pd + c * 4) = a.sm_level[c >> 4] * cube(a.freq_level[c & 15]);
@@ -1290,12 +1502,11 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
   // request's prompt-row offset, SLO and 1 / Lout reach every lane by broadcast reads of the
   // wavefront's LDS scratch (free until pass 2), not through scalar registers.
   float xA[kR], xB[kR];
-  const uint32_t Tw = kL_T + (uint32_t)wv * kL_Tw;
+  const uint32_t Wb = kL_W + (uint32_t)wv * kLw;   // this wavefront's tables
+  const uint32_t Tw = Wb + kLw_T;
+  const char *Rw = L + Wb + kLw_rec;
   if (nq > 0) {
-    if ((lane & 3) == 0)
-      *reinterpret_cast<v4u *>(L + Tw + (lane >> 2) * 16) =
-          v4u{(unsigned)((m * kRows + (has ? rq.row : 0)) * 128), has ? __float_as_uint(rq.slo_ttft) : __float_as_uint(-kInf),
-              has ? __float_as_uint(rq.rlout) : __float_as_uint(1.f), 0u};
+    if ((lane & 3) == 0) *reinterpret_cast<v4u *>(L + Tw + (lane >> 2) * 16) = stage_rec;
     wave_sync();
 #pragma unroll
     for (int q = 0; q < kR; ++q) {
@@ -1340,26 +1551,28 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
     const int n = min(kHcap, hcnt - c0);
     __syncthreads();                      // the previous chunk's records are no longer read
     __builtin_amdgcn_s_setprio(2);
-    for (int i = threadIdx.x; i < n; i += T) {   // this chunk's records, in class and host order
-      const int g = a.host_list[(size_t)m * a.G + c0 + i];
-      const int pos = a.host_pos[(size_t)m * a.G + c0 + i];
-      const HostRec h = a.recs[(size_t)w * a.G + g];
-      v4u e;
-      e.x = kL_dcs + (uint32_t)(max(h.row_off, 0) / 128) * kRowPad;
-      e.y = __float_as_uint(h.kappa);
-      e.z = (uint32_t)g;
-      e.w = (uint32_t)h.caps;
-      *reinterpret_cast<v4u *>(L + kL_rec + pos * 16) = e;
-      *reinterpret_cast<v4u *>(L + kL_rid + i * 16) = e;
-    }
+    for (int i = threadIdx.x; i < n; i += T)     // class-order slot of each chunk host
+      reinterpret_cast<int *>(L + kL_hpos)[i] = a.host_pos[(size_t)m * a.G + c0 + i];
+    if (nq > 0)
+      for (int i = lane; i < n; i += kWave) {    // this wavefront's GPU records, class order
+        const int g = a.host_list[(size_t)m * a.G + c0 + i];
+        const int pos = a.host_pos[(size_t)m * a.G + c0 + i];
+        const HostRec h = a.recs[(size_t)w * a.G + g];
+        v4u e;
+        e.x = kL_dcs + (uint32_t)(max(h.row_off, 0) / 128) * kRowPad;
+        e.y = __float_as_uint(h.kappa);
+        e.z = (uint32_t)g;
+        e.w = (uint32_t)h.caps;
+        *reinterpret_cast<v4u *>(L + Wb + kLw_rec + pos * 16) = e;
+      }
     for (int i = threadIdx.x; i <= kClasses; i += T)
       reinterpret_cast<int *>(L + kL_cls)[i] = a.cls_tab[((size_t)m * a.nch + ch) * (kClasses + 1) + i];
     __syncthreads();
     __builtin_amdgcn_s_setprio(0);
     if (nq > 0) {
       const int ncls = uniform(reinterpret_cast<const int *>(L + kL_cls)[kClasses]);
-      r16_range<0>(L, ncls, xA, xB, p0, accA);
-      r16_range<4>(L, ncls, xA, xB, p0, accB);
+      r16_range<0>(L, Rw, ncls, xA, xB, p0, accA);
+      r16_range<4>(L, Rw, ncls, xA, xB, p0, accB);
     }
   }
   if (nq == 0) return;
@@ -1372,7 +1585,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
   const float lo_l = lo_has;
   const float Ks = lo_l > 0.f && Kl < kInf && lo_l * Kl < kInf ? Kl : kMask;   // NaN: infeasible
   const bool recs_in_lds = hcnt <= kHcap;                     // T[q][j] at Tw + (8q + j) * 4
-  const uint32_t Qi = Tw + kR * 8 * 4;                        // {K*, cell} of request q at Qi + 8q
+  const uint32_t Qi = Wb + kLw_Q;                             // {K*, cell} of request q at Qi + 8q
   int best = INT_MAX;                                         // lanes of request q: its least index
   bool more;
   r16_store_q(L, Qi, Ks, -1);
@@ -1403,7 +1616,8 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
       float kap;
       int g, caps;
       if (recs_in_lds) {
-        const v4u r = *reinterpret_cast<const v4u *>(L + kL_rid + ic * 16);
+        const int slot = reinterpret_cast<const int *>(L + kL_hpos)[ic];
+        const v4u r = *reinterpret_cast<const v4u *>(Rw + slot * 16);
         rowB = r.x;
         kap = __uint_as_float(r.y);
         g = (int)r.z;
@@ -1633,10 +1847,12 @@ __global__ void __launch_bounds__(256) k_migrate(MigArgs a) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct PlaceLayout {
-  size_t cnt, bstart, ntiles, tiles, host_cnt, host_list, recs, preq, key, off;
+  size_t cnt, bstart, ntiles, tiles, gscan, host_cnt, host_list, recs, preq, key, off;
   size_t host_pos, cls_tab, pf_rowmin, pf_rowtiny, dc_min, total;
-  int32_t NB, tile, max_tiles, waves_per_block, nch;
+  int32_t NB, tile, max_tiles, waves_per_block, nch, gpad;
   bool fast;                     // 8 SM x 16 frequency levels: the specialised kernel
+  bool scan_local;               // k_scatter scans the bucket counts (no k_scan launch)
+  size_t scatter_lds;            // dynamic LDS bytes of k_scatter
 };
 
 bool place_shapes_ok(const festina_lut *L, const festina_gpus *G, const festina_requests *Q) {
@@ -1655,12 +1871,9 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   // tile size: large tiles amortise the table staging, small ones fill the chip
   const bool fast = L->n_sm == 8 && L->n_freq == 16;
   int wpb = 4, tile;
-  if (fast) {                    // one group of kR requests per wavefront
-    tile = 4 * kR;
-    if (R < 1024LL * tile) {
-      wpb = 1;
-      tile = kR;
-    }
+  if (fast) {                    // one tile of kR requests per wavefront
+    tile = kR;
+    if (R < 1024LL * 4 * kR) wpb = 1;
   } else {
     tile = 2 * 4 * kQ;
     if (R < 2048LL * tile) {
@@ -1672,7 +1885,10 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
     }
   }
   o->fast = fast;
-  const long long max_tiles = (R + tile - 1) / tile + NB;
+  // the 8 x 16 kernel's workgroups take wpb tiles of one (model, prompt kind) group: each of
+  // the 2M groups is padded with at most wpb - 1 empty tiles
+  const int gpad = fast ? wpb : 1;
+  const long long max_tiles = (R + tile - 1) / tile + NB + (long long)(gpad - 1) * 2 * M;
   if (max_tiles > INT_MAX - 8) return false;   // the grid is rounded up to a multiple of 8
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -1684,6 +1900,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->bstart = take(sizeof(int32_t) * (NB + 1));
   o->ntiles = take(sizeof(int32_t));
   o->tiles = take(sizeof(int2) * max_tiles);
+  o->gscan = take(sizeof(int32_t) * (gpad > 1 ? 2 * (2 * M + 1) : 1));
   o->host_cnt = take(sizeof(int32_t) * M);
   o->host_list = take(sizeof(int32_t) * M * Gn);
   o->recs = take(sizeof(HostRec) * W * Gn);
@@ -1703,6 +1920,10 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->tile = tile;                       // a power of two: the bucket scans shift by its log2
   o->max_tiles = (int32_t)max_tiles;
   o->waves_per_block = wpb;
+  o->gpad = gpad;
+  const long long scan_ints = block_scan_ints(NB, M, gpad > 1);
+  o->scan_local = NB <= kHistMax && scan_ints <= kScanLds;
+  o->scatter_lds = o->scan_local ? sizeof(int32_t) * (size_t)scan_ints : 0;
   return true;
 }
 
@@ -1809,11 +2030,14 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
   a.NB = lay.NB;
   a.tile = lay.tile;
   a.max_tiles = lay.max_tiles;
+  a.gpad = lay.gpad;
+  a.scan_local = lay.scan_local ? 1 : 0;
   a.cnt = reinterpret_cast<int32_t *>(ws + lay.cnt);
   const int nb4 = (lay.NB + 3) & ~3;      // counters padded with zeros to whole int4
   a.bstart = reinterpret_cast<int32_t *>(ws + lay.bstart);
   a.n_tiles = reinterpret_cast<int32_t *>(ws + lay.ntiles);
   a.tiles = reinterpret_cast<int2 *>(ws + lay.tiles);
+  a.gscan = reinterpret_cast<int32_t *>(ws + lay.gscan);
   a.host_cnt = reinterpret_cast<int32_t *>(ws + lay.host_cnt);
   a.host_list = reinterpret_cast<int32_t *>(ws + lay.host_list);
   a.recs = reinterpret_cast<HostRec *>(ws + lay.recs);
@@ -1837,12 +2061,11 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
   const long long nrec = ((long long)a.W * a.G + kPrepBlock - 1) / kPrepBlock;
   k_prep<<<(unsigned)(nbr + a.M + nrec), kPrepBlock, 0, st>>>(a, nbr);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  const bool local = lay.NB <= kHistMax;
-  if (!local) {
+  if (!lay.scan_local) {
     k_scan<<<1, 1024, lay.NB <= kScanLds ? sizeof(int) * lay.NB : 0, st>>>(a);
     if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   }
-  k_scatter<<<nbr, kPrepBlock, local ? sizeof(int) * lay.NB : 0, st>>>(a);
+  k_scatter<<<nbr, kPrepBlock, lay.scatter_lds, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   const int cpl = C <= 64 ? 1 : (C <= 128 ? 2 : 4);
   const int wpb = lay.waves_per_block;
@@ -1854,7 +2077,8 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
   hipError_t e = mark(0, st);
   if (e != hipSuccess) return FESTINA_ERR_DEVICE;
   if (lay.fast) {
-    const int grid = (lay.max_tiles + kXcds - 1) / kXcds * kXcds;
+    const int blocks = (lay.max_tiles + wpb - 1) / wpb;
+    const int grid = (blocks + kXcds - 1) / kXcds * kXcds;
     if (wpb == 4)
       k_score_r16<4><<<grid, 4 * kWave, lds, st>>>(a);
     else
