@@ -225,9 +225,14 @@ __global__ void __launch_bounds__(256) k_init(PlaceArgs a, int32_t zb, int32_t n
     const int row = (b - zb) * 4 + (int)(threadIdx.x >> 6);        // m * 32 + prompt row
     const float *p = a.pf + (size_t)row * a.C;
     float mn = kInf, tiny = kInf;
-    for (int c = lane; c < a.C; c += kWave) {
-      const float v = p[c], av = fabsf(v);
-      mn = v < mn ? v : mn;
+    constexpr int U = FESTINA_MAX_CELLS / kWave;                   // the row's loads together
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = lane + u * kWave < a.C ? p[lane + u * kWave] : kInf;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float av = fabsf(v[u]);
+      mn = v[u] < mn ? v[u] : mn;
       tiny = av > 0.f && av < tiny ? av : tiny;
     }
     mn = wave_minf(mn);
@@ -242,9 +247,13 @@ __global__ void __launch_bounds__(256) k_init(PlaceArgs a, int32_t zb, int32_t n
   const int m = b - zb - 8 * a.M;
   const float *p = a.dc + (size_t)m * kRows * a.C;
   float mn = kInf;
-  for (int c = threadIdx.x; c < kRows * a.C; c += 256) {
-    const float v = p[c];
-    mn = v < mn ? v : mn;
+  constexpr int U = 8;                                             // loads in flight per thread
+  for (int c0 = threadIdx.x; c0 < kRows * a.C; c0 += U * 256) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = c0 + u * 256 < kRows * a.C ? p[c0 + u * 256] : kInf;
+#pragma unroll
+    for (int u = 0; u < U; ++u) mn = v[u] < mn ? v[u] : mn;
   }
   mn = wave_minf(mn);
   if (lane == 0) part[threadIdx.x >> 6] = mn;
@@ -274,12 +283,16 @@ __device__ __forceinline__ int prompt_row(int pt) {
 // the key, or -1 (and writes the infeasible result) for an invalid request and for one that
 // no candidate can serve: no entry of its model's decode table is below its TBT SLO, or no
 // entry of its prefill row is below its TTFT SLO (the SLO test of every candidate reads one
-// of those entries, so none can pass).
+// of those entries, so none can pass).  The stored key carries kKeyTiny when the 8 x 16
+// kernel must not divide the request's prompt row by Lout (see make_req_rec).
+constexpr int kKeyTiny = 1 << 30;                 // bucket numbers stay below 2^30
 __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const ReqKeyFields &f) {
   bool ok = f.m >= 0 && f.m < a.M && f.w >= 0 && f.w < a.W && f.pt >= 0 && f.pr >= 0;
+  bool tiny = false;
   if (ok) {
     const int row = prompt_row(f.pt);
     ok = a.dc_min[f.m] < f.sb && (row < 0 || a.pf_rowmin[f.m * kRows + row] < f.st);
+    tiny = a.fast && row >= 0 && a.pf_rowtiny[f.m * kRows + row] < kTinyLatency;
   }
   if (!ok) {
     a.key[r] = -1;
@@ -289,7 +302,7 @@ __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const Req
     return -1;
   }
   const int k = bucket_of(a, f.w, f.m, f.pt == 0);
-  a.key[r] = k;
+  a.key[r] = k | (tiny ? kKeyTiny : 0);
   return k;
 }
 
@@ -308,13 +321,21 @@ __device__ __forceinline__ int class_caps(int t) {
   return r <= m ? m * kNS8 + r : (r - m - 1) * kNS8 + m;
 }
 
+// SM-cap class of GPU g for the 8 x 16 chunk sort: caps outside [0, 7] (a GPU without
+// candidates) are clamped; absent cap arrays mean 7.
+__device__ __forceinline__ int host_class(const PlaceArgs &a, int g) {
+  const int cp = a.cap_pf ? min(max((int)a.cap_pf[g], 0), kNS8 - 1) : kNS8 - 1;
+  const int cd = a.cap_dc ? min(max((int)a.cap_dc[g], 0), kNS8 - 1) : kNS8 - 1;
+  return class_id(cp, cd);
+}
+
 // Model m's host list, in chunks of kHcap hosts, grouped by SM-cap class within each chunk
 // (8 x 16 tables): host_pos[m][i] = slot of host i within its chunk, and per chunk the list
 // of non-empty classes in ascending class number, each as cap_pf * 8 + cap_dc | first slot
-// << 6 | end slot << 15, with the count at [kClasses].  Caps outside [0, 7] (a GPU without
-// candidates) are clamped; absent cap arrays mean 7.  One block of kPrepBlock threads;
-// `cnt` is LDS scratch of kClasses ints.
-__device__ void sort_host_chunks(const PlaceArgs &a, int m, int hcnt, int *cnt) {
+// << 6 | end slot << 15, with the count at [kClasses].  One block of kPrepBlock threads;
+// `cnt` is LDS scratch of kClasses ints; `keys` holds the class of each of the first nkeys
+// hosts in list order (LDS), the others are looked up.
+__device__ void sort_host_chunks(const PlaceArgs &a, int m, int hcnt, int *cnt, const int *keys, int nkeys) {
   const int t = threadIdx.x;
   for (int c0 = 0, ch = 0; c0 < hcnt; c0 += kHcap, ++ch) {
     __syncthreads();                      // the host list is written; the counts are free
@@ -323,10 +344,7 @@ __device__ void sort_host_chunks(const PlaceArgs &a, int m, int hcnt, int *cnt) 
     const int i = c0 + t;
     int key = -1, rank = 0;
     if (t < kHcap && i < hcnt) {
-      const int g = a.host_list[(size_t)m * a.G + i];
-      const int cp = a.cap_pf ? min(max((int)a.cap_pf[g], 0), kNS8 - 1) : kNS8 - 1;
-      const int cd = a.cap_dc ? min(max((int)a.cap_dc[g], 0), kNS8 - 1) : kNS8 - 1;
-      key = class_id(cp, cd);
+      key = i < nkeys ? keys[i] : host_class(a, a.host_list[(size_t)m * a.G + i]);
       rank = atomicAdd(&cnt[key], 1);
     }
     __syncthreads();
@@ -385,11 +403,19 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
     }
     if (local) {
       __syncthreads();
-      for (int h = threadIdx.x; h < a.NB; h += kPrepBlock)
-        if (hist[h]) {                  // this block's base in the bucket of histogram slot h
-          const int w = h / (2 * a.M), g = h - w * (2 * a.M);
-          hist[h] = atomicAdd(&a.cnt[g * a.W + w], hist[h]);
+      // slot h = w * 2M + g holds bucket g * W + w; (w, g) advance with h, no division per slot
+      const int NG = 2 * a.M;
+      const int dw = kPrepBlock / NG, dg = kPrepBlock - dw * NG;
+      int w = (int)threadIdx.x / NG, g = (int)threadIdx.x - w * NG;
+      for (int h = threadIdx.x; h < a.NB; h += kPrepBlock) {
+        if (hist[h]) hist[h] = atomicAdd(&a.cnt[g * a.W + w], hist[h]);   // this block's base
+        w += dw;
+        g += dg;
+        if (g >= NG) {
+          g -= NG;
+          ++w;
         }
+      }
       __syncthreads();
 #pragma unroll
       for (int u = 0; u < U; ++u)
@@ -401,33 +427,54 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
     return;
   }
   if (b < nbr + a.M) {
-    // ascending list of GPUs whose resident mask has bit m
+    // ascending list of GPUs whose resident mask has bit m, kHostU chunks of kPrepBlock GPUs
+    // per round with their mask words (and SM caps) requested together; with the 8 x 16
+    // tables each listed GPU's SM-cap class goes to LDS for the chunk sort
+    constexpr int kHostU = 4;
     const int m = b - nbr;
-    __shared__ int wsum[kPrepBlock / kWave];
-    __shared__ int base_s;
+    __shared__ int wsum[kHostU][kPrepBlock / kWave];
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x >> 6;
-    if (threadIdx.x == 0) base_s = 0;
-    __syncthreads();
-    for (int g0 = 0; g0 < a.G; g0 += kPrepBlock) {
-      const int g = g0 + threadIdx.x;
-      const bool has = g < a.G && ((a.resident[(size_t)g * a.words + (m >> 5)] >> (m & 31)) & 1u);
-      const unsigned long long bal = __ballot(has);
-      const int before = __popcll(bal & ((1ull << lane) - 1ull));
-      if (lane == 0) wsum[wv] = __popcll(bal);
-      __syncthreads();
-      int off = base_s;
-      for (int i = 0; i < wv; ++i) off += wsum[i];
-      if (has) a.host_list[(size_t)m * a.G + off + before] = g;
-      __syncthreads();
-      if (threadIdx.x == 0) {
-        int t = 0;
-        for (int i = 0; i < kPrepBlock / kWave; ++i) t += wsum[i];
-        base_s += t;
+    int *keys = hist + kClasses;                   // classes of the first nkeys listed hosts
+    const int nkeys = kHistMax - kClasses;
+    int base = 0;
+    for (int G0 = 0; G0 < a.G; G0 += kHostU * kPrepBlock) {
+      bool has[kHostU];
+      int key[kHostU];
+#pragma unroll
+      for (int u = 0; u < kHostU; ++u) {
+        const int g = G0 + u * kPrepBlock + threadIdx.x;
+        const int gc = min(g, a.G - 1);
+        has[u] = g < a.G && ((a.resident[(size_t)gc * a.words + (m >> 5)] >> (m & 31)) & 1u);
+        key[u] = a.fast ? host_class(a, gc) : 0;
+      }
+      int before[kHostU];
+#pragma unroll
+      for (int u = 0; u < kHostU; ++u) {
+        const unsigned long long bal = __ballot(has[u]);
+        before[u] = __popcll(bal & ((1ull << lane) - 1ull));
+        if (lane == 0) wsum[u][wv] = __popcll(bal);
       }
       __syncthreads();
+      int off = base;
+#pragma unroll
+      for (int u = 0; u < kHostU; ++u) {
+        int tot = 0, mine = off;
+        for (int i = 0; i < kPrepBlock / kWave; ++i) {
+          if (i < wv) mine += wsum[u][i];
+          tot += wsum[u][i];
+        }
+        if (has[u]) {
+          const int g = G0 + u * kPrepBlock + threadIdx.x;
+          a.host_list[(size_t)m * a.G + mine + before[u]] = g;
+          if (mine + before[u] < nkeys) keys[mine + before[u]] = key[u];
+        }
+        off += tot;
+      }
+      base = off;
+      __syncthreads();                            // wsum is rewritten next round
     }
-    if (threadIdx.x == 0) a.host_cnt[m] = base_s;
-    if (a.fast) sort_host_chunks(a, m, base_s, hist);
+    if (threadIdx.x == 0) a.host_cnt[m] = base;
+    if (a.fast) sort_host_chunks(a, m, base, hist, keys, nkeys);
     return;
   }
   const long long i = (long long)(b - nbr - a.M) * kPrepBlock + threadIdx.x;
@@ -599,20 +646,19 @@ __global__ void __launch_bounds__(1024) k_scan(PlaceArgs a) {
 // Record of valid request r: prompt bucket min(ceil(tokens / 256), 32) - 1 (unsigned: no
 // overflow for any int32 token count; 0 tokens -> -1, the decode batch row), the 5% output
 // pad ceil(1.05 * pred) = (105 * pred + 99) / 100 in 64-bit, its reciprocal (0 outside
-// [1, 2^40]), and the SLOs.
+// [1, 2^40]), and the SLOs.  The 8 x 16 kernel scores prompt latencies divided by Lout: only
+// while every entry of the prompt row keeps a normal value after the division (or is zero);
+// for a row with a smaller nonzero entry k_prep flags the key (kKeyTiny) and take_key sets
+// the reciprocal to 0, which sends the request's tile to the generic code.
 __device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
   const int pt = a.prompt[r];
-  const int m = a.model[r];
   ReqRec q;
   q.r = r;
   q.row = prompt_row(pt);
   q.lout = (float)(((long long)a.pred[r] * 105 + 99) / 100);
   q.slo_ttft = a.slo_ttft[r];
   q.slo_tbt = a.slo_tbt[r];
-  // the 8 x 16 kernel scores prompt latencies divided by Lout: only while every entry of the
-  // prompt row keeps a normal value after the division (or is zero)
-  const bool tiny = a.fast && q.row >= 0 && m >= 0 && m < a.M && a.pf_rowtiny[m * kRows + q.row] < kTinyLatency;
-  q.rlout = q.lout >= 1.f && q.lout <= 0x1p40f && !tiny ? 1.f / q.lout : 0.f;
+  q.rlout = q.lout >= 1.f && q.lout <= 0x1p40f ? 1.f / q.lout : 0.f;
   q.pad[0] = q.pad[1] = 0;
   return q;
 }
@@ -769,9 +815,10 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
 // has written the bucket starts and the tile table.
 constexpr int kScatterU = kReqPerPrepBlock / kPrepBlock;
 
-// Request u of this thread: bucket key (-1: none), position and record.  Every load is issued
+// Request u of this thread: stored key (-1: none), position and record.  Every load is issued
 // before the first use; a thread past the last request reads the last one (R >= 1) and drops
-// it, and an invalid request's position (never written) is not used.
+// it, and an invalid request's position (never written) is not used.  take_key then splits
+// the key into the bucket and the prompt-row flag.
 __device__ __forceinline__ void scatter_loads(const PlaceArgs &a, int (&key)[kScatterU], int (&pos)[kScatterU],
                                               ReqRec (&rec)[kScatterU]) {
 #pragma unroll
@@ -785,6 +832,15 @@ __device__ __forceinline__ void scatter_loads(const PlaceArgs &a, int (&key)[kSc
   }
 }
 
+__device__ __forceinline__ void take_key(int (&key)[kScatterU], ReqRec (&rec)[kScatterU]) {
+#pragma unroll
+  for (int u = 0; u < kScatterU; ++u)
+    if (key[u] >= 0) {
+      if (key[u] & kKeyTiny) rec[u].rlout = 0.f;
+      key[u] &= kKeyTiny - 1;
+    }
+}
+
 __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
   extern __shared__ int start[];   // [NB] bucket starts, then with group padding [2][2M + 1]
   int key[kScatterU], pos[kScatterU];
@@ -796,11 +852,13 @@ __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
     scatter_loads(a, key, pos, rec);
     __builtin_amdgcn_sched_barrier(0);   // no use of a loaded value is scheduled before a load
     block_scan_buckets(a, start, cv);    // the bucket starts are complete on return
+    take_key(key, rec);
 #pragma unroll
     for (int u = 0; u < kScatterU; ++u)
       if (key[u] >= 0) a.preq[start[key[u]] + pos[u]] = rec[u];
   } else {
     scatter_loads(a, key, pos, rec);
+    take_key(key, rec);
 #pragma unroll
     for (int u = 0; u < kScatterU; ++u)
       if (key[u] >= 0) a.preq[a.bstart[key[u]] + pos[u]] = rec[u];
