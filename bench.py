@@ -25,7 +25,8 @@ transfer plan of a 2,048-GPU reconfiguration (cost matrix, per-request moves), t
 way.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-       python bench.py --per-config     (one JSON line per configuration, then the step line)
+       python bench.py --per-config     (also one JSON line per configuration before the step line;
+                                         the step line always carries them as "per_config")
 """
 from __future__ import annotations
 
@@ -394,27 +395,30 @@ def sweep_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
 _WORKER_INP = None
 
 
-def _worker_init(inp):
+def _worker_init(kind, inp):
     """Pool worker set-up (a fresh interpreter, no GPU): keep the inputs, load the oracle."""
-    global _WORKER_INP
+    global _WORKER_INP, _WORKER_KIND
     import oracle
     oracle.lib()
-    _WORKER_INP = inp
+    _WORKER_INP, _WORKER_KIND = inp, kind
 
 
 def _worker_chunk(sel):
     import oracle
-    oracle.score_placements(_WORKER_INP, sel)
+    if _WORKER_KIND == "placement":
+        oracle.score_placements(_WORKER_INP, sel)
+    else:
+        oracle.score_migrations(_WORKER_INP, sel)
     return len(sel)
 
 
-def oracle_all_cores(place_inp, sel, workers):
-    """The unchanged single-threaded oracle on the same sampled requests, split into chunks
-    over `workers` spawned processes; wall time of the chunks only (inputs are handed to the
-    workers before the clock starts)."""
+def oracle_all_cores(kind, inp, sel, workers):
+    """The unchanged single-threaded oracle on the same sampled requests (kind "placement")
+    or source GPUs ("migration"), split into chunks over `workers` spawned processes; wall
+    time of the chunks only (inputs are handed to the workers before the clock starts)."""
     import multiprocessing as mp
     chunks = np.array_split(sel, workers * 8)
-    with mp.get_context("spawn").Pool(workers, initializer=_worker_init, initargs=(place_inp,)) as pool:
+    with mp.get_context("spawn").Pool(workers, initializer=_worker_init, initargs=(kind, inp)) as pool:
         pool.map_async(_worker_chunk, [c[:1] for c in chunks[:workers]]).get(timeout=300)   # every worker warm
         t0 = time.perf_counter()
         done = sum(pool.map_async(_worker_chunk, chunks).get(timeout=300))
@@ -437,7 +441,40 @@ def host_cpu():
     return {"cpu_model": model, "nproc": os.cpu_count(), "usable": len(os.sched_getaffinity(0))}
 
 
-def cpu_baseline(place_inp, fleet_inp, gpu_place, gpu_mig, stride=4):
+def best_of(fn, n=3):
+    """Least wall time of n calls of fn()."""
+    best = None
+    for _ in range(n):
+        t0 = time.perf_counter()
+        fn()
+        dt = time.perf_counter() - t0
+        best = dt if best is None else min(best, dt)
+    return best
+
+
+def cpu_per_config(W):
+    """The single-threaded oracle on the whole of configurations 1-3 (placement) and 5
+    (consolidation), best of 3 runs each."""
+    import oracle
+    out = {}
+    for cfg in (1, 2, 3, 5):
+        if cfg < 5:
+            inp = W.make_placement(cfg)
+            work = placement_candidates(inp)
+            t = best_of(lambda: oracle.score_placements(inp))
+            what = f"all {inp['requests']['n_requests']} requests, {work} candidates"
+        else:
+            inp = W.make_fleet()
+            G = inp["fleet"]["n_gpus"]
+            work = G * (G - 1)
+            t = best_of(lambda: oracle.score_migrations(inp))
+            what = f"all {work} ordered pairs of {G} GPUs"
+        out[str(cfg)] = {"value": work / t, "unit": "candidate evaluations/s", "cores": 1, "seconds": t,
+                         "sample": what + ", best of 3"}
+    return out
+
+
+def cpu_baseline(place_inp, fleet_inp, gpu_place, gpu_mig, W, stride=4):
     import oracle
     R = place_inp["requests"]["n_requests"]
     sel = np.arange(0, R, stride, dtype=np.int32)
@@ -452,7 +489,8 @@ def cpu_baseline(place_inp, fleet_inp, gpu_place, gpu_mig, stride=4):
     gc, gf, _ = gpu_place
     gb = gpu_mig[0]
     workers = max(1, min(16, os.cpu_count() or 1))        # the machine's CPU share for one GPU
-    t_all = oracle_all_cores(place_inp, sel, workers)
+    t_all = oracle_all_cores("placement", place_inp, sel, workers)
+    t_mig = oracle_all_cores("migration", fleet_inp, np.arange(G, dtype=np.int32), workers)
     return {
         "value": (cand + pairs) / ((t1 - t0) + (t2 - t1)),
         "unit": "candidate evaluations/s",
@@ -461,9 +499,12 @@ def cpu_baseline(place_inp, fleet_inp, gpu_place, gpu_mig, stride=4):
         "sample": (f"every {stride}th request of the placement workload ({len(sel)} requests, {cand} "
                    f"candidates, {t1 - t0:.2f} s) + all {pairs} migration pairs ({t2 - t1:.2f} s); "
                    f"single-threaded C, float64, gcc -O2"),
-        "all_cores": {"value": cand / t_all, "cores": workers,
-                      "sample": f"the same {len(sel)} placement requests in chunks over {workers} processes "
-                                f"({t_all:.2f} s), placement only"},
+        "all_cores": {"value": (cand + pairs) / (t_all + t_mig), "cores": workers,
+                      "sample": f"the same {len(sel)} placement requests ({t_all:.2f} s) and all {pairs} migration "
+                                f"pairs ({t_mig:.2f} s), each in chunks over {workers} processes",
+                      "placement": {"value": cand / t_all, "seconds": t_all},
+                      "migration": {"value": pairs / t_mig, "seconds": t_mig}},
+        "per_config": cpu_per_config(W),
         "host": host_cpu(),
         "agreement": {"placement_flags_equal": float(np.mean(of == gf[sel])),
                       "placement_choice_equal": float(np.mean(oc == gc[sel])),
@@ -502,8 +543,7 @@ def main():
     torch.cuda.set_device(0)
     hip = Hip()
 
-    if args.per_config:
-        per_config(F, W, hip, torch)
+    configs = per_config(F, W, hip, torch, verbose=args.per_config)
     if args.graph:
         graph_compare(F, W, torch)
 
@@ -562,6 +602,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
+        # the same step counted over distinct candidates only (a capped GPU's SM levels above
+        # max(cap_pf, cap_dc) repeat lower cells and are not evaluated)
+        "value_distinct": (n_distinct + n_pairs) / step_s,
         "dtype": "f32",
         "data": "synthetic",
         "config": {
@@ -603,6 +646,7 @@ def main():
         "kernels_ms": {"k_score": score_ms, "k_score_candidates_per_s": n_cand / (score_ms * 1e-3),
                        "migration_call": mig_ms,
                        "migration_pairs_per_s_call": n_pairs / (mig_ms * 1e-3)},
+        "per_config": configs,
         "cpu_baseline": None,
         "next_rows": {"sweep": sweep_row(F, W, hip, torch, not args.no_cpu_baseline),
                       "preferred": preferred_row(F, W, hip, torch, not args.no_cpu_baseline),
@@ -610,7 +654,7 @@ def main():
                       "transfer": transfer_row(F, W, hip, torch, not args.no_cpu_baseline)},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(place, fleet, gpu_place, gpu_mig)
+        line["cpu_baseline"] = cpu_baseline(place, fleet, gpu_place, gpu_mig, W)
     print(json.dumps(line), flush=True)
     if args.copy_calibration > 0:
         n = args.copy_calibration * (1 << 20) // 4
@@ -662,8 +706,10 @@ def graph_compare(F, W, torch, steps=200, rounds=3):
                       "steps": steps, "eager_us_per_step": eager, "graph_replay_us_per_step": graph}), flush=True)
 
 
-def per_config(F, W, hip, torch):
-    """One JSON line per configuration: call time, kernel time, rates, VALU fraction."""
+def per_config(F, W, hip, torch, verbose=False):
+    """Per configuration: call time, kernel time, rates and the kernel's VALU fraction (one
+    JSON line each when verbose); returned as {config: {...}}."""
+    out = {}
     for cfg in (1, 2, 3, 4, 5):
         if cfg < 5:
             inp = W.make_placement(cfg)
@@ -703,9 +749,13 @@ def per_config(F, W, hip, torch):
             # time, more than the kernel itself: time a batch of whole calls instead
             km = timed_batch(hip, torch, dev.run, 50)
             timed = "k_fleet + k_migrate (batch of 50 calls, one event pair)"
-        print(json.dumps({"config": cfg, "work": work, "call_ms": cm, "kernel_ms": km, "kernel_timed": timed,
-                          "evals_per_s_call": work / (cm * 1e-3), "evals_per_s_kernel": work / (km * 1e-3),
-                          "valu_frac_kernel": ops / (km * 1e-3) / VALU_PEAK}), flush=True)
+        rec = {"work": work, "call_ms": cm, "kernel_ms": km, "kernel_timed": timed,
+               "evals_per_s_call": work / (cm * 1e-3), "evals_per_s_kernel": work / (km * 1e-3),
+               "valu_frac_kernel": ops / (km * 1e-3) / VALU_PEAK}
+        out[str(cfg)] = rec
+        if verbose:
+            print(json.dumps({"config": cfg, **rec}), flush=True)
+    return out
 
 
 if __name__ == "__main__":
