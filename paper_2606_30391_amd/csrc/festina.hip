@@ -900,8 +900,8 @@ __device__ void generic_loop(const PlaceArgs &a, int m, int w, int beg, int end,
   const int lane = threadIdx.x & (kWave - 1);
   float *myrows = rows + (size_t)wv * kQ * C;
   const int hcnt = ro(a.host_cnt)[m];
-  const auto hl = ro(a.host_list + (size_t)m * a.G);
-  const auto rw = ro(a.recs + (size_t)w * a.G);
+  const auto hl = ro(a.host_list + (size_t)m * (unsigned)a.G);
+  const auto rw = ro(a.recs + (size_t)w * (unsigned)a.G);
   const float p0 = a.p0;
 
   int cj[CPL], ck[CPL];
@@ -1227,7 +1227,8 @@ constexpr uint32_t kL_W = kL_hpos + kHcap * 4;                  // per wavefront
 constexpr uint32_t kLw_rec = 0;                                 //   [kHcap] records, class order
 constexpr uint32_t kLw_T = kHcap * 16;                          //   [kR][8] pass-2 terms
 constexpr uint32_t kLw_Q = kLw_T + kR * 8 * 4;                  //   [kR] {K*, tied cell}
-constexpr uint32_t kLw = kLw_Q + kR * 8;
+constexpr uint32_t kLw_M = kLw_Q + kR * 8;                      //   [kR] K*, [kR] index: the merge of
+constexpr uint32_t kLw = kLw_M + kR * 8;                        //   a tile split over wavefronts
 static_assert(kL_W % 16 == 0 && kLw % 16 == 0, "per-wave tables start 16-byte aligned");
 __host__ __device__ constexpr size_t r16_lds_bytes(int wpb) { return kL_W + (size_t)wpb * kLw; }
 
@@ -1308,8 +1309,8 @@ __device__ __forceinline__ void r16_steps(const char *L, const char *Rw, int cs,
 
 // Pass 1 over the classes [k, ncls) of one chunk that have n levels in range JB..JB+3, where n
 // = 1 (H = 4 GPUs per step), 2 (H = 2) or at least 3 (H = 1); returns the first other class.
-template <int JB, int H>
-__device__ __forceinline__ int r16_group(const char *L, const char *Rw, int k, int ncls, const float (&xA)[kR],
+template <int JB, int H, int S>
+__device__ __forceinline__ int r16_group(const char *L, const char *Rw, int k, int ncls, int sp, const float (&xA)[kR],
                                          const float (&xB)[kR], float p0, float (&acc)[kR]) {
   constexpr int LP = 4 / H;                       // levels per GPU in a step
   const int lane = __lane_id();
@@ -1320,9 +1321,12 @@ __device__ __forceinline__ int r16_group(const char *L, const char *Rw, int k, i
   for (; k < ncls; ++k) {
     const int packed = uniform(cls[k]);
     const int cp = (packed >> 3) & 7, cd = packed & 7;
-    const int cs = (packed >> 6) & 511, ce = (packed >> 15) & 511;
+    const int c0 = (packed >> 6) & 511, c1 = (packed >> 15) & 511;
     const int n = max(cp, cd) - JB + 1;           // levels of the range this class needs
     if ((H == 4 && n != 1) || (H == 2 && n != 2)) break;
+    // this wavefront's part sp of the class's GPUs (S parts)
+    const int cs = S == 1 ? c0 : c0 + (c1 - c0) * sp / S, ce = S == 1 ? c1 : c0 + (c1 - c0) * (sp + 1) / S;
+    if (cs == ce) continue;
     R16Class c;
     r16_class<JB>(L, jl, kf, cp, cd, xA, xB, c);
     r16_steps<H>(L, Rw, cs, ce, slot, c, p0, acc);
@@ -1353,8 +1357,8 @@ __device__ __forceinline__ void r16_fold(float (&acc)[kR]) {
 
 // Pass 1 of one chunk over range JB..JB+3 (classes in ascending m, so the groups come in the
 // order n = 1, 2, then more; classes with no level in the range come first and are skipped).
-template <int JB>
-__device__ __forceinline__ void r16_range(const char *L, const char *Rw, int ncls, const float (&xA)[kR],
+template <int JB, int S>
+__device__ __forceinline__ void r16_range(const char *L, const char *Rw, int ncls, int sp, const float (&xA)[kR],
                                           const float (&xB)[kR], float p0, float (&acc)[kR]) {
   const int *cls = reinterpret_cast<const int *>(L + kL_cls);
   int k = 0;
@@ -1364,11 +1368,11 @@ __device__ __forceinline__ void r16_range(const char *L, const char *Rw, int ncl
       if (max((packed >> 3) & 7, packed & 7) >= JB) break;
       ++k;
     }
-  const int k1 = r16_group<JB, 4>(L, Rw, k, ncls, xA, xB, p0, acc);
+  const int k1 = r16_group<JB, 4, S>(L, Rw, k, ncls, sp, xA, xB, p0, acc);
   if (k1 > k) r16_fold<4>(acc);
-  const int k2 = r16_group<JB, 2>(L, Rw, k1, ncls, xA, xB, p0, acc);
+  const int k2 = r16_group<JB, 2, S>(L, Rw, k1, ncls, sp, xA, xB, p0, acc);
   if (k2 > k1) r16_fold<2>(acc);
-  r16_group<JB, 1>(L, Rw, k2, ncls, xA, xB, p0, acc);
+  r16_group<JB, 1, S>(L, Rw, k2, ncls, sp, xA, xB, p0, acc);
 }
 
 // One value per request for the 16 requests at once: the reduction (OP) over the wavefront's
@@ -1455,9 +1459,24 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// A fresh copy of a wave-uniform value: whatever is computed from it (addresses, tests) is
+// computed where it is used, not kept in scalar registers from an earlier computation.
+__device__ __forceinline__ int fresh_s(int v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+
+// A fresh copy of the lane id: a test made on it is made where it is used, not kept as a lane
+// mask in scalar registers across a loop.
+__device__ __forceinline__ int lane_fresh() {
+  int l = __lane_id();
+  asm volatile("" : "+v"(l));
+  return l;
+}
+
 // Lanes 4q store request q's {K*, cell} at Qi + 8q, for the lanes' broadcast reads.
 __device__ __forceinline__ void r16_store_q(char *L, uint32_t Qi, float Kl, int cellv) {
-  const int lane = __lane_id();
+  const int lane = lane_fresh();
   if ((lane & 3) == 0) *reinterpret_cast<v2u *>(L + Qi + (lane >> 2) * 8) = v2u{__float_as_uint(Kl), (unsigned)cellv};
   wave_sync();
 }
@@ -1490,34 +1509,42 @@ __device__ __forceinline__ int r16_next_cells(const char *L, uint32_t Qi, const 
   return c;
 }
 
-template <int WPB>
-__global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
+constexpr int kWpb16 = 4;                        // wavefronts per workgroup of the 8 x 16 kernel
+
+// S = wavefronts per tile: with S > 1 (small request counts, too few tiles to fill the chip)
+// the S wavefronts of a tile split each SM-cap class's GPUs into S parts in pass 1, merge the
+// least key per request through LDS, each finds the lowest index reaching it among its own
+// tied cells (over all GPUs), and the least index is merged the same way.
+template <int S>
+__global__ void __launch_bounds__(kWpb16 * 64) k_score_r16(PlaceArgs a) {
+  constexpr int WPB = kWpb16, TPB = WPB / S;     // tiles per workgroup
   extern __shared__ __align__(16) float lds[];
   __shared__ int s_ok[WPB];
   char *L = reinterpret_cast<char *>(lds);
   constexpr int T = WPB * 64;
-  // Workgroup t takes tiles [WPB t, WPB t + WPB) of the table, all of one (model, prompt
-  // kind) group: the tiles of a group are contiguous and padded to a multiple of WPB, so the
-  // first is never empty.  Wavefront v scores tile WPB t + v: up to kR requests of one
-  // (arrival wave, model) bucket.
+  // Workgroup t takes tiles [TPB t, TPB t + TPB) of the table, all of one (model, prompt
+  // kind) group: the tiles of a group are contiguous and padded to a multiple of TPB, so the
+  // first is never empty.  Wavefront v scores part v % S of tile TPB t + v / S: up to kR
+  // requests of one (arrival wave, model) bucket.
   // XCD-aware order: workgroups are dealt to the 8 XCDs round-robin, so XCD x takes the
   // contiguous range [x * per, (x + 1) * per) -- the same models -- instead of every eighth.
-  const int nblk = *ro(a.n_tiles) / WPB;
+  const int nblk = *ro(a.n_tiles) / TPB;
   const int per = (nblk + kXcds - 1) / kXcds;
   const int idx = blockIdx.x / kXcds;
   const int t = (blockIdx.x % kXcds) * per + idx;
   if (idx >= per || t >= nblk) return;
   const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
-  const int beg = tp[2 * WPB * t + 1];    // the workgroup's first request
-  const BucketId grp = bucket_id(a, tp[2 * WPB * t]);
+  const int beg = tp[2 * TPB * t + 1];    // the workgroup's first request
+  const BucketId grp = bucket_id(a, tp[2 * TPB * t]);
   const int m = grp.m;
   const int wv = uniform(threadIdx.x >> 6);
-  const int bk = tp[2 * (WPB * t + wv)];  // this wavefront's bucket (-1: an empty tile)
-  const int q0 = bk >= 0 ? tp[2 * (WPB * t + wv) + 1] : beg;
+  const int ti = wv / S, sp = wv - ti * S;  // this wavefront's tile and part
+  const int bk = tp[2 * (TPB * t + ti)];  // the tile's bucket (-1: an empty tile)
+  const int q0 = bk >= 0 ? tp[2 * (TPB * t + ti) + 1] : beg;
   const int nq = bk >= 0 ? min(kR, ro(a.bstart)[bk + 1] - q0) : 0;
   const int w = bk >= 0 ? bucket_id(a, bk).w : 0;
   if (grp.noprompt) {                     // prompt-less requests: TTFT from the batch row
-    score_requests_generic<2>(a, m, true, w, q0, q0 + nq, kQ, lds);
+    score_requests_generic<2>(a, m, true, w, q0 + sp * kQ, q0 + nq, S * kQ, lds);
     return;
   }
 
@@ -1525,10 +1552,32 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
   // at a raised wavefront priority its instructions issue first.
   __builtin_amdgcn_s_setprio(2);
   const int lane = threadIdx.x & (kWave - 1);
-  // lane l holds the fields of request l / 4 (a missing request reads the workgroup's first
-  // record and is masked)
+  // One round trip for everything that needs only the model and the tile entries, all loads
+  // into registers before any LDS store (a store between loads would order them): the
+  // model's decode table, the power factors, the first host chunk's GPU ids and class slots
+  // (kHk per lane: this wavefront's part of its tile's records), the chunk's class list and
+  // the requests.  Lane l holds the fields of request l / 4, read at the tile's position
+  // clamped into the request array (a missing request is masked below).
+  constexpr int kDcV = kRows * 128 / 4 / T;        // float4 of the decode table per thread
+  constexpr int kHk = kHcap / (S * kWave);         // chunk hosts per lane
+  const float *dsrc = a.dc + (size_t)m * kRows * 128;
+  const bool dc_al = (((uintptr_t)dsrc) & 15) == 0;
+  float4 dcv[kDcV];
+  if (dc_al) {
+#pragma unroll
+    for (int u = 0; u < kDcV; ++u) dcv[u] = reinterpret_cast<const float4 *>(dsrc)[threadIdx.x + u * T];
+  }
+  const float pdv = a.sm_level[(threadIdx.x >> 4) & 7] * cube(a.freq_level[threadIdx.x & 15]);   // cell tid % 128
+  int hl[kHk], hp[kHk];
+#pragma unroll
+  for (int k = 0; k < kHk; ++k) {
+    const int i = (k * S + sp) * kWave + lane;     // chunk-0 host of this lane
+    hl[k] = i < a.G ? a.host_list[(size_t)m * (unsigned)a.G + i] : 0;
+    hp[k] = i < a.G ? a.host_pos[(size_t)m * (unsigned)a.G + i] : 0;
+  }
+  const int clsv = a.cls_tab[(size_t)m * a.nch * (kClasses + 1) + min((int)threadIdx.x, kClasses)];
   const bool has = (lane >> 2) < nq;
-  const ReqRec rq = load_req_lane(a, has ? q0 + (lane >> 2) : beg);
+  const ReqRec rq = load_req_lane(a, min(q0 + (lane >> 2), a.R - 1));
   float lo_has = has ? rq.lout : 0.f;
   // the request's prompt-row offset, TTFT SLO and 1 / Lout for the request-term staging
   // (a missing request: row 0, SLO -inf, so every term is masked)
@@ -1548,96 +1597,128 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
 #pragma unroll
   for (int v = 0; v < WPB; ++v) tile_ok = tile_ok && s_ok[v];
   if (!tile_ok) {                         // mixed TBT SLOs or an unscalable request
-    score_requests_generic<2>(a, m, false, w, q0, q0 + nq, kQ, lds);
+    score_requests_generic<2>(a, m, false, w, q0 + sp * kQ, q0 + nq, S * kQ, lds);
     return;
   }
   const float tsb = r0.slo_tbt;           // every request of the workgroup has this TBT SLO
+  const int hcnt = ro(a.host_cnt)[m];
+  const int n0 = min(kHcap, hcnt);
 
-  for (int c = threadIdx.x; c < 128; c += T)   // s_j * f_k^3 of cell j * 16 + k
-    *reinterpret_cast<float *>(L + kL_pd + c * 4) = a.sm_level[c >> 4] * cube(a.freq_level[c & 15]);
-  // request terms: x = TTFT / Lout where TTFT < the TTFT SLO, else NaN, at this lane's cell of
-  // each range, for the 16 requests (all loads requested before the first use).  Each
-  // request's prompt-row offset, SLO and 1 / Lout reach every lane by broadcast reads of the
-  // wavefront's LDS scratch (free until pass 2), not through scalar registers.
   float xA[kR], xB[kR];
   const uint32_t Wb = kL_W + (uint32_t)wv * kLw;   // this wavefront's tables
   const uint32_t Tw = Wb + kLw_T;
-  const char *Rw = L + Wb + kLw_rec;
+  const uint32_t Wt = kL_W + (uint32_t)(ti * S) * kLw;   // the tile's shared tables
+  const char *Rw = L + Wt + kLw_rec;
+  float *Km = reinterpret_cast<float *>(L + Wt + kLw_M);   // merged K* of the tile's requests
+  int *Bm = reinterpret_cast<int *>(L + Wt + kLw_M + kR * 4);   // merged least index
+  // Second round trip: the request terms x = TTFT / Lout (NaN where TTFT misses the SLO) at
+  // this lane's cell of each range for the 16 requests, each request's row offset, SLO and
+  // 1 / Lout taken from its lane by ds_bpermute; and the GPU records of the chunk's hosts.
+  HostRec hr0[kHk];
   if (nq > 0) {
-    if ((lane & 3) == 0) *reinterpret_cast<v4u *>(L + Tw + (lane >> 2) * 16) = stage_rec;
-    wave_sync();
 #pragma unroll
     for (int q = 0; q < kR; ++q) {
-      const unsigned off = reinterpret_cast<const v4u *>(L + Tw)[q].x;
+      const unsigned off = (unsigned)__builtin_amdgcn_ds_bpermute(q * 16, (int)stage_rec.x);
       xA[q] = a.pf[off + lane];
       xB[q] = a.pf[off + 64 + lane];
     }
 #pragma unroll
+    for (int k = 0; k < kHk; ++k) {
+      const int i = (k * S + sp) * kWave + lane;
+      if (i < n0) hr0[k] = a.recs[(size_t)w * (unsigned)a.G + hl[k]];
+    }
+#pragma unroll
     for (int q = 0; q < kR; ++q) {
-      const v4u f = reinterpret_cast<const v4u *>(L + Tw)[q];
-      const float st = __uint_as_float(f.y), rl = __uint_as_float(f.z);
+      const float st = bperm(q * 16, __uint_as_float(stage_rec.y)), rl = bperm(q * 16, __uint_as_float(stage_rec.z));
       xA[q] = xA[q] < st ? xA[q] * rl : kMask;
       xB[q] = xB[q] < st ? xB[q] * rl : kMask;
     }
-    wave_sync();                          // the scratch is reused by pass 2
   }
-  {  // the model's decode table, rows padded to kRowPad bytes, NaN where TBT misses the SLO
-    const float *src = a.dc + (size_t)m * kRows * 128;
-    if ((((uintptr_t)src) & 15) == 0) {
-      const float4 *s4 = reinterpret_cast<const float4 *>(src);
-#pragma unroll 4
-      for (int i = threadIdx.x; i < kRows * 128 / 4; i += T) {
-        const float4 v = s4[i];
-        v2f *d = reinterpret_cast<v2f *>(L + kL_dcs + (i >> 5) * kRowPad + (i & 31) * 16);
-        d[0] = v2f{v.x < tsb ? v.x : kMask, v.y < tsb ? v.y : kMask};
-        d[1] = v2f{v.z < tsb ? v.z : kMask, v.w < tsb ? v.w : kMask};
-      }
-    } else {
-      for (int i = threadIdx.x; i < kRows * 128; i += T) {
-        const float v = src[i];
-        *reinterpret_cast<float *>(L + kL_dcs + (i >> 7) * kRowPad + (i & 127) * 4) = v < tsb ? v : kMask;
-      }
+  // LDS: the power factors, the decode table (rows padded to kRowPad bytes, NaN where TBT
+  // misses the SLO), the chunk's class list and host slots, the tile's records (class order)
+  // (the thread-index tests below are made here, on a fresh copy, not kept as lane masks)
+  int tid = (int)threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  if (tid < 128) *reinterpret_cast<float *>(L + kL_pd + tid * 4) = pdv;
+  if ((((uintptr_t)(a.dc + (size_t)fresh_s(m) * kRows * 128)) & 15) == 0) {   // dc_al, decided afresh
+#pragma unroll
+    for (int u = 0; u < kDcV; ++u) {
+      const int i = threadIdx.x + u * T;
+      const float4 v = dcv[u];
+      v2f *d = reinterpret_cast<v2f *>(L + kL_dcs + (i >> 5) * kRowPad + (i & 31) * 16);
+      d[0] = v2f{v.x < tsb ? v.x : kMask, v.y < tsb ? v.y : kMask};
+      d[1] = v2f{v.z < tsb ? v.z : kMask, v.w < tsb ? v.w : kMask};
     }
+  } else {
+    for (int i = threadIdx.x; i < kRows * 128; i += T) {
+      const float v = dsrc[i];
+      *reinterpret_cast<float *>(L + kL_dcs + (i >> 7) * kRowPad + (i & 127) * 4) = v < tsb ? v : kMask;
+    }
+  }
+  if (tid <= kClasses) reinterpret_cast<int *>(L + kL_cls)[tid] = clsv;
+#pragma unroll
+  for (int k = 0; k < kHk; ++k) {
+    const int i = (k * S + sp) * kWave + lane;
+    if (ti == 0 && i < n0) reinterpret_cast<int *>(L + kL_hpos)[i] = hp[k];
+    if (nq > 0 && i < n0) {
+      v4u e;
+      e.x = kL_dcs + (uint32_t)(max(hr0[k].row_off, 0) / 128) * kRowPad;
+      e.y = __float_as_uint(hr0[k].kappa);
+      e.z = (uint32_t)hl[k];
+      e.w = (uint32_t)hr0[k].caps;
+      *reinterpret_cast<v4u *>(L + Wt + kLw_rec + hp[k] * 16) = e;
+    }
+  }
+  if (S > 1 && sp == 0 && lane < kR) {    // made ready before the first pass-1 barrier
+    Km[lane] = kInf;
+    Bm[lane] = INT_MAX;
   }
 
   float accA[kR], accB[kR];
 #pragma unroll
   for (int q = 0; q < kR; ++q) accA[q] = accB[q] = kInf;
-  const int hcnt = ro(a.host_cnt)[m];
   const float p0 = a.p0;
   for (int c0 = 0, ch = 0; c0 < hcnt; c0 += kHcap, ++ch) {
     const int n = min(kHcap, hcnt - c0);
-    __syncthreads();                      // the previous chunk's records are no longer read
-    __builtin_amdgcn_s_setprio(2);
-    for (int i = threadIdx.x; i < n; i += T)     // class-order slot of each chunk host
-      reinterpret_cast<int *>(L + kL_hpos)[i] = a.host_pos[(size_t)m * a.G + c0 + i];
-    if (nq > 0)
-      for (int i = lane; i < n; i += kWave) {    // this wavefront's GPU records, class order
-        const int g = a.host_list[(size_t)m * a.G + c0 + i];
-        const int pos = a.host_pos[(size_t)m * a.G + c0 + i];
-        const HostRec h = a.recs[(size_t)w * a.G + g];
-        v4u e;
-        e.x = kL_dcs + (uint32_t)(max(h.row_off, 0) / 128) * kRowPad;
-        e.y = __float_as_uint(h.kappa);
-        e.z = (uint32_t)g;
-        e.w = (uint32_t)h.caps;
-        *reinterpret_cast<v4u *>(L + Wb + kLw_rec + pos * 16) = e;
-      }
-    for (int i = threadIdx.x; i <= kClasses; i += T)
-      reinterpret_cast<int *>(L + kL_cls)[i] = a.cls_tab[((size_t)m * a.nch + ch) * (kClasses + 1) + i];
+    if (ch > 0) {                         // later chunks (more than kHcap GPUs host the model)
+      __syncthreads();                    // the previous chunk's records are no longer read
+      __builtin_amdgcn_s_setprio(2);
+      const size_t mg = (size_t)fresh_s(m) * (unsigned)a.G + c0, wg = (size_t)fresh_s(w) * (unsigned)a.G;
+      for (int i = threadIdx.x; i < n; i += T)   // class-order slot of each chunk host
+        reinterpret_cast<int *>(L + kL_hpos)[i] = a.host_pos[mg + i];
+      if (nq > 0)
+        for (int i = sp * kWave + lane; i < n; i += S * kWave) {   // the tile's GPU records, class order
+          const int g = a.host_list[mg + i];
+          const int pos = a.host_pos[mg + i];
+          const HostRec h = a.recs[wg + g];
+          v4u e;
+          e.x = kL_dcs + (uint32_t)(max(h.row_off, 0) / 128) * kRowPad;
+          e.y = __float_as_uint(h.kappa);
+          e.z = (uint32_t)g;
+          e.w = (uint32_t)h.caps;
+          *reinterpret_cast<v4u *>(L + Wt + kLw_rec + pos * 16) = e;
+        }
+      for (int i = threadIdx.x; i <= kClasses; i += T)
+        reinterpret_cast<int *>(L + kL_cls)[i] = a.cls_tab[((size_t)fresh_s(m) * a.nch + ch) * (kClasses + 1) + i];
+    }
     __syncthreads();
     __builtin_amdgcn_s_setprio(0);
     if (nq > 0) {
       const int ncls = uniform(reinterpret_cast<const int *>(L + kL_cls)[kClasses]);
-      r16_range<0>(L, Rw, ncls, xA, xB, p0, accA);
-      r16_range<4>(L, Rw, ncls, xA, xB, p0, accB);
+      r16_range<0, S>(L, Rw, ncls, sp, xA, xB, p0, accA);
+      r16_range<4, S>(L, Rw, ncls, sp, xA, xB, p0, accB);
     }
   }
-  if (nq == 0) return;
+  if (S == 1 && nq == 0) return;          // (with S > 1 every wavefront meets the barriers below)
 
   // pass 2: per request the least key K* and, per tied cell in ascending order, the first host
   // (ascending GPU id) reaching it
-  const float Kl = wave_min16(accA, accB);          // request lane / 4
+  float Kl = wave_min16(accA, accB);                // request lane / 4
+  if (S > 1) {                            // K* over the tile's S parts
+    if (nq > 0 && (lane_fresh() & 3) == 0) atomicMin(&Km[lane >> 2], Kl);
+    __syncthreads();
+    Kl = Km[lane >> 2];
+  }
   // Lout of request lane / 4, 0 for a missing request (tested as a vector value so that no
   // lane mask stays live in scalar registers across pass 1)
   const float lo_l = lo_has;
@@ -1648,7 +1729,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
   bool more;
   r16_store_q(L, Qi, Ks, -1);
   int cellv = r16_next_cells(L, Qi, accA, accB, more);
-  while (__ballot(cellv < kNoCell) != 0ull) {
+  while (nq > 0 && __ballot(cellv < kNoCell) != 0ull) {
     r16_store_q(L, Qi, Ks, cellv);
     // T[q][j] = request q's term at level j and its tied cell's frequency level: lanes j < 8
     // read lane (j % 4) * 16 + k of xA[q] (j < 4) or xB[q]; every request at once
@@ -1664,7 +1745,7 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
     // its tied cell on all of them (four requests at a time, their LDS reads together), and
     // its first matching lane is its lowest GPU id, so a request is done at the first block
     // with a match.
-    unsigned long long pend = __ballot((lane & 3) == 0 && cellv < kNoCell);   // bit 4q: request q
+    unsigned long long pend = __ballot((lane_fresh() & 3) == 0 && cellv < kNoCell);   // bit 4q: request q
     for (int b0 = 0; b0 < hcnt && pend != 0ull; b0 += kWave) {
       asm volatile("" ::: "memory");      // per-request values are reloaded in every block
       const int i = b0 + lane;
@@ -1681,8 +1762,8 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
         g = (int)r.z;
         caps = (int)r.w;
       } else {
-        g = a.host_list[(size_t)m * a.G + ic];
-        const HostRec hr = a.recs[(size_t)w * a.G + g];
+        g = a.host_list[(size_t)fresh_s(m) * (unsigned)a.G + ic];
+        const HostRec hr = a.recs[(size_t)fresh_s(w) * (unsigned)a.G + g];
         rowB = kL_dcs + (uint32_t)(max(hr.row_off, 0) / 128) * kRowPad;
         kap = hr.kappa;
         caps = hr.caps;
@@ -1727,12 +1808,17 @@ __global__ void __launch_bounds__(WPB * 64) k_score_r16(PlaceArgs a) {
     cellv = r16_next_cells(L, Qi, accA, accB, more);
     wave_sync();                          // T is rewritten next round
   }
+  if (S > 1) {                            // the least index over the tile's S parts
+    if (nq > 0 && (lane_fresh() & 3) == 0 && best != INT_MAX) atomicMin(&Bm[lane >> 2], best);
+    __syncthreads();
+    best = Bm[lane >> 2];
+  }
   // fresh copies of the lane id and Lout: tests on them are made here, not kept as lane masks
   // in scalar registers through pass 2
-  int ln = lane;
+  const int ln = lane_fresh();
   float lo_w = lo_l;
-  asm volatile("" : "+v"(ln), "+v"(lo_w));
-  if ((ln & 3) == 0 && lo_w > 0.f) {
+  asm volatile("" : "+v"(lo_w));
+  if (sp == 0 && (ln & 3) == 0 && lo_w > 0.f) {
     const bool found = best != INT_MAX;
     a.choice[rq.r] = found ? best : -1;
     a.feasible[rq.r] = found ? 1 : 0;
@@ -1908,6 +1994,7 @@ struct PlaceLayout {
   size_t cnt, bstart, ntiles, tiles, gscan, host_cnt, host_list, recs, preq, key, off;
   size_t host_pos, cls_tab, pf_rowmin, pf_rowtiny, dc_min, total;
   int32_t NB, tile, max_tiles, waves_per_block, nch, gpad;
+  int32_t split;                 // 8 x 16 kernel: wavefronts per tile (1, 2 or 4)
   bool fast;                     // 8 SM x 16 frequency levels: the specialised kernel
   bool scan_local;               // k_scatter scans the bucket counts (no k_scan launch)
   size_t scatter_lds;            // dynamic LDS bytes of k_scatter
@@ -1928,10 +2015,13 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   if (NB > INT_MAX / 2 - 4 || Gn * C > INT_MAX || W * Gn > INT_MAX || M * Gn > INT_MAX) return false;
   // tile size: large tiles amortise the table staging, small ones fill the chip
   const bool fast = L->n_sm == 8 && L->n_freq == 16;
-  int wpb = 4, tile;
-  if (fast) {                    // one tile of kR requests per wavefront
+  int wpb = 4, tile, split = 1;
+  if (fast) {                    // tiles of kR requests, S wavefronts each
     tile = kR;
-    if (R < 1024LL * 4 * kR) wpb = 1;
+    wpb = kWpb16;
+    // too few tiles for four wavefronts per SIMD: split each tile's GPUs over 2 or 4
+    const long long tiles = (R + kR - 1) / kR;
+    split = tiles <= 1024 ? 4 : (tiles <= 2048 ? 2 : 1);
   } else {
     tile = 2 * 4 * kQ;
     if (R < 2048LL * tile) {
@@ -1943,9 +2033,9 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
     }
   }
   o->fast = fast;
-  // the 8 x 16 kernel's workgroups take wpb tiles of one (model, prompt kind) group: each of
-  // the 2M groups is padded with at most wpb - 1 empty tiles
-  const int gpad = fast ? wpb : 1;
+  // the 8 x 16 kernel's workgroups take wpb / split tiles of one (model, prompt kind) group:
+  // each of the 2M groups is padded with fewer empty tiles than that
+  const int gpad = fast ? wpb / split : 1;
   const long long max_tiles = (R + tile - 1) / tile + NB + (long long)(gpad - 1) * 2 * M;
   if (max_tiles > INT_MAX - 8) return false;   // the grid is rounded up to a multiple of 8
   size_t off = 0;
@@ -1979,6 +2069,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->max_tiles = (int32_t)max_tiles;
   o->waves_per_block = wpb;
   o->gpad = gpad;
+  o->split = split;
   const long long scan_ints = block_scan_ints(NB, M, gpad > 1);
   o->scan_local = NB <= kHistMax && scan_ints <= kScanLds;
   o->scatter_lds = o->scan_local ? sizeof(int32_t) * (size_t)scan_ints : 0;
@@ -2135,12 +2226,14 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
   hipError_t e = mark(0, st);
   if (e != hipSuccess) return FESTINA_ERR_DEVICE;
   if (lay.fast) {
-    const int blocks = (lay.max_tiles + wpb - 1) / wpb;
+    const int blocks = (lay.max_tiles + lay.gpad - 1) / lay.gpad;
     const int grid = (blocks + kXcds - 1) / kXcds * kXcds;
-    if (wpb == 4)
-      k_score_r16<4><<<grid, 4 * kWave, lds, st>>>(a);
+    if (lay.split == 4)
+      k_score_r16<4><<<grid, kWpb16 * kWave, lds, st>>>(a);
+    else if (lay.split == 2)
+      k_score_r16<2><<<grid, kWpb16 * kWave, lds, st>>>(a);
     else
-      k_score_r16<1><<<grid, kWave, lds, st>>>(a);
+      k_score_r16<1><<<grid, kWpb16 * kWave, lds, st>>>(a);
     e = hipGetLastError();
   } else if (cpl == 1)
     e = launch_score<1>(a, lay.max_tiles, wpb, lds, st);
