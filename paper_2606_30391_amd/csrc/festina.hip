@@ -91,7 +91,8 @@ struct PlaceArgs {
   uint8_t *feasible;
   float *energy;
   // workspace
-  int32_t NB;                    // buckets = 2 * W * M, numbered (2 m + prompt-less) * W + w
+  int32_t NB;                    // buckets = 2 * W * M, in groups of gw (see bucket_of)
+  int32_t gw, ng;                // buckets per group, groups (ng * gw = NB)
   int32_t tile;                  // requests per tile
   int32_t max_tiles;
   int32_t gpad;                  // tiles per workgroup of the 8 x 16 kernel: the tiles of each
@@ -102,7 +103,7 @@ struct PlaceArgs {
   int32_t *bstart;               // [NB + 1]
   int32_t *n_tiles;              // [1]
   int2 *tiles;                   // [max_tiles] {bucket, first position}; bucket -1: empty tile
-  int32_t *gscan;                // [2][2M + 1] group tile prefixes and pad prefixes (k_scan)
+  int32_t *gscan;                // [2][ng + 1] group tile prefixes and padded group starts (k_scan)
   int32_t *host_cnt;             // [M]
   int32_t *host_list;            // [M][G]
   HostRec *recs;                 // [W][G]
@@ -176,18 +177,25 @@ __device__ __forceinline__ ReqRec load_req_lane(const PlaceArgs &a, int pos) {
   return q;
 }
 
-// Buckets: the requests of one (wave, model, prompt kind).  The W buckets of a (model, prompt
-// kind) group are consecutive, so a group's tiles are contiguous in the tile table.
+// Buckets: the requests of one (wave, model, prompt kind).  The buckets of a group are
+// consecutive, so a group's tiles are contiguous in the tile table.
+// The arrival waves form ng / 2M slabs of gw consecutive waves; a group is one (slab, model,
+// prompt kind) and its gw buckets, one per wave of the slab, are consecutive: bucket =
+// ((slab * 2M + 2 m + prompt-less) * gw + wave within the slab).  Groups are numbered slab
+// first, so the XCD that takes a contiguous range of groups writes the results of the
+// requests of a few arrival waves (request ids that share cache lines), not of all.
 __device__ __forceinline__ int bucket_of(const PlaceArgs &a, int w, int m, bool noprompt) {
-  return ((m << 1) | (noprompt ? 1 : 0)) * a.W + w;
+  const int sl = w / a.gw;
+  return (sl * 2 * a.M + ((m << 1) | (noprompt ? 1 : 0))) * a.gw + (w - sl * a.gw);
 }
 struct BucketId {
   int w, m;
   bool noprompt;
 };
 __device__ __forceinline__ BucketId bucket_id(const PlaceArgs &a, int bucket) {
-  const int g = bucket / a.W;
-  return BucketId{bucket - g * a.W, g >> 1, (g & 1) != 0};
+  const int q = bucket / a.gw;                    // the group: slab * 2M + 2 m + prompt-less
+  const int sl = q / (2 * a.M), g = q - sl * 2 * a.M;
+  return BucketId{sl * a.gw + (bucket - q * a.gw), g >> 1, (g & 1) != 0};
 }
 
 // ------------------------------------------------------------------ prologue kernels
@@ -403,17 +411,23 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
     }
     if (local) {
       __syncthreads();
-      // slot h = w * 2M + g holds bucket g * W + w; (w, g) advance with h, no division per slot
+      // slot h = w * 2M + g holds the bucket of wave w = sl * gw + wr and 2 m + prompt-less =
+      // g; (sl, wr, g) advance with h, no division per slot
       const int NG = 2 * a.M;
       const int dw = kPrepBlock / NG, dg = kPrepBlock - dw * NG;
-      int w = (int)threadIdx.x / NG, g = (int)threadIdx.x - w * NG;
+      const int w0 = (int)threadIdx.x / NG;
+      int g = (int)threadIdx.x - w0 * NG, sl = w0 / a.gw, wr = w0 - sl * a.gw;
       for (int h = threadIdx.x; h < a.NB; h += kPrepBlock) {
-        if (hist[h]) hist[h] = atomicAdd(&a.cnt[g * a.W + w], hist[h]);   // this block's base
-        w += dw;
+        if (hist[h]) hist[h] = atomicAdd(&a.cnt[(sl * NG + g) * a.gw + wr], hist[h]);   // this block's base
+        wr += dw;
         g += dg;
         if (g >= NG) {
           g -= NG;
-          ++w;
+          ++wr;
+        }
+        while (wr >= a.gw) {
+          wr -= a.gw;
+          ++sl;
         }
       }
       __syncthreads();
@@ -501,14 +515,14 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
 
 constexpr int kScanLds = 16384;   // bucket counts staged in LDS by k_scan (64 KB)
 
-// Group padding: the 2M (model, prompt kind) groups each end with (gP[g] - gP[g + 1]) mod gpad
-// empty tiles.  gP holds the unpadded tile index of each group's first bucket, with the tile
-// total at [2M]; the scan writes pp[g] = the padded index of group g's first tile (gP[g] plus
-// the pads of the groups before it), pp[2M] = the padded total.  The whole block takes part;
+// Group padding: the ng groups each end with (gP[g] - gP[g + 1]) mod gpad empty tiles.  gP
+// holds the unpadded tile index of each group's first bucket, with the tile total at [ng];
+// the scan writes pp[g] = the padded index of group g's first tile (gP[g] plus the pads of
+// the groups before it), pp[ng] = the padded total.  The whole block takes part;
 // s_a is LDS scratch of blockDim / 64 ints that no thread still reads; ends with a barrier.
 template <typename P>
 __device__ void scan_group_pads(const PlaceArgs &a, P gP, P pp, int *s_a) {
-  const int NG = 2 * a.M, T = blockDim.x, gm = a.gpad - 1;
+  const int NG = a.ng, T = blockDim.x, gm = a.gpad - 1;
   const int per = (NG + T - 1) / T;
   const int lo = min((int)threadIdx.x * per, NG), hi = min(lo + per, NG);
   int s = 0;
@@ -568,8 +582,8 @@ __device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_c
     tot_t += s_til[i];
   }
   const bool pad = a.gpad > 1;
-  int *gP = a.gscan, *pp = a.gscan + 2 * a.M + 1;
-  const int g0 = lo / a.W, w0 = lo - g0 * a.W;
+  int *gP = a.gscan, *pp = a.gscan + a.ng + 1;
+  const int g0 = lo / a.gw, w0 = lo - g0 * a.gw;
   {
     int pc = pc0, pt = pt0, g = g0, wi = w0;
     for (int i = lo; i < hi; ++i) {
@@ -581,7 +595,7 @@ __device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_c
         gP[g] = pt;
       pc += n;
       pt += (n + a.tile - 1) / a.tile;
-      if (++wi == a.W) {
+      if (++wi == a.gw) {
         wi = 0;
         ++g;
       }
@@ -589,7 +603,7 @@ __device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_c
   }
   int pads = 0;
   if (pad) {
-    if (threadIdx.x == 0) gP[2 * a.M] = tot_t;
+    if (threadIdx.x == 0) gP[a.ng] = tot_t;
     __syncthreads();
     scan_group_pads(a, gP, pp, s_cnt);
     int pc = pc0, pt = pt0, g = g0, wi = w0;
@@ -597,16 +611,16 @@ __device__ __forceinline__ void scan_buckets(const PlaceArgs &a, P cnt, int *s_c
       const int n = cnt[i];
       const int nt = (n + a.tile - 1) / a.tile;
       put_tiles(a, i, n, pc, pt - gP[g] + pp[g]);
-      if (wi == a.W - 1)                  // the group's empty tiles follow its last bucket
+      if (wi == a.gw - 1)                 // the group's empty tiles follow its last bucket
         for (int k = pt + nt - gP[g] + pp[g]; k < pp[g + 1]; ++k) a.tiles[k] = make_int2(-1, 0);
       pc += n;
       pt += nt;
-      if (++wi == a.W) {
+      if (++wi == a.gw) {
         wi = 0;
         ++g;
       }
     }
-    pads = pp[2 * a.M] - tot_t;
+    pads = pp[a.ng] - tot_t;
   }
   if (threadIdx.x == 0) {
     a.bstart[a.NB] = tot_c;
@@ -691,9 +705,9 @@ __device__ __forceinline__ void load_scan_counts(const PlaceArgs &a, v4i (&v)[kS
 }
 
 // LDS of block_scan_buckets (ints): [NB] bucket starts, [NB + 1] first tile of each bucket
-// and the tile total, then with group padding [2][2M + 1] group tables.
-__host__ __device__ constexpr long long block_scan_ints(long long NB, long long M, bool pad) {
-  return 2 * NB + 1 + (pad ? 2 * (2 * M + 1) : 0);
+// and the tile total, then with group padding [2][ng + 1] group tables.
+__host__ __device__ constexpr long long block_scan_ints(long long NB, long long NG, bool pad) {
+  return 2 * NB + 1 + (pad ? 2 * (NG + 1) : 0);
 }
 
 __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kScanChunks]) {
@@ -735,8 +749,8 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
   const bool writer = (int)threadIdx.x % (int)gridDim.x == (int)blockIdx.x;
   const bool pad = a.gpad > 1;
   int *ts = start + a.NB;                            // [NB + 1] unpadded first tile of each bucket
-  int *gP = ts + a.NB + 1, *pp = gP + 2 * a.M + 1;   // [2M + 1] each, with group padding
-  const int g0 = lo / a.W, w0 = lo - g0 * a.W;
+  int *gP = ts + a.NB + 1, *pp = gP + a.ng + 1;      // [ng + 1] each, with group padding
+  const int g0 = lo / a.gw, w0 = lo - g0 * a.gw;
   {
     int pc = pc0, pt = pt0, g = g0, wi = w0;
 #pragma unroll
@@ -752,7 +766,7 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
           if (pad && wi == 0) gP[g] = pt;
           pc += n;
           pt += (n + a.tile - 1) >> tsh;
-          if (++wi == a.W) {
+          if (++wi == a.gw) {
             wi = 0;
             ++g;
           }
@@ -762,10 +776,10 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
   if (threadIdx.x == 0) ts[a.NB] = tot_t;
   int total = tot_t;
   if (pad) {
-    if (threadIdx.x == 0) gP[2 * a.M] = tot_t;
+    if (threadIdx.x == 0) gP[a.ng] = tot_t;
     __syncthreads();
     scan_group_pads(a, gP, pp, s_c);
-    total = pp[2 * a.M];
+    total = pp[a.ng];
   } else {
     __syncthreads();
   }
@@ -777,7 +791,7 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
     int u = k, l = 0, h = a.NB;                      // ts[l] <= u < ts[h]
     bool empty = false;
     if (pad) {
-      int gl = 0, gh = 2 * a.M;                      // pp[gl] <= k < pp[gh]
+      int gl = 0, gh = a.ng;                         // pp[gl] <= k < pp[gh]
       while (gh - gl > 1) {
         const int mid = (gl + gh) >> 1;
         if (pp[mid] <= k)
@@ -787,8 +801,8 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
       }
       u = k - pp[gl] + gP[gl];
       empty = u >= gP[gl + 1];
-      l = gl * a.W;
-      h = l + a.W;
+      l = gl * a.gw;
+      h = l + a.gw;
     }
     if (!empty) {
       while (h - l > 1) {
@@ -842,7 +856,7 @@ __device__ __forceinline__ void take_key(int (&key)[kScatterU], ReqRec (&rec)[kS
 }
 
 __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
-  extern __shared__ int start[];   // [NB] bucket starts, then with group padding [2][2M + 1]
+  extern __shared__ int start[];   // block_scan_ints(NB, ng, padded) ints
   int key[kScatterU], pos[kScatterU];
   ReqRec rec[kScatterU];
   if (a.scan_local) {
@@ -889,9 +903,9 @@ __host__ __device__ constexpr size_t score_lds_floats(int C, int CPL, int waves)
 // The scoring loop of score_requests_generic for one kind of tile: MODE 0 prompt-less
 // requests, 1 GPUs without SM caps, 2 capped GPUs (one loop per kind keeps the kind's branch
 // out of the loop body).
-template <int CPL, int MODE>
+template <int CPL, int MODE, int FNF>
 __device__ void generic_loop(const PlaceArgs &a, int m, int w, int beg, int end, int stride, float *lds) {
-  const int C = a.C, NF = a.NF;
+  const int C = FNF ? kNS8 * FNF : a.C, NF = FNF ? FNF : a.NF;
   float *dcs = lds;
   float *pds = lds + kRows * C + kWave * CPL;
   float *rows = pds + C;
@@ -1093,10 +1107,11 @@ __device__ void generic_loop(const PlaceArgs &a, int m, int w, int beg, int end,
 // Requests [beg, end) of bucket positions, read by this wavefront kQ at a time from beg with
 // step `stride`, of model m and arrival wave w (both wave-uniform; beg = end: no requests).
 // The whole workgroup calls it (it stages the model's decode table in LDS).
-template <int CPL>
+// FNF = 16: the 8 x 16 tables (their sizes known when compiled), 0: any.
+template <int CPL, int FNF = 0>
 __device__ void score_requests_generic(const PlaceArgs &a, int m, bool noprompt, int w, int beg, int end,
                                        int stride, float *lds) {
-  const int C = a.C, NF = a.NF;
+  const int C = FNF ? kNS8 * FNF : a.C, NF = FNF ? FNF : a.NF;
   float *dcs = lds;                                   // [32 * C + pad] decode table of the tile's model
   float *pds = lds + kRows * C + kWave * CPL;         // [C] s_j * f_k^3
   float *rows = pds + C;                              // [waves][Q][C] prompt rows (capped GPUs)
@@ -1120,11 +1135,11 @@ __device__ void score_requests_generic(const PlaceArgs &a, int m, bool noprompt,
   }
   __syncthreads();
   if (noprompt)
-    generic_loop<CPL, 0>(a, m, w, beg, end, stride, lds);
+    generic_loop<CPL, 0, FNF>(a, m, w, beg, end, stride, lds);
   else if (a.has_caps == 0)
-    generic_loop<CPL, 1>(a, m, w, beg, end, stride, lds);
+    generic_loop<CPL, 1, FNF>(a, m, w, beg, end, stride, lds);
   else
-    generic_loop<CPL, 2>(a, m, w, beg, end, stride, lds);
+    generic_loop<CPL, 2, FNF>(a, m, w, beg, end, stride, lds);
 }
 
 // Tile t of the tile table: its bucket's requests [first, first + tile), wavefront v taking
@@ -1535,19 +1550,19 @@ __global__ void __launch_bounds__(kWpb16 * 64) k_score_r16(PlaceArgs a) {
   if (idx >= per || t >= nblk) return;
   const auto tp = ro(reinterpret_cast<const int32_t *>(a.tiles));
   const int beg = tp[2 * TPB * t + 1];    // the workgroup's first request
-  const BucketId grp = bucket_id(a, tp[2 * TPB * t]);
+  const int b0 = tp[2 * TPB * t];         // the workgroup's first bucket
+  const BucketId grp = bucket_id(a, b0);
   const int m = grp.m;
   const int wv = uniform(threadIdx.x >> 6);
   const int ti = wv / S, sp = wv - ti * S;  // this wavefront's tile and part
   const int bk = tp[2 * (TPB * t + ti)];  // the tile's bucket (-1: an empty tile)
   const int q0 = bk >= 0 ? tp[2 * (TPB * t + ti) + 1] : beg;
   const int nq = bk >= 0 ? min(kR, ro(a.bstart)[bk + 1] - q0) : 0;
-  const int w = bk >= 0 ? bucket_id(a, bk).w : 0;
+  const int w = bk >= 0 ? grp.w + (bk - b0) : 0;   // the group's buckets are consecutive waves
   if (grp.noprompt) {                     // prompt-less requests: TTFT from the batch row
-    score_requests_generic<2>(a, m, true, w, q0 + sp * kQ, q0 + nq, S * kQ, lds);
+    score_requests_generic<2, 16>(a, m, true, w, q0 + sp * kQ, q0 + nq, S * kQ, lds);
     return;
   }
-
   // Staging waits on memory and barriers while other workgroups' pass 1 keeps the VALU busy:
   // at a raised wavefront priority its instructions issue first.
   __builtin_amdgcn_s_setprio(2);
@@ -1597,7 +1612,7 @@ __global__ void __launch_bounds__(kWpb16 * 64) k_score_r16(PlaceArgs a) {
 #pragma unroll
   for (int v = 0; v < WPB; ++v) tile_ok = tile_ok && s_ok[v];
   if (!tile_ok) {                         // mixed TBT SLOs or an unscalable request
-    score_requests_generic<2>(a, m, false, w, q0 + sp * kQ, q0 + nq, S * kQ, lds);
+    score_requests_generic<2, 16>(a, m, false, w, q0 + sp * kQ, q0 + nq, S * kQ, lds);
     return;
   }
   const float tsb = r0.slo_tbt;           // every request of the workgroup has this TBT SLO
@@ -1994,6 +2009,7 @@ struct PlaceLayout {
   size_t cnt, bstart, ntiles, tiles, gscan, host_cnt, host_list, recs, preq, key, off;
   size_t host_pos, cls_tab, pf_rowmin, pf_rowtiny, dc_min, total;
   int32_t NB, tile, max_tiles, waves_per_block, nch, gpad;
+  int32_t gw, ng;                // buckets per group and groups
   int32_t split;                 // 8 x 16 kernel: wavefronts per tile (1, 2 or 4)
   bool fast;                     // 8 SM x 16 frequency levels: the specialised kernel
   bool scan_local;               // k_scatter scans the bucket counts (no k_scan launch)
@@ -2012,6 +2028,14 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   const long long M = L->n_models, Gn = G->n_gpus, W = G->n_waves, R = Q->n_requests;
   const long long C = (long long)L->n_sm * L->n_freq;
   const long long NB = 2 * W * M;
+  // arrival-wave slabs: the largest divisor of W up to kXcds, gw waves each
+  int slabs = 1;
+  for (int d = kXcds; d > 1; --d)
+    if (W % d == 0) {
+      slabs = d;
+      break;
+    }
+  const long long gw = W / slabs, ng = 2 * M * slabs;
   if (NB > INT_MAX / 2 - 4 || Gn * C > INT_MAX || W * Gn > INT_MAX || M * Gn > INT_MAX) return false;
   // tile size: large tiles amortise the table staging, small ones fill the chip
   const bool fast = L->n_sm == 8 && L->n_freq == 16;
@@ -2034,9 +2058,9 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   }
   o->fast = fast;
   // the 8 x 16 kernel's workgroups take wpb / split tiles of one (model, prompt kind) group:
-  // each of the 2M groups is padded with fewer empty tiles than that
+  // each of the ng groups is padded with fewer empty tiles than that
   const int gpad = fast ? wpb / split : 1;
-  const long long max_tiles = (R + tile - 1) / tile + NB + (long long)(gpad - 1) * 2 * M;
+  const long long max_tiles = (R + tile - 1) / tile + NB + (long long)(gpad - 1) * ng;
   if (max_tiles > INT_MAX - 8) return false;   // the grid is rounded up to a multiple of 8
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -2048,7 +2072,7 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->bstart = take(sizeof(int32_t) * (NB + 1));
   o->ntiles = take(sizeof(int32_t));
   o->tiles = take(sizeof(int2) * max_tiles);
-  o->gscan = take(sizeof(int32_t) * (gpad > 1 ? 2 * (2 * M + 1) : 1));
+  o->gscan = take(sizeof(int32_t) * (gpad > 1 ? 2 * (ng + 1) : 1));
   o->host_cnt = take(sizeof(int32_t) * M);
   o->host_list = take(sizeof(int32_t) * M * Gn);
   o->recs = take(sizeof(HostRec) * W * Gn);
@@ -2064,13 +2088,15 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   o->total = off;
   o->nch = (int32_t)nch;
   o->NB = (int32_t)NB;
+  o->gw = (int32_t)gw;
+  o->ng = (int32_t)ng;
   static_assert((kR & (kR - 1)) == 0 && (kQ & (kQ - 1)) == 0, "tile sizes are powers of two");
   o->tile = tile;                       // a power of two: the bucket scans shift by its log2
   o->max_tiles = (int32_t)max_tiles;
   o->waves_per_block = wpb;
   o->gpad = gpad;
   o->split = split;
-  const long long scan_ints = block_scan_ints(NB, M, gpad > 1);
+  const long long scan_ints = block_scan_ints(NB, ng, gpad > 1);
   o->scan_local = NB <= kHistMax && scan_ints <= kScanLds;
   o->scatter_lds = o->scan_local ? sizeof(int32_t) * (size_t)scan_ints : 0;
   return true;
@@ -2177,6 +2203,8 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
   a.feasible = out->feasible;
   a.energy = out->energy_mj;
   a.NB = lay.NB;
+  a.gw = lay.gw;
+  a.ng = lay.ng;
   a.tile = lay.tile;
   a.max_tiles = lay.max_tiles;
   a.gpad = lay.gpad;
