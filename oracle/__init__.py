@@ -29,6 +29,30 @@ def build() -> str:
     return LIB_PATH
 
 
+# AddressSanitizer + UndefinedBehaviorSanitizer build of the same source (host code only, gcc):
+# any report aborts the process.  The library is loaded into an uninstrumented Python, so the
+# sanitizer runtime must come first: sanitized_env() gives the environment for that.
+SANITIZE_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=all", "-ffp-contract=off", "-fPIC", "-shared", "-Wall", "-Wextra"]
+
+
+def build_sanitized(path: str) -> str:
+    """Compile the oracle with ASan and UBSan into `path`."""
+    subprocess.run(["gcc", *SANITIZE_FLAGS, "-o", path, _SRC, "-lm"], check=True)
+    return path
+
+
+def sanitized_env(path: str) -> dict:
+    """Environment for a child Python that loads the sanitized oracle at `path`."""
+    asan = subprocess.run(["gcc", "-print-file-name=libasan.so"], check=True, stdout=subprocess.PIPE,
+                          text=True).stdout.strip()
+    ubsan = subprocess.run(["gcc", "-print-file-name=libubsan.so"], check=True, stdout=subprocess.PIPE,
+                           text=True).stdout.strip()
+    env = dict(os.environ, FESTINA_ORACLE_LIB=path, LD_PRELOAD=f"{asan}:{ubsan}",
+               ASAN_OPTIONS="detect_leaks=0:abort_on_error=1", UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    return env
+
+
 class _Lut(C.Structure):
     _fields_ = [("n_models", C.c_int32), ("n_rows", C.c_int32), ("n_sm", C.c_int32),
                 ("n_freq", C.c_int32), ("sm_level", C.c_void_p), ("freq_level", C.c_void_p),
