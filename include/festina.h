@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define FESTINA_ABI_VERSION 1
+#define FESTINA_ABI_VERSION 2
 #define FESTINA_N_ROWS 32        /* rows of every profile table */
 #define FESTINA_MAX_CELLS 256    /* n_sm * n_freq limit of the placement kernels */
 #define FESTINA_MAX_FREQ_MIG 32  /* n_freq limit of the migration kernels (32-bit level masks) */
@@ -65,6 +65,8 @@ extern "C" {
 #define FESTINA_MAX_TASKS 64     /* task slots per batch of the sweep kernel */
 #define FESTINA_PREFILL 0        /* task phases of the sweep */
 #define FESTINA_DECODE 1
+#define FESTINA_STATIC_PER_TASK 0    /* sweep energy: static power in every task's Power x Latency */
+#define FESTINA_STATIC_PER_BATCH 1   /* sweep energy: static power once, over the batch's longest task */
 /* Device scratch that festina_score_placements_noalloc holds per GPU (32 MiB: the
  * 262,144-request, 1,024-GPU, 64-wave placement search needs 11.3 MiB of it). */
 #define FESTINA_NOALLOC_WORKSPACE_BYTES ((size_t)32 << 20)
@@ -239,13 +241,16 @@ typedef struct festina_batches {
   const float *util;                 /* [B] utilisation u of the batch's GPU in the power model */
   const int32_t *sm_units;           /* [NS] integer SM share of each level */
   int32_t sm_budget;                 /* shares must sum to < sm_budget */
+  int32_t static_power;              /* FESTINA_STATIC_PER_TASK or FESTINA_STATIC_PER_BATCH */
 } festina_batches;
 
 /* Sweep results (device memory, written by the call):
  *   freq_level[b] = least-energy usable frequency level, lowest on exact ties; -1 if none;
  *   feasible[b]   = 1 if a level was chosen, else 0;
- *   energy_mj[b]  = sum over tasks of (P0 + k_dyn * s_j * f^3 * u) * latency at that level
- *                   (float32), +inf if none;
+ *   energy_mj[b]  = at that level, with FESTINA_STATIC_PER_TASK the sum over tasks of
+ *                   (P0 + k_dyn * s_j * f^3 * u) * latency, with FESTINA_STATIC_PER_BATCH
+ *                   P0 * (the longest task's latency) + the sum over tasks of
+ *                   k_dyn * s_j * f^3 * u * latency (float32); +inf if none;
  *   task_sm[b][t] = SM level of task t at that level (the smallest whose latency is below
  *                   the slack); -1 for slots t >= n_tasks[b] and for infeasible batches. */
 typedef struct festina_sweep_result {
@@ -259,7 +264,11 @@ typedef struct festina_sweep_result {
  * share per task that meets its deadline, the device SM budget, the least predicted
  * energy).  Needs no workspace.  Requires n_freq <= FESTINA_MAX_FREQ_SWEEP,
  * n_sm <= FESTINA_MAX_CELLS and max_tasks <= FESTINA_MAX_TASKS.  One kernel launch on
- * `stream`. */
+ * `stream`.  The paper does not say how the tasks' energies combine; static_power selects
+ * the reading (FESTINA_STATIC_PER_TASK, Power x Latency per task as the placement search
+ * charges it per request, or FESTINA_STATIC_PER_BATCH, the device's static power once over
+ * the batch's longest task since the partitions run side by side); any other value is
+ * FESTINA_ERR_INVALID. */
 festina_status festina_sweep_batches(const festina_lut *lut, const festina_batches *batches,
                                      festina_sweep_result *out, void *stream);
 

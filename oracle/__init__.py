@@ -84,7 +84,7 @@ class _Batches(C.Structure):
     _fields_ = [("n_batches", C.c_int32), ("max_tasks", C.c_int32), ("n_tasks", C.c_void_p),
                 ("task_model", C.c_void_p), ("task_phase", C.c_void_p), ("task_tokens", C.c_void_p),
                 ("task_slack_ms", C.c_void_p), ("k_dyn_w", C.c_void_p), ("util", C.c_void_p),
-                ("sm_units", C.c_void_p), ("sm_budget", C.c_int32)]
+                ("sm_units", C.c_void_p), ("sm_budget", C.c_int32), ("static_power", C.c_int32)]
 
 
 class _Llms(C.Structure):
@@ -239,7 +239,7 @@ def _batches(d, pin):
                     pin(d["task_model"], np.int32), pin(d["task_phase"], np.int32),
                     pin(d["task_tokens"], np.int32), pin(d["task_slack_ms"], np.float32),
                     pin(d["k_dyn_w"], np.float32), pin(d["util"], np.float32),
-                    pin(d["sm_units"], np.int32), int(d["sm_budget"]))
+                    pin(d["sm_units"], np.int32), int(d["sm_budget"]), int(d.get("static_power", 0)))
 
 
 def _llms(d, pin):

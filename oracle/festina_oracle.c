@@ -312,8 +312,12 @@ int festina_oracle_score_migrations(const or_lut *L, const or_fleet *F, int32_t 
  * below the task's remaining slack; the level is usable only when every task has such an
  * SM level and the SM shares sum to strictly less than the device budget ("< 100%");
  * the batch's energy at k is the sum over its tasks of Power x Latency with the same
- * closed-form power model as placement, P = P0 + k_dyn * s * f^3 * u.  The chosen level
- * is the least-energy usable one, the lowest k on exact ties. */
+ * closed-form power model as placement, P = P0 + k_dyn * s * f^3 * u.  The paper leaves
+ * open how the tasks' energies combine; static_power selects the reading: 0 charges P0 in
+ * every task's term (as placement charges it per request), 1 charges it once, over the
+ * longest task (the partitions run side by side on one device), the dynamic terms still
+ * per task.  The chosen level is the least-energy usable one, the lowest k on exact
+ * ties. */
 typedef struct {
   int32_t n_batches, max_tasks;
   const int32_t *n_tasks;        /* [B] */
@@ -325,6 +329,7 @@ typedef struct {
   const float *util;             /* [B] */
   const int32_t *sm_units;       /* [NS] integer SM share of each level */
   int32_t sm_budget;
+  int32_t static_power;          /* 0: P0 per task, 1: P0 over the longest task */
 } or_batches;
 
 /* Table row of task t of batch b, or -1 when the task is invalid.  Prefill rows are the
@@ -370,15 +375,21 @@ static int or_sweep_level(const or_lut *L, const or_batches *S, int b, int k, do
   const double f3 = or_cube((double)L->freq_level[k]);
   const double kg = (double)S->k_dyn_w[b], u = (double)S->util[b];
   int64_t units = 0;
-  double E = 0.0;
+  double E = 0.0, longest = 0.0;
   for (int t = 0; t < S->n_tasks[b]; ++t) {
     const int j = or_min_sm(L, S, b, t, k);
     if (j < 0) return 0;
     units += S->sm_units[j];
     const double lat = (double)or_task_latency(L, S, b, t, or_task_row(L, S, b, t), j, k);
-    const double P = L->p0_w + kg * (double)L->sm_level[j] * f3 * u;
-    E += P * lat;
+    const double dyn = kg * (double)L->sm_level[j] * f3 * u;
+    if (S->static_power == 0) {
+      E += (L->p0_w + dyn) * lat;
+    } else {
+      E += dyn * lat;
+      if (lat > longest) longest = lat;
+    }
   }
+  if (S->static_power != 0) E += L->p0_w * longest;
   if (!(units < (int64_t)S->sm_budget)) return 0;
   if (!((float)E < INFINITY)) return 0;
   *energy = E;
@@ -403,6 +414,7 @@ int festina_oracle_sweep(const or_lut *L, const or_batches *S, int32_t n_sel, co
                          int32_t *freq_level, uint8_t *feasible, double *energy_mj, int32_t *task_sm) {
   if (!or_lut_ok(L) || !S || !freq_level || !feasible || !energy_mj || !task_sm) return 1;
   if (S->n_batches < 0 || S->max_tasks < 1 || !S->sm_units) return 1;
+  if (S->static_power != 0 && S->static_power != 1) return 1;
   const int32_t n = sel ? n_sel : S->n_batches;
   for (int32_t i = 0; i < n; ++i) {
     const int32_t b = sel ? sel[i] : i;

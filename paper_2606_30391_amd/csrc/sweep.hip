@@ -6,8 +6,10 @@
 // task takes the smallest SM level whose profiled latency is strictly below its slack;
 // level k is usable when every task has such a level and their integer SM shares sum to
 // strictly less than the device budget; the batch energy at k is the sum over tasks of
-// (P0 + k_dyn * s_j * f_k^3 * u) * latency.  The least-energy usable level wins, the
-// lowest k on exact ties.
+// (P0 + k_dyn * s_j * f_k^3 * u) * latency (static power per task), or P0 times the
+// longest task's latency plus the sum over tasks of k_dyn * s_j * f_k^3 * u * latency
+// (static power per batch).  The least-energy usable level wins, the lowest k on exact
+// ties.
 //
 // Layout of the work: one wavefront per batch.  The batch's slot fields arrive in one
 // memory round trip (lane t loads slot t) and go to LDS as a table offset, phase and slack
@@ -23,7 +25,8 @@
 //
 // Exactness: the SM-level choice compares a float32 table entry with a float32 slack and
 // the budget test adds integers, so both are decided exactly.  Energies are float32:
-// P = fma(k_dyn * u * f^3, s_j, P0), E = sum of fma(P, latency, E).
+// P = fma(k_dyn * u * f^3, s_j, P0), E = sum of fma(P, latency, E) per task; per batch
+// E = fma(P0, longest latency, sum of fma(k_dyn * u * f^3 * s_j, latency, E)).
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -44,12 +47,13 @@ constexpr float kInf = __builtin_huge_valf();
 struct SweepArgs {
   int32_t M, NS, NF;
   const float *sm_level, *freq_level, *pf, *dc;
-  float p0;
   int32_t B, T;
   const int32_t *n_tasks, *model, *phase, *tokens;
   const float *slack, *kdyn, *util;
   const int32_t *units;
   int32_t budget;
+  float p0_task;                 // P0 in each task's power (static power per task), else 0
+  float p0_batch;                // P0 over the longest task (static power per batch), else 0
   int32_t lg;                    // log2 of the lanes per slot group (NF <= 1 << lg)
   int32_t *level;
   uint8_t *feasible;
@@ -175,7 +179,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep(SweepArgs a) {
   const float f = kv ? a.freq_level[k] : 1.f;
   const float c = kd * u * (f * f * f);
   long long units = 0;
-  float E = 0.f;
+  float E = 0.f, lmax = 0.f;     // energy, the longest task's latency
   int miss = 0;                  // some task has no SM level meeting its slack at k
   int jk0 = -1, jk1 = -1;        // SM levels of the lane's first two tasks
   // two tasks per step: 2 * kJChunk table loads in flight per lane
@@ -197,7 +201,8 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep(SweepArgs a) {
       miss = 1;
     } else {
       units += s_units[j0];
-      E = fmaf(fmaf(c, s_lev[j0], a.p0), lat0, E);
+      E = fmaf(fmaf(c, s_lev[j0], a.p0_task), lat0, E);
+      lmax = fmaxf(lmax, lat0);
     }
     int j1 = -1;
     if (on1) {
@@ -209,7 +214,8 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep(SweepArgs a) {
         miss = 1;
       } else {
         units += s_units[j1];
-        E = fmaf(fmaf(c, s_lev[j1], a.p0), lat1, E);
+        E = fmaf(fmaf(c, s_lev[j1], a.p0_task), lat1, E);
+        lmax = fmaxf(lmax, lat1);
       }
     }
     if (t0 == grp) {
@@ -221,8 +227,10 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep(SweepArgs a) {
   for (int off = nfp; off < kWave; off <<= 1) {
     units += __shfl_xor(units, off, kWave);
     E += __shfl_xor(E, off, kWave);
+    lmax = fmaxf(lmax, __shfl_xor(lmax, off, kWave));
     miss |= __shfl_xor(miss, off, kWave);
   }
+  E = fmaf(a.p0_batch, lmax, E);         // static power over the longest task (per batch)
   const bool usable = kv && !bad && !miss && units < (long long)a.budget && E < kInf;
   float be = usable ? E : kInf;
   int bk = usable ? k : INT_MAX;
@@ -318,7 +326,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep_8x16(SweepArgs
 
     const float c = kd * u * f3;
     long long units = 0;
-    float E = 0.f;
+    float E = 0.f, lmax = 0.f;
     int miss = 0;
     for (int t = 0; !bad && t < nn; t += kTasksInFlight) {
       const float *cp[kTasksInFlight];
@@ -344,10 +352,12 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_sweep_8x16(SweepArgs
           miss = 1;
         } else {
           units += s_units[j];
-          E = fmaf(fmaf(c, s_lev[j], a.p0), lat, E);
+          E = fmaf(fmaf(c, s_lev[j], a.p0_task), lat, E);
+          lmax = fmaxf(lmax, lat);
         }
       }
     }
+    E = fmaf(a.p0_batch, lmax, E);       // static power over the longest task (per batch)
     const bool usable = !bad && !miss && units < (long long)a.budget && E < kInf;
     float be = usable ? E : kInf;
     int bk = usable ? k : INT_MAX;
@@ -380,6 +390,8 @@ extern "C" festina_status festina_sweep_batches(const festina_lut *L, const fest
   if (!L || !S || !out) return FESTINA_ERR_INVALID;
   if (L->n_models < 1 || L->n_rows != kRows || L->n_sm < 1 || L->n_freq < 1) return FESTINA_ERR_INVALID;
   if (S->n_batches < 0 || S->max_tasks < 1) return FESTINA_ERR_INVALID;
+  if (S->static_power != FESTINA_STATIC_PER_TASK && S->static_power != FESTINA_STATIC_PER_BATCH)
+    return FESTINA_ERR_INVALID;
   if (L->n_freq > FESTINA_MAX_FREQ_SWEEP || L->n_sm > kMaxSm || S->max_tasks > FESTINA_MAX_TASKS)
     return FESTINA_ERR_UNSUPPORTED;
   if (!L->sm_level || !L->freq_level || !L->pf || !L->dc || !S->sm_units) return FESTINA_ERR_INVALID;
@@ -396,7 +408,6 @@ extern "C" festina_status festina_sweep_batches(const festina_lut *L, const fest
   a.freq_level = L->freq_level;
   a.pf = L->pf;
   a.dc = L->dc;
-  a.p0 = L->p0_w;
   a.B = S->n_batches;
   a.T = S->max_tasks;
   a.n_tasks = S->n_tasks;
@@ -408,6 +419,8 @@ extern "C" festina_status festina_sweep_batches(const festina_lut *L, const fest
   a.util = S->util;
   a.units = S->sm_units;
   a.budget = S->sm_budget;
+  a.p0_task = S->static_power == FESTINA_STATIC_PER_TASK ? L->p0_w : 0.f;
+  a.p0_batch = S->static_power == FESTINA_STATIC_PER_BATCH ? L->p0_w : 0.f;
   a.lg = 0;
   while ((1 << a.lg) < a.NF) ++a.lg;
   a.level = out->freq_level;

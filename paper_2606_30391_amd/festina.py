@@ -22,6 +22,8 @@ FESTINA_ERR_DEVICE = 2
 FESTINA_ERR_UNSUPPORTED = 3
 FESTINA_ERR_TOO_LARGE = 4
 FESTINA_NOALLOC_WORKSPACE_BYTES = 32 << 20
+FESTINA_STATIC_PER_TASK = 0      # sweep energy readings (festina_batches.static_power)
+FESTINA_STATIC_PER_BATCH = 1
 
 
 class FestinaError(RuntimeError):
@@ -69,7 +71,7 @@ class festina_batches(C.Structure):
     _fields_ = [("n_batches", C.c_int32), ("max_tasks", C.c_int32), ("n_tasks", C.c_void_p),
                 ("task_model", C.c_void_p), ("task_phase", C.c_void_p), ("task_tokens", C.c_void_p),
                 ("task_slack_ms", C.c_void_p), ("k_dyn_w", C.c_void_p), ("util", C.c_void_p),
-                ("sm_units", C.c_void_p), ("sm_budget", C.c_int32)]
+                ("sm_units", C.c_void_p), ("sm_budget", C.c_int32), ("static_power", C.c_int32)]
 
 
 class festina_sweep_result(C.Structure):
@@ -346,7 +348,7 @@ class DeviceSweep:
         self.batches = festina_batches(self.B, self.T, _ptr(t["n_tasks"]), _ptr(t["task_model"]),
                                        _ptr(t["task_phase"]), _ptr(t["task_tokens"]), _ptr(t["task_slack_ms"]),
                                        _ptr(t["k_dyn_w"]), _ptr(t["util"]), _ptr(t["sm_units"]),
-                                       int(bt["sm_budget"]))
+                                       int(bt["sm_budget"]), int(bt.get("static_power", 0)))
         n = max(self.B, 1)
         self.level = torch.empty(n, dtype=torch.int32, device=device)
         self.feasible = torch.empty(n, dtype=torch.uint8, device=device)

@@ -195,9 +195,13 @@ def sweep_levels(inp, b):
         if not sum(int(bt["sm_units"][j]) for j in assign) < int(bt["sm_budget"]):
             continue
         f = float(lut["freq_level"][k])
-        e = sum(power(lut["p0_w"], float(bt["k_dyn_w"][b]), float(lut["sm_level"][assign[t]]), f,
-                      float(bt["util"][b])) * float(tab[m, row, assign[t], k])
-                for t, (tab, m, row) in enumerate(rows))
+        lat = [float(tab[m, row, assign[t], k]) for t, (tab, m, row) in enumerate(rows)]
+        if bt.get("static_power", 0) == 0:     # P0 in every task's Power x Latency
+            e = sum(power(lut["p0_w"], float(bt["k_dyn_w"][b]), float(lut["sm_level"][assign[t]]), f,
+                          float(bt["util"][b])) * lat[t] for t in range(n))
+        else:                                  # P0 once, over the longest task
+            e = sum(power(0.0, float(bt["k_dyn_w"][b]), float(lut["sm_level"][assign[t]]), f,
+                          float(bt["util"][b])) * lat[t] for t in range(n)) + lut["p0_w"] * max(lat, default=0.0)
         if not np.float32(e) < np.inf:
             continue
         out.append((e, k, assign))

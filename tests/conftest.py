@@ -108,6 +108,7 @@ def golden_sweep(variant=None):
             spec["p0_w"] = ch["p0_w"]
         bt["sm_units"] = ch.get("sm_units", bt["sm_units"])
         bt["sm_budget"] = ch.get("sm_budget", bt["sm_budget"])
+        bt["static_power"] = ch.get("static_power", 0)
         slack = ch.get("slack_ms", slack)
         exp = v["expected"]
     lut = _tables(spec)
@@ -119,7 +120,8 @@ def golden_sweep(variant=None):
                "task_slack_ms": np.array([slack], np.float32),
                "k_dyn_w": np.array([bt["k_dyn_w"]], np.float32),
                "util": np.array([bt["util"]], np.float32),
-               "sm_units": np.array(bt["sm_units"], np.int32), "sm_budget": int(bt["sm_budget"])}
+               "sm_units": np.array(bt["sm_units"], np.int32), "sm_budget": int(bt["sm_budget"]),
+               "static_power": int(bt.get("static_power", 0))}
     return {"lut": lut, "batches": batches}, exp, d
 
 

@@ -47,7 +47,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert F.festina_abi_version() == 1
+    assert F.festina_abi_version() == 2
     for s in range(5):
         assert F.festina_status_string(s)
     assert "scratch" in F.festina_status_string(F.FESTINA_ERR_TOO_LARGE)
@@ -178,7 +178,7 @@ def test_sweep_rejects_bad_arguments(lib):
         setattr(lut, field, value)
         assert _sweep_status(lut, bat, out) == status, field
     for field, value in [("n_batches", -1), ("max_tasks", 0), ("sm_units", None), ("task_slack_ms", None),
-                         ("n_tasks", None), ("util", None)]:
+                         ("n_tasks", None), ("util", None), ("static_power", 2), ("static_power", -1)]:
         lut, bat, out = _sweep_structs()
         setattr(bat, field, value)
         assert _sweep_status(lut, bat, out) == F.FESTINA_ERR_INVALID, field

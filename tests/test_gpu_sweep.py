@@ -56,13 +56,29 @@ def test_sweep_workload_full_size():
     assert 0.3 < fe.mean() < 0.8
 
 
+def test_sweep_workload_static_power_per_batch():
+    inp = W.make_sweep(n_gpus=512, n_epochs=32)
+    inp["batches"]["static_power"] = 1
+    got, rep = parity_sweep(inp, label="static power per batch, 512 GPUs x 32 epochs")
+
+
+@pytest.mark.parametrize("NS,NF,T", [(4, 8, 7), (8, 16, 16), (3, 5, 40)])
+def test_sweep_static_power_per_batch_shapes(NS, NF, T):
+    rng = np.random.default_rng(900 + NS * 100 + NF)
+    inp = W.make_tiny_sweep(rng, B=517, T=T, M=3, NS=NS, NF=NF, nan_cells=True)
+    inp["batches"]["static_power"] = 1
+    parity_sweep(inp, label=f"static power per batch NS={NS} NF={NF} T={T}")
+
+
 @pytest.mark.parametrize("extra", [100, 200, 300])
 def test_sweep_workload_seeds(extra):
     parity_sweep(W.make_sweep(seed=W.SWEEP_SEED + extra, n_gpus=256, n_epochs=16), label=f"seed +{extra}")
 
 
 @pytest.mark.parametrize("variant", [None, "static power dominates", "budget reached exactly",
-                                     "budget one unit above", "slack equal to a latency"])
+                                     "budget one unit above", "slack equal to a latency",
+                                     "static power per batch", "static power per task, P0 = 640",
+                                     "static power per batch, P0 = 640"])
 def test_sweep_worked_example(variant):
     inp, exp, d = golden_sweep(variant)
     lev, fe, en, tsm = run_sweep(inp)

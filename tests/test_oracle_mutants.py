@@ -55,10 +55,9 @@ SWEEP = [
      "if (or_task_latency(L, S, b, t, row, j, k) <= slack) return j;"),
     ("inclusive SM budget", "if (!(units < (int64_t)S->sm_budget)) return 0;",
      "if (!(units <= (int64_t)S->sm_budget)) return 0;"),
-    ("dropped static power", "const double P = L->p0_w + kg * (double)L->sm_level[j] * f3 * u;",
-     "const double P = kg * (double)L->sm_level[j] * f3 * u;"),
-    ("utilisation dropped", "const double P = L->p0_w + kg * (double)L->sm_level[j] * f3 * u;",
-     "const double P = L->p0_w + kg * (double)L->sm_level[j] * f3;"),
+    ("dropped static power", "E += (L->p0_w + dyn) * lat;", "E += dyn * lat;"),
+    ("utilisation dropped", "const double dyn = kg * (double)L->sm_level[j] * f3 * u;",
+     "const double dyn = kg * (double)L->sm_level[j] * f3;"),
     ("f instead of f^3", "const double f3 = or_cube((double)L->freq_level[k]);\n  const double kg = (double)S->k_dyn_w[b]",
      "const double f3 = (double)L->freq_level[k];\n  const double kg = (double)S->k_dyn_w[b]"),
     ("decode reads the prefill table", "const float *tab = S->task_phase[at] == 0 ? L->pf : L->dc;",
@@ -68,7 +67,12 @@ SWEEP = [
      "for (int j = L->n_sm - 1; j >= 0; --j)\n    if (or_task_latency"),
     ("decode row off by one", "if (ph == 1) return (tok > OR_ROWS ? OR_ROWS : tok) - 1;",
      "if (ph == 1) return tok >= OR_ROWS ? OR_ROWS - 1 : tok;"),
-    ("longest task instead of the sum", "    E += P * lat;", "    E = E > P * lat ? E : P * lat;"),
+    ("longest task instead of the sum", "      E += (L->p0_w + dyn) * lat;",
+     "      E = E > (L->p0_w + dyn) * lat ? E : (L->p0_w + dyn) * lat;"),
+    ("per-batch static power over the sum of latencies", "if (lat > longest) longest = lat;", "longest += lat;"),
+    ("per-batch static power dropped", "if (S->static_power != 0) E += L->p0_w * longest;", ""),
+    ("per-batch reading charges static power per task", "if (S->static_power == 0) {", "if (1) {"),
+    ("per-batch dynamic terms of the longest task only", "      E += dyn * lat;\n", "      E = E > dyn * lat ? E : dyn * lat;\n"),
     ("highest level wins ties", "      if (bk < 0 || e < be) {", "      if (bk < 0 || e <= be) {"),
 ]
 

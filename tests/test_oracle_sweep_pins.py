@@ -42,7 +42,9 @@ def test_sweep_worked_example():
 
 
 @pytest.mark.parametrize("variant", ["static power dominates", "budget reached exactly",
-                                     "budget one unit above", "slack equal to a latency"])
+                                     "budget one unit above", "slack equal to a latency",
+                                     "static power per batch", "static power per task, P0 = 640",
+                                     "static power per batch, P0 = 640"])
 def test_sweep_worked_example_variants(variant):
     inp, exp, d = golden_sweep(variant)
     _expect(oracle.sweep(inp), exp)
@@ -51,10 +53,12 @@ def test_sweep_worked_example_variants(variant):
 
 # ------------------------------------------------------------------ brute force
 @pytest.mark.parametrize("seed", range(6))
-def test_sweep_matches_enumeration(seed):
+@pytest.mark.parametrize("static_power", [0, 1])
+def test_sweep_matches_enumeration(seed, static_power):
     rng = np.random.default_rng(7000 + seed)
     for case in range(40):
         inp = W.make_tiny_sweep(rng, nan_cells=(case % 3 == 0), zero_power=(case % 7 == 0))
+        inp["batches"]["static_power"] = static_power
         lev, fe, en, tsm = oracle.sweep(inp)
         blev, bfe, ben, btsm = brute_sweep(inp)
         assert np.array_equal(fe, bfe), (seed, case)
