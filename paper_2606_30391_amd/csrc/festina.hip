@@ -1747,13 +1747,20 @@ __global__ void __launch_bounds__(kWpb16 * 64) k_score_r16(PlaceArgs a) {
   while (nq > 0 && __ballot(cellv < kNoCell) != 0ull) {
     r16_store_q(L, Qi, Ks, cellv);
     // T[q][j] = request q's term at level j and its tied cell's frequency level: lanes j < 8
-    // read lane (j % 4) * 16 + k of xA[q] (j < 4) or xB[q]; every request at once
+    // read lane (j % 4) * 16 + k of xA[q] (j < 4) or xB[q]; every request at once.  The
+    // cell comes from lane 4q by readlane and every permute is issued before the first store
+    // (a cell read back from LDS would wait behind the previous request's store).
+    float tv[kR];
 #pragma unroll
     for (int q = 0; q < kR; ++q) {
-      const int ck = (int)reinterpret_cast<const v2u *>(L + Qi + q * 8)->y & 15;
+      const int ck = __builtin_amdgcn_readlane(cellv, 4 * q) & 15;
       const uint32_t src = (uint32_t)((lane & 3) * 16 + ck) * 4u;
       const float xa = bperm(src, xA[q]), xb = bperm(src, xB[q]);
-      if (lane < 8) *reinterpret_cast<float *>(L + Tw + (q * 8 + lane) * 4) = lane < 4 ? xa : xb;
+      tv[q] = lane < 4 ? xa : xb;
+    }
+    if (lane < 8) {
+#pragma unroll
+      for (int q = 0; q < kR; ++q) *reinterpret_cast<float *>(L + Tw + (q * 8 + lane) * 4) = tv[q];
     }
     wave_sync();
     // Lanes take 64 hosts at a time in ascending order; each pending request is evaluated at
