@@ -124,6 +124,13 @@ struct PlaceArgs {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// A fresh copy of a wave-uniform value: whatever is computed from it (addresses, tests) is
+// computed where it is used, not kept in scalar registers from an earlier computation.
+__device__ __forceinline__ int fresh_s(int v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+
 __device__ __forceinline__ float cube(float f) { return f * f * f; }
 
 // Read-only view in the constant address space: buffers that a kernel never writes
@@ -914,8 +921,10 @@ __device__ void generic_loop(const PlaceArgs &a, int m, int w, int beg, int end,
   const int lane = threadIdx.x & (kWave - 1);
   float *myrows = rows + (size_t)wv * kQ * C;
   const int hcnt = ro(a.host_cnt)[m];
-  const auto hl = ro(a.host_list + (size_t)m * (unsigned)a.G);
-  const auto rw = ro(a.recs + (size_t)w * (unsigned)a.G);
+  // the model's host list and the wave's records are addressed afresh for each GPU (a few
+  // scalar instructions) instead of holding both 64-bit bases through the request loop
+  const auto hl = [&](int i) { return ro(a.host_list)[(size_t)fresh_s(m) * (unsigned)a.G + i]; };
+  const auto rw = [&]() { return ro(a.recs + (size_t)fresh_s(w) * (unsigned)a.G); };
   const float p0 = a.p0;
 
   int cj[CPL], ck[CPL];
@@ -966,8 +975,8 @@ __device__ void generic_loop(const PlaceArgs &a, int m, int w, int beg, int end,
       // TTFT from the prefill table at the decode batch row (global, L2-resident)
       const float *pfm = a.pf + (size_t)m * kRows * C;
       for (int i = 0; i < hcnt; ++i) {
-        const int g = hl[i];
-        const HostRec rec = load_rec(rw, g);
+        const int g = hl(i);
+        const HostRec rec = load_rec(rw(), g);
         if (rec.row_off < 0) continue;
         const int cp = rec.caps & 0xff, cd = (rec.caps >> 8) & 0xff;
         // the cell tests are remade per GPU from vector values, not held as lane masks in
@@ -1010,8 +1019,8 @@ __device__ void generic_loop(const PlaceArgs &a, int m, int w, int beg, int end,
         }
       }
       for (int i = 0; i < hcnt; ++i) {
-        const int g = hl[i];
-        const HostRec rec = load_rec(rw, g);
+        const int g = hl(i);
+        const HostRec rec = load_rec(rw(), g);
         if (rec.row_off < 0) continue;
         const float *drow = dcs + rec.row_off + lane * CPL;
 #pragma unroll
@@ -1043,8 +1052,8 @@ __device__ void generic_loop(const PlaceArgs &a, int m, int w, int beg, int end,
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       for (int i = 0; i < hcnt; ++i) {
-        const int g = hl[i];
-        const HostRec rec = load_rec(rw, g);
+        const int g = hl(i);
+        const HostRec rec = load_rec(rw(), g);
         if (rec.row_off < 0) continue;
         const int cp = rec.caps & 0xff, cd = (rec.caps >> 8) & 0xff;
         // the cell tests are remade per GPU from vector values, not held as lane masks in
@@ -1474,12 +1483,6 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// A fresh copy of a wave-uniform value: whatever is computed from it (addresses, tests) is
-// computed where it is used, not kept in scalar registers from an earlier computation.
-__device__ __forceinline__ int fresh_s(int v) {
-  asm volatile("" : "+s"(v));
-  return v;
-}
 
 // A fresh copy of the lane id: a test made on it is made where it is used, not kept as a lane
 // mask in scalar registers across a loop.

@@ -70,16 +70,25 @@ __device__ __forceinline__ int task_row(const SweepArgs &a, int m, int ph, int t
   return -1;
 }
 
+// A fresh copy of a wave-uniform value: what is computed from it (the column strides and
+// level tests of a chunk) is computed where it is used instead of being kept, one scalar
+// register pair per level, across the whole task loop.
+__device__ __forceinline__ int fresh_s(int v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+
 // Smallest SM level j with latency[j][k] < slack for the task whose (model, row) table
 // column starts at `col`; -1 if none.  `lat` receives that latency.
 __device__ __forceinline__ int min_sm_level(const SweepArgs &a, const float *col, float slack, float &lat) {
   int jj = -1;
   lat = 0.f;
   for (int j0 = 0; j0 < a.NS && jj < 0; j0 += kJChunk) {
+    const int ns = fresh_s(a.NS), nf = fresh_s(a.NF);
     float v[kJChunk];
 #pragma unroll
     for (int q = 0; q < kJChunk; ++q)
-      v[q] = j0 + q < a.NS ? col[(size_t)(j0 + q) * a.NF] : __builtin_nanf("");
+      v[q] = j0 + q < ns ? col[(size_t)(j0 + q) * nf] : __builtin_nanf("");
 #pragma unroll
     for (int q = kJChunk - 1; q >= 0; --q)
       if (v[q] < slack) {
@@ -93,9 +102,10 @@ __device__ __forceinline__ int min_sm_level(const SweepArgs &a, const float *col
 // First table chunk of a task column: kJChunk loads issued together (NaN past NS and for
 // lanes without work), then the smallest level below the slack; -1 if none in the chunk.
 __device__ __forceinline__ void load_chunk(const SweepArgs &a, const float *col, bool on, float (&v)[kJChunk]) {
+  const int ns = fresh_s(a.NS), nf = fresh_s(a.NF);
 #pragma unroll
   for (int q = 0; q < kJChunk; ++q)
-    v[q] = (on && q < a.NS) ? col[(size_t)q * a.NF] : __builtin_nanf("");
+    v[q] = (on && q < ns) ? col[(size_t)q * nf] : __builtin_nanf("");
 }
 
 __device__ __forceinline__ int first_below(const float (&v)[kJChunk], float slack, float &lat) {
@@ -115,10 +125,11 @@ __device__ int min_sm_level_from_chunk(const SweepArgs &a, const float *col, flo
   int jj = -1;
   lat = 0.f;
   for (int j0 = kJChunk; j0 < a.NS && jj < 0; j0 += kJChunk) {
+    const int ns = fresh_s(a.NS), nf = fresh_s(a.NF);
     float v[kJChunk];
 #pragma unroll
     for (int q = 0; q < kJChunk; ++q)
-      v[q] = j0 + q < a.NS ? col[(size_t)(j0 + q) * a.NF] : __builtin_nanf("");
+      v[q] = j0 + q < ns ? col[(size_t)(j0 + q) * nf] : __builtin_nanf("");
 #pragma unroll
     for (int q = kJChunk - 1; q >= 0; --q)
       if (v[q] < slack) {
