@@ -574,15 +574,10 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
-        if i % SAMPLE == 0:
-            F.festina_set_timing_events(evs[i // SAMPLE][0], evs[i // SAMPLE][1])
-        elif i % SAMPLE == 1:
-            F.festina_set_timing_events()
-        dp.run()
+        dp.run(events=evs[i // SAMPLE] if i % SAMPLE == 0 else None)
         dm.run(side)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    F.festina_set_timing_events()
     score_ms = float(np.mean([hip.elapsed_ms(e[0], e[1]) for e in evs]))
     for e in evs:
         for x in e:
@@ -721,20 +716,19 @@ def per_config(F, W, hip, torch, verbose=False):
             dev = F.DevicePlacement(inp, "cuda")
             work = placement_candidates(inp)
             ops = distinct_candidates(inp) * OPS_PER_CANDIDATE
-            idx = (0, 1)
         else:
             inp = W.make_fleet()
             dev = F.DeviceMigration(inp, "cuda")
             G = inp["fleet"]["n_gpus"]
             work = G * (G - 1)
             ops = work * OPS_PER_PAIR
-            idx = (2, 3)
         reps = 10 if cfg == 4 else 50
         for _ in range(5):
             dev.run()
         torch.cuda.synchronize()
-        # call time with the library's timing events off (each event it records inside the
-        # call adds a few microseconds of stream time), then the kernel time with them on
+        # call time of the plain entry point (each event the timed one records inside the
+        # call adds a few microseconds of stream time), then the kernel time from as many
+        # calls of the timed entry point
         call_ms, kern_ms = [], []
         for _ in range(reps):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -743,13 +737,11 @@ def per_config(F, W, hip, torch, verbose=False):
             b.record()
             torch.cuda.synchronize()
             call_ms.append(a.elapsed_time(b))
-        ev = [hip.event() for _ in range(4)]
-        F.festina_set_timing_events(*ev)
+        ev = (hip.event(), hip.event())
         for _ in range(reps):
-            dev.run()
+            dev.run(events=ev)
             torch.cuda.synchronize()
-            kern_ms.append(hip.elapsed_ms(ev[idx[0]], ev[idx[1]]))
-        F.festina_set_timing_events()
+            kern_ms.append(hip.elapsed_ms(*ev))
         for e in ev:
             hip.destroy(e)
         cm, km = float(np.median(call_ms)), float(np.median(kern_ms))

@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define FESTINA_ABI_VERSION 2
+#define FESTINA_ABI_VERSION 3
 #define FESTINA_N_ROWS 32        /* rows of every profile table */
 #define FESTINA_MAX_CELLS 256    /* n_sm * n_freq limit of the placement kernels */
 #define FESTINA_MAX_FREQ_MIG 32  /* n_freq limit of the migration kernels (32-bit level masks) */
@@ -155,6 +155,19 @@ festina_status festina_score_placements(const festina_lut *lut, const festina_gp
                                         const festina_requests *req, festina_placements *out,
                                         void *workspace, size_t workspace_bytes, void *stream);
 
+/* For callers that time the scoring kernel alone (a measurement, not part of the search):
+ * festina_score_placements, with `score_begin` recorded on `stream` immediately before
+ * the scoring kernel and `score_end` immediately after it, so that hipEventElapsedTime of
+ * the two is that kernel's duration.  Each is a hipEvent_t passed as void*, created by the
+ * caller on the current device; NULL leaves that point unrecorded (both NULL: exactly
+ * festina_score_placements).  Same arguments, checks, outputs and errors otherwise; a
+ * failing record returns FESTINA_ERR_DEVICE.  Each recorded event costs a few microseconds
+ * of stream time. */
+festina_status festina_score_placements_timed(const festina_lut *lut, const festina_gpus *gpus,
+                                              const festina_requests *req, festina_placements *out,
+                                              void *workspace, size_t workspace_bytes, void *stream,
+                                              void *score_begin, void *score_end);
+
 /* For callers that cannot allocate device memory -- code under HIP graph capture,
  * tight serving loops, harnesses that forbid hipMalloc: festina_score_placements with its
  * workspace taken from a fixed device array of FESTINA_NOALLOC_WORKSPACE_BYTES that the
@@ -218,6 +231,14 @@ size_t festina_migrations_workspace_bytes(const festina_lut *lut, const festina_
 festina_status festina_score_migrations(const festina_lut *lut, const festina_fleet *fleet,
                                         festina_migrations *out, void *workspace,
                                         size_t workspace_bytes, void *stream);
+
+/* festina_score_migrations with `pairs_begin` / `pairs_end` recorded around its
+ * pair-scoring kernel (k_migrate), as festina_score_placements_timed does around the
+ * placement scoring kernel. */
+festina_status festina_score_migrations_timed(const festina_lut *lut, const festina_fleet *fleet,
+                                              festina_migrations *out, void *workspace,
+                                              size_t workspace_bytes, void *stream, void *pairs_begin,
+                                              void *pairs_end);
 
 /* Task batches of the local schedulers (Sec. 3.4): batch b holds n_tasks[b] tasks in
  * slots 0..n_tasks[b]-1 of its max_tasks slots.  A task is a prefill unit (phase
@@ -445,16 +466,6 @@ typedef struct festina_moves {
 festina_status festina_request_moves(const festina_lut *lut, const festina_transfer *transfer,
                                      const festina_plan *plan, const festina_inflight *req,
                                      festina_moves *out, void *stream);
-
-/* Measurement hook, not part of the search.  While set, festina_score_placements
- * records `score_begin` on its stream immediately before its scoring kernel and
- * `score_end` immediately after it, and festina_score_migrations does the same with
- * `pairs_begin` / `pairs_end` around its pair-scoring kernel, so that a caller can time
- * those kernels alone with hipEventElapsedTime.  Each argument is a hipEvent_t passed
- * as void*, created by the caller on the device of the following calls; NULL leaves
- * that point unrecorded.  The setting belongs to the calling host thread and stays in
- * force until changed. */
-void festina_set_timing_events(void *score_begin, void *score_end, void *pairs_begin, void *pairs_end);
 
 /* Static, NUL-terminated description of a status code. */
 const char *festina_status_string(festina_status status);

@@ -2112,11 +2112,9 @@ bool place_layout(const festina_lut *L, const festina_gpus *G, const festina_req
   return true;
 }
 
-// events recorded around the scoring kernels (measurement hook; per host thread)
-thread_local hipEvent_t t_events[4] = {nullptr, nullptr, nullptr, nullptr};
-
-hipError_t mark(int which, hipStream_t st) {
-  return t_events[which] ? hipEventRecord(t_events[which], st) : hipSuccess;
+// A caller's event recorded on the stream (the timed entry points); nullptr: nothing.
+hipError_t mark(void *ev, hipStream_t st) {
+  return ev ? hipEventRecord(static_cast<hipEvent_t>(ev), st) : hipSuccess;
 }
 
 template <int CPL>
@@ -2131,13 +2129,6 @@ hipError_t launch_score(const PlaceArgs &a, int blocks, int wpb, size_t lds, hip
 extern "C" {
 
 int32_t festina_abi_version(void) { return FESTINA_ABI_VERSION; }
-
-void festina_set_timing_events(void *score_begin, void *score_end, void *pairs_begin, void *pairs_end) {
-  t_events[0] = static_cast<hipEvent_t>(score_begin);
-  t_events[1] = static_cast<hipEvent_t>(score_end);
-  t_events[2] = static_cast<hipEvent_t>(pairs_begin);
-  t_events[3] = static_cast<hipEvent_t>(pairs_end);
-}
 
 const char *festina_status_string(festina_status s) {
   switch (s) {
@@ -2179,9 +2170,11 @@ festina_status place_args(const festina_lut *L, const festina_gpus *G, const fes
   return FESTINA_OK;
 }
 
-// The launches of one placement call on a checked workspace of lay.total bytes.
+// The launches of one placement call on a checked workspace of lay.total bytes; ev_begin /
+// ev_end (the timed entry point, else nullptr) are recorded around the scoring kernel.
 festina_status place_launch(const festina_lut *L, const festina_gpus *G, const festina_requests *Q,
-                            const festina_placements *out, const PlaceLayout &lay, char *ws, void *stream) {
+                            const festina_placements *out, const PlaceLayout &lay, char *ws, void *stream,
+                            void *ev_begin = nullptr, void *ev_end = nullptr) {
   const long long C = (long long)L->n_sm * L->n_freq;
   PlaceArgs a;
   a.M = L->n_models;
@@ -2261,7 +2254,7 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
     const size_t f = r16_lds_bytes(wpb);
     lds = f > lds ? f : lds;
   }
-  hipError_t e = mark(0, st);
+  hipError_t e = mark(ev_begin, st);
   if (e != hipSuccess) return FESTINA_ERR_DEVICE;
   if (lay.fast) {
     const int blocks = (lay.max_tiles + lay.gpad - 1) / lay.gpad;
@@ -2279,7 +2272,7 @@ festina_status place_launch(const festina_lut *L, const festina_gpus *G, const f
     e = launch_score<2>(a, lay.max_tiles, wpb, lds, st);
   else
     e = launch_score<4>(a, lay.max_tiles, wpb, lds, st);
-  if (e == hipSuccess) e = mark(1, st);
+  if (e == hipSuccess) e = mark(ev_end, st);
   return e == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
 }
 
@@ -2315,15 +2308,22 @@ char *scratch_for_current_device() {
 
 extern "C" {
 
-festina_status festina_score_placements(const festina_lut *L, const festina_gpus *G,
-                                        const festina_requests *Q, festina_placements *out,
-                                        void *workspace, size_t workspace_bytes, void *stream) {
+festina_status festina_score_placements_timed(const festina_lut *L, const festina_gpus *G,
+                                              const festina_requests *Q, festina_placements *out,
+                                              void *workspace, size_t workspace_bytes, void *stream,
+                                              void *score_begin, void *score_end) {
   PlaceLayout lay;
   const festina_status s = place_args(L, G, Q, out, &lay);
   if (s != FESTINA_OK || Q->n_requests == 0) return s;
   if (!workspace || workspace_bytes < lay.total || (((uintptr_t)workspace) & 255) != 0)
     return FESTINA_ERR_INVALID;
-  return place_launch(L, G, Q, out, lay, static_cast<char *>(workspace), stream);
+  return place_launch(L, G, Q, out, lay, static_cast<char *>(workspace), stream, score_begin, score_end);
+}
+
+festina_status festina_score_placements(const festina_lut *L, const festina_gpus *G,
+                                        const festina_requests *Q, festina_placements *out,
+                                        void *workspace, size_t workspace_bytes, void *stream) {
+  return festina_score_placements_timed(L, G, Q, out, workspace, workspace_bytes, stream, nullptr, nullptr);
 }
 
 festina_status festina_score_placements_noalloc(const festina_lut *L, const festina_gpus *G,
@@ -2351,9 +2351,10 @@ size_t festina_migrations_workspace_bytes(const festina_lut *lut, const festina_
   return align256((size_t)32 * fleet->n_gpus);      // one 32-byte destination record per GPU
 }
 
-festina_status festina_score_migrations(const festina_lut *L, const festina_fleet *F,
-                                        festina_migrations *out, void *workspace,
-                                        size_t workspace_bytes, void *stream) {
+festina_status festina_score_migrations_timed(const festina_lut *L, const festina_fleet *F,
+                                              festina_migrations *out, void *workspace,
+                                              size_t workspace_bytes, void *stream, void *pairs_begin,
+                                              void *pairs_end) {
   if (!mig_shapes_ok(L, F) || !out) return FESTINA_ERR_INVALID;
   if (L->n_freq > FESTINA_MAX_FREQ_MIG) return FESTINA_ERR_UNSUPPORTED;
   if (!L->freq_level || !L->pf || !L->dc) return FESTINA_ERR_INVALID;
@@ -2396,10 +2397,16 @@ festina_status festina_score_migrations(const festina_lut *L, const festina_flee
   hipStream_t st = static_cast<hipStream_t>(stream);
   k_fleet<<<(a.G + 3) / 4, 256, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  if (mark(2, st) != hipSuccess) return FESTINA_ERR_DEVICE;
+  if (mark(pairs_begin, st) != hipSuccess) return FESTINA_ERR_DEVICE;
   k_migrate<<<(a.G + kMigSrcPerBlock - 1) / kMigSrcPerBlock, 256, 0, st>>>(a);
-  if (hipGetLastError() != hipSuccess || mark(3, st) != hipSuccess) return FESTINA_ERR_DEVICE;
+  if (hipGetLastError() != hipSuccess || mark(pairs_end, st) != hipSuccess) return FESTINA_ERR_DEVICE;
   return FESTINA_OK;
+}
+
+festina_status festina_score_migrations(const festina_lut *L, const festina_fleet *F,
+                                        festina_migrations *out, void *workspace,
+                                        size_t workspace_bytes, void *stream) {
+  return festina_score_migrations_timed(L, F, out, workspace, workspace_bytes, stream, nullptr, nullptr);
 }
 
 }  // extern "C"

@@ -133,7 +133,8 @@ EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_
             "festina_score_migrations",
             "festina_sweep_batches", "festina_preferred_configs", "festina_ewr_workspace_bytes",
             "festina_fleet_ewr", "festina_dispatch_workspace_bytes", "festina_dispatch_requests",
-            "festina_transfer_costs", "festina_request_moves", "festina_set_timing_events")
+            "festina_transfer_costs", "festina_request_moves", "festina_score_placements_timed",
+            "festina_score_migrations_timed")
 
 _lib = None
 
@@ -198,16 +199,13 @@ def lib():
         L.festina_request_moves.argtypes = [P(festina_lut), P(festina_transfer), P(festina_plan),
                                             P(festina_inflight), P(festina_moves), C.c_void_p]
         L.festina_request_moves.restype = C.c_int
-        L.festina_set_timing_events.argtypes = [C.c_void_p] * 4
-        L.festina_set_timing_events.restype = None
+        L.festina_score_placements_timed.argtypes = L.festina_score_placements.argtypes + [C.c_void_p, C.c_void_p]
+        L.festina_score_placements_timed.restype = C.c_int
+        L.festina_score_migrations_timed.argtypes = L.festina_score_migrations.argtypes + [C.c_void_p, C.c_void_p]
+        L.festina_score_migrations_timed.restype = C.c_int
         _lib = L
     return _lib
 
-
-def festina_set_timing_events(score_begin=None, score_end=None, pairs_begin=None, pairs_end=None) -> None:
-    """Measurement hook: raw hipEvent_t handles (ints) recorded around the scoring kernels."""
-    lib().festina_set_timing_events(*(C.c_void_p(e) if e else None
-                                      for e in (score_begin, score_end, pairs_begin, pairs_end)))
 
 
 def festina_abi_version() -> int:
@@ -274,8 +272,11 @@ class DevicePlacement:
         self.ws_bytes = festina_placements_workspace_bytes(self.lut, self.gpus, self.req)
         self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
 
-    def run(self, stream=None):
-        festina_score_placements(self.lut, self.gpus, self.req, self.out, self.workspace, self.ws_bytes, stream)
+    def run(self, stream=None, events=None):
+        """One search; `events` = (begin, end) raw hipEvent_t handles recorded around the
+        scoring kernel (the timed entry point), else None."""
+        festina_score_placements(self.lut, self.gpus, self.req, self.out, self.workspace, self.ws_bytes, stream,
+                                 events)
 
     def run_noalloc(self, stream=None):
         """The same search through the allocation-free entry point (the library's scratch)."""
@@ -318,8 +319,10 @@ class DeviceMigration:
         self.ws_bytes = festina_migrations_workspace_bytes(self.lut, self.fleet)
         self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
 
-    def run(self, stream=None):
-        festina_score_migrations(self.lut, self.fleet, self.out, self.workspace, self.ws_bytes, stream)
+    def run(self, stream=None, events=None):
+        """One search; `events` = (begin, end) raw hipEvent_t handles recorded around the
+        pair-scoring kernel (the timed entry point), else None."""
+        festina_score_migrations(self.lut, self.fleet, self.out, self.workspace, self.ws_bytes, stream, events)
 
     def results(self):
         return self.best_dst.cpu().numpy(), self.saving.cpu().numpy(), self.level.cpu().numpy()
@@ -535,10 +538,21 @@ def festina_placements_workspace_bytes(lut, gpus, req) -> int:
     return int(lib().festina_placements_workspace_bytes(C.byref(lut), C.byref(gpus), C.byref(req)))
 
 
-def festina_score_placements(lut, gpus, req, out, workspace, workspace_bytes, stream=None) -> None:
+def _events(events):
+    b, e = events
+    return (C.c_void_p(b) if b else None), (C.c_void_p(e) if e else None)
+
+
+def festina_score_placements(lut, gpus, req, out, workspace, workspace_bytes, stream=None, events=None) -> None:
+    """festina_score_placements, or festina_score_placements_timed when `events` = (begin, end)
+    raw hipEvent_t handles."""
     ws = None if workspace is None else C.c_void_p(workspace.data_ptr())
-    st = lib().festina_score_placements(C.byref(lut), C.byref(gpus), C.byref(req), C.byref(out), ws,
-                                        int(workspace_bytes), _stream_handle(stream))
+    args = (C.byref(lut), C.byref(gpus), C.byref(req), C.byref(out), ws, int(workspace_bytes),
+            _stream_handle(stream))
+    if events is None:
+        st = lib().festina_score_placements(*args)
+    else:
+        st = lib().festina_score_placements_timed(*args, *_events(events))
     if st != FESTINA_OK:
         raise FestinaError(st, "festina_score_placements")
 
@@ -554,10 +568,15 @@ def festina_migrations_workspace_bytes(lut, fleet) -> int:
     return int(lib().festina_migrations_workspace_bytes(C.byref(lut), C.byref(fleet)))
 
 
-def festina_score_migrations(lut, fleet, out, workspace, workspace_bytes, stream=None) -> None:
+def festina_score_migrations(lut, fleet, out, workspace, workspace_bytes, stream=None, events=None) -> None:
+    """festina_score_migrations, or festina_score_migrations_timed when `events` = (begin, end)
+    raw hipEvent_t handles."""
     ws = None if workspace is None else C.c_void_p(workspace.data_ptr())
-    st = lib().festina_score_migrations(C.byref(lut), C.byref(fleet), C.byref(out), ws,
-                                        int(workspace_bytes), _stream_handle(stream))
+    args = (C.byref(lut), C.byref(fleet), C.byref(out), ws, int(workspace_bytes), _stream_handle(stream))
+    if events is None:
+        st = lib().festina_score_migrations(*args)
+    else:
+        st = lib().festina_score_migrations_timed(*args, *_events(events))
     if st != FESTINA_OK:
         raise FestinaError(st, "festina_score_migrations")
 

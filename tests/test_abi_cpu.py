@@ -47,7 +47,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert F.festina_abi_version() == 2
+    assert F.festina_abi_version() == 3
     for s in range(5):
         assert F.festina_status_string(s)
     assert "scratch" in F.festina_status_string(F.FESTINA_ERR_TOO_LARGE)

@@ -1,7 +1,7 @@
-"""The measurement hook festina_set_timing_events: while set, the placement call records
-its events around the scoring kernel and the consolidation call around its pair-scoring
-kernel, the outputs stay bit-identical to calls without it, the bracketed time is positive
-and no longer than the whole call, and once cleared no call records the events again."""
+"""The timed entry points festina_score_placements_timed / festina_score_migrations_timed:
+they record the caller's events around the scoring kernel, their outputs are bit-identical
+to the plain calls, the bracketed time is positive and no longer than the whole call, and
+a later plain call records nothing (the library keeps no timing state)."""
 import os
 import sys
 
@@ -17,20 +17,17 @@ pytestmark = [pytest.mark.gpu,
 sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
 
-def _check(hip, F, run, results, which, label):
-    print(f"[gpu] timing hook: {label}", flush=True)
+def _check(hip, run, results, label):
+    print(f"[gpu] timed call: {label}", flush=True)
     run()
     torch.cuda.synchronize()
     ref = [np.copy(x) for x in results()]
     st = torch.cuda.current_stream().cuda_stream
-    ev = [hip.event() for _ in range(4)]
+    ev = [hip.event(), hip.event()]
     whole = [hip.event(), hip.event()]
     try:
-        args = [None] * 4
-        args[2 * which], args[2 * which + 1] = ev[0], ev[1]
-        F.festina_set_timing_events(*args)
         hip.record(whole[0], st)
-        run()
+        run(events=(ev[0], ev[1]))
         hip.record(whole[1], st)
         torch.cuda.synchronize()
         kernel_ms = hip.elapsed_ms(ev[0], ev[1])
@@ -38,21 +35,19 @@ def _check(hip, F, run, results, which, label):
         assert 0.0 < kernel_ms <= call_ms, (kernel_ms, call_ms)
         for a, b in zip(results(), ref):
             assert np.array_equal(np.asarray(a).view(np.uint8), b.view(np.uint8))
-        F.festina_set_timing_events()
-        run()                                   # cleared: the events keep their timestamps
+        run()                                   # plain call: the events keep their timestamps
         torch.cuda.synchronize()
         assert hip.elapsed_ms(ev[0], ev[1]) == kernel_ms
     finally:
-        F.festina_set_timing_events()
         for e in ev + whole:
             hip.destroy(e)
 
 
-def test_timing_hook_around_the_scoring_kernels():
+def test_timed_calls_around_the_scoring_kernels():
     import bench
     from paper_2606_30391_amd import festina as F
     hip = bench.Hip()
     dp = F.DevicePlacement(W.make_placement(3), "cuda")
-    _check(hip, F, dp.run, dp.results, 0, "placement config 3")
+    _check(hip, dp.run, dp.results, "placement config 3")
     dm = F.DeviceMigration(W.make_fleet(), "cuda")
-    _check(hip, F, dm.run, dm.results, 1, "consolidation config 5")
+    _check(hip, dm.run, dm.results, "consolidation config 5")
