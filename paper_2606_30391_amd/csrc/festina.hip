@@ -301,13 +301,23 @@ __device__ __forceinline__ int prompt_row(int pt) {
 // of those entries, so none can pass).  The stored key carries kKeyTiny when the 8 x 16
 // kernel must not divide the request's prompt row by Lout (see make_req_rec).
 constexpr int kKeyTiny = 1 << 30;                 // bucket numbers stay below 2^30
-__device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const ReqKeyFields &f) {
+// The table minima a request's test reads: loaded for every request (at model 0 / row 0 for
+// an invalid one), so that the loads of several requests issue together, before any test.
+struct ReqMins {
+  float dmin, pmin, ptiny;
+};
+__device__ __forceinline__ ReqMins load_req_mins(const PlaceArgs &a, const ReqKeyFields &f) {
+  const bool mv = f.m >= 0 && f.m < a.M;
+  const int m = mv ? f.m : 0, row = f.pt > 0 ? prompt_row(f.pt) : 0;
+  return ReqMins{a.dc_min[m], a.pf_rowmin[m * kRows + row], a.pf_rowtiny[m * kRows + row]};
+}
+__device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const ReqKeyFields &f, const ReqMins &mn) {
   bool ok = f.m >= 0 && f.m < a.M && f.w >= 0 && f.w < a.W && f.pt >= 0 && f.pr >= 0;
   bool tiny = false;
   if (ok) {
     const int row = prompt_row(f.pt);
-    ok = a.dc_min[f.m] < f.sb && (row < 0 || a.pf_rowmin[f.m * kRows + row] < f.st);
-    tiny = a.fast && row >= 0 && a.pf_rowtiny[f.m * kRows + row] < kTinyLatency;
+    ok = mn.dmin < f.sb && (row < 0 || mn.pmin < f.st);
+    tiny = a.fast && row >= 0 && mn.ptiny < kTinyLatency;
   }
   if (!ok) {
     a.key[r] = -1;
@@ -408,34 +418,63 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
     // The LDS histogram is indexed wave-major, h = w * 2M + (2 m + prompt-less): requests that
     // arrive together share w and spread over consecutive words (banks), where the bucket
     // numbers, W apart, would all fall on one bank.
+    // the table minima of all U requests in one round trip, then the tests
+    ReqMins mn[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) mn[u] = load_req_mins(a, f[u]);
     int key[U], pos[U], hk[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = b * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x;
-      key[u] = r < a.R ? prep_request(a, r, f[u]) : -1;
+      key[u] = r < a.R ? prep_request(a, r, f[u], mn[u]) : -1;
       hk[u] = f[u].w * (2 * a.M) + ((f[u].m << 1) | (f[u].pt == 0 ? 1 : 0));
-      pos[u] = key[u] >= 0 ? atomicAdd(local ? &hist[hk[u]] : &a.cnt[key[u]], 1) : 0;
+    }
+    // the LDS histogram and the global counters in separate loops: an atomic through a
+    // pointer that may be either would be a flat atomic, waited for like a global one
+    if (local) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) pos[u] = key[u] >= 0 ? atomicAdd(&hist[hk[u]], 1) : 0;
+    } else {
+#pragma unroll
+      for (int u = 0; u < U; ++u) pos[u] = key[u] >= 0 ? atomicAdd(&a.cnt[key[u]], 1) : 0;
     }
     if (local) {
       __syncthreads();
       // slot h = w * 2M + g holds the bucket of wave w = sl * gw + wr and 2 m + prompt-less =
-      // g; (sl, wr, g) advance with h, no division per slot
+      // g; (sl, wr, g) advance with h by constant steps (two divisions per thread, none per
+      // slot), and kFlush slots per round have their atomics issued together (one round
+      // trip to the counters per round, not per slot)
+      constexpr int kFlush = 4;
       const int NG = 2 * a.M;
       const int dw = kPrepBlock / NG, dg = kPrepBlock - dw * NG;
+      const int dsl = dw / a.gw, dwr = dw - dsl * a.gw;
       const int w0 = (int)threadIdx.x / NG;
       int g = (int)threadIdx.x - w0 * NG, sl = w0 / a.gw, wr = w0 - sl * a.gw;
-      for (int h = threadIdx.x; h < a.NB; h += kPrepBlock) {
-        if (hist[h]) hist[h] = atomicAdd(&a.cnt[(sl * NG + g) * a.gw + wr], hist[h]);   // this block's base
-        wr += dw;
-        g += dg;
-        if (g >= NG) {
-          g -= NG;
-          ++wr;
+      for (int h0 = threadIdx.x; h0 < a.NB; h0 += kFlush * kPrepBlock) {
+        int cv[kFlush], bk[kFlush];
+#pragma unroll
+        for (int u = 0; u < kFlush; ++u) {
+          const int h = h0 + u * kPrepBlock;
+          cv[u] = h < a.NB ? hist[h] : 0;
+          bk[u] = (sl * NG + g) * a.gw + wr;
+          g += dg;                        // next slot: w += dw (sl += dsl, wr += dwr), g += dg
+          sl += dsl;
+          wr += dwr;
+          if (g >= NG) {
+            g -= NG;
+            ++wr;
+          }
+          if (wr >= a.gw) {               // wr < 2 gw here: dwr < gw, plus at most one carry
+            wr -= a.gw;
+            ++sl;
+          }
         }
-        while (wr >= a.gw) {
-          wr -= a.gw;
-          ++sl;
-        }
+        int base[kFlush];
+#pragma unroll
+        for (int u = 0; u < kFlush; ++u) base[u] = cv[u] ? atomicAdd(&a.cnt[bk[u]], cv[u]) : 0;
+#pragma unroll
+        for (int u = 0; u < kFlush; ++u)
+          if (cv[u]) hist[h0 + u * kPrepBlock] = base[u];   // this block's base in the bucket
       }
       __syncthreads();
 #pragma unroll
@@ -688,10 +727,10 @@ __device__ __forceinline__ ReqRec make_req_rec(const PlaceArgs &a, int r) {
 // into the LDS array `start`.  Thread t holds buckets [t*per, t*per + per), per a multiple
 // of 4 (at most 32), loaded by load_scan_counts as 8 int4 loads that are all in flight
 // before the first use; the counter array is padded to a multiple of 4 with zeros.  Every
-// block scans all buckets (a few KB from L2); the global starts of thread t's buckets are
-// written by block t mod grid, the tile table by every thread of the grid (one entry each,
-// its bucket found by a binary search over the buckets' first tiles in LDS), and block 0
-// writes the totals.
+// block scans all buckets (a few KB from L2); the global bucket starts are written by the
+// grid from LDS after the block's last barrier (one bucket per thread), the tile table by
+// every thread of the grid (one entry each, its bucket found by a binary search over the
+// buckets' first tiles in LDS), and block 0 writes the totals.
 constexpr int kScanChunks = kHistMax / kPrepBlock / 4;   // int4 chunks of counts per thread
 
 // Thread t's bucket range [lo, hi) of the block scan: per buckets, a multiple of 4.
@@ -752,8 +791,6 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
     tot_c += s_c[i];
     tot_t += s_t[i];
   }
-  // thread t's bucket starts are published by block t mod grid (every t < 256 names one block)
-  const bool writer = (int)threadIdx.x % (int)gridDim.x == (int)blockIdx.x;
   const bool pad = a.gpad > 1;
   int *ts = start + a.NB;                            // [NB + 1] unpadded first tile of each bucket
   int *gP = ts + a.NB + 1, *pp = gP + a.ng + 1;      // [ng + 1] each, with group padding
@@ -769,7 +806,6 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
           const int n = v[q][e];
           start[i] = pc;
           ts[i] = pt;
-          if (writer) a.bstart[i] = pc;
           if (pad && wi == 0) gP[g] = pt;
           pc += n;
           pt += (n + a.tile - 1) >> tsh;
@@ -790,6 +826,10 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
   } else {
     __syncthreads();
   }
+  // the global bucket starts, copied from LDS after the last barrier (a global store before
+  // a barrier holds the barrier until the store is acknowledged); block b writes buckets
+  // b * 256 + t, (b + grid) * 256 + t, ...
+  for (int i = blockIdx.x * kPrepBlock + threadIdx.x; i < a.NB; i += gridDim.x * kPrepBlock) a.bstart[i] = start[i];
   // Padded tile k: its group g (pp[g] <= k < pp[g + 1]; an empty group's range is empty), its
   // unpadded index u within the group's tiles, and the bucket l of the group with ts[l] <= u <
   // ts[l + 1]; u past the group's tiles is one of its empty tiles.  Without padding the
