@@ -207,13 +207,17 @@ __device__ __forceinline__ BucketId bucket_id(const PlaceArgs &a, int bucket) {
 
 // ------------------------------------------------------------------ prologue kernels
 // Inclusive prefix sum over a wavefront.
+// Inclusive prefix sum over the wavefront's 64 lanes with DPP moves (no LDS permutes):
+// shifts by 1, 2, 4 and 8 lanes within each row of 16 (a lane shifted in from outside its
+// row adds 0), then row_bcast:15 adds row 0's total to row 1 and row 2's to row 3, and
+// row_bcast:31 adds the total of rows 0-1 to rows 2 and 3.
 __device__ __forceinline__ int wave_scan(int v) {
-  const int lane = threadIdx.x & (kWave - 1);
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int o = __shfl_up(v, off, kWave);
-    if (lane >= off) v += o;
-  }
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15, rows 1 and 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31, rows 2 and 3
   return v;
 }
 
