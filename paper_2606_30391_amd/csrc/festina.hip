@@ -1425,9 +1425,14 @@ __device__ __forceinline__ void r16_fold(float (&acc)[kR]) {
 
 // Pass 1 of one chunk over range JB..JB+3 (classes in ascending m, so the groups come in the
 // order n = 1, 2, then more; classes with no level in the range come first and are skipped).
+// The packed groups need the accumulators of the rows they borrow at +inf, which holds in
+// the first chunk only: a fold takes the minimum over rows into the level's own row and
+// resets the others, so in a later chunk it would move the earlier chunks' minima of the
+// other levels onto the wrong cells.  Later chunks therefore score every class one GPU per
+// step (a level above a class's caps gets NaN power and never wins).
 template <int JB, int S>
 __device__ __forceinline__ void r16_range(const char *L, const char *Rw, int ncls, int sp, const float (&xA)[kR],
-                                          const float (&xB)[kR], float p0, float (&acc)[kR]) {
+                                          const float (&xB)[kR], float p0, float (&acc)[kR], bool first_chunk) {
   const int *cls = reinterpret_cast<const int *>(L + kL_cls);
   int k = 0;
   if (JB > 0)
@@ -1436,11 +1441,13 @@ __device__ __forceinline__ void r16_range(const char *L, const char *Rw, int ncl
       if (max((packed >> 3) & 7, packed & 7) >= JB) break;
       ++k;
     }
-  const int k1 = r16_group<JB, 4, S>(L, Rw, k, ncls, sp, xA, xB, p0, acc);
-  if (k1 > k) r16_fold<4>(acc);
-  const int k2 = r16_group<JB, 2, S>(L, Rw, k1, ncls, sp, xA, xB, p0, acc);
-  if (k2 > k1) r16_fold<2>(acc);
-  r16_group<JB, 1, S>(L, Rw, k2, ncls, sp, xA, xB, p0, acc);
+  if (first_chunk) {
+    const int k1 = r16_group<JB, 4, S>(L, Rw, k, ncls, sp, xA, xB, p0, acc);
+    if (k1 > k) r16_fold<4>(acc);
+    k = r16_group<JB, 2, S>(L, Rw, k1, ncls, sp, xA, xB, p0, acc);
+    if (k > k1) r16_fold<2>(acc);
+  }
+  r16_group<JB, 1, S>(L, Rw, k, ncls, sp, xA, xB, p0, acc);
 }
 
 // One value per request for the 16 requests at once: the reduction (OP) over the wavefront's
@@ -1767,8 +1774,8 @@ __global__ void __launch_bounds__(kWpb16 * 64) k_score_r16(PlaceArgs a) {
     __builtin_amdgcn_s_setprio(0);
     if (nq > 0) {
       const int ncls = uniform(reinterpret_cast<const int *>(L + kL_cls)[kClasses]);
-      r16_range<0, S>(L, Rw, ncls, sp, xA, xB, p0, accA);
-      r16_range<4, S>(L, Rw, ncls, sp, xA, xB, p0, accB);
+      r16_range<0, S>(L, Rw, ncls, sp, xA, xB, p0, accA, ch == 0);
+      r16_range<4, S>(L, Rw, ncls, sp, xA, xB, p0, accB, ch == 0);
     }
   }
   if (S == 1 && nq == 0) return;          // (with S > 1 every wavefront meets the barriers below)

@@ -311,14 +311,43 @@ def test_fast_kernel_mixed_slo_groups():
     parity_place(inp, label="cfg3 mixed TBT SLOs")
 
 
+def one_slo_pair_per_model(rng, inp):
+    """One (TTFT, TBT) SLO pair per model and Lout >= 1: the tiles take the 8x16 kernel's
+    own scoring (mixed TBT SLOs in a tile send it to the generic code)."""
+    q = inp["requests"]
+    M, R = inp["lut"]["n_models"], q["n_requests"]
+    q["slo_ttft_ms"] = rng.uniform(20.0, 70.0, M).astype(np.float32)[q["model"]]
+    q["slo_tbt_ms"] = rng.uniform(10.0, 45.0, M).astype(np.float32)[q["model"]]
+    q["pred_out_tokens"] = rng.integers(1, 300, R).astype(np.int32)
+
+
 def test_fast_kernel_more_hosts_than_one_lds_chunk():
     """8x16 tables with > 256 hosting GPUs per model: host records are staged in several
     chunks and pass 2 reads them from global memory."""
     rng = np.random.default_rng(606)
     inp = W.make_tiny_placement(rng, R=203, G=700, M=2, NS=8, NF=16, W=2, caps=True)
+    one_slo_pair_per_model(rng, inp)
     hosts = [int(((inp["gpus"]["resident"][:, 0] >> m) & 1).sum()) for m in range(2)]
     assert max(hosts) > 256
     parity_place(inp, label=f"8x16 with {hosts} hosts per model")
+
+
+@pytest.mark.parametrize("split", [0, 1])
+def test_fast_kernel_packed_classes_after_the_first_chunk(split):
+    """8x16 tables, > 256 hosting GPUs per model, and GPUs capped at SM level 0 (or 1) only
+    after the first LDS chunk of hosts: pass 1 scores their classes without the packed
+    groups, whose folds would move the earlier chunks' minima of the other SM levels onto
+    the wrong cells (pass 2 then finds no host and reports the request infeasible)."""
+    rng = np.random.default_rng(607 + split)
+    inp = W.make_tiny_placement(rng, R=220, G=700, M=1, NS=8, NF=16, W=1, caps=True)
+    g = inp["gpus"]
+    g["resident"][:, 0] |= 1                    # every GPU hosts the model
+    g["cap_pf"][:] = 3                         # the first 300 hosts score SM levels 0-3 only,
+    g["cap_dc"][:] = 3                         # so their minima lie in the first range of levels
+    g["cap_pf"][300:] = split
+    g["cap_dc"][300:] = split
+    one_slo_pair_per_model(rng, inp)
+    parity_place(inp, label=f"8x16, 700 hosts, caps 3 then {split} after host 300")
 
 
 @pytest.mark.parametrize("seed,variant", [(0, "plain"), (1, "plain"), (2, "ties"), (3, "ties"),
