@@ -43,12 +43,12 @@ constexpr int kWave = 64;
 constexpr int kQ = 4;            // requests scored together by one wavefront
 constexpr int kNS8 = 8;
 constexpr int kClasses = kNS8 * kNS8;            // (cap_pf, cap_dc) pairs of 8 SM levels
-constexpr int kHcap = 256;                       // host records staged in LDS per chunk
+constexpr int kHcap = 128;                       // host records staged in LDS per chunk
 // A prompt latency at least this large keeps a normal value when divided by any Lout up to
 // 2^40 (2^-86 * 2^-40 = 2^-126, the least normal float).
 constexpr float kTinyLatency = 0x1p-86f;
 constexpr int kPrepBlock = 256;
-static_assert(kHcap == kPrepBlock, "a chunk's class sort takes one host per thread");
+static_assert(kHcap <= kPrepBlock, "a chunk's class sort takes one host per thread");
 constexpr float kInf = __builtin_huge_valf();
 // Value of a masked (SLO-missing) latency: a quiet NaN stays NaN through every multiply and
 // FMA whatever the sign of the power terms, and NaN < x is false, so it never wins.
@@ -351,10 +351,14 @@ __device__ __forceinline__ int class_caps(int t) {
 }
 
 // SM-cap class of GPU g for the 8 x 16 chunk sort: caps outside [0, 7] (a GPU without
-// candidates) are clamped; absent cap arrays mean 7.
+// candidates) are clamped; absent cap arrays mean 7.  The loads are unconditional (an
+// absent array reads kNoCap), so that a caller's loads of several GPUs issue together.
+__device__ const int8_t kNoCap = 0;                // read in place of absent cap arrays
 __device__ __forceinline__ int host_class(const PlaceArgs &a, int g) {
-  const int cp = a.cap_pf ? min(max((int)a.cap_pf[g], 0), kNS8 - 1) : kNS8 - 1;
-  const int cd = a.cap_dc ? min(max((int)a.cap_dc[g], 0), kNS8 - 1) : kNS8 - 1;
+  const int8_t cpv = *(a.cap_pf ? a.cap_pf + g : &kNoCap);
+  const int8_t cdv = *(a.cap_dc ? a.cap_dc + g : &kNoCap);
+  const int cp = a.cap_pf ? min(max((int)cpv, 0), kNS8 - 1) : kNS8 - 1;
+  const int cd = a.cap_dc ? min(max((int)cdv, 0), kNS8 - 1) : kNS8 - 1;
   return class_id(cp, cd);
 }
 
@@ -392,7 +396,46 @@ __device__ void sort_host_chunks(const PlaceArgs &a, int m, int hcnt, int *cnt, 
   }
 }
 
-__device__ const int8_t kNoCap = 0;                // read in place of absent cap arrays
+// The LDS histogram's flush: each non-empty slot's count is added to its bucket's global
+// counter, and the returned old value (this block's base within the bucket) replaces it.
+// Slot h = w * 2M + g holds the bucket of wave w = sl * gw + wr and 2 m + prompt-less = g;
+// (sl, wr, g) advance with h by constant steps (two divisions per thread, none per slot),
+// and the KF slots of a round have their atomics issued together (one round trip to the
+// counters per round, not per slot).  Called by the whole block between two barriers.
+template <int KF>
+__device__ __forceinline__ void flush_hist(const PlaceArgs &a, int *hist) {
+  const int NG = 2 * a.M;
+  const int dw = kPrepBlock / NG, dg = kPrepBlock - dw * NG;
+  const int dsl = dw / a.gw, dwr = dw - dsl * a.gw;
+  const int w0 = (int)threadIdx.x / NG;
+  int g = (int)threadIdx.x - w0 * NG, sl = w0 / a.gw, wr = w0 - sl * a.gw;
+  for (int h0 = threadIdx.x; h0 < a.NB; h0 += KF * kPrepBlock) {
+    int cv[KF], bk[KF];
+#pragma unroll
+    for (int u = 0; u < KF; ++u) {
+      const int h = h0 + u * kPrepBlock;
+      cv[u] = h < a.NB ? hist[h] : 0;
+      bk[u] = (sl * NG + g) * a.gw + wr;
+      g += dg;                            // next slot: w += dw (sl += dsl, wr += dwr), g += dg
+      sl += dsl;
+      wr += dwr;
+      if (g >= NG) {
+        g -= NG;
+        ++wr;
+      }
+      if (wr >= a.gw) {                   // wr < 2 gw here: dwr < gw, plus at most one carry
+        wr -= a.gw;
+        ++sl;
+      }
+    }
+    int base[KF];
+#pragma unroll
+    for (int u = 0; u < KF; ++u) base[u] = cv[u] ? atomicAdd(&a.cnt[bk[u]], cv[u]) : 0;
+#pragma unroll
+    for (int u = 0; u < KF; ++u)
+      if (cv[u]) hist[h0 + u * kPrepBlock] = base[u];
+  }
+}
 
 constexpr int kReqPerPrepBlock = 4 * kPrepBlock;  // requests per request block of k_prep / k_scatter
 constexpr int kHistMax = 8192;                    // buckets counted in LDS (else global atomics)
@@ -444,42 +487,12 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
     }
     if (local) {
       __syncthreads();
-      // slot h = w * 2M + g holds the bucket of wave w = sl * gw + wr and 2 m + prompt-less =
-      // g; (sl, wr, g) advance with h by constant steps (two divisions per thread, none per
-      // slot), and kFlush slots per round have their atomics issued together (one round
-      // trip to the counters per round, not per slot)
-      constexpr int kFlush = 4;
-      const int NG = 2 * a.M;
-      const int dw = kPrepBlock / NG, dg = kPrepBlock - dw * NG;
-      const int dsl = dw / a.gw, dwr = dw - dsl * a.gw;
-      const int w0 = (int)threadIdx.x / NG;
-      int g = (int)threadIdx.x - w0 * NG, sl = w0 / a.gw, wr = w0 - sl * a.gw;
-      for (int h0 = threadIdx.x; h0 < a.NB; h0 += kFlush * kPrepBlock) {
-        int cv[kFlush], bk[kFlush];
-#pragma unroll
-        for (int u = 0; u < kFlush; ++u) {
-          const int h = h0 + u * kPrepBlock;
-          cv[u] = h < a.NB ? hist[h] : 0;
-          bk[u] = (sl * NG + g) * a.gw + wr;
-          g += dg;                        // next slot: w += dw (sl += dsl, wr += dwr), g += dg
-          sl += dsl;
-          wr += dwr;
-          if (g >= NG) {
-            g -= NG;
-            ++wr;
-          }
-          if (wr >= a.gw) {               // wr < 2 gw here: dwr < gw, plus at most one carry
-            wr -= a.gw;
-            ++sl;
-          }
-        }
-        int base[kFlush];
-#pragma unroll
-        for (int u = 0; u < kFlush; ++u) base[u] = cv[u] ? atomicAdd(&a.cnt[bk[u]], cv[u]) : 0;
-#pragma unroll
-        for (int u = 0; u < kFlush; ++u)
-          if (cv[u]) hist[h0 + u * kPrepBlock] = base[u];   // this block's base in the bucket
-      }
+      // KF slots per thread per round (all slots of the histogram in one round up to 16 per
+      // thread; four per round for small histograms, whose extra slots would only cost the walk)
+      if (a.NB > 4 * kPrepBlock)
+        flush_hist<16>(a, hist);
+      else
+        flush_hist<4>(a, hist);
       __syncthreads();
 #pragma unroll
       for (int u = 0; u < U; ++u)
@@ -508,8 +521,10 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
       for (int u = 0; u < kHostU; ++u) {
         const int g = G0 + u * kPrepBlock + threadIdx.x;
         const int gc = min(g, a.G - 1);
-        has[u] = g < a.G && ((a.resident[(size_t)gc * a.words + (m >> 5)] >> (m & 31)) & 1u);
-        key[u] = a.fast ? host_class(a, gc) : 0;
+        const uint32_t word = a.resident[(size_t)gc * a.words + (m >> 5)];   // loads unconditional
+        const int cls = host_class(a, gc);
+        has[u] = g < a.G && ((word >> (m & 31)) & 1u);
+        key[u] = a.fast ? cls : 0;
       }
       int before[kHostU];
 #pragma unroll
@@ -1628,7 +1643,7 @@ __global__ void __launch_bounds__(kWpb16 * 64) k_score_r16(PlaceArgs a) {
   // the requests.  Lane l holds the fields of request l / 4, read at the tile's position
   // clamped into the request array (a missing request is masked below).
   constexpr int kDcV = kRows * 128 / 4 / T;        // float4 of the decode table per thread
-  constexpr int kHk = kHcap / (S * kWave);         // chunk hosts per lane
+  constexpr int kHk = kHcap >= S * kWave ? kHcap / (S * kWave) : 1;   // chunk hosts per lane
   const float *dsrc = a.dc + (size_t)m * kRows * 128;
   const bool dc_al = (((uintptr_t)dsrc) & 15) == 0;
   float4 dcv[kDcV];
