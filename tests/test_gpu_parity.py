@@ -350,6 +350,19 @@ def test_fast_kernel_packed_classes_after_the_first_chunk(split):
     parity_place(inp, label=f"8x16, 700 hosts, caps 3 then {split} after host 300")
 
 
+@pytest.mark.parametrize("R", [20011, 40009])
+def test_fast_kernel_several_chunks_one_or_two_wavefronts_per_tile(R):
+    """8x16 tables, more hosts per model than one LDS chunk and random SM caps, with enough
+    requests for two wavefronts per tile (20,011: 1,024 < tiles <= 2,048) or one (40,009)."""
+    rng = np.random.default_rng(R)
+    inp = W.make_tiny_placement(rng, R=R, G=330, M=2, NS=8, NF=16, W=2, caps=True)
+    one_slo_pair_per_model(rng, inp)
+    hosts = [int(((inp["gpus"]["resident"][:, 0] >> m) & 1).sum()) for m in range(2)]
+    assert min(hosts) > 128, hosts
+    sel = np.random.default_rng(3).choice(R, 2500, replace=False)
+    parity_place(inp, sel, label=f"8x16, {hosts} hosts, {R} requests")
+
+
 @pytest.mark.parametrize("seed,variant", [(0, "plain"), (1, "plain"), (2, "ties"), (3, "ties"),
                                           (4, "negative"), (5, "low caps")])
 def test_fast_kernel_packed_capped_classes(seed, variant):
