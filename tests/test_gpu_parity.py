@@ -350,6 +350,16 @@ def test_fast_kernel_packed_classes_after_the_first_chunk(split):
     parity_place(inp, label=f"8x16, 700 hosts, caps 3 then {split} after host 300")
 
 
+@pytest.mark.parametrize("seed", range(2))
+def test_fast_kernel_nan_and_inf_cells(seed):
+    """8x16 tables with NaN and infinite entries, one SLO pair per model (the tiles take the
+    8x16 kernel's own scoring): such cells never pass an SLO test, in pass 1 or pass 2."""
+    rng = np.random.default_rng(7300 + seed)
+    inp = W.make_tiny_placement(rng, R=400, G=40, M=2, NS=8, NF=16, W=2, caps=True, nan_cells=True)
+    one_slo_pair_per_model(rng, inp)
+    parity_place(inp, label=f"8x16 nan/inf cells, seed {seed}")
+
+
 @pytest.mark.parametrize("R", [20011, 40009])
 def test_fast_kernel_several_chunks_one_or_two_wavefronts_per_tile(R):
     """8x16 tables, more hosts per model than one LDS chunk and random SM caps, with enough
