@@ -1,20 +1,22 @@
 // festina.hip -- MI355X (gfx950) kernels and C-ABI host dispatch of the batched
 // energy-aware placement and migration search (Festina, Sec. 3.3 and Sec. 3.5).
 //
-// Placement pipeline (one call, five launches on the caller's stream):
-//   k_zero      clear the bucket counters
+// Placement pipeline (one call, four launches on the caller's stream, five with k_scan):
+//   k_init      clear the bucket counters; the table minima (least entry of each prefill
+//                 row, its least nonzero magnitude, least decode entry of each model)
 //   k_prep      requests: validity, bucket key (wave, model, has-prompt), the bucket count
 //                 and the request's position within its bucket; hosts: per-model list of
-//                 hosting GPUs in ascending order; GPU records: per (wave, GPU) the
-//                 post-admission batch row, k_g * u_g and the SM caps
+//                 hosting GPUs in ascending order (for 8 x 16 tables sorted by SM-cap class
+//                 within chunks); GPU records: per (wave, GPU) the post-admission batch row,
+//                 k_g * u_g and the SM caps
 //   k_scan      one block: bucket offsets and the tile table (only with more buckets than
 //                 an LDS histogram holds)
-//   k_scatter   request records (5% output pad, prompt bucket, SLOs) grouped by bucket
-//   k_score     one workgroup per tile (requests of one bucket): the model's decode table is
-//                 staged in LDS; each wave scores Q requests at once, lanes spanning the
-//                 (SM level, frequency level) cells, looping over the hosting GPUs; the
-//                 per-request argmin is fused (running minimum per lane, then a wavefront
-//                 reduction with lowest-index tie-break); only 9 bytes per request reach HBM
+//   k_scatter   bucket offsets and the tile table (each block scans the counts itself),
+//                 request records (5% output pad, prompt bucket, SLOs) grouped by bucket
+//   k_score_r16 (8 x 16 tables) / k_score (any shape): workgroups of tiles of one bucket's
+//                 requests: the model's decode table is staged in LDS, lanes span the
+//                 (SM level, frequency level) cells, and the per-request argmin with the
+//                 lowest-index tie-break is fused; only 9 bytes per request reach HBM
 // Migration pipeline:
 //   k_fleet     per GPU: bitmask of frequency levels at which all instances meet their SLOs,
 //                 its lowest level and the dynamic-power baseline f[kd0]^3 * u
