@@ -771,10 +771,11 @@ __device__ __forceinline__ void load_scan_counts(const PlaceArgs &a, v4i (&v)[kS
   for (int q = 0; q < kScanChunks; ++q) v[q] = *reinterpret_cast<const v4i *>(a.cnt + min(lo + 4 * q, last4));
 }
 
-// LDS of block_scan_buckets (ints): [NB] bucket starts, [NB + 1] first tile of each bucket
-// and the tile total, then with group padding [2][ng + 1] group tables.
+// LDS of block_scan_buckets (ints): [NB4] bucket starts, [NB4 + 4] first tile of each bucket
+// and the tile total (NB4 = NB rounded up to 4, so both arrays take 16-byte stores), then
+// with group padding [2][ng + 1] group tables.
 __host__ __device__ constexpr long long block_scan_ints(long long NB, long long NG, bool pad) {
-  return 2 * NB + 1 + (pad ? 2 * (NG + 1) : 0);
+  return 2 * ((NB + 3) & ~3LL) + 4 + (pad ? 2 * (NG + 1) : 0);
 }
 
 __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kScanChunks]) {
@@ -813,28 +814,36 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
     tot_t += s_t[i];
   }
   const bool pad = a.gpad > 1;
-  int *ts = start + a.NB;                            // [NB + 1] unpadded first tile of each bucket
-  int *gP = ts + a.NB + 1, *pp = gP + a.ng + 1;      // [ng + 1] each, with group padding
+  const int NB4 = (a.NB + 3) & ~3;
+  int *ts = start + NB4;                             // [NB + 1] unpadded first tile of each bucket
+  int *gP = ts + NB4 + 4, *pp = gP + a.ng + 1;       // [ng + 1] each, with group padding
   const int g0 = lo / a.gw, w0 = lo - g0 * a.gw;
   {
+    // a thread's buckets are 4-aligned and contiguous: each chunk of 4 starts goes to LDS as
+    // one 16-byte store per array (a chunk past NB holds zero counts, so its entries past NB
+    // repeat the totals, and ts[NB] gets the tile total)
     int pc = pc0, pt = pt0, g = g0, wi = w0;
 #pragma unroll
     for (int q = 0; q < V; ++q)
+      if (lo + 4 * q < hi) {
+        v4i sv, tv;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int i = lo + 4 * q + e;
-        if (i < hi) {
+        for (int e = 0; e < 4; ++e) {
           const int n = v[q][e];
-          start[i] = pc;
-          ts[i] = pt;
-          if (pad && wi == 0) gP[g] = pt;
+          sv[e] = pc;
+          tv[e] = pt;
+          if (lo + 4 * q + e < hi) {
+            if (pad && wi == 0) gP[g] = pt;
+            if (++wi == a.gw) {
+              wi = 0;
+              ++g;
+            }
+          }
           pc += n;
           pt += (n + a.tile - 1) >> tsh;
-          if (++wi == a.gw) {
-            wi = 0;
-            ++g;
-          }
         }
+        *reinterpret_cast<v4i *>(start + lo + 4 * q) = sv;
+        *reinterpret_cast<v4i *>(ts + lo + 4 * q) = tv;
       }
   }
   if (threadIdx.x == 0) ts[a.NB] = tot_t;
@@ -924,7 +933,7 @@ __device__ __forceinline__ void take_key(int (&key)[kScatterU], ReqRec (&rec)[kS
 }
 
 __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
-  extern __shared__ int start[];   // block_scan_ints(NB, ng, padded) ints
+  extern __shared__ __align__(16) int start[];   // block_scan_ints(NB, ng, padded) ints
   int key[kScatterU], pos[kScatterU];
   ReqRec rec[kScatterU];
   if (a.scan_local) {
