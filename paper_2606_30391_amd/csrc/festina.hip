@@ -1874,33 +1874,36 @@ __global__ void __launch_bounds__(kWpb16 * 64) k_score_r16(PlaceArgs a) {
 #pragma unroll
       for (int q0 = 0; q0 < kR; q0 += 4) {
         if (((pend >> (4 * q0)) & 0x1111ull) == 0ull) continue;
-        bool hit[4];
+        unsigned long long mk[4];
         int cq[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int q = q0 + t;
-          const v2u qi = *reinterpret_cast<const v2u *>(L + Qi + q * 8);
-          const float K = __uint_as_float(qi.x);
-          const int c = (int)qi.y;
+          // request q's K* and tied cell, wave-uniform: read from its lane into scalar
+          // registers, so the cell's level, frequency and offsets are scalar arithmetic
+          const float K = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(Ks), 4 * q));
+          const int c = __builtin_amdgcn_readlane(cellv, 4 * q);
           cq[t] = c;
-          const int cj = c >> 4, ck = c & 15;
+          const int cj = c >> 4, ck4 = (c & 15) * 4;
           const int jp = min(cj, cp), jd = min(cj, cd);
-          const float pdp = *reinterpret_cast<const float *>(L + kL_pd + (jp * 16 + ck) * 4);
-          const float pdd = *reinterpret_cast<const float *>(L + kL_pd + (jd * 16 + ck) * 4);
-          const float tbt = *reinterpret_cast<const float *>(L + rowB + (uint32_t)(jd * 16 + ck) * 4u);
-          const float x = *reinterpret_cast<const float *>(L + Tw + (uint32_t)(q * 8 + jp) * 4u);
+          const float pdp = *reinterpret_cast<const float *>(L + kL_pd + ck4 + jp * 64);
+          const float pdd = *reinterpret_cast<const float *>(L + kL_pd + ck4 + jd * 64);
+          const float tbt = *reinterpret_cast<const float *>(L + rowB + (uint32_t)(ck4 + jd * 64));
+          const float x = *reinterpret_cast<const float *>(L + Tw + (uint32_t)(q * 32 + jp * 4));
           // a cell above max(cap_pf, cap_dc) repeats a lower cell of the same GPU: pass 1 gave
-          // it NaN power, so it never matches
-          hit[t] = valid && cj <= mx && r16_key(kap, pdp, pdd, tbt, x, p0) == K;
+          // it NaN power, so it never matches; the ballot is taken here, from the compares'
+          // own masks
+          mk[t] = __ballot(valid && cj <= mx && r16_key(kap, pdp, pdd, tbt, x, p0) == K);
         }
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int q = q0 + t;
-          const unsigned long long mk = __ballot(hit[t]);
-          if (((pend >> (4 * q)) & 1ull) && mk != 0ull) {
-            const int first = __builtin_ctzll(mk);
+          if (((pend >> (4 * q)) & 1ull) && mk[t] != 0ull) {
+            const int first = __builtin_ctzll(mk[t]);
             const int gw = __builtin_amdgcn_readlane(g, first);
-            best = (lane >> 2) == q ? min(best, gw * 128 + cq[t]) : best;
+            // the lane test on a fresh lane id: made here, not kept as 16 lane masks in
+            // scalar registers through pass 2
+            best = (lane_fresh() >> 2) == q ? min(best, gw * 128 + cq[t]) : best;
             pend &= ~(1ull << (4 * q));
           }
         }
