@@ -1543,16 +1543,6 @@ __device__ __forceinline__ float wave_min16(const float (&a)[kR], const float (&
 // Cell value meaning "no tied cell left" (cells are 0-127).
 constexpr int kNoCell = 128;
 
-// v with lane LANE set to the wave-uniform value x (v_writelane_b32, the lane an immediate).
-// The compiler does not insert hazard wait states around inline assembly, so the asm brings
-// its own: five before (x may have just been written by a VALU instruction, e.g. a compare
-// writing VCC) and two after (the next instruction may read v through DPP).
-template <int LANE>
-__device__ __forceinline__ int writelane_imm(int v, int x) {
-  asm volatile("s_nop 4\n\tv_writelane_b32 %0, %1, %2\n\ts_nop 1" : "+v"(v) : "s"(x), "n"(LANE));
-  return v;
-}
-
 // Wave-level LDS barrier: stores by any lane of the wavefront are visible to its loads after.
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
