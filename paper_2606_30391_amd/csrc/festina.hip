@@ -333,7 +333,7 @@ __device__ __forceinline__ int prep_request(const PlaceArgs &a, int r, const Req
     return -1;
   }
   const int k = bucket_of(a, f.w, f.m, f.pt == 0);
-  a.key[r] = k | (tiny ? kKeyTiny : 0);
+  __builtin_nontemporal_store(k | (tiny ? kKeyTiny : 0), &a.key[r]);   // read by the next kernel
   return k;
 }
 
@@ -502,7 +502,7 @@ __global__ void __launch_bounds__(kPrepBlock) k_prep(PlaceArgs a, int32_t nbr) {
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (key[u] >= 0) a.off[b * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x] = pos[u];
+      if (key[u] >= 0) __builtin_nontemporal_store(pos[u], &a.off[b * kReqPerPrepBlock + u * kPrepBlock + threadIdx.x]);
     return;
   }
   if (b < nbr + a.M) {
@@ -906,6 +906,15 @@ __device__ void block_scan_buckets(const PlaceArgs &a, int *start, v4i (&v)[kSca
 // has written the bucket starts and the tile table.
 constexpr int kScatterU = kReqPerPrepBlock / kPrepBlock;
 
+// A request record written with streaming (nontemporal) stores: the next kernel reads it on
+// any XCD, so it is not kept in this XCD's L2 to be written back when the kernel ends.
+__device__ __forceinline__ void store_rec_nt(ReqRec *p, const ReqRec &r) {
+  const v4i lo = v4i{r.r, r.row, __float_as_int(r.lout), __float_as_int(r.slo_ttft)};
+  const v4i hi = v4i{__float_as_int(r.slo_tbt), __float_as_int(r.rlout), 0, 0};
+  __builtin_nontemporal_store(lo, reinterpret_cast<v4i *>(p));
+  __builtin_nontemporal_store(hi, reinterpret_cast<v4i *>(p) + 1);
+}
+
 // Request u of this thread: stored key (-1: none), position and record.  Every load is issued
 // before the first use; a thread past the last request reads the last one (R >= 1) and drops
 // it, and an invalid request's position (never written) is not used.  take_key then splits
@@ -946,13 +955,13 @@ __global__ void __launch_bounds__(kPrepBlock) k_scatter(PlaceArgs a) {
     take_key(key, rec);
 #pragma unroll
     for (int u = 0; u < kScatterU; ++u)
-      if (key[u] >= 0) a.preq[start[key[u]] + pos[u]] = rec[u];
+      if (key[u] >= 0) store_rec_nt(a.preq + start[key[u]] + pos[u], rec[u]);
   } else {
     scatter_loads(a, key, pos, rec);
     take_key(key, rec);
 #pragma unroll
     for (int u = 0; u < kScatterU; ++u)
-      if (key[u] >= 0) a.preq[a.bstart[key[u]] + pos[u]] = rec[u];
+      if (key[u] >= 0) store_rec_nt(a.preq + a.bstart[key[u]] + pos[u], rec[u]);
   }
 }
 
