@@ -170,6 +170,9 @@ def lib():
         L.festina_oracle_preferred_at.restype = C.c_int
         L.festina_oracle_dispatch.argtypes = [P(_Lut), P(_Avail), P(_Requests), C.c_int32, C.c_void_p, C.c_void_p]
         L.festina_oracle_dispatch.restype = C.c_int
+        L.festina_oracle_dispatch_waves.argtypes = [P(_Lut), P(_Avail), P(_Requests), C.c_int32, C.c_void_p,
+                                                    C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.festina_oracle_dispatch_waves.restype = C.c_int
         L.festina_oracle_transfer_costs.argtypes = [P(_Transfer), C.c_int32, C.c_void_p]
         L.festina_oracle_transfer_costs.restype = C.c_int
         L.festina_oracle_request_moves.argtypes = [P(_Lut), P(_Transfer), P(_Plan), P(_Moves), C.c_void_p,
@@ -437,6 +440,28 @@ def dispatch(inp: dict, sel=None):
     a = np.frombuffer(buf, dtype=np.dtype([("gpu", "<i4"), ("freq_level", "<i4"), ("sm_level", "<i4"),
                                            ("phase", "<i4"), ("energy", "<f8")]), count=n)
     return (a["gpu"].copy(), a["freq_level"].copy(), a["sm_level"].copy(), a["phase"].copy(), a["energy"].copy())
+
+
+def dispatch_waves(inp: dict, wave_start):
+    """Oracle dispatch wave by wave, each wave committed to the GPUs' state before the next
+    (requests ordered by wave; wave w = requests wave_start[w] .. wave_start[w+1]-1).
+    Returns (gpu, freq_level, sm_level, phase int32, energy float64) and the final state
+    {"freq_cur", "batch", "mem_free_mib"}."""
+    pin = _Pinned()
+    lut, av, req = _lut(inp["lut"], pin), _avail(inp["avail"], pin), _requests(inp["requests"], pin)
+    n = int(inp["requests"]["n_requests"])
+    ws = _arr(wave_start, np.int32)
+    G, S = int(inp["avail"]["n_gpus"]), int(inp["avail"]["n_steps"])
+    freq, batch, mem = np.zeros(G, np.int32), np.zeros(G, np.int32), np.zeros((G, S), np.int32)
+    buf = (_Dispatch * max(n, 1))()
+    rc = lib().festina_oracle_dispatch_waves(C.byref(lut), C.byref(av), C.byref(req), len(ws) - 1, _p(ws),
+                                             _p(freq), _p(batch), _p(mem), C.cast(buf, C.c_void_p))
+    if rc != 0:
+        raise ValueError("oracle rejected the wave dispatch arguments")
+    a = np.frombuffer(buf, dtype=np.dtype([("gpu", "<i4"), ("freq_level", "<i4"), ("sm_level", "<i4"),
+                                           ("phase", "<i4"), ("energy", "<f8")]), count=n)
+    return ((a["gpu"].copy(), a["freq_level"].copy(), a["sm_level"].copy(), a["phase"].copy(), a["energy"].copy()),
+            {"freq_cur": freq, "batch": batch, "mem_free_mib": mem})
 
 
 def transfer_costs(inp: dict) -> np.ndarray:

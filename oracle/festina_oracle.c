@@ -74,6 +74,8 @@
 #include <math.h>
 #include <stddef.h>
 #include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
 
 #define OR_ROWS 32
 #define OR_ROW_TOKENS 256
@@ -803,6 +805,76 @@ int festina_oracle_dispatch(const or_lut *L, const or_avail *A, const or_request
   if (!or_lut_ok(L) || !A || !Q || !out || A->n_gpus < 0 || A->n_steps < 1 || Q->n_requests < 0) return 1;
   const int32_t n = sel ? n_sel : Q->n_requests;
   for (int32_t i = 0; i < n; ++i) or_dispatch_one(L, A, Q, sel ? sel[i] : i, &out[i]);
+  return 0;
+}
+
+/* The same dispatcher run over arrival waves, each wave committed before the next one is
+ * dispatched (Sec. 3.3 decides one request at a time against the state its local
+ * schedulers report; here the requests of one wave share a snapshot, and the waves follow
+ * one another).  Requests are ordered by wave: wave w is requests wave_start[w] ..
+ * wave_start[w+1]-1.  After every request of a wave is decided, each one placed on a GPU of
+ * the table (Phase Two, or the F_max fallback) is committed to that GPU:
+ *   its decode batch grows by one (B -> B + 1, so the next request sees row b = min(B+2, 32));
+ *   it holds its memory from its start on: every profile step from the one that admitted it
+ *   loses ceil(Req_mem / 1024) MiB (a step short of memory reads -1 MiB: nothing fits);
+ *   an F_max placement leaves the GPU at the top frequency level (it was boosted).
+ * Free SM levels and the profile's times stay as reported; a new GPU (Phase Three's scale
+ * out) is not a row of the table and commits nothing.  The state after the last wave is
+ * returned in freq_out [G], batch_out [G] and mem_out [G][S]. */
+int festina_oracle_dispatch_waves(const or_lut *L, const or_avail *A, const or_requests *Q, int32_t n_waves,
+                                  const int32_t *wave_start, int32_t *freq_out, int32_t *batch_out,
+                                  int32_t *mem_out, or_dispatch *out) {
+  if (!or_lut_ok(L) || !A || !Q || !out || !freq_out || !batch_out || !mem_out || A->n_gpus < 0 ||
+      A->n_steps < 1 || Q->n_requests < 0 || n_waves < 0 || (n_waves > 0 && !wave_start))
+    return 1;
+  if (n_waves == 0 ? Q->n_requests != 0 : (wave_start[0] != 0 || wave_start[n_waves] != Q->n_requests)) return 1;
+  for (int32_t w = 0; w < n_waves; ++w)
+    if (wave_start[w + 1] < wave_start[w]) return 1;
+  const int G = A->n_gpus, S = A->n_steps;
+  for (int g = 0; g < G; ++g) {
+    freq_out[g] = A->freq_cur[g];
+    batch_out[g] = A->batch[g];
+    for (int s = 0; s < S; ++s) mem_out[(size_t)g * S + s] = A->mem_free_mib[(size_t)g * S + s];
+  }
+  int32_t *snap = (int32_t *)malloc(sizeof(int32_t) * ((size_t)G * S + 1));
+  if (!snap) return 1;
+  or_avail now = *A;              /* the state the wave sees */
+  now.freq_cur = freq_out;
+  now.batch = batch_out;
+  now.mem_free_mib = snap;
+  for (int32_t w = 0; w < n_waves; ++w) {
+    memcpy(snap, mem_out, sizeof(int32_t) * (size_t)G * S);
+    for (int32_t r = wave_start[w]; r < wave_start[w + 1]; ++r) or_dispatch_one(L, &now, Q, r, &out[r]);
+    /* decisions first (on the snapshot), then the commits */
+    int32_t *boost = (int32_t *)calloc((size_t)G + 1, sizeof(int32_t));
+    int32_t *grow = (int32_t *)calloc((size_t)G + 1, sizeof(int32_t));
+    int64_t *taken = (int64_t *)calloc((size_t)G * S + 1, sizeof(int64_t));
+    if (!boost || !grow || !taken) {
+      free(boost), free(grow), free(taken), free(snap);
+      return 1;
+    }
+    for (int32_t r = wave_start[w]; r < wave_start[w + 1]; ++r) {
+      const int g = out[r].gpu;
+      if (out[r].phase != 1 && out[r].phase != 2) continue;
+      const int m = Q->model[r];
+      const int64_t need = (int64_t)A->kv_kib_per_token[m] * ((int64_t)Q->prompt_tokens[r] + or_padded_out(Q->pred_out_tokens[r]));
+      int first = 0;                /* the admitting step: the first whose memory holds Req_mem */
+      while ((int64_t)snap[(size_t)g * S + first] * 1024 < need) ++first;
+      for (int s = first; s < S; ++s) taken[(size_t)g * S + s] += (need + 1023) / 1024;
+      grow[g] += 1;
+      if (out[r].phase == 2) boost[g] = 1;
+    }
+    for (int g = 0; g < G; ++g) {
+      batch_out[g] += grow[g];
+      if (boost[g]) freq_out[g] = L->n_freq - 1;
+      for (int s = 0; s < S; ++s) {
+        const int64_t v = (int64_t)mem_out[(size_t)g * S + s] - taken[(size_t)g * S + s];
+        mem_out[(size_t)g * S + s] = (int32_t)(v < -1 ? -1 : v);
+      }
+    }
+    free(boost), free(grow), free(taken);
+  }
+  free(snap);
   return 0;
 }
 

@@ -127,6 +127,19 @@ DISPATCH = [
 ]
 
 
+WAVES = [
+    ("memory taken from every step", "for (int s = first; s < S; ++s) taken", "for (int s = 0; s < S; ++s) taken"),
+    ("batch does not grow", "batch_out[g] += grow[g];", ""),
+    ("no boost after an F_max placement", "if (boost[g]) freq_out[g] = L->n_freq - 1;", ""),
+    ("a wave sees its own commits", "memcpy(snap, mem_out, sizeof(int32_t) * (size_t)G * S);\n    for (int32_t r = wave_start[w]; r < wave_start[w + 1]; ++r) or_dispatch_one(L, &now, Q, r, &out[r]);",
+     "memcpy(snap, mem_out, sizeof(int32_t) * (size_t)G * S);\n    for (int32_t r = wave_start[w]; r < wave_start[w + 1]; ++r) {\n      or_dispatch_one(L, &now, Q, r, &out[r]);\n      if (out[r].phase == 1 || out[r].phase == 2) { batch_out[out[r].gpu] += 1; for (int s = 0; s < S; ++s) snap[(size_t)out[r].gpu * S + s] -= (int32_t)((A->kv_kib_per_token[Q->model[r]] * ((int64_t)Q->prompt_tokens[r] + or_padded_out(Q->pred_out_tokens[r])) + 1023) / 1024); }\n    }"),
+    ("memory floor at zero", "(int32_t)(v < -1 ? -1 : v)", "(int32_t)(v < 0 ? 0 : v)"),
+    ("demand rounded down", "taken[(size_t)g * S + s] += (need + 1023) / 1024;", "taken[(size_t)g * S + s] += need / 1024;"),
+    ("F_max placement not committed", "if (out[r].phase != 1 && out[r].phase != 2) continue;",
+     "if (out[r].phase != 1) continue;"),
+]
+
+
 TRANSFER = [
     ("weights the destination already holds", "if (on_u && !on_v) mib += T->weights_mib[m];",
      "if (on_u) mib += T->weights_mib[m];"),
@@ -190,4 +203,10 @@ def test_dispatch_pins_reject_mutant(tmp_path, name, old, new):
 @pytest.mark.parametrize("name,old,new", TRANSFER, ids=[p[0] for p in TRANSFER])
 def test_transfer_pins_reject_mutant(tmp_path, name, old, new):
     rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_transfer_pins.py")
+    assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
+
+
+@pytest.mark.parametrize("name,old,new", WAVES, ids=[p[0] for p in WAVES])
+def test_wave_dispatch_pins_reject_mutant(tmp_path, name, old, new):
+    rc, tail = _run_pins(tmp_path, name, old, new, "test_oracle_dispatch_waves_pins.py")
     assert rc != 0, f"pins accepted the mutant '{name}':\n{tail}"
