@@ -29,6 +29,8 @@
  * and the paper's own dispatcher, for comparison with the exhaustive search:
  *   festina_dispatch_requests -- one operating point per GPU (its current frequency),
  *       the 2% stability tie-break, the F_max fallback and scale-out (Sec. 3.3).
+ *   festina_dispatch_waves    -- the same over arrival waves, each wave's placements
+ *       committed to the GPUs' batch, memory and frequency before the next wave.
  *
  * Conventions shared by every entry point
  *  - All array pointers inside the structs are DEVICE pointers (HIP global memory
@@ -57,7 +59,7 @@
 extern "C" {
 #endif
 
-#define FESTINA_ABI_VERSION 3
+#define FESTINA_ABI_VERSION 4
 #define FESTINA_N_ROWS 32        /* rows of every profile table */
 #define FESTINA_MAX_CELLS 256    /* n_sm * n_freq limit of the placement kernels */
 #define FESTINA_MAX_FREQ_MIG 32  /* n_freq limit of the migration kernels (32-bit level masks) */
@@ -410,6 +412,36 @@ size_t festina_dispatch_workspace_bytes(const festina_lut *lut, const festina_gp
 festina_status festina_dispatch_requests(const festina_lut *lut, const festina_gpu_avail *avail,
                                          const festina_requests *req, festina_dispatches *out,
                                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* The GPUs' state that a wave-by-wave dispatch carries from one wave to the next (device
+ * memory written by the call; the arrays may be avail's own, which are then updated in
+ * place).  On return it is the state after the last wave. */
+typedef struct festina_gpu_state {
+  int32_t *freq_cur;                 /* [G] current frequency level */
+  int32_t *batch;                    /* [G] decode batch */
+  int32_t *mem_free_mib;             /* [G][S] free-memory profile */
+} festina_gpu_state;
+
+size_t festina_dispatch_waves_workspace_bytes(const festina_lut *lut, const festina_gpu_avail *avail);
+
+/* The dispatcher over arrival waves (Sec. 3.3 decides each request on the state the local
+ * schedulers report; here one wave of requests shares a snapshot and the waves follow one
+ * another).  Requests are ordered by wave: wave w is requests wave_start[w] ..
+ * wave_start[w+1]-1 (wave_start: HOST array of n_waves + 1 entries, wave_start[0] = 0,
+ * non-decreasing, wave_start[n_waves] = n_requests; requests' wave field is ignored).
+ * The state starts as avail's freq_cur, batch and mem_free_mib.  Each wave is dispatched
+ * exactly as festina_dispatch_requests would on the current state, then each of its
+ * requests placed on a GPU of the table (phase 1 or 2) is committed to that GPU: the batch
+ * grows by one; ceil(Req_mem / 1024) MiB are taken from every profile step at or after the
+ * one that admitted it (a step left short reads -1 MiB); a phase-2 (F_max) placement leaves
+ * the GPU at the top frequency level.  Profile times, free SM levels, k and residency stay
+ * as given; a scale-out (phase 3) commits nothing.  Workspace from
+ * festina_dispatch_waves_workspace_bytes (256-byte aligned, clobbered).  2 + 2 x (non-empty
+ * waves) kernel launches on `stream`, nothing allocated or synchronised. */
+festina_status festina_dispatch_waves(const festina_lut *lut, const festina_gpu_avail *avail,
+                                      const festina_requests *req, int32_t n_waves, const int32_t *wave_start,
+                                      festina_gpu_state *state, festina_dispatches *out, void *workspace,
+                                      size_t workspace_bytes, void *stream);
 
 /* Transfer plan after a reconfiguration (App. F).  A GPU's state is its resident models'
  * weights plus its request state selected for migration.  Sending GPU u's state to GPU v

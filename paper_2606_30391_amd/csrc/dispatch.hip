@@ -61,6 +61,19 @@ struct DspArgs {
   int32_t *host_cnt, *host_list;     // workspace: [M], [M][G]
   int4 *hrec;                        // workspace: [M][G][4] host records when S <= 4
   int32_t packed;
+  int32_t r0;                        // first request of the launch (a.R: one past the last)
+  // wave commits (null when not committing): placements per GPU, MiB taken per (GPU,
+  // admitting step), F_max placements per GPU
+  int32_t *grow, *boost;
+  unsigned long long *taken;
+};
+
+// The state a wave-by-wave call carries from one wave to the next, and its pending commits.
+struct WaveState {
+  int32_t G, S, top;
+  int32_t *freq, *batch, *mem;       // [G], [G], [G][S]
+  int32_t *grow, *boost;             // [G]
+  unsigned long long *taken;         // [G][S]
 };
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -239,7 +252,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
 #pragma clang fp contract(off)
   const int lane = threadIdx.x & (kWave - 1);
   const int sub = lane & (kGroup - 1);
-  const int r = (blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kReqPerWave + lane / kGroup;
+  const int r = a.r0 + (blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kReqPerWave + lane / kGroup;
   if (r >= a.R) return;
   const double inf = __builtin_huge_val();
   const int m = a.model[r];
@@ -248,11 +261,12 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
   int gsel = -1, ksel = -1, jsel = -1, phase = 0;
   double esel = inf;
   bool writer = sub == 0;
+  long long need = 0;
   if (m >= 0 && m < a.M && pd >= 0 && pt >= 0) {
     const int prow = pt == 0 ? -1 : (min((int)(((unsigned)pt + 255u) >> 8), kRows) - 1);
     const long long lout_i = ((long long)pd * 105 + 99) / 100;
     const double lout = (double)lout_i;
-    const long long need = (long long)a.kv[m] * ((long long)pt + lout_i);
+    need = (long long)a.kv[m] * ((long long)pt + lout_i);
     const int nh = a.host_cnt[m];
     const int *hl = a.host_list + (size_t)m * a.G;
     // Phase One at every host, least energy; the first kCached hosts of a lane are kept
@@ -383,6 +397,53 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
     a.out_sm[r] = jsel;
     a.out_phase[r] = (uint8_t)phase;
     a.out_energy[r] = (float)esel;
+    if (a.grow && (phase == 1 || phase == 2)) {
+      // commit to the chosen GPU: one more request in its batch, and ceil(Req_mem / 1024)
+      // MiB from the step that admitted it (the first whose free memory holds Req_mem) on
+      const int32_t *mf = a.mem_free + (size_t)gsel * a.S;
+      int st = 0;
+      while (st < a.S - 1 && (long long)mf[st] * 1024 < need) ++st;
+      atomicAdd(&a.grow[gsel], 1);
+      atomicAdd(&a.taken[(size_t)gsel * a.S + st], (unsigned long long)((need + 1023) / 1024));
+      if (phase == 2) a.boost[gsel] = 1;
+    }
+  }
+}
+
+// Start of a wave-by-wave call: the caller's state copied into the carried state (the two
+// may be the same arrays), no commit pending.
+__global__ void __launch_bounds__(kHostBlock) k_wave_init(WaveState w, const int32_t *freq0, const int32_t *batch0,
+                                                          const int32_t *mem0) {
+  const int g = blockIdx.x * kHostBlock + threadIdx.x;
+  if (g >= w.G) return;
+  w.freq[g] = freq0[g];
+  w.batch[g] = batch0[g];
+  w.grow[g] = 0;
+  w.boost[g] = 0;
+  for (int s = 0; s < w.S; ++s) {
+    w.mem[(size_t)g * w.S + s] = mem0[(size_t)g * w.S + s];
+    w.taken[(size_t)g * w.S + s] = 0ull;
+  }
+}
+
+// End of a wave: each GPU applies its pending commits (batch, boost, and the MiB taken from
+// every step at or after the admitting ones; a step short of memory reads -1) and clears them.
+__global__ void __launch_bounds__(kHostBlock) k_wave_commit(WaveState w) {
+  const int g = blockIdx.x * kHostBlock + threadIdx.x;
+  if (g >= w.G) return;
+  w.batch[g] += w.grow[g];
+  w.grow[g] = 0;
+  if (w.boost[g]) {
+    w.freq[g] = w.top;
+    w.boost[g] = 0;
+  }
+  unsigned long long run = 0ull;
+  for (int s = 0; s < w.S; ++s) {
+    const size_t at = (size_t)g * w.S + s;
+    run += w.taken[at];
+    w.taken[at] = 0ull;
+    const long long v = (long long)w.mem[at] - (long long)run;
+    w.mem[at] = v < -1 ? -1 : (int32_t)v;
   }
 }
 
@@ -406,9 +467,9 @@ extern "C" size_t festina_dispatch_workspace_bytes(const festina_lut *L, const f
   return bytes;
 }
 
-extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const festina_gpu_avail *A,
-                                                    const festina_requests *Q, festina_dispatches *out,
-                                                    void *workspace, size_t workspace_bytes, void *stream) {
+// Checks the arguments common to both dispatch calls; fills everything but the workspace.
+static festina_status dsp_args(const festina_lut *L, const festina_gpu_avail *A, const festina_requests *Q,
+                               festina_dispatches *out, DspArgs &a) {
   if (!dsp_shapes_ok(L, A) || !Q || !out || Q->n_requests < 0) return FESTINA_ERR_INVALID;
   const long long C = (long long)L->n_sm * L->n_freq;
   if (C > FESTINA_MAX_CELLS) return FESTINA_ERR_UNSUPPORTED;
@@ -416,13 +477,11 @@ extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const 
   if (!A->freq_cur || !A->batch || !A->k_dyn_w || !A->resident || !A->t_avail_ms || !A->mem_free_mib ||
       !A->sm_free || !A->kv_kib_per_token)
     return FESTINA_ERR_INVALID;
-  const size_t need = festina_dispatch_workspace_bytes(L, A);
-  if (!workspace || workspace_bytes < need || (((uintptr_t)workspace) & 255) != 0) return FESTINA_ERR_INVALID;
-  if (Q->n_requests == 0) return FESTINA_OK;
-  if (!Q->model || !Q->prompt_tokens || !Q->pred_out_tokens || !Q->slo_ttft_ms || !Q->slo_tbt_ms)
-    return FESTINA_ERR_INVALID;
-  if (!out->gpu || !out->freq_level || !out->sm_level || !out->phase || !out->energy_mj) return FESTINA_ERR_INVALID;
-  DspArgs a;
+  if (Q->n_requests > 0) {
+    if (!Q->model || !Q->prompt_tokens || !Q->pred_out_tokens || !Q->slo_ttft_ms || !Q->slo_tbt_ms)
+      return FESTINA_ERR_INVALID;
+    if (!out->gpu || !out->freq_level || !out->sm_level || !out->phase || !out->energy_mj) return FESTINA_ERR_INVALID;
+  }
   a.M = L->n_models;
   a.NS = L->n_sm;
   a.NF = L->n_freq;
@@ -455,6 +514,23 @@ extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const 
   a.out_sm = out->sm_level;
   a.out_phase = out->phase;
   a.out_energy = out->energy_mj;
+  a.r0 = 0;
+  a.grow = a.boost = nullptr;
+  a.taken = nullptr;
+  a.packed = 0;
+  a.hrec = nullptr;
+  return FESTINA_OK;
+}
+
+extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const festina_gpu_avail *A,
+                                                    const festina_requests *Q, festina_dispatches *out,
+                                                    void *workspace, size_t workspace_bytes, void *stream) {
+  DspArgs a;
+  const festina_status chk = dsp_args(L, A, Q, out, a);
+  if (chk != FESTINA_OK) return chk;
+  const size_t need = festina_dispatch_workspace_bytes(L, A);
+  if (!workspace || workspace_bytes < need || (((uintptr_t)workspace) & 255) != 0) return FESTINA_ERR_INVALID;
+  if (Q->n_requests == 0) return FESTINA_OK;
   char *ws = static_cast<char *>(workspace);
   a.host_cnt = reinterpret_cast<int32_t *>(ws);
   a.host_list = reinterpret_cast<int32_t *>(ws + align256(sizeof(int32_t) * L->n_models));
@@ -468,4 +544,76 @@ extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const 
   const long long blocks = ((long long)a.R + per_block - 1) / per_block;
   k_dispatch<<<(unsigned)blocks, kWavesPerBlock * kWave, 0, st>>>(a);
   return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
+}
+
+extern "C" size_t festina_dispatch_waves_workspace_bytes(const festina_lut *L, const festina_gpu_avail *A) {
+  if (!dsp_shapes_ok(L, A)) return 0;
+  const size_t G = (size_t)A->n_gpus;
+  return align256(sizeof(int32_t) * L->n_models) + align256(sizeof(int32_t) * (size_t)L->n_models * G) +
+         2 * align256(sizeof(int32_t) * G) + align256(sizeof(unsigned long long) * G * A->n_steps);
+}
+
+extern "C" festina_status festina_dispatch_waves(const festina_lut *L, const festina_gpu_avail *A,
+                                                 const festina_requests *Q, int32_t n_waves,
+                                                 const int32_t *wave_start, festina_gpu_state *state,
+                                                 festina_dispatches *out, void *workspace, size_t workspace_bytes,
+                                                 void *stream) {
+  DspArgs a;
+  const festina_status chk = dsp_args(L, A, Q, out, a);
+  if (chk != FESTINA_OK) return chk;
+  if (!state || !state->freq_cur || !state->batch || !state->mem_free_mib || n_waves < 0) return FESTINA_ERR_INVALID;
+  if (n_waves == 0) {
+    if (Q->n_requests != 0) return FESTINA_ERR_INVALID;
+  } else {
+    if (!wave_start || wave_start[0] != 0 || wave_start[n_waves] != Q->n_requests) return FESTINA_ERR_INVALID;
+    for (int32_t w = 0; w < n_waves; ++w)
+      if (wave_start[w + 1] < wave_start[w]) return FESTINA_ERR_INVALID;
+  }
+  const size_t need = festina_dispatch_waves_workspace_bytes(L, A);
+  if (!workspace || workspace_bytes < need || (((uintptr_t)workspace) & 255) != 0) return FESTINA_ERR_INVALID;
+  const size_t G = (size_t)A->n_gpus;
+  char *ws = static_cast<char *>(workspace);
+  size_t at = 0;
+  a.host_cnt = reinterpret_cast<int32_t *>(ws + at);
+  at += align256(sizeof(int32_t) * L->n_models);
+  a.host_list = reinterpret_cast<int32_t *>(ws + at);
+  at += align256(sizeof(int32_t) * (size_t)L->n_models * G);
+  WaveState w;
+  w.G = A->n_gpus;
+  w.S = A->n_steps;
+  w.top = L->n_freq - 1;
+  w.freq = state->freq_cur;
+  w.batch = state->batch;
+  w.mem = state->mem_free_mib;
+  w.grow = reinterpret_cast<int32_t *>(ws + at);
+  at += align256(sizeof(int32_t) * G);
+  w.boost = reinterpret_cast<int32_t *>(ws + at);
+  at += align256(sizeof(int32_t) * G);
+  w.taken = reinterpret_cast<unsigned long long *>(ws + at);
+  // the waves read the carried state; their commits go to the pending arrays
+  a.freq_cur = w.freq;
+  a.batch = w.batch;
+  a.mem_free = w.mem;
+  a.grow = w.grow;
+  a.boost = w.boost;
+  a.taken = w.taken;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const unsigned gblocks = (unsigned)((G + kHostBlock - 1) / kHostBlock);
+  k_wave_init<<<gblocks, kHostBlock, 0, st>>>(w, A->freq_cur, A->batch, A->mem_free_mib);
+  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  if (Q->n_requests == 0) return FESTINA_OK;
+  k_dsp_hosts<<<a.M, kHostBlock, 0, st>>>(a);
+  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  const long long per_block = (long long)kWavesPerBlock * kReqPerWave;
+  for (int32_t v = 0; v < n_waves; ++v) {
+    const int32_t lo = wave_start[v], hi = wave_start[v + 1];
+    if (hi == lo) continue;
+    a.r0 = lo;
+    a.R = hi;
+    k_dispatch<<<(unsigned)((hi - lo + per_block - 1) / per_block), kWavesPerBlock * kWave, 0, st>>>(a);
+    if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+    k_wave_commit<<<gblocks, kHostBlock, 0, st>>>(w);
+    if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
+  }
+  return FESTINA_OK;
 }

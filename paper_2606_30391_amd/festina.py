@@ -108,6 +108,10 @@ class festina_dispatches(C.Structure):
                 ("phase", C.c_void_p), ("energy_mj", C.c_void_p)]
 
 
+class festina_gpu_state(C.Structure):
+    _fields_ = [("freq_cur", C.c_void_p), ("batch", C.c_void_p), ("mem_free_mib", C.c_void_p)]
+
+
 class festina_transfer(C.Structure):
     _fields_ = [("n_gpus", C.c_int32), ("n_models", C.c_int32), ("resident", C.c_void_p),
                 ("weights_mib", C.c_void_p), ("state_mib", C.c_void_p), ("node", C.c_void_p),
@@ -134,7 +138,7 @@ EXPORTED = ("festina_abi_version", "festina_status_string", "festina_placements_
             "festina_sweep_batches", "festina_preferred_configs", "festina_ewr_workspace_bytes",
             "festina_fleet_ewr", "festina_dispatch_workspace_bytes", "festina_dispatch_requests",
             "festina_transfer_costs", "festina_request_moves", "festina_score_placements_timed",
-            "festina_score_migrations_timed")
+            "festina_score_migrations_timed", "festina_dispatch_waves_workspace_bytes", "festina_dispatch_waves")
 
 _lib = None
 
@@ -194,6 +198,12 @@ def lib():
         L.festina_dispatch_requests.argtypes = [P(festina_lut), P(festina_gpu_avail), P(festina_requests),
                                                 P(festina_dispatches), C.c_void_p, C.c_size_t, C.c_void_p]
         L.festina_dispatch_requests.restype = C.c_int
+        L.festina_dispatch_waves_workspace_bytes.argtypes = [P(festina_lut), P(festina_gpu_avail)]
+        L.festina_dispatch_waves_workspace_bytes.restype = C.c_size_t
+        L.festina_dispatch_waves.argtypes = [P(festina_lut), P(festina_gpu_avail), P(festina_requests), C.c_int32,
+                                             C.c_void_p, P(festina_gpu_state), P(festina_dispatches), C.c_void_p,
+                                             C.c_size_t, C.c_void_p]
+        L.festina_dispatch_waves.restype = C.c_int
         L.festina_transfer_costs.argtypes = [P(festina_transfer), C.c_void_p, C.c_void_p]
         L.festina_transfer_costs.restype = C.c_int
         L.festina_request_moves.argtypes = [P(festina_lut), P(festina_transfer), P(festina_plan),
@@ -478,9 +488,30 @@ class DeviceDispatch:
     def run(self, stream=None):
         festina_dispatch_requests(self.lut, self.avail, self.req, self.out, self.workspace, self.ws_bytes, stream)
 
+    def run_waves(self, wave_start, stream=None):
+        """Dispatch wave by wave (requests ordered by wave), committing each wave; the
+        carried state lands in self.state_t."""
+        import torch
+        if not hasattr(self, "state_t"):
+            dev = self.t["batch"].device
+            G, S = int(self.avail.n_gpus), int(self.avail.n_steps)
+            self.state_t = {"freq_cur": torch.empty(G, dtype=torch.int32, device=dev),
+                            "batch": torch.empty(G, dtype=torch.int32, device=dev),
+                            "mem_free_mib": torch.empty(G * S, dtype=torch.int32, device=dev)}
+            self.state = festina_gpu_state(*(_ptr(self.state_t[k]) for k in ("freq_cur", "batch", "mem_free_mib")))
+            self.wws_bytes = festina_dispatch_waves_workspace_bytes(self.lut, self.avail)
+            self.wworkspace = torch.empty(max(self.wws_bytes, 256), dtype=torch.uint8, device=dev)
+        festina_dispatch_waves(self.lut, self.avail, self.req, wave_start, self.state, self.out, self.wworkspace,
+                               self.wws_bytes, stream)
+
     def results(self):
         R = self.R
         return tuple(self.o[k][:R].cpu().numpy() for k in ("gpu", "freq_level", "sm_level", "phase", "energy_mj"))
+
+    def state_results(self):
+        G, S = int(self.avail.n_gpus), int(self.avail.n_steps)
+        return {"freq_cur": self.state_t["freq_cur"].cpu().numpy(), "batch": self.state_t["batch"].cpu().numpy(),
+                "mem_free_mib": self.state_t["mem_free_mib"].cpu().numpy().reshape(G, S)}
 
 
 class DeviceTransfer:
@@ -615,6 +646,21 @@ def festina_dispatch_requests(lut, avail, req, out, workspace, workspace_bytes, 
                                          int(workspace_bytes), _stream_handle(stream))
     if st != FESTINA_OK:
         raise FestinaError(st, "festina_dispatch_requests")
+
+
+def festina_dispatch_waves_workspace_bytes(lut, avail) -> int:
+    return int(lib().festina_dispatch_waves_workspace_bytes(C.byref(lut), C.byref(avail)))
+
+
+def festina_dispatch_waves(lut, avail, req, wave_start, state, out, workspace, workspace_bytes, stream=None) -> None:
+    """wave_start: host sequence of n_waves + 1 request offsets."""
+    ws = None if workspace is None else C.c_void_p(workspace.data_ptr())
+    bounds = np.ascontiguousarray(wave_start, dtype=np.int32)
+    st = lib().festina_dispatch_waves(C.byref(lut), C.byref(avail), C.byref(req), int(bounds.size) - 1,
+                                      bounds.ctypes.data if bounds.size else None, C.byref(state), C.byref(out), ws,
+                                      int(workspace_bytes), _stream_handle(stream))
+    if st != FESTINA_OK:
+        raise FestinaError(st, "festina_dispatch_waves")
 
 
 def festina_transfer_costs(transfer, cost, stream=None) -> None:

@@ -579,6 +579,27 @@ def make_dispatch(seed: int | None = None, n_requests: int = 65536, n_gpus: int 
             "meta": {"seed": seed, "models_per_gpu": models_per_gpu}}
 
 
+def wave_bounds(n_requests: int, n_waves: int) -> np.ndarray:
+    """Offsets of n_waves arrival waves of near-equal size over requests ordered by wave
+    (wave w holds requests bounds[w] .. bounds[w+1]-1), as the placement workloads assign
+    waves: request r arrives in wave floor(r * W / R)."""
+    R, Wn = int(n_requests), int(n_waves)
+    wave = (np.arange(R, dtype=np.int64) * Wn) // max(R, 1)
+    return np.searchsorted(wave, np.arange(Wn + 1), side="left").astype(np.int32)
+
+
+def make_dispatch_waves(seed: int | None = None, n_requests: int = 65536, n_gpus: int = 512,
+                        n_waves: int = 64) -> dict:
+    """The dispatcher workload of make_dispatch with its requests split into n_waves arrival
+    waves (configuration 4's 64 waves), for the wave-by-wave dispatch: same GPUs, tables
+    and request laws; ``wave_start`` holds the wave offsets."""
+    inp = make_dispatch(seed=seed, n_requests=n_requests, n_gpus=n_gpus)
+    ws = wave_bounds(n_requests, n_waves)
+    inp["requests"]["wave"] = (np.searchsorted(ws, np.arange(n_requests), side="right") - 1).astype(np.int32)
+    inp["wave_start"] = ws
+    return inp
+
+
 def make_tiny_dispatch(rng: np.random.Generator, R=None, G=None, M=None, NS=None, NF=None, S=None,
                        ties=False) -> dict:
     """Small random dispatch instance for pins and parity edge cases.  With ``ties`` every

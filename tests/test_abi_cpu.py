@@ -47,7 +47,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert F.festina_abi_version() == 3
+    assert F.festina_abi_version() == 4
     for s in range(5):
         assert F.festina_status_string(s)
     assert "scratch" in F.festina_status_string(F.FESTINA_ERR_TOO_LARGE)
@@ -283,6 +283,50 @@ def test_dispatch_rejects_bad_arguments(lib):
     req.model = None
     out.gpu = None
     assert call(lut, av, req, out, ws, need) == F.FESTINA_OK
+
+
+@no_gpu
+def test_dispatch_waves_rejects_bad_arguments(lib):
+    fake = C.c_void_p(0x1000)
+    L = F.lib()
+    R = 512
+
+    def structs(NS=8, NF=16, G=64, S=4):
+        lut = F.festina_lut(32, 32, NS, NF, fake, fake, fake, fake, 120.0)
+        av = F.festina_gpu_avail(G, S, *([fake] * 8), 400.0)
+        req = F.festina_requests(R, fake, None, fake, fake, fake, fake)
+        out = F.festina_dispatches(*([fake] * 5))
+        state = F.festina_gpu_state(fake, fake, fake)
+        return lut, av, req, out, state
+
+    def call(lut, av, req, out, state, bounds, ws, nbytes):
+        b = np.ascontiguousarray(bounds, np.int32)
+        return L.festina_dispatch_waves(C.byref(lut), C.byref(av), C.byref(req), b.size - 1,
+                                        b.ctypes.data if b.size else None, None if state is None else C.byref(state),
+                                        C.byref(out), ws, nbytes, None)
+
+    lut, av, req, out, state = structs()
+    need = F.festina_dispatch_waves_workspace_bytes(lut, av)
+    assert need > 0 and need % 256 == 0
+    ws = C.c_void_p(0x100000)
+    good = [0, 100, 100, 512]
+    assert call(lut, av, req, out, None, good, ws, need) == F.FESTINA_ERR_INVALID
+    for bad in ([0, 511], [1, 512], [0, 300, 200, 512], [0, 513], [], [0]):
+        assert call(lut, av, req, out, state, bad, ws, need) == F.FESTINA_ERR_INVALID, bad
+    assert L.festina_dispatch_waves(C.byref(lut), C.byref(av), C.byref(req), 2, None, C.byref(state), C.byref(out),
+                                    ws, need, None) == F.FESTINA_ERR_INVALID
+    assert call(lut, av, req, out, state, good, None, need) == F.FESTINA_ERR_INVALID
+    assert call(lut, av, req, out, state, good, ws, need - 1) == F.FESTINA_ERR_INVALID
+    assert call(lut, av, req, out, state, good, C.c_void_p(0x100008), need) == F.FESTINA_ERR_INVALID
+    assert call(*structs(NS=16, NF=17), good, ws, 1 << 30) == F.FESTINA_ERR_UNSUPPORTED
+    for obj, field, value in [("state", "freq_cur", None), ("state", "batch", None), ("state", "mem_free_mib", None),
+                              ("av", "n_gpus", 0), ("av", "n_steps", 0), ("av", "mem_free_mib", None),
+                              ("req", "model", None), ("out", "gpu", None), ("lut", "dc", None)]:
+        s = dict(zip(("lut", "av", "req", "out", "state"), structs()))
+        setattr(s[obj], field, value)
+        assert call(s["lut"], s["av"], s["req"], s["out"], s["state"], good, ws, 1 << 30) == F.FESTINA_ERR_INVALID, \
+            (obj, field)
+    assert F.festina_dispatch_waves_workspace_bytes(*structs()[:1], F.festina_gpu_avail(0, 4, *([fake] * 8), 1.0)) == 0
 
 
 @no_gpu

@@ -108,3 +108,105 @@ def test_dispatch_negative_energies():
     inp["avail"]["k_dyn_w"] = (-rng.uniform(0.0, 500.0, 60)).astype(np.float32)
     got = parity(inp, label="negative energies")
     assert np.any(got[4][got[3] == 1] < 0)
+
+
+# ------------------------------------------------------------------ wave by wave
+def run_waves(inp, ws, dd=None):
+    from paper_2606_30391_amd import festina as F
+    F.lib()
+    dd = dd or F.DeviceDispatch(inp, "cuda")
+    dd.run_waves(ws)
+    torch.cuda.synchronize()
+    return dd.results(), dd.state_results(), dd
+
+
+def wave_parity(inp, ws, label="", dd=None):
+    ws = np.asarray(ws, np.int32)
+    say(f"[gpu] wave dispatch {label}: R={inp['requests']['n_requests']} G={inp['avail']['n_gpus']} "
+        f"S={inp['avail']['n_steps']} waves={len(ws) - 1}")
+    got, st, dd = run_waves(inp, ws, dd)
+    ref, ref_st = oracle.dispatch_waves(inp, ws)
+    rep = check_dispatch(ref, got)
+    say(f"      {rep}; phases {np.bincount(got[3], minlength=4).tolist()}")
+    assert rep.ok, str(rep)
+    for k, v in ref_st.items():
+        assert np.array_equal(st[k], v), k
+    return got, st, dd
+
+
+def test_wave_dispatch_worked_example():
+    from test_oracle_dispatch_waves_pins import worked_example
+    inp, ws, exp = worked_example()
+    (g, k, j, ph, e), st, _ = run_waves(inp, ws)
+    assert (g.tolist(), k.tolist(), j.tolist(), ph.tolist()) == (exp["gpu"], exp["freq_level"], exp["sm_level"],
+                                                                  exp["phase"])
+    assert e.tolist() == [float(np.float32(x)) for x in exp["energy"]]
+    for key, v in exp["state"].items():
+        assert st[key].tolist() == v, key
+
+
+def test_wave_dispatch_workload_full_size():
+    inp = W.make_dispatch_waves()
+    got, st, _ = wave_parity(inp, inp["wave_start"], label="65536 requests, 512 GPUs, 64 waves")
+    ph = np.bincount(got[3], minlength=4)
+    assert ph[1] > 0 and ph[2] > 0 and ph[3] > 0
+    assert (st["batch"] >= inp["avail"]["batch"]).all() and (st["batch"] > inp["avail"]["batch"]).any()
+
+
+@pytest.mark.parametrize("n_waves", [1, 7, 300])
+def test_wave_dispatch_workload_seeds(n_waves):
+    inp = W.make_dispatch_waves(seed=W.DISPATCH_SEED + 300, n_requests=6000, n_gpus=256, n_waves=n_waves)
+    wave_parity(inp, inp["wave_start"], label=f"{n_waves} waves")
+
+
+@pytest.mark.parametrize("NS,NF,S", [(1, 1, 1), (3, 5, 2), (4, 8, 3), (8, 16, 9), (2, 70, 1)])
+def test_wave_dispatch_shapes_and_empty_waves(NS, NF, S):
+    rng = np.random.default_rng(1700 + NS * 100 + NF)
+    inp = W.make_tiny_dispatch(rng, R=2000, G=60, M=3, NS=NS, NF=NF, S=S)
+    cuts = np.sort(rng.integers(0, 2001, 40))
+    cuts[:3] = cuts[3]                                   # empty waves
+    wave_parity(inp, [0, *cuts.tolist(), 2000], label="shapes")
+
+
+def test_wave_dispatch_ties_and_one_request_per_wave():
+    rng = np.random.default_rng(1800)
+    inp = W.make_tiny_dispatch(rng, R=300, G=12, M=2, NS=3, NF=4, S=2, ties=True)
+    wave_parity(inp, np.arange(301), label="ties, one request per wave")
+    inp["avail"]["k_dyn_w"][:] = 0.0
+    wave_parity(inp, [0, 150, 300], label="exact ties, two waves")
+
+
+def test_wave_dispatch_repeated_calls_and_no_requests():
+    """Pending commits never leak from one call into the next; no requests: the state is the
+    caller's, copied."""
+    rng = np.random.default_rng(1900)
+    inp = W.make_tiny_dispatch(rng, R=1500, G=40, M=3, NS=4, NF=6, S=3)
+    _, _, dd = wave_parity(inp, [0, 500, 1000, 1500], label="first call")
+    wave_parity(inp, [0, 1500], label="second call, one wave", dd=dd)
+    wave_parity(inp, W.wave_bounds(1500, 11), label="third call, 11 waves", dd=dd)
+    empty = W.make_tiny_dispatch(rng, R=0, G=9, M=2, NS=2, NF=3, S=2)
+    for ws in ([0], [0, 0, 0]):
+        _, st, _ = run_waves(empty, ws)
+        for k in ("freq_cur", "batch", "mem_free_mib"):
+            assert np.array_equal(st[k], empty["avail"][k]), k
+
+
+def test_wave_dispatch_state_in_place():
+    """The carried state may be the caller's own arrays: they then end as the final state."""
+    from paper_2606_30391_amd import festina as F
+    rng = np.random.default_rng(2000)
+    inp = W.make_tiny_dispatch(rng, R=1200, G=30, M=2, NS=4, NF=5, S=2)
+    ws = W.wave_bounds(1200, 9)
+    ref, ref_st = oracle.dispatch_waves(inp, ws)
+    dd = F.DeviceDispatch(inp, "cuda")
+    state = F.festina_gpu_state(*(F._ptr(dd.t[k]) for k in ("freq_cur", "batch", "mem_free_mib")))
+    nbytes = F.festina_dispatch_waves_workspace_bytes(dd.lut, dd.avail)
+    wsp = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    F.festina_dispatch_waves(dd.lut, dd.avail, dd.req, ws, state, dd.out, wsp, nbytes)
+    torch.cuda.synchronize()
+    rep = check_dispatch(ref, dd.results())
+    assert rep.ok, str(rep)
+    G, S = inp["avail"]["n_gpus"], inp["avail"]["n_steps"]
+    assert np.array_equal(dd.t["freq_cur"].cpu().numpy(), ref_st["freq_cur"])
+    assert np.array_equal(dd.t["batch"].cpu().numpy(), ref_st["batch"])
+    assert np.array_equal(dd.t["mem_free_mib"].cpu().numpy().reshape(G, S), ref_st["mem_free_mib"])
