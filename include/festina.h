@@ -436,8 +436,9 @@ size_t festina_dispatch_waves_workspace_bytes(const festina_lut *lut, const fest
  * one that admitted it (a step left short reads -1 MiB); a phase-2 (F_max) placement leaves
  * the GPU at the top frequency level.  Profile times, free SM levels, k and residency stay
  * as given; a scale-out (phase 3) commits nothing.  Workspace from
- * festina_dispatch_waves_workspace_bytes (256-byte aligned, clobbered).  2 + 2 x (non-empty
- * waves) kernel launches on `stream`, nothing allocated or synchronised. */
+ * festina_dispatch_waves_workspace_bytes (256-byte aligned, clobbered).  One kernel launch
+ * per non-empty wave plus three (two without requests) on `stream`, nothing allocated or
+ * synchronised. */
 festina_status festina_dispatch_waves(const festina_lut *lut, const festina_gpu_avail *avail,
                                       const festina_requests *req, int32_t n_waves, const int32_t *wave_start,
                                       festina_gpu_state *state, festina_dispatches *out, void *workspace,

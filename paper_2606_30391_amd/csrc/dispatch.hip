@@ -41,6 +41,18 @@ constexpr int kHostBlock = 256;
 constexpr int kMaxSteps = 8;                 // profile steps loaded at once
 constexpr double kStability = 0.02;          // energies within 2% of the least tie
 
+// One wave's commits: requests placed per GPU, F_max placements per GPU, and the MiB taken
+// from each profile step (a request admitted at step s counts at s and at every later step).
+struct Commits {
+  int32_t *grow, *boost;             // [G]
+  unsigned long long *taken;         // [G][S]
+};
+
+// The GPUs' state that a wave-by-wave call carries: current level, batch, free memory.
+struct State {
+  int32_t *freq, *batch, *mem;       // [G], [G], [G][S]
+};
+
 struct DspArgs {
   int32_t M, NS, NF, C, words;
   const float *sm_level, *freq_level, *pf, *dc;
@@ -62,18 +74,12 @@ struct DspArgs {
   int4 *hrec;                        // workspace: [M][G][4] host records when S <= 4
   int32_t packed;
   int32_t r0;                        // first request of the launch (a.R: one past the last)
-  // wave commits (null when not committing): placements per GPU, MiB taken per (GPU,
-  // admitting step), F_max placements per GPU
-  int32_t *grow, *boost;
-  unsigned long long *taken;
-};
-
-// The state a wave-by-wave call carries from one wave to the next, and its pending commits.
-struct WaveState {
-  int32_t G, S, top;
-  int32_t *freq, *batch, *mem;       // [G], [G], [G][S]
-  int32_t *grow, *boost;             // [G]
-  unsigned long long *taken;         // [G][S]
+  // Wave-by-wave calls only (the kWaves kernels): the state this wave sees is (freq_cur,
+  // batch, mem_free) with the previous wave's commits `prev` applied.  The launch also
+  // writes that state to `fold` (the next wave's freq_cur, batch, mem_free), commits this
+  // wave's placements to `cur`, and clears `next` (the commits of the wave after).
+  Commits prev, cur, next;
+  State fold;
 };
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -142,17 +148,36 @@ struct Point {
   int sm, mem, b;
 };
 
+// GPU g's state as the launch sees it: the stored one, and in a wave-by-wave call with
+// the previous wave's commits applied (batch grown, level boosted, memory taken; a step
+// left short of memory reads -1 MiB).
+template <bool kWaves>
+__device__ __forceinline__ int view_batch(const DspArgs &a, int g) {
+  return kWaves ? a.batch[g] + a.prev.grow[g] : a.batch[g];
+}
+template <bool kWaves>
+__device__ __forceinline__ int view_freq(const DspArgs &a, int g) {
+  return (kWaves && a.prev.boost[g]) ? a.NF - 1 : a.freq_cur[g];
+}
+template <bool kWaves>
+__device__ __forceinline__ int view_mem(const DspArgs &a, size_t at) {
+  if (!kWaves) return a.mem_free[at];
+  const long long v = (long long)a.mem_free[at] - (long long)a.prev.taken[at];
+  return v < -1 ? -1 : (int)v;
+}
+
 // Phase One for host g: first profile step whose free memory holds `need` KiB.
+template <bool kWaves>
 __device__ __forceinline__ Point host_point(const DspArgs &a, int g, long long need) {
   Point p{0, 0.0, -1, 0, 1};
-  const int B = a.batch[g];
+  const int B = view_batch<kWaves>(a, g);
   if (B < 0) return p;
   p.b = B + 1 > kRows ? kRows : B + 1;
   const size_t base = (size_t)g * a.S;
   if (a.S <= kMaxSteps) {
     int mem[kMaxSteps];
 #pragma unroll
-    for (int s = 0; s < kMaxSteps; ++s) mem[s] = s < a.S ? a.mem_free[base + s] : 0;
+    for (int s = 0; s < kMaxSteps; ++s) mem[s] = s < a.S ? view_mem<kWaves>(a, base + s) : 0;
     int st = -1;
 #pragma unroll
     for (int s = kMaxSteps - 1; s >= 0; --s)
@@ -161,17 +186,21 @@ __device__ __forceinline__ Point host_point(const DspArgs &a, int g, long long n
     p.ok = 1;
     p.ta = (double)a.t_avail[base + st];
     p.sm = a.sm_free[base + st];
-    p.mem = a.mem_free[base + st];
+#pragma unroll
+    for (int s = 0; s < kMaxSteps; ++s)
+      if (s == st) p.mem = mem[s];
     return p;
   }
-  for (int s = 0; s < a.S; ++s)
-    if ((long long)a.mem_free[base + s] * 1024 >= need) {
+  for (int s = 0; s < a.S; ++s) {
+    const int mem = view_mem<kWaves>(a, base + s);
+    if ((long long)mem * 1024 >= need) {
       p.ok = 1;
       p.ta = (double)a.t_avail[base + s];
       p.sm = a.sm_free[base + s];
-      p.mem = a.mem_free[base + s];
+      p.mem = mem;
       return p;
     }
+  }
   return p;
 }
 
@@ -182,9 +211,10 @@ struct Host {
 };
 
 // Phase One inputs of host number h of model m: from the packed record, or gathered.
+template <bool kWaves>
 __device__ __forceinline__ Host load_host(const DspArgs &a, int m, int h, const int *hl, long long need) {
   Host o;
-  if (a.packed) {
+  if (!kWaves && a.packed) {
     const v4i *rec = reinterpret_cast<const v4i *>(a.hrec + ((size_t)m * a.G + h) * 4);
     const v4i r0 = rec[0], mem = rec[1], tt = rec[2], sm = rec[3];
     __builtin_amdgcn_sched_barrier(0);   // the four loads in flight together, before any test
@@ -205,9 +235,9 @@ __device__ __forceinline__ Host load_host(const DspArgs &a, int m, int h, const 
     return o;
   }
   o.g = hl[h];
-  o.kcur = a.freq_cur[o.g];
+  o.kcur = view_freq<kWaves>(a, o.g);
   o.kd = (double)a.kdyn[o.g];
-  o.p = host_point(a, o.g, need);
+  o.p = host_point<kWaves>(a, o.g, need);
   return o;
 }
 
@@ -237,19 +267,38 @@ __device__ __forceinline__ unsigned long long stability_key(int mem, int sm, int
          (unsigned long long)(0xffffffu - (unsigned)g);
 }
 
-constexpr int kGroup = 16;                       // lanes per request
-constexpr int kReqPerWave = kWave / kGroup;
+// Lanes per request: 16 (four requests per wavefront) when a launch holds enough requests
+// to fill the GPU, else 64, so that a request's hosts take one round of loads, not four.
+constexpr int kGroupWide = 64;
+constexpr int kWideRequests = 8192;              // at most this many requests: 64 lanes each
 constexpr int kCached = 4;                       // hosts per lane whose Phase One result stays in registers
 
+template <int kGroup>
 __device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int off) {
   const unsigned lo = __shfl_xor((unsigned)v, off, kGroup), hi = __shfl_xor((unsigned)(v >> 32), off, kGroup);
   return ((unsigned long long)hi << 32) | lo;
 }
 
-// Four requests per wavefront, 16 lanes each; lane s of a request strides over its
-// model's hosts (s, s + 16, ...), all reductions stay inside the 16-lane group.
+// kGroup lanes per request (64 / kGroup requests per wavefront); lane s of a request strides
+// over its model's hosts (s, s + kGroup, ...), all reductions stay inside the group.
+template <int kGroup, bool kWaves>
 __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) {
 #pragma clang fp contract(off)
+  constexpr int kReqPerWave = kWave / kGroup;
+  if (kWaves) {
+    // the state this wave sees, stored for the next wave; the commits after that cleared
+    for (int g = blockIdx.x * blockDim.x + threadIdx.x; g < a.G; g += gridDim.x * blockDim.x) {
+      a.fold.batch[g] = view_batch<true>(a, g);
+      a.fold.freq[g] = view_freq<true>(a, g);
+      a.next.grow[g] = 0;
+      a.next.boost[g] = 0;
+      for (int s = 0; s < a.S; ++s) {
+        const size_t at = (size_t)g * a.S + s;
+        a.fold.mem[at] = view_mem<true>(a, at);
+        a.next.taken[at] = 0ull;
+      }
+    }
+  }
   const int lane = threadIdx.x & (kWave - 1);
   const int sub = lane & (kGroup - 1);
   const int r = a.r0 + (blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kReqPerWave + lane / kGroup;
@@ -279,7 +328,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       kc[i] = 0ull;
     }
     for (int i = 0, h = sub; h < nh; ++i, h += kGroup) {
-      const Host H = load_host(a, m, h, hl, need);
+      const Host H = load_host<kWaves>(a, m, h, hl, need);
       const int g = H.g;
       const Point &p = H.p;
       double e;
@@ -305,7 +354,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
           ebest = ec[c];
         }
       for (int h = sub + kCached * kGroup; h < nh; h += kGroup) {   // hosts past the cached ones
-        const Host H = load_host(a, m, h, hl, need);
+        const Host H = load_host<kWaves>(a, m, h, hl, need);
         const int g = H.g;
         const Point &p = H.p;
         double e;
@@ -318,14 +367,14 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       }
       unsigned long long wbest = best;
       for (int off = kGroup / 2; off >= 1; off >>= 1) {
-        const unsigned long long o = shfl_xor_u64(wbest, off);
+        const unsigned long long o = shfl_xor_u64<kGroup>(wbest, off);
         wbest = o > wbest ? o : wbest;
       }
       if (wbest != 0ull) {                 // the least-energy host is always within the bound
         writer = best == wbest;            // exactly one lane of the group holds the winning key
         gsel = (int)(0xffffffu - (unsigned)(wbest & 0xffffffull));
         jsel = (int)((wbest >> 24) & 0xffull);
-        ksel = a.freq_cur[gsel];        // the winner's current level
+        ksel = view_freq<kWaves>(a, gsel);   // the winner's current level
         phase = 1;
         esel = ebest;
       }
@@ -335,7 +384,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       int bg = INT_MAX, bsm = -1;
       double bt = inf, be = inf;
       for (int h = sub; h < nh; h += kGroup) {
-        const Host H = load_host(a, m, h, hl, need);
+        const Host H = load_host<kWaves>(a, m, h, hl, need);
         const int g = H.g;
         const Point &p = H.p;
         double e;
@@ -397,54 +446,46 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
     a.out_sm[r] = jsel;
     a.out_phase[r] = (uint8_t)phase;
     a.out_energy[r] = (float)esel;
-    if (a.grow && (phase == 1 || phase == 2)) {
+    if (kWaves && (phase == 1 || phase == 2)) {
       // commit to the chosen GPU: one more request in its batch, and ceil(Req_mem / 1024)
       // MiB from the step that admitted it (the first whose free memory holds Req_mem) on
-      const int32_t *mf = a.mem_free + (size_t)gsel * a.S;
+      const size_t base = (size_t)gsel * a.S;
       int st = 0;
-      while (st < a.S - 1 && (long long)mf[st] * 1024 < need) ++st;
-      atomicAdd(&a.grow[gsel], 1);
-      atomicAdd(&a.taken[(size_t)gsel * a.S + st], (unsigned long long)((need + 1023) / 1024));
-      if (phase == 2) a.boost[gsel] = 1;
+      while (st < a.S - 1 && (long long)view_mem<true>(a, base + st) * 1024 < need) ++st;
+      const unsigned long long q = (unsigned long long)((need + 1023) / 1024);
+      atomicAdd(&a.cur.grow[gsel], 1);
+      for (int s = st; s < a.S; ++s) atomicAdd(&a.cur.taken[base + s], q);
+      if (phase == 2) a.cur.boost[gsel] = 1;
     }
   }
 }
 
-// Start of a wave-by-wave call: the caller's state copied into the carried state (the two
-// may be the same arrays), no commit pending.
-__global__ void __launch_bounds__(kHostBlock) k_wave_init(WaveState w, const int32_t *freq0, const int32_t *batch0,
+// Start of a wave-by-wave call: the caller's state copied into the first state buffer, the
+// commit buffers of the first two waves and of the "wave before the first" cleared.
+__global__ void __launch_bounds__(kHostBlock) k_wave_init(int32_t G, int32_t S, State s0, Commits d0, Commits d1,
+                                                          Commits d2, const int32_t *freq0, const int32_t *batch0,
                                                           const int32_t *mem0) {
   const int g = blockIdx.x * kHostBlock + threadIdx.x;
-  if (g >= w.G) return;
-  w.freq[g] = freq0[g];
-  w.batch[g] = batch0[g];
-  w.grow[g] = 0;
-  w.boost[g] = 0;
-  for (int s = 0; s < w.S; ++s) {
-    w.mem[(size_t)g * w.S + s] = mem0[(size_t)g * w.S + s];
-    w.taken[(size_t)g * w.S + s] = 0ull;
+  if (g >= G) return;
+  s0.freq[g] = freq0[g];
+  s0.batch[g] = batch0[g];
+  d0.grow[g] = d1.grow[g] = d2.grow[g] = 0;
+  d0.boost[g] = d1.boost[g] = d2.boost[g] = 0;
+  for (int s = 0; s < S; ++s) {
+    const size_t at = (size_t)g * S + s;
+    s0.mem[at] = mem0[at];
+    d0.taken[at] = d1.taken[at] = d2.taken[at] = 0ull;
   }
 }
 
-// End of a wave: each GPU applies its pending commits (batch, boost, and the MiB taken from
-// every step at or after the admitting ones; a step short of memory reads -1) and clears them.
-__global__ void __launch_bounds__(kHostBlock) k_wave_commit(WaveState w) {
+// End of a wave-by-wave call: the last state with the last wave's commits applied, into
+// the caller's arrays.
+__global__ void __launch_bounds__(kHostBlock) k_wave_final(DspArgs a, State out) {
   const int g = blockIdx.x * kHostBlock + threadIdx.x;
-  if (g >= w.G) return;
-  w.batch[g] += w.grow[g];
-  w.grow[g] = 0;
-  if (w.boost[g]) {
-    w.freq[g] = w.top;
-    w.boost[g] = 0;
-  }
-  unsigned long long run = 0ull;
-  for (int s = 0; s < w.S; ++s) {
-    const size_t at = (size_t)g * w.S + s;
-    run += w.taken[at];
-    w.taken[at] = 0ull;
-    const long long v = (long long)w.mem[at] - (long long)run;
-    w.mem[at] = v < -1 ? -1 : (int32_t)v;
-  }
+  if (g >= a.G) return;
+  out.batch[g] = view_batch<true>(a, g);
+  out.freq[g] = view_freq<true>(a, g);
+  for (int s = 0; s < a.S; ++s) out.mem[(size_t)g * a.S + s] = view_mem<true>(a, (size_t)g * a.S + s);
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -465,6 +506,22 @@ extern "C" size_t festina_dispatch_workspace_bytes(const festina_lut *L, const f
   size_t bytes = align256(sizeof(int32_t) * L->n_models) + align256(sizeof(int32_t) * (size_t)L->n_models * A->n_gpus);
   if (A->n_steps <= 4) bytes += align256((size_t)64 * L->n_models * A->n_gpus);     // host records
   return bytes;
+}
+
+// k_dispatch over requests lo .. hi-1, with the group width their number calls for.
+template <bool kWaves>
+static festina_status launch_dispatch(DspArgs a, int32_t lo, int32_t hi, hipStream_t st) {
+  a.r0 = lo;
+  a.R = hi;
+  const long long n = (long long)hi - lo;
+  if (n <= kWideRequests) {
+    const long long per_block = (long long)kWavesPerBlock * (kWave / kGroupWide);
+    k_dispatch<kGroupWide, kWaves><<<(unsigned)((n + per_block - 1) / per_block), kWavesPerBlock * kWave, 0, st>>>(a);
+  } else {
+    const long long per_block = (long long)kWavesPerBlock * (kWave / 16);
+    k_dispatch<16, kWaves><<<(unsigned)((n + per_block - 1) / per_block), kWavesPerBlock * kWave, 0, st>>>(a);
+  }
+  return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
 }
 
 // Checks the arguments common to both dispatch calls; fills everything but the workspace.
@@ -515,8 +572,8 @@ static festina_status dsp_args(const festina_lut *L, const festina_gpu_avail *A,
   a.out_phase = out->phase;
   a.out_energy = out->energy_mj;
   a.r0 = 0;
-  a.grow = a.boost = nullptr;
-  a.taken = nullptr;
+  a.prev = a.cur = a.next = Commits{nullptr, nullptr, nullptr};
+  a.fold = State{nullptr, nullptr, nullptr};
   a.packed = 0;
   a.hrec = nullptr;
   return FESTINA_OK;
@@ -540,17 +597,22 @@ extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const 
   hipStream_t st = static_cast<hipStream_t>(stream);
   k_dsp_hosts<<<a.M, kHostBlock, 0, st>>>(a);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  const long long per_block = (long long)kWavesPerBlock * kReqPerWave;
-  const long long blocks = ((long long)a.R + per_block - 1) / per_block;
-  k_dispatch<<<(unsigned)blocks, kWavesPerBlock * kWave, 0, st>>>(a);
-  return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
+  return launch_dispatch<false>(a, 0, a.R, st);
+}
+
+// Workspace of a wave-by-wave call: host counts and lists, two state buffers (the state
+// each wave sees alternates between them) and three commit buffers (the previous wave's,
+// read; the current wave's, written; the next wave's, cleared).
+static size_t state_bytes(size_t G, size_t S) { return 2 * align256(sizeof(int32_t) * G) + align256(sizeof(int32_t) * G * S); }
+static size_t commit_bytes(size_t G, size_t S) {
+  return 2 * align256(sizeof(int32_t) * G) + align256(sizeof(unsigned long long) * G * S);
 }
 
 extern "C" size_t festina_dispatch_waves_workspace_bytes(const festina_lut *L, const festina_gpu_avail *A) {
   if (!dsp_shapes_ok(L, A)) return 0;
-  const size_t G = (size_t)A->n_gpus;
+  const size_t G = (size_t)A->n_gpus, S = (size_t)A->n_steps;
   return align256(sizeof(int32_t) * L->n_models) + align256(sizeof(int32_t) * (size_t)L->n_models * G) +
-         2 * align256(sizeof(int32_t) * G) + align256(sizeof(unsigned long long) * G * A->n_steps);
+         2 * state_bytes(G, S) + 3 * commit_bytes(G, S);
 }
 
 extern "C" festina_status festina_dispatch_waves(const festina_lut *L, const festina_gpu_avail *A,
@@ -571,49 +633,57 @@ extern "C" festina_status festina_dispatch_waves(const festina_lut *L, const fes
   }
   const size_t need = festina_dispatch_waves_workspace_bytes(L, A);
   if (!workspace || workspace_bytes < need || (((uintptr_t)workspace) & 255) != 0) return FESTINA_ERR_INVALID;
-  const size_t G = (size_t)A->n_gpus;
+  const size_t G = (size_t)A->n_gpus, S = (size_t)A->n_steps;
   char *ws = static_cast<char *>(workspace);
   size_t at = 0;
-  a.host_cnt = reinterpret_cast<int32_t *>(ws + at);
-  at += align256(sizeof(int32_t) * L->n_models);
-  a.host_list = reinterpret_cast<int32_t *>(ws + at);
-  at += align256(sizeof(int32_t) * (size_t)L->n_models * G);
-  WaveState w;
-  w.G = A->n_gpus;
-  w.S = A->n_steps;
-  w.top = L->n_freq - 1;
-  w.freq = state->freq_cur;
-  w.batch = state->batch;
-  w.mem = state->mem_free_mib;
-  w.grow = reinterpret_cast<int32_t *>(ws + at);
-  at += align256(sizeof(int32_t) * G);
-  w.boost = reinterpret_cast<int32_t *>(ws + at);
-  at += align256(sizeof(int32_t) * G);
-  w.taken = reinterpret_cast<unsigned long long *>(ws + at);
-  // the waves read the carried state; their commits go to the pending arrays
-  a.freq_cur = w.freq;
-  a.batch = w.batch;
-  a.mem_free = w.mem;
-  a.grow = w.grow;
-  a.boost = w.boost;
-  a.taken = w.taken;
+  auto take = [&](size_t bytes) {
+    char *p = ws + at;
+    at += align256(bytes);
+    return p;
+  };
+  a.host_cnt = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * L->n_models));
+  a.host_list = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (size_t)L->n_models * G));
+  State sb[2];
+  for (State &x : sb) {
+    x.freq = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G));
+    x.batch = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G));
+    x.mem = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G * S));
+  }
+  Commits db[3];
+  for (Commits &x : db) {
+    x.grow = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G));
+    x.boost = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G));
+    x.taken = reinterpret_cast<unsigned long long *>(take(sizeof(unsigned long long) * G * S));
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   const unsigned gblocks = (unsigned)((G + kHostBlock - 1) / kHostBlock);
-  k_wave_init<<<gblocks, kHostBlock, 0, st>>>(w, A->freq_cur, A->batch, A->mem_free_mib);
+  k_wave_init<<<gblocks, kHostBlock, 0, st>>>(A->n_gpus, A->n_steps, sb[0], db[0], db[1], db[2], A->freq_cur,
+                                              A->batch, A->mem_free_mib);
   if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  if (Q->n_requests == 0) return FESTINA_OK;
-  k_dsp_hosts<<<a.M, kHostBlock, 0, st>>>(a);
-  if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-  const long long per_block = (long long)kWavesPerBlock * kReqPerWave;
-  for (int32_t v = 0; v < n_waves; ++v) {
-    const int32_t lo = wave_start[v], hi = wave_start[v + 1];
-    if (hi == lo) continue;
-    a.r0 = lo;
-    a.R = hi;
-    k_dispatch<<<(unsigned)((hi - lo + per_block - 1) / per_block), kWavesPerBlock * kWave, 0, st>>>(a);
-    if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
-    k_wave_commit<<<gblocks, kHostBlock, 0, st>>>(w);
+  if (Q->n_requests > 0) {
+    k_dsp_hosts<<<a.M, kHostBlock, 0, st>>>(a);
     if (hipGetLastError() != hipSuccess) return FESTINA_ERR_DEVICE;
   }
-  return FESTINA_OK;
+  // Launch v (of the non-empty waves) sees sb[v % 2] with db[(v + 2) % 3] applied, stores
+  // that in sb[(v + 1) % 2], commits to db[v % 3] and clears db[(v + 1) % 3].
+  int v = 0;
+  for (int32_t w = 0; w < n_waves; ++w) {
+    const int32_t lo = wave_start[w], hi = wave_start[w + 1];
+    if (hi == lo) continue;
+    a.freq_cur = sb[v % 2].freq;
+    a.batch = sb[v % 2].batch;
+    a.mem_free = sb[v % 2].mem;
+    a.prev = db[(v + 2) % 3];
+    a.cur = db[v % 3];
+    a.next = db[(v + 1) % 3];
+    a.fold = sb[(v + 1) % 2];
+    if (launch_dispatch<true>(a, lo, hi, st) != FESTINA_OK) return FESTINA_ERR_DEVICE;
+    ++v;
+  }
+  a.freq_cur = sb[v % 2].freq;
+  a.batch = sb[v % 2].batch;
+  a.mem_free = sb[v % 2].mem;
+  a.prev = db[(v + 2) % 3];
+  k_wave_final<<<gblocks, kHostBlock, 0, st>>>(a, State{state->freq_cur, state->batch, state->mem_free_mib});
+  return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
 }

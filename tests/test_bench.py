@@ -73,7 +73,7 @@ def test_short_run_prints_one_line_with_the_contract_fields():
     for row in ("sweep", "preferred", "dispatch", "transfer"):
         assert row in b["next_rows"] and b["next_rows"][row]["roofline"]["frac"] > 0
     wv = b["next_rows"]["dispatch_waves"]
-    assert wv["waves"] == 64 and wv["launches"] == 130 and wv["call_ms"] > 0
+    assert wv["waves"] == 64 and wv["launches"] == 67 and wv["call_ms"] > 0
     if wv["cpu_baseline"] is not None:
         assert wv["cpu_baseline"]["agreement"]["all_outputs_equal"] == 1.0
         assert wv["cpu_baseline"]["agreement"]["final_state_equal"]
