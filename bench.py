@@ -70,6 +70,7 @@ SWEEP_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "sweep.hip")
 TRANSFER_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_transfer_costs_traffic.json")
 TRANSFER_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "transfer.hip")
 DISPATCH_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_dispatch_traffic.json")
+DISPATCH_WAVES_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_dispatch_waves_traffic.json")
 MIGRATE_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_migrate_traffic.json")
 DISPATCH_SRC = os.path.join(ROOT, "paper_2606_30391_amd", "csrc", "dispatch.hip")
 PREFERRED_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_preferred_traffic.json")
@@ -332,12 +333,24 @@ def dispatch_waves_row(F, W, hip, torch, with_cpu, calls=100, warmup=5):
     ms = timed_calls(hip, torch, lambda: dd.run_waves(ws), calls, warmup)
     R, G, n_waves = inp["requests"]["n_requests"], inp["avail"]["n_gpus"], len(ws) - 1
     launches = 3 + int(np.count_nonzero(np.diff(ws)))
+    lut, av = inp["lut"], inp["avail"]
+    M, S = lut["n_models"], av["n_steps"]
+    per_wave = R // n_waves
+    # per wave launch: its requests' fields and results, the carried state and the previous
+    # wave's commits read once, the folded state written and the next commits cleared, the
+    # two tables once
+    nbytes = per_wave * (5 * 4 + 3 * 4 + 1 + 4) + G * (4 + 4 * ((M + 31) // 32) + 8 * S) \
+        + 2 * G * ((8 + 4 * S) + (8 + 8 * S)) + M * 4 + 2 * lut["pf"].nbytes
+    wave_ms = ms / n_waves
     row = {
         "workload": ("paper's current-frequency dispatcher over arrival waves: 65536 requests in 64 waves of 1024, "
                      "512 GPUs, each wave committed before the next"),
         "requests": R, "waves": n_waves, "launches": launches, "call_ms": ms, "requests_per_s": R / (ms * 1e-3),
         "us_per_wave": ms * 1e3 / n_waves,
-        "bound": "launch: one kernel per wave (1024 requests), each shorter than a launch's own cost",
+        "roofline": {"kernel": "k_dispatch (one wave)", "bound": "hbm", "achieved": nbytes / (wave_ms * 1e-3) / 1e9,
+                     "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": nbytes / (wave_ms * 1e-3) / HBM_PEAK,
+                     "traffic": load_traffic(DISPATCH_WAVES_TRAFFIC_FILE, DISPATCH_SRC), "algorithmic_bytes": nbytes,
+                     "note": "latency-bound: a chain of dependent loads and a launch per wave"},
         "cpu_baseline": None,
     }
     if with_cpu:

@@ -704,6 +704,11 @@ static int or_point_ok(const or_lut *L, const or_requests *Q, int r, int m, int 
   return 1;
 }
 
+/* Req_mem in KiB: the model's KV cache per token times the prompt and the padded output. */
+static int64_t or_request_kib(const or_avail *A, const or_requests *Q, int r) {
+  return (int64_t)A->kv_kib_per_token[Q->model[r]] * ((int64_t)Q->prompt_tokens[r] + or_padded_out(Q->pred_out_tokens[r]));
+}
+
 static void or_dispatch_one(const or_lut *L, const or_avail *A, const or_requests *Q, int r, or_dispatch *o) {
   o->gpu = o->freq_level = o->sm_level = -1;
   o->phase = 0;
@@ -712,7 +717,7 @@ static void or_dispatch_one(const or_lut *L, const or_avail *A, const or_request
   if (m < 0 || m >= L->n_models || Q->pred_out_tokens[r] < 0) return;
   const int prow = or_prompt_row(Q->prompt_tokens[r]);
   if (prow == -2) return;
-  const int64_t need = (int64_t)A->kv_kib_per_token[m] * ((int64_t)Q->prompt_tokens[r] + or_padded_out(Q->pred_out_tokens[r]));
+  const int64_t need = or_request_kib(A, Q, r);
   /* Phase One and the least energy */
   double emin = INFINITY;
   int any = 0;
@@ -856,8 +861,7 @@ int festina_oracle_dispatch_waves(const or_lut *L, const or_avail *A, const or_r
     for (int32_t r = wave_start[w]; r < wave_start[w + 1]; ++r) {
       const int g = out[r].gpu;
       if (out[r].phase != 1 && out[r].phase != 2) continue;
-      const int m = Q->model[r];
-      const int64_t need = (int64_t)A->kv_kib_per_token[m] * ((int64_t)Q->prompt_tokens[r] + or_padded_out(Q->pred_out_tokens[r]));
+      const int64_t need = or_request_kib(A, Q, r);
       int first = 0;                /* the admitting step: the first whose memory holds Req_mem */
       while ((int64_t)snap[(size_t)g * S + first] * 1024 < need) ++first;
       for (int s = first; s < S; ++s) taken[(size_t)g * S + s] += (need + 1023) / 1024;

@@ -103,6 +103,19 @@ def test_dispatch_call_in_a_graph():
     _replay_matches_eager(d.run, d.results, list(d.o.values()), "dispatcher")
 
 
+def test_wave_dispatch_call_in_a_graph():
+    from paper_2606_30391_amd import festina as F
+    inp = W.make_dispatch_waves()
+    d = F.DeviceDispatch(inp, "cuda")
+
+    def results():
+        return list(d.results()) + _flat(d.state_results())
+
+    d.run_waves(inp["wave_start"])                # sizes the state and workspace before capture
+    _replay_matches_eager(lambda: d.run_waves(inp["wave_start"]), results,
+                          list(d.o.values()) + list(d.state_t.values()), "dispatcher over 64 waves")
+
+
 def test_transfer_calls_in_a_graph():
     from paper_2606_30391_amd import festina as F
     d = F.DeviceTransfer(W.make_transfer(), "cuda")
