@@ -41,17 +41,14 @@ constexpr int kHostBlock = 256;
 constexpr int kMaxSteps = 8;                 // profile steps loaded at once
 constexpr double kStability = 0.02;          // energies within 2% of the least tie
 
-// One wave's commits: requests placed per GPU, F_max placements per GPU, and the MiB taken
-// from each profile step (a request admitted at step s counts at s and at every later step).
-struct Commits {
-  int32_t *grow, *boost;             // [G]
-  unsigned long long *taken;         // [G][S]
-};
-
-// The GPUs' state that a wave-by-wave call carries: current level, batch, free memory.
-struct State {
-  int32_t *freq, *batch, *mem;       // [G], [G], [G][S]
-};
+// Wave-by-wave calls keep two kinds of buffers in the workspace, each one allocation:
+//   state   int32 [G][2] (current level, batch) then int32 [G][S] free MiB per profile step;
+//   commits uint64 [G] (requests placed in the low 32 bits, bit 32 set by an F_max
+//           placement) then uint64 [G][S] MiB taken per step (a request admitted at step s
+//           counts at s and at every later step).
+__device__ __forceinline__ int2 *state_fb(int32_t *st) { return reinterpret_cast<int2 *>(st); }
+__device__ __forceinline__ int32_t *state_mem(int32_t *st, int G) { return st + 2 * (size_t)G; }
+__device__ __forceinline__ unsigned long long *commit_taken(unsigned long long *c, int G) { return c + G; }
 
 struct DspArgs {
   int32_t M, NS, NF, C, words;
@@ -74,12 +71,12 @@ struct DspArgs {
   int4 *hrec;                        // workspace: [M][G][4] host records when S <= 4
   int32_t packed;
   int32_t r0;                        // first request of the launch (a.R: one past the last)
-  // Wave-by-wave calls only (the kWaves kernels): the state this wave sees is (freq_cur,
-  // batch, mem_free) with the previous wave's commits `prev` applied.  The launch also
-  // writes that state to `fold` (the next wave's freq_cur, batch, mem_free), commits this
-  // wave's placements to `cur`, and clears `next` (the commits of the wave after).
-  Commits prev, cur, next;
-  State fold;
+  // Wave-by-wave calls only (the kWaves kernels): the state this wave sees is `wstate` with
+  // the previous wave's commits `wprev` applied (freq_cur, batch and mem_free are unused).
+  // The launch also writes that state to `wfold` (the next wave's state), commits this
+  // wave's placements to `wcur`, and clears `wnext` (the commits of the wave after).
+  int32_t *wstate, *wfold;
+  unsigned long long *wprev, *wcur, *wnext;
 };
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -153,16 +150,18 @@ struct Point {
 // left short of memory reads -1 MiB).
 template <bool kWaves>
 __device__ __forceinline__ int view_batch(const DspArgs &a, int g) {
-  return kWaves ? a.batch[g] + a.prev.grow[g] : a.batch[g];
+  if (!kWaves) return a.batch[g];
+  return state_fb(a.wstate)[g].y + (int)(uint32_t)a.wprev[g];
 }
 template <bool kWaves>
 __device__ __forceinline__ int view_freq(const DspArgs &a, int g) {
-  return (kWaves && a.prev.boost[g]) ? a.NF - 1 : a.freq_cur[g];
+  if (!kWaves) return a.freq_cur[g];
+  return (a.wprev[g] >> 32) ? a.NF - 1 : state_fb(a.wstate)[g].x;
 }
 template <bool kWaves>
-__device__ __forceinline__ int view_mem(const DspArgs &a, size_t at) {
-  if (!kWaves) return a.mem_free[at];
-  const long long v = (long long)a.mem_free[at] - (long long)a.prev.taken[at];
+__device__ __forceinline__ int view_mem(const DspArgs &a, int g, int s) {
+  if (!kWaves) return a.mem_free[(size_t)g * a.S + s];
+  const long long v = (long long)state_mem(a.wstate, a.G)[(size_t)g * a.S + s] - (long long)commit_taken(a.wprev, a.G)[(size_t)g * a.S + s];
   return v < -1 ? -1 : (int)v;
 }
 
@@ -177,7 +176,7 @@ __device__ __forceinline__ Point host_point(const DspArgs &a, int g, long long n
   if (a.S <= kMaxSteps) {
     int mem[kMaxSteps];
 #pragma unroll
-    for (int s = 0; s < kMaxSteps; ++s) mem[s] = s < a.S ? view_mem<kWaves>(a, base + s) : 0;
+    for (int s = 0; s < kMaxSteps; ++s) mem[s] = s < a.S ? view_mem<kWaves>(a, g, s) : 0;
     int st = -1;
 #pragma unroll
     for (int s = kMaxSteps - 1; s >= 0; --s)
@@ -192,7 +191,7 @@ __device__ __forceinline__ Point host_point(const DspArgs &a, int g, long long n
     return p;
   }
   for (int s = 0; s < a.S; ++s) {
-    const int mem = view_mem<kWaves>(a, base + s);
+    const int mem = view_mem<kWaves>(a, g, s);
     if ((long long)mem * 1024 >= need) {
       p.ok = 1;
       p.ta = (double)a.t_avail[base + s];
@@ -288,14 +287,12 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
   if (kWaves) {
     // the state this wave sees, stored for the next wave; the commits after that cleared
     for (int g = blockIdx.x * blockDim.x + threadIdx.x; g < a.G; g += gridDim.x * blockDim.x) {
-      a.fold.batch[g] = view_batch<true>(a, g);
-      a.fold.freq[g] = view_freq<true>(a, g);
-      a.next.grow[g] = 0;
-      a.next.boost[g] = 0;
+      state_fb(a.wfold)[g] = make_int2(view_freq<true>(a, g), view_batch<true>(a, g));
+      a.wnext[g] = 0ull;
       for (int s = 0; s < a.S; ++s) {
         const size_t at = (size_t)g * a.S + s;
-        a.fold.mem[at] = view_mem<true>(a, at);
-        a.next.taken[at] = 0ull;
+        state_mem(a.wfold, a.G)[at] = view_mem<true>(a, g, s);
+        commit_taken(a.wnext, a.G)[at] = 0ull;
       }
     }
   }
@@ -451,41 +448,39 @@ __global__ void __launch_bounds__(kWavesPerBlock * kWave) k_dispatch(DspArgs a) 
       // MiB from the step that admitted it (the first whose free memory holds Req_mem) on
       const size_t base = (size_t)gsel * a.S;
       int st = 0;
-      while (st < a.S - 1 && (long long)view_mem<true>(a, base + st) * 1024 < need) ++st;
+      while (st < a.S - 1 && (long long)view_mem<true>(a, gsel, st) * 1024 < need) ++st;
       const unsigned long long q = (unsigned long long)((need + 1023) / 1024);
-      atomicAdd(&a.cur.grow[gsel], 1);
-      for (int s = st; s < a.S; ++s) atomicAdd(&a.cur.taken[base + s], q);
-      if (phase == 2) a.cur.boost[gsel] = 1;
+      atomicAdd(&a.wcur[gsel], phase == 2 ? (1ull << 32) | 1ull : 1ull);
+      for (int s = st; s < a.S; ++s) atomicAdd(&commit_taken(a.wcur, a.G)[base + s], q);
     }
   }
 }
 
 // Start of a wave-by-wave call: the caller's state copied into the first state buffer, the
-// commit buffers of the first two waves and of the "wave before the first" cleared.
-__global__ void __launch_bounds__(kHostBlock) k_wave_init(int32_t G, int32_t S, State s0, Commits d0, Commits d1,
-                                                          Commits d2, const int32_t *freq0, const int32_t *batch0,
+// three commit buffers cleared.
+__global__ void __launch_bounds__(kHostBlock) k_wave_init(int32_t G, int32_t S, int32_t *st0, unsigned long long *c0,
+                                                          unsigned long long *c1, unsigned long long *c2,
+                                                          const int32_t *freq0, const int32_t *batch0,
                                                           const int32_t *mem0) {
   const int g = blockIdx.x * kHostBlock + threadIdx.x;
   if (g >= G) return;
-  s0.freq[g] = freq0[g];
-  s0.batch[g] = batch0[g];
-  d0.grow[g] = d1.grow[g] = d2.grow[g] = 0;
-  d0.boost[g] = d1.boost[g] = d2.boost[g] = 0;
+  state_fb(st0)[g] = make_int2(freq0[g], batch0[g]);
+  c0[g] = c1[g] = c2[g] = 0ull;
   for (int s = 0; s < S; ++s) {
     const size_t at = (size_t)g * S + s;
-    s0.mem[at] = mem0[at];
-    d0.taken[at] = d1.taken[at] = d2.taken[at] = 0ull;
+    state_mem(st0, G)[at] = mem0[at];
+    commit_taken(c0, G)[at] = commit_taken(c1, G)[at] = commit_taken(c2, G)[at] = 0ull;
   }
 }
 
 // End of a wave-by-wave call: the last state with the last wave's commits applied, into
 // the caller's arrays.
-__global__ void __launch_bounds__(kHostBlock) k_wave_final(DspArgs a, State out) {
+__global__ void __launch_bounds__(kHostBlock) k_wave_final(DspArgs a, int32_t *freq, int32_t *batch, int32_t *mem) {
   const int g = blockIdx.x * kHostBlock + threadIdx.x;
   if (g >= a.G) return;
-  out.batch[g] = view_batch<true>(a, g);
-  out.freq[g] = view_freq<true>(a, g);
-  for (int s = 0; s < a.S; ++s) out.mem[(size_t)g * a.S + s] = view_mem<true>(a, (size_t)g * a.S + s);
+  batch[g] = view_batch<true>(a, g);
+  freq[g] = view_freq<true>(a, g);
+  for (int s = 0; s < a.S; ++s) mem[(size_t)g * a.S + s] = view_mem<true>(a, g, s);
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -572,8 +567,8 @@ static festina_status dsp_args(const festina_lut *L, const festina_gpu_avail *A,
   a.out_phase = out->phase;
   a.out_energy = out->energy_mj;
   a.r0 = 0;
-  a.prev = a.cur = a.next = Commits{nullptr, nullptr, nullptr};
-  a.fold = State{nullptr, nullptr, nullptr};
+  a.wstate = a.wfold = nullptr;
+  a.wprev = a.wcur = a.wnext = nullptr;
   a.packed = 0;
   a.hrec = nullptr;
   return FESTINA_OK;
@@ -603,10 +598,8 @@ extern "C" festina_status festina_dispatch_requests(const festina_lut *L, const 
 // Workspace of a wave-by-wave call: host counts and lists, two state buffers (the state
 // each wave sees alternates between them) and three commit buffers (the previous wave's,
 // read; the current wave's, written; the next wave's, cleared).
-static size_t state_bytes(size_t G, size_t S) { return 2 * align256(sizeof(int32_t) * G) + align256(sizeof(int32_t) * G * S); }
-static size_t commit_bytes(size_t G, size_t S) {
-  return 2 * align256(sizeof(int32_t) * G) + align256(sizeof(unsigned long long) * G * S);
-}
+static size_t state_bytes(size_t G, size_t S) { return align256(sizeof(int32_t) * (2 * G + G * S)); }
+static size_t commit_bytes(size_t G, size_t S) { return align256(sizeof(unsigned long long) * (G + G * S)); }
 
 extern "C" size_t festina_dispatch_waves_workspace_bytes(const festina_lut *L, const festina_gpu_avail *A) {
   if (!dsp_shapes_ok(L, A)) return 0;
@@ -643,18 +636,10 @@ extern "C" festina_status festina_dispatch_waves(const festina_lut *L, const fes
   };
   a.host_cnt = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * L->n_models));
   a.host_list = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (size_t)L->n_models * G));
-  State sb[2];
-  for (State &x : sb) {
-    x.freq = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G));
-    x.batch = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G));
-    x.mem = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G * S));
-  }
-  Commits db[3];
-  for (Commits &x : db) {
-    x.grow = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G));
-    x.boost = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * G));
-    x.taken = reinterpret_cast<unsigned long long *>(take(sizeof(unsigned long long) * G * S));
-  }
+  int32_t *sb[2];
+  for (int32_t *&x : sb) x = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (2 * G + G * S)));
+  unsigned long long *db[3];
+  for (unsigned long long *&x : db) x = reinterpret_cast<unsigned long long *>(take(sizeof(unsigned long long) * (G + G * S)));
   hipStream_t st = static_cast<hipStream_t>(stream);
   const unsigned gblocks = (unsigned)((G + kHostBlock - 1) / kHostBlock);
   k_wave_init<<<gblocks, kHostBlock, 0, st>>>(A->n_gpus, A->n_steps, sb[0], db[0], db[1], db[2], A->freq_cur,
@@ -666,24 +651,21 @@ extern "C" festina_status festina_dispatch_waves(const festina_lut *L, const fes
   }
   // Launch v (of the non-empty waves) sees sb[v % 2] with db[(v + 2) % 3] applied, stores
   // that in sb[(v + 1) % 2], commits to db[v % 3] and clears db[(v + 1) % 3].
+  a.freq_cur = a.batch = a.mem_free = nullptr;
   int v = 0;
   for (int32_t w = 0; w < n_waves; ++w) {
     const int32_t lo = wave_start[w], hi = wave_start[w + 1];
     if (hi == lo) continue;
-    a.freq_cur = sb[v % 2].freq;
-    a.batch = sb[v % 2].batch;
-    a.mem_free = sb[v % 2].mem;
-    a.prev = db[(v + 2) % 3];
-    a.cur = db[v % 3];
-    a.next = db[(v + 1) % 3];
-    a.fold = sb[(v + 1) % 2];
+    a.wstate = sb[v % 2];
+    a.wfold = sb[(v + 1) % 2];
+    a.wprev = db[(v + 2) % 3];
+    a.wcur = db[v % 3];
+    a.wnext = db[(v + 1) % 3];
     if (launch_dispatch<true>(a, lo, hi, st) != FESTINA_OK) return FESTINA_ERR_DEVICE;
     ++v;
   }
-  a.freq_cur = sb[v % 2].freq;
-  a.batch = sb[v % 2].batch;
-  a.mem_free = sb[v % 2].mem;
-  a.prev = db[(v + 2) % 3];
-  k_wave_final<<<gblocks, kHostBlock, 0, st>>>(a, State{state->freq_cur, state->batch, state->mem_free_mib});
+  a.wstate = sb[v % 2];
+  a.wprev = db[(v + 2) % 3];
+  k_wave_final<<<gblocks, kHostBlock, 0, st>>>(a, state->freq_cur, state->batch, state->mem_free_mib);
   return hipGetLastError() == hipSuccess ? FESTINA_OK : FESTINA_ERR_DEVICE;
 }
