@@ -210,3 +210,28 @@ def test_wave_dispatch_state_in_place():
     assert np.array_equal(dd.t["freq_cur"].cpu().numpy(), ref_st["freq_cur"])
     assert np.array_equal(dd.t["batch"].cpu().numpy(), ref_st["batch"])
     assert np.array_equal(dd.t["mem_free_mib"].cpu().numpy().reshape(G, S), ref_st["mem_free_mib"])
+
+
+def test_wave_dispatch_invalid_elements_and_many_hosts():
+    rng = np.random.default_rng(2100)
+    inp = W.make_tiny_dispatch(rng, R=600, G=40, M=3, NS=4, NF=6, S=3)
+    rq, av = inp["requests"], inp["avail"]
+    rq["model"][:20] = 3
+    rq["model"][20:30] = -1
+    rq["prompt_tokens"][30:40] = -5
+    rq["pred_out_tokens"][40:50] = -1
+    av["batch"][:5] = -1
+    av["freq_cur"][5:10] = 9
+    av["sm_free"][10:15] = 7
+    av["sm_free"][15:20] = -1
+    got, st, _ = wave_parity(inp, W.wave_bounds(600, 6), label="invalid elements")
+    assert np.all(got[3][:50] == 0) and np.array_equal(st["batch"][:5], av["batch"][:5])
+    # more hosts per model than 64 lanes x 4 cached hosts: the second pass over the rest
+    wave_parity(W.make_tiny_dispatch(rng, R=700, G=700, M=2, NS=4, NF=6, S=2), W.wave_bounds(700, 5),
+                label="700 GPUs")
+
+
+def test_wave_dispatch_waves_of_16_lanes_per_request():
+    """Waves above 8,192 requests take the 16-lanes-per-request kernel."""
+    inp = W.make_dispatch_waves(seed=W.DISPATCH_SEED + 400, n_requests=20000, n_gpus=256, n_waves=2)
+    wave_parity(inp, inp["wave_start"], label="two waves of 10000")
