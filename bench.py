@@ -325,9 +325,10 @@ def dispatch_row(F, W, hip, torch, with_cpu, calls=200, warmup=10):
 
 
 def dispatch_waves_row(F, W, hip, torch, with_cpu, calls=100, warmup=5):
-    """The same dispatcher over 64 arrival waves, each wave committed to the GPUs' batch,
-    memory and frequency before the next: call time from HIP events and the oracle."""
-    inp = W.make_dispatch_waves()
+    """The same dispatcher over configuration 4's 64 arrival waves (262,144 requests, 1,024
+    GPUs), each wave committed to the GPUs' batch, memory and frequency before the next:
+    call time from HIP events and the oracle."""
+    inp = W.make_dispatch_waves(n_requests=262144, n_gpus=1024, n_waves=64)
     ws = inp["wave_start"]
     dd = F.DeviceDispatch(inp, "cuda")
     ms = timed_calls(hip, torch, lambda: dd.run_waves(ws), calls, warmup)
@@ -343,8 +344,8 @@ def dispatch_waves_row(F, W, hip, torch, with_cpu, calls=100, warmup=5):
         + 2 * G * ((8 + 4 * S) + (8 + 8 * S)) + M * 4 + 2 * lut["pf"].nbytes
     wave_ms = ms / n_waves
     row = {
-        "workload": ("paper's current-frequency dispatcher over arrival waves: 65536 requests in 64 waves of 1024, "
-                     "512 GPUs, each wave committed before the next"),
+        "workload": ("paper's current-frequency dispatcher over configuration 4's arrival waves: 262144 requests "
+                     "in 64 waves of 4096, 1024 GPUs (1-4 of 32 models each), each wave committed before the next"),
         "requests": R, "waves": n_waves, "launches": launches, "call_ms": ms, "requests_per_s": R / (ms * 1e-3),
         "us_per_wave": ms * 1e3 / n_waves,
         "roofline": {"kernel": "k_dispatch (one wave)", "bound": "hbm", "achieved": nbytes / (wave_ms * 1e-3) / 1e9,
@@ -361,7 +362,7 @@ def dispatch_waves_row(F, W, hip, torch, with_cpu, calls=100, warmup=5):
         t1 = time.perf_counter()
         row["cpu_baseline"] = {
             "value": R / (t1 - t0), "unit": "requests/s", "cores": 1, "kind": "oracle",
-            "sample": f"all {R} requests, 64 waves ({t1 - t0:.3f} s); single-threaded C, float64, gcc -O2",
+            "sample": f"all {R} requests, {n_waves} waves ({t1 - t0:.3f} s); single-threaded C, float64, gcc -O2",
             "agreement": {"all_outputs_equal": float(np.mean(
                 (got[0] == ref[0]) & (got[1] == ref[1]) & (got[2] == ref[2]) & (got[3] == ref[3])
                 & (got[4] == ref[4].astype(np.float32)))),

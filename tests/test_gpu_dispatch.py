@@ -153,6 +153,14 @@ def test_wave_dispatch_workload_full_size():
     assert (st["batch"] >= inp["avail"]["batch"]).all() and (st["batch"] > inp["avail"]["batch"]).any()
 
 
+def test_wave_dispatch_configuration_4_shape():
+    """Configuration 4's arrival structure: 262,144 requests in 64 waves of 4,096, 1,024 GPUs."""
+    inp = W.make_dispatch_waves(n_requests=262144, n_gpus=1024, n_waves=64)
+    got, st, _ = wave_parity(inp, inp["wave_start"], label="262144 requests, 1024 GPUs, 64 waves")
+    ph = np.bincount(got[3], minlength=4)
+    assert ph[1] > 0 and ph[2] > 0 and ph[3] > 0 and ph[0] > 0
+
+
 @pytest.mark.parametrize("n_waves", [1, 7, 300])
 def test_wave_dispatch_workload_seeds(n_waves):
     inp = W.make_dispatch_waves(seed=W.DISPATCH_SEED + 300, n_requests=6000, n_gpus=256, n_waves=n_waves)
