@@ -8,7 +8,8 @@
 //                ballots), in the caller's workspace; with at most 4 profile steps, also a
 //                64-byte record per (model, host) with everything Phase One reads, so that
 //                the 16 lanes of a request load their hosts with coalesced 16-byte loads.
-// k_dispatch   16 lanes per request (four per wavefront) stride over the model's hosts.  Per host:
+// k_dispatch   16 lanes per request (four per wavefront; 64 lanes, a wavefront each, in a
+//                launch of at most 8,192 requests) stride over the model's hosts.  Per host:
 //                the first free-memory profile step that holds Req_mem gives T_avail and
 //                SM_free; the point (SM_free, F_curr) is feasible when T_avail + TTFT and
 //                TBT meet the SLOs; E = P * (TTFT + Lout * TBT) in float64.  One pass
@@ -19,6 +20,11 @@
 //                candidate: the hosts feasible at the top level, earliest T_avail (then
 //                lowest id).  Else lane k scores a new GPU at level k and the least energy
 //                (lowest k on ties) wins.
+// Over arrival waves (festina_dispatch_waves): k_wave_init copies the caller's state into a
+//                workspace buffer; one k_dispatch per wave reads the state with the previous
+//                wave's commits applied, stores that state for the next wave, and commits its
+//                own placements (batch, memory from the admitting step on, F_max boost) with
+//                atomics; k_wave_final writes the last state back.
 //
 // Exactness: the energies are float64 in the same order of operations as any float64
 // evaluation of P0 + k*s*f^3*u and P * (TTFT + Lout*TBT) without contraction, so the 2%
