@@ -8,8 +8,8 @@
 //                ballots), in the caller's workspace; with at most 4 profile steps, also a
 //                64-byte record per (model, host) with everything Phase One reads, so that
 //                the 16 lanes of a request load their hosts with coalesced 16-byte loads.
-// k_dispatch   16 lanes per request (four per wavefront; 64 lanes, a wavefront each, in a
-//                launch of at most 8,192 requests) stride over the model's hosts.  Per host:
+// k_dispatch   16 lanes per request (four per wavefront; 32 lanes in a launch of at most
+//                8,192 requests, 64 in one of at most 2,048) stride over the model's hosts.  Per host:
 //                the first free-memory profile step that holds Req_mem gives T_avail and
 //                SM_free; the point (SM_free, F_curr) is feasible when T_avail + TTFT and
 //                TBT meet the SLOs; E = P * (TTFT + Lout * TBT) in float64.  One pass
@@ -273,9 +273,9 @@ __device__ __forceinline__ unsigned long long stability_key(int mem, int sm, int
 }
 
 // Lanes per request: 16 (four requests per wavefront) when a launch holds enough requests
-// to fill the GPU, else 64, so that a request's hosts take one round of loads, not four.
-constexpr int kGroupWide = 64;
-constexpr int kWideRequests = 8192;              // at most this many requests: 64 lanes each
+// to fill the GPU, else 32 or 64, so that a request's hosts take fewer rounds of loads.
+constexpr int kWideRequests = 2048;              // at most this many requests: 64 lanes each
+constexpr int kMidRequests = 8192;               // at most this many: 32 lanes each
 constexpr int kCached = 4;                       // hosts per lane whose Phase One result stays in registers
 
 template <int kGroup>
@@ -516,8 +516,11 @@ static festina_status launch_dispatch(DspArgs a, int32_t lo, int32_t hi, hipStre
   a.R = hi;
   const long long n = (long long)hi - lo;
   if (n <= kWideRequests) {
-    const long long per_block = (long long)kWavesPerBlock * (kWave / kGroupWide);
-    k_dispatch<kGroupWide, kWaves><<<(unsigned)((n + per_block - 1) / per_block), kWavesPerBlock * kWave, 0, st>>>(a);
+    const long long per_block = (long long)kWavesPerBlock * (kWave / 64);
+    k_dispatch<64, kWaves><<<(unsigned)((n + per_block - 1) / per_block), kWavesPerBlock * kWave, 0, st>>>(a);
+  } else if (n <= kMidRequests) {
+    const long long per_block = (long long)kWavesPerBlock * (kWave / 32);
+    k_dispatch<32, kWaves><<<(unsigned)((n + per_block - 1) / per_block), kWavesPerBlock * kWave, 0, st>>>(a);
   } else {
     const long long per_block = (long long)kWavesPerBlock * (kWave / 16);
     k_dispatch<16, kWaves><<<(unsigned)((n + per_block - 1) / per_block), kWavesPerBlock * kWave, 0, st>>>(a);
