@@ -49,7 +49,9 @@
  *     E_waste = sum t_l (F_g^3 - F_l^3), E_optimal = sum t_l F_l^3, EWR = their ratio.
  *
  *   current-frequency dispatch (Sec. 3.3 as the paper runs it, Phases One to Three with
- *   the 2% stability tie-break and the F_max fallback): see the section at the end.
+ *   the 2% stability tie-break and the F_max fallback), on one snapshot of the GPUs or
+ *   over arrival waves with each wave committed to the GPUs' state before the next: see
+ *   the section at the end.
  *
  *   transfer plan (App. F): the cost matrix e_uv = Bytes(u -> v) / BW(u, v) of the
  *   minimum-cost device mapping, and the per-request choice to finish in place or move
