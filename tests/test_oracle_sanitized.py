@@ -13,7 +13,8 @@ import oracle
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 PIN_SUITES = ["test_oracle_placement_pins.py", "test_oracle_migration_pins.py", "test_oracle_sweep_pins.py",
-              "test_oracle_preferred_pins.py", "test_oracle_dispatch_pins.py", "test_oracle_transfer_pins.py"]
+              "test_oracle_preferred_pins.py", "test_oracle_dispatch_pins.py", "test_oracle_dispatch_waves_pins.py",
+              "test_oracle_transfer_pins.py"]
 
 
 def test_pin_suites_under_asan_and_ubsan(tmp_path):
