@@ -1201,8 +1201,8 @@ __device__ void score_requests_generic(const PlaceArgs &a, int m, bool noprompt,
                                        int stride, float *lds) {
   const int C = FNF ? kNS8 * FNF : a.C, NF = FNF ? FNF : a.NF;
   float *dcs = lds;                                   // [32 * C + pad] decode table of the tile's model
-  float *pds = lds + kRows * C + kWave * CPL;         // [C] s_j * f_k^3
-  float *rows = pds + C;                              // [waves][Q][C] prompt rows (capped GPUs)
+  float *pds = lds + kRows * C + kWave * CPL;         // [C] s_j * f_k^3, then per wavefront
+                                                      // [Q][C] prompt rows (capped GPUs)
 
   // stage the model's decode table and the dynamic-power factors
   {
